@@ -1,0 +1,433 @@
+"""Pins for the CPU oracle: each test checks the oracle against something other
+than itself (brute-force integrals of the defining equations, library routines,
+closed forms, invariances, finite differences).  CPU only."""
+import mpmath as mp
+import numpy as np
+import pytest
+from scipy import special
+
+import oracle
+from oracle import constants
+from paper_2609_05709_amd import workloads
+
+
+# ------------------------------------------------------------------ helpers
+
+def real_sph_scipy(l, m, theta, phi):
+    """Real Y_lm from scipy's complex harmonics (which carry the Condon-Shortley
+    phase): m > 0 ~ cos(m phi), m < 0 ~ sin(|m| phi), no CS phase."""
+    if m == 0:
+        return special.sph_harm_y(l, 0, theta, phi).real
+    y = special.sph_harm_y(l, abs(m), theta, phi)
+    s = np.sqrt(2.0) * (-1) ** abs(m)
+    return s * (y.real if m > 0 else y.imag)
+
+
+def angular_grid(nt, nph):
+    t, wt = np.polynomial.legendre.leggauss(nt)  # cos(theta)
+    ph = 2 * np.pi * np.arange(nph) / nph
+    theta = np.arccos(t)
+    TH, PH = np.meshgrid(theta, ph, indexing="ij")
+    W = np.outer(wt, np.full(nph, 2 * np.pi / nph))
+    return TH.ravel(), PH.ravel(), W.ravel()
+
+
+def radial_grid(a, b, n):
+    t, w = np.polynomial.legendre.leggauss(n)
+    return a + (b - a) * (t + 1) / 2, (b - a) * w / 2
+
+
+def rand_rotation(rng):
+    q, r = np.linalg.qr(rng.normal(size=(3, 3)))
+    q = q * np.sign(np.diag(r))
+    if np.linalg.det(q) < 0:
+        q[:, 0] = -q[:, 0]
+    return q
+
+
+# ------------------------------------------------------------ constants
+
+def test_gauss_legendre_matches_numpy():
+    for q in (8, 24, 64):
+        xs, ws = constants.gauss_legendre_mp(q)
+        x = np.array([float(v) for v in xs])
+        w = np.array([float(v) for v in ws])
+        xn, wn = np.polynomial.legendre.leggauss(q)
+        order = np.argsort(x)
+        assert np.allclose(x[order], xn, rtol=0, atol=2e-15)
+        assert np.allclose(w[order], wn, rtol=0, atol=1e-14)  # numpy is good to ~2e-15 absolute
+
+
+@pytest.mark.parametrize("r_cut,n_max,l_max", [(5.0, 4, 4), (6.0, 8, 6), (6.0, 1, 3)])
+def test_gto_primitive_reaches_threshold_at_z(r_cut, n_max, l_max):
+    """Sec. 2.2: the k-th primitive r^l exp(-alpha_kl r^2) decays to 1e-3 at z_k,
+    z_k spaced uniformly from 1 A to r_cut."""
+    z, alpha, _ = constants.gto_mp(r_cut, n_max, l_max)
+    zs = np.linspace(1.0, r_cut, n_max) if n_max > 1 else np.array([1.0])
+    assert np.allclose([float(v) for v in z], zs, rtol=1e-15)
+    with mp.workdps(50):
+        for l in range(l_max + 1):
+            for k in range(n_max):
+                val = z[k] ** l * mp.exp(-alpha[l][k] * z[k] ** 2)
+                assert abs(val - mp.mpf("1e-3")) < mp.mpf("1e-40")
+
+
+@pytest.mark.parametrize("r_cut,n_max,l_max", [(5.0, 4, 4), (6.0, 8, 6), (6.0, 12, 12)])
+def test_gto_basis_orthonormal_by_quadrature(r_cut, n_max, l_max):
+    """g_nl = sum_k beta^l_nk r^l exp(-alpha_kl r^2) is orthonormal on [0, inf)
+    with weight r^2 (the range the closed-form coefficients assume)."""
+    z, alpha, beta = constants.gto_mp(r_cut, n_max, l_max)
+    with mp.workdps(40):
+        xs, ws = constants.gauss_legendre_mp(160)
+        R = mp.mpf(16)
+        rs = [R * (x + 1) / 2 for x in xs]
+        wr = [R * w / 2 for w in ws]
+        for l in sorted({0, l_max // 2, l_max}):
+            g = [[mp.fsum(beta[l][a, k] * r ** l * mp.exp(-alpha[l][k] * r * r) for k in range(n_max))
+                  for r in rs] for a in range(n_max)]
+            for a in range(n_max):
+                for b in range(a, n_max):
+                    val = mp.fsum(w * r * r * g[a][q] * g[b][q] for q, (r, w) in enumerate(zip(rs, wr)))
+                    assert abs(val - (1 if a == b else 0)) < 1e-20, (l, a, b, val)
+
+
+@pytest.mark.parametrize("n_max", [2, 5, 10, 12])
+def test_poly_basis_orthonormal_by_quadrature(n_max):
+    """Sec. 2.3: g_n = sum_k W_nk (r_cut - r)^(k+2) / N_k with W = S^(-1/2) is
+    orthonormal on [0, r_cut] in the measure dr (Eqs. poly-norm, poly-overlap)."""
+    r_cut = 5.0
+    N, W, rq, wq, g = constants.poly_mp(r_cut, n_max, 64)
+    with mp.workdps(50):
+        # g_n g_n' is a polynomial of degree <= 2 n_max + 4: exact with 64 nodes
+        for a in range(n_max):
+            for b in range(a, n_max):
+                val = mp.fsum(wq[q] * g[a][q] * g[b][q] for q in range(64))
+                assert abs(val - (1 if a == b else 0)) < 1e-30, (a, b, val)
+
+
+def test_poly_quadrature_table_integrates_r2_weight():
+    """G[n][q] = w_q r_q^2 g_n(r_q): sum_q G[n][q] h(r_q) equals the integral
+    of r^2 g_n(r) h(r) over [0, r_cut] (mpmath adaptive quadrature)."""
+    r_cut, n_max = 5.0, 6
+    N, W, rq, wq, g = constants.poly_mp(r_cut, n_max, 64)
+    G = constants.poly_arrays(r_cut, n_max, 64)
+    Gv = (G["G_hi"] + G["G_lo"]).reshape(n_max, 64)
+    rqv = G["rq_hi"]
+    with mp.workdps(30):
+        for a in (0, 3, 5):
+            def gn(r):
+                return mp.fsum(W[a, k] * (r_cut - r) ** (k + 3) / N[k] for k in range(n_max))
+            for h in (lambda r: mp.exp(-r), lambda r: mp.exp(-(r - 2.2) ** 2 / 0.32)):
+                ref = mp.quad(lambda r: r * r * gn(r) * h(r), [0, 2.2, r_cut])
+                got = sum(Gv[a, q] * float(h(mp.mpf(rqv[q]))) for q in range(64))
+                assert abs(got - float(ref)) < 1e-11 * max(1.0, abs(float(ref)))
+
+
+# ------------------------------------------------------------ harmonics
+
+def test_real_harmonics_match_scipy_convention(oracle_lib):
+    o = oracle.OracleSOAP((1,), 5.0, 2, 9, 0.5)
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        v = rng.normal(size=3)
+        Y, _ = o.solid_harmonics(v, 9)
+        r = np.linalg.norm(v)
+        th, ph = np.arccos(v[2] / r), np.arctan2(v[1], v[0])
+        for l in range(10):
+            for m in range(-l, l + 1):
+                assert abs(Y[l * l + l + m] - real_sph_scipy(l, m, th, ph)) < 1e-13
+
+
+def test_real_harmonics_addition_theorem(oracle_lib):
+    """sum_m Y_lm(a) Y_lm(b) = (2l+1)/(4 pi) P_l(a.b)."""
+    o = oracle.OracleSOAP((1,), 5.0, 2, 13, 0.5)
+    rng = np.random.default_rng(6)
+    for _ in range(10):
+        a, b = rng.normal(size=3), rng.normal(size=3)
+        Ya, _ = o.solid_harmonics(a, 13)
+        Yb, _ = o.solid_harmonics(b, 13)
+        cg = a @ b / np.linalg.norm(a) / np.linalg.norm(b)
+        for l in range(14):
+            s = Ya[l * l:(l + 1) ** 2] @ Yb[l * l:(l + 1) ** 2]
+            assert abs(s - (2 * l + 1) / (4 * np.pi) * special.eval_legendre(l, cg)) < 1e-13
+
+
+def test_real_harmonics_orthonormal_on_sphere(oracle_lib):
+    o = oracle.OracleSOAP((1,), 5.0, 2, 8, 0.5)
+    TH, PH, W = angular_grid(20, 40)
+    pts = np.stack([np.sin(TH) * np.cos(PH), np.sin(TH) * np.sin(PH), np.cos(TH)], 1)
+    Y = np.array([o.solid_harmonics(p, 8)[0] for p in pts])
+    gram = (Y * W[:, None]).T @ Y
+    assert np.abs(gram - np.eye(gram.shape[0])).max() < 1e-12
+
+
+def test_solid_harmonic_gradient_by_finite_differences(oracle_lib):
+    o = oracle.OracleSOAP((1,), 5.0, 2, 7, 0.5)
+    rng = np.random.default_rng(7)
+    h = 1e-6
+    for _ in range(5):
+        u = rng.normal(size=3)
+        u /= np.linalg.norm(u)
+        _, G = o.solid_harmonics(u, 7)
+        for d in range(3):
+            e = np.zeros(3)
+            e[d] = h
+            # r^l Y_lm(v/|v|) evaluated away from the unit sphere
+            def solid(v):
+                Y, _ = o.solid_harmonics(v, 7)
+                r = np.linalg.norm(v)
+                ls = np.concatenate([[l] * (2 * l + 1) for l in range(8)])
+                return Y * r ** ls
+            fd = (solid(u + e) - solid(u - e)) / (2 * h)
+            assert np.abs(fd - G[d]).max() < 1e-8
+
+
+# --------------------------------------------------------------- Bessel
+
+@pytest.mark.parametrize("x", [1e-3, 0.05, 0.7, 3.0, 11.0, 26.0, 60.0, 120.0, 200.0])
+def test_bessel_il_matches_mpmath(oracle_lib, x):
+    got = oracle.bessel_il(13, x)
+    with mp.workdps(40):
+        for l in range(14):
+            ref = mp.sqrt(mp.pi / (2 * mp.mpf(x))) * mp.besseli(l + mp.mpf(1) / 2, x)
+            assert abs(got[l] - float(ref)) <= 2e-15 * abs(float(ref)) + 1e-300, (l, got[l], ref)
+
+
+# ----------------------------------------------- projection, brute force
+
+def _brute_coefficients(sp, pos, Z, n_max, l_max, sigma, g_of_r, r_hi, nr=140, nt=56, nph=112):
+    """c^mu_nlm = int r^2 dr dOmega g_nl(r) Y_lm rho^mu(r) on a dense grid, with
+    rho^mu the sum of unnormalised Gaussians of the species-mu atoms (center at
+    the origin included)."""
+    TH, PH, W = angular_grid(nt, nph)
+    rs, wr = radial_grid(0.0, r_hi, nr)
+    Yg = np.array([[real_sph_scipy(l, m, TH, PH) for m in range(-l, l + 1)] for l in range(l_max + 1)],
+                  dtype=object)
+    dirs = np.stack([np.sin(TH) * np.cos(PH), np.sin(TH) * np.sin(PH), np.cos(TH)], 1)
+    gvals = g_of_r(rs)  # (n, l+1, nr)
+    out = np.zeros((len(sp), n_max, (l_max + 1) ** 2))
+    for si, z in enumerate(sp):
+        atoms = pos[Z == z]
+        # rho on the grid: (nr, nang)
+        pts = rs[:, None, None] * dirs[None, :, :]
+        rho = np.zeros((nr, dirs.shape[0]))
+        for a in atoms:
+            rho += np.exp(-np.sum((pts - a) ** 2, axis=2) / (2 * sigma ** 2))
+        for l in range(l_max + 1):
+            for mi, m in enumerate(range(-l, l + 1)):
+                ang = rho @ (Yg[l][mi] * W)  # (nr,)
+                for n in range(n_max):
+                    out[si, n, l * l + l + m] = np.sum(wr * rs ** 2 * gvals[n, l] * ang)
+    return out
+
+
+def test_gto_coefficients_equal_bruteforce_projection(oracle_lib):
+    """Eq. (gto-coefficients) (closed form incl. the on-site term) equals the
+    direct 3-D integral of Eqs. (density) + (projection) with the radial range
+    extended to infinity."""
+    r_cut, n_max, l_max, sigma = 5.0, 4, 4, 0.5
+    o = oracle.OracleSOAP((1, 8), r_cut, n_max, l_max, sigma, "gto")
+    pos = np.array([[0, 0, 0], [0.61, -0.52, 0.83], [-1.3, 0.4, -0.9], [0.2, 1.7, 0.35]])
+    Z = np.array([1, 1, 8, 1])
+    got = o.compute(pos, Z, centers=[0], coefficients=True)["c"][0]
+    z, alpha, beta = constants.gto_mp(r_cut, n_max, l_max)
+    al = np.array([[float(alpha[l][k]) for k in range(n_max)] for l in range(l_max + 1)])
+    be = np.array([[[float(beta[l][a, k]) for k in range(n_max)] for a in range(n_max)] for l in range(l_max + 1)])
+
+    def g(rs):
+        return np.einsum("lak,lkr->alr", be, rs[None, None, :] ** np.arange(l_max + 1)[:, None, None]
+                         * np.exp(-al[:, :, None] * rs[None, None, :] ** 2))
+    ref = _brute_coefficients([1, 8], pos, Z, n_max, l_max, sigma, g, 12.0)
+    scale = np.abs(ref).max()
+    assert np.abs(got - ref).max() < 2e-10 * scale
+
+
+def test_poly_coefficients_equal_bruteforce_projection(oracle_lib):
+    """Eq. (poly-coefficients-exact) with the Gauss-Legendre radial rule equals
+    the direct 3-D integral of Eqs. (density) + (projection) on [0, r_cut]."""
+    r_cut, n_max, l_max, sigma = 5.0, 5, 5, 0.4
+    o = oracle.OracleSOAP((1, 6), r_cut, n_max, l_max, sigma, "polynomial")
+    pos = np.array([[0, 0, 0], [0.91, -0.52, 0.33], [-1.6, 1.4, -1.9], [0.2, 2.7, 0.35]])
+    Z = np.array([6, 1, 6, 1])
+    got = o.compute(pos, Z, centers=[0], coefficients=True)["c"][0]
+    N, W, _, _, _ = constants.poly_mp(r_cut, n_max, 64)
+
+    def g(rs):
+        out = np.zeros((n_max, l_max + 1, len(rs)))
+        with mp.workdps(40):
+            for a in range(n_max):
+                vals = [float(mp.fsum(W[a, k] * (r_cut - mp.mpf(r)) ** (k + 3) / N[k] for k in range(n_max)))
+                        for r in rs]
+                out[a, :, :] = np.array(vals)[None, :]
+        return out
+    ref = _brute_coefficients([1, 6], pos, Z, n_max, l_max, sigma, g, r_cut, nr=160)
+    scale = np.abs(ref).max()
+    assert np.abs(got - ref).max() < 2e-10 * scale
+
+
+def test_gaussian_bessel_radial_integral(oracle_lib):
+    """Eq. (bessel-integral) by 1-D quadrature (uses the oracle's i_l)."""
+    for l, p, c in [(0, 1.7, 2.3), (3, 0.9, 4.1), (7, 2.5, 6.0)]:
+        with mp.workdps(30):
+            ref = mp.sqrt(mp.pi) * c ** l / (2 ** (l + 2) * mp.mpf(p) ** (l + mp.mpf(3) / 2)) * mp.exp(c * c / (4 * p))
+        rs, wr = radial_grid(0, 12, 200)
+        val = sum(w * r ** (l + 2) * np.exp(-p * r * r) * oracle.bessel_il(l, c * r)[l] for r, w in zip(rs, wr))
+        assert abs(val - float(ref)) < 1e-12 * float(ref)
+
+
+# ---------------------------------------------- power spectrum, SH-free
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_power_spectrum_equals_two_body_legendre_form(oracle_lib, rbf):
+    """By the addition theorem, Eq. (powerspectrum) equals
+    sqrt((2l+1)/2) sum_{a in mu} sum_{b in nu} phi_nl(a) phi_n'l(b) P_l(cos g_ab),
+    phi_nl(a) = R_nl(r_a) (times r_a^l for GTO); the center contributes at l = 0
+    through its on-site term sqrt(4 pi) c0_n.  No spherical harmonics used."""
+    sp = (1, 6, 8)
+    o = oracle.OracleSOAP(sp, 4.5, 5, 6, 0.45, rbf)
+    rng = np.random.default_rng(11)
+    pos = rng.uniform(-2.2, 2.2, size=(9, 3))
+    pos[0] = 0
+    Z = np.array([6, 1, 8, 6, 1, 1, 8, 6, 1])
+    got = o.compute(pos, Z, centers=[0])["desc"][0]
+    sidx = o.species_index(Z)
+    nb = [j for j in range(1, 9) if np.linalg.norm(pos[j]) < 4.5]
+    phi = {}
+    for j in nb:
+        r = np.linalg.norm(pos[j])
+        R, _, c0 = o.radial(r)
+        phi[j] = R * (r ** np.arange(7)[None, :] if rbf == "gto" else 1.0)
+    c0 = o.radial(1.0)[2]
+    ref = []
+    for mu, nu, a, b, l in o.features():
+        s = 0.0
+        for j in nb:
+            for k in nb:
+                if sidx[j] != mu or sidx[k] != nu:
+                    continue
+                cg = pos[j] @ pos[k] / np.linalg.norm(pos[j]) / np.linalg.norm(pos[k])
+                s += phi[j][a, l] * phi[k][b, l] * special.eval_legendre(l, cg)
+        if l == 0:
+            f0 = np.sqrt(4 * np.pi) * c0
+            if sidx[0] == mu:
+                s += f0[a] * sum(phi[k][b, 0] for k in nb if sidx[k] == nu)
+            if sidx[0] == nu:
+                s += f0[b] * sum(phi[j][a, 0] for j in nb if sidx[j] == mu)
+            if sidx[0] == mu == nu:
+                s += f0[a] * f0[b]
+        ref.append(np.sqrt((2 * l + 1) / 2) * s)
+    ref = np.array(ref)
+    assert np.abs(got - ref).max() < 1e-12 * np.abs(ref).max()
+
+
+def test_isolated_atom_descriptor_is_onsite_only(oracle_lib):
+    o = oracle.OracleSOAP((1, 8), 5.0, 3, 2, 0.5, "gto")
+    pos = np.array([[0.0, 0, 0], [10.0, 0, 0]])
+    out = o.compute(pos, np.array([8, 1]), jacobian=True)
+    c0 = o.radial(1.0)[2]
+    feats = o.features()
+    for f, (mu, nu, a, b, l) in enumerate(feats):
+        exp = np.pi * np.sqrt(8.0) * c0[a] * c0[b] if (mu == nu == 1 and l == 0) else 0.0
+        assert abs(out["desc"][0, f] - exp) < 1e-14
+    assert np.all(out["jac"] == 0)
+
+
+# ------------------------------------------------------- invariances
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_descriptor_invariances(oracle_lib, rbf):
+    s = workloads.random_small(14, 21, 3.2, species=(1, 6, 8))
+    o = oracle.OracleSOAP((1, 6, 8), 4.0, 4, 5, 0.5, rbf)
+    base = o.compute(s.pos64, s.Z)["desc"]
+    rng = np.random.default_rng(3)
+    Q = rand_rotation(rng)
+    scale = np.abs(base).max()
+    rot = o.compute(s.pos64 @ Q.T, s.Z)["desc"]
+    assert np.abs(rot - base).max() < 1e-12 * scale
+    refl = o.compute(s.pos64 * np.array([1, -1, 1]), s.Z)["desc"]
+    assert np.abs(refl - base).max() < 1e-12 * scale
+    tr = o.compute(s.pos64 + np.array([3.3, -7.1, 0.25]), s.Z)["desc"]
+    assert np.abs(tr - base).max() < 1e-12 * scale
+    perm = np.arange(s.n_atoms)
+    like = np.where(s.Z == s.Z[0])[0]
+    perm[like] = like[::-1]
+    pp = o.compute(s.pos64[perm], s.Z[perm])["desc"]
+    assert np.abs(pp - base[perm]).max() < 1e-12 * scale
+
+
+# --------------------------------------------------------- Jacobian
+
+def _blocks(out, c):
+    b0, b1 = out["blk_ptr"][c], out["blk_ptr"][c + 1]
+    return {int(j): out["jac"][b] for j, b in zip(out["blk_j"][b0:b1], range(b0, b1))}
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_jacobian_central_finite_differences(oracle_lib, rbf):
+    s = workloads.random_small(8, 31, 2.6, species=(1, 8))
+    o = oracle.OracleSOAP((1, 8), 4.5, 4, 4, 0.5, rbf)
+    pos = s.pos64
+    out = o.compute(pos, s.Z, jacobian=True)
+    h = 1e-5
+    for c in (0, 3):
+        blk = _blocks(out, c)
+        for j, J in blk.items():
+            fd = np.empty_like(J)
+            for d in range(3):
+                pp, pm = pos.copy(), pos.copy()
+                pp[j, d] += h
+                pm[j, d] -= h
+                fd[d] = (o.compute(pp, s.Z, centers=[c])["desc"][0] - o.compute(pm, s.Z, centers=[c])["desc"][0]) / (2 * h)
+            assert np.abs(fd - J).max() < 1e-8 * max(np.abs(J).max(), 1e-3), (c, j)
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_jacobian_rotational_sum_rule(oracle_lib, rbf):
+    """p_i is invariant under rotations about r_i: sum_j r_ij x J[i<-j] = 0."""
+    s = workloads.random_small(20, 41, 3.5, species=(1, 6))
+    o = oracle.OracleSOAP((1, 6), 4.0, 5, 6, 0.5, rbf)
+    out = o.compute(s.pos64, s.Z, jacobian=True)
+    for c in range(0, 20, 4):
+        blk = _blocks(out, c)
+        torque = np.zeros((3, o.n_features))
+        scale = 0.0
+        for j, J in blk.items():
+            rij = s.pos64[j] - s.pos64[c]
+            torque += np.cross(rij[:, None], J, axisa=0, axisb=0, axisc=0)
+            scale = max(scale, np.abs(J).max() * np.linalg.norm(rij))
+        assert np.abs(torque).max() < 1e-12 * scale
+
+
+def test_jacobian_covariant_under_rotation(oracle_lib):
+    s = workloads.random_small(10, 51, 3.0, species=(1, 8))
+    o = oracle.OracleSOAP((1, 8), 4.5, 3, 4, 0.5, "gto")
+    Q = rand_rotation(np.random.default_rng(9))
+    a = o.compute(s.pos64, s.Z, jacobian=True)
+    b = o.compute(s.pos64 @ Q.T, s.Z, jacobian=True)
+    assert np.array_equal(a["blk_j"], b["blk_j"])
+    assert np.abs(np.einsum("xy,byf->bxf", Q, a["jac"]) - b["jac"]).max() < 1e-12 * np.abs(a["jac"]).max()
+
+
+# ------------------------------------------------------- neighbours
+
+def test_neighbor_sets_brute_grid_and_kdtree(oracle_lib):
+    from scipy.spatial import cKDTree
+    st = workloads.WATER1000.structure()
+    pos = st.pos64
+    rc = 6.0
+    row_b, col_b = oracle.neighbors(pos, rc)
+    row_g, col_g = oracle.neighbors_grid(pos, rc)
+    assert np.array_equal(row_b, row_g) and np.array_equal(col_b, col_g)
+    pairs = cKDTree(pos).query_pairs(rc, output_type="ndarray")
+    d2 = np.sum((pos[pairs[:, 0]] - pos[pairs[:, 1]]) ** 2, 1)
+    pairs = pairs[d2 < rc * rc]
+    assert 2 * len(pairs) == len(col_b)
+    got = set(zip(np.repeat(np.arange(len(pos)), np.diff(row_b)).tolist(), col_b.tolist()))
+    ref = set(map(tuple, pairs.tolist())) | set(map(tuple, pairs[:, ::-1].tolist()))
+    assert got == ref
+
+
+def test_unknown_species_rejected(oracle_lib):
+    o = oracle.OracleSOAP((1, 8), 5.0, 2, 2, 0.5)
+    with pytest.raises(ValueError):
+        o.compute(np.zeros((2, 3)) + [[0, 0, 0], [1, 0, 0]], np.array([1, 6]))
