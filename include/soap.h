@@ -1,0 +1,195 @@
+/*
+ * soap.h -- C ABI of the MI355X SOAP descriptor + analytic Jacobian library.
+ *
+ * What is computed (arXiv 2609.05709, Sec. 2):
+ *   - species-resolved Gaussian-smeared neighbour densities, Eq. (density):
+ *     every atom j != i with |r_j - r_i| < r_cut contributes an unnormalised
+ *     Gaussian of width sigma to the density of its species; the center atom
+ *     itself is included in its own species' density through the
+ *     position-independent l = 0 on-site term (Sec. 2.2, last term of
+ *     Eq. (gto-coefficients); Sec. 2.3 for the polynomial basis);
+ *   - expansion coefficients c^mu_nlm, Eq. (projection), in real spherical
+ *     harmonics and either the GTO radial basis (Sec. 2.2, Eqs. (gto-basis),
+ *     (gto-alphas), (gto-lowdin), closed form Eq. (gto-coefficients)) or the
+ *     polynomial radial basis (Sec. 2.3, Eqs. (poly-basis)-(poly-overlap),
+ *     coefficients Eq. (poly-coefficients-exact) with the radial integral
+ *     Eq. (poly-radial-integral) evaluated by a fixed Gauss-Legendre rule on
+ *     [0, r_cut], Sec. 3.1);
+ *   - the power spectrum p^{mu nu}_{n n' l}, Eq. (powerspectrum);
+ *   - its Cartesian Jacobian by the product rule, Eq. (powerspectrum-derivative),
+ *     with d c / d r_j from Eq. (gto-derivative) or
+ *     Eq. (poly-cartesian-derivative), and the center's own block from
+ *     translational invariance (end of Sec. 2.1).
+ *
+ * Feature order (Sec. 3.1): species pairs (mu, nu) with mu <= nu over the
+ * species sorted by ascending Z, then n, then n' (n' >= n when mu == nu, all
+ * n' when mu < nu), then l innermost.  F = (l_max+1) * S n (S n + 1) / 2.
+ *
+ * Conventions shared by all entry points:
+ *   - Units: angstrom.
+ *   - Device pointers ("_dev") are HIP device memory on the context's device,
+ *     owned by the caller; they must stay valid until the work enqueued on
+ *     `stream` has completed.  `stream` is a hipStream_t (NULL = the default
+ *     stream).  All calls are asynchronous on `stream` unless stated.
+ *   - dtype (option "dtype"): SOAP_FP32 (default) = float32 positions and
+ *     outputs; SOAP_FP64 = float64 positions and outputs.  Internal
+ *     arithmetic is float64 in both modes.
+ *   - Every function returns SOAP_OK or a negative status; on error nothing
+ *     is enqueued and soap_last_error() describes the cause.  No function
+ *     aborts or throws across this interface.
+ *   - A context is not thread-safe; use one context per host thread.
+ */
+#ifndef SOAP_MI355X_H
+#define SOAP_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct soap_ctx soap_ctx;
+
+#define SOAP_OK 0
+#define SOAP_EINVAL (-1)    /* argument out of range */
+#define SOAP_ESPECIES (-2)  /* an atomic number is not in the species list */
+#define SOAP_ENOMEM (-3)    /* device or host allocation failed */
+#define SOAP_EHIP (-4)      /* a HIP runtime call failed */
+#define SOAP_ECAPACITY (-5) /* a neighbour row exceeds the supported degree */
+#define SOAP_ESTATE (-6)    /* call order violated (e.g. compute before build) */
+
+#define SOAP_RBF_GTO 0
+#define SOAP_RBF_POLYNOMIAL 1
+
+#define SOAP_FP32 0
+#define SOAP_FP64 1
+
+/* Largest neighbour count per center the neighbour builder accepts. */
+#define SOAP_MAX_DEGREE 2048
+
+/*
+ * Create a context on the current HIP device.  Arguments follow the paper's
+ * problem statement (Sec. 3.1: r_cut, n_max, l_max, sigma, rbf, species).
+ *   species_Z : n_species distinct atomic numbers (1..127), any order (host).
+ *   r_cut     : cutoff radius; GTO requires r_cut > 1 (the widths of
+ *               Eq. (gto-alphas) place the first primitive at 1 A).
+ *   n_max     : 1..16 radial functions;  l_max: 0..14;  sigma > 0.
+ *   rbf       : SOAP_RBF_GTO or SOAP_RBF_POLYNOMIAL.
+ * Basis constants (Loewdin coefficients, quadrature tables) are computed here
+ * on the host in 113-bit floating point and uploaded once.
+ * Errors: SOAP_EINVAL, SOAP_ENOMEM, SOAP_EHIP.  *out is NULL on error.
+ */
+int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32_t n_max, int32_t l_max,
+                double sigma, int32_t rbf, soap_ctx **out);
+
+/*
+ * Set an option.  Keys:
+ *   "dtype"  : SOAP_FP32 or SOAP_FP64 (default SOAP_FP32);
+ *   "quad_n" : Gauss-Legendre order for the polynomial basis, 8..256
+ *              (default 64); rebuilds the quadrature table.
+ * Options take effect for calls made after this one; changing "dtype"
+ * discards the neighbour list.  Errors: SOAP_EINVAL.
+ */
+int soap_set_option(soap_ctx *ctx, const char *key, int64_t value);
+
+/* Number of descriptor features F (see feature order above); -1 if ctx is NULL. */
+int64_t soap_num_features(const soap_ctx *ctx);
+
+/*
+ * Number of features F_e a neighbour block can touch: the features whose
+ * species pair contains the neighbour's species,
+ * F_e = (l_max+1) (n(n+1)/2 + (S-1) n^2), the same for every species.
+ */
+int64_t soap_num_edge_features(const soap_ctx *ctx);
+
+/*
+ * Feature labels: out[5*f + {0..4}] = (mu, nu, n, n', l) for f < F (host
+ * buffer of 5F int32).  Species indices refer to the sorted species list.
+ */
+int soap_feature_labels(const soap_ctx *ctx, int32_t *out);
+
+/*
+ * For species index s (0..S-1 in sorted order), write to host buffer out[F_e]
+ * the full feature index of each compressed slot of a neighbour block.
+ */
+int soap_feature_map(const soap_ctx *ctx, int32_t species_index, int32_t *out);
+
+/*
+ * Build the neighbour list of a structure (the neighbour-search step of
+ * Sec. 3.1, here a hashed cell list on the device):
+ *   N(i) = { j != i : |r_j - r_i|^2 < r_cut^2 }, the squared distance formed
+ *   in float64 as ((dx*dx + dy*dy) + dz*dz), dx = (double)x_j - (double)x_i,
+ *   without fused multiply-adds.  Coincident atoms (distance 0) are kept as
+ *   edges; they add their on-site term to the density and have a zero
+ *   Jacobian block.
+ *   n_atoms     : >= 1.
+ *   pos_dev     : n_atoms x 3 positions (AoS), float32 or float64 per "dtype".
+ *   Z_dev       : n_atoms atomic numbers (int32).
+ *   n_centers   : number of centers (>= 1);
+ *   centers_dev : n_centers atom indices (int32), or NULL for all atoms in
+ *                 order (then n_centers must equal n_atoms).
+ *   n_edges_out : host; receives E = sum_i |N(i)|.
+ * Rows are ordered by species index (sorted Z), then by ascending atom
+ * index.  The context keeps the rows and the input pointers for the calls
+ * below.  This call synchronises `stream` once (to read E and device-side
+ * checks).  Errors: SOAP_EINVAL, SOAP_ESPECIES (unknown Z),
+ * SOAP_ECAPACITY (a row longer than SOAP_MAX_DEGREE), SOAP_ENOMEM, SOAP_EHIP.
+ */
+int soap_build_neighbors(soap_ctx *ctx, int64_t n_atoms, const void *pos_dev, const int32_t *Z_dev,
+                         int64_t n_centers, const int32_t *centers_dev, int64_t *n_edges_out, void *stream);
+
+/*
+ * Copy the neighbour rows of the last build: row_ptr_dev[n_centers+1]
+ * (int64, CSR offsets into the edge list) and cols_dev[E] (int32 atom
+ * indices).  Either pointer may be NULL.  Errors: SOAP_ESTATE, SOAP_EHIP.
+ */
+int soap_get_neighbors(soap_ctx *ctx, int64_t *row_ptr_dev, int32_t *cols_dev, void *stream);
+
+/*
+ * Descriptor: desc_dev[n_centers][F] (dtype), Eq. (powerspectrum).
+ * Errors: SOAP_ESTATE (no neighbour list), SOAP_ENOMEM, SOAP_EHIP.
+ */
+int soap_compute(soap_ctx *ctx, void *desc_dev, void *stream);
+
+/*
+ * Expansion coefficients c^mu_nlm (the raw coefficients of Eq. (projection),
+ * the "cc" quantity of Sec. 3.1): c_dev[n_centers][S][n_max][(l_max+1)^2]
+ * (dtype), index lm = l*l + l + m; real harmonics with m > 0 ~ cos(m phi),
+ * m < 0 ~ sin(|m| phi), no Condon-Shortley phase.
+ */
+int soap_coefficients(soap_ctx *ctx, void *c_dev, void *stream);
+
+/*
+ * Descriptor and Jacobian, Eqs. (powerspectrum), (powerspectrum-derivative):
+ *   desc_dev     [n_centers][F]        p_i
+ *   jac_edge_dev [E][3][F_e]           d p_i / d r_j for the e-th edge (i, j)
+ *                                      of the neighbour rows, compressed to the
+ *                                      F_e features that can be non-zero (the
+ *                                      pairs containing species(j); the map
+ *                                      is soap_feature_map(species(j)));
+ *   jac_self_dev [n_centers][3][F]     d p_i / d r_i = - sum_j d p_i / d r_j.
+ * All derivatives not stored are exactly zero (atoms outside the cutoff,
+ * features whose pair lacks species(j)).  Errors: SOAP_ESTATE, SOAP_ENOMEM,
+ * SOAP_EHIP.
+ */
+int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *jac_self_dev, void *stream);
+
+/*
+ * Expand a soap_derivatives result into the dense layout
+ * dense_dev[n_centers][n_atoms][3][F] (dtype), zeros included.  Intended for
+ * small structures (the dense array grows as n_centers * n_atoms).
+ */
+int soap_scatter_dense(soap_ctx *ctx, const void *jac_edge_dev, const void *jac_self_dev, void *dense_dev,
+                       void *stream);
+
+/* Message for the last error on this context ("" if none). */
+const char *soap_last_error(const soap_ctx *ctx);
+
+/* Free the context and its device buffers (synchronises the device). NULL ok. */
+void soap_destroy(soap_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOAP_MI355X_H */

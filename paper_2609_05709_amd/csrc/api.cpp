@@ -1,0 +1,535 @@
+// C ABI of the SOAP library (declared in include/soap.h).
+#include "../../include/soap.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "basis.h"
+#include "soap_internal.h"
+
+using namespace soap;
+
+namespace {
+
+// grow-only device buffer
+struct DevBuf {
+    void *p = nullptr;
+    size_t cap = 0;
+    hipError_t ensure(size_t bytes) {
+        if (bytes <= cap && p) return hipSuccess;
+        if (p) {
+            hipError_t e = hipFree(p);
+            p = nullptr;
+            cap = 0;
+            if (e != hipSuccess) return e;
+        }
+        size_t b = bytes < 256 ? 256 : bytes;
+        hipError_t e = hipMalloc(&p, b);
+        if (e == hipSuccess) cap = b;
+        return e;
+    }
+    void release() {
+        if (p) (void)hipFree(p);
+        p = nullptr;
+        cap = 0;
+    }
+    template <typename T> T *as() const { return static_cast<T *>(p); }
+};
+
+constexpr size_t DENSITY_LDS_BUDGET = 64 * 1024;
+constexpr size_t JACOBIAN_LDS_BUDGET = 80 * 1024;
+constexpr size_t LDS_HARD_LIMIT = 160 * 1024;
+
+} // namespace
+
+struct soap_ctx {
+    int device = 0;
+    std::vector<int32_t> Z; // sorted
+    double r_cut = 0, sigma = 0;
+    int n = 0, lmax = 0, rbf = 0, Q = 64, dtype = SOAP_FP32;
+    int64_t F = 0, Fe = 0;
+    int nq_full = 0;
+    std::vector<uint32_t> fq;
+    std::vector<uint2> fe;        // [S][Fe]
+    std::vector<int32_t> fmap;    // [S][Fe]
+    Params P{};
+    // device constants
+    DevBuf d_const, d_fq, d_fe, d_fmap, d_lut;
+    // neighbour workspace
+    NbrWork nw{};
+    DevBuf b_bcount, b_bstart, b_bfill, b_acell, b_scell, b_spos, b_satom, b_deg, b_scan, b_flags, b_spec,
+        b_row, b_cols, b_cscratch;
+    int32_t *h_flags = nullptr; // pinned: [0..3] flags, then int64 E at offset 8
+    // state of the last neighbour build
+    bool have_rows = false;
+    int64_t n_atoms = 0, nc = 0, E = 0;
+    const void *pos = nullptr;
+    const int32_t *Zdev = nullptr, *centers = nullptr;
+    bool built_f64 = false;
+    // launch configuration
+    DensityLaunch dens_cfg[2]{};  // [jac]
+    JacLaunch jac_cfg{};
+    int groups_jac = 1, groups_desc = 1;
+    int lgrp_jac[MAX_GROUPS + 1]{}, lgrp_desc[MAX_GROUPS + 1]{};
+    std::string err;
+};
+
+namespace {
+
+int fail(soap_ctx *c, int code, const char *fmt, ...) {
+    if (c) {
+        char buf[512];
+        va_list ap;
+        va_start(ap, fmt);
+        vsnprintf(buf, sizeof buf, fmt, ap);
+        va_end(ap);
+        c->err = buf;
+    }
+    return code;
+}
+
+int hip_fail(soap_ctx *c, hipError_t e, const char *where) {
+    return fail(c, e == hipErrorOutOfMemory ? SOAP_ENOMEM : SOAP_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+// feature tables: full (mu,nu,n,n') combinations and the per-species edge terms
+void build_feature_tables(soap_ctx *c) {
+    const int S = (int)c->Z.size(), n = c->n, lw = c->lmax + 1;
+    c->fq.clear();
+    for (int mu = 0; mu < S; ++mu)
+        for (int nu = mu; nu < S; ++nu)
+            for (int a = 0; a < n; ++a)
+                for (int b = (mu == nu ? a : 0); b < n; ++b)
+                    c->fq.push_back((uint32_t)mu | (uint32_t)nu << 8 | (uint32_t)a << 16 | (uint32_t)b << 24);
+    c->nq_full = (int)c->fq.size();
+    c->F = (int64_t)c->nq_full * lw;
+    c->Fe = (int64_t)lw * (n * (n + 1) / 2 + (S - 1) * n * n);
+    c->fe.assign((size_t)S * c->Fe, make_uint2(0, 0));
+    c->fmap.assign((size_t)S * c->Fe, 0);
+    for (int s = 0; s < S; ++s) {
+        int64_t k = 0;
+        for (int q = 0; q < c->nq_full; ++q) {
+            const uint32_t f = c->fq[q];
+            const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
+            if (mu != s && nu != s) continue;
+            int nb1, u1, two = 0, nb2 = 0, u2 = 0;
+            if (mu == s && nu == s) { // d/dr_j of sum_m c^s_a c^s_b: both factors
+                nb1 = a; u1 = s * n + b; two = 1; nb2 = b; u2 = s * n + a;
+            } else if (mu == s) {     // derivative of the first factor
+                nb1 = a; u1 = nu * n + b;
+            } else {                  // derivative of the second factor
+                nb1 = b; u1 = mu * n + a;
+            }
+            for (int l = 0; l < lw; ++l, ++k) {
+                c->fe[(size_t)s * c->Fe + k] = make_uint2((uint32_t)l | (uint32_t)nb1 << 8 | (uint32_t)u1 << 16 |
+                                                              (uint32_t)two << 24,
+                                                          (uint32_t)nb2 | (uint32_t)u2 << 8);
+                c->fmap[(size_t)s * c->Fe + k] = q * lw + l;
+            }
+        }
+    }
+}
+
+// Split l = 0..lmax into groups whose density-kernel LDS fits the budget.
+int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *EC_out, size_t *lds_out) {
+    const int lw = P.lmax + 1;
+    for (int G = 1; G <= lw; ++G) {
+        // balance sum over l of (2l+1) across G contiguous groups
+        int bounds[MAX_GROUPS + 1];
+        bounds[0] = 0;
+        int g = 1;
+        const double target = (double)(lw * lw) / G;
+        for (int l = 1; l < lw && g < G; ++l)
+            if ((double)(l * l) >= target * g) bounds[g++] = l;
+        while (g < G) { // degenerate: fill the remainder one l each
+            bounds[g] = bounds[g - 1] + 1;
+            ++g;
+        }
+        bounds[G] = lw;
+        bool ok = true;
+        for (int k = 0; k < G; ++k)
+            if (bounds[k + 1] <= bounds[k]) ok = false;
+        if (!ok) continue;
+        for (int EC : {64, 32, 16, 8, 4}) {
+            size_t worst = 0;
+            for (int k = 0; k < G; ++k) worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], EC));
+            if (worst <= DENSITY_LDS_BUDGET || (G == lw && EC == 4 && worst <= LDS_HARD_LIMIT)) {
+                for (int k = 0; k <= G; ++k) lgrp[k] = bounds[k];
+                *ngroups = G;
+                *EC_out = EC;
+                *lds_out = worst;
+                return 0;
+            }
+        }
+    }
+    return -1;
+}
+
+int plan_launches(soap_ctx *c) {
+    Params &P = c->P;
+    int EC;
+    size_t lds;
+    if (plan_groups(P, 0, c->lgrp_desc, &c->groups_desc, &EC, &lds) != 0)
+        return fail(c, SOAP_EINVAL, "basis too large for the descriptor kernel's on-chip memory");
+    c->dens_cfg[0].EC = EC;
+    c->dens_cfg[0].lds = lds;
+    if (plan_groups(P, 1, c->lgrp_jac, &c->groups_jac, &EC, &lds) != 0)
+        return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
+    c->dens_cfg[1].EC = EC;
+    c->dens_cfg[1].lds = lds;
+    int EB = 16;
+    while (EB > 1 && jacobian_lds_bytes(P, EB) > JACOBIAN_LDS_BUDGET) --EB;
+    if (jacobian_lds_bytes(P, EB) > LDS_HARD_LIMIT)
+        return fail(c, SOAP_EINVAL, "basis too large for the Jacobian kernel's on-chip memory");
+    c->jac_cfg.EB = EB;
+    c->jac_cfg.lds = jacobian_lds_bytes(P, EB);
+    return SOAP_OK;
+}
+
+int upload_constants(soap_ctx *c) {
+    const int n = c->n, lw = c->lmax + 1, S = (int)c->Z.size();
+    char msg[256] = {0};
+    std::vector<double> betaC, betaCa, aprime, G, rq, c0(n), Nlm((size_t)lw * lw);
+    if (c->rbf == SOAP_RBF_GTO) {
+        betaC.resize((size_t)lw * n * n);
+        betaCa.resize((size_t)lw * n * n);
+        aprime.resize((size_t)lw * n);
+        if (soap_basis_gto(c->r_cut, n, c->lmax, c->sigma, betaC.data(), betaCa.data(), aprime.data(), c0.data(),
+                           msg, sizeof msg) != 0)
+            return fail(c, SOAP_EINVAL, "%s", msg);
+    } else {
+        G.resize((size_t)n * c->Q);
+        rq.resize(c->Q);
+        if (soap_basis_poly(c->r_cut, n, c->sigma, c->Q, G.data(), rq.data(), c0.data(), msg, sizeof msg) != 0)
+            return fail(c, SOAP_EINVAL, "%s", msg);
+    }
+    soap_basis_sh_norms(c->lmax, Nlm.data());
+    // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nlm
+    std::vector<double> all;
+    size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
+    size_t o_ba = all.size(); all.insert(all.end(), betaCa.begin(), betaCa.end());
+    size_t o_ap = all.size(); all.insert(all.end(), aprime.begin(), aprime.end());
+    size_t o_G = all.size(); all.insert(all.end(), G.begin(), G.end());
+    size_t o_rq = all.size(); all.insert(all.end(), rq.begin(), rq.end());
+    size_t o_c0 = all.size(); all.insert(all.end(), c0.begin(), c0.end());
+    size_t o_N = all.size(); all.insert(all.end(), Nlm.begin(), Nlm.end());
+    hipError_t e;
+    if ((e = c->d_const.ensure(all.size() * 8)) != hipSuccess) return hip_fail(c, e, "hipMalloc(constants)");
+    if ((e = hipMemcpy(c->d_const.p, all.data(), all.size() * 8, hipMemcpyHostToDevice)) != hipSuccess)
+        return hip_fail(c, e, "hipMemcpy(constants)");
+    double *d = c->d_const.as<double>();
+    build_feature_tables(c);
+    if ((e = c->d_fq.ensure(c->fq.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fq)");
+    if ((e = hipMemcpy(c->d_fq.p, c->fq.data(), c->fq.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+        return hip_fail(c, e, "hipMemcpy(fq)");
+    if ((e = c->d_fe.ensure(c->fe.size() * sizeof(uint2))) != hipSuccess) return hip_fail(c, e, "hipMalloc(fe)");
+    if ((e = hipMemcpy(c->d_fe.p, c->fe.data(), c->fe.size() * sizeof(uint2), hipMemcpyHostToDevice)) != hipSuccess)
+        return hip_fail(c, e, "hipMemcpy(fe)");
+    if ((e = c->d_fmap.ensure(c->fmap.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fmap)");
+    if ((e = hipMemcpy(c->d_fmap.p, c->fmap.data(), c->fmap.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+        return hip_fail(c, e, "hipMemcpy(fmap)");
+    int8_t lut[128];
+    std::memset(lut, -1, sizeof lut);
+    for (int s = 0; s < S; ++s) lut[c->Z[s]] = (int8_t)s;
+    if ((e = c->d_lut.ensure(128)) != hipSuccess) return hip_fail(c, e, "hipMalloc(lut)");
+    if ((e = hipMemcpy(c->d_lut.p, lut, 128, hipMemcpyHostToDevice)) != hipSuccess) return hip_fail(c, e, "hipMemcpy(lut)");
+
+    Params &P = c->P;
+    P.S = S;
+    P.n = n;
+    P.lmax = c->lmax;
+    P.L = lw * lw;
+    P.rbf = c->rbf;
+    P.Q = c->Q;
+    P.F = (int)c->F;
+    P.Fe = (int)c->Fe;
+    P.nq_full = c->nq_full;
+    P.sigma = c->sigma;
+    P.inv_s2 = 1.0 / (c->sigma * c->sigma);
+    P.betaC = d + o_bc;
+    P.betaCa = d + o_ba;
+    P.aprime = d + o_ap;
+    P.G = d + o_G;
+    P.rq = d + o_rq;
+    P.c0 = d + o_c0;
+    P.Nlm = d + o_N;
+    P.fq = c->d_fq.as<uint32_t>();
+    P.fe = c->d_fe.as<uint2>();
+    return plan_launches(c);
+}
+
+hipStream_t to_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+int check_ctx_device(soap_ctx *c) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(c, e, "hipGetDevice");
+    if (dev != c->device) return fail(c, SOAP_EINVAL, "current device %d differs from the context's device %d", dev, c->device);
+    return SOAP_OK;
+}
+
+Rows rows_of(const soap_ctx *c) {
+    Rows R;
+    R.n_atoms = c->n_atoms;
+    R.nc = c->nc;
+    R.centers = c->centers;
+    R.spec = c->b_spec.as<uint8_t>();
+    R.row_ptr = c->b_row.as<int64_t>();
+    R.cols = c->b_cols.as<int32_t>();
+    return R;
+}
+
+Params params_for(const soap_ctx *c, bool jac) {
+    Params P = c->P;
+    const int G = jac ? c->groups_jac : c->groups_desc;
+    P.n_groups = G;
+    for (int k = 0; k <= G; ++k) P.lgrp[k] = jac ? c->lgrp_jac[k] : c->lgrp_desc[k];
+    return P;
+}
+
+} // namespace
+
+extern "C" {
+
+int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32_t n_max, int32_t l_max, double sigma,
+                int32_t rbf, soap_ctx **out) {
+    if (!out) return SOAP_EINVAL;
+    *out = nullptr;
+    if (!species_Z || n_species < 1 || n_species > 64) return SOAP_EINVAL;
+    if (n_max < 1 || n_max > NMAX || l_max < 0 || l_max > LMAX || !(sigma > 0) || !(r_cut > 0)) return SOAP_EINVAL;
+    if (rbf != SOAP_RBF_GTO && rbf != SOAP_RBF_POLYNOMIAL) return SOAP_EINVAL;
+    if (rbf == SOAP_RBF_GTO && !(r_cut > 1.0)) return SOAP_EINVAL;
+    if (n_species * n_max > 255) return SOAP_EINVAL;
+    std::vector<int32_t> Z(species_Z, species_Z + n_species);
+    std::sort(Z.begin(), Z.end());
+    for (int k = 0; k < n_species; ++k)
+        if (Z[k] < 1 || Z[k] > 127 || (k > 0 && Z[k] == Z[k - 1])) return SOAP_EINVAL;
+    soap_ctx *c = new (std::nothrow) soap_ctx();
+    if (!c) return SOAP_ENOMEM;
+    c->Z = Z;
+    c->r_cut = r_cut;
+    c->sigma = sigma;
+    c->n = n_max;
+    c->lmax = l_max;
+    c->rbf = rbf;
+    int rc;
+    hipError_t e = hipGetDevice(&c->device);
+    if (e == hipSuccess) e = set_lds_limits();
+    if (e == hipSuccess) e = hipHostMalloc((void **)&c->h_flags, 64, hipHostMallocDefault);
+    if (e != hipSuccess) {
+        delete c;
+        return e == hipErrorOutOfMemory ? SOAP_ENOMEM : SOAP_EHIP;
+    }
+    if ((rc = upload_constants(c)) != SOAP_OK) {
+        soap_destroy(c);
+        return rc;
+    }
+    *out = c;
+    return SOAP_OK;
+}
+
+int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
+    if (!c || !key) return SOAP_EINVAL;
+    if (!std::strcmp(key, "dtype")) {
+        if (value != SOAP_FP32 && value != SOAP_FP64) return fail(c, SOAP_EINVAL, "dtype must be SOAP_FP32 or SOAP_FP64");
+        if (value != c->dtype) c->have_rows = false;
+        c->dtype = (int)value;
+        return SOAP_OK;
+    }
+    if (!std::strcmp(key, "quad_n")) {
+        if (value < 8 || value > 256) return fail(c, SOAP_EINVAL, "quad_n must be in 8..256");
+        if ((int)value == c->Q) return SOAP_OK;
+        c->Q = (int)value;
+        return upload_constants(c);
+    }
+    return fail(c, SOAP_EINVAL, "unknown option '%s'", key);
+}
+
+int64_t soap_num_features(const soap_ctx *c) { return c ? c->F : -1; }
+int64_t soap_num_edge_features(const soap_ctx *c) { return c ? c->Fe : -1; }
+
+int soap_feature_labels(const soap_ctx *c, int32_t *out) {
+    if (!c || !out) return SOAP_EINVAL;
+    const int lw = c->lmax + 1;
+    for (int q = 0; q < c->nq_full; ++q) {
+        const uint32_t f = c->fq[q];
+        for (int l = 0; l < lw; ++l) {
+            int32_t *o = out + 5 * ((int64_t)q * lw + l);
+            o[0] = f & 0xff;
+            o[1] = (f >> 8) & 0xff;
+            o[2] = (f >> 16) & 0xff;
+            o[3] = f >> 24;
+            o[4] = l;
+        }
+    }
+    return SOAP_OK;
+}
+
+int soap_feature_map(const soap_ctx *c, int32_t s, int32_t *out) {
+    if (!c || !out || s < 0 || s >= (int32_t)c->Z.size()) return SOAP_EINVAL;
+    std::memcpy(out, c->fmap.data() + (size_t)s * c->Fe, sizeof(int32_t) * c->Fe);
+    return SOAP_OK;
+}
+
+int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, const int32_t *Z_dev, int64_t n_centers,
+                         const int32_t *centers_dev, int64_t *n_edges_out, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    c->have_rows = false;
+    if (n_atoms < 1 || n_atoms > INT32_MAX || !pos_dev || !Z_dev || n_centers < 1 || !n_edges_out)
+        return fail(c, SOAP_EINVAL, "invalid arguments to soap_build_neighbors");
+    if (!centers_dev && n_centers != n_atoms)
+        return fail(c, SOAP_EINVAL, "n_centers must equal n_atoms when centers_dev is NULL");
+    int rc;
+    if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
+    hipStream_t st = to_stream(stream);
+    const bool f64 = c->dtype == SOAP_FP64;
+    int64_t H = 1024;
+    while (H < 2 * n_atoms) H <<= 1;
+    const int64_t tiles = (std::max(H, n_centers) + 2047) / 2048 + 2;
+    hipError_t e = hipSuccess;
+    auto need = [&](DevBuf &b, size_t bytes) {
+        if (e == hipSuccess) e = b.ensure(bytes);
+    };
+    need(c->b_bcount, 4 * H);
+    need(c->b_bstart, 4 * (H + 1));
+    need(c->b_bfill, 4 * H);
+    need(c->b_acell, 16 * n_atoms);
+    need(c->b_scell, 16 * n_atoms);
+    need(c->b_spos, 32 * n_atoms);
+    need(c->b_satom, 4 * n_atoms);
+    need(c->b_spec, n_atoms);
+    need(c->b_deg, 4 * n_centers);
+    need(c->b_scan, 8 * tiles);
+    need(c->b_flags, 16);
+    need(c->b_row, 8 * (n_centers + 1));
+    if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(neighbour workspace)");
+    NbrWork &w = c->nw;
+    w.H = H;
+    w.bucket_count = c->b_bcount.as<int32_t>();
+    w.bucket_start = c->b_bstart.as<int32_t>();
+    w.bucket_fill = c->b_bfill.as<int32_t>();
+    w.atom_cell = c->b_acell.as<int4>();
+    w.sorted_cell = c->b_scell.as<int4>();
+    w.sorted_pos = c->b_spos.as<double4>();
+    w.sorted_atom = c->b_satom.as<int32_t>();
+    w.deg = c->b_deg.as<int32_t>();
+    w.scan_tmp = c->b_scan.as<int64_t>();
+    w.flags = c->b_flags.as<int32_t>();
+    int64_t *row = c->b_row.as<int64_t>();
+    e = nbr_phase1(w, n_atoms, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(), n_centers,
+                   centers_dev, c->r_cut, row, st);
+    if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
+    if ((e = hipMemcpyAsync(c->h_flags, w.flags, 16, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+        (e = hipMemcpyAsync(c->h_flags + 4, row + n_centers, 8, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+        (e = hipStreamSynchronize(st)) != hipSuccess)
+        return hip_fail(c, e, "neighbour search (sync)");
+    const int32_t bad = c->h_flags[0], maxdeg = c->h_flags[1];
+    int64_t E;
+    std::memcpy(&E, c->h_flags + 4, 8);
+    if (bad & 1) return fail(c, SOAP_ESPECIES, "an atomic number is not in the species list");
+    if (bad & 2) return fail(c, SOAP_EINVAL, "a center index is out of range");
+    if (maxdeg > MAX_DEGREE)
+        return fail(c, SOAP_ECAPACITY, "a center has %d neighbours (limit %d)", maxdeg, MAX_DEGREE);
+    if ((e = c->b_cols.ensure(4 * (size_t)std::max<int64_t>(E, 1))) != hipSuccess)
+        return hip_fail(c, e, "hipMalloc(neighbour rows)");
+    e = nbr_phase2(w, n_atoms, pos_dev, f64, c->b_spec.as<uint8_t>(), n_centers, centers_dev, c->r_cut, row,
+                   c->b_cols.as<int32_t>(), st);
+    if (e != hipSuccess) return hip_fail(c, e, "neighbour rows");
+    c->have_rows = true;
+    c->n_atoms = n_atoms;
+    c->nc = n_centers;
+    c->E = E;
+    c->pos = pos_dev;
+    c->Zdev = Z_dev;
+    c->centers = centers_dev;
+    c->built_f64 = f64;
+    *n_edges_out = E;
+    return SOAP_OK;
+}
+
+int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    hipStream_t st = to_stream(stream);
+    hipError_t e = hipSuccess;
+    if (row_ptr_dev)
+        e = hipMemcpyAsync(row_ptr_dev, c->b_row.p, 8 * (c->nc + 1), hipMemcpyDeviceToDevice, st);
+    if (e == hipSuccess && cols_dev && c->E > 0)
+        e = hipMemcpyAsync(cols_dev, c->b_cols.p, 4 * c->E, hipMemcpyDeviceToDevice, st);
+    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_get_neighbors");
+}
+
+static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jself, void *stream) {
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    int rc;
+    if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
+    const Params P = params_for(c, jac);
+    double *scratch = nullptr;
+    if (jac) {
+        hipError_t e = c->b_cscratch.ensure(8 * (size_t)c->nc * P.S * P.n * P.L);
+        if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
+        scratch = c->b_cscratch.as<double>();
+    }
+    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0], desc, c_out,
+                                  jself, scratch, to_stream(stream));
+    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "density kernel");
+}
+
+int soap_compute(soap_ctx *c, void *desc_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!desc_dev) return fail(c, SOAP_EINVAL, "desc_dev is NULL");
+    return run_density(c, false, desc_dev, nullptr, nullptr, stream);
+}
+
+int soap_coefficients(soap_ctx *c, void *c_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!c_dev) return fail(c, SOAP_EINVAL, "c_dev is NULL");
+    return run_density(c, false, nullptr, c_dev, nullptr, stream);
+}
+
+int soap_derivatives(soap_ctx *c, void *desc_dev, void *jac_edge_dev, void *jac_self_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!desc_dev || !jac_self_dev || (!jac_edge_dev && c->E > 0))
+        return fail(c, SOAP_EINVAL, "output pointer is NULL");
+    int rc = run_density(c, true, desc_dev, nullptr, jac_self_dev, stream);
+    if (rc != SOAP_OK) return rc;
+    if (c->E == 0) return SOAP_OK;
+    hipError_t e = launch_jacobian(c->P, rows_of(c), c->pos, c->built_f64, c->jac_cfg, c->b_cscratch.as<double>(),
+                                   jac_edge_dev, to_stream(stream));
+    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "Jacobian kernel");
+}
+
+int soap_scatter_dense(soap_ctx *c, const void *jac_edge_dev, const void *jac_self_dev, void *dense_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    if (!jac_self_dev || !dense_dev || (!jac_edge_dev && c->E > 0)) return fail(c, SOAP_EINVAL, "NULL pointer");
+    hipStream_t st = to_stream(stream);
+    const size_t elt = c->built_f64 ? 8 : 4;
+    hipError_t e = hipMemsetAsync(dense_dev, 0, elt * (size_t)c->nc * c->n_atoms * 3 * c->F, st);
+    if (e == hipSuccess)
+        e = launch_scatter_dense(c->P, rows_of(c), c->built_f64, jac_edge_dev, jac_self_dev, c->d_fmap.as<int32_t>(),
+                                 dense_dev, st);
+    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_scatter_dense");
+}
+
+const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : "null context"; }
+
+void soap_destroy(soap_ctx *c) {
+    if (!c) return;
+    (void)hipDeviceSynchronize();
+    for (DevBuf *b : {&c->d_const, &c->d_fq, &c->d_fe, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
+                      &c->b_acell, &c->b_scell, &c->b_spos, &c->b_satom, &c->b_deg, &c->b_scan, &c->b_flags,
+                      &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch})
+        b->release();
+    if (c->h_flags) (void)hipHostFree(c->h_flags);
+    delete c;
+}
+
+} // extern "C"

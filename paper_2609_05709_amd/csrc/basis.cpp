@@ -1,0 +1,226 @@
+// Host-side basis constants in 113-bit binary floating point (__float128).
+//
+// The Loewdin orthonormalisation of both radial bases is severely
+// ill-conditioned (Sec. 3.1 notes coefficients of order 1e6 and heavy
+// cancellation; the overlap matrices reach condition numbers of 1e15 (GTO,
+// r_cut 6, n_max 12) and 1e17 (polynomial, n_max 12)), so the inverse square
+// roots and everything that sums Loewdin-weighted terms into a table are
+// formed here in quad precision and rounded once to float64.
+//
+// Compiled by the host C++ compiler only (no device code).
+#include "basis.h"
+
+#include <quadmath.h>
+
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+namespace {
+
+typedef __float128 q128;
+
+const q128 PI_Q = M_PIq;
+
+// Cyclic Jacobi eigen-decomposition of a symmetric n x n matrix A (row major,
+// destroyed).  V receives the eigenvectors as columns, w the eigenvalues.
+bool jacobi_eigen(int n, std::vector<q128> &A, std::vector<q128> &V, std::vector<q128> &w) {
+    V.assign((size_t)n * n, 0);
+    for (int i = 0; i < n; ++i) V[(size_t)i * n + i] = 1;
+    for (int sweep = 0; sweep < 200; ++sweep) {
+        q128 off = 0, diag = 0;
+        for (int p = 0; p < n; ++p) {
+            diag += A[(size_t)p * n + p] * A[(size_t)p * n + p];
+            for (int q = p + 1; q < n; ++q) off += A[(size_t)p * n + q] * A[(size_t)p * n + q];
+        }
+        if (off <= diag * (q128)1e-66Q) break;
+        for (int p = 0; p < n; ++p)
+            for (int q = p + 1; q < n; ++q) {
+                q128 apq = A[(size_t)p * n + q];
+                if (apq == 0) continue;
+                q128 app = A[(size_t)p * n + p], aqq = A[(size_t)q * n + q];
+                q128 theta = (aqq - app) / (2 * apq);
+                q128 t = (theta >= 0 ? 1 : -1) / (fabsq(theta) + sqrtq(theta * theta + 1));
+                q128 c = 1 / sqrtq(t * t + 1), s = t * c;
+                for (int k = 0; k < n; ++k) { // columns p, q
+                    q128 akp = A[(size_t)k * n + p], akq = A[(size_t)k * n + q];
+                    A[(size_t)k * n + p] = c * akp - s * akq;
+                    A[(size_t)k * n + q] = s * akp + c * akq;
+                }
+                for (int k = 0; k < n; ++k) { // rows p, q
+                    q128 apk = A[(size_t)p * n + k], aqk = A[(size_t)q * n + k];
+                    A[(size_t)p * n + k] = c * apk - s * aqk;
+                    A[(size_t)q * n + k] = s * apk + c * aqk;
+                }
+                for (int k = 0; k < n; ++k) {
+                    q128 vkp = V[(size_t)k * n + p], vkq = V[(size_t)k * n + q];
+                    V[(size_t)k * n + p] = c * vkp - s * vkq;
+                    V[(size_t)k * n + q] = s * vkp + c * vkq;
+                }
+            }
+    }
+    w.resize(n);
+    for (int i = 0; i < n; ++i) w[i] = A[(size_t)i * n + i];
+    return true;
+}
+
+// Principal inverse square root of a symmetric positive-definite matrix.
+bool inv_sqrt_spd(int n, const std::vector<q128> &S, std::vector<q128> &X) {
+    std::vector<q128> A = S, V, w;
+    jacobi_eigen(n, A, V, w);
+    for (int i = 0; i < n; ++i)
+        if (!(w[i] > 0)) return false;
+    X.assign((size_t)n * n, 0);
+    for (int i = 0; i < n; ++i)
+        for (int j = 0; j < n; ++j) {
+            q128 acc = 0;
+            for (int k = 0; k < n; ++k) acc += V[(size_t)i * n + k] * V[(size_t)j * n + k] / sqrtq(w[k]);
+            X[(size_t)i * n + j] = acc;
+        }
+    return true;
+}
+
+q128 half_int_pow(q128 x, int l) { // x^(l + 3/2)
+    return powq(x, (q128)l) * x * sqrtq(x);
+}
+
+void set_err(char *err, int errlen, const char *msg) {
+    if (err && errlen > 0) {
+        std::strncpy(err, msg, (size_t)errlen - 1);
+        err[errlen - 1] = 0;
+    }
+}
+
+} // namespace
+
+extern "C" int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, double *betaC, double *betaCa,
+                              double *aprime, double *c0, char *err, int errlen) {
+    const int n = n_max;
+    const q128 rc = r_cut, sg = sigma, s2 = sg * sg;
+    std::vector<q128> z(n);
+    for (int k = 0; k < n; ++k) z[k] = (n == 1) ? (q128)1 : 1 + (q128)k * (rc - 1) / (q128)(n - 1);
+    const q128 ln1000 = logq((q128)1000);
+    const q128 pref = powq(2 * PI_Q, (q128)1.5Q) * s2 * sg; // (2 pi)^{3/2} sigma^3
+    std::vector<q128> beta0;
+    for (int l = 0; l <= l_max; ++l) {
+        // Eq. (gto-alphas): alpha_kl = -ln(1e-3 / z_k^l) / z_k^2
+        std::vector<q128> al(n);
+        for (int k = 0; k < n; ++k) al[k] = (ln1000 + (q128)l * logq(z[k])) / (z[k] * z[k]);
+        // Eq. (gto-overlap-approx): Gamma(l+3/2) / (2 (a_k + a_k')^{l+3/2})
+        q128 gam = sqrtq(PI_Q);
+        for (int j = 0; j <= l; ++j) gam *= ((q128)j + (q128)0.5Q);
+        std::vector<q128> S((size_t)n * n), B;
+        for (int a = 0; a < n; ++a)
+            for (int b = 0; b < n; ++b) S[(size_t)a * n + b] = gam / (2 * half_int_pow(al[a] + al[b], l));
+        if (!inv_sqrt_spd(n, S, B)) { // Eq. (gto-lowdin)
+            set_err(err, errlen, "GTO overlap matrix is not positive definite");
+            return -1;
+        }
+        if (l == 0) beta0 = B;
+        for (int k = 0; k < n; ++k) {
+            q128 den = 1 + 2 * s2 * al[k];
+            q128 ap = al[k] / den;              // envelope exponent of Eq. (gto-coefficients)
+            q128 C = pref / half_int_pow(den, l); // prefactor of Eq. (gto-coefficients)
+            aprime[l * n + k] = (double)ap;
+            for (int a = 0; a < n; ++a) {
+                q128 bc = B[(size_t)a * n + k] * C;
+                betaC[((size_t)l * n + a) * n + k] = (double)bc;
+                betaCa[((size_t)l * n + a) * n + k] = (double)(-2 * bc * ap);
+            }
+        }
+    }
+    // on-site term: sqrt(2) pi sigma^3 sum_k beta^0_nk / (1 + 2 sigma^2 alpha_k0)^{3/2}
+    for (int a = 0; a < n; ++a) {
+        q128 acc = 0;
+        for (int k = 0; k < n; ++k) {
+            q128 al = ln1000 / (z[k] * z[k]);
+            acc += beta0[(size_t)a * n + k] / half_int_pow(1 + 2 * s2 * al, 0);
+        }
+        c0[a] = (double)(sqrtq((q128)2) * PI_Q * s2 * sg * acc);
+    }
+    return 0;
+}
+
+extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n, double *G, double *rq_out,
+                               double *c0, char *err, int errlen) {
+    const int n = n_max, Q = quad_n;
+    const q128 rc = r_cut, s2 = (q128)sigma * (q128)sigma;
+    // Eqs. (poly-norm), (poly-overlap); W = S^{-1/2}
+    std::vector<q128> N(n), S((size_t)n * n), W;
+    for (int a = 0; a < n; ++a) {
+        int k = a + 1;
+        N[a] = sqrtq(powq(rc, (q128)(2 * k + 5)) / (q128)(2 * k + 5));
+    }
+    for (int a = 0; a < n; ++a)
+        for (int b = 0; b < n; ++b) {
+            int k = a + 1, kp = b + 1;
+            S[(size_t)a * n + b] = sqrtq((q128)((5 + 2 * k) * (5 + 2 * kp))) / (q128)(5 + k + kp);
+        }
+    if (!inv_sqrt_spd(n, S, W)) {
+        set_err(err, errlen, "polynomial overlap matrix is not positive definite");
+        return -1;
+    }
+    // Gauss-Legendre nodes on [-1, 1] by Newton iteration on P_Q
+    std::vector<q128> t(Q), wt(Q);
+    for (int i = 0; i < Q; ++i) {
+        q128 x = std::cos(M_PI * (i + 0.75) / (Q + 0.5));
+        q128 dp = 1;
+        for (int it = 0; it < 100; ++it) {
+            q128 p0 = 1, p1 = x;
+            for (int k = 2; k <= Q; ++k) {
+                q128 p2 = ((2 * k - 1) * x * p1 - (k - 1) * p0) / k;
+                p0 = p1;
+                p1 = p2;
+            }
+            dp = (q128)Q * (x * p1 - p0) / (x * x - 1);
+            q128 dx = p1 / dp;
+            x -= dx;
+            if (fabsq(dx) < (q128)1e-33Q) break;
+        }
+        q128 p0 = 1, p1 = x;
+        for (int k = 2; k <= Q; ++k) {
+            q128 p2 = ((2 * k - 1) * x * p1 - (k - 1) * p0) / k;
+            p0 = p1;
+            p1 = p2;
+        }
+        dp = (q128)Q * (x * p1 - p0) / (x * x - 1);
+        t[i] = x;
+        wt[i] = 2 / ((1 - x * x) * dp * dp);
+    }
+    // G[n][q] = 4 pi w_q r_q^2 g_n(r_q), g_n of Eq. (poly-basis) summed in quad
+    const q128 fourpi = 4 * PI_Q;
+    for (int q = 0; q < Q; ++q) {
+        q128 r = rc * (t[q] + 1) / 2, w = rc * wt[q] / 2;
+        rq_out[q] = (double)r;
+        for (int a = 0; a < n; ++a) {
+            q128 g = 0;
+            for (int b = 0; b < n; ++b) g += W[(size_t)a * n + b] * powq(rc - r, (q128)(b + 3)) / N[b];
+            G[(size_t)a * Q + q] = (double)(fourpi * w * r * r * g);
+        }
+    }
+    // on-site term: sqrt(4 pi) sum_q w_q r_q^2 g_n(r_q) exp(-r_q^2 / 2 sigma^2)
+    for (int a = 0; a < n; ++a) {
+        q128 acc = 0;
+        for (int q = 0; q < Q; ++q) {
+            q128 r = rc * (t[q] + 1) / 2, w = rc * wt[q] / 2;
+            q128 g = 0;
+            for (int b = 0; b < n; ++b) g += W[(size_t)a * n + b] * powq(rc - r, (q128)(b + 3)) / N[b];
+            acc += w * r * r * g * expq(-r * r / (2 * s2));
+        }
+        c0[a] = (double)(sqrtq(fourpi) * acc);
+    }
+    return 0;
+}
+
+// Normalisation of the real solid harmonics: N[l][m] for 0 <= m <= l,
+// sqrt((2l+1)/(4 pi) (l-m)!/(l+m)!) times sqrt(2) when m > 0.
+extern "C" void soap_basis_sh_norms(int l_max, double *Nlm) {
+    for (int l = 0; l <= l_max; ++l)
+        for (int m = 0; m <= l; ++m) {
+            q128 ratio = 1;
+            for (int k = l - m + 1; k <= l + m; ++k) ratio /= (q128)k;
+            q128 v = sqrtq((q128)(2 * l + 1) / (4 * PI_Q) * ratio);
+            if (m > 0) v *= sqrtq((q128)2);
+            Nlm[l * (l_max + 1) + m] = (double)v;
+        }
+}

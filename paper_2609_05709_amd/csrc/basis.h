@@ -1,0 +1,29 @@
+// Host-side basis constants (see basis.cpp).  Internal to the library.
+#pragma once
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+// GTO basis (Sec. 2.2).  Outputs, all row-major:
+//   betaC [l][n][k] = beta^l_nk * (2 pi)^{3/2} sigma^3 / (1 + 2 sigma^2 alpha_kl)^{l+3/2}
+//   betaCa[l][n][k] = -2 * betaC[l][n][k] * aprime[l][k]
+//   aprime[l][k]    = alpha_kl / (1 + 2 sigma^2 alpha_kl)
+//   c0[n]           = on-site l = 0 term of Eq. (gto-coefficients)
+// so that B_nl(r) = sum_k betaC e^{-aprime r^2} and c_nlm = B_nl r^l Y_lm.
+// Returns 0, or -1 with a message in err.
+int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, double *betaC, double *betaCa,
+                   double *aprime, double *c0, char *err, int errlen);
+
+// Polynomial basis (Sec. 2.3) with a quad_n-point Gauss-Legendre rule on
+// [0, r_cut]:  G[n][q] = 4 pi w_q r_q^2 g_n(r_q),  rq[q] = r_q,
+// c0[n] = on-site l = 0 term.  Returns 0 or -1.
+int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n, double *G, double *rq, double *c0,
+                    char *err, int errlen);
+
+// Real solid-harmonic normalisation N[l][m], 0 <= m <= l, row stride l_max+1.
+void soap_basis_sh_norms(int l_max, double *Nlm);
+
+#ifdef __cplusplus
+}
+#endif

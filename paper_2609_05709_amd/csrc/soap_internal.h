@@ -1,0 +1,87 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace soap {
+
+constexpr int NMAX = 16;       // largest n_max
+constexpr int LMAX = 14;       // largest l_max
+constexpr int LT_MAX = LMAX + 2;
+constexpr int MAX_GROUPS = LMAX + 1;
+constexpr int MAX_DEGREE = 2048;
+
+// Everything the descriptor kernels need about the basis; passed by value.
+struct Params {
+    int S, n, lmax, L, rbf, Q; // L = (lmax+1)^2, rbf 0 = GTO, 1 = polynomial
+    int F, Fe, nq_full;        // features, edge features, (mu,nu,n,n') combinations
+    double sigma, inv_s2;      // 1 / sigma^2
+    const double *betaC;       // GTO [l][n][k]
+    const double *betaCa;      // GTO [l][n][k]
+    const double *aprime;      // GTO [l][k]
+    const double *G;           // polynomial [n][Q], includes 4 pi
+    const double *rq;          // polynomial [Q]
+    const double *c0;          // on-site term [n]
+    const double *Nlm;         // [lmax+1][lmax+1]
+    const uint32_t *fq;        // [nq_full] mu | nu<<8 | n<<16 | n'<<24
+    const uint2 *fe;           // [S][Fe] edge-feature terms
+    int n_groups;              // l-groups of the density kernel
+    int lgrp[MAX_GROUPS + 1];  // group g covers l in [lgrp[g], lgrp[g+1])
+};
+
+// Neighbour rows of the current structure.
+struct Rows {
+    int64_t n_atoms, nc;
+    const int32_t *centers; // NULL = identity
+    const uint8_t *spec;    // species index per atom
+    const int64_t *row_ptr; // [nc+1]
+    const int32_t *cols;    // [E]
+};
+
+// ---- neighbour search (neighbors.hip) ----
+struct NbrWork {
+    int64_t H;              // hash buckets (power of two)
+    int32_t *bucket_count;  // [H]
+    int32_t *bucket_start;  // [H+1]
+    int32_t *bucket_fill;   // [H]
+    int4 *atom_cell;        // [n_atoms] cx, cy, cz, bucket
+    int4 *sorted_cell;      // [n_atoms]
+    double4 *sorted_pos;    // [n_atoms]
+    int32_t *sorted_atom;   // [n_atoms]
+    int32_t *deg;           // [nc]
+    int64_t *scan_tmp;      // block sums
+    int32_t *flags;         // [4]: error bits, max degree
+};
+
+hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const int32_t *Z,
+                      const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers, double r_cut,
+                      int64_t *row_ptr, hipStream_t st);
+hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const uint8_t *spec,
+                      int64_t nc, const int32_t *centers, double r_cut, const int64_t *row_ptr, int32_t *cols,
+                      hipStream_t st);
+
+// ---- descriptor kernels (soap_kernels.hip) ----
+struct DensityLaunch {
+    int EC;          // edges staged per chunk
+    size_t lds;      // dynamic LDS bytes
+};
+struct JacLaunch {
+    int EB;
+    size_t lds;
+};
+
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int EC);
+size_t jacobian_lds_bytes(const Params &P, int EB);
+hipError_t set_lds_limits();
+
+// desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)
+hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
+                          const DensityLaunch &cfg, void *desc, void *c_out, void *jself, double *c_scratch,
+                          hipStream_t st);
+hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
+                           const double *c_scratch, void *jedge, hipStream_t st);
+hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,
+                                const int32_t *fmap, void *dense, hipStream_t st);
+
+} // namespace soap

@@ -1,0 +1,144 @@
+"""Edge cases of the HIP path, compared with the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_05709_amd import workloads
+from tests.parity import TOL, check_rows, gpu_run, jacobian_errors, row_errors
+
+pytestmark = pytest.mark.gpu
+
+
+def _wl(species=(1, 8), rbf="gto", r_cut=5.0, sigma=0.5, n_max=4, l_max=4):
+    return workloads.Workload("edge", tuple(species), rbf, r_cut, sigma, n_max, l_max, True, ("none",))
+
+
+def _st(pos, Z):
+    return workloads.Structure(np.asarray(pos, dtype=np.float32), np.asarray(Z, dtype=np.int32), 0.0, 0)
+
+
+def _compare(wl, st, dtype, centers=None):
+    g = gpu_run(wl, st, dtype, centers=centers)
+    o = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    cen = np.arange(st.n_atoms) if centers is None else np.asarray(centers)
+    check_rows(g, st, wl.r_cut, cen, wl.species)
+    ref = o.compute(st.pos64, st.Z, centers=cen, jacobian=True)
+    assert row_errors(g["desc"], ref["desc"]).max() < TOL[dtype]
+    assert jacobian_errors(g, ref, st, wl.species, list(range(len(cen))), cen) < TOL[dtype]
+    return g, ref
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_isolated_atoms_and_single_atom(rbf):
+    wl = _wl(rbf=rbf)
+    _compare(wl, _st([[0, 0, 0], [20, 0, 0], [0, 30, 0]], [1, 8, 1]), "float32")
+    g, _ = _compare(wl, _st([[1.0, 2.0, 3.0]], [8]), "float64")
+    assert g["E"] == 0
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_coincident_atoms(rbf):
+    wl = _wl(rbf=rbf)
+    pos = [[0, 0, 0], [0, 0, 0], [1.1, 0.3, -0.4], [1.1, 0.3, -0.4], [-0.9, 1.2, 0.2]]
+    _compare(wl, _st(pos, [8, 1, 1, 8, 1]), "float64")
+
+
+def test_species_absent_from_structure_and_center_subset():
+    wl = _wl(species=(1, 6, 8))
+    st = workloads.random_small(30, 7, 3.5, species=(1, 8))
+    _compare(wl, st, "float32", centers=[5, 0, 17, 29, 5])
+
+
+@pytest.mark.parametrize("nl", [(1, 0), (1, 5), (6, 0)])
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_minimal_basis(nl, rbf):
+    wl = _wl(rbf=rbf, n_max=nl[0], l_max=nl[1])
+    st = workloads.random_small(25, 11, 3.0, species=(1, 8))
+    _compare(wl, st, "float64")
+
+
+def test_neighbors_at_exact_cutoff():
+    """Lattice points at exactly r_cut are excluded (strict <); float32 points a
+    few ulp inside and outside are classified as the oracle does."""
+    rc = 5.0
+    pts = [[0, 0, 0], [rc, 0, 0], [0, rc, 0], [0, 0, -rc], [rc, rc, 0]]
+    for k in range(1, 6):
+        v = np.nextafter(np.float32(rc), np.float32(0), dtype=np.float32)
+        for _ in range(k - 1):
+            v = np.nextafter(v, np.float32(0), dtype=np.float32)
+        pts.append([0, 0, float(v) + 11.0 * k])
+        pts.append([0, 0, 11.0 * k])
+        w = np.nextafter(np.float32(rc), np.float32(10), dtype=np.float32)
+        pts.append([float(w) + 40.0, 0, 11.0 * k])
+        pts.append([40.0, 0, 11.0 * k])
+    # 3-4-5 triangles: distance exactly 5 in every coordinate split
+    pts += [[100, 100, 100], [103, 104, 100], [100, 103, 104], [96, 100, 97]]
+    st = _st(pts, [1] * len(pts))
+    wl = _wl(species=(1,), r_cut=rc, n_max=2, l_max=2)
+    g = gpu_run(wl, st, "float32")
+    check_rows(g, st, rc, np.arange(st.n_atoms), wl.species)
+    g64 = gpu_run(wl, st, "float64")
+    check_rows(g64, st, rc, np.arange(st.n_atoms), wl.species)
+
+
+def test_unknown_species_is_an_error():
+    import torch
+    from paper_2609_05709_amd.soap import SOAP_ESPECIES, Soap, SoapError
+    sp = Soap((1, 8), 5.0, 3, 3, 0.5)
+    pos = torch.zeros((3, 3), device="cuda")
+    pos[1, 0] = 1.0
+    pos[2, 1] = 1.0
+    Z = torch.tensor([1, 6, 8], dtype=torch.int32, device="cuda")
+    with pytest.raises(SoapError) as ei:
+        sp.build_neighbors(pos, Z)
+    assert ei.value.code == SOAP_ESPECIES
+    with pytest.raises(SoapError):
+        sp.compute()  # no neighbour list after the failed build
+    sp.close()
+
+
+def test_bad_arguments_rejected():
+    import torch
+    from paper_2609_05709_amd.soap import SOAP_EINVAL, Soap, SoapError
+    for args in [((1,), 1.0, 3, 3, 0.5, "gto"), ((1,), 5.0, 0, 3, 0.5, "gto"), ((1,), 5.0, 3, -1, 0.5, "gto"),
+                 ((1,), 5.0, 3, 3, 0.0, "gto"), ((1,), 5.0, 17, 3, 0.5, "gto")]:
+        with pytest.raises(SoapError) as ei:
+            Soap(*args)
+        assert ei.value.code == SOAP_EINVAL
+    sp = Soap((1, 8), 5.0, 3, 3, 0.5)
+    with pytest.raises(SoapError):
+        sp.build_neighbors(torch.zeros((4, 3), device="cuda"), torch.ones(4, dtype=torch.int32, device="cuda"),
+                           torch.tensor([0, 7], dtype=torch.int32, device="cuda"))
+    sp.close()
+
+
+def test_repeatable_bitwise():
+    wl = workloads.WATER64
+    st = wl.structure()
+    a = gpu_run(wl, st, "float32")
+    b = gpu_run(wl, st, "float32")
+    assert np.array_equal(a["desc"], b["desc"])
+    for c in range(st.n_atoms):
+        assert np.array_equal(a["jedge"][c], b["jedge"][c]) and np.array_equal(a["jself"][c], b["jself"][c])
+
+
+def test_dense_scatter_matches_blocks():
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    wl = workloads.WATER64
+    st = wl.structure()
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    sp.build_neighbors(torch.from_numpy(st.pos).cuda(), torch.from_numpy(st.Z).cuda())
+    desc, je, js = sp.derivatives()
+    dense = sp.scatter_dense(je, js).cpu().numpy()
+    row, cols = [t.cpu().numpy() for t in sp.neighbors()]
+    je, js = je.cpu().numpy(), js.cpu().numpy()
+    spec = {z: k for k, z in enumerate(sorted(wl.species))}
+    for c in range(0, st.n_atoms, 7):
+        expect = np.zeros((st.n_atoms, 3, sp.n_features), dtype=np.float32)
+        expect[c] = js[c]
+        for e in range(row[c], row[c + 1]):
+            j = cols[e]
+            expect[j][:, sp.feature_map(spec[int(st.Z[j])])] = je[e]
+        assert np.array_equal(dense[c], expect)
+    sp.close()
