@@ -160,6 +160,7 @@ class Soap:
             nc = centers.shape[0]
             cptr = centers.data_ptr()
         E = ctypes.c_int64()
+        self.E = self.n_centers = None
         self._check(self._L.soap_build_neighbors(self._h, pos.shape[0], pos.data_ptr(), Z.data_ptr(), nc, cptr,
                                                  ctypes.byref(E), _stream()))
         self._keep = (pos, Z, centers)  # the library reads these in later calls
@@ -168,6 +169,8 @@ class Soap:
 
     def neighbors(self):
         import torch
+        if self.E is None:
+            raise SoapError(SOAP_ESTATE, "no neighbour list: call build_neighbors first")
         row = torch.empty(self.n_centers + 1, dtype=torch.int64, device="cuda")
         cols = torch.empty(max(self.E, 1), dtype=torch.int32, device="cuda")
         self._check(self._L.soap_get_neighbors(self._h, row.data_ptr(), cols.data_ptr(), _stream()))
@@ -176,6 +179,8 @@ class Soap:
     # -- outputs ----------------------------------------------------------------
     def _out(self, t, shape):
         import torch
+        if self.E is None:
+            raise SoapError(SOAP_ESTATE, "no neighbour list: call build_neighbors first")
         if t is None:
             return torch.empty(shape, dtype=self.dtype, device="cuda")
         if tuple(t.shape) != tuple(shape) or t.dtype != self.dtype or not t.is_contiguous():
