@@ -1,0 +1,206 @@
+"""Benchmark of the SOAP descriptor + analytic Jacobian hot path on one MI355X.
+
+One step = one pass of the whole path over the structure: neighbour search
+(soap_build_neighbors), then descriptor + Jacobian (soap_derivatives), or the
+descriptor alone (soap_compute) for descriptor-only workloads.  Inputs are
+resident in HBM before the timed region; output buffers are allocated once.
+
+Default workload: the 3000-atom water cluster (1000 H2O), GTO basis,
+r_cut 6 A, sigma 0.5 A, n_max 8, l_max 6, descriptor + Jacobian, float32
+outputs.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--dtype float32|float64]
+                  [--grid OUT.jsonl] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SOAP atoms/s (desc+Jacobian), 3000-atom water, per (n_max,l_max); % roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP64_PEAK_TFLOPS = 78.6        # MI355X FP64 vector
+
+
+def workload_by_name(name):
+    from paper_2609_05709_amd import workloads as w
+    table = {"water64": w.WATER64, "water1000": w.WATER1000, "chno4096": w.CHNO4096, "water1m": w.WATER1M}
+    if name in table:
+        return table[name]
+    # water1000_<rbf>_n<N>l<L>, e.g. water1000_polynomial_n12l12
+    parts = name.split("_")
+    if parts[0] == "water1000" and len(parts) == 3:
+        nl = parts[2]
+        n, l = nl[1:].split("l")
+        return w.WATER1000.with_basis(int(n), int(l), parts[1])
+    raise SystemExit(f"unknown workload {name}")
+
+
+def algorithmic(wl, st_n, E, F, Fe, out_bytes, jac):
+    """Algorithmic HBM bytes per step and per kernel launch: the outputs the
+    method must write (descriptor rows, the center blocks and the neighbour
+    blocks restricted to the species pairs that can be non-zero)."""
+    desc = st_n * F * out_bytes
+    self_blocks = st_n * 3 * F * out_bytes if jac else 0
+    edge_blocks = E * 3 * Fe * out_bytes if jac else 0
+    return dict(step=desc + self_blocks + edge_blocks, density=desc + self_blocks, jacobian=edge_blocks)
+
+
+def density_flops(wl, E, n_centers, F):
+    """Algorithmic float64 operations of the descriptor-only density kernel
+    (GTO), per step: per edge, the real solid harmonics (about 3 flops per
+    (l, m)), the radial factors B_nl = sum_k beta C exp(-a' r^2) (2 n^2 (l+1)
+    flops plus n (l+1) exponentials, each counted as 1), and the projection
+    c += B Y (2 n L flops); per center, the power spectrum (2 (2l+1) flops per
+    feature)."""
+    n, l = wl.n_max, wl.l_max
+    L = (l + 1) ** 2
+    per_edge = 3 * L + 2 * n * n * (l + 1) + n * (l + 1) + 2 * n * L
+    per_center = sum(2 * (2 * ll + 1) for ll in range(l + 1)) * (F // (l + 1))
+    return E * per_edge + n_centers * per_center
+
+
+def cpu_baseline(wl, st, budget_s=12.0):
+    """The oracle as it stands, on the host cores, over a bounded sample of
+    centers (batches of 128 until ~budget_s of wall time)."""
+    import oracle
+    o = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    rng = np.random.default_rng(12345)
+    order = rng.permutation(st.n_atoms)
+    done, t0 = 0, time.perf_counter()
+    while done < st.n_atoms and time.perf_counter() - t0 < budget_s:
+        batch = np.sort(order[done:done + 128])
+        o.compute(st.pos64, st.Z, centers=batch, jacobian=wl.jacobian)
+        done += len(batch)
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": done / dt, "unit": "atoms/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {st.n_atoms} centers (seeded random), neighbour search + "
+                      f"{'descriptor + Jacobian' if wl.jacobian else 'descriptor'}, {dt:.1f} s"}
+
+
+def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    st = wl.structure()
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    out_bytes = 8 if dtype == "float64" else 4
+    dev = torch.device("cuda:0")
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to(dev, tdt)
+    Z = torch.from_numpy(st.Z).to(dev)
+    E = sp.build_neighbors(pos, Z)
+    nc = st.n_atoms
+    desc = torch.empty((nc, sp.n_features), dtype=tdt, device=dev)
+    if wl.jacobian:
+        jedge = torch.empty((E, 3, sp.n_edge_features), dtype=tdt, device=dev)
+        jself = torch.empty((nc, 3, sp.n_features), dtype=tdt, device=dev)
+
+    def step():
+        sp.build_neighbors(pos, Z)
+        if wl.jacobian:
+            sp.derivatives(desc, jedge, jself)
+        else:
+            sp.compute(desc)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    sp.timing(reset=True)
+    sp.set_timing(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(stop)
+    seg_ms, seg_n = sp.timing(reset=True)
+    sp.set_timing(False)
+    ms_step = ms_total / steps
+
+    alg = algorithmic(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, wl.jacobian)
+    kern = {"neighbors": seg_ms[0] / max(seg_n[0], 1), "density": seg_ms[1] / max(seg_n[1], 1),
+            "jacobian": seg_ms[2] / max(seg_n[2], 1)}
+    if wl.jacobian:
+        # the edge-block writes dominate: HBM-bound kernel
+        t = kern["jacobian"] * 1e-3
+        roof = {"kernel": "k_jacobian", "bound": "hbm", "achieved": alg["jacobian"] / t / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "traffic": None}
+    else:
+        fl = density_flops(wl, E, nc, sp.n_features)
+        t = kern["density"] * 1e-3
+        roof = {"kernel": "k_density", "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "traffic": None}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    line = {
+        "metric": METRIC,
+        "value": nc * steps / (ms_total * 1e-3),
+        "unit": "atoms/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
+                   "l_max": wl.l_max, "r_cut": wl.r_cut, "sigma": wl.sigma, "species": list(wl.species),
+                   "output": dtype, "jacobian": wl.jacobian, "features": sp.n_features,
+                   "edge_features": sp.n_edge_features},
+        "kernel_ms": kern,
+        "step_alg_bytes": alg["step"],
+        "step_hbm_fraction": alg["step"] / (ms_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
+        "wall_s": wall,
+        "roofline": roof,
+    }
+    sp.close()
+    if with_cpu:
+        line["cpu_baseline"] = cpu_baseline(wl, st)
+    return line
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="water1000")
+    ap.add_argument("--dtype", default="float32", choices=["float32", "float64"])
+    ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for both bases; write JSONL here")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the SOAP path here is built and timed on a single MI355X "
+              "(centers shard across GPUs without communication; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    if a.grid:
+        from paper_2609_05709_amd import workloads as w
+        with open(a.grid, "w") as f:
+            for wl in w.hyperparameter_grid():
+                line = run(wl, max(3, a.steps // 4), 2, a.dtype, with_cpu=False)
+                f.write(json.dumps(line) + "\n")
+                f.flush()
+                print(f"{wl.name}: {line['value']:.4g} atoms/s, {line['ms_per_step']:.3f} ms, "
+                      f"jac {line['roofline']['frac']:.3f} of HBM", flush=True)
+        return
+    wl = workload_by_name(a.workload)
+    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -86,7 +86,9 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  * Set an option.  Keys:
  *   "dtype"  : SOAP_FP32 or SOAP_FP64 (default SOAP_FP32);
  *   "quad_n" : Gauss-Legendre order for the polynomial basis, 8..256
- *              (default 64); rebuilds the quadrature table.
+ *              (default 64); rebuilds the quadrature table;
+ *   "timing" : 1 = record HIP events around every segment of later calls
+ *              (see soap_timing), 0 = off (default).
  * Options take effect for calls made after this one; changing "dtype"
  * discards the neighbour list.  Errors: SOAP_EINVAL.
  */
@@ -182,7 +184,20 @@ int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *ja
 int soap_scatter_dense(soap_ctx *ctx, const void *jac_edge_dev, const void *jac_self_dev, void *dense_dev,
                        void *stream);
 
-/* Message for the last error on this context ("" if none). */
+/*
+ * Per-segment device times of the calls made while option "timing" was on
+ * (the per-segment profiler of Sec. 3.1).  Segments: 0 = neighbour search
+ * (soap_build_neighbors, including its one host synchronisation),
+ * 1 = density kernel (coefficients, power spectrum, center Jacobian block),
+ * 2 = edge Jacobian kernel.  ms_out[3] receives the summed milliseconds and
+ * count_out[3] (may be NULL) the number of timed launches per segment.
+ * Synchronises on the recorded events; reset != 0 clears the records.
+ * Errors: SOAP_EHIP.
+ */
+int soap_timing(soap_ctx *ctx, double *ms_out, int64_t *count_out, int32_t reset);
+
+/* Message for the last error on this context ("" if none); with ctx = NULL,
+ * the reason the calling thread's last soap_create failed. */
 const char *soap_last_error(const soap_ctx *ctx);
 
 /* Free the context and its device buffers (synchronises the device). NULL ok. */

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -47,6 +48,8 @@ constexpr size_t DENSITY_LDS_BUDGET = 64 * 1024;
 constexpr size_t JACOBIAN_LDS_BUDGET = 80 * 1024;
 constexpr size_t LDS_HARD_LIMIT = 160 * 1024;
 
+thread_local std::string g_create_error = "";
+
 } // namespace
 
 struct soap_ctx {
@@ -57,7 +60,7 @@ struct soap_ctx {
     int64_t F = 0, Fe = 0;
     int nq_full = 0;
     std::vector<uint32_t> fq;
-    std::vector<uint2> fe;        // [S][Fe]
+    std::vector<uint32_t> fe;     // [S][Fe] packed slots
     std::vector<int32_t> fmap;    // [S][Fe]
     Params P{};
     // device constants
@@ -78,6 +81,14 @@ struct soap_ctx {
     JacLaunch jac_cfg{};
     int groups_jac = 1, groups_desc = 1;
     int lgrp_jac[MAX_GROUPS + 1]{}, lgrp_desc[MAX_GROUPS + 1]{};
+    // per-segment timing
+    bool timing = false;
+    struct Rec {
+        int seg;
+        hipEvent_t a, b;
+    };
+    std::vector<Rec> recs;
+    std::vector<hipEvent_t> pool;
     std::string err;
 };
 
@@ -111,26 +122,28 @@ void build_feature_tables(soap_ctx *c) {
     c->nq_full = (int)c->fq.size();
     c->F = (int64_t)c->nq_full * lw;
     c->Fe = (int64_t)lw * (n * (n + 1) / 2 + (S - 1) * n * n);
-    c->fe.assign((size_t)S * c->Fe, make_uint2(0, 0));
+    c->fe.assign((size_t)S * c->Fe, 0u);
     c->fmap.assign((size_t)S * c->Fe, 0);
+    // slot of species s: ob1 = n1 * lw + l | ou1 = u1 * lw + l << 8 | diag << 20
+    // (on the diagonal pair the second term uses ob2 = ou1 - s n lw,
+    // ou2 = ob1 + s n lw)
     for (int s = 0; s < S; ++s) {
         int64_t k = 0;
         for (int q = 0; q < c->nq_full; ++q) {
             const uint32_t f = c->fq[q];
             const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
             if (mu != s && nu != s) continue;
-            int nb1, u1, two = 0, nb2 = 0, u2 = 0;
+            int nb1, u1, two = 0;
             if (mu == s && nu == s) { // d/dr_j of sum_m c^s_a c^s_b: both factors
-                nb1 = a; u1 = s * n + b; two = 1; nb2 = b; u2 = s * n + a;
+                nb1 = a; u1 = s * n + b; two = 1;
             } else if (mu == s) {     // derivative of the first factor
                 nb1 = a; u1 = nu * n + b;
             } else {                  // derivative of the second factor
                 nb1 = b; u1 = mu * n + a;
             }
             for (int l = 0; l < lw; ++l, ++k) {
-                c->fe[(size_t)s * c->Fe + k] = make_uint2((uint32_t)l | (uint32_t)nb1 << 8 | (uint32_t)u1 << 16 |
-                                                              (uint32_t)two << 24,
-                                                          (uint32_t)nb2 | (uint32_t)u2 << 8);
+                c->fe[(size_t)s * c->Fe + k] =
+                    (uint32_t)(nb1 * lw + l) | (uint32_t)(u1 * lw + l) << 8 | (uint32_t)two << 20;
                 c->fmap[(size_t)s * c->Fe + k] = q * lw + l;
             }
         }
@@ -141,22 +154,18 @@ void build_feature_tables(soap_ctx *c) {
 int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *EC_out, size_t *lds_out) {
     const int lw = P.lmax + 1;
     for (int G = 1; G <= lw; ++G) {
-        // balance sum over l of (2l+1) across G contiguous groups
+        // contiguous groups balancing sum over l of (2l+1): cut k at the l with
+        // l^2 closest above k L / G, kept strictly increasing and leaving one l
+        // for every later group
         int bounds[MAX_GROUPS + 1];
         bounds[0] = 0;
-        int g = 1;
-        const double target = (double)(lw * lw) / G;
-        for (int l = 1; l < lw && g < G; ++l)
-            if ((double)(l * l) >= target * g) bounds[g++] = l;
-        while (g < G) { // degenerate: fill the remainder one l each
-            bounds[g] = bounds[g - 1] + 1;
-            ++g;
+        for (int k = 1; k < G; ++k) {
+            int b = (int)std::ceil(std::sqrt((double)k * lw * lw / G) - 1e-9);
+            b = std::max(b, bounds[k - 1] + 1);
+            b = std::min(b, lw - (G - k));
+            bounds[k] = b;
         }
         bounds[G] = lw;
-        bool ok = true;
-        for (int k = 0; k < G; ++k)
-            if (bounds[k + 1] <= bounds[k]) ok = false;
-        if (!ok) continue;
         for (int EC : {64, 32, 16, 8, 4}) {
             size_t worst = 0;
             for (int k = 0; k < G; ++k) worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], EC));
@@ -184,19 +193,23 @@ int plan_launches(soap_ctx *c) {
         return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
     c->dens_cfg[1].EC = EC;
     c->dens_cfg[1].lds = lds;
-    int EB = 16;
-    while (EB > 1 && jacobian_lds_bytes(P, EB) > JACOBIAN_LDS_BUDGET) --EB;
-    if (jacobian_lds_bytes(P, EB) > LDS_HARD_LIMIT)
+    // Jacobian kernel: W edges per wave iteration; slot table in LDS when small
+    const int tab = (size_t)P.S * P.Fe * 4 <= 16 * 1024 ? 1 : 0;
+    int W = 2;
+    while (W > 1 && jacobian_lds_bytes(P, W, tab) > JACOBIAN_LDS_BUDGET) --W;
+    if (jacobian_lds_bytes(P, W, tab) > LDS_HARD_LIMIT)
         return fail(c, SOAP_EINVAL, "basis too large for the Jacobian kernel's on-chip memory");
-    c->jac_cfg.EB = EB;
-    c->jac_cfg.lds = jacobian_lds_bytes(P, EB);
+    c->jac_cfg.W = W;
+    c->jac_cfg.tab_lds = tab;
+    c->jac_cfg.lds = jacobian_lds_bytes(P, W, tab);
     return SOAP_OK;
 }
 
 int upload_constants(soap_ctx *c) {
     const int n = c->n, lw = c->lmax + 1, S = (int)c->Z.size();
     char msg[256] = {0};
-    std::vector<double> betaC, betaCa, aprime, G, rq, c0(n), Nlm((size_t)lw * lw);
+    const int ldN = lw + 1; // harmonics tables cover l <= l_max + 1
+    std::vector<double> betaC, betaCa, aprime, G, rq, c0(n), Nlm((size_t)ldN * ldN), rcoef((size_t)2 * ldN * ldN, 0.0);
     if (c->rbf == SOAP_RBF_GTO) {
         betaC.resize((size_t)lw * n * n);
         betaCa.resize((size_t)lw * n * n);
@@ -210,7 +223,12 @@ int upload_constants(soap_ctx *c) {
         if (soap_basis_poly(c->r_cut, n, c->sigma, c->Q, G.data(), rq.data(), c0.data(), msg, sizeof msg) != 0)
             return fail(c, SOAP_EINVAL, "%s", msg);
     }
-    soap_basis_sh_norms(c->lmax, Nlm.data());
+    soap_basis_sh_norms(c->lmax + 1, Nlm.data());
+    for (int l = 0; l < ldN; ++l)
+        for (int m = 0; m + 2 <= l; ++m) {
+            rcoef[2 * (l * ldN + m)] = (double)(2 * l - 1) / (double)(l - m);
+            rcoef[2 * (l * ldN + m) + 1] = (double)(l + m - 1) / (double)(l - m);
+        }
     // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nlm
     std::vector<double> all;
     size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
@@ -220,6 +238,8 @@ int upload_constants(soap_ctx *c) {
     size_t o_rq = all.size(); all.insert(all.end(), rq.begin(), rq.end());
     size_t o_c0 = all.size(); all.insert(all.end(), c0.begin(), c0.end());
     size_t o_N = all.size(); all.insert(all.end(), Nlm.begin(), Nlm.end());
+    if (all.size() & 1) all.push_back(0.0); // 16-byte alignment of the double2 table
+    size_t o_rc = all.size(); all.insert(all.end(), rcoef.begin(), rcoef.end());
     hipError_t e;
     if ((e = c->d_const.ensure(all.size() * 8)) != hipSuccess) return hip_fail(c, e, "hipMalloc(constants)");
     if ((e = hipMemcpy(c->d_const.p, all.data(), all.size() * 8, hipMemcpyHostToDevice)) != hipSuccess)
@@ -229,8 +249,8 @@ int upload_constants(soap_ctx *c) {
     if ((e = c->d_fq.ensure(c->fq.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fq)");
     if ((e = hipMemcpy(c->d_fq.p, c->fq.data(), c->fq.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
         return hip_fail(c, e, "hipMemcpy(fq)");
-    if ((e = c->d_fe.ensure(c->fe.size() * sizeof(uint2))) != hipSuccess) return hip_fail(c, e, "hipMalloc(fe)");
-    if ((e = hipMemcpy(c->d_fe.p, c->fe.data(), c->fe.size() * sizeof(uint2), hipMemcpyHostToDevice)) != hipSuccess)
+    if ((e = c->d_fe.ensure(c->fe.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fe)");
+    if ((e = hipMemcpy(c->d_fe.p, c->fe.data(), c->fe.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
         return hip_fail(c, e, "hipMemcpy(fe)");
     if ((e = c->d_fmap.ensure(c->fmap.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fmap)");
     if ((e = hipMemcpy(c->d_fmap.p, c->fmap.data(), c->fmap.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
@@ -260,12 +280,42 @@ int upload_constants(soap_ctx *c) {
     P.rq = d + o_rq;
     P.c0 = d + o_c0;
     P.Nlm = d + o_N;
+    P.rcoef = reinterpret_cast<const double2 *>(d + o_rc);
     P.fq = c->d_fq.as<uint32_t>();
-    P.fe = c->d_fe.as<uint2>();
+    P.fe = c->d_fe.as<uint32_t>();
     return plan_launches(c);
 }
 
 hipStream_t to_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+hipEvent_t take_event(soap_ctx *c) {
+    if (!c->pool.empty()) {
+        hipEvent_t e = c->pool.back();
+        c->pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// RAII bracket of one timed segment on a stream
+struct SegTimer {
+    soap_ctx *c;
+    int seg;
+    hipStream_t st;
+    hipEvent_t a = nullptr;
+    SegTimer(soap_ctx *c_, int seg_, hipStream_t st_) : c(c_), seg(seg_), st(st_) {
+        if (c->timing && (a = take_event(c)) != nullptr) (void)hipEventRecord(a, st);
+    }
+    void done() {
+        if (!a) return;
+        hipEvent_t b = take_event(c);
+        if (b && hipEventRecord(b, st) == hipSuccess) c->recs.push_back({seg, a, b});
+        else c->pool.push_back(a);
+        a = nullptr;
+    }
+};
 
 int check_ctx_device(soap_ctx *c) {
     int dev = -1;
@@ -300,17 +350,25 @@ extern "C" {
 
 int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32_t n_max, int32_t l_max, double sigma,
                 int32_t rbf, soap_ctx **out) {
-    if (!out) return SOAP_EINVAL;
+    g_create_error.clear();
+    auto bad = [](const char *msg) {
+        g_create_error = msg;
+        return SOAP_EINVAL;
+    };
+    if (!out) return bad("out is NULL");
     *out = nullptr;
-    if (!species_Z || n_species < 1 || n_species > 64) return SOAP_EINVAL;
-    if (n_max < 1 || n_max > NMAX || l_max < 0 || l_max > LMAX || !(sigma > 0) || !(r_cut > 0)) return SOAP_EINVAL;
-    if (rbf != SOAP_RBF_GTO && rbf != SOAP_RBF_POLYNOMIAL) return SOAP_EINVAL;
-    if (rbf == SOAP_RBF_GTO && !(r_cut > 1.0)) return SOAP_EINVAL;
-    if (n_species * n_max > 255) return SOAP_EINVAL;
+    if (!species_Z || n_species < 1 || n_species > 64) return bad("n_species must be in 1..64");
+    if (n_max < 1 || n_max > NMAX) return bad("n_max must be in 1..16");
+    if (l_max < 0 || l_max > LMAX) return bad("l_max must be in 0..14");
+    if (!(sigma > 0) || !(r_cut > 0)) return bad("sigma and r_cut must be positive");
+    if (rbf != SOAP_RBF_GTO && rbf != SOAP_RBF_POLYNOMIAL) return bad("unknown rbf");
+    if (rbf == SOAP_RBF_GTO && !(r_cut > 1.0)) return bad("the GTO basis needs r_cut > 1");
+    if (n_species * n_max > 255) return bad("n_species * n_max must not exceed 255");
     std::vector<int32_t> Z(species_Z, species_Z + n_species);
     std::sort(Z.begin(), Z.end());
     for (int k = 0; k < n_species; ++k)
-        if (Z[k] < 1 || Z[k] > 127 || (k > 0 && Z[k] == Z[k - 1])) return SOAP_EINVAL;
+        if (Z[k] < 1 || Z[k] > 127 || (k > 0 && Z[k] == Z[k - 1]))
+            return bad("atomic numbers must be distinct and in 1..127");
     soap_ctx *c = new (std::nothrow) soap_ctx();
     if (!c) return SOAP_ENOMEM;
     c->Z = Z;
@@ -328,6 +386,7 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
         return e == hipErrorOutOfMemory ? SOAP_ENOMEM : SOAP_EHIP;
     }
     if ((rc = upload_constants(c)) != SOAP_OK) {
+        g_create_error = c->err;
         soap_destroy(c);
         return rc;
     }
@@ -341,6 +400,11 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         if (value != SOAP_FP32 && value != SOAP_FP64) return fail(c, SOAP_EINVAL, "dtype must be SOAP_FP32 or SOAP_FP64");
         if (value != c->dtype) c->have_rows = false;
         c->dtype = (int)value;
+        return SOAP_OK;
+    }
+    if (!std::strcmp(key, "timing")) {
+        if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "timing must be 0 or 1");
+        c->timing = value == 1;
         return SOAP_OK;
     }
     if (!std::strcmp(key, "quad_n")) {
@@ -423,6 +487,7 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     w.scan_tmp = c->b_scan.as<int64_t>();
     w.flags = c->b_flags.as<int32_t>();
     int64_t *row = c->b_row.as<int64_t>();
+    SegTimer timer(c, 0, st);
     e = nbr_phase1(w, n_atoms, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(), n_centers,
                    centers_dev, c->r_cut, row, st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
@@ -442,6 +507,7 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     e = nbr_phase2(w, n_atoms, pos_dev, f64, c->b_spec.as<uint8_t>(), n_centers, centers_dev, c->r_cut, row,
                    c->b_cols.as<int32_t>(), st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour rows");
+    timer.done();
     c->have_rows = true;
     c->n_atoms = n_atoms;
     c->nc = n_centers;
@@ -477,9 +543,12 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
+    SegTimer timer(c, 1, to_stream(stream));
     hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0], desc, c_out,
                                   jself, scratch, to_stream(stream));
-    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "density kernel");
+    if (e != hipSuccess) return hip_fail(c, e, "density kernel");
+    timer.done();
+    return SOAP_OK;
 }
 
 int soap_compute(soap_ctx *c, void *desc_dev, void *stream) {
@@ -501,9 +570,12 @@ int soap_derivatives(soap_ctx *c, void *desc_dev, void *jac_edge_dev, void *jac_
     int rc = run_density(c, true, desc_dev, nullptr, jac_self_dev, stream);
     if (rc != SOAP_OK) return rc;
     if (c->E == 0) return SOAP_OK;
+    SegTimer timer(c, 2, to_stream(stream));
     hipError_t e = launch_jacobian(c->P, rows_of(c), c->pos, c->built_f64, c->jac_cfg, c->b_cscratch.as<double>(),
                                    jac_edge_dev, to_stream(stream));
-    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "Jacobian kernel");
+    if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
+    timer.done();
+    return SOAP_OK;
 }
 
 int soap_scatter_dense(soap_ctx *c, const void *jac_edge_dev, const void *jac_self_dev, void *dense_dev, void *stream) {
@@ -519,7 +591,33 @@ int soap_scatter_dense(soap_ctx *c, const void *jac_edge_dev, const void *jac_se
     return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_scatter_dense");
 }
 
-const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : "null context"; }
+int soap_timing(soap_ctx *c, double *ms_out, int64_t *count_out, int32_t reset) {
+    if (!c || !ms_out) return SOAP_EINVAL;
+    double ms[3] = {0, 0, 0};
+    int64_t cnt[3] = {0, 0, 0};
+    for (auto &r : c->recs) {
+        hipError_t e = hipEventSynchronize(r.b);
+        float t = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, r.a, r.b);
+        if (e != hipSuccess) return hip_fail(c, e, "soap_timing");
+        ms[r.seg] += t;
+        cnt[r.seg] += 1;
+    }
+    for (int k = 0; k < 3; ++k) {
+        ms_out[k] = ms[k];
+        if (count_out) count_out[k] = cnt[k];
+    }
+    if (reset) {
+        for (auto &r : c->recs) {
+            c->pool.push_back(r.a);
+            c->pool.push_back(r.b);
+        }
+        c->recs.clear();
+    }
+    return SOAP_OK;
+}
+
+const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : g_create_error.c_str(); }
 
 void soap_destroy(soap_ctx *c) {
     if (!c) return;
@@ -529,6 +627,11 @@ void soap_destroy(soap_ctx *c) {
                       &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
+    for (auto &r : c->recs) {
+        (void)hipEventDestroy(r.a);
+        (void)hipEventDestroy(r.b);
+    }
+    for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
     delete c;
 }
 

@@ -74,26 +74,32 @@ __global__ void k_bucket_fill(int64_t n, const PosT *__restrict__ pos, const int
     satom[slot] = (int32_t)i;
 }
 
+// One 64-lane wave per center (four centers per workgroup); lanes 0..26
+// each walk one of the 27 neighbouring cells.
 template <typename PosT>
-__global__ void k_count(int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers,
-                        const PosT *__restrict__ pos, const int4 *__restrict__ cell,
-                        const int32_t *__restrict__ start, const int4 *__restrict__ scell,
-                        const double4 *__restrict__ spos, const int32_t *__restrict__ satom, uint32_t mask,
-                        double rc2, int32_t *__restrict__ deg, int32_t *__restrict__ flags) {
-    int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+__global__ __launch_bounds__(256) void k_count(int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers,
+                                               const PosT *__restrict__ pos, const int4 *__restrict__ cell,
+                                               const int32_t *__restrict__ start, const int4 *__restrict__ scell,
+                                               const double4 *__restrict__ spos, const int32_t *__restrict__ satom,
+                                               uint32_t mask, double rc2, int32_t *__restrict__ deg,
+                                               int32_t *__restrict__ flags) {
+    const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
     if (c >= nc) return;
-    int64_t i = centers ? (int64_t)centers[c] : c;
+    const int64_t i = centers ? (int64_t)centers[c] : c;
     if (i < 0 || i >= n_atoms) {
-        atomicOr(&flags[0], 2);
-        deg[c] = 0;
+        if (lane == 0) {
+            atomicOr(&flags[0], 2);
+            deg[c] = 0;
+        }
         return;
     }
-    int4 ci = cell[i];
-    double3 pi = load_pos(pos, i);
     int cnt = 0;
-    for (int d = 0; d < 27; ++d) {
-        int tx = ci.x + d % 3 - 1, ty = ci.y + (d / 3) % 3 - 1, tz = ci.z + d / 9 - 1;
-        uint32_t b = cell_hash(tx, ty, tz, mask);
+    if (lane < 27) {
+        const int4 ci = cell[i];
+        const double3 pi = load_pos(pos, i);
+        const int tx = ci.x + lane % 3 - 1, ty = ci.y + (lane / 3) % 3 - 1, tz = ci.z + lane / 9 - 1;
+        const uint32_t b = cell_hash(tx, ty, tz, mask);
         for (int t = start[b]; t < start[b + 1]; ++t) {
             int4 sc = scell[t];
             if (sc.x != tx || sc.y != ty || sc.z != tz || satom[t] == (int32_t)i) continue;
@@ -101,8 +107,11 @@ __global__ void k_count(int64_t n_atoms, int64_t nc, const int32_t *__restrict__
             if (within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2)) ++cnt;
         }
     }
-    deg[c] = cnt;
-    atomicMax(&flags[1], cnt);
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_down(cnt, off, 64);
+    if (lane == 0) {
+        deg[c] = cnt;
+        atomicMax(&flags[1], cnt);
+    }
 }
 
 // One 64-lane workgroup per center.  Lanes 0..26 each walk one neighbour
@@ -268,7 +277,7 @@ hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool p
     else
         hipLaunchKernelGGL(k_bucket_fill<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos,
                            w.atom_cell, w.bucket_start, w.bucket_fill, w.sorted_cell, w.sorted_pos, w.sorted_atom);
-    const unsigned gc = blocks_for(nc, 256);
+    const unsigned gc = blocks_for(nc, 4);
     if (pos64)
         hipLaunchKernelGGL(k_count<double>, dim3(gc), dim3(256), 0, st, n_atoms, nc, centers, (const double *)pos,
                            w.atom_cell, w.bucket_start, w.sorted_cell, w.sorted_pos, w.sorted_atom, mask, rc2, w.deg,

@@ -23,9 +23,10 @@ struct Params {
     const double *G;           // polynomial [n][Q], includes 4 pi
     const double *rq;          // polynomial [Q]
     const double *c0;          // on-site term [n]
-    const double *Nlm;         // [lmax+1][lmax+1]
+    const double *Nlm;         // [lmax+2][lmax+2] real solid-harmonic normalisation
+    const double2 *rcoef;      // [lmax+2][lmax+2] recurrence coefficients of the harmonics
     const uint32_t *fq;        // [nq_full] mu | nu<<8 | n<<16 | n'<<24
-    const uint2 *fe;           // [S][Fe] edge-feature terms
+    const uint32_t *fe;        // [S][Fe] packed neighbour-block slots (see k_jacobian)
     int n_groups;              // l-groups of the density kernel
     int lgrp[MAX_GROUPS + 1];  // group g covers l in [lgrp[g], lgrp[g+1])
 };
@@ -67,12 +68,13 @@ struct DensityLaunch {
     size_t lds;      // dynamic LDS bytes
 };
 struct JacLaunch {
-    int EB;
+    int W;          // edges per wave iteration
+    int tab_lds;    // 1 = slot table staged in LDS, 0 = decoded arithmetically
     size_t lds;
 };
 
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int EC);
-size_t jacobian_lds_bytes(const Params &P, int EB);
+size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds);
 hipError_t set_lds_limits();
 
 // desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)

@@ -58,10 +58,11 @@ template <typename T> __device__ __forceinline__ void store_nt(T *p, double v) {
 // Writes Y[lm - lm0] and dY[d*ldd + lm - lm0] for l in [l_lo, l_hi).
 // grad = false skips the gradient.  zero_grad forces the gradient to 0.
 // ---------------------------------------------------------------------------
+// rc[(l * ldN + m) * 2 + {0, 1}] = ((2l-1)/(l-m), (l+m-1)/(l-m)) for l >= m + 2
 template <bool GRAD>
-__device__ void sh_column(int m, int l_lo, int l_hi, double x, double y, double z, const double *__restrict__ Nlm,
-                          int ldN, double *__restrict__ Y, double *__restrict__ dY, int ldd, int lm0,
-                          bool zero_grad) {
+__device__ __forceinline__ void sh_column(int m, int l_lo, int l_hi, double x, double y, double z, const double *__restrict__ Nlm,
+                          const double2 *__restrict__ rcoef, int ldN, double *__restrict__ Y,
+                          double *__restrict__ dY, int ldd, int lm0, bool zero_grad) {
     const double r2 = x * x + y * y + z * z;
     double c = 1.0, s = 0.0, cm1 = 0.0, sm1 = 0.0;
     for (int k = 1; k <= m; ++k) {
@@ -80,13 +81,19 @@ __device__ void sh_column(int m, int l_lo, int l_hi, double x, double y, double 
         double q; // Q_l^m
         if (l == m) q = dfm;
         else if (l == m + 1) q = (double)(2 * m + 1) * z * dfm;
-        else q = ((double)(2 * l - 1) * z * q1 - (double)(l + m - 1) * r2 * q2) / (double)(l - m);
+        else {
+            const double2 k = rcoef[l * ldN + m];
+            q = k.x * z * q1 - k.y * r2 * q2;
+        }
         double p; // Q_{l-1}^{m+1}
         const int lp = l - 1;
         if (lp < m + 1) p = 0.0;
         else if (lp == m + 1) p = dfm * (double)(2 * m + 1);
         else if (lp == m + 2) p = (double)(2 * m + 3) * z * dfm * (double)(2 * m + 1);
-        else p = ((double)(2 * lp - 1) * z * p1 - (double)(lp + m) * r2 * p2) / (double)(lp - m - 1);
+        else {
+            const double2 k = rcoef[lp * ldN + m + 1];
+            p = k.x * z * p1 - k.y * r2 * p2;
+        }
         if (l >= l_lo) {
             const double N = Nlm[l * ldN + m];
             const int base = l * l + l - lm0;
@@ -145,111 +152,206 @@ __device__ double bessel_series_scaled(int l, double x) {
     return s * exp(-x);
 }
 
-__device__ void bessel_scaled_all(int Lt, double x, double *v /* [LT_MAX+1] */) {
+// Writes ii_l(x) * g for l = 0..Lt to t[0..Lt] (LDS).
+__device__ __forceinline__ void bessel_scaled_lds(int Lt, double x, double g, double *t) {
     if (x == 0.0) {
-#pragma unroll
-        for (int k = 0; k <= LT_MAX; ++k) v[k] = (k == 0) ? 1.0 : 0.0;
+        t[0] = g;
+        for (int k = 1; k <= Lt; ++k) t[k] = 0.0;
         return;
     }
     const double ix = 1.0 / x;
     if (x * 6.9 >= (double)(Lt * (Lt + 1))) {
         const double em = exp(-2.0 * x);
-        v[0] = 0.5 * (1.0 - em) * ix;
-        v[1] = 0.5 * (1.0 + em) * ix - 0.5 * (1.0 - em) * ix * ix;
-#pragma unroll
-        for (int k = 1; k < LT_MAX; ++k)
-            if (k < Lt) v[k + 1] = v[k - 1] - (double)(2 * k + 1) * ix * v[k];
-    } else {
-        // seeds at Lt and Lt-1, then downward
-        double top = bessel_series_scaled(Lt, x);
-        double nxt = (Lt >= 1) ? bessel_series_scaled(Lt - 1, x) : 0.0;
-#pragma unroll
-        for (int k = 0; k <= LT_MAX; ++k) {
-            if (k == Lt) v[k] = top;
-            if (k == Lt - 1) v[k] = nxt;
+        double a = 0.5 * (1.0 - em) * ix;              // ii_0
+        double b = 0.5 * (1.0 + em) * ix - a * ix;     // ii_1
+        t[0] = g * a;
+        if (Lt >= 1) t[1] = g * b;
+        for (int k = 1; k < Lt; ++k) {
+            const double c = a - (double)(2 * k + 1) * ix * b;
+            t[k + 1] = g * c;
+            a = b;
+            b = c;
         }
-#pragma unroll
-        for (int k = LT_MAX - 1; k >= 1; --k)
-            if (k < Lt) v[k - 1] = v[k + 1] + (double)(2 * k + 1) * ix * v[k];
+    } else {
+        double b = bessel_series_scaled(Lt, x);                     // ii_Lt
+        double a = (Lt >= 1) ? bessel_series_scaled(Lt - 1, x) : 0; // ii_{Lt-1}
+        t[Lt] = g * b;
+        if (Lt >= 1) t[Lt - 1] = g * a;
+        for (int k = Lt - 1; k >= 1; --k) {
+            const double c = b + (double)(2 * k + 1) * ix * a;      // ii_{k-1}
+            t[k - 1] = g * c;
+            b = a;
+            a = c;
+        }
     }
 }
 
 // ---------------------------------------------------------------------------
-// Per-chunk edge staging, shared by both kernels.  LDS arrays:
-//   geo[EC][4] (x, y, z, r), sp[EC] species,
-//   Y[EC][Lg], dY[EC][3][Lg] (harmonics for lm in [lm0, lm0+Lg)),
-//   B[EC][n][lgc], Bh[EC][n][lgc] (radial factors for l in [lg0, lg0+lgc)),
-//   T[EC][Q][lgc+1] polynomial quadrature scratch.
-// scaleK multiplies B and Bh by K_l = pi sqrt(8/(2l+1)).
+// LDS layout helpers.  Every region starts on a 16-byte boundary.
 // ---------------------------------------------------------------------------
+__host__ __device__ __forceinline__ size_t even(size_t nd) { return (nd + 1) & ~(size_t)1; }
+
+struct Carver {
+    double *base;
+    size_t off = 0;
+    __device__ __forceinline__ double *take(size_t nd) {
+        double *p = base + off;
+        off += even(nd);
+        return p;
+    }
+};
+
+// Neighbour rows are prefetched into LDS in blocks of row_block(EC) edges.
+__host__ __device__ __forceinline__ int row_block(int EC) { return EC >= 128 ? EC : EC * (128 / EC); }
+
+// Basis tables copied to LDS once per workgroup (for l in [lg0, lg1)), so
+// that no global load sits on the per-edge path: with the chip's store
+// traffic in flight, global load latency runs to microseconds.
+struct Tables {
+    const double *betaC, *betaCa, *aprime; // GTO: [lc][n][k], [lc][n][k], [lc][k]
+    const double *G, *rq;                  // polynomial: [n][Q], [Q]
+    const double *Nlm;                     // [ldN][ldN]
+    const double2 *rcoef;                  // [ldN][ldN]
+};
+
+__host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lgc) {
+    const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
+    size_t d = even(ldN * ldN) + even(2 * ldN * ldN);
+    if (P.rbf == 0) d += 2 * even((size_t)lgc * n * n) + even((size_t)lgc * n);
+    else d += even(n * P.Q) + even((size_t)P.Q);
+    return d;
+}
+
+__device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables &T, int lg0, int lg1) {
+    const int ldN = P.lmax + 2, n = P.n, lgc = lg1 - lg0, tid = threadIdx.x, bs = blockDim.x;
+    // every pointer is assigned on every path, so the struct stays in
+    // registers and the compiler keeps LDS (ds_*) addressing for it
+    double *Nl = cv.take((size_t)ldN * ldN);
+    double *rc = cv.take(2 * (size_t)ldN * ldN);
+    const bool poly = P.rbf != 0;
+    const size_t szA = poly ? (size_t)n * P.Q : (size_t)lgc * n * n; // betaC | G
+    const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n * n;     // betaCa | rq
+    const size_t szC = poly ? 0 : (size_t)lgc * n;                   // aprime
+    double *A = cv.take(szA), *B = cv.take(szB), *C = cv.take(szC);
+    for (int k = tid; k < ldN * ldN; k += bs) Nl[k] = P.Nlm[k];
+    for (int k = tid; k < 2 * ldN * ldN; k += bs) rc[k] = ((const double *)P.rcoef)[k];
+    if (!poly) {
+        const size_t o = (size_t)lg0 * n * n;
+        for (int k = tid; k < (int)szA; k += bs) {
+            A[k] = P.betaC[o + k];
+            B[k] = P.betaCa[o + k];
+        }
+        for (int k = tid; k < (int)szC; k += bs) C[k] = P.aprime[(size_t)lg0 * n + k];
+    } else {
+        for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
+        for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
+    }
+    T.Nlm = Nl;
+    T.rcoef = (const double2 *)rc;
+    T.betaC = A;
+    T.G = A;
+    T.betaCa = B;
+    T.rq = B;
+    T.aprime = C;
+}
+
+// Per-chunk edge staging, shared by both kernels.  LDS arrays:
+//   geo[.][4] (x, y, z, r), sp[.] species   (views into the prefetched rows)
+//   Y[EC][Lg], dY[EC][3][Lg]  harmonics for lm in [lm0, lm0+Lg),
+//   BB[EC][n][lgc] = (B, Bh)  radial factors for l in [lg0, lg0+lgc),
+//   X  scratch: GTO exponentials [EC][lgc][n], or the polynomial quadrature
+//      table [EC][Q][lgc+1].
+// scaleK multiplies B and Bh by K_l = pi sqrt(8/(2l+1)).
 struct Stage {
-    double *geo, *Y, *dY, *B, *Bh, *T;
+    double *geo, *Y, *dY, *X;
+    double2 *BB;
     int *sp;
 };
 
-template <bool GRAD>
-__device__ void stage_angular_radial(const Params &P, const Stage &st, int nb, int lg0, int lg1, bool scaleK) {
-    const int tid = threadIdx.x;
-    const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0, lgc = lg1 - lg0, n = P.n;
-    // harmonics: items (edge, m), m < lg1
-    for (int it = tid; it < nb * lg1; it += BS) {
-        const int e = it / lg1, m = it - e * lg1;
-        const double *g = st.geo + 4 * e;
-        sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], P.Nlm, P.lmax + 1, st.Y + e * Lg,
-                        GRAD ? st.dY + e * 3 * Lg : nullptr, Lg, lm0, g[3] == 0.0);
+// X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
+// Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place)
+__host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int lgc, int lg1) {
+    return P.rbf ? (size_t)P.Q * (lg1 + 1) : (size_t)P.n * lgc;
+}
+
+// Synchronisation inside one wave: LDS writes become visible to the other
+// lanes and the compiler keeps LDS accesses on their side of the point.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Staging work is spread over `bs` threads starting at `tid`: the whole
+// workgroup (WAVE = false, workgroup barriers) or one wave (WAVE = true).
+template <bool GRAD, bool WAVE = false>
+__device__ __forceinline__ void stage_angular_radial(const Params &P, const Tables &T, const Stage &st, int nb, int lg0,
+                                                     int lg1, bool scaleK, int tid = -1, int bs = 0) {
+    if (!WAVE) {
+        tid = threadIdx.x;
+        bs = blockDim.x;
     }
+    const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0, lgc = lg1 - lg0, n = P.n, ldN = P.lmax + 2;
+    const int n_sh = nb * lg1;
     if (P.rbf == 0) {
-        // GTO: items (edge, l)
-        for (int it = tid; it < nb * lgc; it += BS) {
-            const int e = it / lgc, lc = it - e * lgc, l = lg0 + lc;
-            const double r = st.geo[4 * e + 3], r2 = r * r;
-            double E[NMAX];
-#pragma unroll
-            for (int k = 0; k < NMAX; ++k) E[k] = (k < n) ? exp(-P.aprime[l * n + k] * r2) : 0.0;
-            const double K = scaleK ? M_PI * sqrt(8.0 / (double)(2 * l + 1)) : 1.0;
-            for (int a = 0; a < n; ++a) {
-                const double *bc = P.betaC + ((size_t)l * n + a) * n;
-                double b = 0.0;
-#pragma unroll
-                for (int k = 0; k < NMAX; ++k)
-                    if (k < n) b += bc[k] * E[k];
-                st.B[(e * n + a) * lgc + lc] = K * b;
-                if (GRAD) {
-                    const double *ba = P.betaCa + ((size_t)l * n + a) * n;
-                    double bh = 0.0;
-#pragma unroll
-                    for (int k = 0; k < NMAX; ++k)
-                        if (k < n) bh += ba[k] * E[k];
-                    st.Bh[(e * n + a) * lgc + lc] = K * bh;
-                }
+        // harmonics (edge, m) and exponentials (edge, l, k) in one pass
+        const int n_ex = nb * lgc * n;
+        for (int it = tid; it < n_sh + n_ex; it += bs) {
+            if (it < n_sh) {
+                const int e = it / lg1, m = it - e * lg1;
+                const double *g = st.geo + 4 * e;
+                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * Lg,
+                                GRAD ? st.dY + e * 3 * Lg : nullptr, Lg, lm0, g[3] == 0.0);
+            } else {
+                const int x = it - n_sh, e = x / (lgc * n), rem = x - e * (lgc * n);
+                const double r = st.geo[4 * e + 3];
+                st.X[x] = exp(-T.aprime[rem] * r * r);
             }
         }
-    } else {
-        // polynomial: items (edge, q) fill T = e^{-(r_q - r)^2/2s^2} ii_l(r_q r/s^2), l in [lg0, lg1]
-        const int Q = P.Q, tw = lgc + 1;
-        for (int it = tid; it < nb * Q; it += BS) {
-            const int e = it / Q, q = it - e * Q;
-            const double r = st.geo[4 * e + 3], rq = P.rq[q];
-            const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
-            double v[LT_MAX + 1];
-            bessel_scaled_all(lg1, rq * r * P.inv_s2, v);
-            double *t = st.T + ((size_t)e * Q + q) * tw;
-#pragma unroll
-            for (int k = 0; k <= LT_MAX; ++k)
-                if (k >= lg0 && k <= lg1) t[k - lg0] = gq * v[k];
+        if (WAVE) wave_sync(); else __syncthreads();
+        // B_nl = sum_k betaC^l_nk E_k, Bh_nl = sum_k betaCa^l_nk E_k
+        for (int it = tid; it < nb * n * lgc; it += bs) {
+            const int e = it / (n * lgc), rem = it - e * (n * lgc), a = rem / lgc, lc = rem - a * lgc;
+            const double *E = st.X + (size_t)(e * lgc + lc) * n;
+            const double *bc = T.betaC + ((size_t)lc * n + a) * n;
+            const double *ba = T.betaCa + ((size_t)lc * n + a) * n;
+            double b = 0.0, bh = 0.0;
+            for (int k = 0; k < n; ++k) {
+                b += bc[k] * E[k];
+                if (GRAD) bh += ba[k] * E[k];
+            }
+            const double K = scaleK ? M_PI * sqrt(8.0 / (double)(2 * (lg0 + lc) + 1)) : 1.0;
+            st.BB[it] = make_double2(K * b, K * bh);
         }
-        __syncthreads();
-        for (int it = tid; it < nb * n * lgc; it += BS) {
+    } else {
+        // harmonics (edge, m) and quadrature table (edge, q):
+        //   X[e][q][l] = e^{-(r_q - r)^2/2s^2} ii_l(r_q r/s^2), l in [0, lg1]
+        const int Q = P.Q, tw = lg1 + 1;
+        for (int it = tid; it < n_sh + nb * Q; it += bs) {
+            if (it < n_sh) {
+                const int e = it / lg1, m = it - e * lg1;
+                const double *g = st.geo + 4 * e;
+                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * Lg,
+                                GRAD ? st.dY + e * 3 * Lg : nullptr, Lg, lm0, g[3] == 0.0);
+            } else {
+                const int x = it - n_sh, e = x / Q, q = x - e * Q;
+                const double r = st.geo[4 * e + 3], rq = T.rq[q];
+                const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
+                bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, st.X + (size_t)x * tw);
+            }
+        }
+        if (WAVE) wave_sync(); else __syncthreads();
+        for (int it = tid; it < nb * n * lgc; it += bs) {
             const int e = it / (n * lgc), rem = it - e * (n * lgc), a = rem / lgc, lc = rem - a * lgc;
             const int l = lg0 + lc;
             const double r = st.geo[4 * e + 3];
-            const double *G = P.G + (size_t)a * Q;
-            const double *t = st.T + (size_t)e * Q * tw;
+            const double *G = T.G + (size_t)a * Q;
+            const double *t = st.X + (size_t)e * Q * tw;
             double b = 0.0, bh = 0.0;
             for (int q = 0; q < Q; ++q) {
-                const double tl = t[q * tw + lc];
+                const double tl = t[q * tw + l];
                 b += G[q] * tl;
-                if (GRAD) bh += G[q] * (P.rq[q] * t[q * tw + lc + 1] - r * tl);
+                if (GRAD) bh += G[q] * (T.rq[q] * t[q * tw + l + 1] - r * tl);
             }
             const double K = scaleK ? M_PI * sqrt(8.0 / (double)(2 * l + 1)) : 1.0;
             if (r == 0.0) {
@@ -261,30 +363,28 @@ __device__ void stage_angular_radial(const Params &P, const Stage &st, int nb, i
                 b *= rl;
                 bh *= rl * ir * P.inv_s2;
             }
-            st.B[(e * n + a) * lgc + lc] = K * b;
-            if (GRAD) st.Bh[(e * n + a) * lgc + lc] = K * bh;
+            st.BB[it] = make_double2(K * b, K * bh);
         }
     }
 }
 
+// Prefetch the rows [r0, r0+cnt) of the center: edge vectors r_j - r_i in
+// float64 (exact for float32 inputs), |r|, species.
 template <typename PosT>
-__device__ __forceinline__ void stage_geometry(const Stage &st, const PosT *__restrict__ pos,
-                                               const uint8_t *__restrict__ spec, const int32_t *__restrict__ cols,
-                                               int64_t base, int nb, double3 pi) {
-    const int tid = threadIdx.x;
-    if (tid < nb) {
-        const int64_t j = cols[base + tid];
+__device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__restrict__ pos,
+                                          const uint8_t *__restrict__ spec, const int32_t *__restrict__ cols,
+                                          int64_t r0, int cnt, double3 pi) {
+    for (int t = threadIdx.x; t < cnt; t += blockDim.x) {
+        const int64_t j = cols[r0 + t];
         const double x = (double)pos[3 * j] - pi.x, y = (double)pos[3 * j + 1] - pi.y,
                      z = (double)pos[3 * j + 2] - pi.z;
-        st.geo[4 * tid] = x;
-        st.geo[4 * tid + 1] = y;
-        st.geo[4 * tid + 2] = z;
-        st.geo[4 * tid + 3] = sqrt(x * x + y * y + z * z);
-        st.sp[tid] = spec[j];
+        geo[4 * t] = x;
+        geo[4 * t + 1] = y;
+        geo[4 * t + 2] = z;
+        geo[4 * t + 3] = sqrt(x * x + y * y + z * z);
+        sp[t] = spec[j];
     }
 }
-
-__device__ __forceinline__ size_t align8(size_t b) { return (b + 7) & ~(size_t)7; }
 
 // ---------------------------------------------------------------------------
 // k_density
@@ -301,17 +401,20 @@ __global__ __launch_bounds__(BS) void k_density(Params P, Rows R, const PosT *__
     const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
     const int S = P.S, n = P.n, tid = threadIdx.x;
     const int nL = n * Lg, SnL = S * nL;
+    const int RBk = row_block(EC);
 
-    double *cacc = smem;
+    Carver cv{smem};
+    Tables T;
+    load_tables(P, cv, T, lg0, lg1);
+    double *cacc = cv.take((size_t)SnL * (JAC ? 4 : 1));
     double *Dacc = cacc + SnL; // [3][S][n][Lg]
+    double *rgeo = cv.take(4 * (size_t)RBk);
+    int *rsp = (int *)cv.take((RBk + 1) / 2);
     Stage st;
-    st.geo = Dacc + (JAC ? 3 * SnL : 0);
-    st.Y = st.geo + 4 * EC;
-    st.dY = st.Y + EC * Lg;
-    st.B = st.dY + (JAC ? 3 * EC * Lg : 0);
-    st.Bh = st.B + EC * n * lgc;
-    st.T = st.Bh + (JAC ? EC * n * lgc : 0);
-    st.sp = (int *)(st.T + (P.rbf ? (size_t)EC * P.Q * (lgc + 1) : 0));
+    st.Y = cv.take((size_t)EC * Lg);
+    st.dY = cv.take(JAC ? 3 * (size_t)EC * Lg : 0);
+    st.BB = (double2 *)cv.take(2 * (size_t)EC * n * lgc);
+    st.X = cv.take(EC * stage_x_doubles(P, lgc, lg1));
 
     for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BS) cacc[k] = 0.0;
 
@@ -319,43 +422,47 @@ __global__ __launch_bounds__(BS) void k_density(Params P, Rows R, const PosT *__
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
     const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
 
-    for (int64_t base = e0; base < e1; base += EC) {
-        const int nb = (int)((e1 - base) < EC ? (e1 - base) : EC);
+    for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
+        const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
         __syncthreads();
-        stage_geometry(st, pos, R.spec, R.cols, base, nb, pi);
-        __syncthreads();
-        stage_angular_radial<JAC>(P, st, nb, lg0, lg1, false);
-        __syncthreads();
-        // accumulate: each thread owns entries (a, lm) for every species
-        for (int ent = tid; ent < nL; ent += BS) {
-            const int a = ent / Lg, lmg = ent - a * Lg;
-            const int lc = isqrt_lm(lmg + lm0) - lg0;
-            double acc = 0.0, ax = 0.0, ay = 0.0, az = 0.0;
-            int cur = st.sp[0];
-            for (int e = 0; e < nb; ++e) {
-                const int s = st.sp[e];
-                if (s != cur) {
-                    cacc[cur * nL + ent] += acc;
-                    if (JAC) {
-                        Dacc[cur * nL + ent] += ax;
-                        Dacc[SnL + cur * nL + ent] += ay;
-                        Dacc[2 * SnL + cur * nL + ent] += az;
+        load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
+        for (int off = 0; off < rbn; off += EC) {
+            const int nb = (rbn - off) < EC ? (rbn - off) : EC;
+            st.geo = rgeo + 4 * off;
+            st.sp = rsp + off;
+            __syncthreads();
+            stage_angular_radial<JAC>(P, T, st, nb, lg0, lg1, false);
+            __syncthreads();
+            // accumulate: each thread owns entries (a, lm) for every species
+            for (int ent = tid; ent < nL; ent += BS) {
+                const int a = ent / Lg, lmg = ent - a * Lg;
+                const int lc = isqrt_lm(lmg + lm0) - lg0;
+                double acc = 0.0, ax = 0.0, ay = 0.0, az = 0.0;
+                int cur = st.sp[0];
+                for (int e = 0; e < nb; ++e) {
+                    const int s = st.sp[e];
+                    if (s != cur) {
+                        cacc[cur * nL + ent] += acc;
+                        if (JAC) {
+                            Dacc[cur * nL + ent] += ax;
+                            Dacc[SnL + cur * nL + ent] += ay;
+                            Dacc[2 * SnL + cur * nL + ent] += az;
+                        }
+                        acc = ax = ay = az = 0.0;
+                        cur = s;
                     }
-                    acc = ax = ay = az = 0.0;
-                    cur = s;
+                    const double2 bb = st.BB[(e * n + a) * lgc + lc];
+                    const double y = st.Y[e * Lg + lmg];
+                    acc += bb.x * y;
+                    if (JAC) {
+                        const double bh = bb.y * y;
+                        const double *gg = st.geo + 4 * e;
+                        const double *dy = st.dY + e * 3 * Lg + lmg;
+                        ax += bh * gg[0] + bb.x * dy[0];
+                        ay += bh * gg[1] + bb.x * dy[Lg];
+                        az += bh * gg[2] + bb.x * dy[2 * Lg];
+                    }
                 }
-                const double b = st.B[(e * n + a) * lgc + lc], y = st.Y[e * Lg + lmg];
-                acc += b * y;
-                if (JAC) {
-                    const double bh = st.Bh[(e * n + a) * lgc + lc] * y;
-                    const double *gg = st.geo + 4 * e;
-                    const double *dy = st.dY + e * 3 * Lg + lmg;
-                    ax += bh * gg[0] + b * dy[0];
-                    ay += bh * gg[1] + b * dy[Lg];
-                    az += bh * gg[2] + b * dy[2 * Lg];
-                }
-            }
-            if (nb > 0) {
                 cacc[cur * nL + ent] += acc;
                 if (JAC) {
                     Dacc[cur * nL + ent] += ax;
@@ -413,85 +520,154 @@ __global__ __launch_bounds__(BS) void k_density(Params P, Rows R, const PosT *__
 
 // ---------------------------------------------------------------------------
 // k_jacobian
+//
+// One workgroup of NWJ waves per center.  The workgroup shares the basis
+// tables, the center's coefficients and the prefetched neighbour rows; each
+// wave then runs its own pipeline over its own edges (W at a time):
+// harmonics + radial factors -> U/V precontraction -> stores, synchronising
+// only within the wave, so one wave's latency-bound staging overlaps the
+// other waves' store streams.
+//
+// Neighbour-block slots of species s are the features whose pair contains s,
+// in feature order: pairs (mu, s), mu < s (all n, n'); then (s, s) (n' >= n);
+// then (s, nu), nu > s.  A slot is stored packed:
+//   ob1 = n1 * lw + l  (bits 0-7),  ou1 = u1 * lw + l (bits 8-19),
+//   diag (bit 20): on the diagonal pair the mirrored term has
+//   ob2 = ou1 - s n lw and ou2 = ob1 + s n lw,
+// and evaluates K_l [Bh_{n1,l} r U_{u1,l} + B_{n1,l} V_{u1,l}] (+ mirror),
+// u = species * n + n'.
 // ---------------------------------------------------------------------------
+constexpr int NWJ = 4, BSJ = 64 * NWJ;
+
+__device__ __forceinline__ uint32_t decode_slot(int fe, int s, int n, int lw) {
+    const int q = fe / lw, l = fe - q * lw, nn = n * n, tri = n * (n + 1) / 2;
+    int n1, u1, two = 0;
+    if (q < s * nn) { // pair (mu, s): derivative of the second factor c^s_{n'}
+        const int mu = q / nn, r = q - mu * nn, a = r / n, b = r - a * n;
+        n1 = b;
+        u1 = mu * n + a;
+    } else if (q < s * nn + tri) { // pair (s, s), n' >= n: both factors
+        int r = q - s * nn, a = 0;
+        while (r >= n - a) {
+            r -= n - a;
+            ++a;
+        }
+        n1 = a;
+        u1 = s * n + a + r;
+        two = 1;
+    } else { // pair (s, nu): derivative of the first factor c^s_n
+        const int r0 = q - s * nn - tri, nu = s + 1 + r0 / nn, r = r0 - (nu - s - 1) * nn, a = r / n, b = r - a * n;
+        n1 = a;
+        u1 = nu * n + b;
+    }
+    return (uint32_t)(n1 * lw + l) | (uint32_t)(u1 * lw + l) << 8 | (uint32_t)two << 20;
+}
+
+__host__ __device__ __forceinline__ size_t jac_wave_doubles(const Params &P, int W) {
+    const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1, Sn = (size_t)P.S * P.n;
+    const size_t xd = stage_x_doubles(P, (int)lw, (int)lw);
+    const size_t xu = xd > 4 * Sn * lw ? xd : 4 * Sn * lw;
+    return even(W * L) + even(3 * W * L) + even(2 * W * P.n * lw) + even(W * xu);
+}
+
 template <typename PosT, typename OutT>
-__global__ __launch_bounds__(BS) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos, int EB,
-                                                 const double *__restrict__ c_scratch, OutT *__restrict__ jedge) {
+__global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos, int W,
+                                                  int tab_lds, const double *__restrict__ c_scratch,
+                                                  OutT *__restrict__ jedge) {
     extern __shared__ double smem[];
     const int64_t ci = blockIdx.x;
     const int S = P.S, n = P.n, lw = P.lmax + 1, L = P.L, Sn = S * n, tid = threadIdx.x;
-    const int Fe = P.Fe;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int Fe = P.Fe, half = Sn * lw, snl = n * lw;
     const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
     if (e1 == e0) return;
+    const int RBk = row_block(NWJ * W);
 
-    double *cc = smem;                // [S][n][L]
-    double *U4 = cc + (size_t)Sn * L; // [EB][Sn][lw][4]
+    Carver cv{smem};
+    Tables T;
+    load_tables(P, cv, T, 0, lw);
+    double *cc = cv.take((size_t)Sn * L); // [S][n][L]
+    double *rgeo = cv.take(4 * (size_t)RBk);
+    int *rsp = (int *)cv.take((RBk + 1) / 2);
+    uint32_t *tab = (uint32_t *)cv.take(tab_lds ? ((size_t)S * Fe + 1) / 2 : 0);
+    // this wave's private staging
+    double *wbase = cv.take(0) + (size_t)wave * jac_wave_doubles(P, W);
+    Carver wv{wbase};
     Stage st;
-    st.geo = U4 + (size_t)EB * Sn * lw * 4;
-    st.Y = st.geo + 4 * EB;
-    st.dY = st.Y + EB * L;
-    st.B = st.dY + 3 * EB * L;
-    st.Bh = st.B + EB * n * lw;
-    st.T = st.Bh + EB * n * lw;
-    st.sp = (int *)(st.T + (P.rbf ? (size_t)EB * P.Q * (lw + 1) : 0));
+    st.Y = wv.take((size_t)W * L);
+    st.dY = wv.take(3 * (size_t)W * L);
+    st.BB = (double2 *)wv.take(2 * (size_t)W * n * lw);
+    const size_t xd = stage_x_doubles(P, lw, lw);
+    const size_t xu = xd > (size_t)4 * half ? xd : (size_t)4 * half;
+    double *XU = wv.take((size_t)W * xu);
+    st.X = XU;                 // quadrature / exponential scratch, dead after the radial factors
+    double2 *U2 = (double2 *)XU; // U2[e][0][u][l] = (U, Vx), U2[e][1][u][l] = (Vy, Vz)
 
     const double *cg = c_scratch + ci * (size_t)Sn * L;
-    for (int k = tid; k < Sn * L; k += BS) cc[k] = cg[k];
+    for (int k = tid; k < Sn * L; k += BSJ) cc[k] = cg[k];
+    if (tab_lds)
+        for (int k = tid; k < S * Fe; k += BSJ) tab[k] = P.fe[k];
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
 
-    for (int64_t base = e0; base < e1; base += EB) {
-        const int nb = (int)((e1 - base) < EB ? (e1 - base) : EB);
+    for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
+        const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
         __syncthreads();
-        stage_geometry(st, pos, R.spec, R.cols, base, nb, pi);
+        load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
         __syncthreads();
-        stage_angular_radial<true>(P, st, nb, 0, lw, true);
-        __syncthreads();
-        // U/V precontraction: items (edge, u = (nu, n'), l)
-        for (int it = tid; it < nb * Sn * lw; it += BS) {
-            const int e = it / (Sn * lw), rem = it - e * (Sn * lw), u = rem / lw, l = rem - u * lw;
-            const double *c = cc + (size_t)u * L + l * l;
-            const double *y = st.Y + e * L + l * l;
-            const double *dy = st.dY + e * 3 * L + l * l;
-            double U = 0.0, Vx = 0.0, Vy = 0.0, Vz = 0.0;
-            for (int m = 0; m < 2 * l + 1; ++m) {
-                const double cv = c[m];
-                U += y[m] * cv;
-                Vx += dy[m] * cv;
-                Vy += dy[L + m] * cv;
-                Vz += dy[2 * L + m] * cv;
+        for (int off = wave * W; off < rbn; off += NWJ * W) {
+            const int nb = (rbn - off) < W ? (rbn - off) : W;
+            const int64_t base = rb0 + off;
+            st.geo = rgeo + 4 * off;
+            st.sp = rsp + off;
+            stage_angular_radial<true, true>(P, T, st, nb, 0, lw, true, lane, 64);
+            wave_sync();
+            // U/V precontraction: items (l, edge, u = (nu, n'))
+            for (int it = lane; it < nb * half; it += 64) {
+                const int l = it / (nb * Sn), r2 = it - l * (nb * Sn), e = r2 / Sn, u = r2 - e * Sn;
+                const double *c = cc + (size_t)u * L + l * l;
+                const double *y = st.Y + e * L + l * l;
+                const double *dy = st.dY + e * 3 * L + l * l;
+                double U = 0.0, Vx = 0.0, Vy = 0.0, Vz = 0.0;
+                for (int m = 0; m < 2 * l + 1; ++m) {
+                    const double cv2 = c[m];
+                    U += y[m] * cv2;
+                    Vx += dy[m] * cv2;
+                    Vy += dy[L + m] * cv2;
+                    Vz += dy[2 * L + m] * cv2;
+                }
+                const int rem = u * lw + l;
+                U2[(size_t)(2 * e) * half + rem] = make_double2(U, Vx);
+                U2[(size_t)(2 * e + 1) * half + rem] = make_double2(Vy, Vz);
             }
-            double *o = U4 + (size_t)it * 4;
-            o[0] = U;
-            o[1] = Vx;
-            o[2] = Vy;
-            o[3] = Vz;
-        }
-        __syncthreads();
-        // assembly: items (edge, compressed feature)
-        for (int it = tid; it < nb * Fe; it += BS) {
-            const int e = it / Fe, fe = it - e * Fe;
-            const int s = st.sp[e];
-            const uint2 t = P.fe[(size_t)s * Fe + fe];
-            const int l = t.x & 0xff, nb1 = (t.x >> 8) & 0xff, u1 = (t.x >> 16) & 0xff, two = t.x >> 24;
-            const double *g = st.geo + 4 * e;
-            const double bh1 = st.Bh[(e * n + nb1) * lw + l] , b1 = st.B[(e * n + nb1) * lw + l];
-            const double *w1 = U4 + ((size_t)(e * Sn + u1) * lw + l) * 4;
-            double hu = bh1 * w1[0];
-            double jx = b1 * w1[1], jy = b1 * w1[2], jz = b1 * w1[3];
-            if (two) {
-                const int nb2 = t.y & 0xff, u2 = (t.y >> 8) & 0xff;
-                const double bh2 = st.Bh[(e * n + nb2) * lw + l], b2 = st.B[(e * n + nb2) * lw + l];
-                const double *w2 = U4 + ((size_t)(e * Sn + u2) * lw + l) * 4;
-                hu += bh2 * w2[0];
-                jx += b2 * w2[1];
-                jy += b2 * w2[2];
-                jz += b2 * w2[3];
+            wave_sync();
+            // stores: lanes own consecutive slots of each edge
+            for (int e = 0; e < nb; ++e) {
+                const int s = st.sp[e], sh = s * n * lw;
+                const double gx = st.geo[4 * e], gy = st.geo[4 * e + 1], gz = st.geo[4 * e + 2];
+                const double2 *BB = st.BB + e * snl;
+                const double2 *UA = U2 + (size_t)(2 * e) * half, *UB = U2 + (size_t)(2 * e + 1) * half;
+                OutT *o = jedge + ((base + e) * 3) * Fe;
+                for (int fe = lane; fe < Fe; fe += 64) {
+                    const uint32_t t = tab_lds ? tab[s * Fe + fe] : decode_slot(fe, s, n, lw);
+                    const int ob1 = t & 0xff, ou1 = (t >> 8) & 0xfff;
+                    const double2 bb1 = BB[ob1], w1 = UA[ou1], z1 = UB[ou1];
+                    double hu = bb1.y * w1.x;
+                    double jx = bb1.x * w1.y, jy = bb1.x * z1.x, jz = bb1.x * z1.y;
+                    if (t >> 20) {
+                        const int ob2 = ou1 - sh, ou2 = ob1 + sh;
+                        const double2 bb2 = BB[ob2], w2 = UA[ou2], z2 = UB[ou2];
+                        hu += bb2.y * w2.x;
+                        jx += bb2.x * w2.y;
+                        jy += bb2.x * z2.x;
+                        jz += bb2.x * z2.y;
+                    }
+                    store_nt(o + fe, hu * gx + jx);
+                    store_nt(o + Fe + fe, hu * gy + jy);
+                    store_nt(o + 2 * Fe + fe, hu * gz + jz);
+                }
             }
-            OutT *o = jedge + ((base + e) * 3) * Fe + fe;
-            store_nt(o, hu * g[0] + jx);
-            store_nt(o + Fe, hu * g[1] + jy);
-            store_nt(o + 2 * Fe, hu * g[2] + jz);
+            wave_sync();
         }
     }
 }
@@ -520,15 +696,19 @@ __global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int EC) {
     const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0), lgc = (size_t)(lg1 - lg0);
     const size_t SnL = (size_t)P.S * P.n * Lg;
-    size_t d = SnL * (jac ? 4 : 1);
-    d += (size_t)EC * (4 + Lg * (jac ? 4 : 1) + P.n * lgc * (jac ? 2 : 1) + (P.rbf ? P.Q * (lgc + 1) : 0));
-    return d * 8 + (size_t)EC * 4;
+    const int RBk = row_block(EC);
+    size_t d = table_doubles(P, (int)lgc) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
+               even(EC * Lg) + even(jac ? 3 * EC * Lg : 0) + even(2 * EC * P.n * lgc) +
+               even(EC * stage_x_doubles(P, (int)lgc, lg1));
+    return d * 8;
 }
 
-size_t jacobian_lds_bytes(const Params &P, int EB) {
-    const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1, Sn = (size_t)P.S * P.n;
-    size_t d = Sn * L + (size_t)EB * (Sn * lw * 4 + 4 + 4 * L + 2 * P.n * lw + (P.rbf ? P.Q * (lw + 1) : 0));
-    return d * 8 + (size_t)EB * 4;
+size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds) {
+    const size_t L = (size_t)P.L, Sn = (size_t)P.S * P.n;
+    const int RBk = row_block(NWJ * W);
+    size_t d = table_doubles(P, P.lmax + 1) + even(Sn * L) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
+               even(tab_lds ? ((size_t)P.S * P.Fe + 1) / 2 : 0) + NWJ * jac_wave_doubles(P, W);
+    return d * 8;
 }
 
 hipError_t set_lds_limits() {
@@ -574,13 +754,13 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
-    dim3 grid((unsigned)R.nc), block(BS);
+    dim3 grid((unsigned)R.nc), block(BSJ);
     if (f64)
-        hipLaunchKernelGGL((k_jacobian<double, double>), grid, block, cfg.lds, st, P, R, (const double *)pos, cfg.EB,
-                           c_scratch, (double *)jedge);
+        hipLaunchKernelGGL((k_jacobian<double, double>), grid, block, cfg.lds, st, P, R, (const double *)pos, cfg.W,
+                           cfg.tab_lds, c_scratch, (double *)jedge);
     else
-        hipLaunchKernelGGL((k_jacobian<float, float>), grid, block, cfg.lds, st, P, R, (const float *)pos, cfg.EB,
-                           c_scratch, (float *)jedge);
+        hipLaunchKernelGGL((k_jacobian<float, float>), grid, block, cfg.lds, st, P, R, (const float *)pos, cfg.W,
+                           cfg.tab_lds, c_scratch, (float *)jedge);
     return hipGetLastError();
 }
 

@@ -20,8 +20,8 @@ MAX_DEGREE = 2048
 # every entry point declared in include/soap.h
 ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_num_features", "soap_num_edge_features",
                "soap_feature_labels", "soap_feature_map", "soap_build_neighbors", "soap_get_neighbors",
-               "soap_compute", "soap_coefficients", "soap_derivatives", "soap_scatter_dense", "soap_last_error",
-               "soap_destroy")
+               "soap_compute", "soap_coefficients", "soap_derivatives", "soap_scatter_dense", "soap_timing",
+               "soap_last_error", "soap_destroy")
 
 _STATUS = {SOAP_EINVAL: "EINVAL", SOAP_ESPECIES: "ESPECIES", SOAP_ENOMEM: "ENOMEM", SOAP_EHIP: "EHIP",
            SOAP_ECAPACITY: "ECAPACITY", SOAP_ESTATE: "ESTATE"}
@@ -69,6 +69,8 @@ def load_library(path: str = LIB_PATH):
     L.soap_derivatives.argtypes = [vp, vp, vp, vp, vp]
     L.soap_scatter_dense.restype = ctypes.c_int
     L.soap_scatter_dense.argtypes = [vp, vp, vp, vp, vp]
+    L.soap_timing.restype = ctypes.c_int
+    L.soap_timing.argtypes = [vp, vp, vp, i32]
     L.soap_last_error.restype = ctypes.c_char_p
     L.soap_last_error.argtypes = [vp]
     L.soap_destroy.restype = None
@@ -101,7 +103,7 @@ class Soap:
         code = self._L.soap_create(z.ctypes.data, len(z), self.r_cut, self.n_max, self.l_max, self.sigma,
                                    SOAP_RBF_GTO if rbf == "gto" else SOAP_RBF_POLYNOMIAL, ctypes.byref(h))
         if code != SOAP_OK:
-            raise SoapError(code, "soap_create failed")
+            raise SoapError(code, "soap_create: " + self._L.soap_last_error(None).decode())
         self._h = h
         if self.dtype == torch.float64:
             self._check(self._L.soap_set_option(self._h, b"dtype", SOAP_FP64))
@@ -128,6 +130,18 @@ class Soap:
             self.close()
         except Exception:
             pass
+
+    def set_timing(self, on: bool):
+        self._check(self._L.soap_set_option(self._h, b"timing", 1 if on else 0))
+
+    def timing(self, reset: bool = True):
+        """(ms[3], counts[3]) summed over timed calls: neighbour search, density
+        kernel, edge Jacobian kernel."""
+        import numpy as np
+        ms = np.zeros(3)
+        cnt = np.zeros(3, dtype=np.int64)
+        self._check(self._L.soap_timing(self._h, ms.ctypes.data, cnt.ctypes.data, 1 if reset else 0))
+        return ms, cnt
 
     def feature_labels(self):
         import numpy as np
