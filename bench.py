@@ -68,6 +68,37 @@ def density_flops(wl, E, n_centers, F):
     return E * per_edge + n_centers * per_center
 
 
+def measured_traffic(workload_name, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    runs (FETCH_SIZE, WRITE_SIZE, each scaled by the reading of a plain copy of
+    known size), or None if absent or taken on different kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    src = os.path.join(ROOT, "paper_2609_05709_amd", "csrc", "soap_kernels.hip")
+    try:
+        doc = json.load(open(path))[workload_name]
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        if doc["kernels_source_sha256_16"] != sha:
+            return None
+        k = doc["per_launch"][kernel]
+        return k["fetch_bytes"] + k["write_bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    """A plain device copy of 1 GiB, three times: the reference reading for
+    scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+    n = 256 * 1024 * 1024
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "repeats": 3}))
+
+
 def cpu_baseline(wl, st, budget_s=12.0):
     """The oracle as it stands, on the host cores, over a bounded sample of
     centers (batches of 128 until ~budget_s of wall time)."""
@@ -137,12 +168,13 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
         # the edge-block writes dominate: HBM-bound kernel
         t = kern["jacobian"] * 1e-3
         roof = {"kernel": "k_jacobian", "bound": "hbm", "achieved": alg["jacobian"] / t / 1e9, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "traffic": None}
+                "unit": "GB/s", "traffic": measured_traffic(wl.name, "k_jacobian"),
+                "alg_bytes_per_launch": alg["jacobian"]}
     else:
         fl = density_flops(wl, E, nc, sp.n_features)
         t = kern["density"] * 1e-3
         roof = {"kernel": "k_density", "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "traffic": None}
+                "unit": "TFLOP/s", "traffic": measured_traffic(wl.name, "k_density"), "alg_flops_per_launch": fl}
     roof["frac"] = roof["achieved"] / roof["peak"]
     line = {
         "metric": METRIC,
@@ -182,11 +214,15 @@ def main():
     ap.add_argument("--dtype", default="float32", choices=["float32", "float64"])
     ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for both bases; write JSONL here")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the SOAP path here is built and timed on a single MI355X "
               "(centers shard across GPUs without communication; see DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+    if a.copy_calibration:
+        copy_calibration()
+        return
     if a.grid:
         from paper_2609_05709_amd import workloads as w
         with open(a.grid, "w") as f:

@@ -46,7 +46,7 @@ struct DevBuf {
 
 constexpr size_t DENSITY_LDS_BUDGET = 64 * 1024;
 constexpr size_t JACOBIAN_LDS_BUDGET = 80 * 1024;
-constexpr size_t LDS_HARD_LIMIT = 160 * 1024;
+constexpr size_t LDS_HARD_LIMIT = 159 * 1024; // leaves room for static LDS
 
 thread_local std::string g_create_error = "";
 
@@ -68,7 +68,7 @@ struct soap_ctx {
     // neighbour workspace
     NbrWork nw{};
     DevBuf b_bcount, b_bstart, b_bfill, b_acell, b_scell, b_spos, b_satom, b_deg, b_scan, b_flags, b_spec,
-        b_row, b_cols, b_cscratch;
+        b_row, b_cols, b_cscratch, b_work;
     int32_t *h_flags = nullptr; // pinned: [0..3] flags, then int64 E at offset 8
     // state of the last neighbour build
     bool have_rows = false;
@@ -150,8 +150,10 @@ void build_feature_tables(soap_ctx *c) {
     }
 }
 
-// Split l = 0..lmax into groups whose density-kernel LDS fits the budget.
-int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *EC_out, size_t *lds_out) {
+// Split l = 0..lmax into contiguous groups such that each group's
+// coefficient entries fit the density kernel's registers (n * Lg <= 512) and
+// its LDS fits the budget; W = edges per wave iteration.
+int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *W_out, size_t *lds_out) {
     const int lw = P.lmax + 1;
     for (int G = 1; G <= lw; ++G) {
         // contiguous groups balancing sum over l of (2l+1): cut k at the l with
@@ -166,13 +168,17 @@ int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *EC_out, 
             bounds[k] = b;
         }
         bounds[G] = lw;
-        for (int EC : {64, 32, 16, 8, 4}) {
+        bool ok = true;
+        for (int k = 0; k < G; ++k)
+            if (P.n * (bounds[k + 1] * bounds[k + 1] - bounds[k] * bounds[k]) > 64 * DENSITY_KE) ok = false;
+        if (!ok) continue;
+        for (int W : {4, 2, 1}) {
             size_t worst = 0;
-            for (int k = 0; k < G; ++k) worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], EC));
-            if (worst <= DENSITY_LDS_BUDGET || (G == lw && EC == 4 && worst <= LDS_HARD_LIMIT)) {
+            for (int k = 0; k < G; ++k) worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], W));
+            if (worst <= DENSITY_LDS_BUDGET || (W == 1 && worst <= LDS_HARD_LIMIT)) {
                 for (int k = 0; k <= G; ++k) lgrp[k] = bounds[k];
                 *ngroups = G;
-                *EC_out = EC;
+                *W_out = W;
                 *lds_out = worst;
                 return 0;
             }
@@ -183,16 +189,19 @@ int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *EC_out, 
 
 int plan_launches(soap_ctx *c) {
     Params &P = c->P;
-    int EC;
+    int Wd;
     size_t lds;
-    if (plan_groups(P, 0, c->lgrp_desc, &c->groups_desc, &EC, &lds) != 0)
-        return fail(c, SOAP_EINVAL, "basis too large for the descriptor kernel's on-chip memory");
-    c->dens_cfg[0].EC = EC;
-    c->dens_cfg[0].lds = lds;
-    if (plan_groups(P, 1, c->lgrp_jac, &c->groups_jac, &EC, &lds) != 0)
-        return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
-    c->dens_cfg[1].EC = EC;
-    c->dens_cfg[1].lds = lds;
+    int ncu = 256;
+    (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
+    for (int jac = 0; jac < 2; ++jac) {
+        int *lgrp = jac ? c->lgrp_jac : c->lgrp_desc, *G = jac ? &c->groups_jac : &c->groups_desc;
+        if (plan_groups(P, jac, lgrp, G, &Wd, &lds) != 0)
+            return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
+        c->dens_cfg[jac].W = Wd;
+        c->dens_cfg[jac].lds = lds;
+        const int per_cu = density_blocks_per_cu(c->dtype == SOAP_FP64, jac != 0, lds);
+        c->dens_cfg[jac].blocks = std::max(1, ncu * per_cu / *G);
+    }
     // Jacobian kernel: W edges per wave iteration; slot table in LDS when small
     const int tab = (size_t)P.S * P.Fe * 4 <= 16 * 1024 ? 1 : 0;
     int W = 2;
@@ -382,6 +391,7 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
     if (e == hipSuccess) e = set_lds_limits();
     if (e == hipSuccess) e = hipHostMalloc((void **)&c->h_flags, 64, hipHostMallocDefault);
     if (e != hipSuccess) {
+        g_create_error = std::string("HIP setup failed: ") + hipGetErrorString(e);
         delete c;
         return e == hipErrorOutOfMemory ? SOAP_ENOMEM : SOAP_EHIP;
     }
@@ -543,9 +553,11 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
+    hipError_t e0 = c->b_work.ensure(sizeof(int) * (MAX_GROUPS + 1));
+    if (e0 != hipSuccess) return hip_fail(c, e0, "hipMalloc(work counters)");
     SegTimer timer(c, 1, to_stream(stream));
-    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0], desc, c_out,
-                                  jself, scratch, to_stream(stream));
+    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0],
+                                  c->b_work.as<int>(), desc, c_out, jself, scratch, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
     timer.done();
     return SOAP_OK;
@@ -624,7 +636,7 @@ void soap_destroy(soap_ctx *c) {
     (void)hipDeviceSynchronize();
     for (DevBuf *b : {&c->d_const, &c->d_fq, &c->d_fe, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
                       &c->b_acell, &c->b_scell, &c->b_spos, &c->b_satom, &c->b_deg, &c->b_scan, &c->b_flags,
-                      &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch})
+                      &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch, &c->b_work})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
     for (auto &r : c->recs) {

@@ -74,8 +74,55 @@ __global__ void k_bucket_fill(int64_t n, const PosT *__restrict__ pos, const int
     satom[slot] = (int32_t)i;
 }
 
-// One 64-lane wave per center (four centers per workgroup); lanes 0..26
-// each walk one of the 27 neighbouring cells.
+// Candidate enumeration shared by the count and fill passes: one 64-lane wave
+// per center.  Lanes 0..26 look up one neighbouring cell each (bucket range
+// and cell coordinates) into the wave's LDS slots; a prefix over the 27
+// bucket sizes then lets every lane take candidates t = lane, lane + 64, ...
+// of the concatenated buckets, so the loads of one center are spread over
+// the whole wave instead of walking each bucket serially.
+struct CellSlots {
+    int off[28];   // prefix of bucket sizes
+    int start[27]; // first sorted slot of each bucket
+    int cx[27], cy[27], cz[27];
+};
+
+__device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 ci, const int32_t *__restrict__ start,
+                                                 uint32_t mask) {
+    int sz = 0;
+    if (lane < 27) {
+        const int tx = ci.x + lane % 3 - 1, ty = ci.y + (lane / 3) % 3 - 1, tz = ci.z + lane / 9 - 1;
+        const uint32_t b = cell_hash(tx, ty, tz, mask);
+        const int s0 = start[b];
+        sz = start[b + 1] - s0;
+        cs.start[lane] = s0;
+        cs.cx[lane] = tx;
+        cs.cy[lane] = ty;
+        cs.cz[lane] = tz;
+    }
+    // inclusive scan of sz over lanes 0..26
+    int v = sz;
+    for (int d = 1; d < 32; d <<= 1) {
+        const int u = __shfl_up(v, d, 64);
+        if (lane >= d) v += u;
+    }
+    if (lane < 27) cs.off[lane + 1] = v;
+    if (lane == 0) cs.off[0] = 0;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    return cs.off[27];
+}
+
+// Candidate t of the concatenated buckets: its sorted slot, or -1 if it
+// belongs to another cell that shares the bucket.
+__device__ __forceinline__ int candidate_slot(const CellSlots &cs, int t, const int4 *__restrict__ scell) {
+    int d = 0;
+    while (cs.off[d + 1] <= t) ++d;
+    const int slot = cs.start[d] + (t - cs.off[d]);
+    const int4 sc = scell[slot];
+    return (sc.x == cs.cx[d] && sc.y == cs.cy[d] && sc.z == cs.cz[d]) ? slot : -1;
+}
+
 template <typename PosT>
 __global__ __launch_bounds__(256) void k_count(int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers,
                                                const PosT *__restrict__ pos, const int4 *__restrict__ cell,
@@ -83,8 +130,9 @@ __global__ __launch_bounds__(256) void k_count(int64_t n_atoms, int64_t nc, cons
                                                const double4 *__restrict__ spos, const int32_t *__restrict__ satom,
                                                uint32_t mask, double rc2, int32_t *__restrict__ deg,
                                                int32_t *__restrict__ flags) {
-    const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
+    __shared__ CellSlots slots[4];
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t c = (int64_t)blockIdx.x * 4 + w;
     if (c >= nc) return;
     const int64_t i = centers ? (int64_t)centers[c] : c;
     if (i < 0 || i >= n_atoms) {
@@ -94,18 +142,15 @@ __global__ __launch_bounds__(256) void k_count(int64_t n_atoms, int64_t nc, cons
         }
         return;
     }
+    CellSlots &cs = slots[w];
+    const int total = wave_prefix_cells(cs, lane, cell[i], start, mask);
+    const double3 pi = load_pos(pos, i);
     int cnt = 0;
-    if (lane < 27) {
-        const int4 ci = cell[i];
-        const double3 pi = load_pos(pos, i);
-        const int tx = ci.x + lane % 3 - 1, ty = ci.y + (lane / 3) % 3 - 1, tz = ci.z + lane / 9 - 1;
-        const uint32_t b = cell_hash(tx, ty, tz, mask);
-        for (int t = start[b]; t < start[b + 1]; ++t) {
-            int4 sc = scell[t];
-            if (sc.x != tx || sc.y != ty || sc.z != tz || satom[t] == (int32_t)i) continue;
-            double4 q = spos[t];
-            if (within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2)) ++cnt;
-        }
+    for (int t = lane; t < total; t += 64) {
+        const int slot = candidate_slot(cs, t, scell);
+        if (slot < 0 || satom[slot] == (int32_t)i) continue;
+        const double4 q = spos[slot];
+        if (within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2)) ++cnt;
     }
     for (int off = 32; off > 0; off >>= 1) cnt += __shfl_down(cnt, off, 64);
     if (lane == 0) {
@@ -114,9 +159,9 @@ __global__ __launch_bounds__(256) void k_count(int64_t n_atoms, int64_t nc, cons
     }
 }
 
-// One 64-lane workgroup per center.  Lanes 0..26 each walk one neighbour
-// cell; keys (species << 32 | atom) land in LDS; each key's rank among the
-// row's keys is its position in the output row.
+// One 64-lane workgroup per center: matching candidates are appended to the
+// LDS key list (slot from a ballot prefix), keys (species << 32 | atom) are
+// unique and each key's rank among the row's keys is its output position.
 template <typename PosT>
 __global__ __launch_bounds__(64) void k_fill_sort(int64_t nc, const int32_t *__restrict__ centers,
                                                   const PosT *__restrict__ pos, const uint8_t *__restrict__ spec,
@@ -125,46 +170,38 @@ __global__ __launch_bounds__(64) void k_fill_sort(int64_t nc, const int32_t *__r
                                                   const int32_t *__restrict__ satom, uint32_t mask, double rc2,
                                                   const int64_t *__restrict__ row_ptr, int32_t *__restrict__ cols) {
     __shared__ int64_t keys[MAX_DEGREE];
-    __shared__ int cnt[32];
+    __shared__ CellSlots cs;
     const int64_t c = blockIdx.x;
     const int lane = threadIdx.x;
-    const int64_t i = centers ? (int64_t)centers[c] : c;
     const int64_t r0 = row_ptr[c];
     const int deg = (int)(row_ptr[c + 1] - r0);
     if (deg == 0) return;
-    const int4 ci = cell[i];
+    const int64_t i = centers ? (int64_t)centers[c] : c;
+    const int total = wave_prefix_cells(cs, lane, cell[i], start, mask);
     const double3 pi = load_pos(pos, i);
-    int tx = 0, ty = 0, tz = 0, mine = 0;
-    uint32_t b = 0;
-    if (lane < 27) {
-        tx = ci.x + lane % 3 - 1;
-        ty = ci.y + (lane / 3) % 3 - 1;
-        tz = ci.z + lane / 9 - 1;
-        b = cell_hash(tx, ty, tz, mask);
-        for (int t = start[b]; t < start[b + 1]; ++t) {
-            int4 sc = scell[t];
-            if (sc.x != tx || sc.y != ty || sc.z != tz || satom[t] == (int32_t)i) continue;
-            double4 q = spos[t];
-            if (within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2)) ++mine;
+    int base = 0;
+    for (int t0 = 0; t0 < total; t0 += 64) {
+        const int t = t0 + lane;
+        bool hit = false;
+        int j = 0;
+        if (t < total) {
+            const int slot = candidate_slot(cs, t, scell);
+            if (slot >= 0) {
+                j = satom[slot];
+                if (j != (int32_t)i) {
+                    const double4 q = spos[slot];
+                    hit = within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2);
+                }
+            }
         }
-        cnt[lane] = mine;
-    }
-    __syncthreads();
-    if (lane < 27) {
-        int off = 0;
-        for (int k = 0; k < lane; ++k) off += cnt[k];
-        for (int t = start[b]; t < start[b + 1]; ++t) {
-            int4 sc = scell[t];
-            int j = satom[t];
-            if (sc.x != tx || sc.y != ty || sc.z != tz || j == (int32_t)i) continue;
-            double4 q = spos[t];
-            if (within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2) && off < MAX_DEGREE)
-                keys[off++] = ((int64_t)spec[j] << 32) | (int64_t)(uint32_t)j;
-        }
+        const uint64_t m = __ballot(hit);
+        const int pre = __popcll(m & ((1ull << lane) - 1ull));
+        if (hit && base + pre < MAX_DEGREE) keys[base + pre] = ((int64_t)spec[j] << 32) | (int64_t)(uint32_t)j;
+        base += __popcll(m);
     }
     __syncthreads();
     for (int k = lane; k < deg; k += 64) {
-        int64_t key = keys[k];
+        const int64_t key = keys[k];
         int rank = 0;
         for (int t = 0; t < deg; ++t) rank += keys[t] < key;
         cols[r0 + rank] = (int32_t)(key & 0xffffffff);

@@ -64,8 +64,9 @@ hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool p
 
 // ---- descriptor kernels (soap_kernels.hip) ----
 struct DensityLaunch {
-    int EC;          // edges staged per chunk
+    int W;           // edges per wave iteration
     size_t lds;      // dynamic LDS bytes
+    int blocks;      // persistent workgroups per l-group
 };
 struct JacLaunch {
     int W;          // edges per wave iteration
@@ -73,13 +74,15 @@ struct JacLaunch {
     size_t lds;
 };
 
-size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int EC);
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W);
+int density_blocks_per_cu(bool f64, bool jac, size_t lds);
+constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds);
 hipError_t set_lds_limits();
 
 // desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
-                          const DensityLaunch &cfg, void *desc, void *c_out, void *jself, double *c_scratch,
+                          const DensityLaunch &cfg, int *work, void *desc, void *c_out, void *jself, double *c_scratch,
                           hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);

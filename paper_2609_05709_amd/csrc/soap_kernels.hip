@@ -30,6 +30,8 @@
 // All arithmetic is float64; outputs are converted once at the store.
 #include "soap_internal.h"
 
+#include <algorithm>
+
 namespace soap {
 namespace {
 
@@ -208,6 +210,7 @@ __host__ __device__ __forceinline__ int row_block(int EC) { return EC >= 128 ? E
 // that no global load sits on the per-edge path: with the chip's store
 // traffic in flight, global load latency runs to microseconds.
 struct Tables {
+    const double *Kl;                      // K_l = pi sqrt(8/(2l+1)), l < 16
     const double *betaC, *betaCa, *aprime; // GTO: [lc][n][k], [lc][n][k], [lc][k]
     const double *G, *rq;                  // polynomial: [n][Q], [Q]
     const double *Nlm;                     // [ldN][ldN]
@@ -216,7 +219,7 @@ struct Tables {
 
 __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lgc) {
     const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
-    size_t d = even(ldN * ldN) + even(2 * ldN * ldN);
+    size_t d = 16 + even(ldN * ldN) + even(2 * ldN * ldN);
     if (P.rbf == 0) d += 2 * even((size_t)lgc * n * n) + even((size_t)lgc * n);
     else d += even(n * P.Q) + even((size_t)P.Q);
     return d;
@@ -226,9 +229,11 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     const int ldN = P.lmax + 2, n = P.n, lgc = lg1 - lg0, tid = threadIdx.x, bs = blockDim.x;
     // every pointer is assigned on every path, so the struct stays in
     // registers and the compiler keeps LDS (ds_*) addressing for it
+    double *Kl = cv.take(16);
     double *Nl = cv.take((size_t)ldN * ldN);
     double *rc = cv.take(2 * (size_t)ldN * ldN);
     const bool poly = P.rbf != 0;
+    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     const size_t szA = poly ? (size_t)n * P.Q : (size_t)lgc * n * n; // betaC | G
     const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n * n;     // betaCa | rq
     const size_t szC = poly ? 0 : (size_t)lgc * n;                   // aprime
@@ -246,6 +251,7 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
         for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
         for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
     }
+    T.Kl = Kl;
     T.Nlm = Nl;
     T.rcoef = (const double2 *)rc;
     T.betaC = A;
@@ -320,7 +326,7 @@ __device__ __forceinline__ void stage_angular_radial(const Params &P, const Tabl
                 b += bc[k] * E[k];
                 if (GRAD) bh += ba[k] * E[k];
             }
-            const double K = scaleK ? M_PI * sqrt(8.0 / (double)(2 * (lg0 + lc) + 1)) : 1.0;
+            const double K = scaleK ? T.Kl[lg0 + lc] : 1.0;
             st.BB[it] = make_double2(K * b, K * bh);
         }
     } else {
@@ -353,7 +359,7 @@ __device__ __forceinline__ void stage_angular_radial(const Params &P, const Tabl
                 b += G[q] * tl;
                 if (GRAD) bh += G[q] * (T.rq[q] * t[q * tw + l + 1] - r * tl);
             }
-            const double K = scaleK ? M_PI * sqrt(8.0 / (double)(2 * l + 1)) : 1.0;
+            const double K = scaleK ? T.Kl[l] : 1.0;
             if (r == 0.0) {
                 b = (l == 0) ? b : 0.0;
                 bh = 0.0;
@@ -388,20 +394,41 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
 
 // ---------------------------------------------------------------------------
 // k_density
+//
+// Persistent: a workgroup is bound to one l-group g (blockIdx % G), keeps
+// that group's basis tables in LDS, and takes centers from an atomic work
+// counter.  Per center, each wave runs its own pipeline over its own edges
+// (W at a time): harmonics + radial factors in the wave's LDS, then every
+// lane adds the edges' contributions to the coefficient entries (a, lm) it
+// owns, in registers: c^s_{a lm} += B_al S_lm and, for the Jacobian,
+// D^s_{a lm} += Bh_al r S_lm + B_al grad S_lm (D = sum over neighbours of
+// dc/dr_j = -dc/dr_i).  Register sums are flushed into the shared LDS
+// accumulators with atomic adds when the (sorted) neighbour species changes.
+// Then the whole workgroup writes the power spectrum and the center block
+// -K_l sum_m (D^mu c^nu + c^mu D^nu).
 // ---------------------------------------------------------------------------
+constexpr int NWD = 4, BSD = 64 * NWD;
+constexpr int KE = 8; // coefficient entries owned per lane: n * Lg <= 64 * KE
+
+__host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, int jac, int lg0, int lg1, int W) {
+    const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0), lgc = (size_t)(lg1 - lg0);
+    return even(W * Lg) + even(jac ? 3 * W * Lg : 0) + even(2 * W * P.n * lgc) + even(W * stage_x_doubles(P, (int)lgc, lg1));
+}
+
 template <typename PosT, typename OutT, bool JAC>
-__global__ __launch_bounds__(BS) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int EC,
-                                                OutT *__restrict__ desc, OutT *__restrict__ c_out,
-                                                OutT *__restrict__ jself, double *__restrict__ c_scratch) {
+__global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
+                                                 int *__restrict__ work, OutT *__restrict__ desc,
+                                                 OutT *__restrict__ c_out, OutT *__restrict__ jself,
+                                                 double *__restrict__ c_scratch) {
     extern __shared__ double smem[];
+    __shared__ int64_t s_next;
     const int G = P.n_groups;
-    const int64_t ci = blockIdx.x / G;
-    const int g = blockIdx.x - (int)(ci * G);
+    const int g = blockIdx.x % G;
     const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0;
     const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
-    const int S = P.S, n = P.n, tid = threadIdx.x;
-    const int nL = n * Lg, SnL = S * nL;
-    const int RBk = row_block(EC);
+    const int S = P.S, n = P.n, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int nL = n * Lg, SnL = S * nL, lw = P.lmax + 1, Lfull = P.L;
+    const int RBk = row_block(NWD * W);
 
     Carver cv{smem};
     Tables T;
@@ -410,111 +437,127 @@ __global__ __launch_bounds__(BS) void k_density(Params P, Rows R, const PosT *__
     double *Dacc = cacc + SnL; // [3][S][n][Lg]
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
+    Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W)};
     Stage st;
-    st.Y = cv.take((size_t)EC * Lg);
-    st.dY = cv.take(JAC ? 3 * (size_t)EC * Lg : 0);
-    st.BB = (double2 *)cv.take(2 * (size_t)EC * n * lgc);
-    st.X = cv.take(EC * stage_x_doubles(P, lgc, lg1));
+    st.Y = wv.take((size_t)W * Lg);
+    st.dY = wv.take(JAC ? 3 * (size_t)W * Lg : 0);
+    st.BB = (double2 *)wv.take(2 * (size_t)W * n * lgc);
+    st.X = wv.take(W * stage_x_doubles(P, lgc, lg1));
 
-    for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BS) cacc[k] = 0.0;
+    // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg
+    int ent[KE], oY[KE], oB[KE];
+#pragma unroll
+    for (int k = 0; k < KE; ++k) {
+        const int e = lane + 64 * k;
+        ent[k] = e < nL ? e : -1;
+        const int a = e / Lg, lmg = e - a * Lg;
+        oY[k] = lmg;
+        oB[k] = a * lgc + (e < nL ? isqrt_lm(lmg + lm0) - lg0 : 0);
+    }
 
-    const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
-    const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
-    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
-
-    for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
-        const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
+    for (;;) {
+        if (tid == 0) s_next = atomicAdd(&work[g], 1);
         __syncthreads();
-        load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
-        for (int off = 0; off < rbn; off += EC) {
-            const int nb = (rbn - off) < EC ? (rbn - off) : EC;
-            st.geo = rgeo + 4 * off;
-            st.sp = rsp + off;
+        const int64_t ci = s_next;
+        if (ci >= R.nc) break;
+        const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
+        const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
+        const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
+        for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BSD) cacc[k] = 0.0;
+
+        for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
+            const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
             __syncthreads();
-            stage_angular_radial<JAC>(P, T, st, nb, lg0, lg1, false);
+            load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
             __syncthreads();
-            // accumulate: each thread owns entries (a, lm) for every species
-            for (int ent = tid; ent < nL; ent += BS) {
-                const int a = ent / Lg, lmg = ent - a * Lg;
-                const int lc = isqrt_lm(lmg + lm0) - lg0;
-                double acc = 0.0, ax = 0.0, ay = 0.0, az = 0.0;
-                int cur = st.sp[0];
-                for (int e = 0; e < nb; ++e) {
-                    const int s = st.sp[e];
-                    if (s != cur) {
-                        cacc[cur * nL + ent] += acc;
-                        if (JAC) {
-                            Dacc[cur * nL + ent] += ax;
-                            Dacc[SnL + cur * nL + ent] += ay;
-                            Dacc[2 * SnL + cur * nL + ent] += az;
+            for (int off = wave * W; off < rbn; off += NWD * W) {
+                const int nb = (rbn - off) < W ? (rbn - off) : W;
+                st.geo = rgeo + 4 * off;
+                st.sp = rsp + off;
+                stage_angular_radial<JAC, true>(P, T, st, nb, lg0, lg1, false, lane, 64);
+                wave_sync();
+                // per owned entry: register sums over this group's edges, flushed
+                // to the shared accumulators at each species change
+#pragma unroll
+                for (int k = 0; k < KE; ++k) {
+                    if (ent[k] < 0) continue;
+                    double a0 = 0.0, ax = 0.0, ay = 0.0, az = 0.0;
+                    int cur = st.sp[0];
+                    for (int e = 0; e < nb; ++e) {
+                        const int s = st.sp[e];
+                        if (s != cur) {
+                            const int idx = cur * nL + ent[k];
+                            atomicAdd(&cacc[idx], a0);
+                            if (JAC) {
+                                atomicAdd(&Dacc[idx], ax);
+                                atomicAdd(&Dacc[SnL + idx], ay);
+                                atomicAdd(&Dacc[2 * SnL + idx], az);
+                            }
+                            a0 = ax = ay = az = 0.0;
+                            cur = s;
                         }
-                        acc = ax = ay = az = 0.0;
-                        cur = s;
+                        const double2 bb = st.BB[e * n * lgc + oB[k]];
+                        const double y = st.Y[e * Lg + oY[k]];
+                        a0 += bb.x * y;
+                        if (JAC) {
+                            const double bh = bb.y * y;
+                            const double *gg = st.geo + 4 * e, *dy = st.dY + e * 3 * Lg + oY[k];
+                            ax += bh * gg[0] + bb.x * dy[0];
+                            ay += bh * gg[1] + bb.x * dy[Lg];
+                            az += bh * gg[2] + bb.x * dy[2 * Lg];
+                        }
                     }
-                    const double2 bb = st.BB[(e * n + a) * lgc + lc];
-                    const double y = st.Y[e * Lg + lmg];
-                    acc += bb.x * y;
+                    const int idx = cur * nL + ent[k];
+                    atomicAdd(&cacc[idx], a0);
                     if (JAC) {
-                        const double bh = bb.y * y;
-                        const double *gg = st.geo + 4 * e;
-                        const double *dy = st.dY + e * 3 * Lg + lmg;
-                        ax += bh * gg[0] + bb.x * dy[0];
-                        ay += bh * gg[1] + bb.x * dy[Lg];
-                        az += bh * gg[2] + bb.x * dy[2 * Lg];
+                        atomicAdd(&Dacc[idx], ax);
+                        atomicAdd(&Dacc[SnL + idx], ay);
+                        atomicAdd(&Dacc[2 * SnL + idx], az);
                     }
                 }
-                cacc[cur * nL + ent] += acc;
-                if (JAC) {
-                    Dacc[cur * nL + ent] += ax;
-                    Dacc[SnL + cur * nL + ent] += ay;
-                    Dacc[2 * SnL + cur * nL + ent] += az;
-                }
+                wave_sync();
             }
         }
-    }
-    __syncthreads();
-    // on-site term of the center (its species, l = 0)
-    if (lg0 == 0)
-        for (int a = tid; a < n; a += BS) cacc[(int)R.spec[i] * nL + a * Lg] += P.c0[a];
-    __syncthreads();
-
-    const int lw = P.lmax + 1;
-    // power spectrum for the group's l
-    if (desc) {
-        for (int it = tid; it < P.nq_full * lgc; it += BS) {
-            const int q = it / lgc, lc = it - q * lgc, l = lg0 + lc;
-            const uint32_t f = P.fq[q];
-            const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
-            const double *x = cacc + mu * nL + a * Lg + l * l - lm0;
-            const double *y = cacc + nu * nL + b * Lg + l * l - lm0;
-            double acc = 0.0;
-            for (int m = 0; m < 2 * l + 1; ++m) acc += x[m] * y[m];
-            desc[ci * P.F + q * lw + l] = (OutT)(M_PI * sqrt(8.0 / (double)(2 * l + 1)) * acc);
+        __syncthreads();
+        // on-site term of the center (its species, l = 0)
+        if (lg0 == 0)
+            for (int a = tid; a < n; a += BSD) cacc[(int)R.spec[i] * nL + a * Lg] += P.c0[a];
+        __syncthreads();
+        // power spectrum for the group's l
+        if (desc)
+            for (int it = tid; it < P.nq_full * lgc; it += BSD) {
+                const int q = it / lgc, lc = it - q * lgc, l = lg0 + lc;
+                const uint32_t f = P.fq[q];
+                const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
+                const double *x = cacc + mu * nL + a * Lg + l * l - lm0;
+                const double *y = cacc + nu * nL + b * Lg + l * l - lm0;
+                double sum = 0.0;
+                for (int m = 0; m < 2 * l + 1; ++m) sum += x[m] * y[m];
+                desc[ci * P.F + q * lw + l] = (OutT)(T.Kl[l] * sum);
+            }
+        if (c_out)
+            for (int it = tid; it < SnL; it += BSD) {
+                const int sa = it / Lg, lmg = it - sa * Lg;
+                c_out[(ci * S * n + sa) * Lfull + lm0 + lmg] = (OutT)cacc[it];
+            }
+        if (JAC) {
+            for (int it = tid; it < SnL; it += BSD) {
+                const int sa = it / Lg, lmg = it - sa * Lg;
+                c_scratch[(ci * S * n + sa) * Lfull + lm0 + lmg] = cacc[it];
+            }
+            for (int it = tid; it < 3 * P.nq_full * lgc; it += BSD) {
+                const int d = it / (P.nq_full * lgc), rem = it - d * (P.nq_full * lgc);
+                const int q = rem / lgc, lc = rem - q * lgc, l = lg0 + lc;
+                const uint32_t f = P.fq[q];
+                const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
+                const int oa = mu * nL + a * Lg + l * l - lm0, ob = nu * nL + b * Lg + l * l - lm0;
+                const double *Dd = Dacc + d * SnL;
+                double sum = 0.0;
+                for (int m = 0; m < 2 * l + 1; ++m) sum += Dd[oa + m] * cacc[ob + m] + cacc[oa + m] * Dd[ob + m];
+                jself[(ci * 3 + d) * P.F + q * lw + l] = (OutT)(-T.Kl[l] * sum);
+            }
         }
-    }
-    const int Lfull = P.L;
-    if (c_out)
-        for (int it = tid; it < SnL; it += BS) {
-            const int sa = it / Lg, lmg = it - sa * Lg;
-            c_out[(ci * S * n + sa) * Lfull + lm0 + lmg] = (OutT)cacc[it];
-        }
-    if (JAC) {
-        for (int it = tid; it < SnL; it += BS) {
-            const int sa = it / Lg, lmg = it - sa * Lg;
-            c_scratch[(ci * S * n + sa) * Lfull + lm0 + lmg] = cacc[it];
-        }
-        // center block: -K_l sum_m (D^mu_{n l m} c^nu_{n' l m} + c^mu D^nu)
-        for (int it = tid; it < 3 * P.nq_full * lgc; it += BS) {
-            const int d = it / (P.nq_full * lgc), rem = it - d * (P.nq_full * lgc);
-            const int q = rem / lgc, lc = rem - q * lgc, l = lg0 + lc;
-            const uint32_t f = P.fq[q];
-            const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
-            const int oa = mu * nL + a * Lg + l * l - lm0, ob = nu * nL + b * Lg + l * l - lm0;
-            const double *Dd = Dacc + d * SnL;
-            double acc = 0.0;
-            for (int m = 0; m < 2 * l + 1; ++m) acc += Dd[oa + m] * cacc[ob + m] + cacc[oa + m] * Dd[ob + m];
-            jself[(ci * 3 + d) * P.F + q * lw + l] = (OutT)(-M_PI * sqrt(8.0 / (double)(2 * l + 1)) * acc);
-        }
+        __syncthreads();
     }
 }
 
@@ -693,14 +736,25 @@ __global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge
 
 } // namespace
 
-size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int EC) {
-    const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0), lgc = (size_t)(lg1 - lg0);
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W) {
+    const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0);
     const size_t SnL = (size_t)P.S * P.n * Lg;
-    const int RBk = row_block(EC);
-    size_t d = table_doubles(P, (int)lgc) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               even(EC * Lg) + even(jac ? 3 * EC * Lg : 0) + even(2 * EC * P.n * lgc) +
-               even(EC * stage_x_doubles(P, (int)lgc, lg1));
+    const int RBk = row_block(NWD * W);
+    size_t d = table_doubles(P, lg1 - lg0) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
+               NWD * dens_wave_doubles(P, jac, lg0, lg1, W);
     return d * 8;
+}
+
+int density_blocks_per_cu(bool f64, bool jac, size_t lds) {
+    int nb = 0;
+    hipError_t e;
+    if (f64)
+        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<double, double, true>, BSD, lds)
+                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<double, double, false>, BSD, lds);
+    else
+        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<float, float, true>, BSD, lds)
+                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<float, float, false>, BSD, lds);
+    return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
 size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds) {
@@ -712,7 +766,7 @@ size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds) {
 }
 
 hipError_t set_lds_limits() {
-    const int lim = 160 * 1024;
+    const int lim = 159 * 1024; // the kernels' static LDS uses part of the 160 KB
     hipError_t e = hipSuccess;
 #define SOAP_SET(K)                                                                                          \
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
@@ -727,26 +781,28 @@ hipError_t set_lds_limits() {
 }
 
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
-                          const DensityLaunch &cfg, void *desc, void *c_out, void *jself, double *c_scratch,
+                          const DensityLaunch &cfg, int *work, void *desc, void *c_out, void *jself, double *c_scratch,
                           hipStream_t st) {
-    const int64_t blocks = R.nc * P.n_groups;
-    if (blocks <= 0) return hipSuccess;
-    dim3 grid((unsigned)blocks), block(BS);
+    if (R.nc <= 0) return hipSuccess;
+    hipError_t e = hipMemsetAsync(work, 0, sizeof(int) * P.n_groups, st);
+    if (e != hipSuccess) return e;
+    int64_t per_group = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
+    dim3 grid((unsigned)(per_group * P.n_groups)), block(BSD);
     if (f64) {
         if (jac)
             hipLaunchKernelGGL((k_density<double, double, true>), grid, block, cfg.lds, st, P, R, (const double *)pos,
-                               cfg.EC, (double *)desc, (double *)c_out, (double *)jself, c_scratch);
+                               cfg.W, work, (double *)desc, (double *)c_out, (double *)jself, c_scratch);
         else
             hipLaunchKernelGGL((k_density<double, double, false>), grid, block, cfg.lds, st, P, R,
-                               (const double *)pos, cfg.EC, (double *)desc, (double *)c_out, (double *)jself,
+                               (const double *)pos, cfg.W, work, (double *)desc, (double *)c_out, (double *)jself,
                                c_scratch);
     } else {
         if (jac)
             hipLaunchKernelGGL((k_density<float, float, true>), grid, block, cfg.lds, st, P, R, (const float *)pos,
-                               cfg.EC, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
+                               cfg.W, work, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
         else
             hipLaunchKernelGGL((k_density<float, float, false>), grid, block, cfg.lds, st, P, R, (const float *)pos,
-                               cfg.EC, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
+                               cfg.W, work, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
     }
     return hipGetLastError();
 }
