@@ -19,6 +19,9 @@ HIP_FLAGS = [
     "-O3", "-fPIC", "-std=c++17", f"--offload-arch={ARCH}",
     # keep the compiler from emitting packed fp32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the accumulation chains are
+    # loop-carried, and the AGPR form copies them out and back per MFMA
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=gnu++17", "-fext-numeric-literals", "-I", os.path.join(ROOT, "include"), "-I", CSRC]

@@ -60,11 +60,11 @@ struct soap_ctx {
     int64_t F = 0, Fe = 0;
     int nq_full = 0;
     std::vector<uint32_t> fq;
-    std::vector<uint32_t> fe;     // [S][Fe] packed slots
+    std::vector<uint32_t> dtab;   // [tri lw] diagonal-pair slots of the Jacobian kernel
     std::vector<int32_t> fmap;    // [S][Fe]
     Params P{};
     // device constants
-    DevBuf d_const, d_fq, d_fe, d_fmap, d_lut;
+    DevBuf d_const, d_fq, d_dtab, d_fmap, d_lut;
     // neighbour workspace
     NbrWork nw{};
     DevBuf b_bcount, b_bstart, b_bfill, b_acell, b_scell, b_spos, b_satom, b_deg, b_scan, b_flags, b_spec,
@@ -122,32 +122,22 @@ void build_feature_tables(soap_ctx *c) {
     c->nq_full = (int)c->fq.size();
     c->F = (int64_t)c->nq_full * lw;
     c->Fe = (int64_t)lw * (n * (n + 1) / 2 + (S - 1) * n * n);
-    c->fe.assign((size_t)S * c->Fe, 0u);
     c->fmap.assign((size_t)S * c->Fe, 0);
-    // slot of species s: ob1 = n1 * lw + l | ou1 = u1 * lw + l << 8 | diag << 20
-    // (on the diagonal pair the second term uses ob2 = ou1 - s n lw,
-    // ou2 = ob1 + s n lw)
+    // fmap[s][k]: feature index of slot k of a species-s neighbour block
     for (int s = 0; s < S; ++s) {
         int64_t k = 0;
         for (int q = 0; q < c->nq_full; ++q) {
             const uint32_t f = c->fq[q];
-            const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
+            const int mu = f & 0xff, nu = (f >> 8) & 0xff;
             if (mu != s && nu != s) continue;
-            int nb1, u1, two = 0;
-            if (mu == s && nu == s) { // d/dr_j of sum_m c^s_a c^s_b: both factors
-                nb1 = a; u1 = s * n + b; two = 1;
-            } else if (mu == s) {     // derivative of the first factor
-                nb1 = a; u1 = nu * n + b;
-            } else {                  // derivative of the second factor
-                nb1 = b; u1 = mu * n + a;
-            }
-            for (int l = 0; l < lw; ++l, ++k) {
-                c->fe[(size_t)s * c->Fe + k] =
-                    (uint32_t)(nb1 * lw + l) | (uint32_t)(u1 * lw + l) << 8 | (uint32_t)two << 20;
-                c->fmap[(size_t)s * c->Fe + k] = q * lw + l;
-            }
+            for (int l = 0; l < lw; ++l, ++k) c->fmap[(size_t)s * c->Fe + k] = q * lw + l;
         }
     }
+    // diagonal-pair slots in feature order: (n, n' >= n, l) -> (n lw + l) | (n' lw + l) << 16
+    c->dtab.clear();
+    for (int a = 0; a < n; ++a)
+        for (int b = a; b < n; ++b)
+            for (int l = 0; l < lw; ++l) c->dtab.push_back((uint32_t)(a * lw + l) | (uint32_t)(b * lw + l) << 16);
 }
 
 // Split l = 0..lmax into contiguous groups such that each group's
@@ -202,15 +192,13 @@ int plan_launches(soap_ctx *c) {
         const int per_cu = density_blocks_per_cu(c->dtype == SOAP_FP64, jac != 0, lds);
         c->dens_cfg[jac].blocks = std::max(1, ncu * per_cu / *G);
     }
-    // Jacobian kernel: W edges per wave iteration; slot table in LDS when small
-    const int tab = (size_t)P.S * P.Fe * 4 <= 16 * 1024 ? 1 : 0;
-    int W = 2;
-    while (W > 1 && jacobian_lds_bytes(P, W, tab) > JACOBIAN_LDS_BUDGET) --W;
-    if (jacobian_lds_bytes(P, W, tab) > LDS_HARD_LIMIT)
+    // Jacobian kernel: W edges per wave tile
+    int W = jacobian_max_w();
+    while (W > 1 && jacobian_lds_bytes(P, W) > JACOBIAN_LDS_BUDGET) --W;
+    if (jacobian_lds_bytes(P, W) > LDS_HARD_LIMIT)
         return fail(c, SOAP_EINVAL, "basis too large for the Jacobian kernel's on-chip memory");
     c->jac_cfg.W = W;
-    c->jac_cfg.tab_lds = tab;
-    c->jac_cfg.lds = jacobian_lds_bytes(P, W, tab);
+    c->jac_cfg.lds = jacobian_lds_bytes(P, W);
     return SOAP_OK;
 }
 
@@ -238,7 +226,35 @@ int upload_constants(soap_ctx *c) {
             rcoef[2 * (l * ldN + m)] = (double)(2 * l - 1) / (double)(l - m);
             rcoef[2 * (l * ldN + m) + 1] = (double)(l + m - 1) / (double)(l - m);
         }
-    // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nlm
+    // gradient identities of the harmonics per (l, m >= 0): with the degree
+    // l-1 harmonics S', grad S_l,+-m takes S'_{m+1} with cA, S'_{m-1} with
+    // cB and S'_m with cC (the combinations are written out in the kernels)
+    std::vector<double> gcoef;
+    for (int l = 0; l <= c->lmax; ++l)
+        for (int m = 0; m <= l; ++m) {
+            const long double N = Nlm[(size_t)l * ldN + m];
+            auto Np = [&](int k) { return (long double)Nlm[(size_t)(l - 1) * ldN + k]; };
+            long double cA = 0, cB = 0, cC = 0;
+            if (l >= 1) {
+                if (m + 1 <= l - 1) cA = (m == 0 ? N : N / 2) / Np(m + 1);
+                if (m >= 1) cB = N * (long double)((l + m) * (l + m - 1)) / (2 * Np(m - 1));
+                if (m <= l - 1) cC = N * (long double)(l + m) / Np(m);
+            }
+            gcoef.push_back((double)cA);
+            gcoef.push_back((double)cB);
+            gcoef.push_back((double)cC);
+            gcoef.push_back((double)(l | m << 8));
+        }
+    // normalisation of the division-free harmonic recurrence: N_lm (2m-1)!! / (l-m)!
+    std::vector<double> Nt((size_t)ldN * ldN, 0.0);
+    for (int l = 0; l < ldN; ++l)
+        for (int m = 0; m <= l; ++m) {
+            long double v = Nlm[(size_t)l * ldN + m];
+            for (int k = 1; k <= m; ++k) v *= (long double)(2 * k - 1);
+            for (int k = 2; k <= l - m; ++k) v /= (long double)k;
+            Nt[(size_t)l * ldN + m] = (double)v;
+        }
+    // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nlm | Nt | rcoef | gcoef
     std::vector<double> all;
     size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
     size_t o_ba = all.size(); all.insert(all.end(), betaCa.begin(), betaCa.end());
@@ -247,8 +263,10 @@ int upload_constants(soap_ctx *c) {
     size_t o_rq = all.size(); all.insert(all.end(), rq.begin(), rq.end());
     size_t o_c0 = all.size(); all.insert(all.end(), c0.begin(), c0.end());
     size_t o_N = all.size(); all.insert(all.end(), Nlm.begin(), Nlm.end());
+    size_t o_Nt = all.size(); all.insert(all.end(), Nt.begin(), Nt.end());
     if (all.size() & 1) all.push_back(0.0); // 16-byte alignment of the double2 table
     size_t o_rc = all.size(); all.insert(all.end(), rcoef.begin(), rcoef.end());
+    size_t o_gc = all.size(); all.insert(all.end(), gcoef.begin(), gcoef.end());
     hipError_t e;
     if ((e = c->d_const.ensure(all.size() * 8)) != hipSuccess) return hip_fail(c, e, "hipMalloc(constants)");
     if ((e = hipMemcpy(c->d_const.p, all.data(), all.size() * 8, hipMemcpyHostToDevice)) != hipSuccess)
@@ -258,9 +276,9 @@ int upload_constants(soap_ctx *c) {
     if ((e = c->d_fq.ensure(c->fq.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fq)");
     if ((e = hipMemcpy(c->d_fq.p, c->fq.data(), c->fq.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
         return hip_fail(c, e, "hipMemcpy(fq)");
-    if ((e = c->d_fe.ensure(c->fe.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fe)");
-    if ((e = hipMemcpy(c->d_fe.p, c->fe.data(), c->fe.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
-        return hip_fail(c, e, "hipMemcpy(fe)");
+    if ((e = c->d_dtab.ensure(c->dtab.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(dtab)");
+    if ((e = hipMemcpy(c->d_dtab.p, c->dtab.data(), c->dtab.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+        return hip_fail(c, e, "hipMemcpy(dtab)");
     if ((e = c->d_fmap.ensure(c->fmap.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fmap)");
     if ((e = hipMemcpy(c->d_fmap.p, c->fmap.data(), c->fmap.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
         return hip_fail(c, e, "hipMemcpy(fmap)");
@@ -289,9 +307,12 @@ int upload_constants(soap_ctx *c) {
     P.rq = d + o_rq;
     P.c0 = d + o_c0;
     P.Nlm = d + o_N;
+    P.Nt = d + o_Nt;
     P.rcoef = reinterpret_cast<const double2 *>(d + o_rc);
+    P.gcoef = d + o_gc;
     P.fq = c->d_fq.as<uint32_t>();
-    P.fe = c->d_fe.as<uint32_t>();
+    P.dtab = c->d_dtab.as<uint32_t>();
+    P.tri_lw = (int)c->dtab.size();
     return plan_launches(c);
 }
 
@@ -408,9 +429,10 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
     if (!c || !key) return SOAP_EINVAL;
     if (!std::strcmp(key, "dtype")) {
         if (value != SOAP_FP32 && value != SOAP_FP64) return fail(c, SOAP_EINVAL, "dtype must be SOAP_FP32 or SOAP_FP64");
-        if (value != c->dtype) c->have_rows = false;
+        if (value == c->dtype) return SOAP_OK;
+        c->have_rows = false;
         c->dtype = (int)value;
-        return SOAP_OK;
+        return plan_launches(c); // occupancy of the float64 kernels
     }
     if (!std::strcmp(key, "timing")) {
         if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "timing must be 0 or 1");
@@ -634,7 +656,7 @@ const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : g_c
 void soap_destroy(soap_ctx *c) {
     if (!c) return;
     (void)hipDeviceSynchronize();
-    for (DevBuf *b : {&c->d_const, &c->d_fq, &c->d_fe, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
+    for (DevBuf *b : {&c->d_const, &c->d_fq, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
                       &c->b_acell, &c->b_scell, &c->b_spos, &c->b_satom, &c->b_deg, &c->b_scan, &c->b_flags,
                       &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch, &c->b_work})
         b->release();

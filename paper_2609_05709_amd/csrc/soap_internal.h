@@ -24,9 +24,12 @@ struct Params {
     const double *rq;          // polynomial [Q]
     const double *c0;          // on-site term [n]
     const double *Nlm;         // [lmax+2][lmax+2] real solid-harmonic normalisation
+    const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double2 *rcoef;      // [lmax+2][lmax+2] recurrence coefficients of the harmonics
+    const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)
     const uint32_t *fq;        // [nq_full] mu | nu<<8 | n<<16 | n'<<24
-    const uint32_t *fe;        // [S][Fe] packed neighbour-block slots (see k_jacobian)
+    const uint32_t *dtab;      // [tri_lw] diagonal-pair slots: (n lw + l) | (n' lw + l) << 16, n' >= n
+    int tri_lw;                // n (n + 1) / 2 * (l_max + 1)
     int n_groups;              // l-groups of the density kernel
     int lgrp[MAX_GROUPS + 1];  // group g covers l in [lgrp[g], lgrp[g+1])
 };
@@ -69,15 +72,15 @@ struct DensityLaunch {
     int blocks;      // persistent workgroups per l-group
 };
 struct JacLaunch {
-    int W;          // edges per wave iteration
-    int tab_lds;    // 1 = slot table staged in LDS, 0 = decoded arithmetically
+    int W;          // edges per wave tile (at most jacobian_max_w())
     size_t lds;
 };
 
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W);
 int density_blocks_per_cu(bool f64, bool jac, size_t lds);
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
-size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds);
+size_t jacobian_lds_bytes(const Params &P, int W);
+int jacobian_max_w();
 hipError_t set_lds_limits();
 
 // desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)

@@ -44,9 +44,10 @@ __device__ __forceinline__ int isqrt_lm(int lm) { // l such that l*l <= lm < (l+
     return l;
 }
 
-template <typename T> __device__ __forceinline__ void store_nt(T *p, double v) {
-    __builtin_nontemporal_store((T)v, p);
-}
+// Output stores are plain (write-back) stores: on this chip non-temporal
+// stores of the neighbour blocks' partial-line runs write back at about half
+// the bandwidth.
+template <typename T> __device__ __forceinline__ void store_out(T *p, double v) { *p = (T)v; }
 
 // ---------------------------------------------------------------------------
 // Real solid harmonics for one |m| column.
@@ -132,6 +133,39 @@ __device__ __forceinline__ void sh_column(int m, int l_lo, int l_hi, double x, d
     }
 }
 
+// Real solid harmonics of one column m (l = m .. lw-1) without gradients and
+// without divisions: with R_m = 1, R_{m+1} = (2m+1) z and
+//   R_l = (2l-1) z R_{l-1} - (l+m-1)(l-m-1) r^2 R_{l-2},
+// Q_l^m = (2m-1)!! R_l / (l-m)!, so S_l,m = Nt_lm R_l C_m, S_l,-m = Nt_lm R_l S_m
+// with Nt_lm = N_lm (2m-1)!! / (l-m)!.
+__device__ __forceinline__ void sh_col_y(int m, int lw, double x, double y, double z, const double *__restrict__ Nt,
+                                         int ldN, double *__restrict__ Y) {
+    const double r2 = x * x + y * y + z * z;
+    double c = 1.0, s = 0.0;
+    for (int k = 0; k < m; ++k) {
+        const double cn = x * c - y * s;
+        s = x * s + y * c;
+        c = cn;
+    }
+    double R1 = 0.0, R = 1.0; // R_{l-1}, R_l
+    for (int l = m; l < lw; ++l) {
+        if (l > m) {
+            const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
+            const double Rn = a * z * R - b * r2 * R1;
+            R1 = R;
+            R = Rn;
+        }
+        const double v = Nt[l * ldN + m] * R;
+        const int o = l * l + l;
+        if (m == 0) {
+            Y[o] = v;
+        } else {
+            Y[o + m] = v * c;
+            Y[o - m] = v * s;
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Scaled modified spherical Bessel functions ii_l(x) = e^-x i_l(x), l = 0..Lt.
 // x >= Lt(Lt+1)/6.9: upward recurrence from the closed forms of ii_0, ii_1
@@ -210,17 +244,22 @@ __host__ __device__ __forceinline__ int row_block(int EC) { return EC >= 128 ? E
 // that no global load sits on the per-edge path: with the chip's store
 // traffic in flight, global load latency runs to microseconds.
 struct Tables {
-    const double *Kl;                      // K_l = pi sqrt(8/(2l+1)), l < 16
-    const double *betaC, *betaCa, *aprime; // GTO: [lc][n][k], [lc][n][k], [lc][k]
-    const double *G, *rq;                  // polynomial: [n][Q], [Q]
-    const double *Nlm;                     // [ldN][ldN]
-    const double2 *rcoef;                  // [ldN][ldN]
+    const double *Kl;      // K_l = pi sqrt(8/(2l+1)), l < 16
+    const double2 *bcp;    // GTO: [k][n][lc] = (betaC, -2 betaC a') of B_nl = sum_k betaC_nk e^{-a'_kl r^2}
+    const double *aprime;  // GTO: [k][lc]
+    const double *G, *rq;  // polynomial: [n][Q], [Q]
+    const double *Nlm;     // [ldN][ldN]
+    const double *Nt;      // [ldN][ldN] N_lm (2m-1)!! / (l-m)!, for sh_col_y
+    const double2 *rcoef;  // [ldN][ldN]
+    const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_jac
 };
+
+__host__ __device__ __forceinline__ int grad_pairs(int lmax) { return (lmax + 1) * (lmax + 2) / 2; }
 
 __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lgc) {
     const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
-    size_t d = 16 + even(ldN * ldN) + even(2 * ldN * ldN);
-    if (P.rbf == 0) d += 2 * even((size_t)lgc * n * n) + even((size_t)lgc * n);
+    size_t d = 16 + 2 * even(ldN * ldN) + even(2 * ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
+    if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
     else d += even(n * P.Q) + even((size_t)P.Q);
     return d;
 }
@@ -231,34 +270,46 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     // registers and the compiler keeps LDS (ds_*) addressing for it
     double *Kl = cv.take(16);
     double *Nl = cv.take((size_t)ldN * ldN);
+    double *Ntl = cv.take((size_t)ldN * ldN);
     double *rc = cv.take(2 * (size_t)ldN * ldN);
+    double *gc = cv.take(4 * (size_t)grad_pairs(P.lmax));
     const bool poly = P.rbf != 0;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    const size_t szA = poly ? (size_t)n * P.Q : (size_t)lgc * n * n; // betaC | G
-    const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n * n;     // betaCa | rq
-    const size_t szC = poly ? 0 : (size_t)lgc * n;                   // aprime
-    double *A = cv.take(szA), *B = cv.take(szB), *C = cv.take(szC);
-    for (int k = tid; k < ldN * ldN; k += bs) Nl[k] = P.Nlm[k];
+    const size_t szA = poly ? (size_t)n * P.Q : 2 * (size_t)lgc * n * n; // (betaC, betaCa) pairs | G
+    const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n;              // aprime | rq
+    double *A = cv.take(szA), *B = cv.take(szB);
+    for (int k = tid; k < ldN * ldN; k += bs) {
+        Nl[k] = P.Nlm[k];
+        Ntl[k] = P.Nt[k];
+    }
     for (int k = tid; k < 2 * ldN * ldN; k += bs) rc[k] = ((const double *)P.rcoef)[k];
+    for (int k = tid; k < 4 * grad_pairs(P.lmax); k += bs) gc[k] = P.gcoef[k];
     if (!poly) {
+        // global [l][n][k] -> LDS [k][n][lc]; global [l][k] -> LDS [k][lc]
         const size_t o = (size_t)lg0 * n * n;
-        for (int k = tid; k < (int)szA; k += bs) {
-            A[k] = P.betaC[o + k];
-            B[k] = P.betaCa[o + k];
+        for (int s = tid; s < (int)(szA / 2); s += bs) {
+            const int lc = s / (n * n), r = s - lc * n * n, a = r / n, k = r - a * n;
+            const int d = (k * n + a) * lgc + lc;
+            A[2 * d] = P.betaC[o + s];
+            A[2 * d + 1] = P.betaCa[o + s];
         }
-        for (int k = tid; k < (int)szC; k += bs) C[k] = P.aprime[(size_t)lg0 * n + k];
+        for (int s = tid; s < (int)szB; s += bs) {
+            const int lc = s / n, k = s - lc * n;
+            B[k * lgc + lc] = P.aprime[(size_t)lg0 * n + s];
+        }
     } else {
         for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
         for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
     }
     T.Kl = Kl;
     T.Nlm = Nl;
+    T.Nt = Ntl;
     T.rcoef = (const double2 *)rc;
-    T.betaC = A;
+    T.gcoef = (const double2 *)gc;
+    T.bcp = (const double2 *)A;
     T.G = A;
-    T.betaCa = B;
+    T.aprime = B;
     T.rq = B;
-    T.aprime = C;
 }
 
 // Per-chunk edge staging, shared by both kernels.  LDS arrays:
@@ -272,6 +323,7 @@ struct Stage {
     double *geo, *Y, *dY, *X;
     double2 *BB;
     int *sp;
+    int ys, dys; // per-edge strides of Y and dY (dY components are Lg apart)
 };
 
 // X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
@@ -283,9 +335,19 @@ __host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int 
 // Synchronisation inside one wave: LDS writes become visible to the other
 // lanes and the compiler keeps LDS accesses on their side of the point.
 __device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
     __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+// Workgroup barrier ordering LDS only.  __syncthreads() also fences global
+// memory, which makes every wave wait for all of its outstanding output
+// stores; nothing here reads another wave's global writes, so the output
+// stream keeps flowing across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // Staging work is spread over `bs` threads starting at `tid`: the whole
@@ -300,31 +362,32 @@ __device__ __forceinline__ void stage_angular_radial(const Params &P, const Tabl
     const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0, lgc = lg1 - lg0, n = P.n, ldN = P.lmax + 2;
     const int n_sh = nb * lg1;
     if (P.rbf == 0) {
-        // harmonics (edge, m) and exponentials (edge, l, k) in one pass
+        // harmonics (edge, m) and exponentials X[e][k][lc] in one pass
         const int n_ex = nb * lgc * n;
         for (int it = tid; it < n_sh + n_ex; it += bs) {
             if (it < n_sh) {
                 const int e = it / lg1, m = it - e * lg1;
                 const double *g = st.geo + 4 * e;
-                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * Lg,
-                                GRAD ? st.dY + e * 3 * Lg : nullptr, Lg, lm0, g[3] == 0.0);
+                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * st.ys,
+                                GRAD ? st.dY + e * st.dys : nullptr, Lg, lm0, g[3] == 0.0);
             } else {
                 const int x = it - n_sh, e = x / (lgc * n), rem = x - e * (lgc * n);
                 const double r = st.geo[4 * e + 3];
                 st.X[x] = exp(-T.aprime[rem] * r * r);
             }
         }
-        if (WAVE) wave_sync(); else __syncthreads();
+        if (WAVE) wave_sync(); else lds_barrier();
         // B_nl = sum_k betaC^l_nk E_k, Bh_nl = sum_k betaCa^l_nk E_k
         for (int it = tid; it < nb * n * lgc; it += bs) {
             const int e = it / (n * lgc), rem = it - e * (n * lgc), a = rem / lgc, lc = rem - a * lgc;
-            const double *E = st.X + (size_t)(e * lgc + lc) * n;
-            const double *bc = T.betaC + ((size_t)lc * n + a) * n;
-            const double *ba = T.betaCa + ((size_t)lc * n + a) * n;
+            const double *E = st.X + (size_t)e * n * lgc + lc;
+            const double2 *bc = T.bcp + (size_t)a * lgc + lc;
             double b = 0.0, bh = 0.0;
             for (int k = 0; k < n; ++k) {
-                b += bc[k] * E[k];
-                if (GRAD) bh += ba[k] * E[k];
+                const double2 c = bc[(size_t)k * n * lgc];
+                const double v = E[k * lgc];
+                b += c.x * v;
+                if (GRAD) bh += c.y * v;
             }
             const double K = scaleK ? T.Kl[lg0 + lc] : 1.0;
             st.BB[it] = make_double2(K * b, K * bh);
@@ -337,8 +400,8 @@ __device__ __forceinline__ void stage_angular_radial(const Params &P, const Tabl
             if (it < n_sh) {
                 const int e = it / lg1, m = it - e * lg1;
                 const double *g = st.geo + 4 * e;
-                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * Lg,
-                                GRAD ? st.dY + e * 3 * Lg : nullptr, Lg, lm0, g[3] == 0.0);
+                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * st.ys,
+                                GRAD ? st.dY + e * st.dys : nullptr, Lg, lm0, g[3] == 0.0);
             } else {
                 const int x = it - n_sh, e = x / Q, q = x - e * Q;
                 const double r = st.geo[4 * e + 3], rq = T.rq[q];
@@ -346,7 +409,7 @@ __device__ __forceinline__ void stage_angular_radial(const Params &P, const Tabl
                 bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, st.X + (size_t)x * tw);
             }
         }
-        if (WAVE) wave_sync(); else __syncthreads();
+        if (WAVE) wave_sync(); else lds_barrier();
         for (int it = tid; it < nb * n * lgc; it += bs) {
             const int e = it / (n * lgc), rem = it - e * (n * lgc), a = rem / lgc, lc = rem - a * lgc;
             const int l = lg0 + lc;
@@ -441,6 +504,8 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     Stage st;
     st.Y = wv.take((size_t)W * Lg);
     st.dY = wv.take(JAC ? 3 * (size_t)W * Lg : 0);
+    st.ys = Lg;
+    st.dys = 3 * Lg;
     st.BB = (double2 *)wv.take(2 * (size_t)W * n * lgc);
     st.X = wv.take(W * stage_x_doubles(P, lgc, lg1));
 
@@ -457,8 +522,8 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
 
     for (;;) {
         if (tid == 0) s_next = atomicAdd(&work[g], 1);
-        __syncthreads();
-        const int64_t ci = s_next;
+        lds_barrier();
+        const int64_t ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
         if (ci >= R.nc) break;
         const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
         const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
@@ -467,9 +532,9 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
 
         for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
             const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
-            __syncthreads();
+            lds_barrier();
             load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
-            __syncthreads();
+            lds_barrier();
             for (int off = wave * W; off < rbn; off += NWD * W) {
                 const int nb = (rbn - off) < W ? (rbn - off) : W;
                 st.geo = rgeo + 4 * off;
@@ -518,11 +583,11 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                 wave_sync();
             }
         }
-        __syncthreads();
+        lds_barrier();
         // on-site term of the center (its species, l = 0)
         if (lg0 == 0)
             for (int a = tid; a < n; a += BSD) cacc[(int)R.spec[i] * nL + a * Lg] += P.c0[a];
-        __syncthreads();
+        lds_barrier();
         // power spectrum for the group's l
         if (desc)
             for (int it = tid; it < P.nq_full * lgc; it += BSD) {
@@ -543,7 +608,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
         if (JAC) {
             for (int it = tid; it < SnL; it += BSD) {
                 const int sa = it / Lg, lmg = it - sa * Lg;
-                c_scratch[(ci * S * n + sa) * Lfull + lm0 + lmg] = cacc[it];
+                c_scratch[(ci * Lfull + lm0 + lmg) * S * n + sa] = cacc[it];
             }
             for (int it = tid; it < 3 * P.nq_full * lgc; it += BSD) {
                 const int d = it / (P.nq_full * lgc), rem = it - d * (P.nq_full * lgc);
@@ -557,162 +622,385 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                 jself[(ci * 3 + d) * P.F + q * lw + l] = (OutT)(-T.Kl[l] * sum);
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
+}
+
+// floor(x / d) for 0 <= x < 2^22 with inv = 1/d correctly rounded: the
+// relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
+// next integer
+__device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x + 0.5f) * inv); }
+
+// ---------------------------------------------------------------------------
+// Per-tile staging of the Jacobian kernel: one wave, nb <= W edges.
+//   YY[e][0][lm] = S_lm, YY[e][1 + d][lm] = dS_lm/dx_d
+//   BB[e][n][l]  = K_l (B_nl, Bh_nl)
+//   X: GTO exponentials [e][k][l], or the polynomial table [e][q][0..l_max+1]
+// Phase 1 runs the harmonic columns (edge, m) without gradients next to the
+// exponentials; phase 2 takes each gradient from the degree l-1 harmonics.
+// With H_l^m = (x + iy)^m Q_l^m (so S_l,m = N_lm Re H, S_l,-m = N_lm Im H):
+//   d/dz H_l^m = (l+m) H_{l-1}^m,  (d/dx + i d/dy) H_l^m = -H_{l-1}^{m+1},
+//   (d/dx - i d/dy) H_l^m = (l+m)(l+m-1) H_{l-1}^{m-1},
+// so every component is at most two degree l-1 harmonics.  Per (l, m >= 0),
+// with S' = S_{l-1,.} and gcoef = (cA, cB, cC):
+//   m = 0:  grad S_l0 = (-cA S'_1, -cA S'_-1, cC S'_0)
+//   m > 0:  grad S_lm  = (-cA S'_{m+1} + cB S'_{m-1}, -cA S'_{-(m+1)} - cB S'_{-(m-1)}, cC S'_m)
+//           grad S_l-m = (-cA S'_{-(m+1)} + cB S'_{-(m-1)}, cA S'_{m+1} + cB S'_{m-1}, cC S'_-m)
+// (S'_k = 0 for |k| > l-1, S'_-0 = 0).  A zero-length edge gets a zero gradient.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void stage_jac(const Params &P, const Tables &T, double *__restrict__ YY,
+                                          double2 *__restrict__ BB, double *__restrict__ X,
+                                          const double *__restrict__ geo, int nb, int lane) {
+    const int n = P.n, lw = P.lmax + 1, L = P.L, nl = n * lw, ldN = P.lmax + 2;
+    const float inv_lw = 1.0f / (float)lw, inv_nl = 1.0f / (float)nl;
+    const int n_sh = nb * lw;
+    const bool poly = P.rbf != 0;
+    const int Q = P.Q, tw = lw + 1;
+    const float inv_Q = 1.0f / (float)Q;
+    // phase 1: harmonic columns (edge, m), then the radial scratch, two
+    // independent items per lane trip
+    for (int it = lane; it < n_sh; it += 64) {
+        const int e = qdiv(it, inv_lw), m = it - e * lw;
+        const double *g = geo + 4 * e;
+        sh_col_y(m, lw, g[0], g[1], g[2], T.Nt, ldN, YY + e * 4 * L);
+    }
+    if (!poly) {
+        const int nx = nb * nl;
+        for (int it = lane; it < nx; it += 128) {
+            const int i2 = it + 64 < nx ? it + 64 : it;
+            const int e1 = qdiv(it, inv_nl), e2 = qdiv(i2, inv_nl);
+            const double r1 = geo[4 * e1 + 3], r2 = geo[4 * e2 + 3];
+            const double v1 = exp(-T.aprime[it - e1 * nl] * r1 * r1), v2 = exp(-T.aprime[i2 - e2 * nl] * r2 * r2);
+            X[it] = v1;
+            X[i2] = v2;
+        }
+    } else {
+        for (int it = lane; it < nb * Q; it += 64) {
+            const int e = qdiv(it, inv_Q), q = it - e * Q;
+            const double r = geo[4 * e + 3], rq = T.rq[q];
+            const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
+            bessel_scaled_lds(lw, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
+        }
+    }
+    wave_sync();
+    // phase 2: gradients (edge, (l, m >= 0)), then the radial factors (edge, n, l)
+    const int Tn = grad_pairs(P.lmax), n_g = nb * Tn;
+    const float inv_T = 1.0f / (float)Tn;
+    for (int it = lane; it < n_g; it += 64) {
+        const int e = qdiv(it, inv_T), t = it - e * Tn;
+        const double2 c01 = T.gcoef[2 * t], c2p = T.gcoef[2 * t + 1];
+        const int lm = (int)c2p.y, l = lm & 0xff, m = lm >> 8;
+        double *Y = YY + e * 4 * L;
+        const int lp = l > 0 ? l - 1 : 0, c0 = lp * lp + lp;
+        const bool live = geo[4 * e + 3] != 0.0 && l > 0;
+        // S'_k for k in {m+1, -(m+1), m-1, -(m-1), m, -m}, clamped into degree l-1
+        auto sp = [&](int k) -> double {
+            const int kc = k < -lp ? -lp : (k > lp ? lp : k);
+            const double v = Y[c0 + kc];
+            return (live && k >= -lp && k <= lp) ? v : 0.0;
+        };
+        const double cA = c01.x, cB = c01.y, cC = c2p.x;
+        const int o = l * l + l;
+        if (m == 0) {
+            Y[L + o] = -cA * sp(1);
+            Y[2 * L + o] = -cA * sp(-1);
+            Y[3 * L + o] = cC * sp(0);
+        } else {
+            const double pp = sp(m + 1), pn = sp(-(m + 1)), qp = sp(m - 1), qn = m > 1 ? sp(-(m - 1)) : 0.0;
+            const double zp = sp(m), zn = sp(-m);
+            Y[L + o + m] = -cA * pp + cB * qp;
+            Y[2 * L + o + m] = -cA * pn - cB * qn;
+            Y[3 * L + o + m] = cC * zp;
+            Y[L + o - m] = -cA * pn + cB * qn;
+            Y[2 * L + o - m] = cA * pp + cB * qp;
+            Y[3 * L + o - m] = cC * zn;
+        }
+    }
+    const int nd = nb * nl;
+    if (!poly) {
+        for (int it = lane; it < nd; it += 128) {
+            const int i2 = it + 64 < nd ? it + 64 : it;
+            const int e1 = qdiv(it, inv_nl), t1 = it - e1 * nl, l1 = t1 - qdiv(t1, inv_lw) * lw;
+            const int e2 = qdiv(i2, inv_nl), t2 = i2 - e2 * nl, l2 = t2 - qdiv(t2, inv_lw) * lw;
+            const double2 *bc1 = T.bcp + t1, *bc2 = T.bcp + t2; // [k][n][l]: t = a lw + l
+            const double *E1 = X + (size_t)e1 * nl + l1, *E2 = X + (size_t)e2 * nl + l2;
+            double b1 = 0.0, h1 = 0.0, b2 = 0.0, h2 = 0.0;
+#pragma unroll 2
+            for (int k = 0; k < n; ++k) {
+                const double2 c1 = bc1[k * nl], c2 = bc2[k * nl];
+                const double v1 = E1[k * lw], v2 = E2[k * lw];
+                b1 += c1.x * v1;
+                h1 += c1.y * v1;
+                b2 += c2.x * v2;
+                h2 += c2.y * v2;
+            }
+            const double K1 = T.Kl[l1], K2 = T.Kl[l2];
+            BB[it] = make_double2(K1 * b1, K1 * h1);
+            BB[i2] = make_double2(K2 * b2, K2 * h2);
+        }
+    } else {
+        for (int it = lane; it < nd; it += 64) {
+            const int e = qdiv(it, inv_nl), t = it - e * nl, a = qdiv(t, inv_lw), l = t - a * lw;
+            const double r = geo[4 * e + 3];
+            const double *G = T.G + (size_t)a * Q;
+            const double *tq = X + (size_t)e * Q * tw;
+            double b = 0.0, bh = 0.0;
+            for (int q = 0; q < Q; ++q) {
+                const double tl = tq[q * tw + l];
+                b += G[q] * tl;
+                bh += G[q] * (T.rq[q] * tq[q * tw + l + 1] - r * tl);
+            }
+            if (r == 0.0) {
+                b = (l == 0) ? b : 0.0;
+                bh = 0.0;
+            } else {
+                double ir = 1.0 / r, rl = 1.0;
+                for (int k = 0; k < l; ++k) rl *= ir;
+                b *= rl;
+                bh *= rl * ir * P.inv_s2;
+            }
+            const double K = T.Kl[l];
+            BB[it] = make_double2(K * b, K * bh);
+        }
+    }
+    wave_sync();
 }
 
 // ---------------------------------------------------------------------------
 // k_jacobian
 //
 // One workgroup of NWJ waves per center.  The workgroup shares the basis
-// tables, the center's coefficients and the prefetched neighbour rows; each
-// wave then runs its own pipeline over its own edges (W at a time):
-// harmonics + radial factors -> U/V precontraction -> stores, synchronising
-// only within the wave, so one wave's latency-bound staging overlaps the
-// other waves' store streams.
+// tables, the center's coefficients (transposed, cT[lm][u], u = species * n
+// + n') and the prefetched neighbour rows; each wave then runs its own
+// pipeline over tiles of W <= 4 edges, synchronising only within the wave:
 //
-// Neighbour-block slots of species s are the features whose pair contains s,
-// in feature order: pairs (mu, s), mu < s (all n, n'); then (s, s) (n' >= n);
-// then (s, nu), nu > s.  A slot is stored packed:
-//   ob1 = n1 * lw + l  (bits 0-7),  ou1 = u1 * lw + l (bits 8-19),
-//   diag (bit 20): on the diagonal pair the mirrored term has
-//   ob2 = ou1 - s n lw and ou2 = ob1 + s n lw,
-// and evaluates K_l [Bh_{n1,l} r U_{u1,l} + B_{n1,l} V_{u1,l}] (+ mirror),
-// u = species * n + n'.
+//   1. harmonics S_lm and grad S_lm, radial factors K_l B_nl and K_l Bh_nl;
+//   2. the precontraction U^u_l = sum_m S_lm c^u_lm, V^u_l = sum_m grad S_lm
+//      c^u_lm on the matrix cores: per l, a 16 x 16 x 4 float64 MFMA chain
+//      with A rows (component, edge) = (S, dS/dx, dS/dy, dS/dz) of up to four
+//      edges, K = m (2l + 1 padded to a multiple of 4), B columns = u;
+//   3. assembly of the neighbour block of each edge j (species s), whose
+//      slots are the features with s in their species pair, in feature
+//      order: pairs (mu, s), mu < s; the diagonal pair (s, s), n' >= n;
+//      pairs (s, nu), nu > s.  With r = r_j - r_i,
+//        (mu, s):  K_l [U^mu_nl Bh_n'l r + V^mu_nl B_n'l]
+//        (s, nu):  K_l [Bh_nl r U^nu_n'l + B_nl V^nu_n'l]
+//        (s, s):   both of the above with mu = nu = s
+//      (Eq. powerspectrum-derivative).  On the off-diagonal pairs a lane owns
+//      one (n', l) and walks n, so consecutive lanes store consecutive
+//      floats; the diagonal triangle is walked flat with a decode table.
 // ---------------------------------------------------------------------------
 constexpr int NWJ = 4, BSJ = 64 * NWJ;
+constexpr int JAC_MAX_W = 4;  // edges per MFMA tile: A rows are (component, edge)
+constexpr int JAC_MAX_NP = 4; // lanes passes over (n', l): n * (l_max + 1) <= 256
+constexpr int JB = 8;         // MFMA operand pairs loaded ahead of their chain
 
-__device__ __forceinline__ uint32_t decode_slot(int fe, int s, int n, int lw) {
-    const int q = fe / lw, l = fe - q * lw, nn = n * n, tri = n * (n + 1) / 2;
-    int n1, u1, two = 0;
-    if (q < s * nn) { // pair (mu, s): derivative of the second factor c^s_{n'}
-        const int mu = q / nn, r = q - mu * nn, a = r / n, b = r - a * n;
-        n1 = b;
-        u1 = mu * n + a;
-    } else if (q < s * nn + tri) { // pair (s, s), n' >= n: both factors
-        int r = q - s * nn, a = 0;
-        while (r >= n - a) {
-            r -= n - a;
-            ++a;
-        }
-        n1 = a;
-        u1 = s * n + a + r;
-        two = 1;
-    } else { // pair (s, nu): derivative of the first factor c^s_n
-        const int r0 = q - s * nn - tri, nu = s + 1 + r0 / nn, r = r0 - (nu - s - 1) * nn, a = r / n, b = r - a * n;
-        n1 = a;
-        u1 = nu * n + b;
-    }
-    return (uint32_t)(n1 * lw + l) | (uint32_t)(u1 * lw + l) << 8 | (uint32_t)two << 20;
+typedef double dbl4 __attribute__((ext_vector_type(4)));
+
+__host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l of ceil((2l'+1)/4)
+    const int a = l >> 1;
+    return (l & 1) ? (a + 1) * (a + 1) : a * (a + 1);
+}
+
+__host__ __device__ __forceinline__ size_t jac_xu_doubles(const Params &P) {
+    const size_t lw = (size_t)P.lmax + 1, Sn = (size_t)P.S * P.n;
+    const size_t xd = stage_x_doubles(P, (int)lw, (int)lw);
+    return xd > 4 * Sn * lw ? xd : 4 * Sn * lw;
 }
 
 __host__ __device__ __forceinline__ size_t jac_wave_doubles(const Params &P, int W) {
-    const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1, Sn = (size_t)P.S * P.n;
-    const size_t xd = stage_x_doubles(P, (int)lw, (int)lw);
-    const size_t xu = xd > 4 * Sn * lw ? xd : 4 * Sn * lw;
-    return even(W * L) + even(3 * W * L) + even(2 * W * P.n * lw) + even(W * xu);
+    const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1;
+    return even(W * 4 * L) + even(2 * W * P.n * lw) + even(W * jac_xu_doubles(P));
+}
+
+// o: wave-uniform row base; idx: per-lane offset (unsigned, so the stores
+// can take the scalar-base + 32-bit-offset form)
+template <typename T> __device__ __forceinline__ void store3(T *o, uint32_t Fe, uint32_t idx, double x, double y, double z) {
+    store_out(o + idx, x);
+    store_out(o + (Fe + idx), y);
+    store_out(o + (2 * Fe + idx), z);
 }
 
 template <typename PosT, typename OutT>
 __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos, int W,
-                                                  int tab_lds, const double *__restrict__ c_scratch,
-                                                  OutT *__restrict__ jedge) {
+                                                  const double *__restrict__ c_scratch, OutT *__restrict__ jedge) {
     extern __shared__ double smem[];
-    const int64_t ci = blockIdx.x;
     const int S = P.S, n = P.n, lw = P.lmax + 1, L = P.L, Sn = S * n, tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
-    const int Fe = P.Fe, half = Sn * lw, snl = n * lw;
-    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
-    if (e1 == e0) return;
+    const int Fe = P.Fe, nl = n * lw, nnl = n * nl, tri_lw = P.tri_lw;
     const int RBk = row_block(NWJ * W);
 
     Carver cv{smem};
     Tables T;
     load_tables(P, cv, T, 0, lw);
-    double *cc = cv.take((size_t)Sn * L); // [S][n][L]
+    double *cT = cv.take((size_t)Sn * L); // [L][Sn]
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
-    uint32_t *tab = (uint32_t *)cv.take(tab_lds ? ((size_t)S * Fe + 1) / 2 : 0);
+    uint32_t *dtab = (uint32_t *)cv.take(((size_t)tri_lw + 1) / 2);
     // this wave's private staging
-    double *wbase = cv.take(0) + (size_t)wave * jac_wave_doubles(P, W);
-    Carver wv{wbase};
-    Stage st;
-    st.Y = wv.take((size_t)W * L);
-    st.dY = wv.take(3 * (size_t)W * L);
-    st.BB = (double2 *)wv.take(2 * (size_t)W * n * lw);
-    const size_t xd = stage_x_doubles(P, lw, lw);
-    const size_t xu = xd > (size_t)4 * half ? xd : (size_t)4 * half;
-    double *XU = wv.take((size_t)W * xu);
-    st.X = XU;                 // quadrature / exponential scratch, dead after the radial factors
-    double2 *U2 = (double2 *)XU; // U2[e][0][u][l] = (U, Vx), U2[e][1][u][l] = (Vy, Vz)
+    Carver wv{cv.take(0) + (size_t)wave * jac_wave_doubles(P, W)};
+    double *YY = wv.take((size_t)W * 4 * L); // [e][S, dS/dx, dS/dy, dS/dz][L]
+    double2 *BB = (double2 *)wv.take(2 * (size_t)W * nl); // [e][n][l] = K_l (B, Bh)
+    double *XU = wv.take((size_t)W * jac_xu_doubles(P));
+    // precontraction results, aliasing the radial scratch: U2a[e][u][l] =
+    // (U, Vx), U2b[e][u][l] = (Vy, Vz)
+    double2 *U2a = (double2 *)XU, *U2b = U2a + (size_t)W * Sn * lw;
 
+    for (int k = tid; k < tri_lw; k += BSJ) dtab[k] = P.dtab[k];
+
+    // lane roles.  MFMA operands: A row (lane & 15) = (component, edge) =
+    // (row >> 2, row & 3), B column (lane & 15) = u within the tile, K index
+    // lane >> 4; result register r of lane holds row (lane >> 4) + 4 r, i.e.
+    // component r of edge lane >> 4.
+    const int a_comp = (lane & 15) >> 2, a_e = lane & 3, kk = lane >> 4, bj = lane & 15, o_e = lane >> 4;
+    const int ntile = (Sn + 15) >> 4, nj = chunks_below(lw);
+    // assembly: lane pass p owns tt = lane + 64 p = n' lw + l
+    const float inv_lw = 1.0f / (float)lw;
+    const int NP = (nl + 63) >> 6;
+    int tp[JAC_MAX_NP], lp[JAC_MAX_NP];
+#pragma unroll
+    for (int p = 0; p < JAC_MAX_NP; ++p) {
+        tp[p] = lane + 64 * p;
+        lp[p] = tp[p] - qdiv(tp[p], inv_lw) * lw;
+    }
+
+    // One center per workgroup.  (A persistent loop over centers is slower:
+    // vmcnt counts loads and stores together, so the next center's row and
+    // coefficient loads would wait for all of the previous center's output
+    // stores to drain.)
+    {
+    const int64_t ci = blockIdx.x;
+    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
+    if (e1 == e0) return;
     const double *cg = c_scratch + ci * (size_t)Sn * L;
-    for (int k = tid; k < Sn * L; k += BSJ) cc[k] = cg[k];
-    if (tab_lds)
-        for (int k = tid; k < S * Fe; k += BSJ) tab[k] = P.fe[k];
+    for (int k = tid; k < Sn * L; k += BSJ) cT[k] = cg[k];
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
 
     for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
         const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
-        __syncthreads();
+        lds_barrier();
         load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
-        __syncthreads();
+        lds_barrier();
         for (int off = wave * W; off < rbn; off += NWJ * W) {
             const int nb = (rbn - off) < W ? (rbn - off) : W;
             const int64_t base = rb0 + off;
-            st.geo = rgeo + 4 * off;
-            st.sp = rsp + off;
-            stage_angular_radial<true, true>(P, T, st, nb, 0, lw, true, lane, 64);
-            wave_sync();
-            // U/V precontraction: items (l, edge, u = (nu, n'))
-            for (int it = lane; it < nb * half; it += 64) {
-                const int l = it / (nb * Sn), r2 = it - l * (nb * Sn), e = r2 / Sn, u = r2 - e * Sn;
-                const double *c = cc + (size_t)u * L + l * l;
-                const double *y = st.Y + e * L + l * l;
-                const double *dy = st.dY + e * 3 * L + l * l;
-                double U = 0.0, Vx = 0.0, Vy = 0.0, Vz = 0.0;
-                for (int m = 0; m < 2 * l + 1; ++m) {
-                    const double cv2 = c[m];
-                    U += y[m] * cv2;
-                    Vx += dy[m] * cv2;
-                    Vy += dy[L + m] * cv2;
-                    Vz += dy[2 * L + m] * cv2;
+            const double *geo = rgeo + 4 * off;
+            const int *spc = rsp + off;
+            stage_jac(P, T, YY, BB, XU, geo, nb, lane);
+
+            // ---- precontraction on the matrix cores ----
+            // chunks j = (l, ch) in l-major order, operands loaded JB at a time
+            {
+                const bool aok = a_e < nb;
+                const double *Arow = YY + ((aok ? a_e : 0) * 4 + a_comp) * L;
+                for (int t = 0; t < ntile; ++t) {
+                    const int u = 16 * t + bj;
+                    const bool uok = u < Sn;
+                    const int uc = uok ? u : Sn - 1;
+                    dbl4 acc = {0.0, 0.0, 0.0, 0.0};
+                    int l = 0, ch = 0;
+                    for (int j0 = 0; j0 < nj; j0 += JB) {
+                        double av[JB], bv[JB];
+                        int lq = l, cq = ch;
+#pragma unroll
+                        for (int q = 0; q < JB; ++q) {
+                            const int m = 4 * cq + kk;
+                            const bool ok = j0 + q < nj && m <= 2 * lq;
+                            const int row = lq * lq + (ok ? m : 0);
+                            const double a = Arow[row], b = cT[row * Sn + uc];
+                            av[q] = (ok && aok) ? a : 0.0;
+                            bv[q] = (ok && uok) ? b : 0.0;
+                            if (++cq == (lq >> 1) + 1) {
+                                cq = 0;
+                                lq = lq + 1 < lw ? lq + 1 : lq;
+                            }
+                        }
+#pragma unroll
+                        for (int q = 0; q < JB; ++q) {
+                            if (j0 + q < nj) {
+                                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[q], bv[q], acc, 0, 0, 0);
+                                if (++ch == (l >> 1) + 1) {
+                                    if (o_e < nb && uok) {
+                                        const size_t qq = (size_t)(o_e * Sn + u) * lw + l;
+                                        U2a[qq] = make_double2(acc[0], acc[1]);
+                                        U2b[qq] = make_double2(acc[2], acc[3]);
+                                    }
+                                    acc = dbl4{0.0, 0.0, 0.0, 0.0};
+                                    ch = 0;
+                                    ++l;
+                                }
+                            }
+                        }
+                    }
                 }
-                const int rem = u * lw + l;
-                U2[(size_t)(2 * e) * half + rem] = make_double2(U, Vx);
-                U2[(size_t)(2 * e + 1) * half + rem] = make_double2(Vy, Vz);
             }
             wave_sync();
-            // stores: lanes own consecutive slots of each edge
+
+            // ---- assembly and stores ----
             for (int e = 0; e < nb; ++e) {
-                const int s = st.sp[e], sh = s * n * lw;
-                const double gx = st.geo[4 * e], gy = st.geo[4 * e + 1], gz = st.geo[4 * e + 2];
-                const double2 *BB = st.BB + e * snl;
-                const double2 *UA = U2 + (size_t)(2 * e) * half, *UB = U2 + (size_t)(2 * e + 1) * half;
-                OutT *o = jedge + ((base + e) * 3) * Fe;
-                for (int fe = lane; fe < Fe; fe += 64) {
-                    const uint32_t t = tab_lds ? tab[s * Fe + fe] : decode_slot(fe, s, n, lw);
-                    const int ob1 = t & 0xff, ou1 = (t >> 8) & 0xfff;
-                    const double2 bb1 = BB[ob1], w1 = UA[ou1], z1 = UB[ou1];
-                    double hu = bb1.y * w1.x;
-                    double jx = bb1.x * w1.y, jy = bb1.x * z1.x, jz = bb1.x * z1.y;
-                    if (t >> 20) {
-                        const int ob2 = ou1 - sh, ou2 = ob1 + sh;
-                        const double2 bb2 = BB[ob2], w2 = UA[ou2], z2 = UB[ou2];
-                        hu += bb2.y * w2.x;
-                        jx += bb2.x * w2.y;
-                        jy += bb2.x * z2.x;
-                        jz += bb2.x * z2.y;
+                const int s = __builtin_amdgcn_readfirstlane(spc[e]);
+                const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
+                const double2 *Be = BB + (size_t)e * nl;
+                const double2 *Ua = U2a + (size_t)e * Sn * lw, *Ub = U2b + (size_t)e * Sn * lw;
+                OutT *o = jedge + (base + e) * 3 * Fe;
+                // pairs (mu, s), mu < s
+                if (s > 0) {
+#pragma unroll
+                    for (int p = 0; p < JAC_MAX_NP; ++p) {
+                        if (p >= NP || tp[p] >= nl) continue;
+                        const int tt = tp[p], l = lp[p];
+                        const double2 bb = Be[tt];
+                        const double bhx = bb.y * rx, bhy = bb.y * ry, bhz = bb.y * rz;
+                        for (int mu = 0; mu < s; ++mu) {
+                            const double2 *Uma = Ua + mu * nl + l, *Umb = Ub + mu * nl + l;
+                            OutT *ob = o + mu * nnl;
+                            for (int a = 0; a < n; ++a) {
+                                const double2 q0 = Uma[a * lw], q1 = Umb[a * lw];
+                                store3(ob + a * nl, Fe, tt, q0.x * bhx + q0.y * bb.x, q0.x * bhy + q1.x * bb.x,
+                                       q0.x * bhz + q1.y * bb.x);
+                            }
+                        }
                     }
-                    store_nt(o + fe, hu * gx + jx);
-                    store_nt(o + Fe + fe, hu * gy + jy);
-                    store_nt(o + 2 * Fe + fe, hu * gz + jz);
+                }
+                // diagonal pair (s, s), n' >= n, flat over (n, n', l)
+                {
+                    OutT *ob = o + s * nnl;
+                    const double2 *Usa = Ua + s * nl, *Usb = Ub + s * nl;
+                    for (int f = lane; f < tri_lw; f += 64) {
+                        const uint32_t d = dtab[f];
+                        const int ta = d & 0xffff, tb = d >> 16; // n lw + l, n' lw + l
+                        const double2 A = Be[ta], B = Be[tb];
+                        const double2 a0 = Usa[ta], a1 = Usb[ta], b0 = Usa[tb], b1 = Usb[tb];
+                        const double hu = B.y * a0.x + A.y * b0.x;
+                        store3(ob, Fe, f, hu * rx + (B.x * a0.y + A.x * b0.y), hu * ry + (B.x * a1.x + A.x * b1.x),
+                               hu * rz + (B.x * a1.y + A.x * b1.y));
+                    }
+                }
+                // pairs (s, nu), nu > s
+                if (s + 1 < S) {
+#pragma unroll
+                    for (int p = 0; p < JAC_MAX_NP; ++p) {
+                        if (p >= NP || tp[p] >= nl) continue;
+                        const int tt = tp[p], l = lp[p];
+                        for (int nu = s + 1; nu < S; ++nu) {
+                            const double2 q0 = Ua[nu * nl + tt], q1 = Ub[nu * nl + tt];
+                            const double ux = q0.x * rx, uy = q0.x * ry, uz = q0.x * rz;
+                            OutT *ob = o + s * nnl + tri_lw + (nu - s - 1) * nnl;
+                            const double2 *Bl = Be + l;
+                            for (int a = 0; a < n; ++a) {
+                                const double2 bb = Bl[a * lw];
+                                store3(ob + a * nl, Fe, tt, bb.y * ux + bb.x * q0.y, bb.y * uy + bb.x * q1.x,
+                                       bb.y * uz + bb.x * q1.y);
+                            }
+                        }
+                    }
                 }
             }
             wave_sync();
         }
     }
+    } // center
 }
 
 // dense[ci][j][3][F]: zero-filled by the caller; each stored block is copied
@@ -757,13 +1045,15 @@ int density_blocks_per_cu(bool f64, bool jac, size_t lds) {
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
-size_t jacobian_lds_bytes(const Params &P, int W, int tab_lds) {
+size_t jacobian_lds_bytes(const Params &P, int W) {
     const size_t L = (size_t)P.L, Sn = (size_t)P.S * P.n;
     const int RBk = row_block(NWJ * W);
     size_t d = table_doubles(P, P.lmax + 1) + even(Sn * L) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               even(tab_lds ? ((size_t)P.S * P.Fe + 1) / 2 : 0) + NWJ * jac_wave_doubles(P, W);
+               even(((size_t)P.tri_lw + 1) / 2) + NWJ * jac_wave_doubles(P, W);
     return d * 8;
 }
+
+int jacobian_max_w() { return JAC_MAX_W; }
 
 hipError_t set_lds_limits() {
     const int lim = 159 * 1024; // the kernels' static LDS uses part of the 160 KB
@@ -813,10 +1103,10 @@ hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool
     dim3 grid((unsigned)R.nc), block(BSJ);
     if (f64)
         hipLaunchKernelGGL((k_jacobian<double, double>), grid, block, cfg.lds, st, P, R, (const double *)pos, cfg.W,
-                           cfg.tab_lds, c_scratch, (double *)jedge);
+                           c_scratch, (double *)jedge);
     else
         hipLaunchKernelGGL((k_jacobian<float, float>), grid, block, cfg.lds, st, P, R, (const float *)pos, cfg.W,
-                           cfg.tab_lds, c_scratch, (float *)jedge);
+                           c_scratch, (float *)jedge);
     return hipGetLastError();
 }
 
