@@ -206,7 +206,7 @@ int upload_constants(soap_ctx *c) {
     const int n = c->n, lw = c->lmax + 1, S = (int)c->Z.size();
     char msg[256] = {0};
     const int ldN = lw + 1; // harmonics tables cover l <= l_max + 1
-    std::vector<double> betaC, betaCa, aprime, G, rq, c0(n), Nlm((size_t)ldN * ldN), rcoef((size_t)2 * ldN * ldN, 0.0);
+    std::vector<double> betaC, betaCa, aprime, G, rq, c0(n), Nlm((size_t)ldN * ldN);
     if (c->rbf == SOAP_RBF_GTO) {
         betaC.resize((size_t)lw * n * n);
         betaCa.resize((size_t)lw * n * n);
@@ -221,11 +221,6 @@ int upload_constants(soap_ctx *c) {
             return fail(c, SOAP_EINVAL, "%s", msg);
     }
     soap_basis_sh_norms(c->lmax + 1, Nlm.data());
-    for (int l = 0; l < ldN; ++l)
-        for (int m = 0; m + 2 <= l; ++m) {
-            rcoef[2 * (l * ldN + m)] = (double)(2 * l - 1) / (double)(l - m);
-            rcoef[2 * (l * ldN + m) + 1] = (double)(l + m - 1) / (double)(l - m);
-        }
     // gradient identities of the harmonics per (l, m >= 0): with the degree
     // l-1 harmonics S', grad S_l,+-m takes S'_{m+1} with cA, S'_{m-1} with
     // cB and S'_m with cC (the combinations are written out in the kernels)
@@ -254,7 +249,7 @@ int upload_constants(soap_ctx *c) {
             for (int k = 2; k <= l - m; ++k) v /= (long double)k;
             Nt[(size_t)l * ldN + m] = (double)v;
         }
-    // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nlm | Nt | rcoef | gcoef
+    // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nt | gcoef
     std::vector<double> all;
     size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
     size_t o_ba = all.size(); all.insert(all.end(), betaCa.begin(), betaCa.end());
@@ -262,10 +257,7 @@ int upload_constants(soap_ctx *c) {
     size_t o_G = all.size(); all.insert(all.end(), G.begin(), G.end());
     size_t o_rq = all.size(); all.insert(all.end(), rq.begin(), rq.end());
     size_t o_c0 = all.size(); all.insert(all.end(), c0.begin(), c0.end());
-    size_t o_N = all.size(); all.insert(all.end(), Nlm.begin(), Nlm.end());
     size_t o_Nt = all.size(); all.insert(all.end(), Nt.begin(), Nt.end());
-    if (all.size() & 1) all.push_back(0.0); // 16-byte alignment of the double2 table
-    size_t o_rc = all.size(); all.insert(all.end(), rcoef.begin(), rcoef.end());
     size_t o_gc = all.size(); all.insert(all.end(), gcoef.begin(), gcoef.end());
     hipError_t e;
     if ((e = c->d_const.ensure(all.size() * 8)) != hipSuccess) return hip_fail(c, e, "hipMalloc(constants)");
@@ -306,9 +298,7 @@ int upload_constants(soap_ctx *c) {
     P.G = d + o_G;
     P.rq = d + o_rq;
     P.c0 = d + o_c0;
-    P.Nlm = d + o_N;
     P.Nt = d + o_Nt;
-    P.rcoef = reinterpret_cast<const double2 *>(d + o_rc);
     P.gcoef = d + o_gc;
     P.fq = c->d_fq.as<uint32_t>();
     P.dtab = c->d_dtab.as<uint32_t>();

@@ -23,9 +23,7 @@ struct Params {
     const double *G;           // polynomial [n][Q], includes 4 pi
     const double *rq;          // polynomial [Q]
     const double *c0;          // on-site term [n]
-    const double *Nlm;         // [lmax+2][lmax+2] real solid-harmonic normalisation
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
-    const double2 *rcoef;      // [lmax+2][lmax+2] recurrence coefficients of the harmonics
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)
     const uint32_t *fq;        // [nq_full] mu | nu<<8 | n<<16 | n'<<24
     const uint32_t *dtab;      // [tri_lw] diagonal-pair slots: (n lw + l) | (n' lw + l) << 16, n' >= n

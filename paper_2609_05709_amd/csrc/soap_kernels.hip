@@ -2,8 +2,9 @@
 //
 // Both kernels evaluate, per directed edge e = (i -> j) with r = r_j - r_i
 // formed in float64 (exact for float32 inputs):
-//   * real solid harmonics S_lm(r) = r^l Y_lm(r_hat) and their Cartesian
-//     gradients, by the recurrences below (one thread per (edge, |m|));
+//   * real solid harmonics S_lm(r) = r^l Y_lm(r_hat) by a division-free
+//     column recurrence, and their Cartesian gradients from the degree l-1
+//     harmonics (stage_edges);
 //   * radial factors B_nl(r) and Bh_nl(r) = (1/r) dB_nl/dr such that the
 //     edge's contribution to the coefficients is c_nlm += B_nl S_lm and its
 //     gradient is dc_nlm/dr_j = Bh_nl r S_lm + B_nl grad S_lm:
@@ -15,18 +16,16 @@
 //         Bh_nl = r^-(l+1) / s^2 sum_q G_nq e^{-(r_q-r)^2/2s^2} (r_q ii_{l+1} - r ii_l)
 //       with ii_l(x) = e^-x i_l(x) and d/dx (x^-l i_l) = x^-l i_{l+1}.
 //
-// k_density: one workgroup per (center, l-group).  Accumulates c (and, for
-//   the Jacobian, D = sum over edges of dc, i.e. minus the derivative of c
-//   with respect to the center) in LDS, then writes the power spectrum
-//   Eq. (powerspectrum) and the center's own Jacobian block
-//   -K_l sum_m (D^mu c^nu + c^mu D^nu) (Eq. powerspectrum-derivative with
-//   translational invariance).  c goes to a float64 scratch for k_jacobian.
-// k_jacobian: one workgroup per center, edges in chunks.  Per edge it forms
-//   U^nu_{n'l} = sum_m S_lm c^nu_{n'lm} and V = sum_m grad S_lm c^nu_{n'lm}
-//   (the per-edge precontraction the paper describes in Sec. 3.2), then each
-//   output is K_l (Bh_nl r_x U + B_nl V_x) [+ the mirrored term on a
-//   diagonal species pair]: no (2l+1)-long sums in the store loop.
-//   Output rows are the F_e features whose pair contains species(j).
+// k_density: persistent workgroups, each bound to one l-group and taking
+//   centers from a counter.  Accumulates c (and, for the Jacobian, D = sum
+//   over edges of dc, i.e. minus the derivative of c with respect to the
+//   center), then writes the power spectrum Eq. (powerspectrum) and the
+//   center's own Jacobian block -K_l sum_m (D^mu c^nu + c^mu D^nu)
+//   (Eq. powerspectrum-derivative with translational invariance).  c goes to
+//   a float64 scratch for k_jacobian.
+// k_jacobian: one workgroup per center; per edge the precontraction
+//   U = sum_m S_lm c, V = sum_m grad S_lm c on the matrix cores, then the
+//   neighbour block from U, V, B, Bh (see the kernel).
 // All arithmetic is float64; outputs are converted once at the store.
 #include "soap_internal.h"
 
@@ -35,111 +34,27 @@
 namespace soap {
 namespace {
 
-constexpr int BS = 256; // workgroup size of both kernels
-
-__device__ __forceinline__ int isqrt_lm(int lm) { // l such that l*l <= lm < (l+1)^2
-    int l = (int)sqrtf((float)lm);
-    while (l * l > lm) --l;
-    while ((l + 1) * (l + 1) <= lm) ++l;
-    return l;
-}
-
 // Output stores are plain (write-back) stores: on this chip non-temporal
 // stores of the neighbour blocks' partial-line runs write back at about half
 // the bandwidth.
 template <typename T> __device__ __forceinline__ void store_out(T *p, double v) { *p = (T)v; }
 
-// ---------------------------------------------------------------------------
-// Real solid harmonics for one |m| column.
-//   (C_m + i S_m) = (x + i y)^m
-//   Q_m^m = (2m-1)!!,  Q_{m+1}^m = (2m+1) z Q_m^m,
-//   Q_l^m = ((2l-1) z Q_{l-1}^m - (l+m-1) r^2 Q_{l-2}^m) / (l-m)
-//   S_l0 = N_l0 Q_l^0,  S_{l,m} = N_lm Q_l^m C_m,  S_{l,-m} = N_lm Q_l^m S_m
-//   dQ_l^m/dx = -x Q_{l-1}^{m+1}, dQ_l^m/dy = -y Q_{l-1}^{m+1},
-//   dQ_l^m/dz = (l+m) Q_{l-1}^m;  dC_m/dx = m C_{m-1}, dC_m/dy = -m S_{m-1},
-//   dS_m/dx = m S_{m-1}, dS_m/dy = m C_{m-1}.
-// Writes Y[lm - lm0] and dY[d*ldd + lm - lm0] for l in [l_lo, l_hi).
-// grad = false skips the gradient.  zero_grad forces the gradient to 0.
-// ---------------------------------------------------------------------------
-// rc[(l * ldN + m) * 2 + {0, 1}] = ((2l-1)/(l-m), (l+m-1)/(l-m)) for l >= m + 2
-template <bool GRAD>
-__device__ __forceinline__ void sh_column(int m, int l_lo, int l_hi, double x, double y, double z, const double *__restrict__ Nlm,
-                          const double2 *__restrict__ rcoef, int ldN, double *__restrict__ Y,
-                          double *__restrict__ dY, int ldd, int lm0, bool zero_grad) {
-    const double r2 = x * x + y * y + z * z;
-    double c = 1.0, s = 0.0, cm1 = 0.0, sm1 = 0.0;
-    for (int k = 1; k <= m; ++k) {
-        cm1 = c;
-        sm1 = s;
-        double cn = x * c - y * s;
-        s = x * s + y * c;
-        c = cn;
-    }
-    double dfm = 1.0; // (2m-1)!!
-    for (int k = 1; k <= m; ++k) dfm *= (double)(2 * k - 1);
-    // column m: q1 = Q_{l-1}^m, q2 = Q_{l-2}^m ; column m+1: p1 = Q_{l-2}^{m+1} ... tracked as "prev"
-    double q1 = 0.0, q2 = 0.0; // Q_{l-1}^m, Q_{l-2}^m
-    double p1 = 0.0, p2 = 0.0; // Q_{l-2}^{m+1}, Q_{l-3}^{m+1}
-    for (int l = m; l < l_hi; ++l) {
-        double q; // Q_l^m
-        if (l == m) q = dfm;
-        else if (l == m + 1) q = (double)(2 * m + 1) * z * dfm;
-        else {
-            const double2 k = rcoef[l * ldN + m];
-            q = k.x * z * q1 - k.y * r2 * q2;
-        }
-        double p; // Q_{l-1}^{m+1}
-        const int lp = l - 1;
-        if (lp < m + 1) p = 0.0;
-        else if (lp == m + 1) p = dfm * (double)(2 * m + 1);
-        else if (lp == m + 2) p = (double)(2 * m + 3) * z * dfm * (double)(2 * m + 1);
-        else {
-            const double2 k = rcoef[lp * ldN + m + 1];
-            p = k.x * z * p1 - k.y * r2 * p2;
-        }
-        if (l >= l_lo) {
-            const double N = Nlm[l * ldN + m];
-            const int base = l * l + l - lm0;
-            if (m == 0) {
-                Y[base] = N * q;
-                if (GRAD) {
-                    double gx = -N * x * p, gy = -N * y * p, gz = N * (double)l * q1;
-                    if (zero_grad) gx = gy = gz = 0.0;
-                    dY[base] = gx;
-                    dY[ldd + base] = gy;
-                    dY[2 * ldd + base] = gz;
-                }
-            } else {
-                Y[base + m] = N * q * c;
-                Y[base - m] = N * q * s;
-                if (GRAD) {
-                    const double qm = (double)m * q, dz = N * (double)(l + m) * q1;
-                    double gxc = N * (-x * p * c + qm * cm1), gyc = N * (-y * p * c - qm * sm1), gzc = dz * c;
-                    double gxs = N * (-x * p * s + qm * sm1), gys = N * (-y * p * s + qm * cm1), gzs = dz * s;
-                    if (zero_grad) gxc = gyc = gzc = gxs = gys = gzs = 0.0;
-                    dY[base + m] = gxc;
-                    dY[ldd + base + m] = gyc;
-                    dY[2 * ldd + base + m] = gzc;
-                    dY[base - m] = gxs;
-                    dY[ldd + base - m] = gys;
-                    dY[2 * ldd + base - m] = gzs;
-                }
-            }
-        }
-        q2 = q1;
-        q1 = q;
-        p2 = p1;
-        p1 = p;
-    }
-}
+// floor(x / d) for 0 <= x < 2^22 with inv = 1/d correctly rounded: the
+// relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
+// next integer
+__device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x + 0.5f) * inv); }
 
-// Real solid harmonics of one column m (l = m .. lw-1) without gradients and
-// without divisions: with R_m = 1, R_{m+1} = (2m+1) z and
+// ---------------------------------------------------------------------------
+// Real solid harmonics of one column m without gradients and without
+// divisions.  With (C_m + i S_m) = (x + i y)^m, R_m = 1, R_{m+1} = (2m+1) z,
 //   R_l = (2l-1) z R_{l-1} - (l+m-1)(l-m-1) r^2 R_{l-2},
-// Q_l^m = (2m-1)!! R_l / (l-m)!, so S_l,m = Nt_lm R_l C_m, S_l,-m = Nt_lm R_l S_m
-// with Nt_lm = N_lm (2m-1)!! / (l-m)!.
-__device__ __forceinline__ void sh_col_y(int m, int lw, double x, double y, double z, const double *__restrict__ Nt,
-                                         int ldN, double *__restrict__ Y) {
+// the associated Legendre part is Q_l^m = (2m-1)!! R_l / (l-m)!, so
+//   S_l,m = Nt_lm R_l C_m, S_l,-m = Nt_lm R_l S_m, Nt_lm = N_lm (2m-1)!! / (l-m)!.
+// Stores l in [l_lo, l_hi) at Y[(l^2 + l +- m - lm_base) * ls].
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void sh_col_y(int m, int l_lo, int l_hi, double x, double y, double z,
+                                         const double *__restrict__ Nt, int ldN, double *__restrict__ Y, int ls,
+                                         int lm_base) {
     const double r2 = x * x + y * y + z * z;
     double c = 1.0, s = 0.0;
     for (int k = 0; k < m; ++k) {
@@ -148,20 +63,22 @@ __device__ __forceinline__ void sh_col_y(int m, int lw, double x, double y, doub
         c = cn;
     }
     double R1 = 0.0, R = 1.0; // R_{l-1}, R_l
-    for (int l = m; l < lw; ++l) {
+    for (int l = m; l < l_hi; ++l) {
         if (l > m) {
             const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
             const double Rn = a * z * R - b * r2 * R1;
             R1 = R;
             R = Rn;
         }
-        const double v = Nt[l * ldN + m] * R;
-        const int o = l * l + l;
-        if (m == 0) {
-            Y[o] = v;
-        } else {
-            Y[o + m] = v * c;
-            Y[o - m] = v * s;
+        if (l >= l_lo) {
+            const double v = Nt[l * ldN + m] * R;
+            const int o = l * l + l - lm_base;
+            if (m == 0) {
+                Y[o * ls] = v;
+            } else {
+                Y[(o + m) * ls] = v * c;
+                Y[(o - m) * ls] = v * s;
+            }
         }
     }
 }
@@ -248,17 +165,15 @@ struct Tables {
     const double2 *bcp;    // GTO: [k][n][lc] = (betaC, -2 betaC a') of B_nl = sum_k betaC_nk e^{-a'_kl r^2}
     const double *aprime;  // GTO: [k][lc]
     const double *G, *rq;  // polynomial: [n][Q], [Q]
-    const double *Nlm;     // [ldN][ldN]
     const double *Nt;      // [ldN][ldN] N_lm (2m-1)!! / (l-m)!, for sh_col_y
-    const double2 *rcoef;  // [ldN][ldN]
-    const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_jac
+    const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_edges
 };
 
 __host__ __device__ __forceinline__ int grad_pairs(int lmax) { return (lmax + 1) * (lmax + 2) / 2; }
 
 __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lgc) {
     const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
-    size_t d = 16 + 2 * even(ldN * ldN) + even(2 * ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
+    size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
     if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
     else d += even(n * P.Q) + even((size_t)P.Q);
     return d;
@@ -269,20 +184,14 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     // every pointer is assigned on every path, so the struct stays in
     // registers and the compiler keeps LDS (ds_*) addressing for it
     double *Kl = cv.take(16);
-    double *Nl = cv.take((size_t)ldN * ldN);
     double *Ntl = cv.take((size_t)ldN * ldN);
-    double *rc = cv.take(2 * (size_t)ldN * ldN);
     double *gc = cv.take(4 * (size_t)grad_pairs(P.lmax));
     const bool poly = P.rbf != 0;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     const size_t szA = poly ? (size_t)n * P.Q : 2 * (size_t)lgc * n * n; // (betaC, betaCa) pairs | G
     const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n;              // aprime | rq
     double *A = cv.take(szA), *B = cv.take(szB);
-    for (int k = tid; k < ldN * ldN; k += bs) {
-        Nl[k] = P.Nlm[k];
-        Ntl[k] = P.Nt[k];
-    }
-    for (int k = tid; k < 2 * ldN * ldN; k += bs) rc[k] = ((const double *)P.rcoef)[k];
+    for (int k = tid; k < ldN * ldN; k += bs) Ntl[k] = P.Nt[k];
     for (int k = tid; k < 4 * grad_pairs(P.lmax); k += bs) gc[k] = P.gcoef[k];
     if (!poly) {
         // global [l][n][k] -> LDS [k][n][lc]; global [l][k] -> LDS [k][lc]
@@ -302,29 +211,13 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
         for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
     }
     T.Kl = Kl;
-    T.Nlm = Nl;
     T.Nt = Ntl;
-    T.rcoef = (const double2 *)rc;
     T.gcoef = (const double2 *)gc;
     T.bcp = (const double2 *)A;
     T.G = A;
     T.aprime = B;
     T.rq = B;
 }
-
-// Per-chunk edge staging, shared by both kernels.  LDS arrays:
-//   geo[.][4] (x, y, z, r), sp[.] species   (views into the prefetched rows)
-//   Y[EC][Lg], dY[EC][3][Lg]  harmonics for lm in [lm0, lm0+Lg),
-//   BB[EC][n][lgc] = (B, Bh)  radial factors for l in [lg0, lg0+lgc),
-//   X  scratch: GTO exponentials [EC][lgc][n], or the polynomial quadrature
-//      table [EC][Q][lgc+1].
-// scaleK multiplies B and Bh by K_l = pi sqrt(8/(2l+1)).
-struct Stage {
-    double *geo, *Y, *dY, *X;
-    double2 *BB;
-    int *sp;
-    int ys, dys; // per-edge strides of Y and dY (dY components are Lg apart)
-};
 
 // X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
 // Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place)
@@ -350,79 +243,137 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// Staging work is spread over `bs` threads starting at `tid`: the whole
-// workgroup (WAVE = false, workgroup barriers) or one wave (WAVE = true).
-template <bool GRAD, bool WAVE = false>
-__device__ __forceinline__ void stage_angular_radial(const Params &P, const Tables &T, const Stage &st, int nb, int lg0,
-                                                     int lg1, bool scaleK, int tid = -1, int bs = 0) {
-    if (!WAVE) {
-        tid = threadIdx.x;
-        bs = blockDim.x;
+// ---------------------------------------------------------------------------
+// Per-tile edge staging (one wave, nb edges), shared by both kernels, for
+// l in [lg0, lg1).
+//   YY: harmonics, element (edge e, component c, lm) at
+//       e es + c cs + (lm - lmY0) ls; component 0 = S, 1..3 = dS/dx_d (GRAD).
+//       Degrees from lgY0 = lg0 - 1 (GRAD and lg0 > 0) or lg0 are stored.
+//   BB[e][n][lc] = K (B_nl, Bh_nl), K = K_l if scaleK else 1
+//   X: GTO exponentials [e][k][lc], or the polynomial table [e][q][0..lg1]
+// Phase 1 runs the harmonic columns (edge, m), then the radial scratch;
+// phase 2 the gradients, then the radial factors.  Each gradient component
+// is at most two degree l-1 harmonics: with H_l^m = (x + iy)^m Q_l^m (so
+// S_l,m = N_lm Re H, S_l,-m = N_lm Im H),
+//   d/dz H_l^m = (l+m) H_{l-1}^m,  (d/dx + i d/dy) H_l^m = -H_{l-1}^{m+1},
+//   (d/dx - i d/dy) H_l^m = (l+m)(l+m-1) H_{l-1}^{m-1}.
+// Per (l, m >= 0), with S' = S_{l-1,.} and gcoef = (cA, cB, cC):
+//   m = 0:  grad S_l0 = (-cA S'_1, -cA S'_-1, cC S'_0)
+//   m > 0:  grad S_lm  = (-cA S'_{m+1} + cB S'_{m-1}, -cA S'_{-(m+1)} - cB S'_{-(m-1)}, cC S'_m)
+//           grad S_l-m = (-cA S'_{-(m+1)} + cB S'_{-(m-1)}, cA S'_{m+1} + cB S'_{m-1}, cC S'_-m)
+// (S'_k = 0 for |k| > l-1, S'_-0 = 0).  A zero-length edge gets a zero gradient.
+// ---------------------------------------------------------------------------
+struct YLayout {
+    int es, cs, ls, lmY0;
+};
+
+template <bool GRAD>
+__device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, double *__restrict__ YY, YLayout yl,
+                                            double2 *__restrict__ BB, double *__restrict__ X,
+                                            const double *__restrict__ geo, int nb, int lane, int lg0, int lg1,
+                                            bool scaleK) {
+    const int n = P.n, ldN = P.lmax + 2, lgc = lg1 - lg0, nlc = n * lgc;
+    const int lgY0 = (GRAD && lg0 > 0) ? lg0 - 1 : lg0;
+    const float inv_lg1 = 1.0f / (float)lg1, inv_nlc = 1.0f / (float)nlc, inv_lgc = 1.0f / (float)lgc;
+    const bool poly = P.rbf != 0;
+    const int Q = P.Q, tw = lg1 + 1;
+    const float inv_Q = 1.0f / (float)Q;
+    // phase 1: harmonic columns (edge, m), then the radial scratch (two
+    // independent exponentials per lane trip)
+    for (int it = lane; it < nb * lg1; it += 64) {
+        const int e = qdiv(it, inv_lg1), m = it - e * lg1;
+        const double *g = geo + 4 * e;
+        sh_col_y(m, m > lgY0 ? m : lgY0, lg1, g[0], g[1], g[2], T.Nt, ldN, YY + e * yl.es, yl.ls, yl.lmY0);
     }
-    const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0, lgc = lg1 - lg0, n = P.n, ldN = P.lmax + 2;
-    const int n_sh = nb * lg1;
-    if (P.rbf == 0) {
-        // harmonics (edge, m) and exponentials X[e][k][lc] in one pass
-        const int n_ex = nb * lgc * n;
-        for (int it = tid; it < n_sh + n_ex; it += bs) {
-            if (it < n_sh) {
-                const int e = it / lg1, m = it - e * lg1;
-                const double *g = st.geo + 4 * e;
-                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * st.ys,
-                                GRAD ? st.dY + e * st.dys : nullptr, Lg, lm0, g[3] == 0.0);
-            } else {
-                const int x = it - n_sh, e = x / (lgc * n), rem = x - e * (lgc * n);
-                const double r = st.geo[4 * e + 3];
-                st.X[x] = exp(-T.aprime[rem] * r * r);
-            }
-        }
-        if (WAVE) wave_sync(); else lds_barrier();
-        // B_nl = sum_k betaC^l_nk E_k, Bh_nl = sum_k betaCa^l_nk E_k
-        for (int it = tid; it < nb * n * lgc; it += bs) {
-            const int e = it / (n * lgc), rem = it - e * (n * lgc), a = rem / lgc, lc = rem - a * lgc;
-            const double *E = st.X + (size_t)e * n * lgc + lc;
-            const double2 *bc = T.bcp + (size_t)a * lgc + lc;
-            double b = 0.0, bh = 0.0;
-            for (int k = 0; k < n; ++k) {
-                const double2 c = bc[(size_t)k * n * lgc];
-                const double v = E[k * lgc];
-                b += c.x * v;
-                if (GRAD) bh += c.y * v;
-            }
-            const double K = scaleK ? T.Kl[lg0 + lc] : 1.0;
-            st.BB[it] = make_double2(K * b, K * bh);
+    if (!poly) {
+        const int nx = nb * nlc;
+        for (int it = lane; it < nx; it += 128) {
+            const int i2 = it + 64 < nx ? it + 64 : it;
+            const int e1 = qdiv(it, inv_nlc), e2 = qdiv(i2, inv_nlc);
+            const double r1 = geo[4 * e1 + 3], r2 = geo[4 * e2 + 3];
+            const double v1 = exp(-T.aprime[it - e1 * nlc] * r1 * r1), v2 = exp(-T.aprime[i2 - e2 * nlc] * r2 * r2);
+            X[it] = v1;
+            X[i2] = v2;
         }
     } else {
-        // harmonics (edge, m) and quadrature table (edge, q):
-        //   X[e][q][l] = e^{-(r_q - r)^2/2s^2} ii_l(r_q r/s^2), l in [0, lg1]
-        const int Q = P.Q, tw = lg1 + 1;
-        for (int it = tid; it < n_sh + nb * Q; it += bs) {
-            if (it < n_sh) {
-                const int e = it / lg1, m = it - e * lg1;
-                const double *g = st.geo + 4 * e;
-                sh_column<GRAD>(m, lg0 > m ? lg0 : m, lg1, g[0], g[1], g[2], T.Nlm, T.rcoef, ldN, st.Y + e * st.ys,
-                                GRAD ? st.dY + e * st.dys : nullptr, Lg, lm0, g[3] == 0.0);
+        for (int it = lane; it < nb * Q; it += 64) {
+            const int e = qdiv(it, inv_Q), q = it - e * Q;
+            const double r = geo[4 * e + 3], rq = T.rq[q];
+            const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
+            bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
+        }
+    }
+    wave_sync();
+    // phase 2: gradients (edge, (l, m >= 0)), then the radial factors (edge, n, lc)
+    if (GRAD) {
+        const int t0 = lg0 * (lg0 + 1) / 2, Tg = lg1 * (lg1 + 1) / 2 - t0;
+        const float inv_T = 1.0f / (float)Tg;
+        for (int it = lane; it < nb * Tg; it += 64) {
+            const int e = qdiv(it, inv_T), t = it - e * Tg + t0;
+            const double2 c01 = T.gcoef[2 * t], c2p = T.gcoef[2 * t + 1];
+            const int lm = (int)c2p.y, l = lm & 0xff, m = lm >> 8;
+            double *Y = YY + e * yl.es;
+            const int lp = l > 0 ? l - 1 : 0, c0 = lp * lp + lp - yl.lmY0;
+            const bool live = geo[4 * e + 3] != 0.0 && l > 0;
+            // S'_k for k in {m+1, -(m+1), m-1, -(m-1), m, -m}, clamped into degree l-1
+            auto sp = [&](int k) -> double {
+                const int kc = k < -lp ? -lp : (k > lp ? lp : k);
+                const double v = Y[(c0 + kc) * yl.ls];
+                return (live && k >= -lp && k <= lp) ? v : 0.0;
+            };
+            const double cA = c01.x, cB = c01.y, cC = c2p.x;
+            double *Dx = Y + yl.cs, *Dy = Y + 2 * yl.cs, *Dz = Y + 3 * yl.cs;
+            const int o = l * l + l - yl.lmY0;
+            if (m == 0) {
+                Dx[o * yl.ls] = -cA * sp(1);
+                Dy[o * yl.ls] = -cA * sp(-1);
+                Dz[o * yl.ls] = cC * sp(0);
             } else {
-                const int x = it - n_sh, e = x / Q, q = x - e * Q;
-                const double r = st.geo[4 * e + 3], rq = T.rq[q];
-                const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
-                bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, st.X + (size_t)x * tw);
+                const double pp = sp(m + 1), pn = sp(-(m + 1)), qp = sp(m - 1), qn = m > 1 ? sp(-(m - 1)) : 0.0;
+                const double zp = sp(m), zn = sp(-m);
+                Dx[(o + m) * yl.ls] = -cA * pp + cB * qp;
+                Dy[(o + m) * yl.ls] = -cA * pn - cB * qn;
+                Dz[(o + m) * yl.ls] = cC * zp;
+                Dx[(o - m) * yl.ls] = -cA * pn + cB * qn;
+                Dy[(o - m) * yl.ls] = cA * pp + cB * qp;
+                Dz[(o - m) * yl.ls] = cC * zn;
             }
         }
-        if (WAVE) wave_sync(); else lds_barrier();
-        for (int it = tid; it < nb * n * lgc; it += bs) {
-            const int e = it / (n * lgc), rem = it - e * (n * lgc), a = rem / lgc, lc = rem - a * lgc;
-            const int l = lg0 + lc;
-            const double r = st.geo[4 * e + 3];
+    }
+    const int nd = nb * nlc;
+    if (!poly) {
+        for (int it = lane; it < nd; it += 128) {
+            const int i2 = it + 64 < nd ? it + 64 : it;
+            const int e1 = qdiv(it, inv_nlc), t1 = it - e1 * nlc, l1 = t1 - qdiv(t1, inv_lgc) * lgc;
+            const int e2 = qdiv(i2, inv_nlc), t2 = i2 - e2 * nlc, l2 = t2 - qdiv(t2, inv_lgc) * lgc;
+            const double2 *bc1 = T.bcp + t1, *bc2 = T.bcp + t2; // [k][n][lc]: t = a lgc + lc
+            const double *E1 = X + (size_t)e1 * nlc + l1, *E2 = X + (size_t)e2 * nlc + l2;
+            double b1 = 0.0, h1 = 0.0, b2 = 0.0, h2 = 0.0;
+#pragma unroll 2
+            for (int k = 0; k < n; ++k) {
+                const double2 c1 = bc1[k * nlc], c2 = bc2[k * nlc];
+                const double v1 = E1[k * lgc], v2 = E2[k * lgc];
+                b1 += c1.x * v1;
+                h1 += c1.y * v1;
+                b2 += c2.x * v2;
+                h2 += c2.y * v2;
+            }
+            const double K1 = scaleK ? T.Kl[lg0 + l1] : 1.0, K2 = scaleK ? T.Kl[lg0 + l2] : 1.0;
+            BB[it] = make_double2(K1 * b1, K1 * h1);
+            BB[i2] = make_double2(K2 * b2, K2 * h2);
+        }
+    } else {
+        for (int it = lane; it < nd; it += 64) {
+            const int e = qdiv(it, inv_nlc), t = it - e * nlc, a = qdiv(t, inv_lgc), l = lg0 + t - a * lgc;
+            const double r = geo[4 * e + 3];
             const double *G = T.G + (size_t)a * Q;
-            const double *t = st.X + (size_t)e * Q * tw;
+            const double *tq = X + (size_t)e * Q * tw;
             double b = 0.0, bh = 0.0;
             for (int q = 0; q < Q; ++q) {
-                const double tl = t[q * tw + l];
+                const double tl = tq[q * tw + l];
                 b += G[q] * tl;
-                if (GRAD) bh += G[q] * (T.rq[q] * t[q * tw + l + 1] - r * tl);
+                if (GRAD) bh += G[q] * (T.rq[q] * tq[q * tw + l + 1] - r * tl);
             }
-            const double K = scaleK ? T.Kl[l] : 1.0;
             if (r == 0.0) {
                 b = (l == 0) ? b : 0.0;
                 bh = 0.0;
@@ -432,9 +383,11 @@ __device__ __forceinline__ void stage_angular_radial(const Params &P, const Tabl
                 b *= rl;
                 bh *= rl * ir * P.inv_s2;
             }
-            st.BB[it] = make_double2(K * b, K * bh);
+            const double K = scaleK ? T.Kl[l] : 1.0;
+            BB[it] = make_double2(K * b, K * bh);
         }
     }
+    wave_sync();
 }
 
 // Prefetch the rows [r0, r0+cnt) of the center: edge vectors r_j - r_i in
@@ -460,22 +413,27 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
 //
 // Persistent: a workgroup is bound to one l-group g (blockIdx % G), keeps
 // that group's basis tables in LDS, and takes centers from an atomic work
-// counter.  Per center, each wave runs its own pipeline over its own edges
-// (W at a time): harmonics + radial factors in the wave's LDS, then every
-// lane adds the edges' contributions to the coefficient entries (a, lm) it
-// owns, in registers: c^s_{a lm} += B_al S_lm and, for the Jacobian,
-// D^s_{a lm} += Bh_al r S_lm + B_al grad S_lm (D = sum over neighbours of
-// dc/dr_j = -dc/dr_i).  Register sums are flushed into the shared LDS
-// accumulators with atomic adds when the (sorted) neighbour species changes.
-// Then the whole workgroup writes the power spectrum and the center block
+// counter.  Per center, each wave runs its own tiles of W edges: staging
+// (harmonics, gradients, radial factors) in the wave's LDS, then every lane
+// adds each edge's contribution to the coefficient entries (a, lm) it owns,
+// in registers that persist over the wave's tiles:
+//   c^s_{a lm} += B_al S_lm,
+//   D^s_{a lm} += Bh_al r S_lm + B_al grad S_lm
+// (D = sum over neighbours of dc/dr_j = -dc/dr_i).  Rows are sorted by
+// species, so the registers are flushed into the shared LDS accumulators
+// (float64 LDS atomics) only when the species changes and at the end.  Then
+// the whole workgroup writes the power spectrum and the center block
 // -K_l sum_m (D^mu c^nu + c^mu D^nu).
 // ---------------------------------------------------------------------------
 constexpr int NWD = 4, BSD = 64 * NWD;
-constexpr int KE = 8; // coefficient entries owned per lane: n * Lg <= 64 * KE
+constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 64 * KE
+
+__host__ __device__ __forceinline__ int dens_lgY0(int jac, int lg0) { return (jac && lg0 > 0) ? lg0 - 1 : lg0; }
 
 __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, int jac, int lg0, int lg1, int W) {
-    const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0), lgc = (size_t)(lg1 - lg0);
-    return even(W * Lg) + even(jac ? 3 * W * Lg : 0) + even(2 * W * P.n * lgc) + even(W * stage_x_doubles(P, (int)lgc, lg1));
+    const int lgY0 = dens_lgY0(jac, lg0);
+    const size_t LY = (size_t)(lg1 * lg1 - lgY0 * lgY0), lgc = (size_t)(lg1 - lg0);
+    return even(W * LY * (jac ? 4 : 1)) + 2 * W * P.n * lgc + even(W * stage_x_doubles(P, (int)lgc, lg1));
 }
 
 template <typename PosT, typename OutT, bool JAC>
@@ -483,287 +441,184 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                                                  int *__restrict__ work, OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,
                                                  double *__restrict__ c_scratch) {
-    extern __shared__ double smem[];
+    // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
+    extern __shared__ __align__(16) double smem[];
     __shared__ int64_t s_next;
     const int G = P.n_groups;
     const int g = blockIdx.x % G;
     const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0;
     const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
+    const int lgY0 = dens_lgY0(JAC, lg0), lmY0 = lgY0 * lgY0, LY = lg1 * lg1 - lmY0;
     const int S = P.S, n = P.n, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int nL = n * Lg, SnL = S * nL, lw = P.lmax + 1, Lfull = P.L;
+    const int nL = n * Lg, SnL = S * nL, lw = P.lmax + 1, Lfull = P.L, Sn = S * n, nlc = n * lgc;
     const int RBk = row_block(NWD * W);
 
     Carver cv{smem};
     Tables T;
     load_tables(P, cv, T, lg0, lg1);
-    double *cacc = cv.take((size_t)SnL * (JAC ? 4 : 1));
-    double *Dacc = cacc + SnL; // [3][S][n][Lg]
+    double *cacc = cv.take((size_t)SnL * (JAC ? 4 : 1)); // [s][a][lmg], then D [3][s][a][lmg]
+    double *Dacc = cacc + SnL;
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
+    uint32_t *fq = (uint32_t *)cv.take(((size_t)P.nq_full + 1) / 2);
+    double *c0 = cv.take((size_t)n);
     Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W)};
-    Stage st;
-    st.Y = wv.take((size_t)W * Lg);
-    st.dY = wv.take(JAC ? 3 * (size_t)W * Lg : 0);
-    st.ys = Lg;
-    st.dys = 3 * Lg;
-    st.BB = (double2 *)wv.take(2 * (size_t)W * n * lgc);
-    st.X = wv.take(W * stage_x_doubles(P, lgc, lg1));
+    // harmonics interleaved per lm as (S, dS/dx, dS/dy, dS/dz) for the Jacobian
+    const YLayout yl = JAC ? YLayout{4 * LY, 1, 4, lmY0} : YLayout{LY, 0, 1, lmY0};
+    double *YY = wv.take((size_t)W * yl.es);
+    double2 *BB = (double2 *)wv.take(2 * (size_t)W * nlc);
+    double *X = wv.take((size_t)W * stage_x_doubles(P, lgc, lg1));
 
     // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg
-    int ent[KE], oY[KE], oB[KE];
+    int oY[KE], oB[KE];
+    bool own[KE];
 #pragma unroll
     for (int k = 0; k < KE; ++k) {
         const int e = lane + 64 * k;
-        ent[k] = e < nL ? e : -1;
+        own[k] = e < nL;
         const int a = e / Lg, lmg = e - a * Lg;
-        oY[k] = lmg;
-        oB[k] = a * lgc + (e < nL ? isqrt_lm(lmg + lm0) - lg0 : 0);
+        const int lm = lm0 + (own[k] ? lmg : 0);
+        int l = (int)sqrtf((float)lm);
+        while (l * l > lm) --l;
+        while ((l + 1) * (l + 1) <= lm) ++l;
+        oY[k] = (lm - lmY0) * (JAC ? 4 : 1);
+        oB[k] = own[k] ? a * lgc + (l - lg0) : 0;
     }
 
-    for (;;) {
+    // per-basis tables used by the outputs, in LDS: no global load may sit
+    // between output stores (vmcnt counts loads and stores together)
+    for (int k = tid; k < P.nq_full; k += BSD) fq[k] = P.fq[k];
+    for (int k = tid; k < n; k += BSD) c0[k] = P.c0[k];
+
+    // the next center: its rows are loaded before the current center's
+    // outputs are stored, so those loads never wait behind the stores
+    int64_t ci = 0, i = 0, e0 = 0, e1 = 0;
+    int spec_i = 0;
+    double3 pi = make_double3(0.0, 0.0, 0.0);
+    auto fetch = [&]() {
         if (tid == 0) s_next = atomicAdd(&work[g], 1);
         lds_barrier();
-        const int64_t ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
-        if (ci >= R.nc) break;
-        const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
-        const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
-        const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
+        ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
+        lds_barrier(); // s_next is rewritten by the next fetch
+        if (ci >= R.nc) return;
+        i = R.centers ? (int64_t)R.centers[ci] : ci;
+        pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
+        spec_i = R.spec[i];
+        e0 = R.row_ptr[ci];
+        e1 = R.row_ptr[ci + 1];
+        const int64_t cnt = (e1 - e0) < RBk ? (e1 - e0) : RBk;
+        load_rows(rgeo, rsp, pos, R.spec, R.cols, e0, (int)cnt, pi);
+    };
+    fetch();
+    const float inv_lgc = 1.0f / (float)lgc, inv_qlgc = 1.0f / (float)(P.nq_full * lgc), inv_Lg = 1.0f / (float)Lg;
+
+    while (ci < R.nc) {
         for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BSD) cacc[k] = 0.0;
+        lds_barrier(); // rows of this center and the cleared accumulators
+
+        double acc[KE][4];
+#pragma unroll
+        for (int k = 0; k < KE; ++k) acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
+        int cur = -1; // species of the registers' edges
+        auto flush = [&]() {
+#pragma unroll
+            for (int k = 0; k < KE; ++k) {
+                if (!own[k]) continue;
+                const int idx = cur * nL + lane + 64 * k;
+                atomicAdd(&cacc[idx], acc[k][0]);
+                if (JAC) {
+                    atomicAdd(&Dacc[idx], acc[k][1]);
+                    atomicAdd(&Dacc[SnL + idx], acc[k][2]);
+                    atomicAdd(&Dacc[2 * SnL + idx], acc[k][3]);
+                }
+                acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
+            }
+        };
 
         for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
             const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
-            lds_barrier();
-            load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
-            lds_barrier();
+            if (rb0 != e0) { // further row blocks of a long row (no output stores are pending here)
+                lds_barrier();
+                load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
+                lds_barrier();
+            }
             for (int off = wave * W; off < rbn; off += NWD * W) {
                 const int nb = (rbn - off) < W ? (rbn - off) : W;
-                st.geo = rgeo + 4 * off;
-                st.sp = rsp + off;
-                stage_angular_radial<JAC, true>(P, T, st, nb, lg0, lg1, false, lane, 64);
-                wave_sync();
-                // per owned entry: register sums over this group's edges, flushed
-                // to the shared accumulators at each species change
-#pragma unroll
-                for (int k = 0; k < KE; ++k) {
-                    if (ent[k] < 0) continue;
-                    double a0 = 0.0, ax = 0.0, ay = 0.0, az = 0.0;
-                    int cur = st.sp[0];
-                    for (int e = 0; e < nb; ++e) {
-                        const int s = st.sp[e];
-                        if (s != cur) {
-                            const int idx = cur * nL + ent[k];
-                            atomicAdd(&cacc[idx], a0);
-                            if (JAC) {
-                                atomicAdd(&Dacc[idx], ax);
-                                atomicAdd(&Dacc[SnL + idx], ay);
-                                atomicAdd(&Dacc[2 * SnL + idx], az);
-                            }
-                            a0 = ax = ay = az = 0.0;
-                            cur = s;
-                        }
-                        const double2 bb = st.BB[e * n * lgc + oB[k]];
-                        const double y = st.Y[e * Lg + oY[k]];
-                        a0 += bb.x * y;
-                        if (JAC) {
-                            const double bh = bb.y * y;
-                            const double *gg = st.geo + 4 * e, *dy = st.dY + e * 3 * Lg + oY[k];
-                            ax += bh * gg[0] + bb.x * dy[0];
-                            ay += bh * gg[1] + bb.x * dy[Lg];
-                            az += bh * gg[2] + bb.x * dy[2 * Lg];
-                        }
+                const double *geo = rgeo + 4 * off;
+                stage_edges<JAC>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
+                for (int e = 0; e < nb; ++e) {
+                    const int s = __builtin_amdgcn_readfirstlane(rsp[off + e]);
+                    if (s != cur) {
+                        if (cur >= 0) flush();
+                        cur = s;
                     }
-                    const int idx = cur * nL + ent[k];
-                    atomicAdd(&cacc[idx], a0);
-                    if (JAC) {
-                        atomicAdd(&Dacc[idx], ax);
-                        atomicAdd(&Dacc[SnL + idx], ay);
-                        atomicAdd(&Dacc[2 * SnL + idx], az);
+                    const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
+                    const double *Ye = YY + e * yl.es;
+                    const double2 *Be = BB + e * nlc;
+#pragma unroll
+                    for (int k = 0; k < KE; ++k) {
+                        if (!own[k]) continue;
+                        const double2 bb = Be[oB[k]];
+                        if (JAC) {
+                            const double2 y01 = *(const double2 *)(Ye + oY[k]), y23 = *(const double2 *)(Ye + oY[k] + 2);
+                            const double bh = bb.y * y01.x;
+                            acc[k][0] += bb.x * y01.x;
+                            acc[k][1] += bh * rx + bb.x * y01.y;
+                            acc[k][2] += bh * ry + bb.x * y23.x;
+                            acc[k][3] += bh * rz + bb.x * y23.y;
+                        } else {
+                            acc[k][0] += bb.x * Ye[oY[k]];
+                        }
                     }
                 }
-                wave_sync();
+                wave_sync(); // the next tile's staging overwrites YY and BB
             }
         }
+        if (cur >= 0) flush();
         lds_barrier();
         // on-site term of the center (its species, l = 0)
         if (lg0 == 0)
-            for (int a = tid; a < n; a += BSD) cacc[(int)R.spec[i] * nL + a * Lg] += P.c0[a];
-        lds_barrier();
+            for (int a = tid; a < n; a += BSD) cacc[spec_i * nL + a * Lg] += c0[a];
+        // the next center's rows go in while this center's outputs are written
+        const int64_t cw = ci;
+        fetch(); // its barriers also publish the on-site term
         // power spectrum for the group's l
         if (desc)
             for (int it = tid; it < P.nq_full * lgc; it += BSD) {
-                const int q = it / lgc, lc = it - q * lgc, l = lg0 + lc;
-                const uint32_t f = P.fq[q];
+                const int q = qdiv(it, inv_lgc), lc = it - q * lgc, l = lg0 + lc;
+                const uint32_t f = fq[q];
                 const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
                 const double *x = cacc + mu * nL + a * Lg + l * l - lm0;
                 const double *y = cacc + nu * nL + b * Lg + l * l - lm0;
                 double sum = 0.0;
                 for (int m = 0; m < 2 * l + 1; ++m) sum += x[m] * y[m];
-                desc[ci * P.F + q * lw + l] = (OutT)(T.Kl[l] * sum);
+                store_out(desc + cw * P.F + q * lw + l, T.Kl[l] * sum);
             }
         if (c_out)
             for (int it = tid; it < SnL; it += BSD) {
-                const int sa = it / Lg, lmg = it - sa * Lg;
-                c_out[(ci * S * n + sa) * Lfull + lm0 + lmg] = (OutT)cacc[it];
+                const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
+                store_out(c_out + (cw * Sn + sa) * Lfull + lm0 + lmg, cacc[it]);
             }
         if (JAC) {
+            // c, transposed to [lm][s n] for the Jacobian kernel's matrix-core operand
             for (int it = tid; it < SnL; it += BSD) {
-                const int sa = it / Lg, lmg = it - sa * Lg;
-                c_scratch[(ci * Lfull + lm0 + lmg) * S * n + sa] = cacc[it];
+                const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
+                c_scratch[(cw * Lfull + lm0 + lmg) * Sn + sa] = cacc[it];
             }
             for (int it = tid; it < 3 * P.nq_full * lgc; it += BSD) {
-                const int d = it / (P.nq_full * lgc), rem = it - d * (P.nq_full * lgc);
-                const int q = rem / lgc, lc = rem - q * lgc, l = lg0 + lc;
-                const uint32_t f = P.fq[q];
+                const int d = qdiv(it, inv_qlgc), rem = it - d * (P.nq_full * lgc);
+                const int q = qdiv(rem, inv_lgc), lc = rem - q * lgc, l = lg0 + lc;
+                const uint32_t f = fq[q];
                 const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
                 const int oa = mu * nL + a * Lg + l * l - lm0, ob = nu * nL + b * Lg + l * l - lm0;
                 const double *Dd = Dacc + d * SnL;
                 double sum = 0.0;
                 for (int m = 0; m < 2 * l + 1; ++m) sum += Dd[oa + m] * cacc[ob + m] + cacc[oa + m] * Dd[ob + m];
-                jself[(ci * 3 + d) * P.F + q * lw + l] = (OutT)(-T.Kl[l] * sum);
+                store_out(jself + (cw * 3 + d) * P.F + q * lw + l, -T.Kl[l] * sum);
             }
         }
-        lds_barrier();
+        lds_barrier(); // the outputs are read from cacc before the next center clears it
     }
-}
-
-// floor(x / d) for 0 <= x < 2^22 with inv = 1/d correctly rounded: the
-// relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
-// next integer
-__device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x + 0.5f) * inv); }
-
-// ---------------------------------------------------------------------------
-// Per-tile staging of the Jacobian kernel: one wave, nb <= W edges.
-//   YY[e][0][lm] = S_lm, YY[e][1 + d][lm] = dS_lm/dx_d
-//   BB[e][n][l]  = K_l (B_nl, Bh_nl)
-//   X: GTO exponentials [e][k][l], or the polynomial table [e][q][0..l_max+1]
-// Phase 1 runs the harmonic columns (edge, m) without gradients next to the
-// exponentials; phase 2 takes each gradient from the degree l-1 harmonics.
-// With H_l^m = (x + iy)^m Q_l^m (so S_l,m = N_lm Re H, S_l,-m = N_lm Im H):
-//   d/dz H_l^m = (l+m) H_{l-1}^m,  (d/dx + i d/dy) H_l^m = -H_{l-1}^{m+1},
-//   (d/dx - i d/dy) H_l^m = (l+m)(l+m-1) H_{l-1}^{m-1},
-// so every component is at most two degree l-1 harmonics.  Per (l, m >= 0),
-// with S' = S_{l-1,.} and gcoef = (cA, cB, cC):
-//   m = 0:  grad S_l0 = (-cA S'_1, -cA S'_-1, cC S'_0)
-//   m > 0:  grad S_lm  = (-cA S'_{m+1} + cB S'_{m-1}, -cA S'_{-(m+1)} - cB S'_{-(m-1)}, cC S'_m)
-//           grad S_l-m = (-cA S'_{-(m+1)} + cB S'_{-(m-1)}, cA S'_{m+1} + cB S'_{m-1}, cC S'_-m)
-// (S'_k = 0 for |k| > l-1, S'_-0 = 0).  A zero-length edge gets a zero gradient.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void stage_jac(const Params &P, const Tables &T, double *__restrict__ YY,
-                                          double2 *__restrict__ BB, double *__restrict__ X,
-                                          const double *__restrict__ geo, int nb, int lane) {
-    const int n = P.n, lw = P.lmax + 1, L = P.L, nl = n * lw, ldN = P.lmax + 2;
-    const float inv_lw = 1.0f / (float)lw, inv_nl = 1.0f / (float)nl;
-    const int n_sh = nb * lw;
-    const bool poly = P.rbf != 0;
-    const int Q = P.Q, tw = lw + 1;
-    const float inv_Q = 1.0f / (float)Q;
-    // phase 1: harmonic columns (edge, m), then the radial scratch, two
-    // independent items per lane trip
-    for (int it = lane; it < n_sh; it += 64) {
-        const int e = qdiv(it, inv_lw), m = it - e * lw;
-        const double *g = geo + 4 * e;
-        sh_col_y(m, lw, g[0], g[1], g[2], T.Nt, ldN, YY + e * 4 * L);
-    }
-    if (!poly) {
-        const int nx = nb * nl;
-        for (int it = lane; it < nx; it += 128) {
-            const int i2 = it + 64 < nx ? it + 64 : it;
-            const int e1 = qdiv(it, inv_nl), e2 = qdiv(i2, inv_nl);
-            const double r1 = geo[4 * e1 + 3], r2 = geo[4 * e2 + 3];
-            const double v1 = exp(-T.aprime[it - e1 * nl] * r1 * r1), v2 = exp(-T.aprime[i2 - e2 * nl] * r2 * r2);
-            X[it] = v1;
-            X[i2] = v2;
-        }
-    } else {
-        for (int it = lane; it < nb * Q; it += 64) {
-            const int e = qdiv(it, inv_Q), q = it - e * Q;
-            const double r = geo[4 * e + 3], rq = T.rq[q];
-            const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
-            bessel_scaled_lds(lw, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
-        }
-    }
-    wave_sync();
-    // phase 2: gradients (edge, (l, m >= 0)), then the radial factors (edge, n, l)
-    const int Tn = grad_pairs(P.lmax), n_g = nb * Tn;
-    const float inv_T = 1.0f / (float)Tn;
-    for (int it = lane; it < n_g; it += 64) {
-        const int e = qdiv(it, inv_T), t = it - e * Tn;
-        const double2 c01 = T.gcoef[2 * t], c2p = T.gcoef[2 * t + 1];
-        const int lm = (int)c2p.y, l = lm & 0xff, m = lm >> 8;
-        double *Y = YY + e * 4 * L;
-        const int lp = l > 0 ? l - 1 : 0, c0 = lp * lp + lp;
-        const bool live = geo[4 * e + 3] != 0.0 && l > 0;
-        // S'_k for k in {m+1, -(m+1), m-1, -(m-1), m, -m}, clamped into degree l-1
-        auto sp = [&](int k) -> double {
-            const int kc = k < -lp ? -lp : (k > lp ? lp : k);
-            const double v = Y[c0 + kc];
-            return (live && k >= -lp && k <= lp) ? v : 0.0;
-        };
-        const double cA = c01.x, cB = c01.y, cC = c2p.x;
-        const int o = l * l + l;
-        if (m == 0) {
-            Y[L + o] = -cA * sp(1);
-            Y[2 * L + o] = -cA * sp(-1);
-            Y[3 * L + o] = cC * sp(0);
-        } else {
-            const double pp = sp(m + 1), pn = sp(-(m + 1)), qp = sp(m - 1), qn = m > 1 ? sp(-(m - 1)) : 0.0;
-            const double zp = sp(m), zn = sp(-m);
-            Y[L + o + m] = -cA * pp + cB * qp;
-            Y[2 * L + o + m] = -cA * pn - cB * qn;
-            Y[3 * L + o + m] = cC * zp;
-            Y[L + o - m] = -cA * pn + cB * qn;
-            Y[2 * L + o - m] = cA * pp + cB * qp;
-            Y[3 * L + o - m] = cC * zn;
-        }
-    }
-    const int nd = nb * nl;
-    if (!poly) {
-        for (int it = lane; it < nd; it += 128) {
-            const int i2 = it + 64 < nd ? it + 64 : it;
-            const int e1 = qdiv(it, inv_nl), t1 = it - e1 * nl, l1 = t1 - qdiv(t1, inv_lw) * lw;
-            const int e2 = qdiv(i2, inv_nl), t2 = i2 - e2 * nl, l2 = t2 - qdiv(t2, inv_lw) * lw;
-            const double2 *bc1 = T.bcp + t1, *bc2 = T.bcp + t2; // [k][n][l]: t = a lw + l
-            const double *E1 = X + (size_t)e1 * nl + l1, *E2 = X + (size_t)e2 * nl + l2;
-            double b1 = 0.0, h1 = 0.0, b2 = 0.0, h2 = 0.0;
-#pragma unroll 2
-            for (int k = 0; k < n; ++k) {
-                const double2 c1 = bc1[k * nl], c2 = bc2[k * nl];
-                const double v1 = E1[k * lw], v2 = E2[k * lw];
-                b1 += c1.x * v1;
-                h1 += c1.y * v1;
-                b2 += c2.x * v2;
-                h2 += c2.y * v2;
-            }
-            const double K1 = T.Kl[l1], K2 = T.Kl[l2];
-            BB[it] = make_double2(K1 * b1, K1 * h1);
-            BB[i2] = make_double2(K2 * b2, K2 * h2);
-        }
-    } else {
-        for (int it = lane; it < nd; it += 64) {
-            const int e = qdiv(it, inv_nl), t = it - e * nl, a = qdiv(t, inv_lw), l = t - a * lw;
-            const double r = geo[4 * e + 3];
-            const double *G = T.G + (size_t)a * Q;
-            const double *tq = X + (size_t)e * Q * tw;
-            double b = 0.0, bh = 0.0;
-            for (int q = 0; q < Q; ++q) {
-                const double tl = tq[q * tw + l];
-                b += G[q] * tl;
-                bh += G[q] * (T.rq[q] * tq[q * tw + l + 1] - r * tl);
-            }
-            if (r == 0.0) {
-                b = (l == 0) ? b : 0.0;
-                bh = 0.0;
-            } else {
-                double ir = 1.0 / r, rl = 1.0;
-                for (int k = 0; k < l; ++k) rl *= ir;
-                b *= rl;
-                bh *= rl * ir * P.inv_s2;
-            }
-            const double K = T.Kl[l];
-            BB[it] = make_double2(K * b, K * bh);
-        }
-    }
-    wave_sync();
 }
 
 // ---------------------------------------------------------------------------
@@ -824,7 +679,8 @@ template <typename T> __device__ __forceinline__ void store3(T *o, uint32_t Fe, 
 template <typename PosT, typename OutT>
 __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                                   const double *__restrict__ c_scratch, OutT *__restrict__ jedge) {
-    extern __shared__ double smem[];
+    // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
+    extern __shared__ __align__(16) double smem[];
     const int S = P.S, n = P.n, lw = P.lmax + 1, L = P.L, Sn = S * n, tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
     const int Fe = P.Fe, nl = n * lw, nnl = n * nl, tri_lw = P.tri_lw;
@@ -887,7 +743,7 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
             const int64_t base = rb0 + off;
             const double *geo = rgeo + 4 * off;
             const int *spc = rsp + off;
-            stage_jac(P, T, YY, BB, XU, geo, nb, lane);
+            stage_edges<true>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw, true);
 
             // ---- precontraction on the matrix cores ----
             // chunks j = (l, ch) in l-major order, operands loaded JB at a time
@@ -1029,7 +885,7 @@ size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W) {
     const size_t SnL = (size_t)P.S * P.n * Lg;
     const int RBk = row_block(NWD * W);
     size_t d = table_doubles(P, lg1 - lg0) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               NWD * dens_wave_doubles(P, jac, lg0, lg1, W);
+               even(((size_t)P.nq_full + 1) / 2) + even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W);
     return d * 8;
 }
 
