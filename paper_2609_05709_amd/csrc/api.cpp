@@ -45,7 +45,6 @@ struct DevBuf {
 };
 
 constexpr size_t DENSITY_LDS_BUDGET = 64 * 1024;
-constexpr size_t JACOBIAN_LDS_BUDGET = 80 * 1024;
 constexpr size_t LDS_HARD_LIMIT = 159 * 1024; // leaves room for static LDS
 
 thread_local std::string g_create_error = "";
@@ -192,13 +191,22 @@ int plan_launches(soap_ctx *c) {
         const int per_cu = density_blocks_per_cu(c->dtype == SOAP_FP64, jac != 0, lds);
         c->dens_cfg[jac].blocks = std::max(1, ncu * per_cu / *G);
     }
-    // Jacobian kernel: W edges per wave tile
-    int W = jacobian_max_w();
-    while (W > 1 && jacobian_lds_bytes(P, W) > JACOBIAN_LDS_BUDGET) --W;
-    if (jacobian_lds_bytes(P, W) > LDS_HARD_LIMIT)
-        return fail(c, SOAP_EINVAL, "basis too large for the Jacobian kernel's on-chip memory");
-    c->jac_cfg.W = W;
-    c->jac_cfg.lds = jacobian_lds_bytes(P, W);
+    // Jacobian kernel: W edges per wave tile.  The most resident waves per CU
+    // first (latency hiding for its LDS-bound staging), then the widest tile.
+    const bool f64 = c->dtype == SOAP_FP64;
+    int bestW = 0, bestB = 0;
+    for (int W = jacobian_max_w(); W >= 1; --W) {
+        const size_t lds = jacobian_lds_bytes(P, W, f64);
+        if (lds > LDS_HARD_LIMIT) continue;
+        const int b = jacobian_blocks_per_cu(f64, lds);
+        if (b > bestB) {
+            bestB = b;
+            bestW = W;
+        }
+    }
+    if (bestW == 0) return fail(c, SOAP_EINVAL, "basis too large for the Jacobian kernel's on-chip memory");
+    c->jac_cfg.W = bestW;
+    c->jac_cfg.lds = jacobian_lds_bytes(P, bestW, f64);
     return SOAP_OK;
 }
 

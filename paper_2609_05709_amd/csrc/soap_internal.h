@@ -77,8 +77,9 @@ struct JacLaunch {
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W);
 int density_blocks_per_cu(bool f64, bool jac, size_t lds);
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
-size_t jacobian_lds_bytes(const Params &P, int W);
+size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
 int jacobian_max_w();
+int jacobian_blocks_per_cu(bool f64, size_t lds); // resident workgroups per CU (0 if it does not fit)
 hipError_t set_lds_limits();
 
 // desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)

@@ -38,6 +38,18 @@ namespace {
 // stores of the neighbour blocks' partial-line runs write back at about half
 // the bandwidth.
 template <typename T> __device__ __forceinline__ void store_out(T *p, double v) { *p = (T)v; }
+__device__ __forceinline__ void store_out(float *p, float v) { *p = v; }
+
+// (value, companion) pairs in LDS at the precision T
+template <typename T> struct Pair;
+template <> struct Pair<double> {
+    using type = double2;
+    static __device__ __forceinline__ double2 make(double a, double b) { return make_double2(a, b); }
+};
+template <> struct Pair<float> {
+    using type = float2;
+    static __device__ __forceinline__ float2 make(double a, double b) { return make_float2((float)a, (float)b); }
+};
 
 // floor(x / d) for 0 <= x < 2^22 with inv = 1/d correctly rounded: the
 // relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
@@ -249,7 +261,7 @@ __device__ __forceinline__ void lds_barrier() {
 //   YY: harmonics, element (edge e, component c, lm) at
 //       e es + c cs + (lm - lmY0) ls; component 0 = S, 1..3 = dS/dx_d (GRAD).
 //       Degrees from lgY0 = lg0 - 1 (GRAD and lg0 > 0) or lg0 are stored.
-//   BB[e][n][lc] = K (B_nl, Bh_nl), K = K_l if scaleK else 1
+//   BB[e][n][lc] = K (B_nl, Bh_nl), K = K_l if scaleK else 1, stored at precision BT
 //   X: GTO exponentials [e][k][lc], or the polynomial table [e][q][0..lg1]
 // Phase 1 runs the harmonic columns (edge, m), then the radial scratch;
 // phase 2 the gradients, then the radial factors.  Each gradient component
@@ -267,9 +279,9 @@ struct YLayout {
     int es, cs, ls, lmY0;
 };
 
-template <bool GRAD>
+template <bool GRAD, typename BT = double>
 __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, double *__restrict__ YY, YLayout yl,
-                                            double2 *__restrict__ BB, double *__restrict__ X,
+                                            typename Pair<BT>::type *__restrict__ BB, double *__restrict__ X,
                                             const double *__restrict__ geo, int nb, int lane, int lg0, int lg1,
                                             bool scaleK) {
     const int n = P.n, ldN = P.lmax + 2, lgc = lg1 - lg0, nlc = n * lgc;
@@ -359,8 +371,8 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, do
                 h2 += c2.y * v2;
             }
             const double K1 = scaleK ? T.Kl[lg0 + l1] : 1.0, K2 = scaleK ? T.Kl[lg0 + l2] : 1.0;
-            BB[it] = make_double2(K1 * b1, K1 * h1);
-            BB[i2] = make_double2(K2 * b2, K2 * h2);
+            BB[it] = Pair<BT>::make(K1 * b1, K1 * h1);
+            BB[i2] = Pair<BT>::make(K2 * b2, K2 * h2);
         }
     } else {
         for (int it = lane; it < nd; it += 64) {
@@ -384,7 +396,7 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, do
                 bh *= rl * ir * P.inv_s2;
             }
             const double K = scaleK ? T.Kl[l] : 1.0;
-            BB[it] = make_double2(K * b, K * bh);
+            BB[it] = Pair<BT>::make(K * b, K * bh);
         }
     }
     wave_sync();
@@ -657,28 +669,36 @@ __host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l
     return (l & 1) ? (a + 1) * (a + 1) : a * (a + 1);
 }
 
-__host__ __device__ __forceinline__ size_t jac_xu_doubles(const Params &P) {
+// The assembly works at the output precision (ab = 4 or 8 bytes): U/V and
+// B/Bh are rounded once to it, which keeps the float32 kernel's LDS small
+// enough for three workgroups per CU.
+__host__ __device__ __forceinline__ size_t jac_xu_doubles(const Params &P, int ab) {
     const size_t lw = (size_t)P.lmax + 1, Sn = (size_t)P.S * P.n;
-    const size_t xd = stage_x_doubles(P, (int)lw, (int)lw);
-    return xd > 4 * Sn * lw ? xd : 4 * Sn * lw;
+    const size_t xd = stage_x_doubles(P, (int)lw, (int)lw), ud = 4 * Sn * lw * ab / 8;
+    return xd > ud ? xd : ud;
 }
 
-__host__ __device__ __forceinline__ size_t jac_wave_doubles(const Params &P, int W) {
+__host__ __device__ __forceinline__ size_t jac_wave_doubles(const Params &P, int W, int ab) {
     const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1;
-    return even(W * 4 * L) + even(2 * W * P.n * lw) + even(W * jac_xu_doubles(P));
+    return even(W * 4 * L) + even(2 * W * P.n * lw * ab / 8) + even(W * jac_xu_doubles(P, ab));
 }
 
 // o: wave-uniform row base; idx: per-lane offset (unsigned, so the stores
 // can take the scalar-base + 32-bit-offset form)
-template <typename T> __device__ __forceinline__ void store3(T *o, uint32_t Fe, uint32_t idx, double x, double y, double z) {
+template <typename T, typename V>
+__device__ __forceinline__ void store3(T *o, uint32_t Fe, uint32_t idx, V x, V y, V z) {
     store_out(o + idx, x);
     store_out(o + (Fe + idx), y);
     store_out(o + (2 * Fe + idx), z);
 }
 
 template <typename PosT, typename OutT>
-__global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos, int W,
-                                                  const double *__restrict__ c_scratch, OutT *__restrict__ jedge) {
+__global__ __launch_bounds__(BSJ, sizeof(OutT) == 4 ? 3 : 2) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
+                                                                            int W, const double *__restrict__ c_scratch,
+                                                                            OutT *__restrict__ jedge) {
+    using AT = OutT; // assembly precision
+    using AT2 = typename Pair<AT>::type;
+    constexpr int ab = sizeof(AT);
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
     extern __shared__ __align__(16) double smem[];
     const int S = P.S, n = P.n, lw = P.lmax + 1, L = P.L, Sn = S * n, tid = threadIdx.x;
@@ -694,13 +714,13 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
     int *rsp = (int *)cv.take((RBk + 1) / 2);
     uint32_t *dtab = (uint32_t *)cv.take(((size_t)tri_lw + 1) / 2);
     // this wave's private staging
-    Carver wv{cv.take(0) + (size_t)wave * jac_wave_doubles(P, W)};
+    Carver wv{cv.take(0) + (size_t)wave * jac_wave_doubles(P, W, ab)};
     double *YY = wv.take((size_t)W * 4 * L); // [e][S, dS/dx, dS/dy, dS/dz][L]
-    double2 *BB = (double2 *)wv.take(2 * (size_t)W * nl); // [e][n][l] = K_l (B, Bh)
-    double *XU = wv.take((size_t)W * jac_xu_doubles(P));
+    AT2 *BB = (AT2 *)wv.take(2 * (size_t)W * nl * ab / 8); // [e][n][l] = K_l (B, Bh)
+    double *XU = wv.take((size_t)W * jac_xu_doubles(P, ab));
     // precontraction results, aliasing the radial scratch: U2a[e][u][l] =
     // (U, Vx), U2b[e][u][l] = (Vy, Vz)
-    double2 *U2a = (double2 *)XU, *U2b = U2a + (size_t)W * Sn * lw;
+    AT2 *U2a = (AT2 *)XU, *U2b = U2a + (size_t)W * Sn * lw;
 
     for (int k = tid; k < tri_lw; k += BSJ) dtab[k] = P.dtab[k];
 
@@ -743,7 +763,7 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
             const int64_t base = rb0 + off;
             const double *geo = rgeo + 4 * off;
             const int *spc = rsp + off;
-            stage_edges<true>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw, true);
+            stage_edges<true, AT>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw, true);
 
             // ---- precontraction on the matrix cores ----
             // chunks j = (l, ch) in l-major order, operands loaded JB at a time
@@ -779,8 +799,8 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
                                 if (++ch == (l >> 1) + 1) {
                                     if (o_e < nb && uok) {
                                         const size_t qq = (size_t)(o_e * Sn + u) * lw + l;
-                                        U2a[qq] = make_double2(acc[0], acc[1]);
-                                        U2b[qq] = make_double2(acc[2], acc[3]);
+                                        U2a[qq] = Pair<AT>::make(acc[0], acc[1]);
+                                        U2b[qq] = Pair<AT>::make(acc[2], acc[3]);
                                     }
                                     acc = dbl4{0.0, 0.0, 0.0, 0.0};
                                     ch = 0;
@@ -796,9 +816,9 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
             // ---- assembly and stores ----
             for (int e = 0; e < nb; ++e) {
                 const int s = __builtin_amdgcn_readfirstlane(spc[e]);
-                const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
-                const double2 *Be = BB + (size_t)e * nl;
-                const double2 *Ua = U2a + (size_t)e * Sn * lw, *Ub = U2b + (size_t)e * Sn * lw;
+                const AT rx = (AT)geo[4 * e], ry = (AT)geo[4 * e + 1], rz = (AT)geo[4 * e + 2];
+                const AT2 *Be = BB + (size_t)e * nl;
+                const AT2 *Ua = U2a + (size_t)e * Sn * lw, *Ub = U2b + (size_t)e * Sn * lw;
                 OutT *o = jedge + (base + e) * 3 * Fe;
                 // pairs (mu, s), mu < s
                 if (s > 0) {
@@ -806,13 +826,13 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
                     for (int p = 0; p < JAC_MAX_NP; ++p) {
                         if (p >= NP || tp[p] >= nl) continue;
                         const int tt = tp[p], l = lp[p];
-                        const double2 bb = Be[tt];
-                        const double bhx = bb.y * rx, bhy = bb.y * ry, bhz = bb.y * rz;
+                        const AT2 bb = Be[tt];
+                        const AT bhx = bb.y * rx, bhy = bb.y * ry, bhz = bb.y * rz;
                         for (int mu = 0; mu < s; ++mu) {
-                            const double2 *Uma = Ua + mu * nl + l, *Umb = Ub + mu * nl + l;
+                            const AT2 *Uma = Ua + mu * nl + l, *Umb = Ub + mu * nl + l;
                             OutT *ob = o + mu * nnl;
                             for (int a = 0; a < n; ++a) {
-                                const double2 q0 = Uma[a * lw], q1 = Umb[a * lw];
+                                const AT2 q0 = Uma[a * lw], q1 = Umb[a * lw];
                                 store3(ob + a * nl, Fe, tt, q0.x * bhx + q0.y * bb.x, q0.x * bhy + q1.x * bb.x,
                                        q0.x * bhz + q1.y * bb.x);
                             }
@@ -822,13 +842,13 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
                 // diagonal pair (s, s), n' >= n, flat over (n, n', l)
                 {
                     OutT *ob = o + s * nnl;
-                    const double2 *Usa = Ua + s * nl, *Usb = Ub + s * nl;
+                    const AT2 *Usa = Ua + s * nl, *Usb = Ub + s * nl;
                     for (int f = lane; f < tri_lw; f += 64) {
                         const uint32_t d = dtab[f];
                         const int ta = d & 0xffff, tb = d >> 16; // n lw + l, n' lw + l
-                        const double2 A = Be[ta], B = Be[tb];
-                        const double2 a0 = Usa[ta], a1 = Usb[ta], b0 = Usa[tb], b1 = Usb[tb];
-                        const double hu = B.y * a0.x + A.y * b0.x;
+                        const AT2 A = Be[ta], B = Be[tb];
+                        const AT2 a0 = Usa[ta], a1 = Usb[ta], b0 = Usa[tb], b1 = Usb[tb];
+                        const AT hu = B.y * a0.x + A.y * b0.x;
                         store3(ob, Fe, f, hu * rx + (B.x * a0.y + A.x * b0.y), hu * ry + (B.x * a1.x + A.x * b1.x),
                                hu * rz + (B.x * a1.y + A.x * b1.y));
                     }
@@ -840,12 +860,12 @@ __global__ __launch_bounds__(BSJ) void k_jacobian(Params P, Rows R, const PosT *
                         if (p >= NP || tp[p] >= nl) continue;
                         const int tt = tp[p], l = lp[p];
                         for (int nu = s + 1; nu < S; ++nu) {
-                            const double2 q0 = Ua[nu * nl + tt], q1 = Ub[nu * nl + tt];
-                            const double ux = q0.x * rx, uy = q0.x * ry, uz = q0.x * rz;
+                            const AT2 q0 = Ua[nu * nl + tt], q1 = Ub[nu * nl + tt];
+                            const AT ux = q0.x * rx, uy = q0.x * ry, uz = q0.x * rz;
                             OutT *ob = o + s * nnl + tri_lw + (nu - s - 1) * nnl;
-                            const double2 *Bl = Be + l;
+                            const AT2 *Bl = Be + l;
                             for (int a = 0; a < n; ++a) {
-                                const double2 bb = Bl[a * lw];
+                                const AT2 bb = Bl[a * lw];
                                 store3(ob + a * nl, Fe, tt, bb.y * ux + bb.x * q0.y, bb.y * uy + bb.x * q1.x,
                                        bb.y * uz + bb.x * q1.y);
                             }
@@ -901,15 +921,23 @@ int density_blocks_per_cu(bool f64, bool jac, size_t lds) {
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
-size_t jacobian_lds_bytes(const Params &P, int W) {
+size_t jacobian_lds_bytes(const Params &P, int W, bool f64) {
+    const int ab = f64 ? 8 : 4;
     const size_t L = (size_t)P.L, Sn = (size_t)P.S * P.n;
     const int RBk = row_block(NWJ * W);
     size_t d = table_doubles(P, P.lmax + 1) + even(Sn * L) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               even(((size_t)P.tri_lw + 1) / 2) + NWJ * jac_wave_doubles(P, W);
+               even(((size_t)P.tri_lw + 1) / 2) + NWJ * jac_wave_doubles(P, W, ab);
     return d * 8;
 }
 
 int jacobian_max_w() { return JAC_MAX_W; }
+
+int jacobian_blocks_per_cu(bool f64, size_t lds) {
+    int nb = 0;
+    hipError_t e = f64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_jacobian<double, double>, BSJ, lds)
+                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_jacobian<float, float>, BSJ, lds);
+    return (e == hipSuccess && nb > 0) ? nb : 0;
+}
 
 hipError_t set_lds_limits() {
     const int lim = 159 * 1024; // the kernels' static LDS uses part of the 160 KB
