@@ -36,14 +36,24 @@ def _run(cmd):
     subprocess.check_call(cmd)
 
 
+# the float32 Jacobian kernel for fixed basis sizes, in parts built in parallel
+FIXED_SOURCE, FIXED_PARTS = "jacobian_fixed.hip", 3
+
+
 def build(verbose: bool = True) -> str:
+    from concurrent.futures import ThreadPoolExecutor
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
+    jobs = []
     for src in HIP_SOURCES + HIP_HOST_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         lang = [] if src.endswith(".hip") else ["-x", "hip"]
-        _run([HIPCC, *HIP_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj])
-        objs.append(obj)
+        jobs.append((obj, [HIPCC, *HIP_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]))
+    for part in range(FIXED_PARTS):
+        obj = os.path.join(BUILD, f"{FIXED_SOURCE}.{part}.o")
+        jobs.append((obj, [HIPCC, *HIP_FLAGS, f"-DJF_PART={part}", "-c", os.path.join(CSRC, FIXED_SOURCE), "-o", obj]))
+    with ThreadPoolExecutor(max_workers=min(len(jobs), os.cpu_count() or 1)) as ex:
+        list(ex.map(lambda j: _run(j[1]), jobs))
+    objs = [j[0] for j in jobs]
     for src in HOST_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         _run(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])

@@ -198,7 +198,7 @@ int plan_launches(soap_ctx *c) {
     for (int W = jacobian_max_w(); W >= 1; --W) {
         const size_t lds = jacobian_lds_bytes(P, W, f64);
         if (lds > LDS_HARD_LIMIT) continue;
-        const int b = jacobian_blocks_per_cu(f64, lds);
+        const int b = jacobian_blocks_per_cu(f64, P.n, P.lmax + 1, lds);
         if (b > bestB) {
             bestB = b;
             bestW = W;

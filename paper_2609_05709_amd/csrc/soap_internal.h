@@ -79,7 +79,11 @@ int density_blocks_per_cu(bool f64, bool jac, size_t lds);
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
 int jacobian_max_w();
-int jacobian_blocks_per_cu(bool f64, size_t lds); // resident workgroups per CU (0 if it does not fit)
+int jacobian_blocks_per_cu(bool f64, int n, int lw, size_t lds); // resident workgroups per CU (0 if it does not fit)
+// float32 Jacobian kernels for fixed (n_max, l_max + 1); NULL if not compiled
+const void *jacobian_fixed_0(int n, int lw);
+const void *jacobian_fixed_1(int n, int lw);
+const void *jacobian_fixed_2(int n, int lw);
 hipError_t set_lds_limits();
 
 // desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)

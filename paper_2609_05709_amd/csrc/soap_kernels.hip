@@ -1,904 +1,9 @@
-// SOAP descriptor and Jacobian kernels for gfx950 (wave64).
-//
-// Both kernels evaluate, per directed edge e = (i -> j) with r = r_j - r_i
-// formed in float64 (exact for float32 inputs):
-//   * real solid harmonics S_lm(r) = r^l Y_lm(r_hat) by a division-free
-//     column recurrence, and their Cartesian gradients from the degree l-1
-//     harmonics (stage_edges);
-//   * radial factors B_nl(r) and Bh_nl(r) = (1/r) dB_nl/dr such that the
-//     edge's contribution to the coefficients is c_nlm += B_nl S_lm and its
-//     gradient is dc_nlm/dr_j = Bh_nl r S_lm + B_nl grad S_lm:
-//       GTO (Eq. gto-coefficients, gto-derivative):
-//         B_nl = sum_k betaC^l_nk exp(-a'_kl r^2),  Bh_nl = -2 sum_k betaC a' exp(..)
-//       polynomial (Eq. poly-coefficients-exact with Gauss-Legendre, and the
-//         chain rule Eq. poly-cartesian-derivative written for S_lm):
-//         B_nl  = r^-l sum_q G_nq e^{-(r_q-r)^2/2s^2} ii_l(r_q r/s^2)
-//         Bh_nl = r^-(l+1) / s^2 sum_q G_nq e^{-(r_q-r)^2/2s^2} (r_q ii_{l+1} - r ii_l)
-//       with ii_l(x) = e^-x i_l(x) and d/dx (x^-l i_l) = x^-l i_{l+1}.
-//
-// k_density: persistent workgroups, each bound to one l-group and taking
-//   centers from a counter.  Accumulates c (and, for the Jacobian, D = sum
-//   over edges of dc, i.e. minus the derivative of c with respect to the
-//   center), then writes the power spectrum Eq. (powerspectrum) and the
-//   center's own Jacobian block -K_l sum_m (D^mu c^nu + c^mu D^nu)
-//   (Eq. powerspectrum-derivative with translational invariance).  c goes to
-//   a float64 scratch for k_jacobian.
-// k_jacobian: one workgroup per center; per edge the precontraction
-//   U = sum_m S_lm c, V = sum_m grad S_lm c on the matrix cores, then the
-//   neighbour block from U, V, B, Bh (see the kernel).
-// All arithmetic is float64; outputs are converted once at the store.
-#include "soap_internal.h"
-
-#include <algorithm>
+// Host side of the SOAP kernels: launch configuration and launches.  The
+// device code is in soap_device.h.
+#include "soap_device.h"
 
 namespace soap {
-namespace {
-
-// Output stores are plain (write-back) stores: on this chip non-temporal
-// stores of the neighbour blocks' partial-line runs write back at about half
-// the bandwidth.
-template <typename T> __device__ __forceinline__ void store_out(T *p, double v) { *p = (T)v; }
-__device__ __forceinline__ void store_out(float *p, float v) { *p = v; }
-
-// (value, companion) pairs in LDS at the precision T
-template <typename T> struct Pair;
-template <> struct Pair<double> {
-    using type = double2;
-    static __device__ __forceinline__ double2 make(double a, double b) { return make_double2(a, b); }
-};
-template <> struct Pair<float> {
-    using type = float2;
-    static __device__ __forceinline__ float2 make(double a, double b) { return make_float2((float)a, (float)b); }
-};
-
-// floor(x / d) for 0 <= x < 2^22 with inv = 1/d correctly rounded: the
-// relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
-// next integer
-__device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x + 0.5f) * inv); }
-
-// ---------------------------------------------------------------------------
-// Real solid harmonics of one column m without gradients and without
-// divisions.  With (C_m + i S_m) = (x + i y)^m, R_m = 1, R_{m+1} = (2m+1) z,
-//   R_l = (2l-1) z R_{l-1} - (l+m-1)(l-m-1) r^2 R_{l-2},
-// the associated Legendre part is Q_l^m = (2m-1)!! R_l / (l-m)!, so
-//   S_l,m = Nt_lm R_l C_m, S_l,-m = Nt_lm R_l S_m, Nt_lm = N_lm (2m-1)!! / (l-m)!.
-// Stores l in [l_lo, l_hi) at Y[(l^2 + l +- m - lm_base) * ls].
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void sh_col_y(int m, int l_lo, int l_hi, double x, double y, double z,
-                                         const double *__restrict__ Nt, int ldN, double *__restrict__ Y, int ls,
-                                         int lm_base) {
-    const double r2 = x * x + y * y + z * z;
-    double c = 1.0, s = 0.0;
-    for (int k = 0; k < m; ++k) {
-        const double cn = x * c - y * s;
-        s = x * s + y * c;
-        c = cn;
-    }
-    double R1 = 0.0, R = 1.0; // R_{l-1}, R_l
-    for (int l = m; l < l_hi; ++l) {
-        if (l > m) {
-            const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
-            const double Rn = a * z * R - b * r2 * R1;
-            R1 = R;
-            R = Rn;
-        }
-        if (l >= l_lo) {
-            const double v = Nt[l * ldN + m] * R;
-            const int o = l * l + l - lm_base;
-            if (m == 0) {
-                Y[o * ls] = v;
-            } else {
-                Y[(o + m) * ls] = v * c;
-                Y[(o - m) * ls] = v * s;
-            }
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Scaled modified spherical Bessel functions ii_l(x) = e^-x i_l(x), l = 0..Lt.
-// x >= Lt(Lt+1)/6.9: upward recurrence from the closed forms of ii_0, ii_1
-//   (error growth bounded by about e^{Lt(Lt+1)/x} <= 1e3);
-// otherwise: power series for the two highest orders (positive terms),
-//   i_l(x) = x^l sum_k (x^2/2)^k / (k! (2l+2k+1)!!), then the downward
-//   recurrence i_{l-1} = i_{l+1} + (2l+1)/x i_l (stable downward).
-// ---------------------------------------------------------------------------
-__device__ double bessel_series_scaled(int l, double x) {
-    double t = 1.0;
-    for (int k = 0; k < l; ++k) t *= x / (double)(2 * k + 3);
-    t /= 1.0; // x^l / (2l+1)!! built as prod x/(2k+3) times 1/1
-    double s = t;
-    const double h = 0.5 * x * x;
-    for (int k = 1; k < 400; ++k) {
-        t *= h / ((double)k * (double)(2 * l + 2 * k + 1));
-        s += t;
-        if (t < 1e-17 * s && (double)k * (double)(2 * l + 2 * k + 1) > h) break;
-    }
-    return s * exp(-x);
-}
-
-// Writes ii_l(x) * g for l = 0..Lt to t[0..Lt] (LDS).
-__device__ __forceinline__ void bessel_scaled_lds(int Lt, double x, double g, double *t) {
-    if (x == 0.0) {
-        t[0] = g;
-        for (int k = 1; k <= Lt; ++k) t[k] = 0.0;
-        return;
-    }
-    const double ix = 1.0 / x;
-    if (x * 6.9 >= (double)(Lt * (Lt + 1))) {
-        const double em = exp(-2.0 * x);
-        double a = 0.5 * (1.0 - em) * ix;              // ii_0
-        double b = 0.5 * (1.0 + em) * ix - a * ix;     // ii_1
-        t[0] = g * a;
-        if (Lt >= 1) t[1] = g * b;
-        for (int k = 1; k < Lt; ++k) {
-            const double c = a - (double)(2 * k + 1) * ix * b;
-            t[k + 1] = g * c;
-            a = b;
-            b = c;
-        }
-    } else {
-        double b = bessel_series_scaled(Lt, x);                     // ii_Lt
-        double a = (Lt >= 1) ? bessel_series_scaled(Lt - 1, x) : 0; // ii_{Lt-1}
-        t[Lt] = g * b;
-        if (Lt >= 1) t[Lt - 1] = g * a;
-        for (int k = Lt - 1; k >= 1; --k) {
-            const double c = b + (double)(2 * k + 1) * ix * a;      // ii_{k-1}
-            t[k - 1] = g * c;
-            b = a;
-            a = c;
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// LDS layout helpers.  Every region starts on a 16-byte boundary.
-// ---------------------------------------------------------------------------
-__host__ __device__ __forceinline__ size_t even(size_t nd) { return (nd + 1) & ~(size_t)1; }
-
-struct Carver {
-    double *base;
-    size_t off = 0;
-    __device__ __forceinline__ double *take(size_t nd) {
-        double *p = base + off;
-        off += even(nd);
-        return p;
-    }
-};
-
-// Neighbour rows are prefetched into LDS in blocks of row_block(EC) edges.
-__host__ __device__ __forceinline__ int row_block(int EC) { return EC >= 128 ? EC : EC * (128 / EC); }
-
-// Basis tables copied to LDS once per workgroup (for l in [lg0, lg1)), so
-// that no global load sits on the per-edge path: with the chip's store
-// traffic in flight, global load latency runs to microseconds.
-struct Tables {
-    const double *Kl;      // K_l = pi sqrt(8/(2l+1)), l < 16
-    const double2 *bcp;    // GTO: [k][n][lc] = (betaC, -2 betaC a') of B_nl = sum_k betaC_nk e^{-a'_kl r^2}
-    const double *aprime;  // GTO: [k][lc]
-    const double *G, *rq;  // polynomial: [n][Q], [Q]
-    const double *Nt;      // [ldN][ldN] N_lm (2m-1)!! / (l-m)!, for sh_col_y
-    const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_edges
-};
-
-__host__ __device__ __forceinline__ int grad_pairs(int lmax) { return (lmax + 1) * (lmax + 2) / 2; }
-
-__host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lgc) {
-    const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
-    size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
-    if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
-    else d += even(n * P.Q) + even((size_t)P.Q);
-    return d;
-}
-
-__device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables &T, int lg0, int lg1) {
-    const int ldN = P.lmax + 2, n = P.n, lgc = lg1 - lg0, tid = threadIdx.x, bs = blockDim.x;
-    // every pointer is assigned on every path, so the struct stays in
-    // registers and the compiler keeps LDS (ds_*) addressing for it
-    double *Kl = cv.take(16);
-    double *Ntl = cv.take((size_t)ldN * ldN);
-    double *gc = cv.take(4 * (size_t)grad_pairs(P.lmax));
-    const bool poly = P.rbf != 0;
-    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    const size_t szA = poly ? (size_t)n * P.Q : 2 * (size_t)lgc * n * n; // (betaC, betaCa) pairs | G
-    const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n;              // aprime | rq
-    double *A = cv.take(szA), *B = cv.take(szB);
-    for (int k = tid; k < ldN * ldN; k += bs) Ntl[k] = P.Nt[k];
-    for (int k = tid; k < 4 * grad_pairs(P.lmax); k += bs) gc[k] = P.gcoef[k];
-    if (!poly) {
-        // global [l][n][k] -> LDS [k][n][lc]; global [l][k] -> LDS [k][lc]
-        const size_t o = (size_t)lg0 * n * n;
-        for (int s = tid; s < (int)(szA / 2); s += bs) {
-            const int lc = s / (n * n), r = s - lc * n * n, a = r / n, k = r - a * n;
-            const int d = (k * n + a) * lgc + lc;
-            A[2 * d] = P.betaC[o + s];
-            A[2 * d + 1] = P.betaCa[o + s];
-        }
-        for (int s = tid; s < (int)szB; s += bs) {
-            const int lc = s / n, k = s - lc * n;
-            B[k * lgc + lc] = P.aprime[(size_t)lg0 * n + s];
-        }
-    } else {
-        for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
-        for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
-    }
-    T.Kl = Kl;
-    T.Nt = Ntl;
-    T.gcoef = (const double2 *)gc;
-    T.bcp = (const double2 *)A;
-    T.G = A;
-    T.aprime = B;
-    T.rq = B;
-}
-
-// X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
-// Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place)
-__host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int lgc, int lg1) {
-    return P.rbf ? (size_t)P.Q * (lg1 + 1) : (size_t)P.n * lgc;
-}
-
-// Synchronisation inside one wave: LDS writes become visible to the other
-// lanes and the compiler keeps LDS accesses on their side of the point.
-__device__ __forceinline__ void wave_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-}
-
-// Workgroup barrier ordering LDS only.  __syncthreads() also fences global
-// memory, which makes every wave wait for all of its outstanding output
-// stores; nothing here reads another wave's global writes, so the output
-// stream keeps flowing across the barrier.
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// ---------------------------------------------------------------------------
-// Per-tile edge staging (one wave, nb edges), shared by both kernels, for
-// l in [lg0, lg1).
-//   YY: harmonics, element (edge e, component c, lm) at
-//       e es + c cs + (lm - lmY0) ls; component 0 = S, 1..3 = dS/dx_d (GRAD).
-//       Degrees from lgY0 = lg0 - 1 (GRAD and lg0 > 0) or lg0 are stored.
-//   BB[e][n][lc] = K (B_nl, Bh_nl), K = K_l if scaleK else 1, stored at precision BT
-//   X: GTO exponentials [e][k][lc], or the polynomial table [e][q][0..lg1]
-// Phase 1 runs the harmonic columns (edge, m), then the radial scratch;
-// phase 2 the gradients, then the radial factors.  Each gradient component
-// is at most two degree l-1 harmonics: with H_l^m = (x + iy)^m Q_l^m (so
-// S_l,m = N_lm Re H, S_l,-m = N_lm Im H),
-//   d/dz H_l^m = (l+m) H_{l-1}^m,  (d/dx + i d/dy) H_l^m = -H_{l-1}^{m+1},
-//   (d/dx - i d/dy) H_l^m = (l+m)(l+m-1) H_{l-1}^{m-1}.
-// Per (l, m >= 0), with S' = S_{l-1,.} and gcoef = (cA, cB, cC):
-//   m = 0:  grad S_l0 = (-cA S'_1, -cA S'_-1, cC S'_0)
-//   m > 0:  grad S_lm  = (-cA S'_{m+1} + cB S'_{m-1}, -cA S'_{-(m+1)} - cB S'_{-(m-1)}, cC S'_m)
-//           grad S_l-m = (-cA S'_{-(m+1)} + cB S'_{-(m-1)}, cA S'_{m+1} + cB S'_{m-1}, cC S'_-m)
-// (S'_k = 0 for |k| > l-1, S'_-0 = 0).  A zero-length edge gets a zero gradient.
-// ---------------------------------------------------------------------------
-struct YLayout {
-    int es, cs, ls, lmY0;
-};
-
-template <bool GRAD, typename BT = double>
-__device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, double *__restrict__ YY, YLayout yl,
-                                            typename Pair<BT>::type *__restrict__ BB, double *__restrict__ X,
-                                            const double *__restrict__ geo, int nb, int lane, int lg0, int lg1,
-                                            bool scaleK) {
-    const int n = P.n, ldN = P.lmax + 2, lgc = lg1 - lg0, nlc = n * lgc;
-    const int lgY0 = (GRAD && lg0 > 0) ? lg0 - 1 : lg0;
-    const float inv_lg1 = 1.0f / (float)lg1, inv_nlc = 1.0f / (float)nlc, inv_lgc = 1.0f / (float)lgc;
-    const bool poly = P.rbf != 0;
-    const int Q = P.Q, tw = lg1 + 1;
-    const float inv_Q = 1.0f / (float)Q;
-    // phase 1: harmonic columns (edge, m), then the radial scratch (two
-    // independent exponentials per lane trip)
-    for (int it = lane; it < nb * lg1; it += 64) {
-        const int e = qdiv(it, inv_lg1), m = it - e * lg1;
-        const double *g = geo + 4 * e;
-        sh_col_y(m, m > lgY0 ? m : lgY0, lg1, g[0], g[1], g[2], T.Nt, ldN, YY + e * yl.es, yl.ls, yl.lmY0);
-    }
-    if (!poly) {
-        const int nx = nb * nlc;
-        for (int it = lane; it < nx; it += 128) {
-            const int i2 = it + 64 < nx ? it + 64 : it;
-            const int e1 = qdiv(it, inv_nlc), e2 = qdiv(i2, inv_nlc);
-            const double r1 = geo[4 * e1 + 3], r2 = geo[4 * e2 + 3];
-            const double v1 = exp(-T.aprime[it - e1 * nlc] * r1 * r1), v2 = exp(-T.aprime[i2 - e2 * nlc] * r2 * r2);
-            X[it] = v1;
-            X[i2] = v2;
-        }
-    } else {
-        for (int it = lane; it < nb * Q; it += 64) {
-            const int e = qdiv(it, inv_Q), q = it - e * Q;
-            const double r = geo[4 * e + 3], rq = T.rq[q];
-            const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
-            bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
-        }
-    }
-    wave_sync();
-    // phase 2: gradients (edge, (l, m >= 0)), then the radial factors (edge, n, lc)
-    if (GRAD) {
-        const int t0 = lg0 * (lg0 + 1) / 2, Tg = lg1 * (lg1 + 1) / 2 - t0;
-        const float inv_T = 1.0f / (float)Tg;
-        for (int it = lane; it < nb * Tg; it += 64) {
-            const int e = qdiv(it, inv_T), t = it - e * Tg + t0;
-            const double2 c01 = T.gcoef[2 * t], c2p = T.gcoef[2 * t + 1];
-            const int lm = (int)c2p.y, l = lm & 0xff, m = lm >> 8;
-            double *Y = YY + e * yl.es;
-            const int lp = l > 0 ? l - 1 : 0, c0 = lp * lp + lp - yl.lmY0;
-            const bool live = geo[4 * e + 3] != 0.0 && l > 0;
-            // S'_k for k in {m+1, -(m+1), m-1, -(m-1), m, -m}, clamped into degree l-1
-            auto sp = [&](int k) -> double {
-                const int kc = k < -lp ? -lp : (k > lp ? lp : k);
-                const double v = Y[(c0 + kc) * yl.ls];
-                return (live && k >= -lp && k <= lp) ? v : 0.0;
-            };
-            const double cA = c01.x, cB = c01.y, cC = c2p.x;
-            double *Dx = Y + yl.cs, *Dy = Y + 2 * yl.cs, *Dz = Y + 3 * yl.cs;
-            const int o = l * l + l - yl.lmY0;
-            if (m == 0) {
-                Dx[o * yl.ls] = -cA * sp(1);
-                Dy[o * yl.ls] = -cA * sp(-1);
-                Dz[o * yl.ls] = cC * sp(0);
-            } else {
-                const double pp = sp(m + 1), pn = sp(-(m + 1)), qp = sp(m - 1), qn = m > 1 ? sp(-(m - 1)) : 0.0;
-                const double zp = sp(m), zn = sp(-m);
-                Dx[(o + m) * yl.ls] = -cA * pp + cB * qp;
-                Dy[(o + m) * yl.ls] = -cA * pn - cB * qn;
-                Dz[(o + m) * yl.ls] = cC * zp;
-                Dx[(o - m) * yl.ls] = -cA * pn + cB * qn;
-                Dy[(o - m) * yl.ls] = cA * pp + cB * qp;
-                Dz[(o - m) * yl.ls] = cC * zn;
-            }
-        }
-    }
-    const int nd = nb * nlc;
-    if (!poly) {
-        for (int it = lane; it < nd; it += 128) {
-            const int i2 = it + 64 < nd ? it + 64 : it;
-            const int e1 = qdiv(it, inv_nlc), t1 = it - e1 * nlc, l1 = t1 - qdiv(t1, inv_lgc) * lgc;
-            const int e2 = qdiv(i2, inv_nlc), t2 = i2 - e2 * nlc, l2 = t2 - qdiv(t2, inv_lgc) * lgc;
-            const double2 *bc1 = T.bcp + t1, *bc2 = T.bcp + t2; // [k][n][lc]: t = a lgc + lc
-            const double *E1 = X + (size_t)e1 * nlc + l1, *E2 = X + (size_t)e2 * nlc + l2;
-            double b1 = 0.0, h1 = 0.0, b2 = 0.0, h2 = 0.0;
-#pragma unroll 2
-            for (int k = 0; k < n; ++k) {
-                const double2 c1 = bc1[k * nlc], c2 = bc2[k * nlc];
-                const double v1 = E1[k * lgc], v2 = E2[k * lgc];
-                b1 += c1.x * v1;
-                h1 += c1.y * v1;
-                b2 += c2.x * v2;
-                h2 += c2.y * v2;
-            }
-            const double K1 = scaleK ? T.Kl[lg0 + l1] : 1.0, K2 = scaleK ? T.Kl[lg0 + l2] : 1.0;
-            BB[it] = Pair<BT>::make(K1 * b1, K1 * h1);
-            BB[i2] = Pair<BT>::make(K2 * b2, K2 * h2);
-        }
-    } else {
-        for (int it = lane; it < nd; it += 64) {
-            const int e = qdiv(it, inv_nlc), t = it - e * nlc, a = qdiv(t, inv_lgc), l = lg0 + t - a * lgc;
-            const double r = geo[4 * e + 3];
-            const double *G = T.G + (size_t)a * Q;
-            const double *tq = X + (size_t)e * Q * tw;
-            double b = 0.0, bh = 0.0;
-            for (int q = 0; q < Q; ++q) {
-                const double tl = tq[q * tw + l];
-                b += G[q] * tl;
-                if (GRAD) bh += G[q] * (T.rq[q] * tq[q * tw + l + 1] - r * tl);
-            }
-            if (r == 0.0) {
-                b = (l == 0) ? b : 0.0;
-                bh = 0.0;
-            } else {
-                double ir = 1.0 / r, rl = 1.0;
-                for (int k = 0; k < l; ++k) rl *= ir;
-                b *= rl;
-                bh *= rl * ir * P.inv_s2;
-            }
-            const double K = scaleK ? T.Kl[l] : 1.0;
-            BB[it] = Pair<BT>::make(K * b, K * bh);
-        }
-    }
-    wave_sync();
-}
-
-// Prefetch the rows [r0, r0+cnt) of the center: edge vectors r_j - r_i in
-// float64 (exact for float32 inputs), |r|, species.
-template <typename PosT>
-__device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__restrict__ pos,
-                                          const uint8_t *__restrict__ spec, const int32_t *__restrict__ cols,
-                                          int64_t r0, int cnt, double3 pi) {
-    for (int t = threadIdx.x; t < cnt; t += blockDim.x) {
-        const int64_t j = cols[r0 + t];
-        const double x = (double)pos[3 * j] - pi.x, y = (double)pos[3 * j + 1] - pi.y,
-                     z = (double)pos[3 * j + 2] - pi.z;
-        geo[4 * t] = x;
-        geo[4 * t + 1] = y;
-        geo[4 * t + 2] = z;
-        geo[4 * t + 3] = sqrt(x * x + y * y + z * z);
-        sp[t] = spec[j];
-    }
-}
-
-// ---------------------------------------------------------------------------
-// k_density
-//
-// Persistent: a workgroup is bound to one l-group g (blockIdx % G), keeps
-// that group's basis tables in LDS, and takes centers from an atomic work
-// counter.  Per center, each wave runs its own tiles of W edges: staging
-// (harmonics, gradients, radial factors) in the wave's LDS, then every lane
-// adds each edge's contribution to the coefficient entries (a, lm) it owns,
-// in registers that persist over the wave's tiles:
-//   c^s_{a lm} += B_al S_lm,
-//   D^s_{a lm} += Bh_al r S_lm + B_al grad S_lm
-// (D = sum over neighbours of dc/dr_j = -dc/dr_i).  Rows are sorted by
-// species, so the registers are flushed into the shared LDS accumulators
-// (float64 LDS atomics) only when the species changes and at the end.  Then
-// the whole workgroup writes the power spectrum and the center block
-// -K_l sum_m (D^mu c^nu + c^mu D^nu).
-// ---------------------------------------------------------------------------
-constexpr int NWD = 4, BSD = 64 * NWD;
-constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 64 * KE
-
-__host__ __device__ __forceinline__ int dens_lgY0(int jac, int lg0) { return (jac && lg0 > 0) ? lg0 - 1 : lg0; }
-
-__host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, int jac, int lg0, int lg1, int W) {
-    const int lgY0 = dens_lgY0(jac, lg0);
-    const size_t LY = (size_t)(lg1 * lg1 - lgY0 * lgY0), lgc = (size_t)(lg1 - lg0);
-    return even(W * LY * (jac ? 4 : 1)) + 2 * W * P.n * lgc + even(W * stage_x_doubles(P, (int)lgc, lg1));
-}
-
-template <typename PosT, typename OutT, bool JAC>
-__global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
-                                                 int *__restrict__ work, OutT *__restrict__ desc,
-                                                 OutT *__restrict__ c_out, OutT *__restrict__ jself,
-                                                 double *__restrict__ c_scratch) {
-    // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
-    extern __shared__ __align__(16) double smem[];
-    __shared__ int64_t s_next;
-    const int G = P.n_groups;
-    const int g = blockIdx.x % G;
-    const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0;
-    const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
-    const int lgY0 = dens_lgY0(JAC, lg0), lmY0 = lgY0 * lgY0, LY = lg1 * lg1 - lmY0;
-    const int S = P.S, n = P.n, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int nL = n * Lg, SnL = S * nL, lw = P.lmax + 1, Lfull = P.L, Sn = S * n, nlc = n * lgc;
-    const int RBk = row_block(NWD * W);
-
-    Carver cv{smem};
-    Tables T;
-    load_tables(P, cv, T, lg0, lg1);
-    double *cacc = cv.take((size_t)SnL * (JAC ? 4 : 1)); // [s][a][lmg], then D [3][s][a][lmg]
-    double *Dacc = cacc + SnL;
-    double *rgeo = cv.take(4 * (size_t)RBk);
-    int *rsp = (int *)cv.take((RBk + 1) / 2);
-    uint32_t *fq = (uint32_t *)cv.take(((size_t)P.nq_full + 1) / 2);
-    double *c0 = cv.take((size_t)n);
-    Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W)};
-    // harmonics interleaved per lm as (S, dS/dx, dS/dy, dS/dz) for the Jacobian
-    const YLayout yl = JAC ? YLayout{4 * LY, 1, 4, lmY0} : YLayout{LY, 0, 1, lmY0};
-    double *YY = wv.take((size_t)W * yl.es);
-    double2 *BB = (double2 *)wv.take(2 * (size_t)W * nlc);
-    double *X = wv.take((size_t)W * stage_x_doubles(P, lgc, lg1));
-
-    // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg
-    int oY[KE], oB[KE];
-    bool own[KE];
-#pragma unroll
-    for (int k = 0; k < KE; ++k) {
-        const int e = lane + 64 * k;
-        own[k] = e < nL;
-        const int a = e / Lg, lmg = e - a * Lg;
-        const int lm = lm0 + (own[k] ? lmg : 0);
-        int l = (int)sqrtf((float)lm);
-        while (l * l > lm) --l;
-        while ((l + 1) * (l + 1) <= lm) ++l;
-        oY[k] = (lm - lmY0) * (JAC ? 4 : 1);
-        oB[k] = own[k] ? a * lgc + (l - lg0) : 0;
-    }
-
-    // per-basis tables used by the outputs, in LDS: no global load may sit
-    // between output stores (vmcnt counts loads and stores together)
-    for (int k = tid; k < P.nq_full; k += BSD) fq[k] = P.fq[k];
-    for (int k = tid; k < n; k += BSD) c0[k] = P.c0[k];
-
-    // the next center: its rows are loaded before the current center's
-    // outputs are stored, so those loads never wait behind the stores
-    int64_t ci = 0, i = 0, e0 = 0, e1 = 0;
-    int spec_i = 0;
-    double3 pi = make_double3(0.0, 0.0, 0.0);
-    auto fetch = [&]() {
-        if (tid == 0) s_next = atomicAdd(&work[g], 1);
-        lds_barrier();
-        ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
-        lds_barrier(); // s_next is rewritten by the next fetch
-        if (ci >= R.nc) return;
-        i = R.centers ? (int64_t)R.centers[ci] : ci;
-        pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
-        spec_i = R.spec[i];
-        e0 = R.row_ptr[ci];
-        e1 = R.row_ptr[ci + 1];
-        const int64_t cnt = (e1 - e0) < RBk ? (e1 - e0) : RBk;
-        load_rows(rgeo, rsp, pos, R.spec, R.cols, e0, (int)cnt, pi);
-    };
-    fetch();
-    const float inv_lgc = 1.0f / (float)lgc, inv_qlgc = 1.0f / (float)(P.nq_full * lgc), inv_Lg = 1.0f / (float)Lg;
-
-    while (ci < R.nc) {
-        for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BSD) cacc[k] = 0.0;
-        lds_barrier(); // rows of this center and the cleared accumulators
-
-        double acc[KE][4];
-#pragma unroll
-        for (int k = 0; k < KE; ++k) acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
-        int cur = -1; // species of the registers' edges
-        auto flush = [&]() {
-#pragma unroll
-            for (int k = 0; k < KE; ++k) {
-                if (!own[k]) continue;
-                const int idx = cur * nL + lane + 64 * k;
-                atomicAdd(&cacc[idx], acc[k][0]);
-                if (JAC) {
-                    atomicAdd(&Dacc[idx], acc[k][1]);
-                    atomicAdd(&Dacc[SnL + idx], acc[k][2]);
-                    atomicAdd(&Dacc[2 * SnL + idx], acc[k][3]);
-                }
-                acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
-            }
-        };
-
-        for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
-            const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
-            if (rb0 != e0) { // further row blocks of a long row (no output stores are pending here)
-                lds_barrier();
-                load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
-                lds_barrier();
-            }
-            for (int off = wave * W; off < rbn; off += NWD * W) {
-                const int nb = (rbn - off) < W ? (rbn - off) : W;
-                const double *geo = rgeo + 4 * off;
-                stage_edges<JAC>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
-                for (int e = 0; e < nb; ++e) {
-                    const int s = __builtin_amdgcn_readfirstlane(rsp[off + e]);
-                    if (s != cur) {
-                        if (cur >= 0) flush();
-                        cur = s;
-                    }
-                    const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
-                    const double *Ye = YY + e * yl.es;
-                    const double2 *Be = BB + e * nlc;
-#pragma unroll
-                    for (int k = 0; k < KE; ++k) {
-                        if (!own[k]) continue;
-                        const double2 bb = Be[oB[k]];
-                        if (JAC) {
-                            const double2 y01 = *(const double2 *)(Ye + oY[k]), y23 = *(const double2 *)(Ye + oY[k] + 2);
-                            const double bh = bb.y * y01.x;
-                            acc[k][0] += bb.x * y01.x;
-                            acc[k][1] += bh * rx + bb.x * y01.y;
-                            acc[k][2] += bh * ry + bb.x * y23.x;
-                            acc[k][3] += bh * rz + bb.x * y23.y;
-                        } else {
-                            acc[k][0] += bb.x * Ye[oY[k]];
-                        }
-                    }
-                }
-                wave_sync(); // the next tile's staging overwrites YY and BB
-            }
-        }
-        if (cur >= 0) flush();
-        lds_barrier();
-        // on-site term of the center (its species, l = 0)
-        if (lg0 == 0)
-            for (int a = tid; a < n; a += BSD) cacc[spec_i * nL + a * Lg] += c0[a];
-        // the next center's rows go in while this center's outputs are written
-        const int64_t cw = ci;
-        fetch(); // its barriers also publish the on-site term
-        // power spectrum for the group's l
-        if (desc)
-            for (int it = tid; it < P.nq_full * lgc; it += BSD) {
-                const int q = qdiv(it, inv_lgc), lc = it - q * lgc, l = lg0 + lc;
-                const uint32_t f = fq[q];
-                const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
-                const double *x = cacc + mu * nL + a * Lg + l * l - lm0;
-                const double *y = cacc + nu * nL + b * Lg + l * l - lm0;
-                double sum = 0.0;
-                for (int m = 0; m < 2 * l + 1; ++m) sum += x[m] * y[m];
-                store_out(desc + cw * P.F + q * lw + l, T.Kl[l] * sum);
-            }
-        if (c_out)
-            for (int it = tid; it < SnL; it += BSD) {
-                const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
-                store_out(c_out + (cw * Sn + sa) * Lfull + lm0 + lmg, cacc[it]);
-            }
-        if (JAC) {
-            // c, transposed to [lm][s n] for the Jacobian kernel's matrix-core operand
-            for (int it = tid; it < SnL; it += BSD) {
-                const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
-                c_scratch[(cw * Lfull + lm0 + lmg) * Sn + sa] = cacc[it];
-            }
-            for (int it = tid; it < 3 * P.nq_full * lgc; it += BSD) {
-                const int d = qdiv(it, inv_qlgc), rem = it - d * (P.nq_full * lgc);
-                const int q = qdiv(rem, inv_lgc), lc = rem - q * lgc, l = lg0 + lc;
-                const uint32_t f = fq[q];
-                const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
-                const int oa = mu * nL + a * Lg + l * l - lm0, ob = nu * nL + b * Lg + l * l - lm0;
-                const double *Dd = Dacc + d * SnL;
-                double sum = 0.0;
-                for (int m = 0; m < 2 * l + 1; ++m) sum += Dd[oa + m] * cacc[ob + m] + cacc[oa + m] * Dd[ob + m];
-                store_out(jself + (cw * 3 + d) * P.F + q * lw + l, -T.Kl[l] * sum);
-            }
-        }
-        lds_barrier(); // the outputs are read from cacc before the next center clears it
-    }
-}
-
-// ---------------------------------------------------------------------------
-// k_jacobian
-//
-// One workgroup of NWJ waves per center.  The workgroup shares the basis
-// tables, the center's coefficients (transposed, cT[lm][u], u = species * n
-// + n') and the prefetched neighbour rows; each wave then runs its own
-// pipeline over tiles of W <= 4 edges, synchronising only within the wave:
-//
-//   1. harmonics S_lm and grad S_lm, radial factors K_l B_nl and K_l Bh_nl;
-//   2. the precontraction U^u_l = sum_m S_lm c^u_lm, V^u_l = sum_m grad S_lm
-//      c^u_lm on the matrix cores: per l, a 16 x 16 x 4 float64 MFMA chain
-//      with A rows (component, edge) = (S, dS/dx, dS/dy, dS/dz) of up to four
-//      edges, K = m (2l + 1 padded to a multiple of 4), B columns = u;
-//   3. assembly of the neighbour block of each edge j (species s), whose
-//      slots are the features with s in their species pair, in feature
-//      order: pairs (mu, s), mu < s; the diagonal pair (s, s), n' >= n;
-//      pairs (s, nu), nu > s.  With r = r_j - r_i,
-//        (mu, s):  K_l [U^mu_nl Bh_n'l r + V^mu_nl B_n'l]
-//        (s, nu):  K_l [Bh_nl r U^nu_n'l + B_nl V^nu_n'l]
-//        (s, s):   both of the above with mu = nu = s
-//      (Eq. powerspectrum-derivative).  On the off-diagonal pairs a lane owns
-//      one (n', l) and walks n, so consecutive lanes store consecutive
-//      floats; the diagonal triangle is walked flat with a decode table.
-// ---------------------------------------------------------------------------
-constexpr int NWJ = 4, BSJ = 64 * NWJ;
-constexpr int JAC_MAX_W = 4;  // edges per MFMA tile: A rows are (component, edge)
-constexpr int JAC_MAX_NP = 4; // lanes passes over (n', l): n * (l_max + 1) <= 256
-constexpr int JB = 8;         // MFMA operand pairs loaded ahead of their chain
-
-typedef double dbl4 __attribute__((ext_vector_type(4)));
-
-__host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l of ceil((2l'+1)/4)
-    const int a = l >> 1;
-    return (l & 1) ? (a + 1) * (a + 1) : a * (a + 1);
-}
-
-// The assembly works at the output precision (ab = 4 or 8 bytes): U/V and
-// B/Bh are rounded once to it, which keeps the float32 kernel's LDS small
-// enough for three workgroups per CU.
-__host__ __device__ __forceinline__ size_t jac_xu_doubles(const Params &P, int ab) {
-    const size_t lw = (size_t)P.lmax + 1, Sn = (size_t)P.S * P.n;
-    const size_t xd = stage_x_doubles(P, (int)lw, (int)lw), ud = 4 * Sn * lw * ab / 8;
-    return xd > ud ? xd : ud;
-}
-
-__host__ __device__ __forceinline__ size_t jac_wave_doubles(const Params &P, int W, int ab) {
-    const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1;
-    return even(W * 4 * L) + even(2 * W * P.n * lw * ab / 8) + even(W * jac_xu_doubles(P, ab));
-}
-
-// o: wave-uniform row base; idx: per-lane offset (unsigned, so the stores
-// can take the scalar-base + 32-bit-offset form)
-template <typename T, typename V>
-__device__ __forceinline__ void store3(T *o, uint32_t Fe, uint32_t idx, V x, V y, V z) {
-    store_out(o + idx, x);
-    store_out(o + (Fe + idx), y);
-    store_out(o + (2 * Fe + idx), z);
-}
-
-template <typename PosT, typename OutT>
-__global__ __launch_bounds__(BSJ, sizeof(OutT) == 4 ? 3 : 2) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
-                                                                            int W, const double *__restrict__ c_scratch,
-                                                                            OutT *__restrict__ jedge) {
-    using AT = OutT; // assembly precision
-    using AT2 = typename Pair<AT>::type;
-    constexpr int ab = sizeof(AT);
-    // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
-    extern __shared__ __align__(16) double smem[];
-    const int S = P.S, n = P.n, lw = P.lmax + 1, L = P.L, Sn = S * n, tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
-    const int Fe = P.Fe, nl = n * lw, nnl = n * nl, tri_lw = P.tri_lw;
-    const int RBk = row_block(NWJ * W);
-
-    Carver cv{smem};
-    Tables T;
-    load_tables(P, cv, T, 0, lw);
-    double *cT = cv.take((size_t)Sn * L); // [L][Sn]
-    double *rgeo = cv.take(4 * (size_t)RBk);
-    int *rsp = (int *)cv.take((RBk + 1) / 2);
-    uint32_t *dtab = (uint32_t *)cv.take(((size_t)tri_lw + 1) / 2);
-    // this wave's private staging
-    Carver wv{cv.take(0) + (size_t)wave * jac_wave_doubles(P, W, ab)};
-    double *YY = wv.take((size_t)W * 4 * L); // [e][S, dS/dx, dS/dy, dS/dz][L]
-    AT2 *BB = (AT2 *)wv.take(2 * (size_t)W * nl * ab / 8); // [e][n][l] = K_l (B, Bh)
-    double *XU = wv.take((size_t)W * jac_xu_doubles(P, ab));
-    // precontraction results, aliasing the radial scratch: U2a[e][u][l] =
-    // (U, Vx), U2b[e][u][l] = (Vy, Vz)
-    AT2 *U2a = (AT2 *)XU, *U2b = U2a + (size_t)W * Sn * lw;
-
-    for (int k = tid; k < tri_lw; k += BSJ) dtab[k] = P.dtab[k];
-
-    // lane roles.  MFMA operands: A row (lane & 15) = (component, edge) =
-    // (row >> 2, row & 3), B column (lane & 15) = u within the tile, K index
-    // lane >> 4; result register r of lane holds row (lane >> 4) + 4 r, i.e.
-    // component r of edge lane >> 4.
-    const int a_comp = (lane & 15) >> 2, a_e = lane & 3, kk = lane >> 4, bj = lane & 15, o_e = lane >> 4;
-    const int ntile = (Sn + 15) >> 4, nj = chunks_below(lw);
-    // assembly: lane pass p owns tt = lane + 64 p = n' lw + l
-    const float inv_lw = 1.0f / (float)lw;
-    const int NP = (nl + 63) >> 6;
-    int tp[JAC_MAX_NP], lp[JAC_MAX_NP];
-#pragma unroll
-    for (int p = 0; p < JAC_MAX_NP; ++p) {
-        tp[p] = lane + 64 * p;
-        lp[p] = tp[p] - qdiv(tp[p], inv_lw) * lw;
-    }
-
-    // One center per workgroup.  (A persistent loop over centers is slower:
-    // vmcnt counts loads and stores together, so the next center's row and
-    // coefficient loads would wait for all of the previous center's output
-    // stores to drain.)
-    {
-    const int64_t ci = blockIdx.x;
-    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
-    if (e1 == e0) return;
-    const double *cg = c_scratch + ci * (size_t)Sn * L;
-    for (int k = tid; k < Sn * L; k += BSJ) cT[k] = cg[k];
-    const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
-    const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
-
-    for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
-        const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
-        lds_barrier();
-        load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
-        lds_barrier();
-        for (int off = wave * W; off < rbn; off += NWJ * W) {
-            const int nb = (rbn - off) < W ? (rbn - off) : W;
-            const int64_t base = rb0 + off;
-            const double *geo = rgeo + 4 * off;
-            const int *spc = rsp + off;
-            stage_edges<true, AT>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw, true);
-
-            // ---- precontraction on the matrix cores ----
-            // chunks j = (l, ch) in l-major order, operands loaded JB at a time
-            {
-                const bool aok = a_e < nb;
-                const double *Arow = YY + ((aok ? a_e : 0) * 4 + a_comp) * L;
-                for (int t = 0; t < ntile; ++t) {
-                    const int u = 16 * t + bj;
-                    const bool uok = u < Sn;
-                    const int uc = uok ? u : Sn - 1;
-                    dbl4 acc = {0.0, 0.0, 0.0, 0.0};
-                    int l = 0, ch = 0;
-                    for (int j0 = 0; j0 < nj; j0 += JB) {
-                        double av[JB], bv[JB];
-                        int lq = l, cq = ch;
-#pragma unroll
-                        for (int q = 0; q < JB; ++q) {
-                            const int m = 4 * cq + kk;
-                            const bool ok = j0 + q < nj && m <= 2 * lq;
-                            const int row = lq * lq + (ok ? m : 0);
-                            const double a = Arow[row], b = cT[row * Sn + uc];
-                            av[q] = (ok && aok) ? a : 0.0;
-                            bv[q] = (ok && uok) ? b : 0.0;
-                            if (++cq == (lq >> 1) + 1) {
-                                cq = 0;
-                                lq = lq + 1 < lw ? lq + 1 : lq;
-                            }
-                        }
-#pragma unroll
-                        for (int q = 0; q < JB; ++q) {
-                            if (j0 + q < nj) {
-                                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(av[q], bv[q], acc, 0, 0, 0);
-                                if (++ch == (l >> 1) + 1) {
-                                    if (o_e < nb && uok) {
-                                        const size_t qq = (size_t)(o_e * Sn + u) * lw + l;
-                                        U2a[qq] = Pair<AT>::make(acc[0], acc[1]);
-                                        U2b[qq] = Pair<AT>::make(acc[2], acc[3]);
-                                    }
-                                    acc = dbl4{0.0, 0.0, 0.0, 0.0};
-                                    ch = 0;
-                                    ++l;
-                                }
-                            }
-                        }
-                    }
-                }
-            }
-            wave_sync();
-
-            // ---- assembly and stores ----
-            for (int e = 0; e < nb; ++e) {
-                const int s = __builtin_amdgcn_readfirstlane(spc[e]);
-                const AT rx = (AT)geo[4 * e], ry = (AT)geo[4 * e + 1], rz = (AT)geo[4 * e + 2];
-                const AT2 *Be = BB + (size_t)e * nl;
-                const AT2 *Ua = U2a + (size_t)e * Sn * lw, *Ub = U2b + (size_t)e * Sn * lw;
-                OutT *o = jedge + (base + e) * 3 * Fe;
-                // pairs (mu, s), mu < s
-                if (s > 0) {
-#pragma unroll
-                    for (int p = 0; p < JAC_MAX_NP; ++p) {
-                        if (p >= NP || tp[p] >= nl) continue;
-                        const int tt = tp[p], l = lp[p];
-                        const AT2 bb = Be[tt];
-                        const AT bhx = bb.y * rx, bhy = bb.y * ry, bhz = bb.y * rz;
-                        for (int mu = 0; mu < s; ++mu) {
-                            const AT2 *Uma = Ua + mu * nl + l, *Umb = Ub + mu * nl + l;
-                            OutT *ob = o + mu * nnl;
-                            for (int a = 0; a < n; ++a) {
-                                const AT2 q0 = Uma[a * lw], q1 = Umb[a * lw];
-                                store3(ob + a * nl, Fe, tt, q0.x * bhx + q0.y * bb.x, q0.x * bhy + q1.x * bb.x,
-                                       q0.x * bhz + q1.y * bb.x);
-                            }
-                        }
-                    }
-                }
-                // diagonal pair (s, s), n' >= n, flat over (n, n', l)
-                {
-                    OutT *ob = o + s * nnl;
-                    const AT2 *Usa = Ua + s * nl, *Usb = Ub + s * nl;
-                    for (int f = lane; f < tri_lw; f += 64) {
-                        const uint32_t d = dtab[f];
-                        const int ta = d & 0xffff, tb = d >> 16; // n lw + l, n' lw + l
-                        const AT2 A = Be[ta], B = Be[tb];
-                        const AT2 a0 = Usa[ta], a1 = Usb[ta], b0 = Usa[tb], b1 = Usb[tb];
-                        const AT hu = B.y * a0.x + A.y * b0.x;
-                        store3(ob, Fe, f, hu * rx + (B.x * a0.y + A.x * b0.y), hu * ry + (B.x * a1.x + A.x * b1.x),
-                               hu * rz + (B.x * a1.y + A.x * b1.y));
-                    }
-                }
-                // pairs (s, nu), nu > s
-                if (s + 1 < S) {
-#pragma unroll
-                    for (int p = 0; p < JAC_MAX_NP; ++p) {
-                        if (p >= NP || tp[p] >= nl) continue;
-                        const int tt = tp[p], l = lp[p];
-                        for (int nu = s + 1; nu < S; ++nu) {
-                            const AT2 q0 = Ua[nu * nl + tt], q1 = Ub[nu * nl + tt];
-                            const AT ux = q0.x * rx, uy = q0.x * ry, uz = q0.x * rz;
-                            OutT *ob = o + s * nnl + tri_lw + (nu - s - 1) * nnl;
-                            const AT2 *Bl = Be + l;
-                            for (int a = 0; a < n; ++a) {
-                                const AT2 bb = Bl[a * lw];
-                                store3(ob + a * nl, Fe, tt, bb.y * ux + bb.x * q0.y, bb.y * uy + bb.x * q1.x,
-                                       bb.y * uz + bb.x * q1.y);
-                            }
-                        }
-                    }
-                }
-            }
-            wave_sync();
-        }
-    }
-    } // center
-}
-
-// dense[ci][j][3][F]: zero-filled by the caller; each stored block is copied
-template <typename OutT>
-__global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge, const OutT *__restrict__ jself,
-                                const int32_t *__restrict__ fmap, OutT *__restrict__ dense) {
-    const int64_t ci = blockIdx.x;
-    const int F = P.F, Fe = P.Fe;
-    const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
-    OutT *row = dense + ci * R.n_atoms * 3 * F;
-    for (int k = threadIdx.x; k < 3 * F; k += blockDim.x) row[i * 3 * F + k] = jself[ci * 3 * F + k];
-    for (int64_t e = R.row_ptr[ci]; e < R.row_ptr[ci + 1]; ++e) {
-        const int64_t j = R.cols[e];
-        const int s = R.spec[j];
-        for (int k = threadIdx.x; k < 3 * Fe; k += blockDim.x) {
-            const int d = k / Fe, fe = k - d * Fe;
-            row[(j * 3 + d) * F + fmap[s * Fe + fe]] = jedge[(e * 3 + d) * Fe + fe];
-        }
-    }
-}
-
-} // namespace
+using namespace dev;
 
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W) {
     const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0);
@@ -913,11 +18,11 @@ int density_blocks_per_cu(bool f64, bool jac, size_t lds) {
     int nb = 0;
     hipError_t e;
     if (f64)
-        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<double, double, true>, BSD, lds)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<double, double, false>, BSD, lds);
+        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<double, double, true>, BSD, lds)
+                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<double, double, false>, BSD, lds);
     else
-        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<float, float, true>, BSD, lds)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_density<float, float, false>, BSD, lds);
+        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<float, float, true>, BSD, lds)
+                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<float, float, false>, BSD, lds);
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
@@ -932,10 +37,20 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool f64) {
 
 int jacobian_max_w() { return JAC_MAX_W; }
 
-int jacobian_blocks_per_cu(bool f64, size_t lds) {
+// The float32 Jacobian kernel is also compiled for fixed (n_max, l_max + 1)
+// pairs (jacobian_fixed.hip); the generic kernel covers every other basis and
+// float64.
+const void *jacobian_kernel(bool f64, int n, int lw) {
+    if (f64) return reinterpret_cast<const void *>(&k_jacobian<double, double, 0, 0>);
+    const void *k = jacobian_fixed_0(n, lw);
+    if (!k) k = jacobian_fixed_1(n, lw);
+    if (!k) k = jacobian_fixed_2(n, lw);
+    return k ? k : reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>);
+}
+
+int jacobian_blocks_per_cu(bool f64, int n, int lw, size_t lds) {
     int nb = 0;
-    hipError_t e = f64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_jacobian<double, double>, BSJ, lds)
-                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_jacobian<float, float>, BSJ, lds);
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, jacobian_kernel(f64, n, lw), BSJ, lds);
     return (e == hipSuccess && nb > 0) ? nb : 0;
 }
 
@@ -944,12 +59,17 @@ hipError_t set_lds_limits() {
     hipError_t e = hipSuccess;
 #define SOAP_SET(K)                                                                                          \
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
-    SOAP_SET((k_density<float, float, false>));
-    SOAP_SET((k_density<float, float, true>));
-    SOAP_SET((k_density<double, double, false>));
-    SOAP_SET((k_density<double, double, true>));
-    SOAP_SET((k_jacobian<float, float>));
-    SOAP_SET((k_jacobian<double, double>));
+    SOAP_SET((dev::k_density<float, float, false>));
+    SOAP_SET((dev::k_density<float, float, true>));
+    SOAP_SET((dev::k_density<double, double, false>));
+    SOAP_SET((dev::k_density<double, double, true>));
+    SOAP_SET((k_jacobian<float, float, 0, 0>));
+    SOAP_SET((k_jacobian<double, double, 0, 0>));
+    for (int n = 1; n <= NMAX; ++n)
+        for (int lw = 1; lw <= LMAX + 1; ++lw) {
+            const void *k = jacobian_kernel(false, n, lw);
+            if (k != reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>)) SOAP_SET(k);
+        }
 #undef SOAP_SET
     return e;
 }
@@ -964,18 +84,18 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
     dim3 grid((unsigned)(per_group * P.n_groups)), block(BSD);
     if (f64) {
         if (jac)
-            hipLaunchKernelGGL((k_density<double, double, true>), grid, block, cfg.lds, st, P, R, (const double *)pos,
+            hipLaunchKernelGGL((dev::k_density<double, double, true>), grid, block, cfg.lds, st, P, R, (const double *)pos,
                                cfg.W, work, (double *)desc, (double *)c_out, (double *)jself, c_scratch);
         else
-            hipLaunchKernelGGL((k_density<double, double, false>), grid, block, cfg.lds, st, P, R,
+            hipLaunchKernelGGL((dev::k_density<double, double, false>), grid, block, cfg.lds, st, P, R,
                                (const double *)pos, cfg.W, work, (double *)desc, (double *)c_out, (double *)jself,
                                c_scratch);
     } else {
         if (jac)
-            hipLaunchKernelGGL((k_density<float, float, true>), grid, block, cfg.lds, st, P, R, (const float *)pos,
+            hipLaunchKernelGGL((dev::k_density<float, float, true>), grid, block, cfg.lds, st, P, R, (const float *)pos,
                                cfg.W, work, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
         else
-            hipLaunchKernelGGL((k_density<float, float, false>), grid, block, cfg.lds, st, P, R, (const float *)pos,
+            hipLaunchKernelGGL((dev::k_density<float, float, false>), grid, block, cfg.lds, st, P, R, (const float *)pos,
                                cfg.W, work, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
     }
     return hipGetLastError();
@@ -984,24 +104,21 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
-    dim3 grid((unsigned)R.nc), block(BSJ);
-    if (f64)
-        hipLaunchKernelGGL((k_jacobian<double, double>), grid, block, cfg.lds, st, P, R, (const double *)pos, cfg.W,
-                           c_scratch, (double *)jedge);
-    else
-        hipLaunchKernelGGL((k_jacobian<float, float>), grid, block, cfg.lds, st, P, R, (const float *)pos, cfg.W,
-                           c_scratch, (float *)jedge);
-    return hipGetLastError();
+    Params Pk = P;
+    Rows Rk = R;
+    int W = cfg.W;
+    void *args[] = {&Pk, &Rk, &pos, &W, &c_scratch, &jedge};
+    return hipLaunchKernel(jacobian_kernel(f64, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args, cfg.lds, st);
 }
 
 hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,
                                 const int32_t *fmap, void *dense, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     if (f64)
-        hipLaunchKernelGGL(k_scatter_dense<double>, dim3((unsigned)R.nc), dim3(256), 0, st, P, R,
+        hipLaunchKernelGGL(dev::k_scatter_dense<double>, dim3((unsigned)R.nc), dim3(256), 0, st, P, R,
                            (const double *)jedge, (const double *)jself, fmap, (double *)dense);
     else
-        hipLaunchKernelGGL(k_scatter_dense<float>, dim3((unsigned)R.nc), dim3(256), 0, st, P, R,
+        hipLaunchKernelGGL(dev::k_scatter_dense<float>, dim3((unsigned)R.nc), dim3(256), 0, st, P, R,
                            (const float *)jedge, (const float *)jself, fmap, (float *)dense);
     return hipGetLastError();
 }
