@@ -72,18 +72,29 @@ def measured_traffic(workload_name, kernel):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     runs (FETCH_SIZE, WRITE_SIZE, each scaled by the reading of a plain copy of
     known size), or None if absent or taken on different kernel source."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "traffic.json")
-    src = os.path.join(ROOT, "paper_2609_05709_amd", "csrc", "soap_kernels.hip")
     try:
         doc = json.load(open(path))[workload_name]
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        sha = kernels_source_sha()
         if doc["kernels_source_sha256_16"] != sha:
             return None
         k = doc["per_launch"][kernel]
         return k["fetch_bytes"] + k["write_bytes"]
     except (OSError, KeyError, ValueError):
         return None
+
+
+KERNEL_SOURCES = ("soap_device.h", "soap_kernels.hip", "jacobian_fixed.hip", "soap_internal.h")
+
+
+def kernels_source_sha():
+    """sha256 (16 hex digits) of the descriptor kernels' sources: counter
+    readings taken on other sources do not describe these kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2609_05709_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def copy_calibration():

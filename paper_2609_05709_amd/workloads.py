@@ -142,7 +142,8 @@ class Workload:
         return multispecies_sphere(n, seed, R, dmin, dict(comp))
 
     def with_basis(self, n_max: int, l_max: int, rbf: str | None = None) -> "Workload":
-        return Workload(f"{self.name}_n{n_max}l{l_max}_{rbf or self.rbf}", self.species, rbf or self.rbf,
+        rbf = rbf or self.rbf
+        return Workload(f"{self.name.split('_')[0]}_{rbf}_n{n_max}l{l_max}", self.species, rbf,
                         self.r_cut, self.sigma, n_max, l_max, self.jacobian, self.make)
 
 
