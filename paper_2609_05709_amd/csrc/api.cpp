@@ -569,7 +569,7 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
     const Params P = params_for(c, jac);
     double *scratch = nullptr;
     if (jac) {
-        hipError_t e = c->b_cscratch.ensure(8 * (size_t)c->nc * P.S * P.n * P.L);
+        hipError_t e = c->b_cscratch.ensure(8 * 4 * (size_t)c->nc * P.S * P.n * P.L); // c, Dx, Dy, Dz
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
@@ -579,6 +579,10 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
     hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0],
                                   c->b_work.as<int>(), desc, c_out, jself, scratch, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
+    if (jac) {
+        e = launch_outputs(P, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "output kernel");
+    }
     timer.done();
     return SOAP_OK;
 }

@@ -426,6 +426,85 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
     }
 }
 
+typedef double dbl4 __attribute__((ext_vector_type(4)));
+
+__host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l of ceil((2l'+1)/4)
+    const int a = l >> 1;
+    return (l & 1) ? (a + 1) * (a + 1) : a * (a + 1);
+}
+
+// ---------------------------------------------------------------------------
+// Power spectrum and center Jacobian block of one center for l in
+// [lg0, lg0 + lgc), as products over m of the coefficient matrices
+// C_l[u][m] (u = species * n + n): P_l = K_l C_l C_l^T and, per component d,
+// J_l = -K_l (D_l C_l^T + C_l D_l^T) (Eqs. powerspectrum and
+// powerspectrum-derivative with translational invariance), on the matrix
+// cores in 16 x 16 tiles of (u, v), u <= v.  Work items (component, l, tile
+// pair) go round-robin over the nw waves; only u <= v, i.e. the stored
+// feature pairs (mu <= nu, n' >= n on mu = nu), are written.
+//   C: element (u, lm) at C[u * ldu + (lm - lm0) * ldm]; D_d at D + d * dstride
+// ---------------------------------------------------------------------------
+struct CoefView {
+    const double *C, *D;
+    int ldu, ldm, dstride;
+};
+
+template <typename OutT>
+__device__ __forceinline__ void power_tiles(const CoefView cv, int Sn, int lm0, int lg0, int lgc, int S, int n, int lw,
+                                            int F, OutT *__restrict__ desc_row, OutT *__restrict__ jself_rows,
+                                            int wave, int nw, int lane, const double *__restrict__ Kl) {
+    const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
+    const int first = desc_row ? -1 : 0, ncomp = (desc_row ? 1 : 0) + (jself_rows ? 3 : 0);
+    const int nitem = ncomp * lgc * ntp;
+    const int ro = lane & 15, kk = lane >> 4, tri = n * (n + 1) / 2;
+    for (int item = wave; item < nitem; item += nw) { // uniform per wave
+        const int ci = item / (lgc * ntp), comp = ci + first, rem = item - ci * (lgc * ntp);
+        const int lc = rem / ntp, l = lg0 + lc;
+        int tp = rem - lc * ntp, ti = 0;
+        while (tp >= ntile - ti) {
+            tp -= ntile - ti;
+            ++ti;
+        }
+        const int tj = ti + tp;
+        const int ua = 16 * ti + ro, vb = 16 * tj + ro; // A row, B column of this lane
+        const bool uok = ua < Sn, vok = vb < Sn;
+        const int oa = (uok ? ua : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
+        const int ob = (vok ? vb : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
+        const double *Dd = cv.D + (comp > 0 ? comp : 0) * cv.dstride;
+        dbl4 acc = {0.0, 0.0, 0.0, 0.0};
+        for (int ch = 0; ch < (l >> 1) + 1; ++ch) {
+            const int m = 4 * ch + kk;
+            const bool mok = m <= 2 * l;
+            const int mo = (mok ? m : 0) * cv.ldm;
+            const double ca = cv.C[oa + mo], cb = cv.C[ob + mo];
+            const double xa = (mok && uok) ? ca : 0.0, xb = (mok && vok) ? cb : 0.0;
+            if (comp < 0) {
+                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, xb, acc, 0, 0, 0);
+            } else {
+                const double da = Dd[oa + mo], db = Dd[ob + mo];
+                acc = __builtin_amdgcn_mfma_f64_16x16x4f64((mok && uok) ? da : 0.0, xb, acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, (mok && vok) ? db : 0.0, acc, 0, 0, 0);
+            }
+        }
+        // lane holds rows u = 16 ti + kk + 4 r of column v = 16 tj + ro
+        const int v = 16 * tj + ro, nu = v / n, b = v - nu * n;
+        const double K = comp < 0 ? Kl[l] : -Kl[l];
+        OutT *row = (comp < 0 ? desc_row : jself_rows) + (comp < 0 ? 0 : (size_t)comp * F);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int u = 16 * ti + kk + 4 * r;
+            if (u < Sn && v < Sn && u <= v) {
+                const int mu = u / n, a = u - mu * n;
+                // feature pair (mu, nu), mu <= nu: blocks in (mu outer, nu inner) order
+                int q = mu * tri + n * n * (mu * (S - 1) - mu * (mu - 1) / 2);
+                if (nu > mu) q += tri + (nu - mu - 1) * n * n + a * n + b;
+                else q += a * n - a * (a - 1) / 2 + (b - a);
+                store_out(row + q * lw + l, K * acc[r]);
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // k_density
 //
@@ -440,8 +519,11 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
 // (D = sum over neighbours of dc/dr_j = -dc/dr_i).  Rows are sorted by
 // species, so the registers are flushed into the shared LDS accumulators
 // (float64 LDS atomics) only when the species changes and at the end.  Then
-// the whole workgroup writes the power spectrum and the center block
-// -K_l sum_m (D^mu c^nu + c^mu D^nu).
+// the workgroup writes the power spectrum and the center block
+// -K_l sum_m (D^mu c^nu + c^mu D^nu).  Both are products over m of the
+// coefficient matrices C_l[u][m] (u = species * n + n), per l: P_l = C_l C_l^T
+// and J_l = -K_l (D_l C_l^T + C_l D_l^T), taken on the matrix cores in
+// 16 x 16 tiles of (u, v), u <= v.
 // ---------------------------------------------------------------------------
 constexpr int NWD = 4, BSD = 64 * NWD;
 constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 64 * KE
@@ -467,7 +549,10 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0;
     const int lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
     const int lgY0 = dens_lgY0(JAC, lg0), lmY0 = lgY0 * lgY0, LY = lg1 * lg1 - lmY0;
-    const int S = P.S, n = P.n, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int S = P.S, n = P.n, tid = threadIdx.x, lane = tid & 63;
+    // wave-uniform (the compiler cannot prove tid >> 6 uniform by itself): per-wave
+    // loops then compile to scalar control flow
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nL = n * Lg, SnL = S * nL, lw = P.lmax + 1, Lfull = P.L, Sn = S * n, nlc = n * lgc;
     const int RBk = row_block(NWD * W);
 
@@ -478,7 +563,6 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     double *Dacc = cacc + SnL;
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
-    uint32_t *fq = (uint32_t *)cv.take(((size_t)P.nq_full + 1) / 2);
     double *c0 = cv.take((size_t)n);
     Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W)};
     // harmonics interleaved per lm as (S, dS/dx, dS/dy, dS/dz) for the Jacobian
@@ -503,9 +587,8 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
         oB[k] = own[k] ? a * lgc + (l - lg0) : 0;
     }
 
-    // per-basis tables used by the outputs, in LDS: no global load may sit
-    // between output stores (vmcnt counts loads and stores together)
-    for (int k = tid; k < P.nq_full; k += BSD) fq[k] = P.fq[k];
+    // on-site terms in LDS: no global load may sit between output stores
+    // (vmcnt counts loads and stores together)
     for (int k = tid; k < n; k += BSD) c0[k] = P.c0[k];
 
     // the next center: its rows are loaded before the current center's
@@ -528,7 +611,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
         load_rows(rgeo, rsp, pos, R.spec, R.cols, e0, (int)cnt, pi);
     };
     fetch();
-    const float inv_lgc = 1.0f / (float)lgc, inv_qlgc = 1.0f / (float)(P.nq_full * lgc), inv_Lg = 1.0f / (float)Lg;
+    const float inv_Lg = 1.0f / (float)Lg;
 
     while (ci < R.nc) {
         for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BSD) cacc[k] = 0.0;
@@ -600,43 +683,60 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
         // the next center's rows go in while this center's outputs are written
         const int64_t cw = ci;
         fetch(); // its barriers also publish the on-site term
-        // power spectrum for the group's l
-        if (desc)
-            for (int it = tid; it < P.nq_full * lgc; it += BSD) {
-                const int q = qdiv(it, inv_lgc), lc = it - q * lgc, l = lg0 + lc;
-                const uint32_t f = fq[q];
-                const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
-                const double *x = cacc + mu * nL + a * Lg + l * l - lm0;
-                const double *y = cacc + nu * nL + b * Lg + l * l - lm0;
-                double sum = 0.0;
-                for (int m = 0; m < 2 * l + 1; ++m) sum += x[m] * y[m];
-                store_out(desc + cw * P.F + q * lw + l, T.Kl[l] * sum);
-            }
+        // power spectrum (descriptor path): per l, 16 x 16 matrix-core tiles
+        // (ti <= tj) of u = (species, n) rows and v = (species, n') columns
+        if (!JAC && desc)
+            power_tiles<OutT>(CoefView{cacc, nullptr, Lg, 1, 0}, Sn, lm0, lg0, lgc, S, n, lw, P.F, desc + cw * P.F,
+                              (OutT *)nullptr, wave, NWD, lane, T.Kl);
         if (c_out)
             for (int it = tid; it < SnL; it += BSD) {
                 const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
                 store_out(c_out + (cw * Sn + sa) * Lfull + lm0 + lmg, cacc[it]);
             }
         if (JAC) {
-            // c, transposed to [lm][s n] for the Jacobian kernel's matrix-core operand
-            for (int it = tid; it < SnL; it += BSD) {
-                const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
-                c_scratch[(cw * Lfull + lm0 + lmg) * Sn + sa] = cacc[it];
-            }
-            for (int it = tid; it < 3 * P.nq_full * lgc; it += BSD) {
-                const int d = qdiv(it, inv_qlgc), rem = it - d * (P.nq_full * lgc);
-                const int q = qdiv(rem, inv_lgc), lc = rem - q * lgc, l = lg0 + lc;
-                const uint32_t f = fq[q];
-                const int mu = f & 0xff, nu = (f >> 8) & 0xff, a = (f >> 16) & 0xff, b = f >> 24;
-                const int oa = mu * nL + a * Lg + l * l - lm0, ob = nu * nL + b * Lg + l * l - lm0;
-                const double *Dd = Dacc + d * SnL;
-                double sum = 0.0;
-                for (int m = 0; m < 2 * l + 1; ++m) sum += Dd[oa + m] * cacc[ob + m] + cacc[oa + m] * Dd[ob + m];
-                store_out(jself + (cw * 3 + d) * P.F + q * lw + l, -T.Kl[l] * sum);
+            // c and D, transposed to [comp][lm][s n], for k_outputs and the
+            // Jacobian kernel's matrix-core operand
+            double *sc = c_scratch + cw * 4 * (size_t)Lfull * Sn;
+            for (int it = tid; it < 4 * SnL; it += BSD) {
+                const int comp = it / SnL, rem = it - comp * SnL;
+                const int sa = qdiv(rem, inv_Lg), lmg = rem - sa * Lg;
+                sc[((size_t)comp * Lfull + lm0 + lmg) * Sn + sa] = cacc[it];
             }
         }
         lds_barrier(); // the outputs are read from cacc before the next center clears it
     }
+}
+
+// ---------------------------------------------------------------------------
+// k_outputs: power spectrum and center Jacobian block for the Jacobian path,
+// from the coefficients c and D that k_density left in scratch
+// ([center][c, Dx, Dy, Dz][lm][species n]).  One workgroup per (center,
+// l-group); the group's slice goes to LDS, then power_tiles.  Kept apart
+// from k_density so that neither kernel carries the other's live state.
+// ---------------------------------------------------------------------------
+constexpr int BSO = 256;
+
+template <typename OutT>
+__global__ __launch_bounds__(BSO) void k_outputs(Params P, int64_t nc, const double *__restrict__ scratch,
+                                                 OutT *__restrict__ desc, OutT *__restrict__ jself) {
+    extern __shared__ __align__(16) double smem[];
+    __shared__ double Kl[16];
+    const int G = P.n_groups, g = blockIdx.x % G;
+    const int64_t ci = blockIdx.x / G;
+    const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0, lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
+    const int S = P.S, n = P.n, Sn = S * n, L = P.L, lw = P.lmax + 1, tid = threadIdx.x;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
+    // X[comp][lmg][u], comp = c, Dx, Dy, Dz
+    const double *src = scratch + ci * 4 * (size_t)L * Sn + (size_t)lm0 * Sn;
+    const int slab = Lg * Sn;
+    for (int k = tid; k < 4 * slab; k += BSO) {
+        const int comp = k / slab, r = k - comp * slab;
+        smem[k] = src[(size_t)comp * L * Sn + r];
+    }
+    lds_barrier();
+    power_tiles<OutT>(CoefView{smem, smem + slab, 1, Sn, slab}, Sn, lm0, lg0, lgc, S, n, lw, P.F, desc + ci * P.F,
+                      jself + ci * 3 * P.F, wave, BSO / 64, lane, Kl);
 }
 
 // ---------------------------------------------------------------------------
@@ -668,12 +768,6 @@ constexpr int JAC_MAX_W = 4;  // edges per MFMA tile: A rows are (component, edg
 constexpr int JAC_MAX_NP = 4; // lanes passes over (n', l): n * (l_max + 1) <= 256
 constexpr int JB = 8;         // MFMA operand pairs loaded ahead of their chain
 
-typedef double dbl4 __attribute__((ext_vector_type(4)));
-
-__host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l of ceil((2l'+1)/4)
-    const int a = l >> 1;
-    return (l & 1) ? (a + 1) * (a + 1) : a * (a + 1);
-}
 
 // The assembly works at the output precision (ab = 4 or 8 bytes): U/V and
 // B/Bh are rounded once to it, which keeps the float32 kernel's LDS small
@@ -714,7 +808,8 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
     extern __shared__ __align__(16) double smem[];
     const int S = P.S, n = NT ? NT : P.n, lw = LWT ? LWT : P.lmax + 1, L = lw * lw, Sn = S * n, tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6); // wave-uniform: scalar control flow
     const int Fe = P.Fe, nl = n * lw, nnl = n * nl, tri_lw = P.tri_lw;
     const int RBk = row_block(NWJ * W);
 
@@ -760,7 +855,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
     const int64_t ci = blockIdx.x;
     const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
     if (e1 == e0) return;
-    const double *cg = c_scratch + ci * (size_t)Sn * L;
+    const double *cg = c_scratch + ci * 4 * (size_t)Sn * L; // component c of [c, Dx, Dy, Dz]
     for (int k = tid; k < Sn * L; k += BSJ) cT[k] = cg[k];
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);

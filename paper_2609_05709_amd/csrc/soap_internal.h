@@ -86,9 +86,14 @@ const void *jacobian_fixed_1(int n, int lw);
 const void *jacobian_fixed_2(int n, int lw);
 hipError_t set_lds_limits();
 
-// desc (may be NULL), c_out (may be NULL, dtype), jself (jac only), c_scratch (jac only, float64)
+// desc (may be NULL; descriptor path), c_out (may be NULL, dtype), c_scratch (jac only, float64,
+// [center][c, Dx, Dy, Dz][lm][species n])
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
                           const DensityLaunch &cfg, int *work, void *desc, void *c_out, void *jself, double *c_scratch,
+                          hipStream_t st);
+// power spectrum and center block from the coefficient scratch (Jacobian path)
+size_t outputs_lds_bytes(const Params &P);
+hipError_t launch_outputs(const Params &P, int64_t nc, bool f64, const double *scratch, void *desc, void *jself,
                           hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);

@@ -10,7 +10,7 @@ size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W) {
     const size_t SnL = (size_t)P.S * P.n * Lg;
     const int RBk = row_block(NWD * W);
     size_t d = table_doubles(P, lg1 - lg0) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               even(((size_t)P.nq_full + 1) / 2) + even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W);
+               even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W);
     return d * 8;
 }
 
@@ -33,6 +33,24 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool f64) {
     size_t d = table_doubles(P, P.lmax + 1) + even(Sn * L) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
                even(((size_t)P.tri_lw + 1) / 2) + NWJ * jac_wave_doubles(P, W, ab);
     return d * 8;
+}
+
+size_t outputs_lds_bytes(const Params &P) {
+    int lgmax = 0;
+    for (int g = 0; g < P.n_groups; ++g) lgmax = std::max(lgmax, P.lgrp[g + 1] * P.lgrp[g + 1] - P.lgrp[g] * P.lgrp[g]);
+    return 8 * 4 * (size_t)lgmax * P.S * P.n;
+}
+
+hipError_t launch_outputs(const Params &P, int64_t nc, bool f64, const double *scratch, void *desc, void *jself,
+                          hipStream_t st) {
+    if (nc <= 0) return hipSuccess;
+    dim3 grid((unsigned)(nc * P.n_groups)), block(BSO);
+    const size_t lds = outputs_lds_bytes(P);
+    if (f64)
+        hipLaunchKernelGGL(k_outputs<double>, grid, block, lds, st, P, nc, scratch, (double *)desc, (double *)jself);
+    else
+        hipLaunchKernelGGL(k_outputs<float>, grid, block, lds, st, P, nc, scratch, (float *)desc, (float *)jself);
+    return hipGetLastError();
 }
 
 int jacobian_max_w() { return JAC_MAX_W; }
@@ -63,6 +81,8 @@ hipError_t set_lds_limits() {
     SOAP_SET((dev::k_density<float, float, true>));
     SOAP_SET((dev::k_density<double, double, false>));
     SOAP_SET((dev::k_density<double, double, true>));
+    SOAP_SET(k_outputs<float>);
+    SOAP_SET(k_outputs<double>);
     SOAP_SET((k_jacobian<float, float, 0, 0>));
     SOAP_SET((k_jacobian<double, double, 0, 0>));
     for (int n = 1; n <= NMAX; ++n)
