@@ -60,10 +60,11 @@ struct soap_ctx {
     int nq_full = 0;
     std::vector<uint32_t> fq;
     std::vector<uint32_t> dtab;   // [tri lw] diagonal-pair slots of the Jacobian kernel
+    std::vector<int32_t> qmap;    // [Sn][Sn] pair index of (u, v), u <= v, else -1
     std::vector<int32_t> fmap;    // [S][Fe]
     Params P{};
     // device constants
-    DevBuf d_const, d_fq, d_dtab, d_fmap, d_lut;
+    DevBuf d_const, d_qmap, d_dtab, d_fmap, d_lut;
     // neighbour workspace
     NbrWork nw{};
     DevBuf b_bcount, b_bstart, b_bfill, b_acell, b_scell, b_spos, b_satom, b_deg, b_scan, b_flags, b_spec,
@@ -78,6 +79,7 @@ struct soap_ctx {
     // launch configuration
     DensityLaunch dens_cfg[2]{};  // [jac]
     JacLaunch jac_cfg{};
+    OutPlan out_plan{};
     int groups_jac = 1, groups_desc = 1;
     int lgrp_jac[MAX_GROUPS + 1]{}, lgrp_desc[MAX_GROUPS + 1]{};
     // per-segment timing
@@ -120,6 +122,13 @@ void build_feature_tables(soap_ctx *c) {
                     c->fq.push_back((uint32_t)mu | (uint32_t)nu << 8 | (uint32_t)a << 16 | (uint32_t)b << 24);
     c->nq_full = (int)c->fq.size();
     c->F = (int64_t)c->nq_full * lw;
+    const int Sn = S * n;
+    c->qmap.assign((size_t)Sn * Sn, -1);
+    for (int q = 0; q < c->nq_full; ++q) {
+        const uint32_t f = c->fq[q];
+        const int u = (int)(f & 0xff) * n + (int)((f >> 16) & 0xff), v = (int)((f >> 8) & 0xff) * n + (int)(f >> 24);
+        c->qmap[(size_t)u * Sn + v] = q;
+    }
     c->Fe = (int64_t)lw * (n * (n + 1) / 2 + (S - 1) * n * n);
     c->fmap.assign((size_t)S * c->Fe, 0);
     // fmap[s][k]: feature index of slot k of a species-s neighbour block
@@ -191,6 +200,8 @@ int plan_launches(soap_ctx *c) {
         const int per_cu = density_blocks_per_cu(c->dtype == SOAP_FP64, jac != 0, lds);
         c->dens_cfg[jac].blocks = std::max(1, ncu * per_cu / *G);
     }
+    if (plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) != 0)
+        return fail(c, SOAP_EINVAL, "basis too large for the output kernel's on-chip memory");
     // Jacobian kernel: W edges per wave tile.  The most resident waves per CU
     // first (latency hiding for its LDS-bound staging), then the widest tile.
     const bool f64 = c->dtype == SOAP_FP64;
@@ -273,9 +284,9 @@ int upload_constants(soap_ctx *c) {
         return hip_fail(c, e, "hipMemcpy(constants)");
     double *d = c->d_const.as<double>();
     build_feature_tables(c);
-    if ((e = c->d_fq.ensure(c->fq.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(fq)");
-    if ((e = hipMemcpy(c->d_fq.p, c->fq.data(), c->fq.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
-        return hip_fail(c, e, "hipMemcpy(fq)");
+    if ((e = c->d_qmap.ensure(c->qmap.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(qmap)");
+    if ((e = hipMemcpy(c->d_qmap.p, c->qmap.data(), c->qmap.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+        return hip_fail(c, e, "hipMemcpy(qmap)");
     if ((e = c->d_dtab.ensure(c->dtab.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(dtab)");
     if ((e = hipMemcpy(c->d_dtab.p, c->dtab.data(), c->dtab.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
         return hip_fail(c, e, "hipMemcpy(dtab)");
@@ -308,7 +319,7 @@ int upload_constants(soap_ctx *c) {
     P.c0 = d + o_c0;
     P.Nt = d + o_Nt;
     P.gcoef = d + o_gc;
-    P.fq = c->d_fq.as<uint32_t>();
+    P.qmap = c->d_qmap.as<int32_t>();
     P.dtab = c->d_dtab.as<uint32_t>();
     P.tri_lw = (int)c->dtab.size();
     return plan_launches(c);
@@ -580,7 +591,7 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
                                   c->b_work.as<int>(), desc, c_out, jself, scratch, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
     if (jac) {
-        e = launch_outputs(P, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
+        e = launch_outputs(P, c->out_plan, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
         if (e != hipSuccess) return hip_fail(c, e, "output kernel");
     }
     timer.done();
@@ -658,7 +669,7 @@ const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : g_c
 void soap_destroy(soap_ctx *c) {
     if (!c) return;
     (void)hipDeviceSynchronize();
-    for (DevBuf *b : {&c->d_const, &c->d_fq, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
+    for (DevBuf *b : {&c->d_const, &c->d_qmap, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
                       &c->b_acell, &c->b_scell, &c->b_spos, &c->b_satom, &c->b_deg, &c->b_scan, &c->b_flags,
                       &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch, &c->b_work})
         b->release();

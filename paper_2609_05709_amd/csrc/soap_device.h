@@ -428,39 +428,59 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
 
 typedef double dbl4 __attribute__((ext_vector_type(4)));
 
+// Workgroup copy of cnt doubles from global memory to LDS with U loads in
+// flight per thread (a plain strided loop waits for each load in turn).
+template <int BS, int U>
+__device__ __forceinline__ void copy_to_lds(double *__restrict__ dst, const double *__restrict__ src, int cnt,
+                                            int tid) {
+    for (int base = 0; base < cnt; base += U * BS) {
+        double v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = base + u * BS + tid;
+            v[u] = src[k < cnt ? k : cnt - 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = base + u * BS + tid;
+            if (k < cnt) dst[k] = v[u];
+        }
+    }
+}
+
 __host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l of ceil((2l'+1)/4)
     const int a = l >> 1;
     return (l & 1) ? (a + 1) * (a + 1) : a * (a + 1);
 }
 
-// ---------------------------------------------------------------------------
-// Power spectrum and center Jacobian block of one center for l in
-// [lg0, lg0 + lgc), as products over m of the coefficient matrices
-// C_l[u][m] (u = species * n + n): P_l = K_l C_l C_l^T and, per component d,
-// J_l = -K_l (D_l C_l^T + C_l D_l^T) (Eqs. powerspectrum and
-// powerspectrum-derivative with translational invariance), on the matrix
-// cores in 16 x 16 tiles of (u, v), u <= v.  Work items (component, l, tile
-// pair) go round-robin over the nw waves; only u <= v, i.e. the stored
-// feature pairs (mu <= nu, n' >= n on mu = nu), are written.
-//   C: element (u, lm) at C[u * ldu + (lm - lm0) * ldm]; D_d at D + d * dstride
-// ---------------------------------------------------------------------------
+// Coefficients of one l-range as a matrix view: entry (u, lm) at
+// C[u * ldu + (lm - lm0) * ldm], u = species * n + radial index; D holds
+// one Cartesian component of the center derivative in the same layout.
 struct CoefView {
     const double *C, *D;
-    int ldu, ldm, dstride;
+    int ldu, ldm;
 };
 
+// Power spectrum (comp < 0) or one Cartesian component d = comp of the
+// center block, for l in [lg0, lg0 + lgc): 16 x 16 fp64 matrix-core tiles
+// (ti <= tj) of u = (species, n) rows by v = (species, n') columns,
+//   p(u, v, l)       =  K_l sum_m c_ulm c_vlm,
+//   dp/dr_i(u, v, l) = -K_l sum_m (D_ulm c_vlm + c_ulm D_vlm),
+// feature (u <= v, l) written to row[q * ldq + l - lbase] (Eqs.
+// powerspectrum and powerspectrum-derivative, the center term from
+// translational invariance).  Items (l, tile pair) go round-robin over the
+// nw waves; only u <= v, the stored pairs (mu <= nu, n' >= n on mu = nu),
+// are written.
 template <typename OutT>
-__device__ __forceinline__ void power_tiles(const CoefView cv, int Sn, int lm0, int lg0, int lgc, int S, int n, int lw,
-                                            int F, OutT *__restrict__ desc_row, OutT *__restrict__ jself_rows,
+__device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn, int lm0, int lg0, int lgc,
+                                            OutT *__restrict__ row, int ldq, int lbase, const int *__restrict__ qmap,
                                             int wave, int nw, int lane, const double *__restrict__ Kl) {
     const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
-    const int first = desc_row ? -1 : 0, ncomp = (desc_row ? 1 : 0) + (jself_rows ? 3 : 0);
-    const int nitem = ncomp * lgc * ntp;
-    const int ro = lane & 15, kk = lane >> 4, tri = n * (n + 1) / 2;
+    const int nitem = lgc * ntp;
+    const int ro = lane & 15, kk = lane >> 4;
     for (int item = wave; item < nitem; item += nw) { // uniform per wave
-        const int ci = item / (lgc * ntp), comp = ci + first, rem = item - ci * (lgc * ntp);
-        const int lc = rem / ntp, l = lg0 + lc;
-        int tp = rem - lc * ntp, ti = 0;
+        const int lc = item / ntp, l = lg0 + lc;
+        int tp = item - lc * ntp, ti = 0;
         while (tp >= ntile - ti) {
             tp -= ntile - ti;
             ++ti;
@@ -470,7 +490,6 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int Sn, int lm0, 
         const bool uok = ua < Sn, vok = vb < Sn;
         const int oa = (uok ? ua : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
         const int ob = (vok ? vb : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
-        const double *Dd = cv.D + (comp > 0 ? comp : 0) * cv.dstride;
         dbl4 acc = {0.0, 0.0, 0.0, 0.0};
         for (int ch = 0; ch < (l >> 1) + 1; ++ch) {
             const int m = 4 * ch + kk;
@@ -481,25 +500,21 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int Sn, int lm0, 
             if (comp < 0) {
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, xb, acc, 0, 0, 0);
             } else {
-                const double da = Dd[oa + mo], db = Dd[ob + mo];
+                const double da = cv.D[oa + mo], db = cv.D[ob + mo];
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64((mok && uok) ? da : 0.0, xb, acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, (mok && vok) ? db : 0.0, acc, 0, 0, 0);
             }
         }
         // lane holds rows u = 16 ti + kk + 4 r of column v = 16 tj + ro
-        const int v = 16 * tj + ro, nu = v / n, b = v - nu * n;
+        const int v = 16 * tj + ro;
         const double K = comp < 0 ? Kl[l] : -Kl[l];
-        OutT *row = (comp < 0 ? desc_row : jself_rows) + (comp < 0 ? 0 : (size_t)comp * F);
+        OutT *rl = row + (l - lbase);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int u = 16 * ti + kk + 4 * r;
-            if (u < Sn && v < Sn && u <= v) {
-                const int mu = u / n, a = u - mu * n;
-                // feature pair (mu, nu), mu <= nu: blocks in (mu outer, nu inner) order
-                int q = mu * tri + n * n * (mu * (S - 1) - mu * (mu - 1) / 2);
-                if (nu > mu) q += tri + (nu - mu - 1) * n * n + a * n + b;
-                else q += a * n - a * (a - 1) / 2 + (b - a);
-                store_out(row + q * lw + l, K * acc[r]);
+            if (u < Sn && v < Sn) {
+                const int q = qmap[u * Sn + v];
+                if (q >= 0) store_out(rl + q * ldq, K * acc[r]);
             }
         }
     }
@@ -686,8 +701,8 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
         // power spectrum (descriptor path): per l, 16 x 16 matrix-core tiles
         // (ti <= tj) of u = (species, n) rows and v = (species, n') columns
         if (!JAC && desc)
-            power_tiles<OutT>(CoefView{cacc, nullptr, Lg, 1, 0}, Sn, lm0, lg0, lgc, S, n, lw, P.F, desc + cw * P.F,
-                              (OutT *)nullptr, wave, NWD, lane, T.Kl);
+            power_tiles<OutT>(CoefView{cacc, nullptr, Lg, 1}, -1, Sn, lm0, lg0, lgc, desc + cw * P.F, lw, 0, P.qmap,
+                              wave, NWD, lane, T.Kl);
         if (c_out)
             for (int it = tid; it < SnL; it += BSD) {
                 const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
@@ -708,35 +723,67 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
 }
 
 // ---------------------------------------------------------------------------
-// k_outputs: power spectrum and center Jacobian block for the Jacobian path,
-// from the coefficients c and D that k_density left in scratch
-// ([center][c, Dx, Dy, Dz][lm][species n]).  One workgroup per (center,
-// l-group); the group's slice goes to LDS, then power_tiles.  Kept apart
-// from k_density so that neither kernel carries the other's live state.
+// k_outputs: power spectrum and center block for the Jacobian path, from the
+// coefficients c and D that k_density left in scratch
+// ([center][c, Dx, Dy, Dz][lm][species n]).  Work item = (center, output
+// row): the descriptor row or one Cartesian row of the center block.  A
+// resident grid (a multiple of 8 workgroups) strides over the items: the
+// items are short, and launching one workgroup per item left the CUs mostly
+// empty.  The four items of a center fall to workgroups of one XCD
+// (workgroups are dealt to the 8 XCDs round-robin), so c is read into one
+// L2.  Per l-group of O (usually one group covering every l) c and the needed
+// component of D go to LDS, the tiles fill an LDS copy of the row, and the
+// row leaves in whole, contiguous lines.
 // ---------------------------------------------------------------------------
 constexpr int BSO = 256;
 
+__host__ __device__ __forceinline__ size_t outputs_group_doubles(const Params &P, int lg0, int lg1, int out_bytes) {
+    const size_t Sn = (size_t)P.S * P.n, slab = (size_t)(lg1 * lg1 - lg0 * lg0) * Sn;
+    return even((Sn * Sn + 1) / 2) + 2 * even(slab) + even(((size_t)P.nq_full * (lg1 - lg0) * out_bytes + 7) / 8);
+}
+
 template <typename OutT>
-__global__ __launch_bounds__(BSO) void k_outputs(Params P, int64_t nc, const double *__restrict__ scratch,
+__global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, int64_t nc, const double *__restrict__ scratch,
                                                  OutT *__restrict__ desc, OutT *__restrict__ jself) {
     extern __shared__ __align__(16) double smem[];
     __shared__ double Kl[16];
-    const int G = P.n_groups, g = blockIdx.x % G;
-    const int64_t ci = blockIdx.x / G;
-    const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0, lm0 = lg0 * lg0, Lg = lg1 * lg1 - lm0;
-    const int S = P.S, n = P.n, Sn = S * n, L = P.L, lw = P.lmax + 1, tid = threadIdx.x;
+    const int S = P.S, n = P.n, Sn = S * n, L = P.L, lw = P.lmax + 1, nq = P.nq_full, tid = threadIdx.x;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    // X[comp][lmg][u], comp = c, Dx, Dy, Dz
-    const double *src = scratch + ci * 4 * (size_t)L * Sn + (size_t)lm0 * Sn;
-    const int slab = Lg * Sn;
-    for (int k = tid; k < 4 * slab; k += BSO) {
-        const int comp = k / slab, r = k - comp * slab;
-        smem[k] = src[(size_t)comp * L * Sn + r];
+    int *qmap = (int *)smem; // pair index of (u, v), read once per workgroup
+    for (int t = tid; t < Sn * Sn; t += BSO) qmap[t] = P.qmap[t];
+    double *smem_c = smem + even(((size_t)Sn * Sn + 1) / 2);
+    const int64_t nitem = 4 * 8 * ((nc + 7) / 8);
+    for (int64_t b = blockIdx.x; b < nitem; b += gridDim.x) {
+    // item b on XCD b % 8 (gridDim is a multiple of 8); its k-th item there is
+    // center 8 (k / 4) + b % 8, row k % 4
+    const int64_t k = b >> 3, ci = 8 * (k >> 2) + (b & 7);
+    const int comp = (int)(k & 3) - 1; // -1 descriptor, 0..2 center block d/dx, d/dy, d/dz
+    if (ci >= nc) continue;
+    const double *src = scratch + ci * 4 * (size_t)L * Sn;
+    OutT *dst = comp < 0 ? desc + ci * P.F : jself + (ci * 3 + comp) * P.F;
+    for (int g = 0; g < O.n_groups; ++g) {
+        const int lg0 = O.lgrp[g], lg1 = O.lgrp[g + 1], lgc = lg1 - lg0, lm0 = lg0 * lg0;
+        const int slab = (lg1 * lg1 - lm0) * Sn;
+        double *C = smem_c, *D = smem_c + even((size_t)slab);
+        OutT *row = (OutT *)(D + even((size_t)slab));
+        // (the barrier after these copies also orders the previous row's
+        // reads before this group's tiles rewrite it)
+        copy_to_lds<BSO, 4>(C, src + (size_t)lm0 * Sn, slab, tid);
+        if (comp >= 0) copy_to_lds<BSO, 4>(D, src + ((size_t)(comp + 1) * L + lm0) * Sn, slab, tid);
+        lds_barrier();
+        power_tiles<OutT>(CoefView{C, D, 1, Sn}, comp, Sn, lm0, lg0, lgc, row, lgc, lg0, qmap, wave, BSO / 64, lane,
+                          Kl);
+        lds_barrier();
+        if (lgc == lw)
+            for (int f = tid; f < P.F; f += BSO) dst[f] = row[f];
+        else
+            for (int t = tid; t < nq * lgc; t += BSO) {
+                const int q = t / lgc, lc = t - q * lgc;
+                dst[q * lw + lg0 + lc] = row[t];
+            }
     }
-    lds_barrier();
-    power_tiles<OutT>(CoefView{smem, smem + slab, 1, Sn, slab}, Sn, lm0, lg0, lgc, S, n, lw, P.F, desc + ci * P.F,
-                      jself + ci * 3 * P.F, wave, BSO / 64, lane, Kl);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -856,7 +903,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
     const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
     if (e1 == e0) return;
     const double *cg = c_scratch + ci * 4 * (size_t)Sn * L; // component c of [c, Dx, Dy, Dz]
-    for (int k = tid; k < Sn * L; k += BSJ) cT[k] = cg[k];
+    copy_to_lds<BSJ, 4>(cT, cg, Sn * L, tid);
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
 

@@ -25,7 +25,7 @@ struct Params {
     const double *c0;          // on-site term [n]
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)
-    const uint32_t *fq;        // [nq_full] mu | nu<<8 | n<<16 | n'<<24
+    const int32_t *qmap;       // [Sn][Sn] pair index q of rows u <= v (u = species n + n), else -1
     const uint32_t *dtab;      // [tri_lw] diagonal-pair slots: (n lw + l) | (n' lw + l) << 16, n' >= n
     int tri_lw;                // n (n + 1) / 2 * (l_max + 1)
     int n_groups;              // l-groups of the density kernel
@@ -91,10 +91,17 @@ hipError_t set_lds_limits();
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
                           const DensityLaunch &cfg, int *work, void *desc, void *c_out, void *jself, double *c_scratch,
                           hipStream_t st);
-// power spectrum and center block from the coefficient scratch (Jacobian path)
-size_t outputs_lds_bytes(const Params &P);
-hipError_t launch_outputs(const Params &P, int64_t nc, bool f64, const double *scratch, void *desc, void *jself,
-                          hipStream_t st);
+// power spectrum and center block from the coefficient scratch (Jacobian
+// path): l-groups of the output kernel, each sized to its LDS budget
+struct OutPlan {
+    int n_groups;
+    int lgrp[MAX_GROUPS + 1];
+    size_t lds;
+    int blocks; // resident workgroups on the device
+};
+int plan_outputs(const Params &P, bool f64, OutPlan *O); // 0, or -1 if one l does not fit
+hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
+                          void *jself, hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);
 hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,

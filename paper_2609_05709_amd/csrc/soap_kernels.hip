@@ -35,21 +35,47 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool f64) {
     return d * 8;
 }
 
-size_t outputs_lds_bytes(const Params &P) {
-    int lgmax = 0;
-    for (int g = 0; g < P.n_groups; ++g) lgmax = std::max(lgmax, P.lgrp[g + 1] * P.lgrp[g + 1] - P.lgrp[g] * P.lgrp[g]);
-    return 8 * 4 * (size_t)lgmax * P.S * P.n;
+// Fewest contiguous l-groups whose LDS (c and one component of D for the
+// group, plus the group's part of an output row) stays within 80 KB, two
+// workgroups per CU; a single l above the budget may use up to the hard limit.
+int plan_outputs(const Params &P, bool f64, OutPlan *O) {
+    const int lw = P.lmax + 1, ob = f64 ? 8 : 4;
+    const size_t budget = 80 * 1024, hard = 159 * 1024;
+    int G = 0, l = 0;
+    size_t worst = 0;
+    O->lgrp[0] = 0;
+    while (l < lw) {
+        int e = l + 1;
+        if (8 * outputs_group_doubles(P, l, e, ob) > hard) return -1;
+        while (e < lw && 8 * outputs_group_doubles(P, l, e + 1, ob) <= budget) ++e;
+        worst = std::max(worst, 8 * outputs_group_doubles(P, l, e, ob));
+        O->lgrp[++G] = e;
+        l = e;
+    }
+    O->n_groups = G;
+    O->lds = worst;
+    int nb = 0, ncu = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        ncu = 256;
+    const hipError_t e = f64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_outputs<double>, BSO, worst)
+                             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_outputs<float>, BSO, worst);
+    O->blocks = ncu * ((e == hipSuccess && nb > 0) ? nb : 1);
+    return 0;
 }
 
-hipError_t launch_outputs(const Params &P, int64_t nc, bool f64, const double *scratch, void *desc, void *jself,
-                          hipStream_t st) {
+hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
+                          void *jself, hipStream_t st) {
     if (nc <= 0) return hipSuccess;
-    dim3 grid((unsigned)(nc * P.n_groups)), block(BSO);
-    const size_t lds = outputs_lds_bytes(P);
+    // resident grid, a multiple of 8 (see k_outputs), at most one workgroup per item
+    const int64_t items = 4 * 8 * ((nc + 7) / 8);
+    const int64_t g = std::min<int64_t>(items, 8 * ((O.blocks + 7) / 8));
+    dim3 grid((unsigned)g), block(BSO);
     if (f64)
-        hipLaunchKernelGGL(k_outputs<double>, grid, block, lds, st, P, nc, scratch, (double *)desc, (double *)jself);
+        hipLaunchKernelGGL(k_outputs<double>, grid, block, O.lds, st, P, O, nc, scratch, (double *)desc,
+                           (double *)jself);
     else
-        hipLaunchKernelGGL(k_outputs<float>, grid, block, lds, st, P, nc, scratch, (float *)desc, (float *)jself);
+        hipLaunchKernelGGL(k_outputs<float>, grid, block, O.lds, st, P, O, nc, scratch, (float *)desc, (float *)jself);
     return hipGetLastError();
 }
 
