@@ -67,8 +67,8 @@ struct soap_ctx {
     DevBuf d_const, d_qmap, d_dtab, d_fmap, d_lut;
     // neighbour workspace
     NbrWork nw{};
-    DevBuf b_bcount, b_bstart, b_bfill, b_acell, b_scell, b_spos, b_satom, b_deg, b_scan, b_flags, b_spec,
-        b_row, b_cols, b_cscratch, b_work;
+    DevBuf b_zero, b_bstart, b_acell, b_srec, b_sspec, b_deg, b_slots, b_scan, b_spec, b_row, b_cols, b_cscratch;
+    uint64_t work_epoch = 0; // density work-counter increments since the counters were zeroed
     int32_t *h_flags = nullptr; // pinned: [0..3] flags, then int64 E at offset 8
     // state of the last neighbour build
     bool have_rows = false;
@@ -502,41 +502,44 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     auto need = [&](DevBuf &b, size_t bytes) {
         if (e == hipSuccess) e = b.ensure(bytes);
     };
-    need(c->b_bcount, 4 * H);
+    need(c->b_zero, nbr_zero_bytes(H));
     need(c->b_bstart, 4 * (H + 1));
-    need(c->b_bfill, 4 * H);
     need(c->b_acell, 16 * n_atoms);
-    need(c->b_scell, 16 * n_atoms);
-    need(c->b_spos, 32 * n_atoms);
-    need(c->b_satom, 4 * n_atoms);
+    need(c->b_srec, (f64 ? 32 : 16) * n_atoms);
+    need(c->b_sspec, n_atoms);
     need(c->b_spec, n_atoms);
     need(c->b_deg, 4 * n_centers);
+    need(c->b_slots, 4 * (size_t)TCAP * n_centers);
     need(c->b_scan, 8 * tiles);
-    need(c->b_flags, 16);
     need(c->b_row, 8 * (n_centers + 1));
     if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(neighbour workspace)");
     NbrWork &w = c->nw;
     w.H = H;
-    w.bucket_count = c->b_bcount.as<int32_t>();
+    w.zero = c->b_zero.p;
+    w.zero_bytes = nbr_zero_bytes(H);
+    char *z = (char *)c->b_zero.p;
+    w.flags = (int32_t *)z;
+    w.work = (unsigned long long *)(z + NBR_FLAGS_BYTES);
+    w.bucket_count = (int32_t *)(z + NBR_FLAGS_BYTES + NBR_WORK_BYTES);
+    w.bucket_fill = w.bucket_count + H;
     w.bucket_start = c->b_bstart.as<int32_t>();
-    w.bucket_fill = c->b_bfill.as<int32_t>();
     w.atom_cell = c->b_acell.as<int4>();
-    w.sorted_cell = c->b_scell.as<int4>();
-    w.sorted_pos = c->b_spos.as<double4>();
-    w.sorted_atom = c->b_satom.as<int32_t>();
+    w.sorted_rec = c->b_srec.p;
+    w.sorted_spec = c->b_sspec.as<uint8_t>();
     w.deg = c->b_deg.as<int32_t>();
+    w.slots = c->b_slots.as<int32_t>();
     w.scan_tmp = c->b_scan.as<int64_t>();
-    w.flags = c->b_flags.as<int32_t>();
     int64_t *row = c->b_row.as<int64_t>();
     SegTimer timer(c, 0, st);
     e = nbr_phase1(w, n_atoms, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(), n_centers,
                    centers_dev, c->r_cut, row, st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
-    if ((e = hipMemcpyAsync(c->h_flags, w.flags, 16, hipMemcpyDeviceToHost, st)) != hipSuccess ||
-        (e = hipMemcpyAsync(c->h_flags + 4, row + n_centers, 8, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+    c->work_epoch = 0; // the density work counters were zeroed with the flags
+    // flags[0..3] and the total degree (int64 at flags + 4) in one copy
+    if ((e = hipMemcpyAsync(c->h_flags, w.flags, 24, hipMemcpyDeviceToHost, st)) != hipSuccess ||
         (e = hipStreamSynchronize(st)) != hipSuccess)
         return hip_fail(c, e, "neighbour search (sync)");
-    const int32_t bad = c->h_flags[0], maxdeg = c->h_flags[1];
+    const int32_t bad = c->h_flags[0], maxdeg = c->h_flags[1], n_long = c->h_flags[2];
     int64_t E;
     std::memcpy(&E, c->h_flags + 4, 8);
     if (bad & 1) return fail(c, SOAP_ESPECIES, "an atomic number is not in the species list");
@@ -545,7 +548,7 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
         return fail(c, SOAP_ECAPACITY, "a center has %d neighbours (limit %d)", maxdeg, MAX_DEGREE);
     if ((e = c->b_cols.ensure(4 * (size_t)std::max<int64_t>(E, 1))) != hipSuccess)
         return hip_fail(c, e, "hipMalloc(neighbour rows)");
-    e = nbr_phase2(w, n_atoms, pos_dev, f64, c->b_spec.as<uint8_t>(), n_centers, centers_dev, c->r_cut, row,
+    e = nbr_phase2(w, n_atoms, pos_dev, f64, n_centers, centers_dev, c->r_cut, row, n_long > 0,
                    c->b_cols.as<int32_t>(), st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour rows");
     timer.done();
@@ -584,11 +587,9 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
-    hipError_t e0 = c->b_work.ensure(sizeof(int) * (MAX_GROUPS + 1));
-    if (e0 != hipSuccess) return hip_fail(c, e0, "hipMalloc(work counters)");
     SegTimer timer(c, 1, to_stream(stream));
-    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0],
-                                  c->b_work.as<int>(), desc, c_out, jself, scratch, to_stream(stream));
+    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0], c->nw.work,
+                                  &c->work_epoch, desc, c_out, jself, scratch, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
     if (jac) {
         e = launch_outputs(P, c->out_plan, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
@@ -669,9 +670,9 @@ const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : g_c
 void soap_destroy(soap_ctx *c) {
     if (!c) return;
     (void)hipDeviceSynchronize();
-    for (DevBuf *b : {&c->d_const, &c->d_qmap, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_bcount, &c->b_bstart, &c->b_bfill,
-                      &c->b_acell, &c->b_scell, &c->b_spos, &c->b_satom, &c->b_deg, &c->b_scan, &c->b_flags,
-                      &c->b_spec, &c->b_row, &c->b_cols, &c->b_cscratch, &c->b_work})
+    for (DevBuf *b : {&c->d_const, &c->d_qmap, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_zero, &c->b_bstart, &c->b_acell,
+                      &c->b_srec, &c->b_sspec, &c->b_deg, &c->b_slots, &c->b_scan, &c->b_spec, &c->b_row, &c->b_cols,
+                      &c->b_cscratch})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
     for (auto &r : c->recs) {

@@ -1,15 +1,28 @@
 // Neighbour search on the device: a hashed cell list.
 //
 // Cells are cubes of edge h slightly above r_cut, so two atoms closer than
-// r_cut lie in the same or adjacent cells.  Cells are hashed into H buckets
-// (no bounding box needed, any spatial extent); a bucket can hold atoms of
-// several cells, so every candidate's cell coordinates are compared before
-// its distance is tested, which also rules out visiting a candidate twice.
+// r_cut lie in the same or adjacent cells.  Cells go to H = 2^k buckets by a
+// spatially coherent key: the low b = floor(k / 3) bits of the three cell
+// coordinates, bit-interleaved (Morton order), with a hash of the remaining
+// high bits above them.  Consequences used below:
+//   - neighbouring cells get neighbouring buckets, so the sorted atom order
+//     is spatially local, and so are consecutive centers in that order;
+//   - the 27 cells around a center fall into 27 distinct buckets (b >= 2:
+//     coordinates that differ by at most 2 differ in their low b bits), so
+//     no atom is visited twice;
+//   - another cell sharing a bucket with one of those 27 is at least 2^b - 1
+//     cells away along some axis, i.e. at least 2 h > r_cut from the center,
+//     and its atoms fail the cutoff test; no cell coordinates need comparing.
+// Cells whose box lies farther than r_cut from the center are skipped.
 //
-// Phase 1: species lookup, cell hashing, bucket counts -> bucket offsets,
-//          bucket fill, per-center neighbour counts -> CSR row offsets.
-// Phase 2: per center, gather the neighbour keys (species, atom) in LDS,
-//          order them by rank (keys are unique), write the row.
+// Phase 1: species lookup, cell keys, bucket counts -> bucket offsets,
+//          bucket fill (position + atom records), then one wave per center
+//          collects its neighbour keys (species, atom) in LDS, ranks them
+//          (keys are unique) and writes the ordered row to a fixed-capacity
+//          slot (TCAP entries) with its degree; CSR row offsets by scan.
+// Phase 2 (after the host has read the total): the slots are packed into
+//          the CSR rows; rows longer than TCAP are collected again, with up
+//          to MAX_DEGREE keys in LDS.
 // The cutoff test is the exact float64 one defined in soap.h.
 #include "soap_internal.h"
 
@@ -18,18 +31,50 @@ namespace {
 
 constexpr double CELL_PAD = 1.0001;
 
-__device__ __forceinline__ uint32_t cell_hash(int cx, int cy, int cz, uint32_t mask) {
-    uint32_t h = (uint32_t)cx * 73856093u ^ (uint32_t)cy * 19349663u ^ (uint32_t)cz * 83492791u;
+// spread the low 10 bits of x to every third bit
+__device__ __forceinline__ uint32_t spread3(uint32_t x) {
+    x &= 0x3ff;
+    x = (x | (x << 16)) & 0x030000ff;
+    x = (x | (x << 8)) & 0x0300f00f;
+    x = (x | (x << 4)) & 0x030c30c3;
+    x = (x | (x << 2)) & 0x09249249;
+    return x;
+}
+
+__device__ __forceinline__ uint32_t cell_key(int cx, int cy, int cz, int b, uint32_t mask) {
+    const uint32_t lo_mask = (1u << b) - 1u;
+    const uint32_t m = spread3((uint32_t)cx & lo_mask) | spread3((uint32_t)cy & lo_mask) << 1 |
+                       spread3((uint32_t)cz & lo_mask) << 2;
+    uint32_t h = (uint32_t)(cx >> b) * 73856093u ^ (uint32_t)(cy >> b) * 19349663u ^ (uint32_t)(cz >> b) * 83492791u;
     h ^= h >> 15;
     h *= 0x2c1b3c6du;
     h ^= h >> 12;
-    return h & mask;
+    return (m | (3 * b < 32 ? h << (3 * b) : 0u)) & mask;
 }
 
 template <typename PosT>
 __device__ __forceinline__ double3 load_pos(const PosT *pos, int64_t i) {
     return make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
 }
+
+// sorted-atom record: position at the input precision and the atom index
+template <typename PosT> struct Rec;
+template <> struct Rec<float> {
+    using type = float4;
+    static __device__ __forceinline__ float4 make(const float *p, int32_t i) {
+        return make_float4(p[0], p[1], p[2], __int_as_float(i));
+    }
+    static __device__ __forceinline__ int32_t atom(float4 r) { return __float_as_int(r.w); }
+    static __device__ __forceinline__ double3 pos(float4 r) { return make_double3(r.x, r.y, r.z); }
+};
+template <> struct Rec<double> {
+    using type = double4;
+    static __device__ __forceinline__ double4 make(const double *p, int32_t i) {
+        return make_double4(p[0], p[1], p[2], (double)i);
+    }
+    static __device__ __forceinline__ int32_t atom(double4 r) { return (int32_t)r.w; }
+    static __device__ __forceinline__ double3 pos(double4 r) { return make_double3(r.x, r.y, r.z); }
+};
 
 // |r_j - r_i|^2 < r_cut^2 evaluated as ((dx*dx + dy*dy) + dz*dz), no contraction
 __device__ __forceinline__ bool within_cutoff(double3 a, double3 b, double rc2) {
@@ -43,7 +88,7 @@ __device__ __forceinline__ bool within_cutoff(double3 a, double3 b, double rc2) 
 template <typename PosT>
 __global__ void k_prepare(int64_t n, const PosT *__restrict__ pos, const int32_t *__restrict__ Z,
                           const int8_t *__restrict__ lut, uint8_t *__restrict__ spec, int4 *__restrict__ cell,
-                          int32_t *__restrict__ count, uint32_t mask, double inv_h, int32_t *__restrict__ flags) {
+                          int32_t *__restrict__ count, uint32_t mask, int b, double inv_h, int32_t *__restrict__ flags) {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
     int z = Z[i];
@@ -55,49 +100,51 @@ __global__ void k_prepare(int64_t n, const PosT *__restrict__ pos, const int32_t
     spec[i] = (uint8_t)s;
     double3 p = load_pos(pos, i);
     int cx = (int)floor(p.x * inv_h), cy = (int)floor(p.y * inv_h), cz = (int)floor(p.z * inv_h);
-    uint32_t b = cell_hash(cx, cy, cz, mask);
-    cell[i] = make_int4(cx, cy, cz, (int)b);
-    atomicAdd(&count[b], 1);
+    uint32_t k = cell_key(cx, cy, cz, b, mask);
+    cell[i] = make_int4(cx, cy, cz, (int)k);
+    atomicAdd(&count[k], 1);
 }
 
 template <typename PosT>
-__global__ void k_bucket_fill(int64_t n, const PosT *__restrict__ pos, const int4 *__restrict__ cell,
-                              const int32_t *__restrict__ start, int32_t *__restrict__ fill,
-                              int4 *__restrict__ scell, double4 *__restrict__ spos, int32_t *__restrict__ satom) {
+__global__ void k_bucket_fill(int64_t n, const PosT *__restrict__ pos, const uint8_t *__restrict__ spec,
+                              const int4 *__restrict__ cell, const int32_t *__restrict__ start,
+                              int32_t *__restrict__ fill, typename Rec<PosT>::type *__restrict__ srec,
+                              uint8_t *__restrict__ sspec) {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
-    int4 c = cell[i];
-    int slot = start[c.w] + atomicAdd(&fill[c.w], 1);
-    double3 p = load_pos(pos, i);
-    scell[slot] = c;
-    spos[slot] = make_double4(p.x, p.y, p.z, 0.0);
-    satom[slot] = (int32_t)i;
+    const int k = cell[i].w;
+    const int slot = start[k] + atomicAdd(&fill[k], 1);
+    srec[slot] = Rec<PosT>::make(pos + 3 * i, (int32_t)i);
+    sspec[slot] = spec[i];
 }
 
-// Candidate enumeration shared by the count and fill passes: one 64-lane wave
-// per center.  Lanes 0..26 look up one neighbouring cell each (bucket range
-// and cell coordinates) into the wave's LDS slots; a prefix over the 27
-// bucket sizes then lets every lane take candidates t = lane, lane + 64, ...
-// of the concatenated buckets, so the loads of one center are spread over
-// the whole wave instead of walking each bucket serially.
+// The candidates of one center: the atoms of the buckets of the (up to) 27
+// cells around it, concatenated.  Lanes 0..26 look up one cell each; a
+// prefix over the bucket sizes then lets lane t take candidates t, t + 64,
+// ... so the loads of one center spread over the whole wave.
 struct CellSlots {
     int off[28];   // prefix of bucket sizes
     int start[27]; // first sorted slot of each bucket
-    int cx[27], cy[27], cz[27];
 };
 
-__device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 ci, const int32_t *__restrict__ start,
+__device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 ci, double3 pi, double inv_h,
+                                                 double lim2, int b, const int32_t *__restrict__ start,
                                                  uint32_t mask) {
     int sz = 0;
     if (lane < 27) {
-        const int tx = ci.x + lane % 3 - 1, ty = ci.y + (lane / 3) % 3 - 1, tz = ci.z + lane / 9 - 1;
-        const uint32_t b = cell_hash(tx, ty, tz, mask);
-        const int s0 = start[b];
-        sz = start[b + 1] - s0;
-        cs.start[lane] = s0;
-        cs.cx[lane] = tx;
-        cs.cy[lane] = ty;
-        cs.cz[lane] = tz;
+        const int dx = lane % 3 - 1, dy = (lane / 3) % 3 - 1, dz = lane / 9 - 1;
+        // gap from the center to the cell's box along each axis, in cell units
+        const double ux = pi.x * inv_h, uy = pi.y * inv_h, uz = pi.z * inv_h;
+        const double gx = dx < 0 ? ux - (double)ci.x : dx > 0 ? (double)(ci.x + 1) - ux : 0.0;
+        const double gy = dy < 0 ? uy - (double)ci.y : dy > 0 ? (double)(ci.y + 1) - uy : 0.0;
+        const double gz = dz < 0 ? uz - (double)ci.z : dz > 0 ? (double)(ci.z + 1) - uz : 0.0;
+        const double g2 = fmax(gx, 0.0) * fmax(gx, 0.0) + fmax(gy, 0.0) * fmax(gy, 0.0) + fmax(gz, 0.0) * fmax(gz, 0.0);
+        if (g2 <= lim2) {
+            const uint32_t k = cell_key(ci.x + dx, ci.y + dy, ci.z + dz, b, mask);
+            const int s0 = start[k];
+            sz = start[k + 1] - s0;
+            cs.start[lane] = s0;
+        }
     }
     // inclusive scan of sz over lanes 0..26
     int v = sz;
@@ -113,130 +160,201 @@ __device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 c
     return cs.off[27];
 }
 
-// Candidate t of the concatenated buckets: its sorted slot, or -1 if it
-// belongs to another cell that shares the bucket.
-__device__ __forceinline__ int candidate_slot(const CellSlots &cs, int t, const int4 *__restrict__ scell) {
-    int d = 0;
-    while (cs.off[d + 1] <= t) ++d;
-    const int slot = cs.start[d] + (t - cs.off[d]);
-    const int4 sc = scell[slot];
-    return (sc.x == cs.cx[d] && sc.y == cs.cy[d] && sc.z == cs.cz[d]) ? slot : -1;
-}
-
-template <typename PosT>
-__global__ __launch_bounds__(256) void k_count(int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers,
-                                               const PosT *__restrict__ pos, const int4 *__restrict__ cell,
-                                               const int32_t *__restrict__ start, const int4 *__restrict__ scell,
-                                               const double4 *__restrict__ spos, const int32_t *__restrict__ satom,
-                                               uint32_t mask, double rc2, int32_t *__restrict__ deg,
-                                               int32_t *__restrict__ flags) {
-    __shared__ CellSlots slots[4];
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t c = (int64_t)blockIdx.x * 4 + w;
-    if (c >= nc) return;
-    const int64_t i = centers ? (int64_t)centers[c] : c;
-    if (i < 0 || i >= n_atoms) {
-        if (lane == 0) {
-            atomicOr(&flags[0], 2);
-            deg[c] = 0;
+// Collect the neighbour keys (species << 32 | atom) of center atom i into
+// keys[0..cap) in candidate order; returns the degree (which may exceed cap:
+// the surplus keys are counted, not stored).  U candidates per lane are
+// loaded together.
+template <typename PosT, int U>
+__device__ __forceinline__ int collect_keys(const CellSlots &cs, int total, int lane, int64_t i, double3 pi,
+                                            double rc2, const typename Rec<PosT>::type *__restrict__ srec,
+                                            const uint8_t *__restrict__ sspec, int64_t *keys, int cap) {
+    int base = 0, d = 0;
+    for (int t0 = 0; t0 < total; t0 += 64 * U) {
+        int slot[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int t = t0 + 64 * u + lane;
+            slot[u] = -1;
+            if (t < total) {
+                while (cs.off[d + 1] <= t) ++d; // t grows with u and t0: d only moves forward
+                slot[u] = cs.start[d] + (t - cs.off[d]);
+            }
         }
-        return;
+        typename Rec<PosT>::type r[U];
+        int sp[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = slot[u] < 0 ? 0 : slot[u];
+            r[u] = srec[s];
+            sp[u] = sspec[s];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int32_t j = Rec<PosT>::atom(r[u]);
+            const bool hit = slot[u] >= 0 && j != (int32_t)i && within_cutoff(pi, Rec<PosT>::pos(r[u]), rc2);
+            const uint64_t m = __ballot(hit);
+            const int pre = __popcll(m & ((1ull << lane) - 1ull));
+            if (hit && base + pre < cap) keys[base + pre] = ((int64_t)sp[u] << 32) | (int64_t)(uint32_t)j;
+            base += __popcll(m);
+        }
     }
-    CellSlots &cs = slots[w];
-    const int total = wave_prefix_cells(cs, lane, cell[i], start, mask);
-    const double3 pi = load_pos(pos, i);
-    int cnt = 0;
-    for (int t = lane; t < total; t += 64) {
-        const int slot = candidate_slot(cs, t, scell);
-        if (slot < 0 || satom[slot] == (int32_t)i) continue;
-        const double4 q = spos[slot];
-        if (within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2)) ++cnt;
-    }
-    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_down(cnt, off, 64);
-    if (lane == 0) {
-        deg[c] = cnt;
-        atomicMax(&flags[1], cnt);
+    return base;
+}
+
+// Write the deg (<= what keys holds) keys of a wave in ascending order:
+// each key's rank among the row's keys is its position.
+__device__ __forceinline__ void write_ranked(const int64_t *keys, int deg, int lane, int32_t *__restrict__ out) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int k = lane; k < deg; k += 64) {
+        const int64_t key = keys[k];
+        int rank = 0;
+        for (int t = 0; t < deg; ++t) rank += keys[t] < key;
+        out[rank] = (int32_t)(key & 0xffffffff);
     }
 }
 
-// One 64-lane workgroup per center: matching candidates are appended to the
-// LDS key list (slot from a ballot prefix), keys (species << 32 | atom) are
-// unique and each key's rank among the row's keys is its output position.
+constexpr int NBR_WAVES = 4; // centers per workgroup in the collecting pass
+
+// One wave per center.  Without a center list the centers are taken in
+// sorted-atom (cell) order, so the waves resident on a CU share cells.
 template <typename PosT>
-__global__ __launch_bounds__(64) void k_fill_sort(int64_t nc, const int32_t *__restrict__ centers,
-                                                  const PosT *__restrict__ pos, const uint8_t *__restrict__ spec,
-                                                  const int4 *__restrict__ cell, const int32_t *__restrict__ start,
-                                                  const int4 *__restrict__ scell, const double4 *__restrict__ spos,
-                                                  const int32_t *__restrict__ satom, uint32_t mask, double rc2,
-                                                  const int64_t *__restrict__ row_ptr, int32_t *__restrict__ cols) {
+__global__ __launch_bounds__(64 * NBR_WAVES) void k_collect(
+    int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos,
+    const int4 *__restrict__ cell, const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
+    const uint8_t *__restrict__ sspec, uint32_t mask, int b, double inv_h, double lim2, double rc2,
+    int32_t *__restrict__ deg, int32_t *__restrict__ slots, int32_t *__restrict__ flags) {
+    __shared__ CellSlots cslots[NBR_WAVES];
+    __shared__ int64_t kbuf[NBR_WAVES][TCAP];
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * NBR_WAVES + w;
+    if (t >= nc) return;
+    int64_t c, i;
+    if (centers) {
+        c = t;
+        i = centers[c];
+        if (i < 0 || i >= n_atoms) {
+            if (lane == 0) {
+                atomicOr(&flags[0], 2);
+                deg[c] = 0;
+            }
+            return;
+        }
+    } else {
+        i = Rec<PosT>::atom(srec[t]);
+        c = i;
+    }
+    CellSlots &cs = cslots[w];
+    const double3 pi = load_pos(pos, i);
+    const int total = wave_prefix_cells(cs, lane, cell[i], pi, inv_h, lim2, b, start, mask);
+    int64_t *keys = kbuf[w];
+    const int dg = collect_keys<PosT, 4>(cs, total, lane, i, pi, rc2, srec, sspec, keys, TCAP);
+    if (dg <= TCAP) write_ranked(keys, dg, lane, slots + c * TCAP);
+    if (lane == 0) {
+        deg[c] = dg;
+        atomicMax(&flags[1], dg);
+        if (dg > TCAP) atomicAdd(&flags[2], 1);
+    }
+}
+
+// CSR rows from the fixed-capacity slots; rows longer than TCAP are left to
+// k_collect_long.
+__global__ __launch_bounds__(256) void k_pack(int64_t nc, const int64_t *__restrict__ row_ptr,
+                                              const int32_t *__restrict__ slots, int32_t *__restrict__ cols) {
+    const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (c >= nc) return;
+    const int64_t r0 = row_ptr[c];
+    const int dg = (int)(row_ptr[c + 1] - r0);
+    if (dg > TCAP) return;
+    for (int k = lane; k < dg; k += 64) cols[r0 + k] = slots[c * TCAP + k];
+}
+
+// Rows longer than TCAP, collected again with MAX_DEGREE keys in LDS (one
+// 64-lane workgroup per center; other centers return at once).
+template <typename PosT>
+__global__ __launch_bounds__(64) void k_collect_long(
+    int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos, const int4 *__restrict__ cell,
+    const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
+    const uint8_t *__restrict__ sspec, uint32_t mask, int b, double inv_h, double lim2, double rc2,
+    const int64_t *__restrict__ row_ptr, int32_t *__restrict__ cols) {
     __shared__ int64_t keys[MAX_DEGREE];
     __shared__ CellSlots cs;
     const int64_t c = blockIdx.x;
     const int lane = threadIdx.x;
     const int64_t r0 = row_ptr[c];
-    const int deg = (int)(row_ptr[c + 1] - r0);
-    if (deg == 0) return;
+    const int dg = (int)(row_ptr[c + 1] - r0);
+    if (dg <= TCAP) return;
     const int64_t i = centers ? (int64_t)centers[c] : c;
-    const int total = wave_prefix_cells(cs, lane, cell[i], start, mask);
     const double3 pi = load_pos(pos, i);
-    int base = 0;
-    for (int t0 = 0; t0 < total; t0 += 64) {
-        const int t = t0 + lane;
-        bool hit = false;
-        int j = 0;
-        if (t < total) {
-            const int slot = candidate_slot(cs, t, scell);
-            if (slot >= 0) {
-                j = satom[slot];
-                if (j != (int32_t)i) {
-                    const double4 q = spos[slot];
-                    hit = within_cutoff(pi, make_double3(q.x, q.y, q.z), rc2);
-                }
-            }
-        }
-        const uint64_t m = __ballot(hit);
-        const int pre = __popcll(m & ((1ull << lane) - 1ull));
-        if (hit && base + pre < MAX_DEGREE) keys[base + pre] = ((int64_t)spec[j] << 32) | (int64_t)(uint32_t)j;
-        base += __popcll(m);
-    }
-    __syncthreads();
-    for (int k = lane; k < deg; k += 64) {
-        const int64_t key = keys[k];
-        int rank = 0;
-        for (int t = 0; t < deg; ++t) rank += keys[t] < key;
-        cols[r0 + rank] = (int32_t)(key & 0xffffffff);
-    }
+    const int total = wave_prefix_cells(cs, lane, cell[i], pi, inv_h, lim2, b, start, mask);
+    const int got = collect_keys<PosT, 4>(cs, total, lane, i, pi, rc2, srec, sspec, keys, MAX_DEGREE);
+    write_ranked(keys, got < dg ? got : dg, lane, cols + r0);
 }
 
-// ---- exclusive scan of int32 counts into int64 offsets (out has n+1) ----
+// ---- exclusive scan of int32 counts into offsets (out has n+1) ----
 constexpr int SCAN_THREADS = 256, SCAN_ITEMS = 8, SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+constexpr int SMALL_THREADS = 1024, SMALL_ITEMS = 16, SMALL_MAX = SMALL_THREADS * SMALL_ITEMS;
+
+// workgroup-wide exclusive scan of one value per thread (BS threads); returns
+// the exclusive prefix, *sum gets the total
+template <int BS>
+__device__ __forceinline__ int64_t block_exclusive(int64_t s, int64_t *part, int64_t *sum) {
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int off = 1; off < BS; off <<= 1) {
+        int64_t t = (threadIdx.x >= off) ? part[threadIdx.x - off] : 0;
+        __syncthreads();
+        part[threadIdx.x] += t;
+        __syncthreads();
+    }
+    *sum = part[BS - 1];
+    return part[threadIdx.x] - s;
+}
+
+// one workgroup for n <= SMALL_MAX; total also to *total_copy if given
+template <typename OutT>
+__global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const int32_t *__restrict__ in,
+                                                              OutT *__restrict__ out, int64_t *__restrict__ total_copy) {
+    __shared__ int64_t part[SMALL_THREADS];
+    const int64_t base = (int64_t)threadIdx.x * SMALL_ITEMS;
+    int64_t v[SMALL_ITEMS], s = 0, total;
+#pragma unroll
+    for (int k = 0; k < SMALL_ITEMS; ++k) {
+        v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
+        s += v[k];
+    }
+    int64_t run = block_exclusive<SMALL_THREADS>(s, part, &total);
+#pragma unroll
+    for (int k = 0; k < SMALL_ITEMS; ++k) {
+        if (base + k < n) out[base + k] = (OutT)run;
+        run += v[k];
+    }
+    if (threadIdx.x == 0) {
+        out[n] = (OutT)total;
+        if (total_copy) *total_copy = total;
+    }
+}
 
 template <typename OutT>
 __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile(int64_t n, const int32_t *__restrict__ in,
                                                             OutT *__restrict__ out, int64_t *__restrict__ sums) {
     __shared__ int64_t part[SCAN_THREADS];
     const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
-    int64_t v[SCAN_ITEMS], s = 0;
+    int64_t v[SCAN_ITEMS], s = 0, total;
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
         s += v[k];
     }
-    part[threadIdx.x] = s;
-    __syncthreads();
-    for (int off = 1; off < SCAN_THREADS; off <<= 1) {
-        int64_t t = (threadIdx.x >= off) ? part[threadIdx.x - off] : 0;
-        __syncthreads();
-        part[threadIdx.x] += t;
-        __syncthreads();
-    }
-    int64_t run = part[threadIdx.x] - s; // exclusive within the tile
+    int64_t run = block_exclusive<SCAN_THREADS>(s, part, &total); // exclusive within the tile
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         if (base + k < n) out[base + k] = (OutT)run;
         run += v[k];
     }
-    if (threadIdx.x == SCAN_THREADS - 1) sums[blockIdx.x] = part[threadIdx.x];
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
 }
 
 // single workgroup: exclusive scan of the tile sums in place; total -> *total
@@ -245,102 +363,120 @@ __global__ __launch_bounds__(1024) void k_scan_sums(int64_t m, int64_t *__restri
     __shared__ int64_t part[1024];
     const int per = (int)((m + 1023) / 1024);
     const int64_t base = (int64_t)threadIdx.x * per;
-    int64_t s = 0;
+    int64_t s = 0, tot;
     for (int k = 0; k < per; ++k)
         if (base + k < m) s += sums[base + k];
-    part[threadIdx.x] = s;
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-        int64_t t = (threadIdx.x >= off) ? part[threadIdx.x - off] : 0;
-        __syncthreads();
-        part[threadIdx.x] += t;
-        __syncthreads();
-    }
-    int64_t run = part[threadIdx.x] - s;
+    int64_t run = block_exclusive<1024>(s, part, &tot);
     for (int k = 0; k < per; ++k)
         if (base + k < m) {
             int64_t v = sums[base + k];
             sums[base + k] = run;
             run += v;
         }
-    if (threadIdx.x == 1023) *total = part[1023];
+    if (threadIdx.x == 0) *total = tot;
 }
 
 template <typename OutT>
 __global__ void k_scan_add(int64_t n, OutT *__restrict__ out, const int64_t *__restrict__ sums,
-                           const int64_t *__restrict__ total) {
+                           const int64_t *__restrict__ total, int64_t *__restrict__ total_copy) {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) out[i] += (OutT)sums[i / SCAN_TILE];
-    if (i == n) out[n] = (OutT)*total;
+    if (i == n) {
+        out[n] = (OutT)*total;
+        if (total_copy) *total_copy = *total;
+    }
 }
 
 template <typename OutT>
-hipError_t exclusive_scan(int64_t n, const int32_t *in, OutT *out, int64_t *tmp, hipStream_t st) {
-    int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
-    if (tiles < 1) tiles = 1;
+hipError_t exclusive_scan(int64_t n, const int32_t *in, OutT *out, int64_t *tmp, int64_t *total_copy, hipStream_t st) {
+    if (n <= SMALL_MAX) {
+        hipLaunchKernelGGL(k_scan_small<OutT>, dim3(1), dim3(SMALL_THREADS), 0, st, n, in, out, total_copy);
+        return hipGetLastError();
+    }
+    const int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
     // tmp layout: [tiles] tile sums, then [1] total
     hipLaunchKernelGGL(k_scan_tile<OutT>, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, st, n, in, out, tmp);
     hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, st, tiles, tmp, tmp + tiles);
     hipLaunchKernelGGL(k_scan_add<OutT>, dim3((unsigned)((n + 1 + 255) / 256)), dim3(256), 0, st, n, out, tmp,
-                       tmp + tiles);
+                       tmp + tiles, total_copy);
     return hipGetLastError();
 }
 
 unsigned blocks_for(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
+
+struct Geometry {
+    double inv_h, rc2, lim2;
+    uint32_t mask;
+    int b;
+};
+
+Geometry geometry(const NbrWork &w, double r_cut) {
+    Geometry g;
+    const double h = r_cut * CELL_PAD;
+    g.inv_h = 1.0 / h;
+    g.rc2 = r_cut * r_cut;
+    // a cell is skipped when its box is farther than r_cut from the center,
+    // tested in cell units with a relative margin far above rounding
+    g.lim2 = (r_cut * g.inv_h) * (r_cut * g.inv_h) * (1.0 + 1e-6);
+    g.mask = (uint32_t)(w.H - 1);
+    int k = 0;
+    while ((int64_t(1) << k) < w.H) ++k;
+    g.b = std::min(10, k / 3);
+    return g;
+}
 
 } // namespace
 
 hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const int32_t *Z,
                       const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers, double r_cut,
                       int64_t *row_ptr, hipStream_t st) {
-    const double h = r_cut * CELL_PAD, inv_h = 1.0 / h, rc2 = r_cut * r_cut;
-    const uint32_t mask = (uint32_t)(w.H - 1);
+    const Geometry g = geometry(w, r_cut);
     hipError_t e;
-    if ((e = hipMemsetAsync(w.bucket_count, 0, sizeof(int32_t) * w.H, st)) != hipSuccess) return e;
-    if ((e = hipMemsetAsync(w.bucket_fill, 0, sizeof(int32_t) * w.H, st)) != hipSuccess) return e;
-    if ((e = hipMemsetAsync(w.flags, 0, sizeof(int32_t) * 4, st)) != hipSuccess) return e;
+    // flags, density work counters and both bucket arrays are one zeroed block
+    if ((e = hipMemsetAsync(w.zero, 0, w.zero_bytes, st)) != hipSuccess) return e;
     const unsigned gb = blocks_for(n_atoms, 256);
     if (pos64)
-        hipLaunchKernelGGL(k_prepare<double>, dim3(gb), dim3(256), 0, st, n_atoms, (const double *)pos, Z, lut,
-                           spec, w.atom_cell, w.bucket_count, mask, inv_h, w.flags);
+        hipLaunchKernelGGL(k_prepare<double>, dim3(gb), dim3(256), 0, st, n_atoms, (const double *)pos, Z, lut, spec,
+                           w.atom_cell, w.bucket_count, g.mask, g.b, g.inv_h, w.flags);
     else
-        hipLaunchKernelGGL(k_prepare<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos, Z, lut,
-                           spec, w.atom_cell, w.bucket_count, mask, inv_h, w.flags);
-    if ((e = exclusive_scan<int32_t>(w.H, w.bucket_count, w.bucket_start, w.scan_tmp, st)) != hipSuccess)
+        hipLaunchKernelGGL(k_prepare<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos, Z, lut, spec,
+                           w.atom_cell, w.bucket_count, g.mask, g.b, g.inv_h, w.flags);
+    if ((e = exclusive_scan<int32_t>(w.H, w.bucket_count, w.bucket_start, w.scan_tmp, nullptr, st)) != hipSuccess)
         return e;
-    if (pos64)
-        hipLaunchKernelGGL(k_bucket_fill<double>, dim3(gb), dim3(256), 0, st, n_atoms, (const double *)pos,
-                           w.atom_cell, w.bucket_start, w.bucket_fill, w.sorted_cell, w.sorted_pos, w.sorted_atom);
-    else
-        hipLaunchKernelGGL(k_bucket_fill<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos,
-                           w.atom_cell, w.bucket_start, w.bucket_fill, w.sorted_cell, w.sorted_pos, w.sorted_atom);
-    const unsigned gc = blocks_for(nc, 4);
-    if (pos64)
-        hipLaunchKernelGGL(k_count<double>, dim3(gc), dim3(256), 0, st, n_atoms, nc, centers, (const double *)pos,
-                           w.atom_cell, w.bucket_start, w.sorted_cell, w.sorted_pos, w.sorted_atom, mask, rc2, w.deg,
-                           w.flags);
-    else
-        hipLaunchKernelGGL(k_count<float>, dim3(gc), dim3(256), 0, st, n_atoms, nc, centers, (const float *)pos,
-                           w.atom_cell, w.bucket_start, w.sorted_cell, w.sorted_pos, w.sorted_atom, mask, rc2, w.deg,
-                           w.flags);
+    const unsigned gc = blocks_for(nc, NBR_WAVES);
+    if (pos64) {
+        hipLaunchKernelGGL(k_bucket_fill<double>, dim3(gb), dim3(256), 0, st, n_atoms, (const double *)pos, spec,
+                           w.atom_cell, w.bucket_start, w.bucket_fill, (double4 *)w.sorted_rec, w.sorted_spec);
+        hipLaunchKernelGGL(k_collect<double>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, n_atoms, nc, centers,
+                           (const double *)pos, w.atom_cell, w.bucket_start, (const double4 *)w.sorted_rec,
+                           w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
+    } else {
+        hipLaunchKernelGGL(k_bucket_fill<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos, spec,
+                           w.atom_cell, w.bucket_start, w.bucket_fill, (float4 *)w.sorted_rec, w.sorted_spec);
+        hipLaunchKernelGGL(k_collect<float>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, n_atoms, nc, centers,
+                           (const float *)pos, w.atom_cell, w.bucket_start, (const float4 *)w.sorted_rec,
+                           w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, st);
+    return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, (int64_t *)(w.flags + 4), st);
 }
 
-hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const uint8_t *spec,
-                      int64_t nc, const int32_t *centers, double r_cut, const int64_t *row_ptr, int32_t *cols,
+hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,
+                      const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, int32_t *cols,
                       hipStream_t st) {
     (void)n_atoms;
-    const double rc2 = r_cut * r_cut;
-    const uint32_t mask = (uint32_t)(w.H - 1);
-    if (pos64)
-        hipLaunchKernelGGL(k_fill_sort<double>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers, (const double *)pos,
-                           spec, w.atom_cell, w.bucket_start, w.sorted_cell, w.sorted_pos, w.sorted_atom, mask, rc2,
-                           row_ptr, cols);
-    else
-        hipLaunchKernelGGL(k_fill_sort<float>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers, (const float *)pos,
-                           spec, w.atom_cell, w.bucket_start, w.sorted_cell, w.sorted_pos, w.sorted_atom, mask, rc2,
-                           row_ptr, cols);
+    const Geometry g = geometry(w, r_cut);
+    hipLaunchKernelGGL(k_pack, dim3(blocks_for(nc, 4)), dim3(256), 0, st, nc, row_ptr, w.slots, cols);
+    if (long_rows) {
+        if (pos64)
+            hipLaunchKernelGGL(k_collect_long<double>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers,
+                               (const double *)pos, w.atom_cell, w.bucket_start, (const double4 *)w.sorted_rec,
+                               w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, row_ptr, cols);
+        else
+            hipLaunchKernelGGL(k_collect_long<float>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers,
+                               (const float *)pos, w.atom_cell, w.bucket_start, (const float4 *)w.sorted_rec,
+                               w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, row_ptr, cols);
+    }
     return hipGetLastError();
 }
 

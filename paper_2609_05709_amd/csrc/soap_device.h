@@ -525,7 +525,8 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
 //
 // Persistent: a workgroup is bound to one l-group g (blockIdx % G), keeps
 // that group's basis tables in LDS, and takes centers from an atomic work
-// counter.  Per center, each wave runs its own tiles of W edges: staging
+// counter (64-bit, zeroed with the neighbour list and never reset between
+// launches: a launch subtracts the count taken before it, base).  Per center, each wave runs its own tiles of W edges: staging
 // (harmonics, gradients, radial factors) in the wave's LDS, then every lane
 // adds each edge's contribution to the coefficient entries (a, lm) it owns,
 // in registers that persist over the wave's tiles:
@@ -534,11 +535,9 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
 // (D = sum over neighbours of dc/dr_j = -dc/dr_i).  Rows are sorted by
 // species, so the registers are flushed into the shared LDS accumulators
 // (float64 LDS atomics) only when the species changes and at the end.  Then
-// the workgroup writes the power spectrum and the center block
-// -K_l sum_m (D^mu c^nu + c^mu D^nu).  Both are products over m of the
-// coefficient matrices C_l[u][m] (u = species * n + n), per l: P_l = C_l C_l^T
-// and J_l = -K_l (D_l C_l^T + C_l D_l^T), taken on the matrix cores in
-// 16 x 16 tiles of (u, v), u <= v.
+// the descriptor path writes the power spectrum of the group's l
+// (power_tiles); the Jacobian path leaves c and D in scratch for k_outputs
+// and k_jacobian.
 // ---------------------------------------------------------------------------
 constexpr int NWD = 4, BSD = 64 * NWD;
 constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 64 * KE
@@ -553,7 +552,8 @@ __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, in
 
 template <typename PosT, typename OutT, bool JAC>
 __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
-                                                 int *__restrict__ work, OutT *__restrict__ desc,
+                                                 unsigned long long *__restrict__ work, uint64_t base,
+                                                 OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,
                                                  double *__restrict__ c_scratch) {
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
@@ -612,7 +612,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     int spec_i = 0;
     double3 pi = make_double3(0.0, 0.0, 0.0);
     auto fetch = [&]() {
-        if (tid == 0) s_next = atomicAdd(&work[g], 1);
+        if (tid == 0) s_next = (int64_t)(atomicAdd(&work[g], 1ull) - base);
         lds_barrier();
         ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
         lds_barrier(); // s_next is rewritten by the next fetch

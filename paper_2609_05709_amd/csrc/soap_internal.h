@@ -42,25 +42,34 @@ struct Rows {
 };
 
 // ---- neighbour search (neighbors.hip) ----
+constexpr int TCAP = 128; // neighbours per center kept by the collecting pass (longer rows: second pass)
+
 struct NbrWork {
-    int64_t H;              // hash buckets (power of two)
-    int32_t *bucket_count;  // [H]
-    int32_t *bucket_start;  // [H+1]
-    int32_t *bucket_fill;   // [H]
-    int4 *atom_cell;        // [n_atoms] cx, cy, cz, bucket
-    int4 *sorted_cell;      // [n_atoms]
-    double4 *sorted_pos;    // [n_atoms]
-    int32_t *sorted_atom;   // [n_atoms]
-    int32_t *deg;           // [nc]
-    int64_t *scan_tmp;      // block sums
-    int32_t *flags;         // [4]: error bits, max degree
+    int64_t H;                   // hash buckets (power of two)
+    void *zero;                  // zeroed at every build: flags, work counters, bucket counts and fills
+    size_t zero_bytes;
+    int32_t *flags;              // [4] error bits, max degree, rows above TCAP, -; then int64 total degree
+    unsigned long long *work;    // [MAX_GROUPS] density work counters
+    int32_t *bucket_count;       // [H]
+    int32_t *bucket_fill;        // [H]
+    int32_t *bucket_start;       // [H+1]
+    int4 *atom_cell;             // [n_atoms] cx, cy, cz, bucket
+    void *sorted_rec;            // [n_atoms] float4 / double4: position, atom index
+    uint8_t *sorted_spec;        // [n_atoms]
+    int32_t *deg;                // [nc]
+    int32_t *slots;              // [nc][TCAP] ordered rows of up to TCAP neighbours
+    int64_t *scan_tmp;           // block sums
 };
+// bytes of the zeroed block for H buckets, and the offsets of its parts
+constexpr size_t NBR_FLAGS_BYTES = 64, NBR_WORK_BYTES = 8 * (MAX_GROUPS + 1);
+inline size_t nbr_zero_bytes(int64_t H) { return NBR_FLAGS_BYTES + NBR_WORK_BYTES + 8 * (size_t)H; }
 
 hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const int32_t *Z,
                       const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers, double r_cut,
                       int64_t *row_ptr, hipStream_t st);
-hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const uint8_t *spec,
-                      int64_t nc, const int32_t *centers, double r_cut, const int64_t *row_ptr, int32_t *cols,
+// long_rows: some row is longer than TCAP (flags[2] > 0)
+hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,
+                      const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, int32_t *cols,
                       hipStream_t st);
 
 // ---- descriptor kernels (soap_kernels.hip) ----
@@ -88,9 +97,11 @@ hipError_t set_lds_limits();
 
 // desc (may be NULL; descriptor path), c_out (may be NULL, dtype), c_scratch (jac only, float64,
 // [center][c, Dx, Dy, Dz][lm][species n])
+// work: per-group counters, zeroed at the neighbour build and never reset in
+// between; *epoch counts the increments made since then (advanced here).
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
-                          const DensityLaunch &cfg, int *work, void *desc, void *c_out, void *jself, double *c_scratch,
-                          hipStream_t st);
+                          const DensityLaunch &cfg, unsigned long long *work, uint64_t *epoch, void *desc, void *c_out,
+                          void *jself, double *c_scratch, hipStream_t st);
 // power spectrum and center block from the coefficient scratch (Jacobian
 // path): l-groups of the output kernel, each sized to its LDS budget
 struct OutPlan {

@@ -121,30 +121,32 @@ hipError_t set_lds_limits() {
 }
 
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
-                          const DensityLaunch &cfg, int *work, void *desc, void *c_out, void *jself, double *c_scratch,
-                          hipStream_t st) {
+                          const DensityLaunch &cfg, unsigned long long *work, uint64_t *epoch, void *desc, void *c_out,
+                          void *jself, double *c_scratch, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
-    hipError_t e = hipMemsetAsync(work, 0, sizeof(int) * P.n_groups, st);
-    if (e != hipSuccess) return e;
-    int64_t per_group = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
+    const int64_t per_group = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
+    const uint64_t base = *epoch;
     dim3 grid((unsigned)(per_group * P.n_groups)), block(BSD);
     if (f64) {
         if (jac)
             hipLaunchKernelGGL((dev::k_density<double, double, true>), grid, block, cfg.lds, st, P, R, (const double *)pos,
-                               cfg.W, work, (double *)desc, (double *)c_out, (double *)jself, c_scratch);
+                               cfg.W, work, base, (double *)desc, (double *)c_out, (double *)jself, c_scratch);
         else
             hipLaunchKernelGGL((dev::k_density<double, double, false>), grid, block, cfg.lds, st, P, R,
-                               (const double *)pos, cfg.W, work, (double *)desc, (double *)c_out, (double *)jself,
-                               c_scratch);
+                               (const double *)pos, cfg.W, work, base, (double *)desc, (double *)c_out,
+                               (double *)jself, c_scratch);
     } else {
         if (jac)
             hipLaunchKernelGGL((dev::k_density<float, float, true>), grid, block, cfg.lds, st, P, R, (const float *)pos,
-                               cfg.W, work, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
+                               cfg.W, work, base, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
         else
             hipLaunchKernelGGL((dev::k_density<float, float, false>), grid, block, cfg.lds, st, P, R, (const float *)pos,
-                               cfg.W, work, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
+                               cfg.W, work, base, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
     }
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    // every workgroup takes each of its centers plus one final, empty fetch
+    if (e == hipSuccess) *epoch += (uint64_t)(R.nc + per_group);
+    return e;
 }
 
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,

@@ -81,6 +81,41 @@ def test_neighbors_at_exact_cutoff():
     check_rows(g64, st, rc, np.arange(st.n_atoms), wl.species)
 
 
+def test_rows_longer_than_slot_capacity():
+    """Centers with more than 128 neighbours (the first pass keeps rows up to
+    128 long; longer rows are collected again) next to centers with few."""
+    core = workloads.multispecies_sphere(260, 17, 2.6, 0.3, {1: 130, 8: 130})
+    ring = [[30.0 * np.cos(t), 30.0 * np.sin(t), 0.5 * k] for k, t in enumerate(np.linspace(0, 2 * np.pi, 40,
+                                                                                            endpoint=False))]
+    pos = np.concatenate([core.pos, np.asarray(ring, dtype=np.float32)])
+    Z = np.concatenate([core.Z, np.array([1, 8] * 20, dtype=np.int32)])
+    st = _st(pos, Z)
+    wl = _wl(n_max=2, l_max=2)
+    g, _ = _compare(wl, st, "float32")
+    deg = np.diff(g["row"])
+    assert deg.max() > 128 and deg.min() < 128
+
+
+def test_neighbors_diagonal_far_from_origin():
+    """Neighbours along the cube diagonals, a hair inside and outside r_cut,
+    around centers far from the origin on both sides (negative cell
+    coordinates, high bits of the cell key), classified as the oracle does."""
+    rc = 4.0
+    pts = []
+    for base in ([5123.25, -7311.5, 911.125], [-20480.0, 20480.0, -4096.5], [0.5, 0.25, -0.125]):
+        b = np.asarray(base)
+        pts.append(b)
+        for k, sgn in enumerate(np.array(np.meshgrid([-1, 1], [-1, 1], [-1, 1])).reshape(3, -1).T):
+            for f in (1 - 1e-6, 1 + 1e-6, 0.999, 1.001):
+                pts.append(b + sgn * rc * f / np.sqrt(3.0) + 1e-3 * k)
+    pts = np.asarray(pts, dtype=np.float32)
+    st = _st(pts, [1, 8] * (len(pts) // 2) + [1] * (len(pts) % 2))
+    wl = _wl(species=(1, 8), r_cut=rc, n_max=2, l_max=2)
+    for dtype in ("float32", "float64"):
+        g = gpu_run(wl, st, dtype)
+        check_rows(g, st, rc, np.arange(st.n_atoms), wl.species)
+
+
 def test_unknown_species_is_an_error():
     import torch
     from paper_2609_05709_amd.soap import SOAP_ESPECIES, Soap, SoapError
