@@ -19,7 +19,8 @@
 //          bucket fill (position + atom records), then one wave per center
 //          collects its neighbour keys (species, atom) in LDS, ranks them
 //          (keys are unique) and writes the ordered row to a fixed-capacity
-//          slot (TCAP entries) with its degree; CSR row offsets by scan.
+//          slot (TCAP entries) with its degree; CSR row offsets by scan,
+//          which also finds the largest degree and the rows above TCAP.
 // Phase 2 (after the host has read the total): the slots are packed into
 //          the CSR rows; rows longer than TCAP are collected again, with up
 //          to MAX_DEGREE keys in LDS.
@@ -119,18 +120,26 @@ __global__ void k_bucket_fill(int64_t n, const PosT *__restrict__ pos, const uin
 }
 
 // The candidates of one center: the atoms of the buckets of the (up to) 27
-// cells around it, concatenated.  Lanes 0..26 look up one cell each; a
-// prefix over the bucket sizes then lets lane t take candidates t, t + 64,
-// ... so the loads of one center spread over the whole wave.
+// cells around it, concatenated.  Lanes 0..26 look up one cell each and
+// write the sorted-record index of each of the cell's atoms into the wave's
+// candidate list (cand[t], t < total); then lane l takes candidates l,
+// l + 64, ... so the loads of one center spread over the whole wave.  Lists
+// longer than the LDS list (cap) are walked through the bucket offsets.
 struct CellSlots {
     int off[28];   // prefix of bucket sizes
     int start[27]; // first sorted slot of each bucket
 };
 
-__device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 ci, double3 pi, double inv_h,
-                                                 double lim2, int b, const int32_t *__restrict__ start,
-                                                 uint32_t mask) {
-    int sz = 0;
+// cell of a position: the same expression as k_prepare's
+__device__ __forceinline__ int4 cell_of(double3 p, double inv_h) {
+    return make_int4((int)floor(p.x * inv_h), (int)floor(p.y * inv_h), (int)floor(p.z * inv_h), 0);
+}
+
+__device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int *cand, int cap, int lane, double3 pi,
+                                                 double inv_h, double lim2, int b,
+                                                 const int32_t *__restrict__ start, uint32_t mask) {
+    const int4 ci = cell_of(pi, inv_h);
+    int sz = 0, s0 = 0;
     if (lane < 27) {
         const int dx = lane % 3 - 1, dy = (lane / 3) % 3 - 1, dz = lane / 9 - 1;
         // gap from the center to the cell's box along each axis, in cell units
@@ -141,7 +150,7 @@ __device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 c
         const double g2 = fmax(gx, 0.0) * fmax(gx, 0.0) + fmax(gy, 0.0) * fmax(gy, 0.0) + fmax(gz, 0.0) * fmax(gz, 0.0);
         if (g2 <= lim2) {
             const uint32_t k = cell_key(ci.x + dx, ci.y + dy, ci.z + dz, b, mask);
-            const int s0 = start[k];
+            s0 = start[k];
             sz = start[k + 1] - s0;
             cs.start[lane] = s0;
         }
@@ -154,20 +163,24 @@ __device__ __forceinline__ int wave_prefix_cells(CellSlots &cs, int lane, int4 c
     }
     if (lane < 27) cs.off[lane + 1] = v;
     if (lane == 0) cs.off[0] = 0;
+    const int total = __shfl(v, 26, 64);
+    if (total <= cap)
+        for (int k = 0; k < sz; ++k) cand[v - sz + k] = s0 + k;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    return cs.off[27];
+    return total;
 }
 
 // Collect the neighbour keys (species << 32 | atom) of center atom i into
-// keys[0..cap) in candidate order; returns the degree (which may exceed cap:
-// the surplus keys are counted, not stored).  U candidates per lane are
-// loaded together.
+// keys[0..kcap) in candidate order; returns the degree (which may exceed
+// kcap: the surplus keys are counted, not stored).  U candidates per lane
+// are loaded together.
 template <typename PosT, int U>
-__device__ __forceinline__ int collect_keys(const CellSlots &cs, int total, int lane, int64_t i, double3 pi,
-                                            double rc2, const typename Rec<PosT>::type *__restrict__ srec,
-                                            const uint8_t *__restrict__ sspec, int64_t *keys, int cap) {
+__device__ __forceinline__ int collect_keys(const CellSlots &cs, const int *cand, int cap, int total, int lane,
+                                            int64_t i, double3 pi, double rc2,
+                                            const typename Rec<PosT>::type *__restrict__ srec,
+                                            const uint8_t *__restrict__ sspec, int64_t *keys, int kcap) {
     int base = 0, d = 0;
     for (int t0 = 0; t0 < total; t0 += 64 * U) {
         int slot[U];
@@ -176,8 +189,12 @@ __device__ __forceinline__ int collect_keys(const CellSlots &cs, int total, int 
             const int t = t0 + 64 * u + lane;
             slot[u] = -1;
             if (t < total) {
-                while (cs.off[d + 1] <= t) ++d; // t grows with u and t0: d only moves forward
-                slot[u] = cs.start[d] + (t - cs.off[d]);
+                if (total <= cap) {
+                    slot[u] = cand[t];
+                } else {
+                    while (cs.off[d + 1] <= t) ++d; // t grows with u and t0: d only moves forward
+                    slot[u] = cs.start[d] + (t - cs.off[d]);
+                }
             }
         }
         typename Rec<PosT>::type r[U];
@@ -194,7 +211,7 @@ __device__ __forceinline__ int collect_keys(const CellSlots &cs, int total, int 
             const bool hit = slot[u] >= 0 && j != (int32_t)i && within_cutoff(pi, Rec<PosT>::pos(r[u]), rc2);
             const uint64_t m = __ballot(hit);
             const int pre = __popcll(m & ((1ull << lane) - 1ull));
-            if (hit && base + pre < cap) keys[base + pre] = ((int64_t)sp[u] << 32) | (int64_t)(uint32_t)j;
+            if (hit && base + pre < kcap) keys[base + pre] = ((int64_t)sp[u] << 32) | (int64_t)(uint32_t)j;
             base += __popcll(m);
         }
     }
@@ -209,28 +226,37 @@ __device__ __forceinline__ void write_ranked(const int64_t *keys, int deg, int l
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     for (int k = lane; k < deg; k += 64) {
         const int64_t key = keys[k];
-        int rank = 0;
-        for (int t = 0; t < deg; ++t) rank += keys[t] < key;
-        out[rank] = (int32_t)(key & 0xffffffff);
+        int r0 = 0, r1 = 0, r2 = 0, r3 = 0, t = 0;
+        for (; t + 4 <= deg; t += 4) { // four independent LDS reads in flight
+            r0 += keys[t] < key;
+            r1 += keys[t + 1] < key;
+            r2 += keys[t + 2] < key;
+            r3 += keys[t + 3] < key;
+        }
+        for (; t < deg; ++t) r0 += keys[t] < key;
+        out[r0 + r1 + r2 + r3] = (int32_t)(key & 0xffffffff);
     }
 }
 
-constexpr int NBR_WAVES = 4; // centers per workgroup in the collecting pass
+constexpr int NBR_WAVES = 4;   // centers per workgroup in the collecting pass
+constexpr int CAND_CAP = 1024; // candidate list per wave in LDS
 
 // One wave per center.  Without a center list the centers are taken in
 // sorted-atom (cell) order, so the waves resident on a CU share cells.
 template <typename PosT>
 __global__ __launch_bounds__(64 * NBR_WAVES) void k_collect(
     int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos,
-    const int4 *__restrict__ cell, const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
+    const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
     const uint8_t *__restrict__ sspec, uint32_t mask, int b, double inv_h, double lim2, double rc2,
     int32_t *__restrict__ deg, int32_t *__restrict__ slots, int32_t *__restrict__ flags) {
     __shared__ CellSlots cslots[NBR_WAVES];
     __shared__ int64_t kbuf[NBR_WAVES][TCAP];
+    __shared__ int cbuf[NBR_WAVES][CAND_CAP];
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int64_t t = (int64_t)blockIdx.x * NBR_WAVES + w;
     if (t >= nc) return;
     int64_t c, i;
+    double3 pi;
     if (centers) {
         c = t;
         i = centers[c];
@@ -241,21 +267,21 @@ __global__ __launch_bounds__(64 * NBR_WAVES) void k_collect(
             }
             return;
         }
+        pi = load_pos(pos, i);
     } else {
-        i = Rec<PosT>::atom(srec[t]);
+        const typename Rec<PosT>::type r = srec[t];
+        i = Rec<PosT>::atom(r);
         c = i;
+        pi = Rec<PosT>::pos(r);
     }
     CellSlots &cs = cslots[w];
-    const double3 pi = load_pos(pos, i);
-    const int total = wave_prefix_cells(cs, lane, cell[i], pi, inv_h, lim2, b, start, mask);
+    const int total = wave_prefix_cells(cs, cbuf[w], CAND_CAP, lane, pi, inv_h, lim2, b, start, mask);
     int64_t *keys = kbuf[w];
-    const int dg = collect_keys<PosT, 4>(cs, total, lane, i, pi, rc2, srec, sspec, keys, TCAP);
+    const int dg = collect_keys<PosT, 4>(cs, cbuf[w], CAND_CAP, total, lane, i, pi, rc2, srec, sspec, keys, TCAP);
     if (dg <= TCAP) write_ranked(keys, dg, lane, slots + c * TCAP);
-    if (lane == 0) {
-        deg[c] = dg;
-        atomicMax(&flags[1], dg);
-        if (dg > TCAP) atomicAdd(&flags[2], 1);
-    }
+    // (the largest degree and the rows above TCAP are counted by the scan of
+    // deg: one atomic per center on a single address would serialise)
+    if (lane == 0) deg[c] = dg;
 }
 
 // CSR rows from the fixed-capacity slots; rows longer than TCAP are left to
@@ -275,8 +301,7 @@ __global__ __launch_bounds__(256) void k_pack(int64_t nc, const int64_t *__restr
 // 64-lane workgroup per center; other centers return at once).
 template <typename PosT>
 __global__ __launch_bounds__(64) void k_collect_long(
-    int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos, const int4 *__restrict__ cell,
-    const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
+    int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos, const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
     const uint8_t *__restrict__ sspec, uint32_t mask, int b, double inv_h, double lim2, double rc2,
     const int64_t *__restrict__ row_ptr, int32_t *__restrict__ cols) {
     __shared__ int64_t keys[MAX_DEGREE];
@@ -288,8 +313,8 @@ __global__ __launch_bounds__(64) void k_collect_long(
     if (dg <= TCAP) return;
     const int64_t i = centers ? (int64_t)centers[c] : c;
     const double3 pi = load_pos(pos, i);
-    const int total = wave_prefix_cells(cs, lane, cell[i], pi, inv_h, lim2, b, start, mask);
-    const int got = collect_keys<PosT, 4>(cs, total, lane, i, pi, rc2, srec, sspec, keys, MAX_DEGREE);
+    const int total = wave_prefix_cells(cs, nullptr, 0, lane, pi, inv_h, lim2, b, start, mask);
+    const int got = collect_keys<PosT, 4>(cs, nullptr, 0, total, lane, i, pi, rc2, srec, sspec, keys, MAX_DEGREE);
     write_ranked(keys, got < dg ? got : dg, lane, cols + r0);
 }
 
@@ -313,18 +338,48 @@ __device__ __forceinline__ int64_t block_exclusive(int64_t s, int64_t *part, int
     return part[threadIdx.x] - s;
 }
 
-// one workgroup for n <= SMALL_MAX; total also to *total_copy if given
+// Largest value and number of values above TCAP of the workgroup's inputs,
+// folded into stats[0] (max) and stats[1] (count) with one atomic each.
+template <int BS>
+__device__ __forceinline__ void block_degree_stats(int vmax, int over, int *red, int32_t *__restrict__ stats) {
+    for (int off = 32; off > 0; off >>= 1) {
+        vmax = max(vmax, __shfl_down(vmax, off, 64));
+        over += __shfl_down(over, off, 64);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        red[2 * (threadIdx.x >> 6)] = vmax;
+        red[2 * (threadIdx.x >> 6) + 1] = over;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < BS / 64; ++w) {
+            vmax = max(vmax, red[2 * w]);
+            over += red[2 * w + 1];
+        }
+        atomicMax(&stats[0], vmax);
+        atomicAdd(&stats[1], over);
+    }
+}
+
+// one workgroup for n <= SMALL_MAX; total also to *total_copy and degree
+// statistics to stats if given
 template <typename OutT>
 __global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const int32_t *__restrict__ in,
-                                                              OutT *__restrict__ out, int64_t *__restrict__ total_copy) {
+                                                              OutT *__restrict__ out, int64_t *__restrict__ total_copy,
+                                                              int32_t *__restrict__ stats) {
     __shared__ int64_t part[SMALL_THREADS];
+    __shared__ int red[2 * SMALL_THREADS / 64];
     const int64_t base = (int64_t)threadIdx.x * SMALL_ITEMS;
     int64_t v[SMALL_ITEMS], s = 0, total;
+    int vmax = 0, over = 0;
 #pragma unroll
     for (int k = 0; k < SMALL_ITEMS; ++k) {
         v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
         s += v[k];
+        vmax = max(vmax, (int)v[k]);
+        over += v[k] > TCAP;
     }
+    if (stats) block_degree_stats<SMALL_THREADS>(vmax, over, red, stats);
     int64_t run = block_exclusive<SMALL_THREADS>(s, part, &total);
 #pragma unroll
     for (int k = 0; k < SMALL_ITEMS; ++k) {
@@ -339,15 +394,21 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const i
 
 template <typename OutT>
 __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile(int64_t n, const int32_t *__restrict__ in,
-                                                            OutT *__restrict__ out, int64_t *__restrict__ sums) {
+                                                            OutT *__restrict__ out, int64_t *__restrict__ sums,
+                                                            int32_t *__restrict__ stats) {
     __shared__ int64_t part[SCAN_THREADS];
+    __shared__ int red[2 * SCAN_THREADS / 64];
     const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
     int64_t v[SCAN_ITEMS], s = 0, total;
+    int vmax = 0, over = 0;
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
         v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
         s += v[k];
+        vmax = max(vmax, (int)v[k]);
+        over += v[k] > TCAP;
     }
+    if (stats) block_degree_stats<SCAN_THREADS>(vmax, over, red, stats);
     int64_t run = block_exclusive<SCAN_THREADS>(s, part, &total); // exclusive within the tile
 #pragma unroll
     for (int k = 0; k < SCAN_ITEMS; ++k) {
@@ -387,15 +448,18 @@ __global__ void k_scan_add(int64_t n, OutT *__restrict__ out, const int64_t *__r
     }
 }
 
+// stats (may be NULL): [0] max of in, [1] count of in > TCAP, both folded in
+// with atomics (the caller zeroes them)
 template <typename OutT>
-hipError_t exclusive_scan(int64_t n, const int32_t *in, OutT *out, int64_t *tmp, int64_t *total_copy, hipStream_t st) {
+hipError_t exclusive_scan(int64_t n, const int32_t *in, OutT *out, int64_t *tmp, int64_t *total_copy, int32_t *stats,
+                          hipStream_t st) {
     if (n <= SMALL_MAX) {
-        hipLaunchKernelGGL(k_scan_small<OutT>, dim3(1), dim3(SMALL_THREADS), 0, st, n, in, out, total_copy);
+        hipLaunchKernelGGL(k_scan_small<OutT>, dim3(1), dim3(SMALL_THREADS), 0, st, n, in, out, total_copy, stats);
         return hipGetLastError();
     }
     const int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
     // tmp layout: [tiles] tile sums, then [1] total
-    hipLaunchKernelGGL(k_scan_tile<OutT>, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, st, n, in, out, tmp);
+    hipLaunchKernelGGL(k_scan_tile<OutT>, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, st, n, in, out, tmp, stats);
     hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(1024), 0, st, tiles, tmp, tmp + tiles);
     hipLaunchKernelGGL(k_scan_add<OutT>, dim3((unsigned)((n + 1 + 255) / 256)), dim3(256), 0, st, n, out, tmp,
                        tmp + tiles, total_copy);
@@ -441,24 +505,25 @@ hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool p
     else
         hipLaunchKernelGGL(k_prepare<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos, Z, lut, spec,
                            w.atom_cell, w.bucket_count, g.mask, g.b, g.inv_h, w.flags);
-    if ((e = exclusive_scan<int32_t>(w.H, w.bucket_count, w.bucket_start, w.scan_tmp, nullptr, st)) != hipSuccess)
+    if ((e = exclusive_scan<int32_t>(w.H, w.bucket_count, w.bucket_start, w.scan_tmp, nullptr, nullptr, st)) !=
+        hipSuccess)
         return e;
     const unsigned gc = blocks_for(nc, NBR_WAVES);
     if (pos64) {
         hipLaunchKernelGGL(k_bucket_fill<double>, dim3(gb), dim3(256), 0, st, n_atoms, (const double *)pos, spec,
                            w.atom_cell, w.bucket_start, w.bucket_fill, (double4 *)w.sorted_rec, w.sorted_spec);
         hipLaunchKernelGGL(k_collect<double>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, n_atoms, nc, centers,
-                           (const double *)pos, w.atom_cell, w.bucket_start, (const double4 *)w.sorted_rec,
+                           (const double *)pos, w.bucket_start, (const double4 *)w.sorted_rec,
                            w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
     } else {
         hipLaunchKernelGGL(k_bucket_fill<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos, spec,
                            w.atom_cell, w.bucket_start, w.bucket_fill, (float4 *)w.sorted_rec, w.sorted_spec);
         hipLaunchKernelGGL(k_collect<float>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, n_atoms, nc, centers,
-                           (const float *)pos, w.atom_cell, w.bucket_start, (const float4 *)w.sorted_rec,
+                           (const float *)pos, w.bucket_start, (const float4 *)w.sorted_rec,
                            w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, (int64_t *)(w.flags + 4), st);
+    return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, (int64_t *)(w.flags + 4), w.flags + 1, st);
 }
 
 hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,
@@ -470,11 +535,11 @@ hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool p
     if (long_rows) {
         if (pos64)
             hipLaunchKernelGGL(k_collect_long<double>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers,
-                               (const double *)pos, w.atom_cell, w.bucket_start, (const double4 *)w.sorted_rec,
+                               (const double *)pos, w.bucket_start, (const double4 *)w.sorted_rec,
                                w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, row_ptr, cols);
         else
             hipLaunchKernelGGL(k_collect_long<float>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers,
-                               (const float *)pos, w.atom_cell, w.bucket_start, (const float4 *)w.sorted_rec,
+                               (const float *)pos, w.bucket_start, (const float4 *)w.sorted_rec,
                                w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, row_ptr, cols);
     }
     return hipGetLastError();

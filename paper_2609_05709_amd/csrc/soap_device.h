@@ -525,8 +525,9 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
 //
 // Persistent: a workgroup is bound to one l-group g (blockIdx % G), keeps
 // that group's basis tables in LDS, and takes centers from an atomic work
-// counter (64-bit, zeroed with the neighbour list and never reset between
-// launches: a launch subtracts the count taken before it, base).  Per center, each wave runs its own tiles of W edges: staging
+// counter after a first, static one (64-bit, zeroed with the neighbour list
+// and never reset between launches: a launch subtracts the count taken
+// before it, base).  Per center, each wave runs its own tiles of W edges: staging
 // (harmonics, gradients, radial factors) in the wave's LDS, then every lane
 // adds each edge's contribution to the coefficient entries (a, lm) it owns,
 // in registers that persist over the wave's tiles:
@@ -611,11 +612,22 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     int64_t ci = 0, i = 0, e0 = 0, e1 = 0;
     int spec_i = 0;
     double3 pi = make_double3(0.0, 0.0, 0.0);
+    // the first center of each workgroup is static (blockIdx / G); the later
+    // ones come from the group's counter, past the per_group static ones
+    // (a burst of one atomic per workgroup on one address at the start would
+    // serialise)
+    const int64_t per_group = gridDim.x / G;
+    bool first = true;
     auto fetch = [&]() {
-        if (tid == 0) s_next = (int64_t)(atomicAdd(&work[g], 1ull) - base);
-        lds_barrier();
-        ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
-        lds_barrier(); // s_next is rewritten by the next fetch
+        if (first) {
+            ci = blockIdx.x / G;
+            first = false;
+        } else {
+            if (tid == 0) s_next = per_group + (int64_t)(atomicAdd(&work[g], 1ull) - base);
+            lds_barrier();
+            ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
+            lds_barrier();                                    // s_next is rewritten by the next fetch
+        }
         if (ci >= R.nc) return;
         i = R.centers ? (int64_t)R.centers[ci] : ci;
         pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);

@@ -144,8 +144,9 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
                                cfg.W, work, base, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
     }
     const hipError_t e = hipGetLastError();
-    // every workgroup takes each of its centers plus one final, empty fetch
-    if (e == hipSuccess) *epoch += (uint64_t)(R.nc + per_group);
+    // the counter is taken for every center but the per_group static ones,
+    // plus one final, empty fetch per workgroup
+    if (e == hipSuccess) *epoch += (uint64_t)R.nc;
     return e;
 }
 

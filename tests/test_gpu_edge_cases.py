@@ -157,6 +157,39 @@ def test_repeatable_bitwise():
         assert np.array_equal(a["jedge"][c], b["jedge"][c]) and np.array_equal(a["jself"][c], b["jself"][c])
 
 
+def test_repeated_calls_on_one_neighbour_list():
+    """Descriptor, coefficient and derivative calls repeated in any order on
+    one neighbour list (the density work counters carry over between calls),
+    then a rebuild for a smaller structure: every result equals the first one
+    or a fresh context's."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    wl = workloads.WATER64
+    st = wl.structure()
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    pos, Z = torch.from_numpy(st.pos).cuda(), torch.from_numpy(st.Z).cuda()
+    sp.build_neighbors(pos, Z)
+    d0 = sp.compute().clone()
+    dd, je, js = [t.clone() for t in sp.derivatives()]
+    c0 = sp.coefficients().clone()
+    for _ in range(3):
+        assert torch.equal(sp.compute(), d0)
+        d1, je1, js1 = sp.derivatives()
+        assert torch.equal(d1, dd) and torch.equal(je1, je) and torch.equal(js1, js)
+        assert torch.equal(sp.coefficients(), c0)
+    small = workloads.random_small(40, 5, 4.0, species=(1, 8))
+    p2, Z2 = torch.from_numpy(small.pos).cuda(), torch.from_numpy(small.Z).cuda()
+    sp.build_neighbors(p2, Z2)
+    fresh = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    fresh.build_neighbors(p2, Z2)
+    a, b = sp.derivatives(), fresh.derivatives()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    assert torch.equal(sp.compute(), fresh.compute())
+    sp.close()
+    fresh.close()
+
+
 def test_dense_scatter_matches_blocks():
     import torch
     from paper_2609_05709_amd.soap import Soap
