@@ -44,7 +44,6 @@ struct DevBuf {
     template <typename T> T *as() const { return static_cast<T *>(p); }
 };
 
-constexpr size_t DENSITY_LDS_BUDGET = 64 * 1024;
 constexpr size_t LDS_HARD_LIMIT = 159 * 1024; // leaves room for static LDS
 
 thread_local std::string g_create_error = "";
@@ -150,8 +149,11 @@ void build_feature_tables(soap_ctx *c) {
 
 // Split l = 0..lmax into contiguous groups such that each group's
 // coefficient entries fit the density kernel's registers (n * Lg <= 512) and
-// its LDS fits the budget; W = edges per wave iteration.
-int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *W_out, size_t *lds_out) {
+// its LDS fits the budget (the LDS share of a workgroup at the occupancy the
+// kernel's registers allow); W = edges per wave iteration, the widest that
+// fits.
+int plan_groups(const Params &P, int jac, bool f64, size_t budget, int *lgrp, int *ngroups, int *W_out,
+                size_t *lds_out) {
     const int lw = P.lmax + 1;
     for (int G = 1; G <= lw; ++G) {
         // contiguous groups balancing sum over l of (2l+1): cut k at the l with
@@ -170,10 +172,11 @@ int plan_groups(const Params &P, int jac, int *lgrp, int *ngroups, int *W_out, s
         for (int k = 0; k < G; ++k)
             if (P.n * (bounds[k + 1] * bounds[k + 1] - bounds[k] * bounds[k]) > 64 * DENSITY_KE) ok = false;
         if (!ok) continue;
-        for (int W : {4, 2, 1}) {
+        for (int W : {8, 4, 2, 1}) {
             size_t worst = 0;
-            for (int k = 0; k < G; ++k) worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], W));
-            if (worst <= DENSITY_LDS_BUDGET || (W == 1 && worst <= LDS_HARD_LIMIT)) {
+            for (int k = 0; k < G; ++k)
+                worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], W, f64));
+            if (worst <= budget || (W == 1 && worst <= LDS_HARD_LIMIT)) {
                 for (int k = 0; k <= G; ++k) lgrp[k] = bounds[k];
                 *ngroups = G;
                 *W_out = W;
@@ -191,13 +194,17 @@ int plan_launches(soap_ctx *c) {
     size_t lds;
     int ncu = 256;
     (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
+    const bool f64d = c->dtype == SOAP_FP64;
     for (int jac = 0; jac < 2; ++jac) {
         int *lgrp = jac ? c->lgrp_jac : c->lgrp_desc, *G = jac ? &c->groups_jac : &c->groups_desc;
-        if (plan_groups(P, jac, lgrp, G, &Wd, &lds) != 0)
+        // workgroups per CU the registers allow (no LDS), and the LDS share of each
+        const int by_regs = std::max(1, density_blocks_per_cu(f64d, jac != 0, 0));
+        const size_t budget = std::min(LDS_HARD_LIMIT, (size_t)(159 * 1024) / (size_t)by_regs);
+        if (plan_groups(P, jac, f64d, budget, lgrp, G, &Wd, &lds) != 0)
             return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
         c->dens_cfg[jac].W = Wd;
         c->dens_cfg[jac].lds = lds;
-        const int per_cu = density_blocks_per_cu(c->dtype == SOAP_FP64, jac != 0, lds);
+        const int per_cu = density_blocks_per_cu(f64d, jac != 0, lds);
         c->dens_cfg[jac].blocks = std::max(1, ncu * per_cu / *G);
     }
     if (plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) != 0)

@@ -55,6 +55,22 @@ template <> struct Pair<float> {
     static __device__ __forceinline__ float2 make(double a, double b) { return make_float2((float)a, (float)b); }
 };
 
+// four consecutive LDS values (16-byte aligned) as float64
+__device__ __forceinline__ void load4(const double *p, double &a, double &b, double &c, double &d) {
+    const double2 u = *(const double2 *)p, v = *(const double2 *)(p + 2);
+    a = u.x;
+    b = u.y;
+    c = v.x;
+    d = v.y;
+}
+__device__ __forceinline__ void load4(const float *p, double &a, double &b, double &c, double &d) {
+    const float4 u = *(const float4 *)p;
+    a = u.x;
+    b = u.y;
+    c = u.z;
+    d = u.w;
+}
+
 // floor(x / d) for 0 <= x < 2^22 with inv = 1/d correctly rounded: the
 // relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
 // next integer
@@ -68,8 +84,9 @@ __device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x +
 //   S_l,m = Nt_lm R_l C_m, S_l,-m = Nt_lm R_l S_m, Nt_lm = N_lm (2m-1)!! / (l-m)!.
 // Stores l in [l_lo, l_hi) at Y[(l^2 + l +- m - lm_base) * ls].
 // ---------------------------------------------------------------------------
+template <typename YT>
 __device__ __forceinline__ void sh_col_y(int m, int l_lo, int l_hi, double x, double y, double z,
-                                         const double *__restrict__ Nt, int ldN, double *__restrict__ Y, int ls,
+                                         const double *__restrict__ Nt, int ldN, YT *__restrict__ Y, int ls,
                                          int lm_base) {
     const double r2 = x * x + y * y + z * z;
     double c = 1.0, s = 0.0;
@@ -90,10 +107,10 @@ __device__ __forceinline__ void sh_col_y(int m, int l_lo, int l_hi, double x, do
             const double v = Nt[l * ldN + m] * R;
             const int o = l * l + l - lm_base;
             if (m == 0) {
-                Y[o * ls] = v;
+                Y[o * ls] = (YT)v;
             } else {
-                Y[(o + m) * ls] = v * c;
-                Y[(o - m) * ls] = v * s;
+                Y[(o + m) * ls] = (YT)(v * c);
+                Y[(o - m) * ls] = (YT)(v * s);
             }
         }
     }
@@ -285,8 +302,8 @@ struct YLayout {
     int es, cs, ls, lmY0;
 };
 
-template <bool GRAD, typename BT = double, int NT = 0, int LWT = 0>
-__device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, double *__restrict__ YY, YLayout yl,
+template <bool GRAD, typename BT = double, int NT = 0, int LWT = 0, typename YT = double>
+__device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT *__restrict__ YY, YLayout yl,
                                             typename Pair<BT>::type *__restrict__ BB, double *__restrict__ X,
                                             const double *__restrict__ geo, int nb, int lane, int lg0, int lg1,
                                             bool scaleK) {
@@ -330,31 +347,31 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, do
             const int e = qdiv(it, inv_T), t = it - e * Tg + t0;
             const double2 c01 = T.gcoef[2 * t], c2p = T.gcoef[2 * t + 1];
             const int lm = (int)c2p.y, l = lm & 0xff, m = lm >> 8;
-            double *Y = YY + e * yl.es;
+            YT *Y = YY + e * yl.es;
             const int lp = l > 0 ? l - 1 : 0, c0 = lp * lp + lp - yl.lmY0;
             const bool live = geo[4 * e + 3] != 0.0 && l > 0;
             // S'_k for k in {m+1, -(m+1), m-1, -(m-1), m, -m}, clamped into degree l-1
             auto sp = [&](int k) -> double {
                 const int kc = k < -lp ? -lp : (k > lp ? lp : k);
-                const double v = Y[(c0 + kc) * yl.ls];
+                const double v = (double)Y[(c0 + kc) * yl.ls];
                 return (live && k >= -lp && k <= lp) ? v : 0.0;
             };
             const double cA = c01.x, cB = c01.y, cC = c2p.x;
-            double *Dx = Y + yl.cs, *Dy = Y + 2 * yl.cs, *Dz = Y + 3 * yl.cs;
+            YT *Dx = Y + yl.cs, *Dy = Y + 2 * yl.cs, *Dz = Y + 3 * yl.cs;
             const int o = l * l + l - yl.lmY0;
             if (m == 0) {
-                Dx[o * yl.ls] = -cA * sp(1);
-                Dy[o * yl.ls] = -cA * sp(-1);
-                Dz[o * yl.ls] = cC * sp(0);
+                Dx[o * yl.ls] = (YT)(-cA * sp(1));
+                Dy[o * yl.ls] = (YT)(-cA * sp(-1));
+                Dz[o * yl.ls] = (YT)(cC * sp(0));
             } else {
                 const double pp = sp(m + 1), pn = sp(-(m + 1)), qp = sp(m - 1), qn = m > 1 ? sp(-(m - 1)) : 0.0;
                 const double zp = sp(m), zn = sp(-m);
-                Dx[(o + m) * yl.ls] = -cA * pp + cB * qp;
-                Dy[(o + m) * yl.ls] = -cA * pn - cB * qn;
-                Dz[(o + m) * yl.ls] = cC * zp;
-                Dx[(o - m) * yl.ls] = -cA * pn + cB * qn;
-                Dy[(o - m) * yl.ls] = cA * pp + cB * qp;
-                Dz[(o - m) * yl.ls] = cC * zn;
+                Dx[(o + m) * yl.ls] = (YT)(-cA * pp + cB * qp);
+                Dy[(o + m) * yl.ls] = (YT)(-cA * pn - cB * qn);
+                Dz[(o + m) * yl.ls] = (YT)(cC * zp);
+                Dx[(o - m) * yl.ls] = (YT)(-cA * pn + cB * qn);
+                Dy[(o - m) * yl.ls] = (YT)(cA * pp + cB * qp);
+                Dz[(o - m) * yl.ls] = (YT)(cC * zn);
             }
         }
     }
@@ -545,10 +562,15 @@ constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 
 
 __host__ __device__ __forceinline__ int dens_lgY0(int jac, int lg0) { return (jac && lg0 > 0) ? lg0 - 1 : lg0; }
 
-__host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, int jac, int lg0, int lg1, int W) {
+// Per-wave staging of k_density, in doubles: harmonics YY and radial pairs BB
+// at the output precision (sb = 4 or 8 bytes), the radial scratch X in
+// float64 (it enters dot products with cancelling basis coefficients).
+__host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, int jac, int lg0, int lg1, int W,
+                                                            int sb) {
     const int lgY0 = dens_lgY0(jac, lg0);
     const size_t LY = (size_t)(lg1 * lg1 - lgY0 * lgY0), lgc = (size_t)(lg1 - lg0);
-    return even(W * LY * (jac ? 4 : 1)) + 2 * W * P.n * lgc + even(W * stage_x_doubles(P, (int)lgc, lg1));
+    return even((W * LY * (jac ? 4 : 1) * sb + 7) / 8) + even((2 * W * P.n * lgc * sb + 7) / 8) +
+           even(W * stage_x_doubles(P, (int)lgc, lg1));
 }
 
 template <typename PosT, typename OutT, bool JAC>
@@ -580,11 +602,17 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
     double *c0 = cv.take((size_t)n);
-    Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W)};
+    // staging at the output precision ST: the harmonics and radial factors
+    // enter the float64 accumulators as products with relative rounding
+    // error of ST's order, which float32 outputs carry anyway
+    using ST = OutT;
+    using ST2 = typename Pair<ST>::type;
+    constexpr int SB = sizeof(ST);
+    Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W, SB)};
     // harmonics interleaved per lm as (S, dS/dx, dS/dy, dS/dz) for the Jacobian
     const YLayout yl = JAC ? YLayout{4 * LY, 1, 4, lmY0} : YLayout{LY, 0, 1, lmY0};
-    double *YY = wv.take((size_t)W * yl.es);
-    double2 *BB = (double2 *)wv.take(2 * (size_t)W * nlc);
+    ST *YY = (ST *)wv.take(((size_t)W * yl.es * SB + 7) / 8);
+    ST2 *BB = (ST2 *)wv.take((2 * (size_t)W * nlc * SB + 7) / 8);
     double *X = wv.take((size_t)W * stage_x_doubles(P, lgc, lg1));
 
     // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg
@@ -673,7 +701,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
             for (int off = wave * W; off < rbn; off += NWD * W) {
                 const int nb = (rbn - off) < W ? (rbn - off) : W;
                 const double *geo = rgeo + 4 * off;
-                stage_edges<JAC>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
+                stage_edges<JAC, ST, 0, 0, ST>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
                 for (int e = 0; e < nb; ++e) {
                     const int s = __builtin_amdgcn_readfirstlane(rsp[off + e]);
                     if (s != cur) {
@@ -681,21 +709,23 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                         cur = s;
                     }
                     const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
-                    const double *Ye = YY + e * yl.es;
-                    const double2 *Be = BB + e * nlc;
+                    const ST *Ye = YY + e * yl.es;
+                    const ST2 *Be = BB + e * nlc;
 #pragma unroll
                     for (int k = 0; k < KE; ++k) {
                         if (!own[k]) continue;
-                        const double2 bb = Be[oB[k]];
+                        const ST2 b2 = Be[oB[k]];
+                        const double bx = (double)b2.x, by = (double)b2.y;
                         if (JAC) {
-                            const double2 y01 = *(const double2 *)(Ye + oY[k]), y23 = *(const double2 *)(Ye + oY[k] + 2);
-                            const double bh = bb.y * y01.x;
-                            acc[k][0] += bb.x * y01.x;
-                            acc[k][1] += bh * rx + bb.x * y01.y;
-                            acc[k][2] += bh * ry + bb.x * y23.x;
-                            acc[k][3] += bh * rz + bb.x * y23.y;
+                            double y0, y1, y2, y3;
+                            load4(Ye + oY[k], y0, y1, y2, y3);
+                            const double bh = by * y0;
+                            acc[k][0] += bx * y0;
+                            acc[k][1] += bh * rx + bx * y1;
+                            acc[k][2] += bh * ry + bx * y2;
+                            acc[k][3] += bh * rz + bx * y3;
                         } else {
-                            acc[k][0] += bb.x * Ye[oY[k]];
+                            acc[k][0] += bx * (double)Ye[oY[k]];
                         }
                     }
                 }

@@ -83,7 +83,7 @@ struct JacLaunch {
     size_t lds;
 };
 
-size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W);
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64);
 int density_blocks_per_cu(bool f64, bool jac, size_t lds);
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, bool f64);

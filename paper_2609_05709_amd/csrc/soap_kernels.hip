@@ -5,12 +5,12 @@
 namespace soap {
 using namespace dev;
 
-size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W) {
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64) {
     const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0);
     const size_t SnL = (size_t)P.S * P.n * Lg;
     const int RBk = row_block(NWD * W);
     size_t d = table_doubles(P, lg1 - lg0) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W);
+               even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W, f64 ? 8 : 4);
     return d * 8;
 }
 
