@@ -598,7 +598,7 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
     hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0], c->nw.work,
                                   &c->work_epoch, desc, c_out, jself, scratch, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
-    if (jac) {
+    if (jac && P.n_groups > 1) { // with one l-group the density kernel writes desc and jself
         e = launch_outputs(P, c->out_plan, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
         if (e != hipSuccess) return hip_fail(c, e, "output kernel");
     }

@@ -537,6 +537,71 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
     }
 }
 
+// The four output rows of one center at once, for l in [lg0, lg0 + lgc):
+// the power spectrum and the three center block components, from c (X) and
+// D_x, D_y, D_z (X + d * xs, same layout as c: entry (u, lm) at
+// u * ldu + (lm - lm0) * ldm).  Per item (l, tile pair) the c chunk is read
+// once and the four accumulators are independent matrix-core chains.
+// Feature (q, l) of the power spectrum goes to r0[q * ldq + l - lbase], of
+// component d to r1[d * rs + q * ldq + l - lbase].
+template <typename OutT>
+__device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int xs, int ldu, int ldm, int Sn, int lm0,
+                                             int lg0, int lgc, OutT *__restrict__ r0, OutT *__restrict__ r1, int rs,
+                                             int ldq, int lbase, const int *__restrict__ qmap, int wave, int nw,
+                                             int lane, const double *__restrict__ Kl) {
+    const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
+    const int nitem = lgc * ntp;
+    const int ro = lane & 15, kk = lane >> 4;
+    for (int item = wave; item < nitem; item += nw) { // uniform per wave
+        const int lc = item / ntp, l = lg0 + lc;
+        int tp = item - lc * ntp, ti = 0;
+        while (tp >= ntile - ti) {
+            tp -= ntile - ti;
+            ++ti;
+        }
+        const int tj = ti + tp;
+        const int ua = 16 * ti + ro, vb = 16 * tj + ro; // A row, B column of this lane
+        const bool uok = ua < Sn, vok = vb < Sn;
+        const int oa = (uok ? ua : 0) * ldu + (l * l - lm0) * ldm;
+        const int ob = (vok ? vb : 0) * ldu + (l * l - lm0) * ldm;
+        dbl4 p = {0.0, 0.0, 0.0, 0.0}, jx = p, jy = p, jz = p;
+        for (int ch = 0; ch < (l >> 1) + 1; ++ch) {
+            const int m = 4 * ch + kk;
+            const bool mok = m <= 2 * l;
+            const int mo = (mok ? m : 0) * ldm;
+            const bool ma = mok && uok, mb = mok && vok;
+            const double ca = ma ? X[oa + mo] : 0.0, cb = mb ? X[ob + mo] : 0.0;
+            const double xa = ma ? X[xs + oa + mo] : 0.0, xb = mb ? X[xs + ob + mo] : 0.0;
+            const double ya = ma ? X[2 * xs + oa + mo] : 0.0, yb = mb ? X[2 * xs + ob + mo] : 0.0;
+            const double za = ma ? X[3 * xs + oa + mo] : 0.0, zb = mb ? X[3 * xs + ob + mo] : 0.0;
+            p = __builtin_amdgcn_mfma_f64_16x16x4f64(ca, cb, p, 0, 0, 0);
+            jx = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, cb, jx, 0, 0, 0);
+            jy = __builtin_amdgcn_mfma_f64_16x16x4f64(ya, cb, jy, 0, 0, 0);
+            jz = __builtin_amdgcn_mfma_f64_16x16x4f64(za, cb, jz, 0, 0, 0);
+            jx = __builtin_amdgcn_mfma_f64_16x16x4f64(ca, xb, jx, 0, 0, 0);
+            jy = __builtin_amdgcn_mfma_f64_16x16x4f64(ca, yb, jy, 0, 0, 0);
+            jz = __builtin_amdgcn_mfma_f64_16x16x4f64(ca, zb, jz, 0, 0, 0);
+        }
+        // lane holds rows u = 16 ti + kk + 4 r of column v = 16 tj + ro
+        const int v = 16 * tj + ro;
+        const double K = Kl[l];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int u = 16 * ti + kk + 4 * r;
+            if (u < Sn && v < Sn) {
+                const int q = qmap[u * Sn + v];
+                if (q >= 0) {
+                    const int f = q * ldq + l - lbase;
+                    store_out(r0 + f, K * p[r]);
+                    store_out(r1 + f, -K * jx[r]);
+                    store_out(r1 + (rs + f), -K * jy[r]);
+                    store_out(r1 + (2 * rs + f), -K * jz[r]);
+                }
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------------------
 // k_density
 //
@@ -751,10 +816,18 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                 store_out(c_out + (cw * Sn + sa) * Lfull + lm0 + lmg, cacc[it]);
             }
         if (JAC) {
-            // c and D, transposed to [comp][lm][s n], for k_outputs and the
-            // Jacobian kernel's matrix-core operand
+            // with one l-group the workgroup holds all of c and D: it writes
+            // the power spectrum and the center block itself (whole rows of
+            // one center from one workgroup, so their lines fill in one L2);
+            // the scratch then only needs c.  Otherwise c and D go to
+            // scratch for k_outputs.  Both transposed to [comp][lm][s n]: c
+            // is the Jacobian kernel's matrix-core operand.
+            const bool whole = G == 1;
+            if (whole)
+                power_tiles4<OutT>(cacc, SnL, Lg, 1, Sn, 0, 0, lw, desc + cw * P.F, jself + cw * 3 * P.F, P.F, lw, 0,
+                                   P.qmap, wave, NWD, lane, T.Kl);
             double *sc = c_scratch + cw * 4 * (size_t)Lfull * Sn;
-            for (int it = tid; it < 4 * SnL; it += BSD) {
+            for (int it = tid; it < (whole ? 1 : 4) * SnL; it += BSD) {
                 const int comp = it / SnL, rem = it - comp * SnL;
                 const int sa = qdiv(rem, inv_Lg), lmg = rem - sa * Lg;
                 sc[((size_t)comp * Lfull + lm0 + lmg) * Sn + sa] = cacc[it];
@@ -767,64 +840,78 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
 // ---------------------------------------------------------------------------
 // k_outputs: power spectrum and center block for the Jacobian path, from the
 // coefficients c and D that k_density left in scratch
-// ([center][c, Dx, Dy, Dz][lm][species n]).  Work item = (center, output
-// row): the descriptor row or one Cartesian row of the center block.  A
-// resident grid (a multiple of 8 workgroups) strides over the items: the
-// items are short, and launching one workgroup per item left the CUs mostly
-// empty.  The four items of a center fall to workgroups of one XCD
-// (workgroups are dealt to the 8 XCDs round-robin), so c is read into one
-// L2.  Per l-group of O (usually one group covering every l) c and the needed
-// component of D go to LDS, the tiles fill an LDS copy of the row, and the
-// row leaves in whole, contiguous lines.
+// ([center][c, Dx, Dy, Dz][lm][species n]).  One workgroup per center.  Per
+// l-group of O (usually one group covering every l), the four slabs (c, Dx,
+// Dy, Dz) of the group go to LDS in one pass (all loads in flight together),
+// the matrix-core tiles of the four output rows (descriptor, d/dx, d/dy,
+// d/dz) fill LDS copies of the rows, spread evenly over the waves, and the
+// rows leave in whole, contiguous lines.  One load phase and one store
+// phase per group: the kernel is latency-bound, not bandwidth-bound.
 // ---------------------------------------------------------------------------
 constexpr int BSO = 256;
 
 __host__ __device__ __forceinline__ size_t outputs_group_doubles(const Params &P, int lg0, int lg1, int out_bytes) {
     const size_t Sn = (size_t)P.S * P.n, slab = (size_t)(lg1 * lg1 - lg0 * lg0) * Sn;
-    return even((Sn * Sn + 1) / 2) + 2 * even(slab) + even(((size_t)P.nq_full * (lg1 - lg0) * out_bytes + 7) / 8);
+    return even((Sn * Sn + 1) / 2) + 4 * even(slab) + 4 * even(((size_t)P.nq_full * (lg1 - lg0) * out_bytes + 7) / 8);
 }
 
 template <typename OutT>
-__global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, int64_t nc, const double *__restrict__ scratch,
+__global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const double *__restrict__ scratch,
                                                  OutT *__restrict__ desc, OutT *__restrict__ jself) {
     extern __shared__ __align__(16) double smem[];
     __shared__ double Kl[16];
-    const int S = P.S, n = P.n, Sn = S * n, L = P.L, lw = P.lmax + 1, nq = P.nq_full, tid = threadIdx.x;
+    const int64_t ci = blockIdx.x;
+    const int S = P.S, n = P.n, Sn = S * n, L = P.L, lw = P.lmax + 1, nq = P.nq_full, F = P.F, tid = threadIdx.x;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    constexpr int NW = BSO / 64;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    int *qmap = (int *)smem; // pair index of (u, v), read once per workgroup
+    int *qmap = (int *)smem; // pair index of (u, v)
     for (int t = tid; t < Sn * Sn; t += BSO) qmap[t] = P.qmap[t];
-    double *smem_c = smem + even(((size_t)Sn * Sn + 1) / 2);
-    const int64_t nitem = 4 * 8 * ((nc + 7) / 8);
-    for (int64_t b = blockIdx.x; b < nitem; b += gridDim.x) {
-    // item b on XCD b % 8 (gridDim is a multiple of 8); its k-th item there is
-    // center 8 (k / 4) + b % 8, row k % 4
-    const int64_t k = b >> 3, ci = 8 * (k >> 2) + (b & 7);
-    const int comp = (int)(k & 3) - 1; // -1 descriptor, 0..2 center block d/dx, d/dy, d/dz
-    if (ci >= nc) continue;
+    double *base = smem + even(((size_t)Sn * Sn + 1) / 2);
     const double *src = scratch + ci * 4 * (size_t)L * Sn;
-    OutT *dst = comp < 0 ? desc + ci * P.F : jself + (ci * 3 + comp) * P.F;
+    OutT *drow = desc + ci * F, *jrow = jself + ci * 3 * F; // jself rows d = 0..2 are consecutive
     for (int g = 0; g < O.n_groups; ++g) {
         const int lg0 = O.lgrp[g], lg1 = O.lgrp[g + 1], lgc = lg1 - lg0, lm0 = lg0 * lg0;
-        const int slab = (lg1 * lg1 - lm0) * Sn;
-        double *C = smem_c, *D = smem_c + even((size_t)slab);
-        OutT *row = (OutT *)(D + even((size_t)slab));
-        // (the barrier after these copies also orders the previous row's
-        // reads before this group's tiles rewrite it)
-        copy_to_lds<BSO, 4>(C, src + (size_t)lm0 * Sn, slab, tid);
-        if (comp >= 0) copy_to_lds<BSO, 4>(D, src + ((size_t)(comp + 1) * L + lm0) * Sn, slab, tid);
-        lds_barrier();
-        power_tiles<OutT>(CoefView{C, D, 1, Sn}, comp, Sn, lm0, lg0, lgc, row, lgc, lg0, qmap, wave, BSO / 64, lane,
-                          Kl);
-        lds_barrier();
-        if (lgc == lw)
-            for (int f = tid; f < P.F; f += BSO) dst[f] = row[f];
-        else
-            for (int t = tid; t < nq * lgc; t += BSO) {
-                const int q = t / lgc, lc = t - q * lgc;
-                dst[q * lw + lg0 + lc] = row[t];
+        const int slab = (lg1 * lg1 - lm0) * Sn, sstr = (int)even((size_t)slab);
+        const int rlen = nq * lgc, rstr = (int)even(((size_t)rlen * sizeof(OutT) + 7) / 8) * (8 / (int)sizeof(OutT));
+        double *X = base;                        // [comp][slab], comp = c, Dx, Dy, Dz
+        OutT *rows = (OutT *)(base + 4 * sstr);  // [row][rlen], row = descriptor, d/dx, d/dy, d/dz
+        // the four slabs, eight loads in flight per thread (the barrier after
+        // them also orders the previous group's row reads before the tiles)
+        for (int k0 = 0; k0 < 4 * slab; k0 += 8 * BSO) {
+            double v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int k = k0 + u * BSO + tid, kk = k < 4 * slab ? k : 4 * slab - 1;
+                const int comp = kk / slab, r = kk - comp * slab;
+                v[u] = src[((size_t)comp * L + lm0) * Sn + r];
             }
-    }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int k = k0 + u * BSO + tid;
+                if (k < 4 * slab) {
+                    const int comp = k / slab, r = k - comp * slab;
+                    X[comp * sstr + r] = v[u];
+                }
+            }
+        }
+        lds_barrier();
+        power_tiles4<OutT>(X, sstr, 1, Sn, Sn, lm0, lg0, lgc, rows, rows + rstr, rstr, lgc, lg0, qmap, wave, NW, lane,
+                           Kl);
+        lds_barrier();
+        if (lgc == lw) {
+            for (int f = tid; f < F; f += BSO) drow[f] = rows[f];
+            for (int f = tid; f < 3 * F; f += BSO) {
+                const int d = f >= F ? (f >= 2 * F ? 2 : 1) : 0;
+                jrow[f] = rows[(d + 1) * rstr + (f - d * F)];
+            }
+        } else {
+            for (int t = tid; t < 4 * rlen; t += BSO) {
+                const int c = t / rlen, r = t - c * rlen, q = r / lgc, lc = r - q * lgc;
+                OutT *dst = c == 0 ? drow : jrow + (size_t)(c - 1) * F;
+                dst[q * lw + lg0 + lc] = rows[c * rstr + r];
+            }
+        }
     }
 }
 

@@ -108,7 +108,6 @@ struct OutPlan {
     int n_groups;
     int lgrp[MAX_GROUPS + 1];
     size_t lds;
-    int blocks; // resident workgroups on the device
 };
 int plan_outputs(const Params &P, bool f64, OutPlan *O); // 0, or -1 if one l does not fit
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,

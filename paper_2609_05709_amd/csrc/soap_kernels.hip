@@ -40,7 +40,8 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool f64) {
 // workgroups per CU; a single l above the budget may use up to the hard limit.
 int plan_outputs(const Params &P, bool f64, OutPlan *O) {
     const int lw = P.lmax + 1, ob = f64 ? 8 : 4;
-    const size_t budget = 80 * 1024, hard = 159 * 1024;
+    // up to 52 KB (three workgroups per CU); a single l may use up to the hard limit
+    const size_t budget = 52 * 1024, hard = 159 * 1024;
     int G = 0, l = 0;
     size_t worst = 0;
     O->lgrp[0] = 0;
@@ -54,28 +55,17 @@ int plan_outputs(const Params &P, bool f64, OutPlan *O) {
     }
     O->n_groups = G;
     O->lds = worst;
-    int nb = 0, ncu = 0, dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        ncu = 256;
-    const hipError_t e = f64 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_outputs<double>, BSO, worst)
-                             : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k_outputs<float>, BSO, worst);
-    O->blocks = ncu * ((e == hipSuccess && nb > 0) ? nb : 1);
     return 0;
 }
 
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
                           void *jself, hipStream_t st) {
     if (nc <= 0) return hipSuccess;
-    // resident grid, a multiple of 8 (see k_outputs), at most one workgroup per item
-    const int64_t items = 4 * 8 * ((nc + 7) / 8);
-    const int64_t g = std::min<int64_t>(items, 8 * ((O.blocks + 7) / 8));
-    dim3 grid((unsigned)g), block(BSO);
+    dim3 grid((unsigned)nc), block(BSO);
     if (f64)
-        hipLaunchKernelGGL(k_outputs<double>, grid, block, O.lds, st, P, O, nc, scratch, (double *)desc,
-                           (double *)jself);
+        hipLaunchKernelGGL(k_outputs<double>, grid, block, O.lds, st, P, O, scratch, (double *)desc, (double *)jself);
     else
-        hipLaunchKernelGGL(k_outputs<float>, grid, block, O.lds, st, P, O, nc, scratch, (float *)desc, (float *)jself);
+        hipLaunchKernelGGL(k_outputs<float>, grid, block, O.lds, st, P, O, scratch, (float *)desc, (float *)jself);
     return hipGetLastError();
 }
 
