@@ -74,7 +74,7 @@ def lib():
         L.oracle_num_features.restype = i64
         L.oracle_num_features.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.oracle_soap.restype = ctypes.c_int
-        L.oracle_soap.argtypes = [vp, i64, vp, vp, vp, i64, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp]
+        L.oracle_soap.argtypes = [vp, i64, vp, vp, vp, i64, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -190,12 +190,18 @@ class OracleSOAP:
         lib().oracle_radial(ctypes.byref(self._p), float(r), R.ctypes.data, dR.ctypes.data, c0.ctypes.data)
         return R, dR, c0
 
-    def compute(self, pos64, Z, centers=None, jacobian=False, coefficients=False, nb=None):
+    def compute(self, pos64, Z, centers=None, jacobian=False, coefficients=False, nb=None,
+                coefficient_jacobian=False):
         """Descriptor (and Jacobian blocks, coefficients) for the given centers.
 
         Returns a dict with desc (nc, F); if jacobian: blk_ptr (nc+1), blk_j,
         jac (nblocks, 3, F); if coefficients: c (nc, S, n_max, (l_max+1)^2);
-        always: row_ptr, cols (the neighbour rows used)."""
+        if coefficient_jacobian: dc (E, 3, n_max, (l_max+1)^2), for the e-th
+        neighbour edge (i, j) of the rows, d c^{species(j)}(i) / d r_j (Eqs.
+        gto-derivative, poly-cartesian-derivative; the other species blocks
+        of c do not depend on r_j), and dc_self (nc, 3, S, n_max, L) =
+        d c(i) / d r_i = - sum_j of the edge blocks (translational
+        invariance); always: row_ptr, cols (the neighbour rows used)."""
         pos64 = np.ascontiguousarray(pos64, dtype=np.float64)
         spec = self.species_index(Z)
         n = pos64.shape[0]
@@ -208,6 +214,7 @@ class OracleSOAP:
         cout = np.empty((nc, self.S, self.n_max, L)) if coefficients else None
         out = dict(desc=desc, row_ptr=row, cols=cols)
         blk_ptr = blk_j = jac = None
+        dcout = np.empty((int(row[-1]), 3, self.n_max, L)) if coefficient_jacobian else None
         if jacobian:
             deg = np.diff(row)
             blk_ptr = np.zeros(nc + 1, dtype=np.int64)
@@ -218,9 +225,37 @@ class OracleSOAP:
             out.update(blk_ptr=blk_ptr, blk_j=blk_j, jac=jac)
         rc = lib().oracle_soap(ctypes.byref(self._p), n, _ptr(pos64), _ptr(spec), _ptr(cen), nc, _ptr(row),
                                _ptr(cols), _ptr(desc), _ptr(cout), 1 if jacobian else 0, _ptr(blk_ptr),
-                               _ptr(blk_j), _ptr(jac))
+                               _ptr(blk_j), _ptr(jac), _ptr(dcout))
         if rc != 0:
             raise MemoryError("oracle allocation failed")
         if coefficients:
             out["c"] = cout
+        if coefficient_jacobian:
+            out["dc"] = dcout
+            spec_j = spec[cols]
+            dself = np.zeros((nc, 3, self.S, self.n_max, L))
+            for c in range(nc):
+                for e in range(int(row[c]), int(row[c + 1])):
+                    dself[c, :, spec_j[e]] -= dcout[e]
+            out["dc_self"] = dself
         return out
+
+    def power_spectrum(self, c):
+        """Eq. (powerspectrum) of one coefficient set c (S, n_max, L), in the
+        output feature order: pi sqrt(8/(2l+1)) sum_m c^mu_nlm c^nu_n'lm."""
+        out = []
+        for mu, nu, a, b, l in self.features():
+            m = slice(l * l, (l + 1) * (l + 1))
+            out.append(np.pi * np.sqrt(8.0 / (2 * l + 1)) * float(np.dot(c[mu, a, m], c[nu, b, m])))
+        return np.array(out)
+
+    def averaged(self, pos64, Z, mode, centers=None):
+        """The density-averaged descriptors of the paper's averaging modes:
+        "outer" = mean over the centers of the power spectrum, "inner" = the
+        power spectrum of the mean over the centers of the coefficients."""
+        r = self.compute(pos64, Z, centers=centers, coefficients=True)
+        if mode == "outer":
+            return r["desc"].mean(axis=0)
+        if mode == "inner":
+            return self.power_spectrum(r["c"].mean(axis=0))
+        raise ValueError("mode must be 'inner' or 'outer'")

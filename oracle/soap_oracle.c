@@ -323,11 +323,16 @@ int64_t oracle_num_features(int S, int n, int lmax) {
  *   cout[c][S][n][L] (optional)    expansion coefficients c^mu_nlm
  *   if jac: blocks for j in N(i) and i itself, in ascending atom index,
  *   blk_ptr[c] .. blk_ptr[c+1] (= row length + 1), atom index in blk_j,
- *   jac[b][3][F] = d p_i / d r_j.
+ *   jac[b][3][F] = d p_i / d r_j;
+ *   dcout (optional) [e][3][n][L] for the e-th neighbour edge of the rows
+ *   (row order): d c^{s_j}_{nlm}(i) / d r_j, the gradient of Eqs.
+ *   (gto-derivative) / (poly-cartesian-derivative); only the neighbour's own
+ *   species block of c depends on r_j.
  * Returns 0, or -1 on allocation failure. */
 int oracle_soap(const oracle_params *P, int64_t n_atoms, const double *pos, const int32_t *spec,
                 const int64_t *centers, int64_t nc, const int64_t *nb_ptr, const int32_t *nb_col,
-                double *desc, double *cout, int want_jac, const int64_t *blk_ptr, int32_t *blk_j, double *jac) {
+                double *desc, double *cout, int want_jac, const int64_t *blk_ptr, int32_t *blk_j, double *jac,
+                double *dcout) {
     (void)n_atoms;
     const int S = P->S, n = P->n, lmax = P->lmax, L = (lmax + 1) * (lmax + 1);
     const int64_t F = oracle_num_features(S, n, lmax);
@@ -341,10 +346,11 @@ int oracle_soap(const oracle_params *P, int64_t n_atoms, const double *pos, cons
     for (int64_t ci = 0; ci < nc; ++ci) {
         int64_t i = centers ? centers[ci] : ci;
         int64_t e0 = nb_ptr[ci], deg = nb_ptr[ci + 1] - e0;
+        const int want_dc = want_jac || dcout != NULL;
         double *c = calloc(CSZ, sizeof(double));
-        double *dc = want_jac ? calloc((size_t)(deg > 0 ? deg : 1) * 3 * n * L, sizeof(double)) : NULL;
+        double *dc = want_dc ? calloc((size_t)(deg > 0 ? deg : 1) * 3 * n * L, sizeof(double)) : NULL;
         ld *Y = malloc(sizeof(ld) * 4 * L), *R = malloc(sizeof(ld) * 2 * n * (lmax + 1));
-        if (!c || (want_jac && !dc) || !Y || !R) {
+        if (!c || (want_dc && !dc) || !Y || !R) {
             fail = 1;
             free(c); free(dc); free(Y); free(R);
             continue;
@@ -376,7 +382,7 @@ int oracle_soap(const oracle_params *P, int64_t n_atoms, const double *pos, cons
                                grad(r^l Y)(v) = r^(l-1) grad-poly(u) */
                             ld rl = powl(r, l);
                             c[((size_t)s * n + a) * L + lm] += (double)(Rv * rl * y);
-                            if (want_jac)
+                            if (want_dc)
                                 for (int d = 0; d < 3; ++d) {
                                     ld g = (l > 0) ? powl(r, l - 1) * G[d * L + lm] : 0.0L;
                                     dc[((size_t)(e * 3 + d) * n + a) * L + lm] =
@@ -386,7 +392,7 @@ int oracle_soap(const oracle_params *P, int64_t n_atoms, const double *pos, cons
                             /* Eq. (poly-cartesian-derivative):
                                dc/dx = (x/r) Y f' + f dY/dx,  dY/dx = (grad-poly(u) - l Y u)/r */
                             c[((size_t)s * n + a) * L + lm] += (double)(Rv * y);
-                            if (want_jac)
+                            if (want_dc)
                                 for (int d = 0; d < 3; ++d) {
                                     ld dY = (G[d * L + lm] - (ld)l * y * u[d]) / r;
                                     dc[((size_t)(e * 3 + d) * n + a) * L + lm] = (double)(u[d] * y * dRv + Rv * dY);
@@ -396,6 +402,7 @@ int oracle_soap(const oracle_params *P, int64_t n_atoms, const double *pos, cons
                 }
         }
         if (cout) memcpy(cout + ci * CSZ, c, CSZ * sizeof(double));
+        if (dcout && deg > 0) memcpy(dcout + (size_t)e0 * 3 * n * L, dc, (size_t)deg * 3 * n * L * sizeof(double));
         /* Eq. (powerspectrum) */
         double *drow = desc + ci * F;
         int64_t f = 0;

@@ -408,6 +408,71 @@ def test_jacobian_covariant_under_rotation(oracle_lib):
     assert np.abs(np.einsum("xy,byf->bxf", Q, a["jac"]) - b["jac"]).max() < 1e-12 * np.abs(a["jac"]).max()
 
 
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_coefficient_jacobian_central_finite_differences(oracle_lib, rbf):
+    """d c(i) / d r_j (the "cc" Jacobian) and d c(i) / d r_i against central
+    differences of the coefficients, which are pinned to brute-force projection;
+    species blocks other than species(j) do not move with r_j."""
+    s = workloads.random_small(8, 33, 2.6, species=(1, 8))
+    o = oracle.OracleSOAP((1, 8), 4.5, 3, 4, 0.5, rbf)
+    pos = s.pos64
+    out = o.compute(pos, s.Z, coefficient_jacobian=True)
+    row, cols = out["row_ptr"], out["cols"]
+    spec = o.species_index(s.Z)
+    h = 1e-5
+
+    def c_of(p, c):
+        return o.compute(p, s.Z, centers=[c], coefficients=True)["c"][0]
+
+    for c in (0, 5):
+        moved = [(int(j), e) for e, j in zip(range(int(row[c]), int(row[c + 1])), cols[row[c]:row[c + 1]])]
+        for j, e in moved + [(c, None)]:
+            for d in range(3):
+                pp, pm = pos.copy(), pos.copy()
+                pp[j, d] += h
+                pm[j, d] -= h
+                fd = (c_of(pp, c) - c_of(pm, c)) / (2 * h)
+                if e is None:
+                    got = out["dc_self"][c, d]
+                else:
+                    got = np.zeros_like(fd)
+                    got[spec[j]] = out["dc"][e, d]
+                scale = max(np.abs(got).max(), 1e-3)
+                assert np.abs(fd - got).max() < 1e-8 * scale, (c, j, d)
+
+
+def test_power_spectrum_of_coefficients_matches_descriptor(oracle_lib):
+    """The Python power spectrum of a coefficient set reproduces the C oracle's
+    descriptor row (pinned to the two-body Legendre form)."""
+    s = workloads.random_small(12, 7, 3.0, species=(1, 8))
+    o = oracle.OracleSOAP((1, 8), 4.0, 4, 5, 0.5, "gto")
+    r = o.compute(s.pos64, s.Z, coefficients=True)
+    for c in range(s.n_atoms):
+        p = o.power_spectrum(r["c"][c])
+        assert np.abs(p - r["desc"][c]).max() <= 1e-13 * np.abs(r["desc"][c]).max()
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_averaged_modes_closed_forms(oracle_lib, rbf):
+    """Averaging modes.  One center: inner = outer = its power spectrum.  A
+    homonuclear dimer: the two centers see each other at opposite vectors, so
+    c_2 = (-1)^l c_1; inner therefore has exactly zero odd-l features and equals
+    outer on the even-l features."""
+    o = oracle.OracleSOAP((8,), 4.0, 4, 5, 0.5, rbf)
+    pos = np.array([[0.3, -0.2, 0.1], [1.1, 0.9, -0.6]])
+    Z = np.array([8, 8])
+    one_in = o.averaged(pos, Z, "inner", centers=[1])
+    one_out = o.averaged(pos, Z, "outer", centers=[1])
+    ref = o.compute(pos, Z, centers=[1])["desc"][0]
+    assert np.abs(one_in - ref).max() <= 1e-14 * np.abs(ref).max()
+    assert np.abs(one_out - ref).max() <= 1e-14 * np.abs(ref).max()
+    inner, outer = o.averaged(pos, Z, "inner"), o.averaged(pos, Z, "outer")
+    odd = np.array([f[4] % 2 == 1 for f in o.features()])
+    assert np.abs(inner[odd]).max() <= 1e-14 * np.abs(outer).max()
+    assert np.abs(outer[odd]).max() > 1e-6 * np.abs(outer).max()
+    assert np.abs(inner[~odd] - outer[~odd]).max() <= 1e-13 * np.abs(outer).max()
+
+
 # ------------------------------------------------------- neighbours
 
 def test_neighbor_sets_brute_grid_and_kdtree(oracle_lib):
