@@ -65,6 +65,10 @@ typedef struct soap_ctx soap_ctx;
 #define SOAP_FP64 1
 
 /* Largest neighbour count per center the neighbour builder accepts. */
+/* averaging modes of soap_compute_averaged (Sec. 3, the density-averaged variants) */
+#define SOAP_AVERAGE_INNER 1
+#define SOAP_AVERAGE_OUTER 2
+
 #define SOAP_MAX_DEGREE 2048
 
 /*
@@ -160,6 +164,38 @@ int soap_compute(soap_ctx *ctx, void *desc_dev, void *stream);
  * m < 0 ~ sin(|m| phi), no Condon-Shortley phase.
  */
 int soap_coefficients(soap_ctx *ctx, void *c_dev, void *stream);
+
+/*
+ * Coefficients and their Jacobian (the "cc" mode of Sec. 3, whose kernel
+ * stores the edge gradient of the coefficients directly):
+ *   c_dev       [n_centers][S][n_max][L]  c^mu_nlm(i), as soap_coefficients
+ *                                         (L = (l_max+1)^2, index l*l + l + m);
+ *   jc_edge_dev [E][3][n_max][L]          d c^{species(j)}_nlm(i) / d r_j for
+ *                                         the e-th edge (i, j) of the neighbour
+ *                                         rows: B^_nl r S_lm + B_nl grad S_lm
+ *                                         (Eqs. (gto-derivative),
+ *                                         (poly-cartesian-derivative)); the
+ *                                         other species blocks of c(i) do not
+ *                                         depend on r_j and are not stored;
+ *   jc_self_dev [n_centers][3][S][n_max][L] d c(i) / d r_i = - sum_j d c(i) / d r_j
+ *                                         (translational invariance).
+ * A coincident neighbour (r = 0) contributes its on-site term to c and a zero
+ * gradient.  jc_edge_dev may be NULL when the neighbour list has no edges.
+ * Errors: SOAP_EINVAL, SOAP_ESTATE, SOAP_ENOMEM, SOAP_EHIP.
+ */
+int soap_coefficient_derivatives(soap_ctx *ctx, void *c_dev, void *jc_edge_dev, void *jc_self_dev, void *stream);
+
+/*
+ * Density-averaged descriptor over the centers of the neighbour list (the
+ * "inner" and "outer" modes of Sec. 3), one row desc_dev[F] (dtype):
+ *   SOAP_AVERAGE_OUTER: (1/n_c) sum_i p_i, the mean power spectrum;
+ *   SOAP_AVERAGE_INNER: the power spectrum, Eq. (powerspectrum), of the mean
+ *                       coefficients (1/n_c) sum_i c_i.
+ * Uses a context-owned device scratch of n_c rows (F or S n_max L values of
+ * the dtype).  Errors: SOAP_EINVAL (bad mode, NULL pointer), SOAP_ESTATE,
+ * SOAP_ENOMEM, SOAP_EHIP.
+ */
+int soap_compute_averaged(soap_ctx *ctx, int32_t mode, void *desc_dev, void *stream);
 
 /*
  * Descriptor and Jacobian, Eqs. (powerspectrum), (powerspectrum-derivative):

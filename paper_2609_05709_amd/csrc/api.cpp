@@ -67,6 +67,7 @@ struct soap_ctx {
     // neighbour workspace
     NbrWork nw{};
     DevBuf b_zero, b_bstart, b_acell, b_srec, b_sspec, b_deg, b_slots, b_scan, b_spec, b_row, b_cols, b_cscratch;
+    DevBuf b_avg, b_avg_part; // averaged modes: per-center rows, column partial sums and means
     uint64_t work_epoch = 0; // density work-counter increments since the counters were zeroed
     int32_t *h_flags = nullptr; // pinned: [0..3] flags, then int64 E at offset 8
     // state of the last neighbour build
@@ -76,11 +77,11 @@ struct soap_ctx {
     const int32_t *Zdev = nullptr, *centers = nullptr;
     bool built_f64 = false;
     // launch configuration
-    DensityLaunch dens_cfg[2]{};  // [jac]
+    DensityLaunch dens_cfg[3]{};  // [density kernel mode: descriptor, Jacobian, coefficient Jacobian]
     JacLaunch jac_cfg{};
     OutPlan out_plan{};
-    int groups_jac = 1, groups_desc = 1;
-    int lgrp_jac[MAX_GROUPS + 1]{}, lgrp_desc[MAX_GROUPS + 1]{};
+    int groups[3] = {1, 1, 1};
+    int lgrp[3][MAX_GROUPS + 1]{};
     // per-segment timing
     bool timing = false;
     struct Rec {
@@ -195,17 +196,18 @@ int plan_launches(soap_ctx *c) {
     int ncu = 256;
     (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
     const bool f64d = c->dtype == SOAP_FP64;
-    for (int jac = 0; jac < 2; ++jac) {
-        int *lgrp = jac ? c->lgrp_jac : c->lgrp_desc, *G = jac ? &c->groups_jac : &c->groups_desc;
+    for (int mode = 0; mode < 3; ++mode) {
+        const int jac = mode != 0; // modes 1 and 2 stage gradients
+        int *lgrp = c->lgrp[mode], *G = &c->groups[mode];
         // workgroups per CU the registers allow (no LDS), and the LDS share of each
-        const int by_regs = std::max(1, density_blocks_per_cu(f64d, jac != 0, 0));
+        const int by_regs = std::max(1, density_blocks_per_cu(f64d, mode, 0));
         const size_t budget = std::min(LDS_HARD_LIMIT, (size_t)(159 * 1024) / (size_t)by_regs);
         if (plan_groups(P, jac, f64d, budget, lgrp, G, &Wd, &lds) != 0)
             return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
-        c->dens_cfg[jac].W = Wd;
-        c->dens_cfg[jac].lds = lds;
-        const int per_cu = density_blocks_per_cu(f64d, jac != 0, lds);
-        c->dens_cfg[jac].blocks = std::max(1, ncu * per_cu / *G);
+        c->dens_cfg[mode].W = Wd;
+        c->dens_cfg[mode].lds = lds;
+        const int per_cu = density_blocks_per_cu(f64d, mode, lds);
+        c->dens_cfg[mode].blocks = std::max(1, ncu * per_cu / *G);
     }
     if (plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) != 0)
         return fail(c, SOAP_EINVAL, "basis too large for the output kernel's on-chip memory");
@@ -382,11 +384,11 @@ Rows rows_of(const soap_ctx *c) {
     return R;
 }
 
-Params params_for(const soap_ctx *c, bool jac) {
+Params params_for(const soap_ctx *c, int mode) {
     Params P = c->P;
-    const int G = jac ? c->groups_jac : c->groups_desc;
+    const int G = c->groups[mode];
     P.n_groups = G;
-    for (int k = 0; k <= G; ++k) P.lgrp[k] = jac ? c->lgrp_jac[k] : c->lgrp_desc[k];
+    for (int k = 0; k <= G; ++k) P.lgrp[k] = c->lgrp[mode][k];
     return P;
 }
 
@@ -583,22 +585,24 @@ int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, voi
     return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_get_neighbors");
 }
 
-static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jself, void *stream) {
+// mode as launch_density: 0 descriptor / coefficients, 1 descriptor + Jacobian,
+// 2 coefficient Jacobian
+static int run_density(soap_ctx *c, int mode, void *desc, void *c_out, void *jself, void *jc_edge, void *stream) {
     if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
     int rc;
     if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
-    const Params P = params_for(c, jac);
+    const Params P = params_for(c, mode);
     double *scratch = nullptr;
-    if (jac) {
+    if (mode == 1) {
         hipError_t e = c->b_cscratch.ensure(8 * 4 * (size_t)c->nc * P.S * P.n * P.L); // c, Dx, Dy, Dz
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
     SegTimer timer(c, 1, to_stream(stream));
-    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, jac, c->dens_cfg[jac ? 1 : 0], c->nw.work,
-                                  &c->work_epoch, desc, c_out, jself, scratch, to_stream(stream));
+    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, mode, c->dens_cfg[mode], c->nw.work,
+                                  &c->work_epoch, desc, c_out, jself, scratch, jc_edge, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
-    if (jac && P.n_groups > 1) { // with one l-group the density kernel writes desc and jself
+    if (mode == 1 && P.n_groups > 1) { // with one l-group the density kernel writes desc and jself
         e = launch_outputs(P, c->out_plan, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
         if (e != hipSuccess) return hip_fail(c, e, "output kernel");
     }
@@ -609,20 +613,51 @@ static int run_density(soap_ctx *c, bool jac, void *desc, void *c_out, void *jse
 int soap_compute(soap_ctx *c, void *desc_dev, void *stream) {
     if (!c) return SOAP_EINVAL;
     if (!desc_dev) return fail(c, SOAP_EINVAL, "desc_dev is NULL");
-    return run_density(c, false, desc_dev, nullptr, nullptr, stream);
+    return run_density(c, 0, desc_dev, nullptr, nullptr, nullptr, stream);
 }
 
 int soap_coefficients(soap_ctx *c, void *c_dev, void *stream) {
     if (!c) return SOAP_EINVAL;
     if (!c_dev) return fail(c, SOAP_EINVAL, "c_dev is NULL");
-    return run_density(c, false, nullptr, c_dev, nullptr, stream);
+    return run_density(c, 0, nullptr, c_dev, nullptr, nullptr, stream);
+}
+
+int soap_coefficient_derivatives(soap_ctx *c, void *c_dev, void *jc_edge_dev, void *jc_self_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!c_dev || !jc_self_dev || (!jc_edge_dev && c->E > 0)) return fail(c, SOAP_EINVAL, "output pointer is NULL");
+    return run_density(c, 2, nullptr, c_dev, jc_self_dev, jc_edge_dev, stream);
+}
+
+int soap_compute_averaged(soap_ctx *c, int32_t mode, void *desc_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    if (!desc_dev) return fail(c, SOAP_EINVAL, "desc_dev is NULL");
+    if (mode != SOAP_AVERAGE_INNER && mode != SOAP_AVERAGE_OUTER)
+        return fail(c, SOAP_EINVAL, "averaging mode must be SOAP_AVERAGE_INNER or SOAP_AVERAGE_OUTER");
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    const size_t elt = c->built_f64 ? 8 : 4;
+    const Params &P = c->P;
+    const int64_t cols = mode == SOAP_AVERAGE_OUTER ? c->F : (int64_t)P.S * P.n * P.L;
+    hipError_t e = c->b_avg.ensure(elt * (size_t)c->nc * cols);
+    if (e == hipSuccess) e = c->b_avg_part.ensure(8 * (size_t)cols * (AVG_CHUNKS + 1));
+    if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(averaging scratch)");
+    // per-center rows (descriptor or coefficients), then their column means
+    int rc = mode == SOAP_AVERAGE_OUTER ? run_density(c, 0, c->b_avg.p, nullptr, nullptr, nullptr, stream)
+                                        : run_density(c, 0, nullptr, c->b_avg.p, nullptr, nullptr, stream);
+    if (rc != SOAP_OK) return rc;
+    double *part = c->b_avg_part.as<double>(), *mean = part + (size_t)AVG_CHUNKS * cols;
+    e = launch_column_mean(c->b_avg.p, c->built_f64, c->nc, cols, part, mode == SOAP_AVERAGE_OUTER ? desc_dev : nullptr,
+                           mean, to_stream(stream));
+    if (e == hipSuccess && mode == SOAP_AVERAGE_INNER)
+        e = launch_power_single(P, c->built_f64, mean, desc_dev, to_stream(stream)); // Eq. powerspectrum of the mean c
+    if (e != hipSuccess) return hip_fail(c, e, "averaging kernels");
+    return SOAP_OK;
 }
 
 int soap_derivatives(soap_ctx *c, void *desc_dev, void *jac_edge_dev, void *jac_self_dev, void *stream) {
     if (!c) return SOAP_EINVAL;
     if (!desc_dev || !jac_self_dev || (!jac_edge_dev && c->E > 0))
         return fail(c, SOAP_EINVAL, "output pointer is NULL");
-    int rc = run_density(c, true, desc_dev, nullptr, jac_self_dev, stream);
+    int rc = run_density(c, 1, desc_dev, nullptr, jac_self_dev, nullptr, stream);
     if (rc != SOAP_OK) return rc;
     if (c->E == 0) return SOAP_OK;
     SegTimer timer(c, 2, to_stream(stream));
@@ -679,7 +714,7 @@ void soap_destroy(soap_ctx *c) {
     (void)hipDeviceSynchronize();
     for (DevBuf *b : {&c->d_const, &c->d_qmap, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_zero, &c->b_bstart, &c->b_acell,
                       &c->b_srec, &c->b_sspec, &c->b_deg, &c->b_slots, &c->b_scan, &c->b_spec, &c->b_row, &c->b_cols,
-                      &c->b_cscratch})
+                      &c->b_cscratch, &c->b_avg, &c->b_avg_part})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
     for (auto &r : c->recs) {

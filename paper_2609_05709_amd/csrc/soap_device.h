@@ -645,12 +645,15 @@ __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, in
            even(W * stage_x_doubles(P, (int)lgc, lg1));
 }
 
-template <typename PosT, typename OutT, bool JAC>
+// MODE: 0 descriptor (c, power spectrum); 1 descriptor + Jacobian (c and D);
+// 2 coefficient Jacobian ("cc": c, every edge's dc/dr_j, and -D)
+template <typename PosT, typename OutT, int MODE>
 __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                                  unsigned long long *__restrict__ work, uint64_t base,
                                                  OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,
-                                                 double *__restrict__ c_scratch) {
+                                                 double *__restrict__ c_scratch, OutT *__restrict__ jc_edge) {
+    constexpr bool JAC = MODE != 0, CCJ = MODE == 2;
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
     extern __shared__ __align__(16) double smem[];
     __shared__ int64_t s_next;
@@ -687,8 +690,9 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
     ST2 *BB = (ST2 *)wv.take((2 * (size_t)W * nlc * SB + 7) / 8);
     double *X = wv.take((size_t)W * stage_x_doubles(P, lgc, lg1));
 
-    // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg
-    int oY[KE], oB[KE];
+    // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg;
+    // oC: its offset a L + lm in a coefficient block of one species
+    int oY[KE], oB[KE], oC[KE];
     bool own[KE];
 #pragma unroll
     for (int k = 0; k < KE; ++k) {
@@ -696,6 +700,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
         own[k] = e < nL;
         const int a = e / Lg, lmg = e - a * Lg;
         const int lm = lm0 + (own[k] ? lmg : 0);
+        oC[k] = a * Lfull + lm;
         int l = (int)sqrtf((float)lm);
         while (l * l > lm) --l;
         while ((l + 1) * (l + 1) <= lm) ++l;
@@ -783,6 +788,8 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                     const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
                     const ST *Ye = YY + e * yl.es;
                     const ST2 *Be = BB + e * nlc;
+                    // this edge's block of the coefficient Jacobian: [3][n][L]
+                    OutT *je = CCJ ? jc_edge + (size_t)(rb0 + off + e) * 3 * n * Lfull : nullptr;
 #pragma unroll
                     for (int k = 0; k < KE; ++k) {
                         if (!own[k]) continue;
@@ -792,10 +799,17 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                             double y0, y1, y2, y3;
                             load4(Ye + oY[k], y0, y1, y2, y3);
                             const double bh = by * y0;
+                            // dc/dr_j = Bh r S + B grad S (Eqs. gto-derivative, poly-cartesian-derivative)
+                            const double gx = bh * rx + bx * y1, gy = bh * ry + bx * y2, gz = bh * rz + bx * y3;
                             acc[k][0] += bx * y0;
-                            acc[k][1] += bh * rx + bx * y1;
-                            acc[k][2] += bh * ry + bx * y2;
-                            acc[k][3] += bh * rz + bx * y3;
+                            acc[k][1] += gx;
+                            acc[k][2] += gy;
+                            acc[k][3] += gz;
+                            if (CCJ) {
+                                store_out(je + oC[k], gx);
+                                store_out(je + (n * Lfull + oC[k]), gy);
+                                store_out(je + (2 * n * Lfull + oC[k]), gz);
+                            }
                         } else {
                             acc[k][0] += bx * (double)Ye[oY[k]];
                         }
@@ -822,7 +836,14 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
                 const int sa = qdiv(it, inv_Lg), lmg = it - sa * Lg;
                 store_out(c_out + (cw * Sn + sa) * Lfull + lm0 + lmg, cacc[it]);
             }
-        if (JAC) {
+        if (CCJ) {
+            // center block of the coefficient Jacobian: dc/dr_i = -D, [3][S][n][L]
+            for (int it = tid; it < 3 * SnL; it += BSD) {
+                const int d = it / SnL, rem = it - d * SnL;
+                const int sa = qdiv(rem, inv_Lg), lmg = rem - sa * Lg;
+                store_out(jself + ((cw * 3 + d) * Sn + sa) * Lfull + lm0 + lmg, -Dacc[it]);
+            }
+        } else if (JAC) {
             // with one l-group the workgroup holds all of c and D: it writes
             // the power spectrum and the center block itself (whole rows of
             // one center from one workgroup, so their lines fill in one L2);
@@ -920,6 +941,47 @@ __global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const doub
             }
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Averaged modes: column means over the centers (float64 sums in row chunks,
+// then the chunk sums) and the power spectrum of one coefficient set.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_colsum_partial(const T *__restrict__ in, int64_t rows, int64_t cols,
+                                                        int64_t chunk_rows, double *__restrict__ part) {
+    const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x, ch = blockIdx.y;
+    if (col >= cols) return;
+    const int64_t r0 = ch * chunk_rows, r1 = r0 + chunk_rows < rows ? r0 + chunk_rows : rows;
+    double s = 0.0;
+    for (int64_t r = r0; r < r1; ++r) s += (double)in[r * cols + col];
+    part[ch * cols + col] = s;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_colmean_finish(const double *__restrict__ part, int nchunk, int64_t cols,
+                                                        int64_t rows, T *__restrict__ out, double *__restrict__ mean) {
+    const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (col >= cols) return;
+    double s = 0.0;
+    for (int k = 0; k < nchunk; ++k) s += part[(int64_t)k * cols + col];
+    const double m = s / (double)rows;
+    mean[col] = m;
+    if (out) out[col] = (T)m;
+}
+
+// one workgroup: Eq. (powerspectrum) of c[S][n][L] (float64) into out[F]
+template <typename OutT>
+__global__ __launch_bounds__(256) void k_power_single(Params P, const double *__restrict__ c, OutT *__restrict__ out) {
+    extern __shared__ __align__(16) double smem[];
+    __shared__ double Kl[16];
+    const int Sn = P.S * P.n, L = P.L, tid = threadIdx.x;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
+    copy_to_lds<256, 4>(smem, c, Sn * L, tid);
+    lds_barrier();
+    power_tiles<OutT>(CoefView{smem, nullptr, L, 1}, -1, Sn, 0, 0, P.lmax + 1, out, P.lmax + 1, 0, P.qmap, wave, 4,
+                      lane, Kl);
 }
 
 // ---------------------------------------------------------------------------

@@ -84,7 +84,7 @@ struct JacLaunch {
 };
 
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64);
-int density_blocks_per_cu(bool f64, bool jac, size_t lds);
+int density_blocks_per_cu(bool f64, int mode, size_t lds); // mode as launch_density
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
 int jacobian_max_w();
@@ -99,9 +99,12 @@ hipError_t set_lds_limits();
 // [center][c, Dx, Dy, Dz][lm][species n])
 // work: per-group counters, zeroed at the neighbour build and never reset in
 // between; *epoch counts the increments made since then (advanced here).
-hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
+// mode 0: descriptor (desc, c_out may be NULL); 1: descriptor + Jacobian (desc,
+// jself, c_scratch); 2: coefficient Jacobian (c_out, jself = [n_c][3][S][n][L],
+// jc_edge = [E][3][n][L])
+hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, int mode,
                           const DensityLaunch &cfg, unsigned long long *work, uint64_t *epoch, void *desc, void *c_out,
-                          void *jself, double *c_scratch, hipStream_t st);
+                          void *jself, double *c_scratch, void *jc_edge, hipStream_t st);
 // power spectrum and center block from the coefficient scratch (Jacobian
 // path): l-groups of the output kernel, each sized to its LDS budget
 struct OutPlan {
@@ -114,6 +117,14 @@ hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f6
                           void *jself, hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);
+// column means of a row-major (rows x cols) array of the output type, in
+// float64: part[AVG_CHUNKS][cols] partial sums, then mean[cols] (float64)
+// and, if out is not NULL, out[cols] at the output type
+constexpr int AVG_CHUNKS = 256;
+hipError_t launch_column_mean(const void *in, bool f64, int64_t rows, int64_t cols, double *part, void *out,
+                              double *mean, hipStream_t st);
+// power spectrum of one coefficient set c[S][n][L] (float64) into out[F]
+hipError_t launch_power_single(const Params &P, bool f64, const double *c, void *out, hipStream_t st);
 hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,
                                 const int32_t *fmap, void *dense, hipStream_t st);
 

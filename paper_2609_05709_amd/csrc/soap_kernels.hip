@@ -14,15 +14,16 @@ size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool
     return d * 8;
 }
 
-int density_blocks_per_cu(bool f64, bool jac, size_t lds) {
+int density_blocks_per_cu(bool f64, int mode, size_t lds) {
     int nb = 0;
-    hipError_t e;
+    const void *k = nullptr;
     if (f64)
-        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<double, double, true>, BSD, lds)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<double, double, false>, BSD, lds);
+        k = mode == 0 ? (const void *)dev::k_density<double, double, 0>
+                      : mode == 1 ? (const void *)dev::k_density<double, double, 1> : (const void *)dev::k_density<double, double, 2>;
     else
-        e = jac ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<float, float, true>, BSD, lds)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, dev::k_density<float, float, false>, BSD, lds);
+        k = mode == 0 ? (const void *)dev::k_density<float, float, 0>
+                      : mode == 1 ? (const void *)dev::k_density<float, float, 1> : (const void *)dev::k_density<float, float, 2>;
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, BSD, lds);
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
@@ -93,12 +94,16 @@ hipError_t set_lds_limits() {
     hipError_t e = hipSuccess;
 #define SOAP_SET(K)                                                                                          \
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
-    SOAP_SET((dev::k_density<float, float, false>));
-    SOAP_SET((dev::k_density<float, float, true>));
-    SOAP_SET((dev::k_density<double, double, false>));
-    SOAP_SET((dev::k_density<double, double, true>));
+    SOAP_SET((dev::k_density<float, float, 0>));
+    SOAP_SET((dev::k_density<float, float, 1>));
+    SOAP_SET((dev::k_density<float, float, 2>));
+    SOAP_SET((dev::k_density<double, double, 0>));
+    SOAP_SET((dev::k_density<double, double, 1>));
+    SOAP_SET((dev::k_density<double, double, 2>));
     SOAP_SET(k_outputs<float>);
     SOAP_SET(k_outputs<double>);
+    SOAP_SET(k_power_single<float>);
+    SOAP_SET(k_power_single<double>);
     SOAP_SET((k_jacobian<float, float, 0, 0>));
     SOAP_SET((k_jacobian<double, double, 0, 0>));
     for (int n = 1; n <= NMAX; ++n)
@@ -110,30 +115,25 @@ hipError_t set_lds_limits() {
     return e;
 }
 
-hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool jac,
+hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, int mode,
                           const DensityLaunch &cfg, unsigned long long *work, uint64_t *epoch, void *desc, void *c_out,
-                          void *jself, double *c_scratch, hipStream_t st) {
+                          void *jself, double *c_scratch, void *jc_edge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     const int64_t per_group = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
-    const uint64_t base = *epoch;
-    dim3 grid((unsigned)(per_group * P.n_groups)), block(BSD);
-    if (f64) {
-        if (jac)
-            hipLaunchKernelGGL((dev::k_density<double, double, true>), grid, block, cfg.lds, st, P, R, (const double *)pos,
-                               cfg.W, work, base, (double *)desc, (double *)c_out, (double *)jself, c_scratch);
-        else
-            hipLaunchKernelGGL((dev::k_density<double, double, false>), grid, block, cfg.lds, st, P, R,
-                               (const double *)pos, cfg.W, work, base, (double *)desc, (double *)c_out,
-                               (double *)jself, c_scratch);
-    } else {
-        if (jac)
-            hipLaunchKernelGGL((dev::k_density<float, float, true>), grid, block, cfg.lds, st, P, R, (const float *)pos,
-                               cfg.W, work, base, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
-        else
-            hipLaunchKernelGGL((dev::k_density<float, float, false>), grid, block, cfg.lds, st, P, R, (const float *)pos,
-                               cfg.W, work, base, (float *)desc, (float *)c_out, (float *)jself, c_scratch);
-    }
-    const hipError_t e = hipGetLastError();
+    uint64_t b = *epoch;
+    Params Pk = P;
+    Rows Rk = R;
+    int W = cfg.W;
+    void *args[] = {&Pk, &Rk, &pos, &W, &work, &b, &desc, &c_out, &jself, &c_scratch, &jc_edge};
+    const void *k;
+    if (f64)
+        k = mode == 0 ? (const void *)dev::k_density<double, double, 0>
+                      : mode == 1 ? (const void *)dev::k_density<double, double, 1> : (const void *)dev::k_density<double, double, 2>;
+    else
+        k = mode == 0 ? (const void *)dev::k_density<float, float, 0>
+                      : mode == 1 ? (const void *)dev::k_density<float, float, 1> : (const void *)dev::k_density<float, float, 2>;
+    const hipError_t e =
+        hipLaunchKernel(k, dim3((unsigned)(per_group * P.n_groups)), dim3(BSD), args, cfg.lds, st);
     // the counter is taken for every center but the per_group static ones,
     // plus one final, empty fetch per workgroup
     if (e == hipSuccess) *epoch += (uint64_t)R.nc;
@@ -148,6 +148,35 @@ hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool
     int W = cfg.W;
     void *args[] = {&Pk, &Rk, &pos, &W, &c_scratch, &jedge};
     return hipLaunchKernel(jacobian_kernel(f64, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args, cfg.lds, st);
+}
+
+hipError_t launch_column_mean(const void *in, bool f64, int64_t rows, int64_t cols, double *part, void *out,
+                              double *mean, hipStream_t st) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int nchunk = (int)std::min<int64_t>(rows, AVG_CHUNKS);
+    const int64_t chunk_rows = (rows + nchunk - 1) / nchunk;
+    const unsigned cb = (unsigned)((cols + 255) / 256);
+    if (f64) {
+        hipLaunchKernelGGL(k_colsum_partial<double>, dim3(cb, (unsigned)nchunk), dim3(256), 0, st, (const double *)in,
+                           rows, cols, chunk_rows, part);
+        hipLaunchKernelGGL(k_colmean_finish<double>, dim3(cb), dim3(256), 0, st, part, nchunk, cols, rows,
+                           (double *)out, mean);
+    } else {
+        hipLaunchKernelGGL(k_colsum_partial<float>, dim3(cb, (unsigned)nchunk), dim3(256), 0, st, (const float *)in,
+                           rows, cols, chunk_rows, part);
+        hipLaunchKernelGGL(k_colmean_finish<float>, dim3(cb), dim3(256), 0, st, part, nchunk, cols, rows,
+                           (float *)out, mean);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_power_single(const Params &P, bool f64, const double *c, void *out, hipStream_t st) {
+    const size_t lds = 8 * (size_t)P.S * P.n * P.L;
+    if (f64)
+        hipLaunchKernelGGL(k_power_single<double>, dim3(1), dim3(256), lds, st, P, c, (double *)out);
+    else
+        hipLaunchKernelGGL(k_power_single<float>, dim3(1), dim3(256), lds, st, P, c, (float *)out);
+    return hipGetLastError();
 }
 
 hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,

@@ -15,12 +15,14 @@ LIB_PATH = os.path.join(HERE, "libsoap.so")
 SOAP_OK, SOAP_EINVAL, SOAP_ESPECIES, SOAP_ENOMEM, SOAP_EHIP, SOAP_ECAPACITY, SOAP_ESTATE = 0, -1, -2, -3, -4, -5, -6
 SOAP_RBF_GTO, SOAP_RBF_POLYNOMIAL = 0, 1
 SOAP_FP32, SOAP_FP64 = 0, 1
+SOAP_AVERAGE_INNER, SOAP_AVERAGE_OUTER = 1, 2
 MAX_DEGREE = 2048
 
 # every entry point declared in include/soap.h
 ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_num_features", "soap_num_edge_features",
                "soap_feature_labels", "soap_feature_map", "soap_build_neighbors", "soap_get_neighbors",
-               "soap_compute", "soap_coefficients", "soap_derivatives", "soap_scatter_dense", "soap_timing",
+               "soap_compute", "soap_coefficients", "soap_coefficient_derivatives", "soap_compute_averaged",
+               "soap_derivatives", "soap_scatter_dense", "soap_timing",
                "soap_last_error", "soap_destroy")
 
 _STATUS = {SOAP_EINVAL: "EINVAL", SOAP_ESPECIES: "ESPECIES", SOAP_ENOMEM: "ENOMEM", SOAP_EHIP: "EHIP",
@@ -69,6 +71,10 @@ def load_library(path: str = LIB_PATH):
     L.soap_derivatives.argtypes = [vp, vp, vp, vp, vp]
     L.soap_scatter_dense.restype = ctypes.c_int
     L.soap_scatter_dense.argtypes = [vp, vp, vp, vp, vp]
+    L.soap_coefficient_derivatives.restype = ctypes.c_int
+    L.soap_coefficient_derivatives.argtypes = [vp, vp, vp, vp, vp]
+    L.soap_compute_averaged.restype = ctypes.c_int
+    L.soap_compute_averaged.argtypes = [vp, i32, vp, vp]
     L.soap_timing.restype = ctypes.c_int
     L.soap_timing.argtypes = [vp, vp, vp, i32]
     L.soap_last_error.restype = ctypes.c_char_p
@@ -211,6 +217,28 @@ class Soap:
         c = self._out(out, (self.n_centers, S, self.n_max, L))
         self._check(self._L.soap_coefficients(self._h, c.data_ptr(), _stream()))
         return c
+
+    def coefficient_derivatives(self, c=None, jc_edge=None, jc_self=None):
+        """The "cc" mode: coefficients c (n_c, S, n_max, L), their edge
+        gradients jc_edge (E, 3, n_max, L) = d c^{species(j)}(i) / d r_j and the
+        center blocks jc_self (n_c, 3, S, n_max, L)."""
+        S, L = len(self.species), (self.l_max + 1) ** 2
+        c = self._out(c, (self.n_centers, S, self.n_max, L))
+        jc_edge = self._out(jc_edge, (self.E, 3, self.n_max, L))
+        jc_self = self._out(jc_self, (self.n_centers, 3, S, self.n_max, L))
+        self._check(self._L.soap_coefficient_derivatives(self._h, c.data_ptr(), jc_edge.data_ptr() if self.E else None,
+                                                         jc_self.data_ptr(), _stream()))
+        return c, jc_edge, jc_self
+
+    def compute_averaged(self, mode, out=None):
+        """Density-averaged descriptor (n_features,): mode "outer" (mean power
+        spectrum) or "inner" (power spectrum of the mean coefficients)."""
+        code = {"inner": SOAP_AVERAGE_INNER, "outer": SOAP_AVERAGE_OUTER}.get(mode)
+        if code is None:
+            raise ValueError("mode must be 'inner' or 'outer'")
+        desc = self._out(out, (self.n_features,))
+        self._check(self._L.soap_compute_averaged(self._h, code, desc.data_ptr(), _stream()))
+        return desc
 
     def derivatives(self, desc=None, jac_edge=None, jac_self=None):
         desc = self._out(desc, (self.n_centers, self.n_features))
