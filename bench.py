@@ -10,7 +10,11 @@ r_cut 6 A, sigma 0.5 A, n_max 8, l_max 6, descriptor + Jacobian, float32
 outputs.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--dtype float32|float64]
-                  [--grid OUT.jsonl] [--no-cpu-baseline]
+                  [--mode derivatives|cc|inner|outer] [--grid OUT.jsonl] [--no-cpu-baseline]
+
+--mode picks the output of a Jacobian workload: the descriptor + Jacobian
+(default), the coefficients and their Jacobian ("cc"), or one averaged
+descriptor row ("inner", "outer").
 """
 from __future__ import annotations
 
@@ -129,7 +133,15 @@ def cpu_baseline(wl, st, budget_s=12.0):
                       f"{'descriptor + Jacobian' if wl.jacobian else 'descriptor'}, {dt:.1f} s"}
 
 
-def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
+def cc_bytes(sp, wl, nc, E, out_bytes):
+    """Algorithmic bytes of the coefficient-Jacobian outputs: c, the edge
+    gradients (neighbour's species block) and the center blocks."""
+    nL = wl.n_max * (wl.l_max + 1) ** 2
+    S = len(wl.species)
+    return (nc * S * nL + E * 3 * nL + nc * 3 * S * nL) * out_bytes
+
+
+def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
@@ -141,14 +153,26 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
     Z = torch.from_numpy(st.Z).to(dev)
     E = sp.build_neighbors(pos, Z)
     nc = st.n_atoms
-    desc = torch.empty((nc, sp.n_features), dtype=tdt, device=dev)
-    if wl.jacobian:
-        jedge = torch.empty((E, 3, sp.n_edge_features), dtype=tdt, device=dev)
-        jself = torch.empty((nc, 3, sp.n_features), dtype=tdt, device=dev)
+    S, L = len(wl.species), (wl.l_max + 1) ** 2
+    if mode == "cc":
+        cc = torch.empty((nc, S, wl.n_max, L), dtype=tdt, device=dev)
+        jce = torch.empty((E, 3, wl.n_max, L), dtype=tdt, device=dev)
+        jcs = torch.empty((nc, 3, S, wl.n_max, L), dtype=tdt, device=dev)
+    elif mode in ("inner", "outer"):
+        avg = torch.empty(sp.n_features, dtype=tdt, device=dev)
+    else:
+        desc = torch.empty((nc, sp.n_features), dtype=tdt, device=dev)
+        if wl.jacobian:
+            jedge = torch.empty((E, 3, sp.n_edge_features), dtype=tdt, device=dev)
+            jself = torch.empty((nc, 3, sp.n_features), dtype=tdt, device=dev)
 
     def step():
         sp.build_neighbors(pos, Z)
-        if wl.jacobian:
+        if mode == "cc":
+            sp.coefficient_derivatives(cc, jce, jcs)
+        elif mode in ("inner", "outer"):
+            sp.compute_averaged(mode, avg)
+        elif wl.jacobian:
             sp.derivatives(desc, jedge, jself)
         else:
             sp.compute(desc)
@@ -179,10 +203,18 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
     seg_ms, seg_n = sp.timing(reset=True)
     sp.set_timing(False)
 
-    alg = algorithmic(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, wl.jacobian)
+    jac = wl.jacobian and mode == "derivatives"
+    alg = algorithmic(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, jac)
     kern = {"neighbors": seg_ms[0] / max(seg_n[0], 1), "density": seg_ms[1] / max(seg_n[1], 1),
             "jacobian": seg_ms[2] / max(seg_n[2], 1)}
-    if wl.jacobian:
+    if mode == "cc":
+        # the density kernel's gradient stores dominate: HBM-bound
+        b = cc_bytes(sp, wl, nc, E, out_bytes)
+        alg = dict(step=b, density=b, jacobian=0)
+        t = kern["density"] * 1e-3
+        roof = {"kernel": "k_density", "bound": "hbm", "achieved": b / t / 1e9, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "traffic": None, "alg_bytes_per_launch": b}
+    elif jac:
         # the edge-block writes dominate: HBM-bound kernel
         t = kern["jacobian"] * 1e-3
         roof = {"kernel": "k_jacobian", "bound": "hbm", "achieved": alg["jacobian"] / t / 1e9, "peak": HBM_PEAK_GBS,
@@ -192,7 +224,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
         fl = density_flops(wl, E, nc, sp.n_features)
         t = kern["density"] * 1e-3
         roof = {"kernel": "k_density", "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "traffic": measured_traffic(wl.name, "k_density"), "alg_flops_per_launch": fl}
+                "unit": "TFLOP/s", "traffic": measured_traffic(wl.name + ("" if mode == "derivatives" else "_" + mode),
+                                                               "k_density"), "alg_flops_per_launch": fl}
     roof["frac"] = roof["achieved"] / roof["peak"]
     line = {
         "metric": METRIC,
@@ -207,9 +240,9 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": wl.name, "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
+        "config": {"workload": wl.name + ("" if mode == "derivatives" else "_" + mode), "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
                    "l_max": wl.l_max, "r_cut": wl.r_cut, "sigma": wl.sigma, "species": list(wl.species),
-                   "output": dtype, "jacobian": wl.jacobian, "features": sp.n_features,
+                   "output": dtype, "jacobian": jac or mode == "cc", "mode": mode, "features": sp.n_features,
                    "edge_features": sp.n_edge_features},
         "kernel_ms": kern,
         "kernel_timing": "HIP events per segment over a second pass of the K steps",
@@ -219,7 +252,7 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False):
         "roofline": roof,
     }
     sp.close()
-    if with_cpu:
+    if with_cpu and mode == "derivatives":
         line["cpu_baseline"] = cpu_baseline(wl, st)
     return line
 
@@ -231,6 +264,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="water1000")
     ap.add_argument("--dtype", default="float32", choices=["float32", "float64"])
+    ap.add_argument("--mode", default="derivatives", choices=["derivatives", "cc", "inner", "outer"])
     ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for both bases; write JSONL here")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
@@ -253,7 +287,7 @@ def main():
                       f"jac {line['roofline']['frac']:.3f} of HBM", flush=True)
         return
     wl = workload_by_name(a.workload)
-    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline)
+    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode)
     print(json.dumps(line), flush=True)
 
 
