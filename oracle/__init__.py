@@ -63,6 +63,8 @@ def lib():
         vp, i64, i32, dbl = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
         L.oracle_neighbors.restype = i64
         L.oracle_neighbors.argtypes = [i64, vp, dbl, vp, i64, vp, vp, i64]
+        L.oracle_neighbors_periodic.restype = i64
+        L.oracle_neighbors_periodic.argtypes = [i64, vp, dbl, vp, vp, ctypes.c_int, vp, i64, vp, vp, vp, i64]
         L.oracle_neighbors_grid.restype = i64
         L.oracle_neighbors_grid.argtypes = [i64, vp, dbl, vp, vp, i64]
         L.oracle_solid_harmonics.restype = None
@@ -101,6 +103,51 @@ def neighbors(pos64: np.ndarray, r_cut: float, centers=None):
     cols = np.empty(max(E, 1), dtype=np.int32)
     lib().oracle_neighbors(n, _ptr(pos64), r_cut, _ptr(cen), nc, _ptr(row), _ptr(cols), E)
     return row, cols[:E]
+
+
+def image_bounds(pos64, r_cut, cell, pbc):
+    """Largest image index per direction that can reach the cutoff: the
+    interplanar spacing d_k = V / |b x c| (and cyclic) bounds how far an image
+    moves along each reciprocal direction; the spread of the fractional
+    coordinates adds to it."""
+    cell = np.asarray(cell, dtype=np.float64).reshape(3, 3)
+    frac = np.asarray(pos64, dtype=np.float64) @ np.linalg.inv(cell)
+    vol = abs(np.linalg.det(cell))
+    out = np.zeros(3, dtype=np.int32)
+    for k in range(3):
+        if pbc[k]:
+            cr = np.cross(cell[(k + 1) % 3], cell[(k + 2) % 3])
+            d = vol / np.linalg.norm(cr)
+            spread = frac[:, k].max() - frac[:, k].min() if len(frac) else 0.0
+            out[k] = int(np.ceil(r_cut / d + spread)) + 1
+    return out
+
+
+def neighbors_periodic(pos64, r_cut, cell, pbc, centers=None, f32=True):
+    """Brute-force periodic neighbour rows: (row, cols, img) with img[e] the
+    integer image (n_a, n_b, n_c) of atom cols[e]; ascending j, then n."""
+    pos64 = np.ascontiguousarray(pos64, dtype=np.float64)
+    cellv = np.ascontiguousarray(np.asarray(cell, dtype=np.float64).reshape(9))
+    nimg = np.ascontiguousarray(image_bounds(pos64, r_cut, cell, pbc))
+    n = pos64.shape[0]
+    cen = None if centers is None else np.ascontiguousarray(centers, dtype=np.int64)
+    nc = n if cen is None else len(cen)
+    row = np.zeros(nc + 1, dtype=np.int64)
+    args = (n, _ptr(pos64), r_cut, _ptr(cellv), _ptr(nimg), 1 if f32 else 0, _ptr(cen), nc, _ptr(row))
+    E = lib().oracle_neighbors_periodic(*args, None, None, 0)
+    cols = np.empty(max(E, 1), dtype=np.int32)
+    img = np.empty((max(E, 1), 3), dtype=np.int32)
+    lib().oracle_neighbors_periodic(*args, _ptr(cols), _ptr(img), E)
+    return row, cols[:E], img[:E]
+
+
+def image_position(pos64, cell, j, n, f32=True):
+    """r_j + ((n_a a + n_b b) + n_c c), float64, rounded to float32 if f32."""
+    cell = np.asarray(cell, dtype=np.float64).reshape(3, 3)
+    s = float(n[0]) * cell[0] + float(n[1]) * cell[1]
+    s = s + float(n[2]) * cell[2]
+    v = np.asarray(pos64[j], dtype=np.float64) + s
+    return v.astype(np.float32).astype(np.float64) if f32 else v
 
 
 def neighbors_grid(pos64: np.ndarray, r_cut: float):
@@ -238,6 +285,25 @@ class OracleSOAP:
                 for e in range(int(row[c]), int(row[c + 1])):
                     dself[c, :, spec_j[e]] -= dcout[e]
             out["dc_self"] = dself
+        return out
+
+    def compute_periodic(self, pos64, Z, cell, pbc, centers=None, f32=True, **kw):
+        """compute() for a periodic structure: every neighbour image becomes an
+        atom of an extended structure (the home atoms, then one entry per edge
+        at its image position), whose neighbour rows are the periodic rows.
+        Returns compute()'s dict plus img_atom / img_shift, the atom and image
+        of every extended index (home atoms: their own index, image 0)."""
+        pos64 = np.asarray(pos64, dtype=np.float64)
+        n = pos64.shape[0]
+        row, cols, img = neighbors_periodic(pos64, self.r_cut, cell, pbc, centers, f32)
+        E = len(cols)
+        ext = np.concatenate([pos64, np.array([image_position(pos64, cell, int(j), m, f32)
+                                               for j, m in zip(cols, img)]).reshape(E, 3)])
+        Zx = np.concatenate([np.asarray(Z), np.asarray(Z)[cols]])
+        out = self.compute(ext, Zx, centers=np.arange(n) if centers is None else centers,
+                           nb=(row, np.arange(n, n + E, dtype=np.int32)), **kw)
+        out["img_atom"] = np.concatenate([np.arange(n), cols]).astype(np.int64)
+        out["img_shift"] = np.concatenate([np.zeros((n, 3), dtype=np.int32), img])
         return out
 
     def power_spectrum(self, c):

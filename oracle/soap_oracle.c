@@ -81,6 +81,54 @@ int64_t oracle_neighbors(int64_t n_atoms, const double *pos, double rc, const in
     return e;
 }
 
+/* Periodic images, brute force.  cell[9] holds the lattice vectors a, b, c as
+ * rows; pbc[3] marks the periodic directions; nimg[3] bounds the image index
+ * per direction (0 where not periodic).  An edge (i -> j, n) exists for every
+ * atom j and integer image n with |n_k| <= nimg[k], (j, n) != (i, 0), whose
+ * image r_j + s(n), s(n) = ((n_a a + n_b b) + n_c c) evaluated in float64 in
+ * that order (and rounded to float32 when f32 != 0, the float32-mode reading),
+ * passes the cutoff test against r_i.  Rows: ascending j, then n in
+ * lexicographic (n_a, n_b, n_c) order.  Writes cols[e] = j and img[e][3] = n
+ * when cols is not NULL; returns the edge count. */
+static double image_coord(const double *pos, const double *cell, int64_t j, const int *n, int d, int f32) {
+    double s = (double)n[0] * cell[d];
+    s = s + (double)n[1] * cell[3 + d];
+    s = s + (double)n[2] * cell[6 + d];
+    double v = pos[3 * j + d] + s;
+    return f32 ? (double)(float)v : v;
+}
+
+int64_t oracle_neighbors_periodic(int64_t n_atoms, const double *pos, double rc, const double *cell,
+                                  const int32_t *nimg, int f32, const int64_t *centers, int64_t nc,
+                                  int64_t *row_ptr, int32_t *cols, int32_t *img, int64_t cap) {
+    double rc2 = rc * rc;
+    int64_t e = 0;
+    row_ptr[0] = 0;
+    for (int64_t c = 0; c < nc; ++c) {
+        int64_t i = centers ? centers[c] : c;
+        for (int64_t j = 0; j < n_atoms; ++j)
+            for (int na = -nimg[0]; na <= nimg[0]; ++na)
+                for (int nb = -nimg[1]; nb <= nimg[1]; ++nb)
+                    for (int ncc = -nimg[2]; ncc <= nimg[2]; ++ncc) {
+                        if (j == i && na == 0 && nb == 0 && ncc == 0) continue;
+                        int n[3] = {na, nb, ncc};
+                        double q[3];
+                        for (int d = 0; d < 3; ++d) q[d] = image_coord(pos, cell, j, n, d, f32);
+                        if (is_neighbour(pos + 3 * i, q, rc2)) {
+                            if (cols && e < cap) {
+                                cols[e] = (int32_t)j;
+                                img[3 * e] = na;
+                                img[3 * e + 1] = nb;
+                                img[3 * e + 2] = ncc;
+                            }
+                            ++e;
+                        }
+                    }
+        row_ptr[c + 1] = e;
+    }
+    return e;
+}
+
 /* A second, separately written neighbour builder on a uniform grid (cells of
  * edge >= r_cut), for structures too large for the all-pairs loop.  Returns
  * the directed edge count; cols ascending per row. */

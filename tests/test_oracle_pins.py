@@ -473,6 +473,94 @@ def test_averaged_modes_closed_forms(oracle_lib, rbf):
     assert np.abs(inner[~odd] - outer[~odd]).max() <= 1e-13 * np.abs(outer).max()
 
 
+# ------------------------------------------------------- periodic
+
+def _periodic_case(seed=5):
+    rng = np.random.default_rng(seed)
+    cell = np.array([[4.3, 0.0, 0.0], [0.9, 4.1, 0.0], [-0.4, 0.6, 4.6]])  # triclinic, smaller than 2 r_cut
+    frac = rng.uniform(0, 1, size=(7, 3))
+    return frac @ cell, np.array([1, 8, 1, 1, 8, 1, 8]), cell
+
+
+def test_periodic_neighbors_match_replicated_kdtree():
+    """Brute-force periodic rows equal a cKDTree query over an explicitly
+    replicated block of images."""
+    from scipy.spatial import cKDTree
+    pos, Z, cell = _periodic_case()
+    rc = 4.5
+    row, cols, img = oracle.neighbors_periodic(pos, rc, cell, (1, 1, 1), f32=False)
+    R = 3
+    shifts = np.array([(a, b, c) for a in range(-R, R + 1) for b in range(-R, R + 1) for c in range(-R, R + 1)])
+    rep = (pos[None, :, :] + (shifts @ cell)[:, None, :]).reshape(-1, 3)
+    tree = cKDTree(rep)
+    for i in range(len(pos)):
+        hits = set()
+        for k in tree.query_ball_point(pos[i], rc - 1e-12):
+            s_idx, j = divmod(k, len(pos))
+            if j == i and not shifts[s_idx].any():
+                continue
+            hits.add((j,) + tuple(shifts[s_idx]))
+        got = {(int(j),) + tuple(int(v) for v in m) for j, m in zip(cols[row[i]:row[i + 1]], img[row[i]:row[i + 1]])}
+        assert got == hits, i
+    assert len(cols) > 7 * 20  # several images per pair
+
+
+def test_periodic_large_cell_equals_cluster():
+    s = workloads.random_small(12, 9, 3.0, species=(1, 8))
+    o = oracle.OracleSOAP((1, 8), 4.0, 4, 4, 0.5, "gto")
+    cell = np.diag([60.0, 61.0, 62.0])
+    per = o.compute_periodic(s.pos64 + 20.0, s.Z, cell, (1, 1, 1), f32=False)["desc"]
+    ref = o.compute(s.pos64, s.Z)["desc"]
+    assert np.abs(per - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_periodic_translation_with_wrapping_and_supercell(rbf):
+    """Translating every atom and wrapping it back into the cell leaves each
+    descriptor unchanged; in a 2 x 1 x 1 supercell both copies of an atom have
+    that atom's descriptor."""
+    pos, Z, cell = _periodic_case(7)
+    o = oracle.OracleSOAP((1, 8), 4.5, 3, 4, 0.5, rbf)
+    base = o.compute_periodic(pos, Z, cell, (1, 1, 1), f32=False)["desc"]
+    scale = np.abs(base).max()
+    frac = (pos + np.array([1.7, -2.9, 0.8])) @ np.linalg.inv(cell)
+    wrapped = (frac - np.floor(frac)) @ cell
+    moved = o.compute_periodic(wrapped, Z, cell, (1, 1, 1), f32=False)["desc"]
+    assert np.abs(moved - base).max() < 1e-11 * scale
+    sup = np.concatenate([pos, pos + cell[0]])
+    cell2 = cell.copy()
+    cell2[0] *= 2
+    d2 = o.compute_periodic(sup, np.concatenate([Z, Z]), cell2, (1, 1, 1), f32=False)["desc"]
+    assert np.abs(d2[:7] - base).max() < 1e-11 * scale
+    assert np.abs(d2[7:] - base).max() < 1e-11 * scale
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+def test_periodic_jacobian_finite_differences(rbf):
+    """Moving an atom moves all of its images: the derivative of p_i by r_j is
+    the sum of the blocks of j's images, and by r_i the center block plus the
+    blocks of i's own images."""
+    pos, Z, cell = _periodic_case(11)
+    o = oracle.OracleSOAP((1, 8), 4.5, 3, 3, 0.5, rbf)
+    out = o.compute_periodic(pos, Z, cell, (1, 1, 1), f32=False, jacobian=True)
+    h = 1e-5
+    for c in (0, 4):
+        b0, b1 = out["blk_ptr"][c], out["blk_ptr"][c + 1]
+        total = {}
+        for b in range(b0, b1):
+            a = int(out["img_atom"][out["blk_j"][b]])
+            total[a] = total.get(a, 0) + out["jac"][b]
+        for j, J in total.items():
+            fd = np.empty_like(J)
+            for d in range(3):
+                pp, pm = pos.copy(), pos.copy()
+                pp[j, d] += h
+                pm[j, d] -= h
+                fd[d] = (o.compute_periodic(pp, Z, cell, (1, 1, 1), centers=[c], f32=False)["desc"][0] -
+                         o.compute_periodic(pm, Z, cell, (1, 1, 1), centers=[c], f32=False)["desc"][0]) / (2 * h)
+            assert np.abs(fd - J).max() < 1e-7 * max(np.abs(J).max(), 1e-3), (c, j)
+
+
 # ------------------------------------------------------- neighbours
 
 def test_neighbor_sets_brute_grid_and_kdtree(oracle_lib):
