@@ -140,6 +140,18 @@ int soap_feature_map(const soap_ctx *ctx, int32_t species_index, int32_t *out);
  * below.  This call synchronises `stream` once (to read E and device-side
  * checks).  Errors: SOAP_EINVAL, SOAP_ESPECIES (unknown Z),
  * SOAP_ECAPACITY (a row longer than SOAP_MAX_DEGREE), SOAP_ENOMEM, SOAP_EHIP.
+ *
+ * With a periodic cell (soap_set_cell) the edges run over periodic images:
+ * (i -> j, n) for every atom j and integer image n = (n_a, n_b, n_c) along
+ * the periodic directions with (j, n) != (i, 0) and the image position
+ *   r_j + s(n),  s(n) = ((n_a a + n_b b) + n_c c) evaluated in float64,
+ * rounded to float32 in SOAP_FP32 mode, within the cutoff of r_i by the
+ * test above.  Several images of one atom, and images of the center
+ * itself, are separate edges.  The images that can reach an atom are
+ * copied into a context-owned extended structure (positions are not read
+ * after this call); this takes one more synchronisation of `stream`.  Rows
+ * are ordered by species, then atom, then image (the order of the extended
+ * structure).
  */
 int soap_build_neighbors(soap_ctx *ctx, int64_t n_atoms, const void *pos_dev, const int32_t *Z_dev,
                          int64_t n_centers, const int32_t *centers_dev, int64_t *n_edges_out, void *stream);
@@ -150,6 +162,24 @@ int soap_build_neighbors(soap_ctx *ctx, int64_t n_atoms, const void *pos_dev, co
  * indices).  Either pointer may be NULL.  Errors: SOAP_ESTATE, SOAP_EHIP.
  */
 int soap_get_neighbors(soap_ctx *ctx, int64_t *row_ptr_dev, int32_t *cols_dev, void *stream);
+
+/*
+ * Periodic cell for the following soap_build_neighbors calls (the periodic
+ * flag of the paper's constructor, Sec. 3): cell[9] (host) holds the lattice
+ * vectors a, b, c as rows (angstrom), pbc[3] (host) is non-zero for each
+ * periodic direction.  Positions may lie anywhere; images are generated
+ * around the atoms as given.  cell = NULL returns to open boundaries (the
+ * default).  Discards the neighbour list.  Errors: SOAP_EINVAL (NULL pbc,
+ * degenerate cell).
+ */
+int soap_set_cell(soap_ctx *ctx, const double *cell, const int32_t *pbc);
+
+/*
+ * Image index n = (n_a, n_b, n_c) of every edge of the last build:
+ * img_dev[E][3] (int32, device); all zero without a periodic cell.
+ * Errors: SOAP_EINVAL, SOAP_ESTATE, SOAP_EHIP.
+ */
+int soap_get_neighbor_images(soap_ctx *ctx, int32_t *img_dev, void *stream);
 
 /*
  * Descriptor: desc_dev[n_centers][F] (dtype), Eq. (powerspectrum).
@@ -215,7 +245,10 @@ int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *ja
 /*
  * Expand a soap_derivatives result into the dense layout
  * dense_dev[n_centers][n_atoms][3][F] (dtype), zeros included.  Intended for
- * small structures (the dense array grows as n_centers * n_atoms).
+ * small structures (the dense array grows as n_centers * n_atoms).  With a
+ * periodic cell the blocks of all images of an atom (and of the center's
+ * own images) are summed into that atom's block: the derivative by the
+ * atom's position, all of its images moving with it.
  */
 int soap_scatter_dense(soap_ctx *ctx, const void *jac_edge_dev, const void *jac_self_dev, void *dense_dev,
                        void *stream);

@@ -68,8 +68,13 @@ struct soap_ctx {
     NbrWork nw{};
     DevBuf b_zero, b_bstart, b_acell, b_srec, b_sspec, b_deg, b_slots, b_scan, b_spec, b_row, b_cols, b_cscratch;
     DevBuf b_avg, b_avg_part; // averaged modes: per-center rows, column partial sums and means
+    // periodic cell (soap_set_cell) and the extended structure of the last build
+    bool periodic = false, built_periodic = false;
+    PeriodicCell cell{};
+    int64_t n_ext = 0;
+    DevBuf b_img_lohi, b_img_cnt, b_img_start, b_pos_ext, b_Z_ext, b_map_atom, b_map_img, b_iota;
     uint64_t work_epoch = 0; // density work-counter increments since the counters were zeroed
-    int32_t *h_flags = nullptr; // pinned: [0..3] flags, then int64 E at offset 8
+    int32_t *h_flags = nullptr; // pinned: [0..3] flags, int64 E at byte 16, int64 image count at byte 32
     // state of the last neighbour build
     bool have_rows = false;
     int64_t n_atoms = 0, nc = 0, E = 0;
@@ -492,17 +497,10 @@ int soap_feature_map(const soap_ctx *c, int32_t s, int32_t *out) {
     return SOAP_OK;
 }
 
-int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, const int32_t *Z_dev, int64_t n_centers,
-                         const int32_t *centers_dev, int64_t *n_edges_out, void *stream) {
-    if (!c) return SOAP_EINVAL;
-    c->have_rows = false;
-    if (n_atoms < 1 || n_atoms > INT32_MAX || !pos_dev || !Z_dev || n_centers < 1 || !n_edges_out)
-        return fail(c, SOAP_EINVAL, "invalid arguments to soap_build_neighbors");
-    if (!centers_dev && n_centers != n_atoms)
-        return fail(c, SOAP_EINVAL, "n_centers must equal n_atoms when centers_dev is NULL");
-    int rc;
-    if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
-    hipStream_t st = to_stream(stream);
+// The rows over n_atoms atoms (an extended structure for periodic cells, whose
+// first center_bound atoms are the real ones).
+static int build_rows(soap_ctx *c, int64_t n_atoms, int64_t center_bound, const void *pos_dev, const int32_t *Z_dev,
+                      int64_t n_centers, const int32_t *centers_dev, int64_t *E_out, hipStream_t st) {
     const bool f64 = c->dtype == SOAP_FP64;
     int64_t H = 1024;
     while (H < 2 * n_atoms) H <<= 1;
@@ -539,9 +537,8 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     w.slots = c->b_slots.as<int32_t>();
     w.scan_tmp = c->b_scan.as<int64_t>();
     int64_t *row = c->b_row.as<int64_t>();
-    SegTimer timer(c, 0, st);
-    e = nbr_phase1(w, n_atoms, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(), n_centers,
-                   centers_dev, c->r_cut, row, st);
+    e = nbr_phase1(w, n_atoms, center_bound, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(),
+                   n_centers, centers_dev, c->r_cut, row, st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
     c->work_epoch = 0; // the density work counters were zeroed with the flags
     // flags[0..3] and the total degree (int64 at flags + 4) in one copy
@@ -560,17 +557,144 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     e = nbr_phase2(w, n_atoms, pos_dev, f64, n_centers, centers_dev, c->r_cut, row, n_long > 0,
                    c->b_cols.as<int32_t>(), st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour rows");
+    *E_out = E;
+    return SOAP_OK;
+}
+
+// Periodic cell: the atoms plus their images that can reach an atom within
+// r_cut become an extended structure (context-owned arrays); returns its size.
+static int build_images(soap_ctx *c, int64_t n_atoms, const void *pos_dev, const int32_t *Z_dev, int64_t *n_ext,
+                        hipStream_t st) {
+    const bool f64 = c->dtype == SOAP_FP64;
+    const size_t elt = f64 ? 8 : 4;
+    const int64_t tiles = (n_atoms + 2047) / 2048 + 2;
+    hipError_t e = hipSuccess;
+    auto need = [&](DevBuf &b, size_t bytes) {
+        if (e == hipSuccess) e = b.ensure(bytes);
+    };
+    need(c->b_img_lohi, 8 * 6);
+    need(c->b_img_cnt, 4 * n_atoms);
+    need(c->b_img_start, 8 * (n_atoms + 1));
+    need(c->b_scan, 8 * tiles);
+    if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(periodic workspace)");
+    double *lohi = c->b_img_lohi.as<double>();
+    int64_t *start = c->b_img_start.as<int64_t>();
+    if ((e = periodic_count(n_atoms, pos_dev, f64, c->cell, lohi, c->b_img_cnt.as<int32_t>(), st)) != hipSuccess ||
+        (e = nbr_exclusive_scan(n_atoms, c->b_img_cnt.as<int32_t>(), start, c->b_scan.as<int64_t>(), nullptr, st)) !=
+            hipSuccess ||
+        (e = hipMemcpyAsync(c->h_flags + 8, start + n_atoms, 8, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+        (e = hipStreamSynchronize(st)) != hipSuccess)
+        return hip_fail(c, e, "periodic images");
+    int64_t n_img;
+    std::memcpy(&n_img, c->h_flags + 8, 8);
+    if (n_img < 0 || n_atoms + n_img > INT32_MAX)
+        return fail(c, SOAP_ECAPACITY, "%lld periodic images exceed the supported atom count", (long long)n_img);
+    const int64_t nx = n_atoms + n_img;
+    need(c->b_pos_ext, elt * 3 * nx);
+    need(c->b_Z_ext, 4 * nx);
+    need(c->b_map_atom, 4 * nx);
+    need(c->b_map_img, 12 * nx);
+    if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(periodic images)");
+    e = periodic_fill(n_atoms, pos_dev, f64, Z_dev, c->cell, lohi, start, c->b_pos_ext.p, c->b_Z_ext.as<int32_t>(),
+                      c->b_map_atom.as<int32_t>(), c->b_map_img.as<int32_t>(), st);
+    if (e != hipSuccess) return hip_fail(c, e, "periodic images");
+    *n_ext = nx;
+    return SOAP_OK;
+}
+
+int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, const int32_t *Z_dev, int64_t n_centers,
+                         const int32_t *centers_dev, int64_t *n_edges_out, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    c->have_rows = false;
+    if (n_atoms < 1 || n_atoms > INT32_MAX || !pos_dev || !Z_dev || n_centers < 1 || !n_edges_out)
+        return fail(c, SOAP_EINVAL, "invalid arguments to soap_build_neighbors");
+    if (!centers_dev && n_centers != n_atoms)
+        return fail(c, SOAP_EINVAL, "n_centers must equal n_atoms when centers_dev is NULL");
+    int rc;
+    if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
+    hipStream_t st = to_stream(stream);
+    SegTimer timer(c, 0, st);
+    int64_t E = 0, n_rows_atoms = n_atoms;
+    const void *pos_rows = pos_dev;
+    const int32_t *Z_rows = Z_dev, *cen_rows = centers_dev;
+    if (c->periodic) {
+        if ((rc = build_images(c, n_atoms, pos_dev, Z_dev, &n_rows_atoms, st)) != SOAP_OK) return rc;
+        pos_rows = c->b_pos_ext.p;
+        Z_rows = c->b_Z_ext.as<int32_t>();
+        if (!centers_dev) { // every atom, but not the images: an explicit list
+            hipError_t e = c->b_iota.ensure(4 * (size_t)n_centers);
+            if (e == hipSuccess) e = fill_iota(n_centers, c->b_iota.as<int32_t>(), st);
+            if (e != hipSuccess) return hip_fail(c, e, "periodic centers");
+            cen_rows = c->b_iota.as<int32_t>();
+        }
+    }
+    if ((rc = build_rows(c, n_rows_atoms, n_atoms, pos_rows, Z_rows, n_centers, cen_rows, &E, st)) != SOAP_OK)
+        return rc;
     timer.done();
     c->have_rows = true;
     c->n_atoms = n_atoms;
+    c->n_ext = n_rows_atoms;
     c->nc = n_centers;
     c->E = E;
-    c->pos = pos_dev;
-    c->Zdev = Z_dev;
-    c->centers = centers_dev;
-    c->built_f64 = f64;
+    c->pos = pos_rows;
+    c->Zdev = Z_rows;
+    c->centers = cen_rows;
+    c->built_f64 = c->dtype == SOAP_FP64;
+    c->built_periodic = c->periodic;
     *n_edges_out = E;
     return SOAP_OK;
+}
+
+int soap_set_cell(soap_ctx *c, const double *cell, const int32_t *pbc) {
+    if (!c) return SOAP_EINVAL;
+    c->have_rows = false;
+    if (!cell) {
+        c->periodic = false;
+        return SOAP_OK;
+    }
+    if (!pbc) return fail(c, SOAP_EINVAL, "pbc is NULL");
+    PeriodicCell C{};
+    for (int k = 0; k < 9; ++k) C.M[k] = cell[k];
+    const double *a = C.M, *b = C.M + 3, *cc = C.M + 6;
+    const double det = a[0] * (b[1] * cc[2] - b[2] * cc[1]) - a[1] * (b[0] * cc[2] - b[2] * cc[0]) +
+                       a[2] * (b[0] * cc[1] - b[1] * cc[0]);
+    if (!(std::fabs(det) > 1e-9)) return fail(c, SOAP_EINVAL, "the cell vectors are degenerate");
+    // B = M^-1 (adjugate over the determinant)
+    const double *m = C.M;
+    C.B[0] = (m[4] * m[8] - m[5] * m[7]) / det;
+    C.B[1] = (m[2] * m[7] - m[1] * m[8]) / det;
+    C.B[2] = (m[1] * m[5] - m[2] * m[4]) / det;
+    C.B[3] = (m[5] * m[6] - m[3] * m[8]) / det;
+    C.B[4] = (m[0] * m[8] - m[2] * m[6]) / det;
+    C.B[5] = (m[2] * m[3] - m[0] * m[5]) / det;
+    C.B[6] = (m[3] * m[7] - m[4] * m[6]) / det;
+    C.B[7] = (m[1] * m[6] - m[0] * m[7]) / det;
+    C.B[8] = (m[0] * m[4] - m[1] * m[3]) / det;
+    bool any = false;
+    for (int k = 0; k < 3; ++k) {
+        C.pbc[k] = pbc[k] != 0;
+        any = any || C.pbc[k];
+        if (!C.pbc[k]) continue;
+        // interplanar spacing d_k = |det| / |v_{k+1} x v_{k+2}|: an image n moves by
+        // at least |n_k| d_k, so fractional coordinates beyond r_cut / d_k of every
+        // atom cannot reach the cutoff (padded against rounding)
+        const double *u = C.M + 3 * ((k + 1) % 3), *v = C.M + 3 * ((k + 2) % 3);
+        const double cx = u[1] * v[2] - u[2] * v[1], cy = u[2] * v[0] - u[0] * v[2], cz = u[0] * v[1] - u[1] * v[0];
+        const double d = std::fabs(det) / std::sqrt(cx * cx + cy * cy + cz * cz);
+        C.eps[k] = c->r_cut / d * (1.0 + 1e-9) + 1e-9;
+    }
+    c->cell = C;
+    c->periodic = any;
+    return SOAP_OK;
+}
+
+int soap_get_neighbor_images(soap_ctx *c, int32_t *img_dev, void *stream) {
+    if (!c || !img_dev) return SOAP_EINVAL;
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    hipError_t e = map_edges(c->E, c->b_cols.as<int32_t>(), nullptr,
+                             c->built_periodic ? c->b_map_img.as<int32_t>() : nullptr, nullptr, img_dev,
+                             to_stream(stream));
+    return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_get_neighbor_images");
 }
 
 int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, void *stream) {
@@ -581,7 +705,9 @@ int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, voi
     if (row_ptr_dev)
         e = hipMemcpyAsync(row_ptr_dev, c->b_row.p, 8 * (c->nc + 1), hipMemcpyDeviceToDevice, st);
     if (e == hipSuccess && cols_dev && c->E > 0)
-        e = hipMemcpyAsync(cols_dev, c->b_cols.p, 4 * c->E, hipMemcpyDeviceToDevice, st);
+        e = c->built_periodic ? map_edges(c->E, c->b_cols.as<int32_t>(), c->b_map_atom.as<int32_t>(), nullptr,
+                                          cols_dev, nullptr, st)
+                              : hipMemcpyAsync(cols_dev, c->b_cols.p, 4 * c->E, hipMemcpyDeviceToDevice, st);
     return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_get_neighbors");
 }
 
@@ -677,7 +803,7 @@ int soap_scatter_dense(soap_ctx *c, const void *jac_edge_dev, const void *jac_se
     hipError_t e = hipMemsetAsync(dense_dev, 0, elt * (size_t)c->nc * c->n_atoms * 3 * c->F, st);
     if (e == hipSuccess)
         e = launch_scatter_dense(c->P, rows_of(c), c->built_f64, jac_edge_dev, jac_self_dev, c->d_fmap.as<int32_t>(),
-                                 dense_dev, st);
+                                 c->built_periodic ? c->b_map_atom.as<int32_t>() : nullptr, dense_dev, st);
     return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_scatter_dense");
 }
 
@@ -714,7 +840,8 @@ void soap_destroy(soap_ctx *c) {
     (void)hipDeviceSynchronize();
     for (DevBuf *b : {&c->d_const, &c->d_qmap, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_zero, &c->b_bstart, &c->b_acell,
                       &c->b_srec, &c->b_sspec, &c->b_deg, &c->b_slots, &c->b_scan, &c->b_spec, &c->b_row, &c->b_cols,
-                      &c->b_cscratch, &c->b_avg, &c->b_avg_part})
+                      &c->b_cscratch, &c->b_avg, &c->b_avg_part, &c->b_img_lohi, &c->b_img_cnt, &c->b_img_start,
+                      &c->b_pos_ext, &c->b_Z_ext, &c->b_map_atom, &c->b_map_img, &c->b_iota})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
     for (auto &r : c->recs) {

@@ -245,7 +245,7 @@ constexpr int CAND_CAP = 1024; // candidate list per wave in LDS
 // sorted-atom (cell) order, so the waves resident on a CU share cells.
 template <typename PosT>
 __global__ __launch_bounds__(64 * NBR_WAVES) void k_collect(
-    int64_t n_atoms, int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos,
+    int64_t center_bound, int64_t nc, const int32_t *__restrict__ centers, const PosT *__restrict__ pos,
     const int32_t *__restrict__ start, const typename Rec<PosT>::type *__restrict__ srec,
     const uint8_t *__restrict__ sspec, uint32_t mask, int b, double inv_h, double lim2, double rc2,
     int32_t *__restrict__ deg, int32_t *__restrict__ slots, int32_t *__restrict__ flags) {
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(64 * NBR_WAVES) void k_collect(
     if (centers) {
         c = t;
         i = centers[c];
-        if (i < 0 || i >= n_atoms) {
+        if (i < 0 || i >= center_bound) {
             if (lane == 0) {
                 atomicOr(&flags[0], 2);
                 deg[c] = 0;
@@ -468,6 +468,125 @@ hipError_t exclusive_scan(int64_t n, const int32_t *in, OutT *out, int64_t *tmp,
 
 unsigned blocks_for(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 
+// ---- periodic images ----
+template <typename PosT>
+__device__ __forceinline__ void frac_of(const PosT *pos, int64_t i, const PeriodicCell &C, double *f) {
+    const double r[3] = {(double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]};
+    for (int k = 0; k < 3; ++k) f[k] = (r[0] * C.B[k] + r[1] * C.B[3 + k]) + r[2] * C.B[6 + k];
+}
+
+// image index range of atom i per direction: f + n within [lo - eps, hi + eps]
+__device__ __forceinline__ void image_range(const double *f, const PeriodicCell &C, const double *lohi, int *nlo,
+                                            int *nhi) {
+    for (int k = 0; k < 3; ++k) {
+        const double a = lohi[k] - C.eps[k] - f[k], b = lohi[3 + k] + C.eps[k] - f[k];
+        // (a non-finite coordinate gets no images; the range is capped far above any
+        // count the atom limit allows, so the capped total is rejected on the host)
+        if (C.pbc[k] && isfinite(a) && isfinite(b)) {
+            nlo[k] = (int)fmax(ceil(a), -1e6);
+            nhi[k] = (int)fmin(floor(b), 1e6);
+        } else {
+            nlo[k] = nhi[k] = 0;
+        }
+    }
+}
+
+template <typename PosT>
+__global__ __launch_bounds__(1024) void k_frac_bounds(int64_t n, const PosT *__restrict__ pos, PeriodicCell C,
+                                                      double *__restrict__ lohi) {
+    __shared__ double red[6][1024];
+    double lo[3] = {INFINITY, INFINITY, INFINITY}, hi[3] = {-INFINITY, -INFINITY, -INFINITY};
+    for (int64_t i = threadIdx.x; i < n; i += 1024) {
+        double f[3];
+        frac_of(pos, i, C, f);
+        for (int k = 0; k < 3; ++k) {
+            lo[k] = fmin(lo[k], f[k]);
+            hi[k] = fmax(hi[k], f[k]);
+        }
+    }
+    for (int k = 0; k < 3; ++k) {
+        red[k][threadIdx.x] = lo[k];
+        red[3 + k][threadIdx.x] = hi[k];
+    }
+    __syncthreads();
+    for (int off = 512; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off)
+            for (int k = 0; k < 3; ++k) {
+                red[k][threadIdx.x] = fmin(red[k][threadIdx.x], red[k][threadIdx.x + off]);
+                red[3 + k][threadIdx.x] = fmax(red[3 + k][threadIdx.x], red[3 + k][threadIdx.x + off]);
+            }
+        __syncthreads();
+    }
+    if (threadIdx.x < 6) lohi[threadIdx.x] = red[threadIdx.x][0];
+}
+
+template <typename PosT>
+__global__ void k_image_count(int64_t n, const PosT *__restrict__ pos, PeriodicCell C, const double *__restrict__ lohi,
+                              int32_t *__restrict__ cnt) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    double f[3];
+    int lo[3], hi[3];
+    frac_of(pos, i, C, f);
+    image_range(f, C, lohi, lo, hi);
+    // n = 0 is always in range (lo <= f <= hi)
+    const int64_t m = (int64_t)(hi[0] - lo[0] + 1) * (hi[1] - lo[1] + 1) * (hi[2] - lo[2] + 1) - 1;
+    cnt[i] = (int32_t)(m < INT32_MAX ? m : INT32_MAX);
+}
+
+template <typename PosT>
+__global__ void k_image_fill(int64_t n, const PosT *__restrict__ pos, const int32_t *__restrict__ Z, PeriodicCell C,
+                             const double *__restrict__ lohi, const int64_t *__restrict__ start,
+                             PosT *__restrict__ pos_ext, int32_t *__restrict__ Z_ext, int32_t *__restrict__ map_atom,
+                             int32_t *__restrict__ map_img) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const double r[3] = {(double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]};
+    for (int d = 0; d < 3; ++d) pos_ext[3 * i + d] = pos[3 * i + d];
+    Z_ext[i] = Z[i];
+    map_atom[i] = (int32_t)i;
+    map_img[3 * i] = map_img[3 * i + 1] = map_img[3 * i + 2] = 0;
+    double f[3];
+    int lo[3], hi[3];
+    frac_of(pos, i, C, f);
+    image_range(f, C, lohi, lo, hi);
+    int64_t x = n + start[i];
+    for (int a = lo[0]; a <= hi[0]; ++a)
+        for (int b = lo[1]; b <= hi[1]; ++b)
+            for (int c = lo[2]; c <= hi[2]; ++c) {
+                if (a == 0 && b == 0 && c == 0) continue;
+                for (int d = 0; d < 3; ++d) {
+                    double sft = (double)a * C.M[d];
+                    sft = sft + (double)b * C.M[3 + d];
+                    sft = sft + (double)c * C.M[6 + d];
+                    pos_ext[3 * x + d] = (PosT)(r[d] + sft);
+                }
+                Z_ext[x] = Z[i];
+                map_atom[x] = (int32_t)i;
+                map_img[3 * x] = a;
+                map_img[3 * x + 1] = b;
+                map_img[3 * x + 2] = c;
+                ++x;
+            }
+}
+
+__global__ void k_iota(int64_t n, int32_t *__restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) out[i] = (int32_t)i;
+}
+
+__global__ void k_map_edges(int64_t E, const int32_t *__restrict__ cols, const int32_t *__restrict__ map,
+                            const int32_t *__restrict__ map_img, int32_t *__restrict__ out,
+                            int32_t *__restrict__ img_out) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= E) return;
+    const int32_t x = cols[e];
+    if (out) out[e] = map ? map[x] : x;
+    if (img_out)
+        for (int d = 0; d < 3; ++d) img_out[3 * e + d] = map_img ? map_img[3 * x + d] : 0;
+}
+
+
 struct Geometry {
     double inv_h, rc2, lim2;
     uint32_t mask;
@@ -491,9 +610,9 @@ Geometry geometry(const NbrWork &w, double r_cut) {
 
 } // namespace
 
-hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const int32_t *Z,
-                      const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers, double r_cut,
-                      int64_t *row_ptr, hipStream_t st) {
+hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, int64_t center_bound, const void *pos, bool pos64,
+                      const int32_t *Z, const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers,
+                      double r_cut, int64_t *row_ptr, hipStream_t st) {
     const Geometry g = geometry(w, r_cut);
     hipError_t e;
     // flags, density work counters and both bucket arrays are one zeroed block
@@ -512,18 +631,61 @@ hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool p
     if (pos64) {
         hipLaunchKernelGGL(k_bucket_fill<double>, dim3(gb), dim3(256), 0, st, n_atoms, (const double *)pos, spec,
                            w.atom_cell, w.bucket_start, w.bucket_fill, (double4 *)w.sorted_rec, w.sorted_spec);
-        hipLaunchKernelGGL(k_collect<double>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, n_atoms, nc, centers,
+        hipLaunchKernelGGL(k_collect<double>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, center_bound, nc, centers,
                            (const double *)pos, w.bucket_start, (const double4 *)w.sorted_rec,
                            w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
     } else {
         hipLaunchKernelGGL(k_bucket_fill<float>, dim3(gb), dim3(256), 0, st, n_atoms, (const float *)pos, spec,
                            w.atom_cell, w.bucket_start, w.bucket_fill, (float4 *)w.sorted_rec, w.sorted_spec);
-        hipLaunchKernelGGL(k_collect<float>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, n_atoms, nc, centers,
+        hipLaunchKernelGGL(k_collect<float>, dim3(gc), dim3(64 * NBR_WAVES), 0, st, center_bound, nc, centers,
                            (const float *)pos, w.bucket_start, (const float4 *)w.sorted_rec,
                            w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, (int64_t *)(w.flags + 4), w.flags + 1, st);
+}
+
+hipError_t periodic_count(int64_t n, const void *pos, bool pos64, const PeriodicCell &C, double *lohi, int32_t *cnt,
+                          hipStream_t st) {
+    if (pos64) {
+        hipLaunchKernelGGL(k_frac_bounds<double>, dim3(1), dim3(1024), 0, st, n, (const double *)pos, C, lohi);
+        hipLaunchKernelGGL(k_image_count<double>, dim3(blocks_for(n, 256)), dim3(256), 0, st, n, (const double *)pos,
+                           C, lohi, cnt);
+    } else {
+        hipLaunchKernelGGL(k_frac_bounds<float>, dim3(1), dim3(1024), 0, st, n, (const float *)pos, C, lohi);
+        hipLaunchKernelGGL(k_image_count<float>, dim3(blocks_for(n, 256)), dim3(256), 0, st, n, (const float *)pos, C,
+                           lohi, cnt);
+    }
+    return hipGetLastError();
+}
+
+hipError_t periodic_fill(int64_t n, const void *pos, bool pos64, const int32_t *Z, const PeriodicCell &C,
+                         const double *lohi, const int64_t *start, void *pos_ext, int32_t *Z_ext, int32_t *map_atom,
+                         int32_t *map_img, hipStream_t st) {
+    if (pos64)
+        hipLaunchKernelGGL(k_image_fill<double>, dim3(blocks_for(n, 256)), dim3(256), 0, st, n, (const double *)pos, Z,
+                           C, lohi, start, (double *)pos_ext, Z_ext, map_atom, map_img);
+    else
+        hipLaunchKernelGGL(k_image_fill<float>, dim3(blocks_for(n, 256)), dim3(256), 0, st, n, (const float *)pos, Z,
+                           C, lohi, start, (float *)pos_ext, Z_ext, map_atom, map_img);
+    return hipGetLastError();
+}
+
+hipError_t nbr_exclusive_scan(int64_t n, const int32_t *in, int64_t *out, int64_t *tmp, int64_t *total_copy,
+                              hipStream_t st) {
+    return exclusive_scan<int64_t>(n, in, out, tmp, total_copy, nullptr, st);
+}
+
+hipError_t fill_iota(int64_t n, int32_t *out, hipStream_t st) {
+    if (n > 0) hipLaunchKernelGGL(k_iota, dim3(blocks_for(n, 256)), dim3(256), 0, st, n, out);
+    return hipGetLastError();
+}
+
+hipError_t map_edges(int64_t E, const int32_t *cols, const int32_t *map, const int32_t *map_img, int32_t *out,
+                     int32_t *img_out, hipStream_t st) {
+    if (E > 0)
+        hipLaunchKernelGGL(k_map_edges, dim3(blocks_for(E, 256)), dim3(256), 0, st, E, cols, map, map_img, out, img_out);
+    return hipGetLastError();
 }
 
 hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,

@@ -1234,18 +1234,24 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
 // dense[ci][j][3][F]: zero-filled by the caller; each stored block is copied
 template <typename OutT>
 __global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge, const OutT *__restrict__ jself,
-                                const int32_t *__restrict__ fmap, OutT *__restrict__ dense) {
+                                const int32_t *__restrict__ fmap, const int32_t *__restrict__ atom_of,
+                                OutT *__restrict__ dense) {
     const int64_t ci = blockIdx.x;
     const int F = P.F, Fe = P.Fe;
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
     OutT *row = dense + ci * R.n_atoms * 3 * F;
     for (int k = threadIdx.x; k < 3 * F; k += blockDim.x) row[i * 3 * F + k] = jself[ci * 3 * F + k];
+    __syncthreads(); // a periodic image of the center adds to the center block
+    // thread k always owns component k / Fe, slot k % Fe, so the blocks of
+    // several images of one atom are summed by one thread, in edge order
     for (int64_t e = R.row_ptr[ci]; e < R.row_ptr[ci + 1]; ++e) {
-        const int64_t j = R.cols[e];
-        const int s = R.spec[j];
+        const int64_t x = R.cols[e], j = atom_of ? (int64_t)atom_of[x] : x;
+        const int s = R.spec[x];
         for (int k = threadIdx.x; k < 3 * Fe; k += blockDim.x) {
             const int d = k / Fe, fe = k - d * Fe;
-            row[(j * 3 + d) * F + fmap[s * Fe + fe]] = jedge[(e * 3 + d) * Fe + fe];
+            OutT *o = row + (j * 3 + d) * F + fmap[s * Fe + fe];
+            if (atom_of) *o += jedge[(e * 3 + d) * Fe + fe];
+            else *o = jedge[(e * 3 + d) * Fe + fe];
         }
     }
 }

@@ -64,9 +64,41 @@ struct NbrWork {
 constexpr size_t NBR_FLAGS_BYTES = 64, NBR_WORK_BYTES = 8 * (MAX_GROUPS + 1);
 inline size_t nbr_zero_bytes(int64_t H) { return NBR_FLAGS_BYTES + NBR_WORK_BYTES + 8 * (size_t)H; }
 
-hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, const int32_t *Z,
-                      const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers, double r_cut,
-                      int64_t *row_ptr, hipStream_t st);
+// Periodic structures: the neighbour search runs over the atoms plus the
+// images of them that can lie within r_cut of an atom (an extended
+// structure); the kernels then see each image as an atom.
+struct PeriodicCell {
+    double M[9];   // lattice vectors a, b, c as rows
+    double B[9];   // M^-1: fractional coordinates f = r B (r as a row vector)
+    double eps[3]; // r_cut over the interplanar spacing, padded; 0 for open directions
+    int pbc[3];
+};
+// fractional bounds (lo[3], hi[3]) of the atoms, then per atom the number of
+// its images n != 0 whose fractional coordinates stay within [lo - eps,
+// hi + eps] along every periodic direction (open directions: n = 0)
+hipError_t periodic_count(int64_t n, const void *pos, bool pos64, const PeriodicCell &C, double *lohi, int32_t *cnt,
+                          hipStream_t st);
+// extended structure: the atoms, then their images (atom-major, images in
+// lexicographic (n_a, n_b, n_c) order) at r + ((n_a a + n_b b) + n_c c)
+// evaluated in float64 and stored at the position precision; atom index and
+// image of every entry
+hipError_t periodic_fill(int64_t n, const void *pos, bool pos64, const int32_t *Z, const PeriodicCell &C,
+                         const double *lohi, const int64_t *start, void *pos_ext, int32_t *Z_ext, int32_t *map_atom,
+                         int32_t *map_img, hipStream_t st);
+// int32 counts -> int64 exclusive offsets (out has n+1); the total also to *total_copy
+hipError_t nbr_exclusive_scan(int64_t n, const int32_t *in, int64_t *out, int64_t *tmp, int64_t *total_copy,
+                              hipStream_t st);
+// out[k] = k
+hipError_t fill_iota(int64_t n, int32_t *out, hipStream_t st);
+// out[e] = map[cols[e]] (atom of each edge), and img_out[e][3] = map_img[cols[e]] if given
+hipError_t map_edges(int64_t E, const int32_t *cols, const int32_t *map, const int32_t *map_img, int32_t *out,
+                     int32_t *img_out, hipStream_t st);
+
+// center_bound: centers must index atoms below it (the atoms of an extended
+// periodic structure that are not images)
+hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, int64_t center_bound, const void *pos, bool pos64,
+                      const int32_t *Z, const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers,
+                      double r_cut, int64_t *row_ptr, hipStream_t st);
 // long_rows: some row is longer than TCAP (flags[2] > 0)
 hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,
                       const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, int32_t *cols,
@@ -125,7 +157,9 @@ hipError_t launch_column_mean(const void *in, bool f64, int64_t rows, int64_t co
                               double *mean, hipStream_t st);
 // power spectrum of one coefficient set c[S][n][L] (float64) into out[F]
 hipError_t launch_power_single(const Params &P, bool f64, const double *c, void *out, hipStream_t st);
+// atom_of (may be NULL = identity): atom of every (extended) neighbour index;
+// blocks of several images of one atom are summed
 hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,
-                                const int32_t *fmap, void *dense, hipStream_t st);
+                                const int32_t *fmap, const int32_t *atom_of, void *dense, hipStream_t st);
 
 } // namespace soap

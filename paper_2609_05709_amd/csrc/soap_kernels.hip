@@ -180,14 +180,14 @@ hipError_t launch_power_single(const Params &P, bool f64, const double *c, void 
 }
 
 hipError_t launch_scatter_dense(const Params &P, const Rows &R, bool f64, const void *jedge, const void *jself,
-                                const int32_t *fmap, void *dense, hipStream_t st) {
+                                const int32_t *fmap, const int32_t *atom_of, void *dense, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     if (f64)
         hipLaunchKernelGGL(dev::k_scatter_dense<double>, dim3((unsigned)R.nc), dim3(256), 0, st, P, R,
-                           (const double *)jedge, (const double *)jself, fmap, (double *)dense);
+                           (const double *)jedge, (const double *)jself, fmap, atom_of, (double *)dense);
     else
         hipLaunchKernelGGL(dev::k_scatter_dense<float>, dim3((unsigned)R.nc), dim3(256), 0, st, P, R,
-                           (const float *)jedge, (const float *)jself, fmap, (float *)dense);
+                           (const float *)jedge, (const float *)jself, fmap, atom_of, (float *)dense);
     return hipGetLastError();
 }
 

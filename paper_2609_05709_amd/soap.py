@@ -21,6 +21,7 @@ MAX_DEGREE = 2048
 # every entry point declared in include/soap.h
 ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_num_features", "soap_num_edge_features",
                "soap_feature_labels", "soap_feature_map", "soap_build_neighbors", "soap_get_neighbors",
+               "soap_set_cell", "soap_get_neighbor_images",
                "soap_compute", "soap_coefficients", "soap_coefficient_derivatives", "soap_compute_averaged",
                "soap_derivatives", "soap_scatter_dense", "soap_timing",
                "soap_last_error", "soap_destroy")
@@ -71,6 +72,10 @@ def load_library(path: str = LIB_PATH):
     L.soap_derivatives.argtypes = [vp, vp, vp, vp, vp]
     L.soap_scatter_dense.restype = ctypes.c_int
     L.soap_scatter_dense.argtypes = [vp, vp, vp, vp, vp]
+    L.soap_set_cell.restype = ctypes.c_int
+    L.soap_set_cell.argtypes = [vp, vp, vp]
+    L.soap_get_neighbor_images.restype = ctypes.c_int
+    L.soap_get_neighbor_images.argtypes = [vp, vp, vp]
     L.soap_coefficient_derivatives.restype = ctypes.c_int
     L.soap_coefficient_derivatives.argtypes = [vp, vp, vp, vp, vp]
     L.soap_compute_averaged.restype = ctypes.c_int
@@ -186,6 +191,27 @@ class Soap:
         self._keep = (pos, Z, centers)  # the library reads these in later calls
         self.E, self.n_centers, self.n_atoms = int(E.value), int(nc), int(pos.shape[0])
         return self.E
+
+    def set_cell(self, cell=None, pbc=(True, True, True)):
+        """Periodic cell (3 x 3, lattice vectors as rows, angstrom) and periodic
+        directions for the next build_neighbors; None = open boundaries."""
+        import numpy as np
+        self.E = self.n_centers = None
+        if cell is None:
+            self._check(self._L.soap_set_cell(self._h, None, None))
+            return
+        c = np.ascontiguousarray(np.asarray(cell, dtype=np.float64).reshape(9))
+        p = np.ascontiguousarray(np.asarray(pbc, dtype=np.int32).reshape(3))
+        self._check(self._L.soap_set_cell(self._h, c.ctypes.data, p.ctypes.data))
+
+    def neighbor_images(self):
+        """(E, 3) int32 image index of every edge of the last build."""
+        import torch
+        if self.E is None:
+            raise SoapError(SOAP_ESTATE, "no neighbour list: call build_neighbors first")
+        img = torch.empty((max(self.E, 1), 3), dtype=torch.int32, device="cuda")
+        self._check(self._L.soap_get_neighbor_images(self._h, img.data_ptr(), _stream()))
+        return img[: self.E]
 
     def neighbors(self):
         import torch
