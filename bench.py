@@ -10,11 +10,13 @@ r_cut 6 A, sigma 0.5 A, n_max 8, l_max 6, descriptor + Jacobian, float32
 outputs.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--dtype float32|float64]
-                  [--mode derivatives|cc|inner|outer] [--grid OUT.jsonl] [--no-cpu-baseline]
+                  [--mode derivatives|cc|inner|outer] [--periodic] [--grid OUT.jsonl] [--no-cpu-baseline]
 
 --mode picks the output of a Jacobian workload: the descriptor + Jacobian
 (default), the coefficients and their Jacobian ("cc"), or one averaged
-descriptor row ("inner", "outer").
+descriptor row ("inner", "outer").  --periodic puts the structure in an
+orthorhombic periodic cell 1.6 A wider than its extent (images across the
+faces become neighbours).
 """
 from __future__ import annotations
 
@@ -141,7 +143,7 @@ def cc_bytes(sp, wl, nc, E, out_bytes):
     return (nc * S * nL + E * 3 * nL + nc * 3 * S * nL) * out_bytes
 
 
-def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"):
+def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
@@ -149,6 +151,10 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
     out_bytes = 8 if dtype == "float64" else 4
     dev = torch.device("cuda:0")
     sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+    if periodic:
+        lo = st.pos.min(axis=0) - np.float32(0.8)
+        st = type(st)((st.pos - lo).astype(np.float32), st.Z, st.radius, st.draws, dict(st.recipe, periodic=True))
+        sp.set_cell(np.diag((st.pos.max(axis=0) + 0.8).astype(np.float64)), (1, 1, 1))
     pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to(dev, tdt)
     Z = torch.from_numpy(st.Z).to(dev)
     E = sp.build_neighbors(pos, Z)
@@ -218,7 +224,7 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         # the edge-block writes dominate: HBM-bound kernel
         t = kern["jacobian"] * 1e-3
         roof = {"kernel": "k_jacobian", "bound": "hbm", "achieved": alg["jacobian"] / t / 1e9, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "traffic": measured_traffic(wl.name, "k_jacobian"),
+                "unit": "GB/s", "traffic": None if periodic else measured_traffic(wl.name, "k_jacobian"),
                 "alg_bytes_per_launch": alg["jacobian"]}
     else:
         fl = density_flops(wl, E, nc, sp.n_features)
@@ -240,7 +246,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": wl.name + ("" if mode == "derivatives" else "_" + mode), "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
+        "config": {"workload": wl.name + ("" if mode == "derivatives" else "_" + mode) + ("_periodic" if periodic else ""),
+                   "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
                    "l_max": wl.l_max, "r_cut": wl.r_cut, "sigma": wl.sigma, "species": list(wl.species),
                    "output": dtype, "jacobian": jac or mode == "cc", "mode": mode, "features": sp.n_features,
                    "edge_features": sp.n_edge_features},
@@ -252,7 +259,7 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         "roofline": roof,
     }
     sp.close()
-    if with_cpu and mode == "derivatives":
+    if with_cpu and mode == "derivatives" and not periodic:
         line["cpu_baseline"] = cpu_baseline(wl, st)
     return line
 
@@ -265,6 +272,7 @@ def main():
     ap.add_argument("--workload", default="water1000")
     ap.add_argument("--dtype", default="float32", choices=["float32", "float64"])
     ap.add_argument("--mode", default="derivatives", choices=["derivatives", "cc", "inner", "outer"])
+    ap.add_argument("--periodic", action="store_true")
     ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for both bases; write JSONL here")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
@@ -287,7 +295,7 @@ def main():
                       f"jac {line['roofline']['frac']:.3f} of HBM", flush=True)
         return
     wl = workload_by_name(a.workload)
-    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode)
+    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic)
     print(json.dumps(line), flush=True)
 
 
