@@ -49,7 +49,8 @@ class _Params(ctypes.Structure):
                 ("rq_hi", ctypes.c_void_p), ("rq_lo", ctypes.c_void_p),
                 ("sh_lmax", ctypes.c_int32),
                 ("sh_ptr", ctypes.c_void_p), ("sh_exp", ctypes.c_void_p),
-                ("sh_c_hi", ctypes.c_void_p), ("sh_c_lo", ctypes.c_void_p)]
+                ("sh_c_hi", ctypes.c_void_p), ("sh_c_lo", ctypes.c_void_p),
+                ("wn_hi", ctypes.c_void_p), ("wn_lo", ctypes.c_void_p)]
 
 
 _lib = None
@@ -166,8 +167,8 @@ class OracleSOAP:
 
     def __init__(self, species, r_cut: float, n_max: int, l_max: int, sigma: float, rbf: str = "gto",
                  quad_n: int = 64):
-        if rbf not in ("gto", "polynomial"):
-            raise ValueError("rbf must be 'gto' or 'polynomial'")
+        if rbf not in ("gto", "polynomial", "polynomial-laplace"):
+            raise ValueError("rbf must be 'gto', 'polynomial' or 'polynomial-laplace'")
         if n_max < 1 or l_max < 0 or sigma <= 0:
             raise ValueError("bad basis size or sigma")
         if rbf == "gto" and r_cut <= 1.0:
@@ -178,7 +179,7 @@ class OracleSOAP:
             float(r_cut), int(n_max), int(l_max), float(sigma), rbf, int(quad_n)
         self._keep = []
         p = _Params()
-        p.S, p.n, p.lmax, p.rbf = self.S, self.n_max, self.l_max, 0 if rbf == "gto" else 1
+        p.S, p.n, p.lmax, p.rbf = self.S, self.n_max, self.l_max, {"gto": 0, "polynomial": 1}.get(rbf, 2)
         p.rc, p.sigma = self.r_cut, self.sigma
         if rbf == "gto":
             g = constants.gto_arrays(self.r_cut, self.n_max, self.l_max)
@@ -189,6 +190,10 @@ class OracleSOAP:
             p.Q = self.quad_n
             for k in ("G_hi", "G_lo", "rq_hi", "rq_lo"):
                 setattr(p, k, self._hold(g[k]))
+            if rbf == "polynomial-laplace":
+                wl = constants.poly_laplace_arrays(self.r_cut, self.n_max)
+                for k in ("wn_hi", "wn_lo"):
+                    setattr(p, k, self._hold(wl[k]))
         sh = constants.solid_harmonic_arrays(self.l_max + 1)
         p.sh_lmax = self.l_max + 1
         for k in ("sh_ptr", "sh_exp", "sh_c_hi", "sh_c_lo"):

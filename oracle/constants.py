@@ -147,6 +147,16 @@ def poly_mp(r_cut: float, n_max: int, quad_n: int):
         return N, W, rq, wq, g
 
 
+def poly_laplace_arrays(r_cut: float, n_max: int) -> dict:
+    """W_nk / N_k of the polynomial basis (Eqs. poly-norm, poly-overlap), the
+    coefficients of the Laplace-form radial factors (Eq. poly-coefficients)."""
+    N, W, _, _, _ = poly_mp(r_cut, n_max, 2)
+    with mp.workdps(DPS):
+        wn = [W[a, b] / N[b] for a in range(n_max) for b in range(n_max)]
+        h, l = _split_array(wn)
+    return dict(wn_hi=h, wn_lo=l)
+
+
 def poly_arrays(r_cut: float, n_max: int, quad_n: int) -> dict:
     N, W, rq, wq, g = poly_mp(r_cut, n_max, quad_n)
     with mp.workdps(DPS):

@@ -36,7 +36,7 @@
 typedef long double ld;
 
 typedef struct {
-    int32_t S, n, lmax, rbf; /* rbf: 0 = GTO, 1 = polynomial */
+    int32_t S, n, lmax, rbf; /* rbf: 0 = GTO, 1 = polynomial (quadrature), 2 = polynomial (Laplace) */
     double rc, sigma;
     /* GTO: alpha[l][k], beta[l][n][k] */
     const double *alpha_hi, *alpha_lo, *beta_hi, *beta_lo;
@@ -47,6 +47,8 @@ typedef struct {
     int32_t sh_lmax;
     const int32_t *sh_ptr, *sh_exp;
     const double *sh_c_hi, *sh_c_lo;
+    /* polynomial, Laplace variant: W_nk / N_k (rbf 2; G and rq still give the on-site term) */
+    const double *wn_hi, *wn_lo;
 } oracle_params;
 
 #define LD(h, l) ((ld)(h) + (ld)(l))
@@ -297,6 +299,31 @@ static void radial(const oracle_params *P, ld r, ld *R, ld *dR) {
                     ld e = expl(-al * r * r / den) / powl(den, (ld)l + 1.5L);
                     acc += be * e;
                     dacc += be * e * (-2.0L * al * r / den);
+                }
+                R[a * (lmax + 1) + l] = pref * acc;
+                dR[a * (lmax + 1) + l] = pref * dacc;
+            }
+    } else if (P->rbf == 2) {
+        /* Eqs. (poly-coefficients) and (poly-radial-derivative), the Laplace
+           (steepest-descent) form to first order in sigma^2, k = 1..n_max:
+           f_nl = (2 pi)^{3/2} s^3 sum_k W_nk/N_k (rc-r)^{k+2}
+                  [1 - l(l+1)s^2/(2r^2) - (k+2)s^2/(r(rc-r)) + (k+2)(k+1)s^2/(2(rc-r)^2)]
+           f'_nl = (2 pi)^{3/2} s^3 sum_k W_nk/N_k (rc-r)^{k+1}
+                  [-(k+2) + l(l+1)s^2(rc-r)/r^3 + (k+2)(l(l+1)+2)s^2/(2r^2)
+                   + (k+1)(k+2)s^2/(r(rc-r)) - k(k+1)(k+2)s^2/(2(rc-r)^2)] */
+        ld pref = powl(2.0L * 3.14159265358979323846264338327950288L, 1.5L) * s2 * (ld)P->sigma;
+        ld rc = (ld)P->rc, u = rc - r;
+        for (int a = 0; a < n; ++a)
+            for (int l = 0; l <= lmax; ++l) {
+                ld ll = (ld)(l * (l + 1)), acc = 0, dacc = 0;
+                for (int b = 0; b < n; ++b) {
+                    ld k = (ld)(b + 1), wn = LD(P->wn_hi[a * n + b], P->wn_lo[a * n + b]);
+                    ld br = 1.0L - ll * s2 / (2.0L * r * r) - (k + 2) * s2 / (r * u) +
+                            (k + 2) * (k + 1) * s2 / (2.0L * u * u);
+                    ld dbr = -(k + 2) + ll * s2 * u / (r * r * r) + (k + 2) * (ll + 2) * s2 / (2.0L * r * r) +
+                             (k + 1) * (k + 2) * s2 / (r * u) - k * (k + 1) * (k + 2) * s2 / (2.0L * u * u);
+                    acc += wn * powl(u, k + 2) * br;
+                    dacc += wn * powl(u, k + 1) * dbr;
                 }
                 R[a * (lmax + 1) + l] = pref * acc;
                 dR[a * (lmax + 1) + l] = pref * dacc;

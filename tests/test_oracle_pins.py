@@ -473,6 +473,42 @@ def test_averaged_modes_closed_forms(oracle_lib, rbf):
     assert np.abs(inner[~odd] - outer[~odd]).max() <= 1e-13 * np.abs(outer).max()
 
 
+# ------------------------------------------------- polynomial, Laplace form
+
+def test_poly_laplace_converges_to_quadrature_as_sigma4():
+    """Eq. (poly-coefficients) is the first-order (sigma^2) Laplace expansion of
+    the exact radial integral: its error against the quadrature form falls as
+    sigma^4, i.e. by ~16 when sigma halves (a wrong or missing sigma^2 term
+    would leave a sigma^2 error, a factor ~4)."""
+    r = 2.1
+    errs = []
+    for sigma in (0.4, 0.2):
+        q = oracle.OracleSOAP((8,), 5.0, 4, 4, sigma, "polynomial", quad_n=256).radial(r)[0]
+        la = oracle.OracleSOAP((8,), 5.0, 4, 4, sigma, "polynomial-laplace").radial(r)[0]
+        errs.append(np.abs(la - q).max() / np.abs(q).max())
+    assert errs[1] < 2e-2
+    assert 10.0 < errs[0] / errs[1] < 24.0, errs
+
+
+@pytest.mark.parametrize("r", [0.9, 2.3, 4.1])
+def test_poly_laplace_derivative_by_finite_differences(r):
+    """Eq. (poly-radial-derivative) against central differences of Eq.
+    (poly-coefficients)."""
+    o = oracle.OracleSOAP((1, 8), 5.0, 5, 6, 0.4, "polynomial-laplace")
+    h = 1e-6
+    dR = o.radial(r)[1]
+    fd = (o.radial(r + h)[0] - o.radial(r - h)[0]) / (2 * h)
+    assert np.abs(fd - dR).max() < 1e-7 * np.abs(dR).max()
+
+
+def test_poly_laplace_onsite_equals_quadrature_onsite():
+    """The center's own l = 0 term comes from the one-dimensional integral
+    I_k0(0) in both polynomial forms."""
+    a = oracle.OracleSOAP((8,), 5.0, 4, 4, 0.4, "polynomial").radial(1.0)[2]
+    b = oracle.OracleSOAP((8,), 5.0, 4, 4, 0.4, "polynomial-laplace").radial(1.0)[2]
+    assert np.array_equal(a, b)
+
+
 # ------------------------------------------------------- periodic
 
 def _periodic_case(seed=5):
