@@ -59,16 +59,17 @@ typedef struct soap_ctx soap_ctx;
 #define SOAP_ESTATE (-6)    /* call order violated (e.g. compute before build) */
 
 #define SOAP_RBF_GTO 0
-#define SOAP_RBF_POLYNOMIAL 1
+#define SOAP_RBF_POLYNOMIAL 1         /* exact radial integral, Gauss-Legendre quadrature */
+#define SOAP_RBF_POLYNOMIAL_LAPLACE 2 /* same basis, Laplace (steepest-descent) form to O(sigma^2) */
 
 #define SOAP_FP32 0
 #define SOAP_FP64 1
 
-/* Largest neighbour count per center the neighbour builder accepts. */
 /* averaging modes of soap_compute_averaged (Sec. 3, the density-averaged variants) */
 #define SOAP_AVERAGE_INNER 1
 #define SOAP_AVERAGE_OUTER 2
 
+/* Largest neighbour count per center the neighbour builder accepts. */
 #define SOAP_MAX_DEGREE 2048
 
 /*
@@ -78,7 +79,14 @@ typedef struct soap_ctx soap_ctx;
  *   r_cut     : cutoff radius; GTO requires r_cut > 1 (the widths of
  *               Eq. (gto-alphas) place the first primitive at 1 A).
  *   n_max     : 1..16 radial functions;  l_max: 0..14;  sigma > 0.
- *   rbf       : SOAP_RBF_GTO or SOAP_RBF_POLYNOMIAL.
+ *   rbf       : SOAP_RBF_GTO, SOAP_RBF_POLYNOMIAL (Eq. poly-coefficients-exact,
+ *               the radial integral by Gauss-Legendre quadrature) or
+ *               SOAP_RBF_POLYNOMIAL_LAPLACE (the same basis with the radial
+ *               factors of Eqs. poly-coefficients and poly-radial-derivative,
+ *               the Laplace form to first order in sigma^2: an approximation
+ *               for sigma small against the distances r and r_cut - r; the
+ *               on-site term of a center, and of a neighbour at distance 0,
+ *               stays the quadrature's).
  * Basis constants (Loewdin coefficients, quadrature tables) are computed here
  * on the host in 113-bit floating point and uploaded once.
  * Errors: SOAP_EINVAL, SOAP_ENOMEM, SOAP_EHIP.  *out is NULL on error.

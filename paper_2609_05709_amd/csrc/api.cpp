@@ -239,7 +239,7 @@ int upload_constants(soap_ctx *c) {
     const int n = c->n, lw = c->lmax + 1, S = (int)c->Z.size();
     char msg[256] = {0};
     const int ldN = lw + 1; // harmonics tables cover l <= l_max + 1
-    std::vector<double> betaC, betaCa, aprime, G, rq, c0(n), Nlm((size_t)ldN * ldN);
+    std::vector<double> betaC, betaCa, aprime, G, rq, WN, c0(n), Nlm((size_t)ldN * ldN);
     if (c->rbf == SOAP_RBF_GTO) {
         betaC.resize((size_t)lw * n * n);
         betaCa.resize((size_t)lw * n * n);
@@ -252,6 +252,11 @@ int upload_constants(soap_ctx *c) {
         rq.resize(c->Q);
         if (soap_basis_poly(c->r_cut, n, c->sigma, c->Q, G.data(), rq.data(), c0.data(), msg, sizeof msg) != 0)
             return fail(c, SOAP_EINVAL, "%s", msg);
+        if (c->rbf == SOAP_RBF_POLYNOMIAL_LAPLACE) {
+            WN.resize((size_t)n * n * 4);
+            if (soap_basis_poly_laplace(c->r_cut, n, c->sigma, WN.data(), msg, sizeof msg) != 0)
+                return fail(c, SOAP_EINVAL, "%s", msg);
+        }
     }
     soap_basis_sh_norms(c->lmax + 1, Nlm.data());
     // gradient identities of the harmonics per (l, m >= 0): with the degree
@@ -282,13 +287,14 @@ int upload_constants(soap_ctx *c) {
             for (int k = 2; k <= l - m; ++k) v /= (long double)k;
             Nt[(size_t)l * ldN + m] = (double)v;
         }
-    // one constant buffer: betaC | betaCa | aprime | G | rq | c0 | Nt | gcoef
+    // one constant buffer: betaC | betaCa | aprime | G | rq | WN | c0 | Nt | gcoef
     std::vector<double> all;
     size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
     size_t o_ba = all.size(); all.insert(all.end(), betaCa.begin(), betaCa.end());
     size_t o_ap = all.size(); all.insert(all.end(), aprime.begin(), aprime.end());
     size_t o_G = all.size(); all.insert(all.end(), G.begin(), G.end());
     size_t o_rq = all.size(); all.insert(all.end(), rq.begin(), rq.end());
+    size_t o_wn = all.size(); all.insert(all.end(), WN.begin(), WN.end());
     size_t o_c0 = all.size(); all.insert(all.end(), c0.begin(), c0.end());
     size_t o_Nt = all.size(); all.insert(all.end(), Nt.begin(), Nt.end());
     size_t o_gc = all.size(); all.insert(all.end(), gcoef.begin(), gcoef.end());
@@ -325,11 +331,16 @@ int upload_constants(soap_ctx *c) {
     P.nq_full = c->nq_full;
     P.sigma = c->sigma;
     P.inv_s2 = 1.0 / (c->sigma * c->sigma);
+    P.rc = c->r_cut;
+    P.inv_rc2 = 2.0 / c->r_cut;
+    P.s2 = c->sigma * c->sigma;
+    P.hs2 = 0.5 * P.s2;
     P.betaC = d + o_bc;
     P.betaCa = d + o_ba;
     P.aprime = d + o_ap;
     P.G = d + o_G;
     P.rq = d + o_rq;
+    P.WN = d + o_wn;
     P.c0 = d + o_c0;
     P.Nt = d + o_Nt;
     P.gcoef = d + o_gc;
@@ -414,7 +425,8 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
     if (n_max < 1 || n_max > NMAX) return bad("n_max must be in 1..16");
     if (l_max < 0 || l_max > LMAX) return bad("l_max must be in 0..14");
     if (!(sigma > 0) || !(r_cut > 0)) return bad("sigma and r_cut must be positive");
-    if (rbf != SOAP_RBF_GTO && rbf != SOAP_RBF_POLYNOMIAL) return bad("unknown rbf");
+    if (rbf != SOAP_RBF_GTO && rbf != SOAP_RBF_POLYNOMIAL && rbf != SOAP_RBF_POLYNOMIAL_LAPLACE)
+        return bad("unknown rbf");
     if (rbf == SOAP_RBF_GTO && !(r_cut > 1.0)) return bad("the GTO basis needs r_cut > 1");
     if (n_species * n_max > 255) return bad("n_species * n_max must not exceed 255");
     std::vector<int32_t> Z(species_Z, species_Z + n_species);

@@ -141,12 +141,11 @@ extern "C" int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, 
     return 0;
 }
 
-extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n, double *G, double *rq_out,
-                               double *c0, char *err, int errlen) {
-    const int n = n_max, Q = quad_n;
-    const q128 rc = r_cut, s2 = (q128)sigma * (q128)sigma;
-    // Eqs. (poly-norm), (poly-overlap); W = S^{-1/2}
-    std::vector<q128> N(n), S((size_t)n * n), W;
+// Norms N_k of (r_cut - r)^{k+2} (Eq. poly-norm) and the Loewdin weights
+// W = S^{-1/2} of their overlap matrix (Eq. poly-overlap), k = 1..n.
+static bool poly_weights(q128 rc, int n, std::vector<q128> &N, std::vector<q128> &W, char *err, int errlen) {
+    std::vector<q128> S((size_t)n * n);
+    N.assign(n, 0);
     for (int a = 0; a < n; ++a) {
         int k = a + 1;
         N[a] = sqrtq(powq(rc, (q128)(2 * k + 5)) / (q128)(2 * k + 5));
@@ -158,8 +157,17 @@ extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n
         }
     if (!inv_sqrt_spd(n, S, W)) {
         set_err(err, errlen, "polynomial overlap matrix is not positive definite");
-        return -1;
+        return false;
     }
+    return true;
+}
+
+extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n, double *G, double *rq_out,
+                               double *c0, char *err, int errlen) {
+    const int n = n_max, Q = quad_n;
+    const q128 rc = r_cut, s2 = (q128)sigma * (q128)sigma;
+    std::vector<q128> N, W;
+    if (!poly_weights(rc, n, N, W, err, errlen)) return -1;
     // Gauss-Legendre nodes on [-1, 1] by Newton iteration on P_Q
     std::vector<q128> t(Q), wt(Q);
     for (int i = 0; i < Q; ++i) {
@@ -208,6 +216,38 @@ extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n
             acc += w * r * r * g * expq(-r * r / (2 * s2));
         }
         c0[a] = (double)(sqrtq(fourpi) * acc);
+    }
+    return 0;
+}
+
+extern "C" int soap_basis_poly_laplace(double r_cut, int n_max, double sigma, double *CH, char *err, int errlen) {
+    const int n = n_max;
+    std::vector<q128> N, W;
+    if (!poly_weights((q128)r_cut, n, N, W, err, errlen)) return -1;
+    const q128 rc = r_cut, s = sigma, pref = powq(2 * PI_Q, (q128)1.5) * s * s * s;
+    // values of the four polynomials at the Chebyshev points t_p = cos(pi (p + 1/2) / n)
+    std::vector<q128> val((size_t)n * 4);
+    for (int a = 0; a < n; ++a) {
+        for (int p = 0; p < n; ++p) {
+            const q128 t = cosq(PI_Q * ((q128)p + 0.5Q) / (q128)n), u = (t + 1) * rc / 2;
+            q128 q[4] = {0, 0, 0, 0}, up = 1;
+            for (int k = 1; k <= n; ++k) {
+                const q128 v = pref * W[(size_t)a * n + k - 1] / N[k - 1] * up;
+                q[0] += v;
+                q[1] += (q128)(k + 2) * v;
+                q[2] += (q128)((k + 1) * (k + 2)) * v;
+                q[3] += (q128)(k * (k + 1) * (k + 2)) * v;
+                up *= u;
+            }
+            for (int j = 0; j < 4; ++j) val[(size_t)p * 4 + j] = q[j];
+        }
+        // c_i = (2 - [i = 0]) / n sum_p Q(t_p) T_i(t_p)
+        for (int i = 0; i < n; ++i)
+            for (int j = 0; j < 4; ++j) {
+                q128 acc = 0;
+                for (int p = 0; p < n; ++p) acc += val[(size_t)p * 4 + j] * cosq(PI_Q * (q128)i * ((q128)p + 0.5Q) / (q128)n);
+                CH[((size_t)a * n + i) * 4 + j] = (double)(acc * (i == 0 ? 1 : 2) / (q128)n);
+            }
     }
     return 0;
 }

@@ -15,7 +15,9 @@
 //         chain rule Eq. poly-cartesian-derivative written for S_lm):
 //         B_nl  = r^-l sum_q G_nq e^{-(r_q-r)^2/2s^2} ii_l(r_q r/s^2)
 //         Bh_nl = r^-(l+1) / s^2 sum_q G_nq e^{-(r_q-r)^2/2s^2} (r_q ii_{l+1} - r ii_l)
-//       with ii_l(x) = e^-x i_l(x) and d/dx (x^-l i_l) = x^-l i_{l+1}.
+//       with ii_l(x) = e^-x i_l(x) and d/dx (x^-l i_l) = x^-l i_{l+1};
+//       polynomial, Laplace form (Eqs. poly-coefficients, poly-radial-derivative):
+//         B_nl = r^-l f_nl,  Bh_nl = r^-(l+1) (f'_nl - l f_nl / r)  (see stage_edges).
 //
 // k_density: persistent workgroups, each bound to one l-group and taking
 //   centers from a counter.  Accumulates c (and, for the Jacobian, D = sum
@@ -205,6 +207,7 @@ struct Tables {
     const double2 *bcp;    // GTO: [k][n][lc] = (betaC, -2 betaC a') of B_nl = sum_k betaC_nk e^{-a'_kl r^2}
     const double *aprime;  // GTO: [k][lc]
     const double *G, *rq;  // polynomial: [n][Q], [Q]
+    const double *WN, *B0; // polynomial, Laplace form: [n][i][4] Chebyshev coefficients (stage_edges); B_n0(0) [n]
     const double *Nt;      // [ldN][ldN] N_lm (2m-1)!! / (l-m)!, for sh_col_y
     const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_edges
 };
@@ -215,7 +218,8 @@ __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lg
     const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
     size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
     if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
-    else d += even(n * P.Q) + even((size_t)P.Q);
+    else if (P.rbf == 1) d += even(n * P.Q) + even((size_t)P.Q);
+    else d += 4 * n * n + even(n);
     return d;
 }
 
@@ -228,14 +232,15 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     double *Kl = cv.take(16);
     double *Ntl = cv.take((size_t)ldN * ldN);
     double *gc = cv.take(4 * (size_t)grad_pairs(lmax));
-    const bool poly = P.rbf != 0;
+    const int rbf = P.rbf;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    const size_t szA = poly ? (size_t)n * P.Q : 2 * (size_t)lgc * n * n; // (betaC, betaCa) pairs | G
-    const size_t szB = poly ? (size_t)P.Q : (size_t)lgc * n;              // aprime | rq
+    // (betaC, betaCa) pairs | G | WN, then aprime | rq | B0
+    const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n : (rbf == 1 ? (size_t)n * P.Q : 4 * (size_t)n * n);
+    const size_t szB = rbf == 0 ? (size_t)lgc * n : (rbf == 1 ? (size_t)P.Q : (size_t)n);
     double *A = cv.take(szA), *B = cv.take(szB);
     for (int k = tid; k < ldN * ldN; k += bs) Ntl[k] = P.Nt[k];
     for (int k = tid; k < 4 * grad_pairs(lmax); k += bs) gc[k] = P.gcoef[k];
-    if (!poly) {
+    if (rbf == 0) {
         // global [l][n][k] -> LDS [k][n][lc]; global [l][k] -> LDS [k][lc]
         const size_t o = (size_t)lg0 * n * n;
         for (int s = tid; s < (int)(szA / 2); s += bs) {
@@ -248,23 +253,30 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
             const int lc = s / n, k = s - lc * n;
             B[k * lgc + lc] = P.aprime[(size_t)lg0 * n + s];
         }
-    } else {
+    } else if (rbf == 1) {
         for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
         for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
+    } else {
+        // a neighbour at distance 0 adds the on-site term: B_n0 S_00 = c0_n
+        for (int k = tid; k < (int)szA; k += bs) A[k] = P.WN[k];
+        for (int k = tid; k < (int)szB; k += bs) B[k] = P.c0[k] * sqrt(4.0 * M_PI);
     }
     T.Kl = Kl;
     T.Nt = Ntl;
     T.gcoef = (const double2 *)gc;
     T.bcp = (const double2 *)A;
     T.G = A;
+    T.WN = A;
     T.aprime = B;
     T.rq = B;
+    T.B0 = B;
 }
 
 // X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
-// Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place)
+// Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place);
+// Laplace form: the four l-independent sums per n, 4 n
 __host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int lgc, int lg1) {
-    return P.rbf ? (size_t)P.Q * (lg1 + 1) : (size_t)P.n * lgc;
+    return P.rbf == 0 ? (size_t)P.n * lgc : (P.rbf == 1 ? (size_t)P.Q * (lg1 + 1) : 4 * (size_t)P.n);
 }
 
 // Synchronisation inside one wave: LDS writes become visible to the other
@@ -292,7 +304,8 @@ __device__ __forceinline__ void lds_barrier() {
 //       e es + c cs + (lm - lmY0) ls; component 0 = S, 1..3 = dS/dx_d (GRAD).
 //       Degrees from lgY0 = lg0 - 1 (GRAD and lg0 > 0) or lg0 are stored.
 //   BB[e][n][lc] = K (B_nl, Bh_nl), K = K_l if scaleK else 1, stored at precision BT
-//   X: GTO exponentials [e][k][lc], or the polynomial table [e][q][0..lg1]
+//   X: GTO exponentials [e][k][lc], the polynomial table [e][q][0..lg1], or
+//      the Laplace form's sums [e][n][j]
 // Phase 1 runs the harmonic columns (edge, m), then the radial scratch;
 // phase 2 the gradients, then the radial factors.  Each gradient component
 // is at most two degree l-1 harmonics: with H_l^m = (x + iy)^m Q_l^m (so
@@ -317,9 +330,7 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
     const int n = NT ? NT : P.n, ldN = (LWT ? LWT - 1 : P.lmax) + 2, lgc = lg1 - lg0, nlc = n * lgc;
     const int lgY0 = (GRAD && lg0 > 0) ? lg0 - 1 : lg0;
     const float inv_lg1 = 1.0f / (float)lg1, inv_nlc = 1.0f / (float)nlc, inv_lgc = 1.0f / (float)lgc;
-    const bool poly = P.rbf != 0;
-    const int Q = P.Q, tw = lg1 + 1;
-    const float inv_Q = 1.0f / (float)Q;
+    const int rbf = P.rbf, Q = P.Q, tw = lg1 + 1;
     // phase 1: harmonic columns (edge, m), then the radial scratch (two
     // independent exponentials per lane trip)
     for (int it = lane; it < nb * lg1; it += 64) {
@@ -327,7 +338,7 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
         const double *g = geo + 4 * e;
         sh_col_y(m, m > lgY0 ? m : lgY0, lg1, g[0], g[1], g[2], T.Nt, ldN, YY + e * yl.es, yl.ls, yl.lmY0);
     }
-    if (!poly) {
+    if (rbf == 0) {
         const int nx = nb * nlc;
         for (int it = lane; it < nx; it += 128) {
             const int i2 = it + 64 < nx ? it + 64 : it;
@@ -338,11 +349,30 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
             X[i2] = v2;
         }
     } else {
-        for (int it = lane; it < nb * Q; it += 64) {
-            const int e = qdiv(it, inv_Q), q = it - e * Q;
-            const double r = geo[4 * e + 3], rq = T.rq[q];
-            const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
-            bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
+        // polynomial: the quadrature table [e][q][0..lg1] (rbf 1), or the Laplace form's sums (rbf 2)
+        // Q_j(u) = sum_k w_j(k) WN_nk u^(k-1), u = r_cut - r, at [e][n][j] from their Chebyshev series
+        // in t = 2u/r_cut - 1 (Clenshaw's recurrence).  One loop serves both: a separate loop for
+        // the Laplace form costs every kernel that inlines this staging two more registers.
+        const int per = rbf == 1 ? Q : 4 * n;
+        const float inv_per = 1.0f / (float)per;
+        for (int it = lane; it < nb * per; it += 64) {
+            const int e = qdiv(it, inv_per), q = it - e * per;
+            const double r = geo[4 * e + 3];
+            if (rbf == 1) {
+                const double rq = T.rq[q];
+                const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
+                bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
+            } else {
+                const double tt = (P.rc - r) * P.inv_rc2 - 1.0, t2 = tt + tt;
+                const double *ch = T.WN + (size_t)(q >> 2) * n * 4 + (q & 3);
+                double b1 = 0.0, b2 = 0.0;
+                for (int i = n - 1; i >= 1; --i) {
+                    const double nb1 = t2 * b1 - b2 + ch[4 * i];
+                    b2 = b1;
+                    b1 = nb1;
+                }
+                X[it] = tt * b1 - b2 + ch[0];
+            }
         }
     }
     wave_sync();
@@ -383,7 +413,7 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
         }
     }
     const int nd = nb * nlc;
-    if (!poly) {
+    if (rbf == 0) {
         for (int it = lane; it < nd; it += 128) {
             const int i2 = it + 64 < nd ? it + 64 : it;
             const int e1 = qdiv(it, inv_nlc), t1 = it - e1 * nlc, l1 = t1 - qdiv(t1, inv_lgc) * lgc;
@@ -403,6 +433,37 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
             const double K1 = scaleK ? T.Kl[lg0 + l1] : 1.0, K2 = scaleK ? T.Kl[lg0 + l2] : 1.0;
             BB[it] = Pair<BT>::make(K1 * b1, K1 * h1);
             BB[i2] = Pair<BT>::make(K2 * b2, K2 * h2);
+        }
+    } else if (rbf == 2) {
+        // Laplace form, u = r_cut - r, k = 1..n, f_nl as in Eq. (poly-coefficients) and f'_nl as in Eq.
+        // (poly-radial-derivative), regrouped over the l-independent sums Q_j = sum_k w_j(k) WN_nk u^(k-1)
+        // (phase 1) with w = 1, k+2, (k+1)(k+2), k(k+1)(k+2), so that no term divides by u:
+        //   f  = u^3 (1 - l(l+1) s^2/(2r^2)) Q_0 - s^2 u^2/r Q_1 + s^2 u/2 Q_2
+        //   f' = l(l+1) s^2 u^3/r^3 Q_0 + u^2 ((l(l+1)+2) s^2/(2r^2) - 1) Q_1 + s^2 u/r Q_2 - s^2/2 Q_3
+        // s2, hs2 and inv_rc2 come in as kernel arguments: computed here, the
+        // compiler hoists them into vector registers held through the kernel
+        const double s2 = P.s2, hs2 = P.hs2;
+        for (int it = lane; it < nd; it += 64) {
+            const int e = qdiv(it, inv_nlc), t = it - e * nlc, a = qdiv(t, inv_lgc), l = lg0 + t - a * lgc;
+            const double r = geo[4 * e + 3];
+            double b, bh;
+            if (r == 0.0) {
+                b = (l == 0) ? T.B0[a] : 0.0;
+                bh = 0.0;
+            } else {
+                const double u = P.rc - r, *qs = X + 4 * ((size_t)e * n + a);
+                const double q0 = qs[0], q1 = qs[1], q2 = qs[2], q3 = qs[3];
+                const double ir = 1.0 / r, ll = (double)(l * (l + 1)), u2 = u * u, h = s2 * ir * ir;
+                const double f = u2 * u * (1.0 - 0.5 * ll * h) * q0 - s2 * u2 * ir * q1 + hs2 * u * q2;
+                const double fp = ll * h * u2 * u * ir * q0 + u2 * (0.5 * (ll + 2.0) * h - 1.0) * q1 +
+                                  s2 * u * ir * q2 - hs2 * q3;
+                double rl = 1.0;
+                for (int k = 0; k < l; ++k) rl *= ir;
+                b = rl * f;
+                bh = rl * ir * (fp - (double)l * f * ir);
+            }
+            const double K = scaleK ? T.Kl[l] : 1.0;
+            BB[it] = Pair<BT>::make(K * b, K * bh);
         }
     } else {
         for (int it = lane; it < nd; it += 64) {

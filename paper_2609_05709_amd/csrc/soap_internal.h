@@ -14,14 +14,17 @@ constexpr int MAX_DEGREE = 2048;
 
 // Everything the descriptor kernels need about the basis; passed by value.
 struct Params {
-    int S, n, lmax, L, rbf, Q; // L = (lmax+1)^2, rbf 0 = GTO, 1 = polynomial
+    int S, n, lmax, L, rbf, Q; // L = (lmax+1)^2, rbf 0 = GTO, 1 = polynomial, 2 = polynomial (Laplace form)
     int F, Fe, nq_full;        // features, edge features, (mu,nu,n,n') combinations
     double sigma, inv_s2;      // 1 / sigma^2
+    double rc, inv_rc2;        // cutoff radius, 2 / rc
+    double s2, hs2;            // sigma^2, sigma^2 / 2
     const double *betaC;       // GTO [l][n][k]
     const double *betaCa;      // GTO [l][n][k]
     const double *aprime;      // GTO [l][k]
     const double *G;           // polynomial [n][Q], includes 4 pi
     const double *rq;          // polynomial [Q]
+    const double *WN;          // polynomial, Laplace form [n][i][4]: Chebyshev series of Q_n0..Q_n3 on [0, rc]
     const double *c0;          // on-site term [n]
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)

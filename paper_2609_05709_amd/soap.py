@@ -13,7 +13,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsoap.so")
 
 SOAP_OK, SOAP_EINVAL, SOAP_ESPECIES, SOAP_ENOMEM, SOAP_EHIP, SOAP_ECAPACITY, SOAP_ESTATE = 0, -1, -2, -3, -4, -5, -6
-SOAP_RBF_GTO, SOAP_RBF_POLYNOMIAL = 0, 1
+SOAP_RBF_GTO, SOAP_RBF_POLYNOMIAL, SOAP_RBF_POLYNOMIAL_LAPLACE = 0, 1, 2
+RBF_CODES = {"gto": SOAP_RBF_GTO, "polynomial": SOAP_RBF_POLYNOMIAL,
+             "polynomial-laplace": SOAP_RBF_POLYNOMIAL_LAPLACE}
 SOAP_FP32, SOAP_FP64 = 0, 1
 SOAP_AVERAGE_INNER, SOAP_AVERAGE_OUTER = 1, 2
 MAX_DEGREE = 2048
@@ -97,7 +99,7 @@ def _stream():
 
 class Soap:
     """One library context: species, r_cut, n_max, l_max, sigma, rbf
-    ("gto" | "polynomial"), dtype ("float32" | "float64")."""
+    ("gto" | "polynomial" | "polynomial-laplace"), dtype ("float32" | "float64")."""
 
     def __init__(self, species, r_cut, n_max, l_max, sigma, rbf="gto", dtype="float32", quad_n=None):
         import numpy as np
@@ -107,12 +109,14 @@ class Soap:
             raise RuntimeError("no HIP device available")
         self.species = sorted(int(z) for z in species)
         self.r_cut, self.n_max, self.l_max, self.sigma = float(r_cut), int(n_max), int(l_max), float(sigma)
+        if rbf not in RBF_CODES:
+            raise ValueError(f"unknown rbf {rbf!r}; expected one of {sorted(RBF_CODES)}")
         self.rbf = rbf
         self.dtype = torch.float64 if dtype in ("float64", torch.float64) else torch.float32
         z = np.ascontiguousarray(self.species, dtype=np.int32)
         h = ctypes.c_void_p()
         code = self._L.soap_create(z.ctypes.data, len(z), self.r_cut, self.n_max, self.l_max, self.sigma,
-                                   SOAP_RBF_GTO if rbf == "gto" else SOAP_RBF_POLYNOMIAL, ctypes.byref(h))
+                                   RBF_CODES[rbf], ctypes.byref(h))
         if code != SOAP_OK:
             raise SoapError(code, "soap_create: " + self._L.soap_last_error(None).decode())
         self._h = h

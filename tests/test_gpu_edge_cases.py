@@ -8,6 +8,8 @@ from tests.parity import TOL, check_rows, gpu_run, jacobian_errors, row_errors
 
 pytestmark = pytest.mark.gpu
 
+RBFS = ["gto", "polynomial", "polynomial-laplace"]
+
 
 def _wl(species=(1, 8), rbf="gto", r_cut=5.0, sigma=0.5, n_max=4, l_max=4):
     return workloads.Workload("edge", tuple(species), rbf, r_cut, sigma, n_max, l_max, True, ("none",))
@@ -28,7 +30,7 @@ def _compare(wl, st, dtype, centers=None):
     return g, ref
 
 
-@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+@pytest.mark.parametrize("rbf", RBFS)
 def test_isolated_atoms_and_single_atom(rbf):
     wl = _wl(rbf=rbf)
     _compare(wl, _st([[0, 0, 0], [20, 0, 0], [0, 30, 0]], [1, 8, 1]), "float32")
@@ -36,7 +38,7 @@ def test_isolated_atoms_and_single_atom(rbf):
     assert g["E"] == 0
 
 
-@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+@pytest.mark.parametrize("rbf", RBFS)
 def test_coincident_atoms(rbf):
     wl = _wl(rbf=rbf)
     pos = [[0, 0, 0], [0, 0, 0], [1.1, 0.3, -0.4], [1.1, 0.3, -0.4], [-0.9, 1.2, 0.2]]
@@ -50,11 +52,22 @@ def test_species_absent_from_structure_and_center_subset():
 
 
 @pytest.mark.parametrize("nl", [(1, 0), (1, 5), (6, 0)])
-@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+@pytest.mark.parametrize("rbf", RBFS)
 def test_minimal_basis(nl, rbf):
     wl = _wl(rbf=rbf, n_max=nl[0], l_max=nl[1])
     st = workloads.random_small(25, 11, 3.0, species=(1, 8))
     _compare(wl, st, "float64")
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_laplace_form_near_the_cutoff(dtype):
+    """The Laplace form's terms in 1/(r_cut - r) cancel against powers of
+    r_cut - r; neighbours just inside r_cut stay finite and match the oracle."""
+    wl = _wl(rbf="polynomial-laplace", r_cut=4.0)
+    d = np.float32(4.0) * np.float32(1 - 2e-7)
+    pos = [[0, 0, 0], [d, 0, 0], [0, 0, 3.9999], [1.2, 0.4, 0.1]]
+    g, _ = _compare(wl, _st(pos, [8, 1, 1, 8]), dtype)
+    assert np.all(np.isfinite(g["desc"]))
 
 
 def test_neighbors_at_exact_cutoff():

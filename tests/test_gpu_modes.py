@@ -70,7 +70,7 @@ def test_cc_water1000_sampled(dtype):
     check_cc(wl, wl.structure(), dtype, sample=sorted(rng.choice(3000, size=60, replace=False).tolist()))
 
 
-@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+@pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
 @pytest.mark.parametrize("nl", [(1, 0), (6, 9), (12, 3)])
 def test_cc_small_bases(rbf, nl):
     wl = _wl(species=(1, 6, 8), rbf=rbf, n_max=nl[0], l_max=nl[1])

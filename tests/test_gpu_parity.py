@@ -71,7 +71,17 @@ def test_chno4096_poly_n10l10(dtype):
     full_check(workloads.CHNO4096, dtype, sample=32, seed=3)
 
 
-@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_water64_polynomial_laplace_full(dtype):
+    full_check(workloads.WATER64.with_basis(4, 4, "polynomial-laplace"), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_water1000_polynomial_laplace_n8l6(dtype):
+    full_check(workloads.WATER1000.with_basis(8, 6, "polynomial-laplace"), dtype, sample=24, seed=5)
+
+
+@pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
 @pytest.mark.parametrize("nl", [(2, 2), (2, 12), (12, 2), (12, 12), (6, 8)])
 def test_hyperparameter_grid_points(rbf, nl):
     wl = workloads.WATER1000.with_basis(nl[0], nl[1], rbf)

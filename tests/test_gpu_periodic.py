@@ -88,7 +88,7 @@ def check(wl, pos, Z, cell, pbc, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["float32", "float64"])
-@pytest.mark.parametrize("rbf", ["gto", "polynomial"])
+@pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
 def test_periodic_small_triclinic_cell(rbf, dtype):
     """A cell smaller than 2 r_cut: several images of each atom and of the
     center itself are neighbours."""
