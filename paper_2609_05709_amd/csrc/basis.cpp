@@ -22,38 +22,104 @@ typedef __float128 q128;
 
 const q128 PI_Q = M_PIq;
 
+// Unevaluated sum hi + lo of two __float128 values (about 226 bits), for the
+// polynomial overlap matrix, whose condition number reaches 5.6e25 at
+// n_max = 16: its inverse square root in 113 bits would keep ~9 digits.
+// Error-free transformations: Knuth's two-sum and the fused multiply-add
+// product; division and square root by one Newton correction.
+struct qq {
+    q128 hi = 0, lo = 0;
+    qq() = default;
+    qq(q128 h) : hi(h), lo(0) {}
+    qq(int v) : hi((q128)v), lo(0) {}
+    qq(q128 h, q128 l) : hi(h), lo(l) {}
+    explicit operator q128() const { return hi + lo; }
+};
+inline qq fast_sum(q128 a, q128 b) { // |a| >= |b|
+    q128 s = a + b;
+    return qq(s, b - (s - a));
+}
+inline qq two_sum(q128 a, q128 b) {
+    q128 s = a + b, bb = s - a;
+    return qq(s, (a - (s - bb)) + (b - bb));
+}
+inline qq operator+(const qq &a, const qq &b) {
+    qq s = two_sum(a.hi, b.hi), t = two_sum(a.lo, b.lo);
+    s.lo += t.hi;
+    s = fast_sum(s.hi, s.lo);
+    s.lo += t.lo;
+    return fast_sum(s.hi, s.lo);
+}
+inline qq operator-(const qq &a) { return qq(-a.hi, -a.lo); }
+inline qq operator-(const qq &a, const qq &b) { return a + (-b); }
+inline qq operator*(const qq &a, const qq &b) {
+    q128 p = a.hi * b.hi, e = fmaq(a.hi, b.hi, -p);
+    e += a.hi * b.lo + a.lo * b.hi;
+    return fast_sum(p, e);
+}
+inline qq operator/(const qq &a, const qq &b) {
+    q128 q1 = a.hi / b.hi;
+    qq r = a - b * qq(q1);
+    q128 q2 = r.hi / b.hi;
+    r = r - b * qq(q2);
+    q128 q3 = r.hi / b.hi;
+    qq q = fast_sum(q1, q2);
+    return q + qq(q3);
+}
+inline qq &operator+=(qq &a, const qq &b) { return a = a + b; }
+inline bool operator>=(const qq &a, const qq &b) { return a.hi > b.hi || (a.hi == b.hi && a.lo >= b.lo); }
+inline bool operator<=(const qq &a, const qq &b) { return b >= a; }
+inline bool operator>(const qq &a, const qq &b) { return !(b >= a); }
+inline bool operator==(const qq &a, int b) { return a.hi == (q128)b && a.lo == 0; }
+inline qq qsqrt(const qq &a) {
+    if (!(a.hi > 0)) return qq(0);
+    q128 x = sqrtq(a.hi);
+    qq r = a - qq(x) * qq(x);
+    return qq(x) + qq(r.hi / (2 * x));
+}
+inline qq qabs(const qq &a) { return a.hi < 0 ? -a : a; }
+inline q128 qsqrt(q128 a) { return sqrtq(a); }
+inline q128 qabs(q128 a) { return fabsq(a); }
+
+// off-diagonal / diagonal squared-norm ratio at which the Jacobi sweeps stop
+template <typename T> constexpr double jacobi_tol();
+template <> constexpr double jacobi_tol<q128>() { return 1e-66; }
+template <> constexpr double jacobi_tol<qq>() { return 1e-130; }
+
 // Cyclic Jacobi eigen-decomposition of a symmetric n x n matrix A (row major,
 // destroyed).  V receives the eigenvectors as columns, w the eigenvalues.
-bool jacobi_eigen(int n, std::vector<q128> &A, std::vector<q128> &V, std::vector<q128> &w) {
-    V.assign((size_t)n * n, 0);
-    for (int i = 0; i < n; ++i) V[(size_t)i * n + i] = 1;
+template <typename T>
+bool jacobi_eigen(int n, std::vector<T> &A, std::vector<T> &V, std::vector<T> &w) {
+    V.assign((size_t)n * n, T(0));
+    for (int i = 0; i < n; ++i) V[(size_t)i * n + i] = T(1);
+    const T tol = T((q128)jacobi_tol<T>());
     for (int sweep = 0; sweep < 200; ++sweep) {
-        q128 off = 0, diag = 0;
+        T off = T(0), diag = T(0);
         for (int p = 0; p < n; ++p) {
             diag += A[(size_t)p * n + p] * A[(size_t)p * n + p];
             for (int q = p + 1; q < n; ++q) off += A[(size_t)p * n + q] * A[(size_t)p * n + q];
         }
-        if (off <= diag * (q128)1e-66Q) break;
+        if (off <= diag * tol) break;
         for (int p = 0; p < n; ++p)
             for (int q = p + 1; q < n; ++q) {
-                q128 apq = A[(size_t)p * n + q];
+                T apq = A[(size_t)p * n + q];
                 if (apq == 0) continue;
-                q128 app = A[(size_t)p * n + p], aqq = A[(size_t)q * n + q];
-                q128 theta = (aqq - app) / (2 * apq);
-                q128 t = (theta >= 0 ? 1 : -1) / (fabsq(theta) + sqrtq(theta * theta + 1));
-                q128 c = 1 / sqrtq(t * t + 1), s = t * c;
+                T app = A[(size_t)p * n + p], aqq = A[(size_t)q * n + q];
+                T theta = (aqq - app) / (T(2) * apq);
+                T t = T(theta >= T(0) ? 1 : -1) / (qabs(theta) + qsqrt(theta * theta + T(1)));
+                T c = T(1) / qsqrt(t * t + T(1)), s = t * c;
                 for (int k = 0; k < n; ++k) { // columns p, q
-                    q128 akp = A[(size_t)k * n + p], akq = A[(size_t)k * n + q];
+                    T akp = A[(size_t)k * n + p], akq = A[(size_t)k * n + q];
                     A[(size_t)k * n + p] = c * akp - s * akq;
                     A[(size_t)k * n + q] = s * akp + c * akq;
                 }
                 for (int k = 0; k < n; ++k) { // rows p, q
-                    q128 apk = A[(size_t)p * n + k], aqk = A[(size_t)q * n + k];
+                    T apk = A[(size_t)p * n + k], aqk = A[(size_t)q * n + k];
                     A[(size_t)p * n + k] = c * apk - s * aqk;
                     A[(size_t)q * n + k] = s * apk + c * aqk;
                 }
                 for (int k = 0; k < n; ++k) {
-                    q128 vkp = V[(size_t)k * n + p], vkq = V[(size_t)k * n + q];
+                    T vkp = V[(size_t)k * n + p], vkq = V[(size_t)k * n + q];
                     V[(size_t)k * n + p] = c * vkp - s * vkq;
                     V[(size_t)k * n + q] = s * vkp + c * vkq;
                 }
@@ -65,16 +131,17 @@ bool jacobi_eigen(int n, std::vector<q128> &A, std::vector<q128> &V, std::vector
 }
 
 // Principal inverse square root of a symmetric positive-definite matrix.
-bool inv_sqrt_spd(int n, const std::vector<q128> &S, std::vector<q128> &X) {
-    std::vector<q128> A = S, V, w;
+template <typename T>
+bool inv_sqrt_spd(int n, const std::vector<T> &S, std::vector<T> &X) {
+    std::vector<T> A = S, V, w;
     jacobi_eigen(n, A, V, w);
     for (int i = 0; i < n; ++i)
-        if (!(w[i] > 0)) return false;
-    X.assign((size_t)n * n, 0);
+        if (!(w[i] > T(0))) return false;
+    X.assign((size_t)n * n, T(0));
     for (int i = 0; i < n; ++i)
         for (int j = 0; j < n; ++j) {
-            q128 acc = 0;
-            for (int k = 0; k < n; ++k) acc += V[(size_t)i * n + k] * V[(size_t)j * n + k] / sqrtq(w[k]);
+            T acc = T(0);
+            for (int k = 0; k < n; ++k) acc += V[(size_t)i * n + k] * V[(size_t)j * n + k] / qsqrt(w[k]);
             X[(size_t)i * n + j] = acc;
         }
     return true;
@@ -143,8 +210,10 @@ extern "C" int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, 
 
 // Norms N_k of (r_cut - r)^{k+2} (Eq. poly-norm) and the Loewdin weights
 // W = S^{-1/2} of their overlap matrix (Eq. poly-overlap), k = 1..n.
+// The overlap matrix and its inverse square root are formed in double
+// __float128 (qq), then W is rounded to __float128.
 static bool poly_weights(q128 rc, int n, std::vector<q128> &N, std::vector<q128> &W, char *err, int errlen) {
-    std::vector<q128> S((size_t)n * n);
+    std::vector<qq> S((size_t)n * n), Wq;
     N.assign(n, 0);
     for (int a = 0; a < n; ++a) {
         int k = a + 1;
@@ -153,12 +222,14 @@ static bool poly_weights(q128 rc, int n, std::vector<q128> &N, std::vector<q128>
     for (int a = 0; a < n; ++a)
         for (int b = 0; b < n; ++b) {
             int k = a + 1, kp = b + 1;
-            S[(size_t)a * n + b] = sqrtq((q128)((5 + 2 * k) * (5 + 2 * kp))) / (q128)(5 + k + kp);
+            S[(size_t)a * n + b] = qsqrt(qq((5 + 2 * k) * (5 + 2 * kp))) / qq(5 + k + kp);
         }
-    if (!inv_sqrt_spd(n, S, W)) {
+    if (!inv_sqrt_spd(n, S, Wq)) {
         set_err(err, errlen, "polynomial overlap matrix is not positive definite");
         return false;
     }
+    W.resize(Wq.size());
+    for (size_t i = 0; i < Wq.size(); ++i) W[i] = (q128)Wq[i];
     return true;
 }
 
@@ -195,25 +266,27 @@ extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n
         t[i] = x;
         wt[i] = 2 / ((1 - x * x) * dp * dp);
     }
-    // G[n][q] = 4 pi w_q r_q^2 g_n(r_q), g_n of Eq. (poly-basis) summed in quad
+    // g_n(r_q) of Eq. (poly-basis), summed in quad; then G[n][q] = 4 pi w_q r_q^2 g_n(r_q)
     const q128 fourpi = 4 * PI_Q;
+    std::vector<q128> g((size_t)n * Q), phi(n);
     for (int q = 0; q < Q; ++q) {
-        q128 r = rc * (t[q] + 1) / 2, w = rc * wt[q] / 2;
+        const q128 r = rc * (t[q] + 1) / 2, w = rc * wt[q] / 2, u = rc - r;
+        q128 up = u * u * u; // (r_cut - r)^{k+2}, k = 1..n
+        for (int b = 0; b < n; ++b, up *= u) phi[b] = up / N[b];
         rq_out[q] = (double)r;
         for (int a = 0; a < n; ++a) {
-            q128 g = 0;
-            for (int b = 0; b < n; ++b) g += W[(size_t)a * n + b] * powq(rc - r, (q128)(b + 3)) / N[b];
-            G[(size_t)a * Q + q] = (double)(fourpi * w * r * r * g);
+            q128 acc = 0;
+            for (int b = 0; b < n; ++b) acc += W[(size_t)a * n + b] * phi[b];
+            g[(size_t)a * Q + q] = acc;
+            G[(size_t)a * Q + q] = (double)(fourpi * w * r * r * acc);
         }
     }
     // on-site term: sqrt(4 pi) sum_q w_q r_q^2 g_n(r_q) exp(-r_q^2 / 2 sigma^2)
     for (int a = 0; a < n; ++a) {
         q128 acc = 0;
         for (int q = 0; q < Q; ++q) {
-            q128 r = rc * (t[q] + 1) / 2, w = rc * wt[q] / 2;
-            q128 g = 0;
-            for (int b = 0; b < n; ++b) g += W[(size_t)a * n + b] * powq(rc - r, (q128)(b + 3)) / N[b];
-            acc += w * r * r * g * expq(-r * r / (2 * s2));
+            const q128 r = rc * (t[q] + 1) / 2, w = rc * wt[q] / 2;
+            acc += w * r * r * g[(size_t)a * Q + q] * expq(-r * r / (2 * s2));
         }
         c0[a] = (double)(sqrtq(fourpi) * acc);
     }
