@@ -34,7 +34,7 @@ def build(force: bool = False) -> str:
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-std=gnu11", "-fopenmp", "-ffp-contract=off",
-                               "-o", tmp, _SRC, "-lm"])
+                               "-o", tmp, _SRC, "-lquadmath", "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 

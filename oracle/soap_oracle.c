@@ -7,7 +7,8 @@
  *
  * Precision: float64 throughout, long double (x87, 64-bit mantissa) for the
  * Loewdin-weighted radial sums and the monomial evaluation of the harmonics,
- * where cancellation would otherwise cost digits.  Compiled with
+ * where cancellation would otherwise cost digits, and __float128 for the
+ * Laplace form's monomial sums, which cancel the most.  Compiled with
  * -ffp-contract=off so the cutoff test below is evaluated exactly as written.
  *
  * Paper passages followed (Sec. = section of the paper):
@@ -23,17 +24,21 @@
  *    Gauss-Legendre rule of Sec. 3.1; gradient by the chain rule
  *    Eq. (poly-cartesian-derivative) with df/dr from differentiating the same
  *    quadrature under the integral sign (i_l' = i_{l+1} + (l/x) i_l).
+ *  - polynomial coefficients, Laplace form: Sec. 2.3, Eqs. (poly-laplace),
+ *    (poly-coefficients), (poly-radial-derivative), the same chain rule.
  *  - neighbour set and the on-site term: Sec. 3.1 (zero-length edges are
  *    dropped and the position-independent l = 0 self term is added).
  *  - feature order: Sec. 3.1, species pair (mu <= nu), then n, then n'
  *    (n' >= n on the diagonal), then l innermost.
  */
 #include <math.h>
+#include <quadmath.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 typedef long double ld;
+typedef __float128 qd;
 
 typedef struct {
     int32_t S, n, lmax, rbf; /* rbf: 0 = GTO, 1 = polynomial (quadrature), 2 = polynomial (Laplace) */
@@ -311,22 +316,27 @@ static void radial(const oracle_params *P, ld r, ld *R, ld *dR) {
            f'_nl = (2 pi)^{3/2} s^3 sum_k W_nk/N_k (rc-r)^{k+1}
                   [-(k+2) + l(l+1)s^2(rc-r)/r^3 + (k+2)(l(l+1)+2)s^2/(2r^2)
                    + (k+1)(k+2)s^2/(r(rc-r)) - k(k+1)(k+2)s^2/(2(rc-r)^2)] */
-        ld pref = powl(2.0L * 3.14159265358979323846264338327950288L, 1.5L) * s2 * (ld)P->sigma;
-        ld rc = (ld)P->rc, u = rc - r;
+        /* The sums over k cancel heavily: W_nk/N_k grow large with alternating
+           signs, and at n_max = 16 long double keeps only ~9 digits of f.  They
+           run in __float128, W_nk/N_k taken from its (hi, lo) pair. */
+        const qd pi = 3.14159265358979323846264338327950288Q, sg = (qd)P->sigma, qs2 = sg * sg;
+        const qd pref = 2 * pi * sqrtq(2 * pi) * qs2 * sg;
+        const qd rq = (qd)r, u = (qd)P->rc - rq;
         for (int a = 0; a < n; ++a)
             for (int l = 0; l <= lmax; ++l) {
-                ld ll = (ld)(l * (l + 1)), acc = 0, dacc = 0;
+                qd ll = (qd)(l * (l + 1)), acc = 0, dacc = 0;
                 for (int b = 0; b < n; ++b) {
-                    ld k = (ld)(b + 1), wn = LD(P->wn_hi[a * n + b], P->wn_lo[a * n + b]);
-                    ld br = 1.0L - ll * s2 / (2.0L * r * r) - (k + 2) * s2 / (r * u) +
-                            (k + 2) * (k + 1) * s2 / (2.0L * u * u);
-                    ld dbr = -(k + 2) + ll * s2 * u / (r * r * r) + (k + 2) * (ll + 2) * s2 / (2.0L * r * r) +
-                             (k + 1) * (k + 2) * s2 / (r * u) - k * (k + 1) * (k + 2) * s2 / (2.0L * u * u);
-                    acc += wn * powl(u, k + 2) * br;
-                    dacc += wn * powl(u, k + 1) * dbr;
+                    qd k = (qd)(b + 1), wn = (qd)P->wn_hi[a * n + b] + (qd)P->wn_lo[a * n + b];
+                    qd uk1 = 1; /* u^(k+1) */
+                    for (int e = 0; e < b + 2; ++e) uk1 *= u;
+                    qd br = 1 - ll * qs2 / (2 * rq * rq) - (k + 2) * qs2 / (rq * u) + (k + 2) * (k + 1) * qs2 / (2 * u * u);
+                    qd dbr = -(k + 2) + ll * qs2 * u / (rq * rq * rq) + (k + 2) * (ll + 2) * qs2 / (2 * rq * rq) +
+                             (k + 1) * (k + 2) * qs2 / (rq * u) - k * (k + 1) * (k + 2) * qs2 / (2 * u * u);
+                    acc += wn * uk1 * u * br;
+                    dacc += wn * uk1 * dbr;
                 }
-                R[a * (lmax + 1) + l] = pref * acc;
-                dR[a * (lmax + 1) + l] = pref * dacc;
+                R[a * (lmax + 1) + l] = (ld)(pref * acc);
+                dR[a * (lmax + 1) + l] = (ld)(pref * dacc);
             }
     } else {
         int Q = P->Q;

@@ -501,6 +501,48 @@ def test_poly_laplace_derivative_by_finite_differences(r):
     assert np.abs(fd - dR).max() < 1e-7 * np.abs(dR).max()
 
 
+@pytest.mark.parametrize("n_max", [6, 16])
+def test_poly_laplace_is_the_first_order_heat_kernel_form(n_max):
+    """The bracket of Eq. (poly-coefficients) regroups into the first-order
+    Gaussian-smoothing (heat-kernel) form of the basis function
+    g(r) = (2 pi)^{3/2} s^3 sum_k W_nk/N_k (r_cut - r)^{k+2}:
+        f_nl = g + s^2/2 (g'' + 2 g'/r - l(l+1) g / r^2),
+    and Eq. (poly-radial-derivative) is its r-derivative.  Checked with g and its
+    derivatives in 50 digits, up to n_max = 16, where the sums over k cancel the
+    most (W_nk/N_k large, alternating); a dropped or mis-signed bracket term, or
+    too little working precision, fails it."""
+    rc, s, lmax = 5.0, 0.5, 4
+    o = oracle.OracleSOAP((1, 8), rc, n_max, lmax, s, "polynomial-laplace")
+    N, W, _, _, _ = constants.poly_mp(rc, n_max, 2)
+    with mp.workdps(50):
+        pref = (2 * mp.pi) ** mp.mpf(1.5) * mp.mpf(s) ** 3
+        s2 = mp.mpf(s) ** 2
+        got_f, got_d, ref_f, ref_d = [], [], [], []
+        for r in (0.85, 1.6, 2.9, 4.4, 4.97):
+            R, dR = o.radial(r)[:2]
+            got_f.append(np.asarray(R).reshape(n_max, lmax + 1))
+            got_d.append(np.asarray(dR).reshape(n_max, lmax + 1))
+            rr = mp.mpf(r)
+            u = mp.mpf(rc) - rr
+            rf, rd = np.empty((n_max, lmax + 1)), np.empty((n_max, lmax + 1))
+            for a in range(n_max):
+                # d^j g / dr^j = (-1)^j d^j/du^j
+                g = [(-1) ** j * pref * mp.fsum(W[a, k - 1] / N[k - 1] * mp.ff(k + 2, j) * u ** (k + 2 - j)
+                                                for k in range(1, n_max + 1)) for j in range(4)]
+                for l in range(lmax + 1):
+                    ll = l * (l + 1)
+                    f = g[0] + s2 / 2 * (g[2] + 2 * g[1] / rr - ll * g[0] / rr ** 2)
+                    df = g[1] + s2 / 2 * (g[3] + 2 * g[2] / rr - 2 * g[1] / rr ** 2 - ll * g[1] / rr ** 2
+                                          + 2 * ll * g[0] / rr ** 3)
+                    rf[a, l], rd[a, l] = float(f), float(df)
+            ref_f.append(rf)
+            ref_d.append(rd)
+    for got, ref in ((got_f, ref_f), (got_d, ref_d)):
+        got, ref = np.array(got), np.array(ref)  # [r][n][l]
+        err = np.abs(got - ref).max(axis=0) / np.abs(ref).max(axis=0)
+        assert err.max() < 1e-14, err.max()
+
+
 def test_poly_laplace_onsite_equals_quadrature_onsite():
     """The center's own l = 0 term comes from the one-dimensional integral
     I_k0(0) in both polynomial forms."""
