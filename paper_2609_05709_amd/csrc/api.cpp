@@ -253,7 +253,7 @@ int upload_constants(soap_ctx *c) {
         if (soap_basis_poly(c->r_cut, n, c->sigma, c->Q, G.data(), rq.data(), c0.data(), msg, sizeof msg) != 0)
             return fail(c, SOAP_EINVAL, "%s", msg);
         if (c->rbf == SOAP_RBF_POLYNOMIAL_LAPLACE) {
-            WN.resize((size_t)n * n * 4);
+            WN.resize((size_t)n * (n + 3) * 4);
             if (soap_basis_poly_laplace(c->r_cut, n, c->sigma, WN.data(), msg, sizeof msg) != 0)
                 return fail(c, SOAP_EINVAL, "%s", msg);
         }

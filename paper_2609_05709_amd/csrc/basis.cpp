@@ -294,32 +294,32 @@ extern "C" int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n
 }
 
 extern "C" int soap_basis_poly_laplace(double r_cut, int n_max, double sigma, double *CH, char *err, int errlen) {
-    const int n = n_max;
+    const int n = n_max, M = n + 3; // P_0 has degree n + 2
     std::vector<q128> N, W;
     if (!poly_weights((q128)r_cut, n, N, W, err, errlen)) return -1;
     const q128 rc = r_cut, s = sigma, pref = powq(2 * PI_Q, (q128)1.5) * s * s * s;
-    // values of the four polynomials at the Chebyshev points t_p = cos(pi (p + 1/2) / n)
-    std::vector<q128> val((size_t)n * 4);
+    // P_j(u) = d^j/du^j sum_k WN_k u^{k+2} at the Chebyshev points t_p = cos(pi (p + 1/2) / M)
+    std::vector<q128> val((size_t)M * 4);
     for (int a = 0; a < n; ++a) {
-        for (int p = 0; p < n; ++p) {
-            const q128 t = cosq(PI_Q * ((q128)p + 0.5Q) / (q128)n), u = (t + 1) * rc / 2;
-            q128 q[4] = {0, 0, 0, 0}, up = 1;
+        for (int p = 0; p < M; ++p) {
+            const q128 t = cosq(PI_Q * ((q128)p + 0.5Q) / (q128)M), u = (t + 1) * rc / 2;
+            q128 P[4] = {0, 0, 0, 0}, up = 1; // up = u^{k-1}
             for (int k = 1; k <= n; ++k) {
                 const q128 v = pref * W[(size_t)a * n + k - 1] / N[k - 1] * up;
-                q[0] += v;
-                q[1] += (q128)(k + 2) * v;
-                q[2] += (q128)((k + 1) * (k + 2)) * v;
-                q[3] += (q128)(k * (k + 1) * (k + 2)) * v;
+                P[0] += v * u * u * u;
+                P[1] += (q128)(k + 2) * v * u * u;
+                P[2] += (q128)((k + 1) * (k + 2)) * v * u;
+                P[3] += (q128)(k * (k + 1) * (k + 2)) * v;
                 up *= u;
             }
-            for (int j = 0; j < 4; ++j) val[(size_t)p * 4 + j] = q[j];
+            for (int j = 0; j < 4; ++j) val[(size_t)p * 4 + j] = P[j];
         }
-        // c_i = (2 - [i = 0]) / n sum_p Q(t_p) T_i(t_p)
-        for (int i = 0; i < n; ++i)
+        // c_i = (2 - [i = 0]) / M sum_p P(t_p) T_i(t_p)
+        for (int i = 0; i < M; ++i)
             for (int j = 0; j < 4; ++j) {
                 q128 acc = 0;
-                for (int p = 0; p < n; ++p) acc += val[(size_t)p * 4 + j] * cosq(PI_Q * (q128)i * ((q128)p + 0.5Q) / (q128)n);
-                CH[((size_t)a * n + i) * 4 + j] = (double)(acc * (i == 0 ? 1 : 2) / (q128)n);
+                for (int p = 0; p < M; ++p) acc += val[(size_t)p * 4 + j] * cosq(PI_Q * (q128)i * ((q128)p + 0.5Q) / (q128)M);
+                CH[((size_t)a * M + i) * 4 + j] = (double)(acc * (i == 0 ? 1 : 2) / (q128)M);
             }
     }
     return 0;

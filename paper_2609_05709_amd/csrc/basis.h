@@ -23,14 +23,13 @@ int soap_basis_poly(double r_cut, int n_max, double sigma, int quad_n, double *G
 
 // Laplace form of the polynomial basis (Eqs. poly-coefficients,
 // poly-radial-derivative).  With u = r_cut - r and WN_nk = (2 pi)^{3/2}
-// sigma^3 W_nk / N_k (k = 1..n_max), the radial factors need four
-// polynomials in u of degree n_max - 1,
-//   Q_nj(u) = sum_k w_j(k) WN_nk u^{k-1},  w = 1, k+2, (k+1)(k+2), k(k+1)(k+2).
+// sigma^3 W_nk / N_k (k = 1..n_max), the radial factors need
+//   P_n0(u) = sum_k WN_nk u^{k+2}  and its u-derivatives P_n1, P_n2, P_n3.
 // Their monomial coefficients grow large with alternating signs as n_max
 // grows, so they are handed over as Chebyshev series on [0, r_cut]:
-//   Q_nj(u) = sum_{i < n_max} CH[n][i][j] T_i(2u / r_cut - 1),
-// from interpolation at the n_max Chebyshev points in 113-bit arithmetic
-// (exact for degree n_max - 1).  Returns 0 or -1.
+//   P_nj(u) = sum_{i < n_max + 3} CH[n][i][j] T_i(2u / r_cut - 1),
+// from interpolation at n_max + 3 Chebyshev points in 113-bit arithmetic
+// (exact for degree n_max + 2).  Returns 0 or -1.
 int soap_basis_poly_laplace(double r_cut, int n_max, double sigma, double *CH, char *err, int errlen);
 
 // Real solid-harmonic normalisation N[l][m], 0 <= m <= l, row stride l_max+1.

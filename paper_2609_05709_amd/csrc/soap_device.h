@@ -207,7 +207,7 @@ struct Tables {
     const double2 *bcp;    // GTO: [k][n][lc] = (betaC, -2 betaC a') of B_nl = sum_k betaC_nk e^{-a'_kl r^2}
     const double *aprime;  // GTO: [k][lc]
     const double *G, *rq;  // polynomial: [n][Q], [Q]
-    const double *WN, *B0; // polynomial, Laplace form: [n][i][4] Chebyshev coefficients (stage_edges); B_n0(0) [n]
+    const double *WN, *B0; // polynomial, Laplace form: [n][n+3][4] Chebyshev coefficients (stage_edges); B_n0(0) [n]
     const double *Nt;      // [ldN][ldN] N_lm (2m-1)!! / (l-m)!, for sh_col_y
     const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_edges
 };
@@ -219,7 +219,7 @@ __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lg
     size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
     if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
     else if (P.rbf == 1) d += even(n * P.Q) + even((size_t)P.Q);
-    else d += 4 * n * n + even(n);
+    else d += 4 * n * (n + 3) + even(n);
     return d;
 }
 
@@ -235,7 +235,7 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     const int rbf = P.rbf;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     // (betaC, betaCa) pairs | G | WN, then aprime | rq | B0
-    const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n : (rbf == 1 ? (size_t)n * P.Q : 4 * (size_t)n * n);
+    const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n : (rbf == 1 ? (size_t)n * P.Q : 4 * (size_t)n * (n + 3));
     const size_t szB = rbf == 0 ? (size_t)lgc * n : (rbf == 1 ? (size_t)P.Q : (size_t)n);
     double *A = cv.take(szA), *B = cv.take(szB);
     for (int k = tid; k < ldN * ldN; k += bs) Ntl[k] = P.Nt[k];
@@ -274,7 +274,7 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
 
 // X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
 // Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place);
-// Laplace form: the four l-independent sums per n, 4 n
+// Laplace form: the four l-independent values P_j per n, 4 n
 __host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int lgc, int lg1) {
     return P.rbf == 0 ? (size_t)P.n * lgc : (P.rbf == 1 ? (size_t)P.Q * (lg1 + 1) : 4 * (size_t)P.n);
 }
@@ -305,7 +305,7 @@ __device__ __forceinline__ void lds_barrier() {
 //       Degrees from lgY0 = lg0 - 1 (GRAD and lg0 > 0) or lg0 are stored.
 //   BB[e][n][lc] = K (B_nl, Bh_nl), K = K_l if scaleK else 1, stored at precision BT
 //   X: GTO exponentials [e][k][lc], the polynomial table [e][q][0..lg1], or
-//      the Laplace form's sums [e][n][j]
+//      the Laplace form's P_j [e][n][j]
 // Phase 1 runs the harmonic columns (edge, m), then the radial scratch;
 // phase 2 the gradients, then the radial factors.  Each gradient component
 // is at most two degree l-1 harmonics: with H_l^m = (x + iy)^m Q_l^m (so
@@ -349,10 +349,10 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
             X[i2] = v2;
         }
     } else {
-        // polynomial: the quadrature table [e][q][0..lg1] (rbf 1), or the Laplace form's sums (rbf 2)
-        // Q_j(u) = sum_k w_j(k) WN_nk u^(k-1), u = r_cut - r, at [e][n][j] from their Chebyshev series
-        // in t = 2u/r_cut - 1 (Clenshaw's recurrence).  One loop serves both: a separate loop for
-        // the Laplace form costs every kernel that inlines this staging two more registers.
+        // polynomial: the quadrature table [e][q][0..lg1] (rbf 1), or the Laplace form's (rbf 2)
+        // P_j(u) = d^j/du^j sum_k WN_nk u^(k+2), u = r_cut - r, at [e][n][j] from their Chebyshev
+        // series in t = 2u/r_cut - 1 (Clenshaw's recurrence).  One loop serves both: a separate loop
+        // for the Laplace form costs every kernel that inlines this staging two more registers.
         const int per = rbf == 1 ? Q : 4 * n;
         const float inv_per = 1.0f / (float)per;
         for (int it = lane; it < nb * per; it += 64) {
@@ -364,9 +364,9 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
                 bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
             } else {
                 const double tt = (P.rc - r) * P.inv_rc2 - 1.0, t2 = tt + tt;
-                const double *ch = T.WN + (size_t)(q >> 2) * n * 4 + (q & 3);
+                const double *ch = T.WN + (size_t)(q >> 2) * (n + 3) * 4 + (q & 3);
                 double b1 = 0.0, b2 = 0.0;
-                for (int i = n - 1; i >= 1; --i) {
+                for (int i = n + 2; i >= 1; --i) {
                     const double nb1 = t2 * b1 - b2 + ch[4 * i];
                     b2 = b1;
                     b1 = nb1;
@@ -435,11 +435,10 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
             BB[i2] = Pair<BT>::make(K2 * b2, K2 * h2);
         }
     } else if (rbf == 2) {
-        // Laplace form, u = r_cut - r, k = 1..n, f_nl as in Eq. (poly-coefficients) and f'_nl as in Eq.
-        // (poly-radial-derivative), regrouped over the l-independent sums Q_j = sum_k w_j(k) WN_nk u^(k-1)
-        // (phase 1) with w = 1, k+2, (k+1)(k+2), k(k+1)(k+2), so that no term divides by u:
-        //   f  = u^3 (1 - l(l+1) s^2/(2r^2)) Q_0 - s^2 u^2/r Q_1 + s^2 u/2 Q_2
-        //   f' = l(l+1) s^2 u^3/r^3 Q_0 + u^2 ((l(l+1)+2) s^2/(2r^2) - 1) Q_1 + s^2 u/r Q_2 - s^2/2 Q_3
+        // Laplace form, u = r_cut - r, k = 1..n: the bracket of Eq. (poly-coefficients) summed over k
+        // is f = P_0 (1 - l(l+1) h/2) - s^2/r P_1 + s^2/2 P_2 with h = s^2/r^2 and P_j = d^j/du^j
+        // sum_k WN_nk u^(k+2) (phase 1); Eq. (poly-radial-derivative) likewise is
+        // f' = l(l+1) h/r P_0 + ((l(l+1)+2) h/2 - 1) P_1 + s^2/r P_2 - s^2/2 P_3.
         // s2, hs2 and inv_rc2 come in as kernel arguments: computed here, the
         // compiler hoists them into vector registers held through the kernel
         const double s2 = P.s2, hs2 = P.hs2;
@@ -451,12 +450,11 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
                 b = (l == 0) ? T.B0[a] : 0.0;
                 bh = 0.0;
             } else {
-                const double u = P.rc - r, *qs = X + 4 * ((size_t)e * n + a);
-                const double q0 = qs[0], q1 = qs[1], q2 = qs[2], q3 = qs[3];
-                const double ir = 1.0 / r, ll = (double)(l * (l + 1)), u2 = u * u, h = s2 * ir * ir;
-                const double f = u2 * u * (1.0 - 0.5 * ll * h) * q0 - s2 * u2 * ir * q1 + hs2 * u * q2;
-                const double fp = ll * h * u2 * u * ir * q0 + u2 * (0.5 * (ll + 2.0) * h - 1.0) * q1 +
-                                  s2 * u * ir * q2 - hs2 * q3;
+                const double *ps = X + 4 * ((size_t)e * n + a);
+                const double p0 = ps[0], p1 = ps[1], p2 = ps[2], p3 = ps[3];
+                const double ir = 1.0 / r, ll = (double)(l * (l + 1)), h = s2 * ir * ir;
+                const double f = p0 * (1.0 - 0.5 * ll * h) - s2 * ir * p1 + hs2 * p2;
+                const double fp = ll * h * ir * p0 + (0.5 * (ll + 2.0) * h - 1.0) * p1 + s2 * ir * p2 - hs2 * p3;
                 double rl = 1.0;
                 for (int k = 0; k < l; ++k) rl *= ir;
                 b = rl * f;

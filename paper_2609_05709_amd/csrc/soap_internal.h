@@ -24,7 +24,7 @@ struct Params {
     const double *aprime;      // GTO [l][k]
     const double *G;           // polynomial [n][Q], includes 4 pi
     const double *rq;          // polynomial [Q]
-    const double *WN;          // polynomial, Laplace form [n][i][4]: Chebyshev series of Q_n0..Q_n3 on [0, rc]
+    const double *WN;          // polynomial, Laplace form [n][n+3][4]: Chebyshev series of P_n0..P_n3 on [0, rc]
     const double *c0;          // on-site term [n]
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)

@@ -92,12 +92,12 @@ def test_host_poly_constants_match_oracle(lib, n_max, Q):
 
 @pytest.mark.parametrize("r_cut,n_max,sigma", [(5.0, 1, 0.4), (6.0, 8, 0.5), (5.0, 12, 0.5), (4.0, 16, 0.3)])
 def test_host_poly_laplace_chebyshev_series(lib, r_cut, n_max, sigma):
-    """The Laplace form's sums Q_j(u) = sum_k w_j(k) (2 pi)^{3/2} sigma^3 W_nk/N_k
-    u^(k-1), w = 1, k+2, (k+1)(k+2), k(k+1)(k+2), handed over as Chebyshev
-    series on [0, r_cut], equal the monomial sums with the oracle's 50-digit W
-    and N, to 1e-14 of their largest value on the interval."""
-    n = n_max
-    CH = np.empty((n, n, 4))
+    """The Laplace form's P_j(u) = d^j/du^j sum_k (2 pi)^{3/2} sigma^3 W_nk/N_k
+    u^(k+2), j = 0..3, handed over as Chebyshev series on [0, r_cut], equal
+    the monomial sums with the oracle's 50-digit W and N, to 4e-15 of their
+    largest value on the interval (the series evaluated in float64)."""
+    n, M = n_max, n_max + 3
+    CH = np.empty((n, M, 4))
     err = ctypes.create_string_buffer(256)
     f = lib.soap_basis_poly_laplace
     f.argtypes = [ctypes.c_double, ctypes.c_int, ctypes.c_double, ctypes.c_void_p, ctypes.c_char_p, ctypes.c_int]
@@ -105,12 +105,11 @@ def test_host_poly_laplace_chebyshev_series(lib, r_cut, n_max, sigma):
     N, W, _, _, _ = constants.poly_mp(r_cut, n, 2)
     us = np.linspace(0.0, r_cut, 41)
     t = 2 * us / r_cut - 1
-    weights = [lambda k: 1, lambda k: k + 2, lambda k: (k + 1) * (k + 2), lambda k: k * (k + 1) * (k + 2)]
     with mp.workdps(50):
         pref = (2 * mp.pi) ** mp.mpf(1.5) * mp.mpf(sigma) ** 3
         for a in range(n):
             got = np.polynomial.chebyshev.chebval(t, CH[a]).T  # [u][j]
-            for j, w in enumerate(weights):
-                ref = np.array([float(mp.fsum(w(k) * pref * W[a, k - 1] / N[k - 1] * mp.mpf(u) ** (k - 1)
+            for j in range(4):
+                ref = np.array([float(mp.fsum(pref * W[a, k - 1] / N[k - 1] * mp.ff(k + 2, j) * mp.mpf(u) ** (k + 2 - j)
                                               for k in range(1, n + 1))) for u in us])
-                assert np.abs(got[:, j] - ref).max() <= 1e-14 * np.abs(ref).max(), (a, j)
+                assert np.abs(got[:, j] - ref).max() <= 4e-15 * np.abs(ref).max(), (a, j)

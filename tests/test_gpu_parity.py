@@ -81,6 +81,22 @@ def test_water1000_polynomial_laplace_n8l6(dtype):
     full_check(workloads.WATER1000.with_basis(8, 6, "polynomial-laplace"), dtype, sample=24, seed=5)
 
 
+GTO_F64_N16 = pytest.mark.xfail(
+    strict=True, reason="float64 mode, GTO, n_max 16: the Loewdin coefficients amplify the float64 rounding of "
+    "the radial sum sum_k beta_nk exp(-a'_k r^2) by kappa ~ 5e8 (2e-8 measured); the bar holds to n_max 12")
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+@pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
+def test_largest_radial_basis(rbf, dtype, request):
+    """n_max = 16, the library's largest: the polynomial overlap matrix has
+    condition number 5.6e25 there."""
+    if rbf == "gto" and dtype == "float64":
+        request.applymarker(GTO_F64_N16)
+    wl = workloads.WATER64.with_basis(16, 4, rbf)
+    full_check(wl, dtype, sample=12, seed=16)
+
+
 @pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
 @pytest.mark.parametrize("nl", [(2, 2), (2, 12), (12, 2), (12, 12), (6, 8)])
 def test_hyperparameter_grid_points(rbf, nl):
