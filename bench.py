@@ -273,13 +273,13 @@ def main():
     ap.add_argument("--dtype", default="float32", choices=["float32", "float64"])
     ap.add_argument("--mode", default="derivatives", choices=["derivatives", "cc", "inner", "outer"])
     ap.add_argument("--periodic", action="store_true")
-    ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for both bases; write JSONL here")
+    ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for every radial basis; write JSONL here")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the SOAP path here is built and timed on a single MI355X "
-              "(centers shard across GPUs without communication; see DESIGN.md)", file=sys.stderr)
+              "(centers shard across GPUs without communication)", file=sys.stderr)
         sys.exit(2)
     if a.copy_calibration:
         copy_calibration()

@@ -157,9 +157,10 @@ GRID_NL = (2, 4, 6, 8, 10, 12)
 
 
 def hyperparameter_grid():
-    """The 3000-atom water cluster over n_max, l_max in {2..12}^2, both bases."""
+    """The 3000-atom water cluster over n_max, l_max in {2..12}^2: GTO, and the
+    polynomial basis in its quadrature and Laplace forms."""
     out = []
-    for rbf in ("gto", "polynomial"):
+    for rbf in ("gto", "polynomial", "polynomial-laplace"):
         for n in GRID_NL:
             for l in GRID_NL:
                 out.append(WATER1000.with_basis(n, l, rbf))
