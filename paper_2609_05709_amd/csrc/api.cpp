@@ -205,13 +205,13 @@ int plan_launches(soap_ctx *c) {
         const int jac = mode != 0; // modes 1 and 2 stage gradients
         int *lgrp = c->lgrp[mode], *G = &c->groups[mode];
         // workgroups per CU the registers allow (no LDS), and the LDS share of each
-        const int by_regs = std::max(1, density_blocks_per_cu(f64d, mode, 0));
+        const int by_regs = std::max(1, density_blocks_per_cu(f64d, mode, P.rbf, 0));
         const size_t budget = std::min(LDS_HARD_LIMIT, (size_t)(159 * 1024) / (size_t)by_regs);
         if (plan_groups(P, jac, f64d, budget, lgrp, G, &Wd, &lds) != 0)
             return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
         c->dens_cfg[mode].W = Wd;
         c->dens_cfg[mode].lds = lds;
-        const int per_cu = density_blocks_per_cu(f64d, mode, lds);
+        const int per_cu = density_blocks_per_cu(f64d, mode, P.rbf, lds);
         c->dens_cfg[mode].blocks = std::max(1, ncu * per_cu / *G);
     }
     if (plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) != 0)

@@ -324,18 +324,33 @@ constexpr int SMALL_THREADS = 1024, SMALL_ITEMS = 16, SMALL_MAX = SMALL_THREADS 
 
 // workgroup-wide exclusive scan of one value per thread (BS threads); returns
 // the exclusive prefix, *sum gets the total
+// Exclusive prefix of s over the workgroup (BS threads): a shuffle scan in
+// each wave, then the wave totals scanned by the first wave; two barriers.
+// part holds BS / 64 entries; *sum receives the workgroup total.
 template <int BS>
 __device__ __forceinline__ int64_t block_exclusive(int64_t s, int64_t *part, int64_t *sum) {
-    part[threadIdx.x] = s;
-    __syncthreads();
-    for (int off = 1; off < BS; off <<= 1) {
-        int64_t t = (threadIdx.x >= off) ? part[threadIdx.x - off] : 0;
-        __syncthreads();
-        part[threadIdx.x] += t;
-        __syncthreads();
+    constexpr int NW = BS / 64;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int64_t x = s;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int64_t y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
     }
-    *sum = part[BS - 1];
-    return part[threadIdx.x] - s;
+    if (lane == 63) part[w] = x;
+    __syncthreads();
+    if (w == 0) {
+        int64_t t = lane < NW ? part[lane] : 0;
+#pragma unroll
+        for (int d = 1; d < NW; d <<= 1) {
+            const int64_t y = __shfl_up(t, d, 64);
+            if (lane >= d) t += y;
+        }
+        if (lane < NW) part[lane] = t;
+    }
+    __syncthreads();
+    *sum = part[NW - 1];
+    return (w > 0 ? part[w - 1] : 0) + x - s;
 }
 
 // Largest value and number of values above TCAP of the workgroup's inputs,
@@ -367,7 +382,7 @@ template <typename OutT>
 __global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const int32_t *__restrict__ in,
                                                               OutT *__restrict__ out, int64_t *__restrict__ total_copy,
                                                               int32_t *__restrict__ stats) {
-    __shared__ int64_t part[SMALL_THREADS];
+    __shared__ int64_t part[SMALL_THREADS / 64];
     __shared__ int red[2 * SMALL_THREADS / 64];
     const int64_t base = (int64_t)threadIdx.x * SMALL_ITEMS;
     int64_t v[SMALL_ITEMS], s = 0, total;
@@ -396,7 +411,7 @@ template <typename OutT>
 __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile(int64_t n, const int32_t *__restrict__ in,
                                                             OutT *__restrict__ out, int64_t *__restrict__ sums,
                                                             int32_t *__restrict__ stats) {
-    __shared__ int64_t part[SCAN_THREADS];
+    __shared__ int64_t part[SCAN_THREADS / 64];
     __shared__ int red[2 * SCAN_THREADS / 64];
     const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + threadIdx.x * SCAN_ITEMS;
     int64_t v[SCAN_ITEMS], s = 0, total;
@@ -421,7 +436,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_scan_tile(int64_t n, const int
 // single workgroup: exclusive scan of the tile sums in place; total -> *total
 __global__ __launch_bounds__(1024) void k_scan_sums(int64_t m, int64_t *__restrict__ sums,
                                                     int64_t *__restrict__ total) {
-    __shared__ int64_t part[1024];
+    __shared__ int64_t part[1024 / 64];
     const int per = (int)((m + 1023) / 1024);
     const int64_t base = (int64_t)threadIdx.x * per;
     int64_t s = 0, tot;

@@ -223,7 +223,8 @@ __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lg
     return d;
 }
 
-template <int NT = 0, int LWT = 0>
+// RBF: the radial basis fixed at compile time (0 GTO), or -1 to read it from P
+template <int NT = 0, int LWT = 0, int RBF = -1>
 __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables &T, int lg0, int lg1) {
     const int n = NT ? NT : P.n, lmax = LWT ? LWT - 1 : P.lmax;
     const int ldN = lmax + 2, lgc = lg1 - lg0, tid = threadIdx.x, bs = blockDim.x;
@@ -232,7 +233,7 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     double *Kl = cv.take(16);
     double *Ntl = cv.take((size_t)ldN * ldN);
     double *gc = cv.take(4 * (size_t)grad_pairs(lmax));
-    const int rbf = P.rbf;
+    const int rbf = RBF >= 0 ? RBF : P.rbf;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     // (betaC, betaCa) pairs | G | WN, then aprime | rq | B0
     const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n : (rbf == 1 ? (size_t)n * P.Q : 4 * (size_t)n * (n + 3));
@@ -322,7 +323,7 @@ struct YLayout {
     int es, cs, ls, lmY0;
 };
 
-template <bool GRAD, typename BT = double, int NT = 0, int LWT = 0, typename YT = double>
+template <bool GRAD, typename BT = double, int NT = 0, int LWT = 0, typename YT = double, int RBF = -1>
 __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT *__restrict__ YY, YLayout yl,
                                             typename Pair<BT>::type *__restrict__ BB, double *__restrict__ X,
                                             const double *__restrict__ geo, int nb, int lane, int lg0, int lg1,
@@ -330,7 +331,7 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
     const int n = NT ? NT : P.n, ldN = (LWT ? LWT - 1 : P.lmax) + 2, lgc = lg1 - lg0, nlc = n * lgc;
     const int lgY0 = (GRAD && lg0 > 0) ? lg0 - 1 : lg0;
     const float inv_lg1 = 1.0f / (float)lg1, inv_nlc = 1.0f / (float)nlc, inv_lgc = 1.0f / (float)lgc;
-    const int rbf = P.rbf, Q = P.Q, tw = lg1 + 1;
+    const int rbf = RBF >= 0 ? RBF : P.rbf, Q = P.Q, tw = lg1 + 1;
     // phase 1: harmonic columns (edge, m), then the radial scratch (two
     // independent exponentials per lane trip)
     for (int it = lane; it < nb * lg1; it += 64) {
@@ -705,9 +706,19 @@ __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, in
 }
 
 // MODE: 0 descriptor (c, power spectrum); 1 descriptor + Jacobian (c and D);
-// 2 coefficient Jacobian ("cc": c, every edge's dc/dr_j, and -D)
-template <typename PosT, typename OutT, int MODE>
-__global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
+// 2 coefficient Jacobian ("cc": c, every edge's dc/dr_j, and -D).
+// RBF: the radial basis, fixed at compile time (0 GTO, 1 polynomial by
+// quadrature, 2 polynomial in the Laplace form).  The other bases' branches of
+// the staging then drop out, and with them up to 40 VGPRs: the GTO descriptor
+// kernel runs four waves per SIMD instead of three.
+// Resident waves per SIMD asked of the compiler: 3 for the Jacobian path of
+// GTO and the Laplace form (a small spill; 3 instead of 2 waves), 2 for the
+// coefficient Jacobian (which otherwise takes all 256 VGPRs and runs one
+// wave).  Each measured faster.
+constexpr int dens_min_waves(int mode, int rbf) { return mode == 2 ? 2 : ((mode == 1 && rbf != 1) ? 3 : 1); }
+
+template <typename PosT, typename OutT, int MODE, int RBF>
+__global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF)) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                                  unsigned long long *__restrict__ work, uint64_t base,
                                                  OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,
@@ -730,7 +741,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
 
     Carver cv{smem};
     Tables T;
-    load_tables(P, cv, T, lg0, lg1);
+    load_tables<0, 0, RBF>(P, cv, T, lg0, lg1);
     double *cacc = cv.take((size_t)SnL * (JAC ? 4 : 1)); // [s][a][lmg], then D [3][s][a][lmg]
     double *Dacc = cacc + SnL;
     double *rgeo = cv.take(4 * (size_t)RBk);
@@ -837,7 +848,7 @@ __global__ __launch_bounds__(BSD) void k_density(Params P, Rows R, const PosT *_
             for (int off = wave * W; off < rbn; off += NWD * W) {
                 const int nb = (rbn - off) < W ? (rbn - off) : W;
                 const double *geo = rgeo + 4 * off;
-                stage_edges<JAC, ST, 0, 0, ST>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
+                stage_edges<JAC, ST, 0, 0, ST, RBF>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
                 for (int e = 0; e < nb; ++e) {
                     const int s = __builtin_amdgcn_readfirstlane(rsp[off + e]);
                     if (s != cur) {

@@ -119,7 +119,7 @@ struct JacLaunch {
 };
 
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64);
-int density_blocks_per_cu(bool f64, int mode, size_t lds); // mode as launch_density
+int density_blocks_per_cu(bool f64, int mode, int rbf, size_t lds); // mode as launch_density; rbf as Params
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
 int jacobian_max_w();

@@ -14,16 +14,23 @@ size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool
     return d * 8;
 }
 
-int density_blocks_per_cu(bool f64, int mode, size_t lds) {
+// the density kernel of a precision, mode and radial basis
+template <typename T, int RBF>
+static const void *density_kernel_r(int mode) {
+    return mode == 0 ? (const void *)dev::k_density<T, T, 0, RBF>
+                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF> : (const void *)dev::k_density<T, T, 2, RBF>;
+}
+template <typename T>
+static const void *density_kernel_t(int mode, int rbf) {
+    return rbf == 0 ? density_kernel_r<T, 0>(mode) : (rbf == 1 ? density_kernel_r<T, 1>(mode) : density_kernel_r<T, 2>(mode));
+}
+static const void *density_kernel(bool f64, int mode, int rbf) {
+    return f64 ? density_kernel_t<double>(mode, rbf) : density_kernel_t<float>(mode, rbf);
+}
+
+int density_blocks_per_cu(bool f64, int mode, int rbf, size_t lds) {
     int nb = 0;
-    const void *k = nullptr;
-    if (f64)
-        k = mode == 0 ? (const void *)dev::k_density<double, double, 0>
-                      : mode == 1 ? (const void *)dev::k_density<double, double, 1> : (const void *)dev::k_density<double, double, 2>;
-    else
-        k = mode == 0 ? (const void *)dev::k_density<float, float, 0>
-                      : mode == 1 ? (const void *)dev::k_density<float, float, 1> : (const void *)dev::k_density<float, float, 2>;
-    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, BSD, lds);
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, density_kernel(f64, mode, rbf), BSD, lds);
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
@@ -94,12 +101,9 @@ hipError_t set_lds_limits() {
     hipError_t e = hipSuccess;
 #define SOAP_SET(K)                                                                                          \
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
-    SOAP_SET((dev::k_density<float, float, 0>));
-    SOAP_SET((dev::k_density<float, float, 1>));
-    SOAP_SET((dev::k_density<float, float, 2>));
-    SOAP_SET((dev::k_density<double, double, 0>));
-    SOAP_SET((dev::k_density<double, double, 1>));
-    SOAP_SET((dev::k_density<double, double, 2>));
+    for (int f64 = 0; f64 < 2; ++f64)
+        for (int mode = 0; mode < 3; ++mode)
+            for (int rbf = 0; rbf < 3; ++rbf) SOAP_SET(density_kernel(f64 != 0, mode, rbf));
     SOAP_SET(k_outputs<float>);
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
@@ -125,13 +129,7 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
     Rows Rk = R;
     int W = cfg.W;
     void *args[] = {&Pk, &Rk, &pos, &W, &work, &b, &desc, &c_out, &jself, &c_scratch, &jc_edge};
-    const void *k;
-    if (f64)
-        k = mode == 0 ? (const void *)dev::k_density<double, double, 0>
-                      : mode == 1 ? (const void *)dev::k_density<double, double, 1> : (const void *)dev::k_density<double, double, 2>;
-    else
-        k = mode == 0 ? (const void *)dev::k_density<float, float, 0>
-                      : mode == 1 ? (const void *)dev::k_density<float, float, 1> : (const void *)dev::k_density<float, float, 2>;
+    const void *k = density_kernel(f64, mode, P.rbf);
     const hipError_t e =
         hipLaunchKernel(k, dim3((unsigned)(per_group * P.n_groups)), dim3(BSD), args, cfg.lds, st);
     // the counter is taken for every center but the per_group static ones,
