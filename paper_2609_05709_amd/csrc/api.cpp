@@ -194,8 +194,19 @@ int plan_groups(const Params &P, int jac, bool f64, size_t budget, int *lgrp, in
     return -1;
 }
 
+// The radial basis the kernels evaluate: the user's, except that GTO in
+// float64 from n_max = 10 on takes the compensated evaluation (Params.rbf 3):
+// the Loewdin coefficients amplify the rounding of sum_k beta e^{-a' r^2} by
+// a factor growing from ~1e5 at n_max 10 to ~5e8 at 16.
+constexpr int GTO_COMPENSATED_MIN_N = 10;
+int kernel_basis(const soap_ctx *c) {
+    if (c->rbf == SOAP_RBF_GTO && c->dtype == SOAP_FP64 && c->n >= GTO_COMPENSATED_MIN_N) return 3;
+    return c->rbf;
+}
+
 int plan_launches(soap_ctx *c) {
     Params &P = c->P;
+    P.rbf = kernel_basis(c);
     int Wd;
     size_t lds;
     int ncu = 256;
@@ -223,7 +234,7 @@ int plan_launches(soap_ctx *c) {
     for (int W = jacobian_max_w(); W >= 1; --W) {
         const size_t lds = jacobian_lds_bytes(P, W, f64);
         if (lds > LDS_HARD_LIMIT) continue;
-        const int b = jacobian_blocks_per_cu(f64, P.n, P.lmax + 1, lds);
+        const int b = jacobian_blocks_per_cu(f64, P.rbf, P.n, P.lmax + 1, lds);
         if (b > bestB) {
             bestB = b;
             bestW = W;
@@ -239,13 +250,15 @@ int upload_constants(soap_ctx *c) {
     const int n = c->n, lw = c->lmax + 1, S = (int)c->Z.size();
     char msg[256] = {0};
     const int ldN = lw + 1; // harmonics tables cover l <= l_max + 1
-    std::vector<double> betaC, betaCa, aprime, G, rq, WN, c0(n), Nlm((size_t)ldN * ldN);
+    std::vector<double> betaC, betaCa, aprime, betaC_lo, aprime_lo, G, rq, WN, c0(n), Nlm((size_t)ldN * ldN);
     if (c->rbf == SOAP_RBF_GTO) {
         betaC.resize((size_t)lw * n * n);
         betaCa.resize((size_t)lw * n * n);
         aprime.resize((size_t)lw * n);
+        betaC_lo.resize(betaC.size());
+        aprime_lo.resize(aprime.size());
         if (soap_basis_gto(c->r_cut, n, c->lmax, c->sigma, betaC.data(), betaCa.data(), aprime.data(), c0.data(),
-                           msg, sizeof msg) != 0)
+                           msg, sizeof msg, betaC_lo.data(), nullptr, aprime_lo.data()) != 0)
             return fail(c, SOAP_EINVAL, "%s", msg);
     } else {
         G.resize((size_t)n * c->Q);
@@ -287,11 +300,13 @@ int upload_constants(soap_ctx *c) {
             for (int k = 2; k <= l - m; ++k) v /= (long double)k;
             Nt[(size_t)l * ldN + m] = (double)v;
         }
-    // one constant buffer: betaC | betaCa | aprime | G | rq | WN | c0 | Nt | gcoef
+    // one constant buffer: betaC | betaCa | aprime | remainders of betaC, aprime | G | rq | WN | c0 | Nt | gcoef
     std::vector<double> all;
     size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
     size_t o_ba = all.size(); all.insert(all.end(), betaCa.begin(), betaCa.end());
     size_t o_ap = all.size(); all.insert(all.end(), aprime.begin(), aprime.end());
+    size_t o_bcl = all.size(); all.insert(all.end(), betaC_lo.begin(), betaC_lo.end());
+    size_t o_apl = all.size(); all.insert(all.end(), aprime_lo.begin(), aprime_lo.end());
     size_t o_G = all.size(); all.insert(all.end(), G.begin(), G.end());
     size_t o_rq = all.size(); all.insert(all.end(), rq.begin(), rq.end());
     size_t o_wn = all.size(); all.insert(all.end(), WN.begin(), WN.end());
@@ -338,6 +353,8 @@ int upload_constants(soap_ctx *c) {
     P.betaC = d + o_bc;
     P.betaCa = d + o_ba;
     P.aprime = d + o_ap;
+    P.betaC_lo = d + o_bcl;
+    P.aprime_lo = d + o_apl;
     P.G = d + o_G;
     P.rq = d + o_rq;
     P.WN = d + o_wn;

@@ -161,7 +161,8 @@ void set_err(char *err, int errlen, const char *msg) {
 } // namespace
 
 extern "C" int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, double *betaC, double *betaCa,
-                              double *aprime, double *c0, char *err, int errlen) {
+                              double *aprime, double *c0, char *err, int errlen, double *betaC_lo, double *betaCa_lo,
+                              double *aprime_lo) {
     const int n = n_max;
     const q128 rc = r_cut, sg = sigma, s2 = sg * sg;
     std::vector<q128> z(n);
@@ -189,10 +190,14 @@ extern "C" int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, 
             q128 ap = al[k] / den;              // envelope exponent of Eq. (gto-coefficients)
             q128 C = pref / half_int_pow(den, l); // prefactor of Eq. (gto-coefficients)
             aprime[l * n + k] = (double)ap;
+            if (aprime_lo) aprime_lo[l * n + k] = (double)(ap - (q128)aprime[l * n + k]);
             for (int a = 0; a < n; ++a) {
-                q128 bc = B[(size_t)a * n + k] * C;
-                betaC[((size_t)l * n + a) * n + k] = (double)bc;
-                betaCa[((size_t)l * n + a) * n + k] = (double)(-2 * bc * ap);
+                const size_t o = ((size_t)l * n + a) * n + k;
+                const q128 bc = B[(size_t)a * n + k] * C, bca = -2 * bc * ap;
+                betaC[o] = (double)bc;
+                betaCa[o] = (double)bca;
+                if (betaC_lo) betaC_lo[o] = (double)(bc - (q128)betaC[o]);
+                if (betaCa_lo) betaCa_lo[o] = (double)(bca - (q128)betaCa[o]);
             }
         }
     }

@@ -11,9 +11,12 @@ extern "C" {
 //   aprime[l][k]    = alpha_kl / (1 + 2 sigma^2 alpha_kl)
 //   c0[n]           = on-site l = 0 term of Eq. (gto-coefficients)
 // so that B_nl(r) = sum_k betaC e^{-aprime r^2} and c_nlm = B_nl r^l Y_lm.
+// betaC_lo, betaCa_lo, aprime_lo (each may be NULL): the rounding remainders
+// x - (double)x of the three tables, for the compensated float64 evaluation.
 // Returns 0, or -1 with a message in err.
 int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, double *betaC, double *betaCa,
-                   double *aprime, double *c0, char *err, int errlen);
+                   double *aprime, double *c0, char *err, int errlen, double *betaC_lo, double *betaCa_lo,
+                   double *aprime_lo);
 
 // Polynomial basis (Sec. 2.3) with a quad_n-point Gauss-Legendre rule on
 // [0, r_cut]:  G[n][q] = 4 pi w_q r_q^2 g_n(r_q),  rq[q] = r_q,

@@ -17,7 +17,9 @@
 //         Bh_nl = r^-(l+1) / s^2 sum_q G_nq e^{-(r_q-r)^2/2s^2} (r_q ii_{l+1} - r ii_l)
 //       with ii_l(x) = e^-x i_l(x) and d/dx (x^-l i_l) = x^-l i_{l+1};
 //       polynomial, Laplace form (Eqs. poly-coefficients, poly-radial-derivative):
-//         B_nl = r^-l f_nl,  Bh_nl = r^-(l+1) (f'_nl - l f_nl / r)  (see stage_edges).
+//         B_nl = r^-l f_nl,  Bh_nl = r^-(l+1) (f'_nl - l f_nl / r)  (see stage_edges);
+//       GTO, compensated (float64 mode, larger n_max): the GTO sums with every
+//         exponential in double-double arithmetic and compensated dot products.
 //
 // k_density: persistent workgroups, each bound to one l-group and taking
 //   centers from a counter.  Accumulates c (and, for the Jacobian, D = sum
@@ -77,6 +79,74 @@ __device__ __forceinline__ void load4(const float *p, double &a, double &b, doub
 // relative error of (x + 1/2) * inv stays below 1/(2d) of the gap to the
 // next integer
 __device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x + 0.5f) * inv); }
+
+// ---------------------------------------------------------------------------
+// Double-double arithmetic (unevaluated sums hi + lo) for the compensated GTO
+// radial sums: Knuth's two-sum, the fused multiply-add two-product.  Device
+// code is compiled with multiply-add contraction on; fused into the sums, a
+// product's rounding no longer matches the remainder taken from it, and the
+// compensated sums lose more than they gain.  Every function here, and every
+// block that uses them, turns contraction off.
+// ---------------------------------------------------------------------------
+struct dd {
+    double hi, lo;
+};
+__device__ __forceinline__ dd dd_fast_sum(double a, double b) { // |a| >= |b|
+#pragma clang fp contract(off)
+    const double s = a + b;
+    return dd{s, b - (s - a)};
+}
+__device__ __forceinline__ dd dd_two_sum(double a, double b) {
+#pragma clang fp contract(off)
+    const double s = a + b, bb = s - a;
+    return dd{s, (a - (s - bb)) + (b - bb)};
+}
+__device__ __forceinline__ dd dd_add(dd a, dd b) {
+#pragma clang fp contract(off)
+    dd s = dd_two_sum(a.hi, b.hi);
+    const dd t = dd_two_sum(a.lo, b.lo);
+    s.lo += t.hi;
+    s = dd_fast_sum(s.hi, s.lo);
+    s.lo += t.lo;
+    return dd_fast_sum(s.hi, s.lo);
+}
+__device__ __forceinline__ dd dd_mul(dd a, dd b) {
+#pragma clang fp contract(off)
+    const double p = a.hi * b.hi;
+    double e = fma(a.hi, b.hi, -p);
+    e = fma(a.hi, b.lo, e);
+    e = fma(a.lo, b.hi, e);
+    return dd_fast_sum(p, e);
+}
+// exp(-x) for x >= 0 to ~1e-30 relative: x = k ln 2 + t with ln 2 split in
+// three parts (the first with 32 significant bits, so k times it is exact),
+// then exp(-t) = (exp(-t / 256))^256, the inner factor by its Taylor series
+// to degree 9 (|t| / 256 < 1.4e-3: remainder below 1e-35) and eight squarings.
+__device__ __forceinline__ dd dd_exp_neg(dd x) {
+#pragma clang fp contract(off)
+    if (x.hi > 700.0) return dd{0.0, 0.0};
+    constexpr double L1 = 0.6931471803691238, L2 = 1.9082149292705877e-10, L3 = 1.1612227229362532e-26;
+    // 1/j!, j = 0..9, as (hi, lo)
+    constexpr double FH[10] = {1.0, 1.0, 0.5, 0.16666666666666666, 0.041666666666666664, 0.008333333333333333,
+                               0.001388888888888889, 0.0001984126984126984, 2.48015873015873e-05,
+                               2.7557319223985893e-06};
+    constexpr double FL[10] = {0.0, 0.0, 0.0, 9.25185853854297e-18, 2.3129646346357427e-18, 1.1564823173178714e-19,
+                               -5.300543954373577e-20, 1.7209558293420705e-22, 2.1511947866775882e-23,
+                               -1.858393274046472e-22};
+    const double k = rint(x.hi * 1.4426950408889634);
+    const double t1 = fma(-k, L1, x.hi); // exact
+    const double p2 = k * L2, e2 = fma(k, L2, -p2);
+    dd t = dd_add(dd{t1, x.lo}, dd{-p2, -e2});
+    t.lo -= k * L3;
+    const dd y{-t.hi * (1.0 / 256.0), -t.lo * (1.0 / 256.0)};
+    dd p{FH[9], FL[9]};
+#pragma unroll
+    for (int j = 8; j >= 0; --j) p = dd_add(dd_mul(p, y), dd{FH[j], FL[j]});
+#pragma unroll
+    for (int j = 0; j < 8; ++j) p = dd_mul(p, p);
+    const int ki = (int)k;
+    return dd{ldexp(p.hi, -ki), ldexp(p.lo, -ki)};
+}
 
 // ---------------------------------------------------------------------------
 // Real solid harmonics of one column m without gradients and without
@@ -208,6 +278,8 @@ struct Tables {
     const double *aprime;  // GTO: [k][lc]
     const double *G, *rq;  // polynomial: [n][Q], [Q]
     const double *WN, *B0; // polynomial, Laplace form: [n][n+3][4] Chebyshev coefficients (stage_edges); B_n0(0) [n]
+    const double2 *bcdd;   // GTO, compensated: [k][n][lc] = (betaC, its remainder)
+    const double2 *apdd;   // GTO, compensated: [k][lc] = (a', its remainder)
     const double *Nt;      // [ldN][ldN] N_lm (2m-1)!! / (l-m)!, for sh_col_y
     const double2 *gcoef;  // [(l, m >= 0)][2]: (cA, cB), (cC, l | m << 8), see stage_edges
 };
@@ -219,7 +291,8 @@ __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lg
     size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
     if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
     else if (P.rbf == 1) d += even(n * P.Q) + even((size_t)P.Q);
-    else d += 4 * n * (n + 3) + even(n);
+    else if (P.rbf == 2) d += 4 * n * (n + 3) + even(n);
+    else d += 2 * (size_t)lgc * n * n + 2 * (size_t)lgc * n;
     return d;
 }
 
@@ -235,9 +308,10 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     double *gc = cv.take(4 * (size_t)grad_pairs(lmax));
     const int rbf = RBF >= 0 ? RBF : P.rbf;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    // (betaC, betaCa) pairs | G | WN, then aprime | rq | B0
-    const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n : (rbf == 1 ? (size_t)n * P.Q : 4 * (size_t)n * (n + 3));
-    const size_t szB = rbf == 0 ? (size_t)lgc * n : (rbf == 1 ? (size_t)P.Q : (size_t)n);
+    // (betaC, betaCa) pairs | G | WN | (betaC, remainder) pairs, then aprime | rq | B0 | (a', remainder) pairs
+    const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n
+                                : (rbf == 1 ? (size_t)n * P.Q : (rbf == 2 ? 4 * (size_t)n * (n + 3) : 2 * (size_t)lgc * n * n));
+    const size_t szB = rbf == 0 ? (size_t)lgc * n : (rbf == 1 ? (size_t)P.Q : (rbf == 2 ? (size_t)n : 2 * (size_t)lgc * n));
     double *A = cv.take(szA), *B = cv.take(szB);
     for (int k = tid; k < ldN * ldN; k += bs) Ntl[k] = P.Nt[k];
     for (int k = tid; k < 4 * grad_pairs(lmax); k += bs) gc[k] = P.gcoef[k];
@@ -257,6 +331,20 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     } else if (rbf == 1) {
         for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
         for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
+    } else if (rbf == 3) {
+        // global [l][n][k] -> LDS [k][n][lc] pairs; global [l][k] -> LDS [k][lc] pairs
+        const size_t o = (size_t)lg0 * n * n;
+        for (int s = tid; s < (int)(szA / 2); s += bs) {
+            const int lc = s / (n * n), r = s - lc * n * n, a = r / n, k = r - a * n;
+            const int d = (k * n + a) * lgc + lc;
+            A[2 * d] = P.betaC[o + s];
+            A[2 * d + 1] = P.betaC_lo[o + s];
+        }
+        for (int s = tid; s < (int)(szB / 2); s += bs) {
+            const int lc = s / n, k = s - lc * n;
+            B[2 * (k * lgc + lc)] = P.aprime[(size_t)lg0 * n + s];
+            B[2 * (k * lgc + lc) + 1] = P.aprime_lo[(size_t)lg0 * n + s];
+        }
     } else {
         // a neighbour at distance 0 adds the on-site term: B_n0 S_00 = c0_n
         for (int k = tid; k < (int)szA; k += bs) A[k] = P.WN[k];
@@ -271,13 +359,17 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     T.aprime = B;
     T.rq = B;
     T.B0 = B;
+    T.bcdd = (const double2 *)A;
+    T.apdd = (const double2 *)B;
 }
 
 // X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
 // Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place);
-// Laplace form: the four l-independent values P_j per n, 4 n
+// Laplace form: the four l-independent values P_j per n, 4 n; compensated
+// GTO: the exponentials in double-double, 2 n * lgc
 __host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int lgc, int lg1) {
-    return P.rbf == 0 ? (size_t)P.n * lgc : (P.rbf == 1 ? (size_t)P.Q * (lg1 + 1) : 4 * (size_t)P.n);
+    return P.rbf == 0 ? (size_t)P.n * lgc
+                      : (P.rbf == 1 ? (size_t)P.Q * (lg1 + 1) : (P.rbf == 2 ? 4 * (size_t)P.n : 2 * (size_t)P.n * lgc));
 }
 
 // Synchronisation inside one wave: LDS writes become visible to the other
@@ -339,7 +431,19 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
         const double *g = geo + 4 * e;
         sh_col_y(m, m > lgY0 ? m : lgY0, lg1, g[0], g[1], g[2], T.Nt, ldN, YY + e * yl.es, yl.ls, yl.lmY0);
     }
-    if (rbf == 0) {
+    if constexpr (RBF == 3) {
+#pragma clang fp contract(off)
+        // compensated GTO: x = a' r^2 in double-double (a' as hi + remainder), then exp(-x)
+        for (int it = lane; it < nb * nlc; it += 64) {
+            const int e = qdiv(it, inv_nlc), t = it - e * nlc; // t = k lgc + lc
+            const double r = geo[4 * e + 3], s2r = r * r;
+            const double2 ap = T.apdd[t];
+            const double xh = ap.x * s2r;
+            const dd v = dd_exp_neg(dd_fast_sum(xh, fma(ap.x, s2r, -xh) + ap.y * s2r));
+            X[2 * it] = v.hi;
+            X[2 * it + 1] = v.lo;
+        }
+    } else if (rbf == 0) {
         const int nx = nb * nlc;
         for (int it = lane; it < nx; it += 128) {
             const int i2 = it + 64 < nx ? it + 64 : it;
@@ -414,7 +518,33 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
         }
     }
     const int nd = nb * nlc;
-    if (rbf == 0) {
+    if constexpr (RBF == 3) {
+#pragma clang fp contract(off)
+        // compensated dot products (two-product and two-sum per term, the
+        // errors summed apart): B = sum_k betaC e_k, Bh = -2 sum_k (betaC a') e_k
+        // with betaC a' formed in double-double (no second table: the LDS
+        // then holds what the plain GTO path holds)
+        for (int it = lane; it < nd; it += 64) {
+            const int e = qdiv(it, inv_nlc), t = it - e * nlc, lc = t - qdiv(t, inv_lgc) * lgc;
+            const double2 *bc = T.bcdd + t; // [k][n][lc]
+            const double2 *apk = T.apdd + lc; // [k][lc]
+            const double *E = X + 2 * ((size_t)e * nlc + lc);
+            double sb = 0.0, cb = 0.0, sh = 0.0, ch = 0.0;
+            for (int k = 0; k < n; ++k) {
+                const double2 c = bc[(size_t)k * nlc], ap = apk[k * lgc];
+                const dd m = dd_mul(dd{c.x, c.y}, dd{ap.x, ap.y});
+                const double eh = E[2 * k * lgc], el = E[2 * k * lgc + 1];
+                const double pb = c.x * eh, ph = m.hi * eh;
+                const dd tb = dd_two_sum(sb, pb), th = dd_two_sum(sh, ph);
+                sb = tb.hi;
+                sh = th.hi;
+                cb += (fma(c.x, eh, -pb) + tb.lo) + (c.x * el + c.y * eh);
+                ch += (fma(m.hi, eh, -ph) + th.lo) + (m.hi * el + m.lo * eh);
+            }
+            const double K = scaleK ? T.Kl[lg0 + lc] : 1.0;
+            BB[it] = Pair<BT>::make(K * (sb + cb), -2.0 * K * (sh + ch));
+        }
+    } else if (rbf == 0) {
         for (int it = lane; it < nd; it += 128) {
             const int i2 = it + 64 < nd ? it + 64 : it;
             const int e1 = qdiv(it, inv_nlc), t1 = it - e1 * nlc, l1 = t1 - qdiv(t1, inv_lgc) * lgc;
@@ -708,14 +838,16 @@ __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, in
 // MODE: 0 descriptor (c, power spectrum); 1 descriptor + Jacobian (c and D);
 // 2 coefficient Jacobian ("cc": c, every edge's dc/dr_j, and -D).
 // RBF: the radial basis, fixed at compile time (0 GTO, 1 polynomial by
-// quadrature, 2 polynomial in the Laplace form).  The other bases' branches of
+// quadrature, 2 polynomial in the Laplace form, 3 GTO compensated).  The other bases' branches of
 // the staging then drop out, and with them up to 40 VGPRs: the GTO descriptor
 // kernel runs four waves per SIMD instead of three.
 // Resident waves per SIMD asked of the compiler: 3 for the Jacobian path of
 // GTO and the Laplace form (a small spill; 3 instead of 2 waves), 2 for the
 // coefficient Jacobian (which otherwise takes all 256 VGPRs and runs one
 // wave).  Each measured faster.
-constexpr int dens_min_waves(int mode, int rbf) { return mode == 2 ? 2 : ((mode == 1 && rbf != 1) ? 3 : 1); }
+constexpr int dens_min_waves(int mode, int rbf) {
+    return mode == 2 ? 2 : ((mode == 1 && (rbf == 0 || rbf == 2)) ? 3 : 1);
+}
 
 template <typename PosT, typename OutT, int MODE, int RBF>
 __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF)) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
@@ -1113,7 +1245,8 @@ __device__ __forceinline__ void store3(T *o, uint32_t Fe, uint32_t idx, V x, V y
 // spills.
 constexpr int jac_min_waves(int ab, int LWT) { return (ab == 4 && (LWT == 0 || LWT <= 7)) ? 3 : 2; }
 
-template <typename PosT, typename OutT, int NT, int LWT>
+// RBF: -1 reads the radial basis from P (0..2); 3 is the compensated GTO
+template <typename PosT, typename OutT, int NT, int LWT, int RBF = -1>
 __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
                                                                             int W, const double *__restrict__ c_scratch,
                                                                             OutT *__restrict__ jedge) {
@@ -1130,7 +1263,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
 
     Carver cv{smem};
     Tables T;
-    load_tables<NT, LWT>(P, cv, T, 0, lw);
+    load_tables<NT, LWT, RBF>(P, cv, T, 0, lw);
     double *cT = cv.take((size_t)Sn * L); // [L][Sn]
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
@@ -1185,7 +1318,8 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
             const int64_t base = rb0 + off;
             const double *geo = rgeo + 4 * off;
             const int *spc = rsp + off;
-            stage_edges<true, AT, NT, LWT>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw, true);
+            stage_edges<true, AT, NT, LWT, double, RBF>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw,
+                                                        true);
 
             // ---- precontraction on the matrix cores ----
             // chunks j = (l, ch) in l-major order, operands loaded JB at a time

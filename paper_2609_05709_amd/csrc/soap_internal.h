@@ -14,7 +14,8 @@ constexpr int MAX_DEGREE = 2048;
 
 // Everything the descriptor kernels need about the basis; passed by value.
 struct Params {
-    int S, n, lmax, L, rbf, Q; // L = (lmax+1)^2, rbf 0 = GTO, 1 = polynomial, 2 = polynomial (Laplace form)
+    int S, n, lmax, L, rbf, Q; // L = (lmax+1)^2; rbf 0 GTO, 1 polynomial, 2 polynomial (Laplace form),
+                               // 3 GTO with the compensated float64 evaluation
     int F, Fe, nq_full;        // features, edge features, (mu,nu,n,n') combinations
     double sigma, inv_s2;      // 1 / sigma^2
     double rc, inv_rc2;        // cutoff radius, 2 / rc
@@ -22,6 +23,7 @@ struct Params {
     const double *betaC;       // GTO [l][n][k]
     const double *betaCa;      // GTO [l][n][k]
     const double *aprime;      // GTO [l][k]
+    const double *betaC_lo, *aprime_lo; // GTO: rounding remainders of betaC and aprime (compensated path)
     const double *G;           // polynomial [n][Q], includes 4 pi
     const double *rq;          // polynomial [Q]
     const double *WN;          // polynomial, Laplace form [n][n+3][4]: Chebyshev series of P_n0..P_n3 on [0, rc]
@@ -123,7 +125,7 @@ int density_blocks_per_cu(bool f64, int mode, int rbf, size_t lds); // mode as l
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
 int jacobian_max_w();
-int jacobian_blocks_per_cu(bool f64, int n, int lw, size_t lds); // resident workgroups per CU (0 if it does not fit)
+int jacobian_blocks_per_cu(bool f64, int rbf, int n, int lw, size_t lds); // resident workgroups per CU (0 if it does not fit)
 // float32 Jacobian kernels for fixed (n_max, l_max + 1); NULL if not compiled
 const void *jacobian_fixed_0(int n, int lw);
 const void *jacobian_fixed_1(int n, int lw);

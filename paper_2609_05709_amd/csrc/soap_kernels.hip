@@ -22,6 +22,10 @@ static const void *density_kernel_r(int mode) {
 }
 template <typename T>
 static const void *density_kernel_t(int mode, int rbf) {
+    if (rbf == 3) { // the compensated GTO exists for float64 only
+        if constexpr (sizeof(T) == 8) return density_kernel_r<T, 3>(mode);
+        return nullptr;
+    }
     return rbf == 0 ? density_kernel_r<T, 0>(mode) : (rbf == 1 ? density_kernel_r<T, 1>(mode) : density_kernel_r<T, 2>(mode));
 }
 static const void *density_kernel(bool f64, int mode, int rbf) {
@@ -82,17 +86,20 @@ int jacobian_max_w() { return JAC_MAX_W; }
 // The float32 Jacobian kernel is also compiled for fixed (n_max, l_max + 1)
 // pairs (jacobian_fixed.hip); the generic kernel covers every other basis and
 // float64.
-const void *jacobian_kernel(bool f64, int n, int lw) {
-    if (f64) return reinterpret_cast<const void *>(&k_jacobian<double, double, 0, 0>);
+const void *jacobian_kernel(bool f64, int rbf, int n, int lw) {
+    if (f64)
+        return rbf == 3 ? reinterpret_cast<const void *>(&k_jacobian<double, double, 0, 0, 3>)
+                        : reinterpret_cast<const void *>(&k_jacobian<double, double, 0, 0>);
+    if (rbf == 3) return nullptr; // float64 only
     const void *k = jacobian_fixed_0(n, lw);
     if (!k) k = jacobian_fixed_1(n, lw);
     if (!k) k = jacobian_fixed_2(n, lw);
     return k ? k : reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>);
 }
 
-int jacobian_blocks_per_cu(bool f64, int n, int lw, size_t lds) {
+int jacobian_blocks_per_cu(bool f64, int rbf, int n, int lw, size_t lds) {
     int nb = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, jacobian_kernel(f64, n, lw), BSJ, lds);
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, jacobian_kernel(f64, rbf, n, lw), BSJ, lds);
     return (e == hipSuccess && nb > 0) ? nb : 0;
 }
 
@@ -103,16 +110,17 @@ hipError_t set_lds_limits() {
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
     for (int f64 = 0; f64 < 2; ++f64)
         for (int mode = 0; mode < 3; ++mode)
-            for (int rbf = 0; rbf < 3; ++rbf) SOAP_SET(density_kernel(f64 != 0, mode, rbf));
+            for (int rbf = 0; rbf < (f64 ? 4 : 3); ++rbf) SOAP_SET(density_kernel(f64 != 0, mode, rbf));
     SOAP_SET(k_outputs<float>);
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
     SOAP_SET(k_power_single<double>);
     SOAP_SET((k_jacobian<float, float, 0, 0>));
     SOAP_SET((k_jacobian<double, double, 0, 0>));
+    SOAP_SET((k_jacobian<double, double, 0, 0, 3>));
     for (int n = 1; n <= NMAX; ++n)
         for (int lw = 1; lw <= LMAX + 1; ++lw) {
-            const void *k = jacobian_kernel(false, n, lw);
+            const void *k = jacobian_kernel(false, 0, n, lw);
             if (k != reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>)) SOAP_SET(k);
         }
 #undef SOAP_SET
@@ -145,7 +153,7 @@ hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool
     Rows Rk = R;
     int W = cfg.W;
     void *args[] = {&Pk, &Rk, &pos, &W, &c_scratch, &jedge};
-    return hipLaunchKernel(jacobian_kernel(f64, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args, cfg.lds, st);
+    return hipLaunchKernel(jacobian_kernel(f64, P.rbf, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args, cfg.lds, st);
 }
 
 hipError_t launch_column_mean(const void *in, bool f64, int64_t rows, int64_t cols, double *part, void *out,

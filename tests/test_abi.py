@@ -47,10 +47,13 @@ def test_host_gto_constants_match_oracle(lib, r_cut, n_max, l_max, sigma):
     ba = np.empty(lw * n * n)
     ap = np.empty(lw * n)
     c0 = np.empty(n)
+    bcl, bal, apl = np.empty_like(bc), np.empty_like(ba), np.empty_like(ap)
     err = ctypes.create_string_buffer(256)
     f = lib.soap_basis_gto
-    f.argtypes = [ctypes.c_double, ctypes.c_int, ctypes.c_int, ctypes.c_double] + [ctypes.c_void_p] * 5 + [ctypes.c_int]
-    assert f(r_cut, n, l_max, sigma, bc.ctypes.data, ba.ctypes.data, ap.ctypes.data, c0.ctypes.data, err, 256) == 0
+    f.argtypes = ([ctypes.c_double, ctypes.c_int, ctypes.c_int, ctypes.c_double] + [ctypes.c_void_p] * 5 + [ctypes.c_int]
+                  + [ctypes.c_void_p] * 3)
+    assert f(r_cut, n, l_max, sigma, bc.ctypes.data, ba.ctypes.data, ap.ctypes.data, c0.ctypes.data, err, 256,
+             bcl.ctypes.data, bal.ctypes.data, apl.ctypes.data) == 0
     z, alpha, beta = constants.gto_mp(r_cut, n, l_max)
     with mp.workdps(50):
         s2 = mp.mpf(sigma) ** 2
@@ -59,10 +62,18 @@ def test_host_gto_constants_match_oracle(lib, r_cut, n_max, l_max, sigma):
                 den = 1 + 2 * s2 * alpha[l][k]
                 C = (2 * mp.pi) ** 1.5 * mp.mpf(sigma) ** 3 / den ** (l + mp.mpf(3) / 2)
                 assert abs(ap[l * n + k] - float(alpha[l][k] / den)) <= 2e-16 * abs(float(alpha[l][k] / den))
+                # the remainders make hi + lo the value to the 113-bit setup's accuracy (~1e-22);
+                # the compensated float64 path uses both parts
+                apr = alpha[l][k] / den
+                assert abs(mp.mpf(ap[l * n + k]) + mp.mpf(apl[l * n + k]) - apr) <= 1e-28 * abs(apr)
                 for a in range(n):
                     ref = beta[l][a, k] * C
                     got = bc[(l * n + a) * n + k]
                     assert abs(got - float(ref)) <= 1e-15 * abs(float(ref)) + 1e-300, (l, a, k, got, ref)
+                    i = (l * n + a) * n + k
+                    assert abs(mp.mpf(bc[i]) + mp.mpf(bcl[i]) - ref) <= 1e-20 * abs(ref) + 1e-300, (l, a, k)
+                    refa = -2 * ref * apr
+                    assert abs(mp.mpf(ba[i]) + mp.mpf(bal[i]) - refa) <= 1e-20 * abs(refa) + 1e-300, (l, a, k)
         for a in range(n):
             ref = mp.sqrt(2) * mp.pi * mp.mpf(sigma) ** 3 * mp.fsum(
                 beta[0][a, k] / (1 + 2 * s2 * alpha[0][k]) ** 1.5 for k in range(n))

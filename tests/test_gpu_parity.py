@@ -1,6 +1,8 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
 same seeded inputs, element by element.  Tolerances: 1e-5 (float32 mode) and
 1e-10 (float64 mode), normwise per descriptor row / Jacobian block."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -81,20 +83,22 @@ def test_water1000_polynomial_laplace_n8l6(dtype):
     full_check(workloads.WATER1000.with_basis(8, 6, "polynomial-laplace"), dtype, sample=24, seed=5)
 
 
-GTO_F64_N16 = pytest.mark.xfail(
-    strict=True, reason="float64 mode, GTO, n_max 16: the Loewdin coefficients amplify the float64 rounding of "
-    "the radial sum sum_k beta_nk exp(-a'_k r^2) by kappa ~ 5e8 (2e-8 measured); the bar holds to n_max 12")
-
-
 @pytest.mark.parametrize("dtype", ["float32", "float64"])
 @pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
-def test_largest_radial_basis(rbf, dtype, request):
+def test_largest_radial_basis(rbf, dtype):
     """n_max = 16, the library's largest: the polynomial overlap matrix has
-    condition number 5.6e25 there."""
-    if rbf == "gto" and dtype == "float64":
-        request.applymarker(GTO_F64_N16)
+    condition number 5.6e25 there, and the GTO Loewdin coefficients amplify
+    float64 rounding of the radial sums by ~5e8 (the compensated path)."""
     wl = workloads.WATER64.with_basis(16, 4, rbf)
     full_check(wl, dtype, sample=12, seed=16)
+
+
+@pytest.mark.parametrize("n_max,l_max,sigma", [(10, 6, 0.5), (12, 12, 0.5), (14, 4, 0.3), (16, 8, 0.5)])
+def test_gto_float64_compensated(n_max, l_max, sigma):
+    """GTO in float64 from n_max 10 on: every exponential in double-double and
+    compensated sums over the Loewdin coefficients keep the 1e-10 bar."""
+    wl = dataclasses.replace(workloads.WATER64.with_basis(n_max, l_max, "gto"), sigma=sigma)
+    full_check(wl, "float64", sample=12, seed=n_max + l_max)
 
 
 @pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
