@@ -377,33 +377,80 @@ __device__ __forceinline__ void block_degree_stats(int vmax, int over, int *red,
 }
 
 // one workgroup for n <= SMALL_MAX; total also to *total_copy and degree
-// statistics to stats if given
+// statistics to stats if given.  Rounds of SMALL_THREADS x 4 consecutive
+// items: each thread takes four in one 16-byte load (coalesced across the
+// wave), then a shuffle scan of the threads' sums within the waves and of the
+// wave totals.  The wave-total array alternates between rounds, so a round's
+// two barriers also order the previous round's reads of it.  All loads are
+// issued first; the cross-lane shuffles set the time, so rounds are few.
 template <typename OutT>
 __global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const int32_t *__restrict__ in,
                                                               OutT *__restrict__ out, int64_t *__restrict__ total_copy,
                                                               int32_t *__restrict__ stats) {
-    __shared__ int64_t part[SMALL_THREADS / 64];
-    __shared__ int red[2 * SMALL_THREADS / 64];
-    const int64_t base = (int64_t)threadIdx.x * SMALL_ITEMS;
-    int64_t v[SMALL_ITEMS], s = 0, total;
+    constexpr int NW = SMALL_THREADS / 64, VEC = 4, ROUND = SMALL_THREADS * VEC, MAXR = SMALL_MAX / ROUND;
+    __shared__ int64_t part[2][NW];
+    __shared__ int red[2 * NW];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int64_t carry = 0;
     int vmax = 0, over = 0;
+    int32_t vr[MAXR][VEC];
 #pragma unroll
-    for (int k = 0; k < SMALL_ITEMS; ++k) {
-        v[k] = (base + k < n) ? (int64_t)in[base + k] : 0;
-        s += v[k];
-        vmax = max(vmax, (int)v[k]);
-        over += v[k] > TCAP;
+    for (int r = 0; r < MAXR; ++r) {
+        const int64_t b = (int64_t)r * ROUND + (int64_t)threadIdx.x * VEC;
+        if (b + VEC <= n) {
+            const int4 q = *(const int4 *)(in + b); // in is 16-byte aligned
+            vr[r][0] = q.x;
+            vr[r][1] = q.y;
+            vr[r][2] = q.z;
+            vr[r][3] = q.w;
+        } else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) vr[r][k] = b + k < n ? in[b + k] : 0;
+        }
+    }
+    const int rounds = (int)((n + ROUND - 1) / ROUND);
+#pragma unroll
+    for (int r = 0; r < MAXR; ++r) {
+        if (r >= rounds) break;
+        const int buf = r & 1;
+        const int64_t b = (int64_t)r * ROUND + (int64_t)threadIdx.x * VEC;
+        int64_t v = 0;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            v += vr[r][k];
+            vmax = max(vmax, vr[r][k]);
+            over += vr[r][k] > TCAP;
+        }
+        int64_t x = v;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int64_t y = __shfl_up(x, d, 64);
+            if (lane >= d) x += y;
+        }
+        if (lane == 63) part[buf][w] = x;
+        __syncthreads();
+        if (w == 0) {
+            int64_t t = lane < NW ? part[buf][lane] : 0;
+#pragma unroll
+            for (int d = 1; d < NW; d <<= 1) {
+                const int64_t y = __shfl_up(t, d, 64);
+                if (lane >= d) t += y;
+            }
+            if (lane < NW) part[buf][lane] = t;
+        }
+        __syncthreads();
+        int64_t run = carry + (w > 0 ? part[buf][w - 1] : 0) + x - v;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            if (b + k < n) out[b + k] = (OutT)run;
+            run += vr[r][k];
+        }
+        carry += part[buf][NW - 1];
     }
     if (stats) block_degree_stats<SMALL_THREADS>(vmax, over, red, stats);
-    int64_t run = block_exclusive<SMALL_THREADS>(s, part, &total);
-#pragma unroll
-    for (int k = 0; k < SMALL_ITEMS; ++k) {
-        if (base + k < n) out[base + k] = (OutT)run;
-        run += v[k];
-    }
     if (threadIdx.x == 0) {
-        out[n] = (OutT)total;
-        if (total_copy) *total_copy = total;
+        out[n] = (OutT)carry;
+        if (total_copy) *total_copy = carry;
     }
 }
 
