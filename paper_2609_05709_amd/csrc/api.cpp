@@ -59,11 +59,10 @@ struct soap_ctx {
     int nq_full = 0;
     std::vector<uint32_t> fq;
     std::vector<uint32_t> dtab;   // [tri lw] diagonal-pair slots of the Jacobian kernel
-    std::vector<int32_t> qmap;    // [Sn][Sn] pair index of (u, v), u <= v, else -1
     std::vector<int32_t> fmap;    // [S][Fe]
     Params P{};
     // device constants
-    DevBuf d_const, d_qmap, d_dtab, d_fmap, d_lut;
+    DevBuf d_const, d_dtab, d_fmap, d_lut;
     // neighbour workspace
     NbrWork nw{};
     DevBuf b_zero, b_bstart, b_acell, b_srec, b_sspec, b_deg, b_slots, b_scan, b_spec, b_row, b_cols, b_cscratch;
@@ -127,13 +126,6 @@ void build_feature_tables(soap_ctx *c) {
                     c->fq.push_back((uint32_t)mu | (uint32_t)nu << 8 | (uint32_t)a << 16 | (uint32_t)b << 24);
     c->nq_full = (int)c->fq.size();
     c->F = (int64_t)c->nq_full * lw;
-    const int Sn = S * n;
-    c->qmap.assign((size_t)Sn * Sn, -1);
-    for (int q = 0; q < c->nq_full; ++q) {
-        const uint32_t f = c->fq[q];
-        const int u = (int)(f & 0xff) * n + (int)((f >> 16) & 0xff), v = (int)((f >> 8) & 0xff) * n + (int)(f >> 24);
-        c->qmap[(size_t)u * Sn + v] = q;
-    }
     c->Fe = (int64_t)lw * (n * (n + 1) / 2 + (S - 1) * n * n);
     c->fmap.assign((size_t)S * c->Fe, 0);
     // fmap[s][k]: feature index of slot k of a species-s neighbour block
@@ -319,9 +311,6 @@ int upload_constants(soap_ctx *c) {
         return hip_fail(c, e, "hipMemcpy(constants)");
     double *d = c->d_const.as<double>();
     build_feature_tables(c);
-    if ((e = c->d_qmap.ensure(c->qmap.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(qmap)");
-    if ((e = hipMemcpy(c->d_qmap.p, c->qmap.data(), c->qmap.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
-        return hip_fail(c, e, "hipMemcpy(qmap)");
     if ((e = c->d_dtab.ensure(c->dtab.size() * 4)) != hipSuccess) return hip_fail(c, e, "hipMalloc(dtab)");
     if ((e = hipMemcpy(c->d_dtab.p, c->dtab.data(), c->dtab.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
         return hip_fail(c, e, "hipMemcpy(dtab)");
@@ -361,7 +350,6 @@ int upload_constants(soap_ctx *c) {
     P.c0 = d + o_c0;
     P.Nt = d + o_Nt;
     P.gcoef = d + o_gc;
-    P.qmap = c->d_qmap.as<int32_t>();
     P.dtab = c->d_dtab.as<uint32_t>();
     P.tri_lw = (int)c->dtab.size();
     return plan_launches(c);
@@ -867,7 +855,7 @@ const char *soap_last_error(const soap_ctx *c) { return c ? c->err.c_str() : g_c
 void soap_destroy(soap_ctx *c) {
     if (!c) return;
     (void)hipDeviceSynchronize();
-    for (DevBuf *b : {&c->d_const, &c->d_qmap, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_zero, &c->b_bstart, &c->b_acell,
+    for (DevBuf *b : {&c->d_const, &c->d_dtab, &c->d_fmap, &c->d_lut, &c->b_zero, &c->b_bstart, &c->b_acell,
                       &c->b_srec, &c->b_sspec, &c->b_deg, &c->b_slots, &c->b_scan, &c->b_spec, &c->b_row, &c->b_cols,
                       &c->b_cscratch, &c->b_avg, &c->b_avg_part, &c->b_img_lohi, &c->b_img_cnt, &c->b_img_start,
                       &c->b_pos_ext, &c->b_Z_ext, &c->b_map_atom, &c->b_map_img, &c->b_iota})

@@ -685,13 +685,43 @@ struct CoefView {
 // translational invariance).  Items (l, tile pair) go round-robin over the
 // nw waves; only u <= v, the stored pairs (mu <= nu, n' >= n on mu = nu),
 // are written.
+//
+// Pair index q of rows u <= v (u = species * n + n'), -1 for u > v: the
+// position of the block (mu, nu, n, n') in the feature order (species pairs
+// mu <= nu, then n, then n' with n' >= n on mu = nu).  Computed rather than
+// read from a table: a global load among the output stores would wait for
+// all of them (one vmcnt counter covers loads and stores).
+struct PairIndex {
+    int S, n;
+    float inv_n;
+    __device__ __forceinline__ int operator()(int u, int v) const {
+        if (u > v) return -1;
+        const int mu = qdiv(u, inv_n), a = u - mu * n, nu = qdiv(v, inv_n), b = v - nu * n;
+        const int D = n * (n + 1) / 2, O = n * n;
+        const int q = mu * D + O * (mu * (S - 1) - mu * (mu - 1) / 2); // pairs before (mu, mu)
+        if (mu == nu) return q + a * n - a * (a + 1) / 2 + b;
+        return q + D + (nu - mu - 1) * O + a * n + b;
+    }
+};
+// the four pair indices of a lane's results: rows u = 16 ti + kk + 4 r of column v = 16 tj + ro
+__device__ __forceinline__ void lane_pair_index(const PairIndex &pq, int Sn, int ti, int tj, int kk, int ro, int q[4]) {
+    const int v = 16 * tj + ro;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int u = 16 * ti + kk + 4 * r;
+        q[r] = (u < Sn && v < Sn) ? pq(u, v) : -1;
+    }
+}
+
 template <typename OutT>
 __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn, int lm0, int lg0, int lgc,
-                                            OutT *__restrict__ row, int ldq, int lbase, const int *__restrict__ qmap,
+                                            OutT *__restrict__ row, int ldq, int lbase, const PairIndex pq,
                                             int wave, int nw, int lane, const double *__restrict__ Kl) {
     const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
     const int nitem = lgc * ntp;
     const int ro = lane & 15, kk = lane >> 4;
+    int q[4];
+    if (ntp == 1) lane_pair_index(pq, Sn, 0, 0, kk, ro, q);
     for (int item = wave; item < nitem; item += nw) { // uniform per wave
         const int lc = item / ntp, l = lg0 + lc;
         int tp = item - lc * ntp, ti = 0;
@@ -700,6 +730,7 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
             ++ti;
         }
         const int tj = ti + tp;
+        if (ntp > 1) lane_pair_index(pq, Sn, ti, tj, kk, ro, q);
         const int ua = 16 * ti + ro, vb = 16 * tj + ro; // A row, B column of this lane
         const bool uok = ua < Sn, vok = vb < Sn;
         const int oa = (uok ? ua : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
@@ -720,17 +751,11 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
             }
         }
         // lane holds rows u = 16 ti + kk + 4 r of column v = 16 tj + ro
-        const int v = 16 * tj + ro;
         const double K = comp < 0 ? Kl[l] : -Kl[l];
         OutT *rl = row + (l - lbase);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int u = 16 * ti + kk + 4 * r;
-            if (u < Sn && v < Sn) {
-                const int q = qmap[u * Sn + v];
-                if (q >= 0) store_out(rl + q * ldq, K * acc[r]);
-            }
-        }
+        for (int r = 0; r < 4; ++r)
+            if (q[r] >= 0) store_out(rl + q[r] * ldq, K * acc[r]);
     }
 }
 
@@ -744,11 +769,13 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
 template <typename OutT>
 __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int xs, int ldu, int ldm, int Sn, int lm0,
                                              int lg0, int lgc, OutT *__restrict__ r0, OutT *__restrict__ r1, int rs,
-                                             int ldq, int lbase, const int *__restrict__ qmap, int wave, int nw,
+                                             int ldq, int lbase, const PairIndex pq, int wave, int nw,
                                              int lane, const double *__restrict__ Kl) {
     const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
     const int nitem = lgc * ntp;
     const int ro = lane & 15, kk = lane >> 4;
+    int q[4];
+    if (ntp == 1) lane_pair_index(pq, Sn, 0, 0, kk, ro, q);
     for (int item = wave; item < nitem; item += nw) { // uniform per wave
         const int lc = item / ntp, l = lg0 + lc;
         int tp = item - lc * ntp, ti = 0;
@@ -757,6 +784,7 @@ __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int x
             ++ti;
         }
         const int tj = ti + tp;
+        if (ntp > 1) lane_pair_index(pq, Sn, ti, tj, kk, ro, q);
         const int ua = 16 * ti + ro, vb = 16 * tj + ro; // A row, B column of this lane
         const bool uok = ua < Sn, vok = vb < Sn;
         const int oa = (uok ? ua : 0) * ldu + (l * l - lm0) * ldm;
@@ -780,20 +808,15 @@ __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int x
             jz = __builtin_amdgcn_mfma_f64_16x16x4f64(ca, zb, jz, 0, 0, 0);
         }
         // lane holds rows u = 16 ti + kk + 4 r of column v = 16 tj + ro
-        const int v = 16 * tj + ro;
         const double K = Kl[l];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int u = 16 * ti + kk + 4 * r;
-            if (u < Sn && v < Sn) {
-                const int q = qmap[u * Sn + v];
-                if (q >= 0) {
-                    const int f = q * ldq + l - lbase;
-                    store_out(r0 + f, K * p[r]);
-                    store_out(r1 + f, -K * jx[r]);
-                    store_out(r1 + (rs + f), -K * jy[r]);
-                    store_out(r1 + (2 * rs + f), -K * jz[r]);
-                }
+            if (q[r] >= 0) {
+                const int f = q[r] * ldq + l - lbase;
+                store_out(r0 + f, K * p[r]);
+                store_out(r1 + f, -K * jx[r]);
+                store_out(r1 + (rs + f), -K * jy[r]);
+                store_out(r1 + (2 * rs + f), -K * jz[r]);
             }
         }
     }
@@ -820,6 +843,7 @@ __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int x
 // and k_jacobian.
 // ---------------------------------------------------------------------------
 constexpr int NWD = 4, BSD = 64 * NWD;
+
 constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 64 * KE
 
 __host__ __device__ __forceinline__ int dens_lgY0(int jac, int lg0) { return (jac && lg0 > 0) ? lg0 - 1 : lg0; }
@@ -945,7 +969,8 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF)) void k_density(Para
         load_rows(rgeo, rsp, pos, R.spec, R.cols, e0, (int)cnt, pi);
     };
     fetch();
-    const float inv_Lg = 1.0f / (float)Lg;
+    const float inv_Lg = 1.0f / (float)Lg, inv_Sn = 1.0f / (float)Sn;
+    const PairIndex pq{S, n, 1.0f / (float)n};
 
     while (ci < R.nc) {
         for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BSD) cacc[k] = 0.0;
@@ -1031,7 +1056,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF)) void k_density(Para
         // power spectrum (descriptor path): per l, 16 x 16 matrix-core tiles
         // (ti <= tj) of u = (species, n) rows and v = (species, n') columns
         if (!JAC && desc)
-            power_tiles<OutT>(CoefView{cacc, nullptr, Lg, 1}, -1, Sn, lm0, lg0, lgc, desc + cw * P.F, lw, 0, P.qmap,
+            power_tiles<OutT>(CoefView{cacc, nullptr, Lg, 1}, -1, Sn, lm0, lg0, lgc, desc + cw * P.F, lw, 0, pq,
                               wave, NWD, lane, T.Kl);
         if (c_out)
             for (int it = tid; it < SnL; it += BSD) {
@@ -1055,12 +1080,14 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF)) void k_density(Para
             const bool whole = G == 1;
             if (whole)
                 power_tiles4<OutT>(cacc, SnL, Lg, 1, Sn, 0, 0, lw, desc + cw * P.F, jself + cw * 3 * P.F, P.F, lw, 0,
-                                   P.qmap, wave, NWD, lane, T.Kl);
+                                   pq, wave, NWD, lane, T.Kl);
+            // in destination order (consecutive lanes, consecutive addresses);
+            // the transposition falls on the LDS reads
             double *sc = c_scratch + cw * 4 * (size_t)Lfull * Sn;
             for (int it = tid; it < (whole ? 1 : 4) * SnL; it += BSD) {
                 const int comp = it / SnL, rem = it - comp * SnL;
-                const int sa = qdiv(rem, inv_Lg), lmg = rem - sa * Lg;
-                sc[((size_t)comp * Lfull + lm0 + lmg) * Sn + sa] = cacc[it];
+                const int lmg = qdiv(rem, inv_Sn), sa = rem - lmg * Sn;
+                sc[((size_t)comp * Lfull + lm0 + lmg) * Sn + sa] = cacc[comp * SnL + sa * Lg + lmg];
             }
         }
         lds_barrier(); // the outputs are read from cacc before the next center clears it
@@ -1082,7 +1109,7 @@ constexpr int BSO = 256;
 
 __host__ __device__ __forceinline__ size_t outputs_group_doubles(const Params &P, int lg0, int lg1, int out_bytes) {
     const size_t Sn = (size_t)P.S * P.n, slab = (size_t)(lg1 * lg1 - lg0 * lg0) * Sn;
-    return even((Sn * Sn + 1) / 2) + 4 * even(slab) + 4 * even(((size_t)P.nq_full * (lg1 - lg0) * out_bytes + 7) / 8);
+    return 4 * even(slab) + 4 * even(((size_t)P.nq_full * (lg1 - lg0) * out_bytes + 7) / 8);
 }
 
 template <typename OutT>
@@ -1095,9 +1122,8 @@ __global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const doub
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     constexpr int NW = BSO / 64;
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    int *qmap = (int *)smem; // pair index of (u, v)
-    for (int t = tid; t < Sn * Sn; t += BSO) qmap[t] = P.qmap[t];
-    double *base = smem + even(((size_t)Sn * Sn + 1) / 2);
+    double *base = smem;
+    const PairIndex pq{P.S, P.n, 1.0f / (float)P.n};
     const double *src = scratch + ci * 4 * (size_t)L * Sn;
     OutT *drow = desc + ci * F, *jrow = jself + ci * 3 * F; // jself rows d = 0..2 are consecutive
     for (int g = 0; g < O.n_groups; ++g) {
@@ -1126,7 +1152,7 @@ __global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const doub
             }
         }
         lds_barrier();
-        power_tiles4<OutT>(X, sstr, 1, Sn, Sn, lm0, lg0, lgc, rows, rows + rstr, rstr, lgc, lg0, qmap, wave, NW, lane,
+        power_tiles4<OutT>(X, sstr, 1, Sn, Sn, lm0, lg0, lgc, rows, rows + rstr, rstr, lgc, lg0, pq, wave, NW, lane,
                            Kl);
         lds_barrier();
         if (lgc == lw) {
@@ -1182,7 +1208,8 @@ __global__ __launch_bounds__(256) void k_power_single(Params P, const double *__
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     copy_to_lds<256, 4>(smem, c, Sn * L, tid);
     lds_barrier();
-    power_tiles<OutT>(CoefView{smem, nullptr, L, 1}, -1, Sn, 0, 0, P.lmax + 1, out, P.lmax + 1, 0, P.qmap, wave, 4,
+    power_tiles<OutT>(CoefView{smem, nullptr, L, 1}, -1, Sn, 0, 0, P.lmax + 1, out, P.lmax + 1, 0,
+                      PairIndex{P.S, P.n, 1.0f / (float)P.n}, wave, 4,
                       lane, Kl);
 }
 

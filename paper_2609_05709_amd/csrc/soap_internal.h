@@ -30,7 +30,6 @@ struct Params {
     const double *c0;          // on-site term [n]
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)
-    const int32_t *qmap;       // [Sn][Sn] pair index q of rows u <= v (u = species n + n), else -1
     const uint32_t *dtab;      // [tri_lw] diagonal-pair slots: (n lw + l) | (n' lw + l) << 16, n' >= n
     int tri_lw;                // n (n + 1) / 2 * (l_max + 1)
     int n_groups;              // l-groups of the density kernel
