@@ -208,13 +208,32 @@ int plan_launches(soap_ctx *c) {
         const int jac = mode != 0; // modes 1 and 2 stage gradients
         int *lgrp = c->lgrp[mode], *G = &c->groups[mode];
         // workgroups per CU the registers allow (no LDS), and the LDS share of each
-        const int by_regs = std::max(1, density_blocks_per_cu(f64d, mode, P.rbf, 0));
-        const size_t budget = std::min(LDS_HARD_LIMIT, (size_t)(159 * 1024) / (size_t)by_regs);
-        if (plan_groups(P, jac, f64d, budget, lgrp, G, &Wd, &lds) != 0)
+        auto plan = [&](bool hi, int *lg, int *g, int *w, size_t *ld) {
+            const int by_regs = std::max(1, density_blocks_per_cu(f64d, mode, P.rbf, hi, 0));
+            const size_t budget = std::min(LDS_HARD_LIMIT, (size_t)(159 * 1024) / (size_t)by_regs);
+            return plan_groups(P, jac, f64d, budget, lg, g, w, ld) == 0;
+        };
+        if (!plan(false, lgrp, G, &Wd, &lds))
             return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
+        bool hi = false;
+        if (density_has_high(mode, P.rbf)) {
+            // three workgroups per CU hide more latency, but split the LDS
+            // three ways: taken only if the plan keeps its l-groups and at
+            // least two edges per tile (measured: 3% faster at n_max 8,
+            // l_max 6; up to twice as slow where the tiles shrink)
+            int lg3[MAX_GROUPS + 1], G3 = 0, W3 = 0;
+            size_t lds3 = 0;
+            if (plan(true, lg3, &G3, &W3, &lds3) && G3 == *G && W3 >= 2) {
+                hi = true;
+                std::copy(lg3, lg3 + G3 + 1, lgrp);
+                Wd = W3;
+                lds = lds3;
+            }
+        }
         c->dens_cfg[mode].W = Wd;
         c->dens_cfg[mode].lds = lds;
-        const int per_cu = density_blocks_per_cu(f64d, mode, P.rbf, lds);
+        c->dens_cfg[mode].hi = hi;
+        const int per_cu = density_blocks_per_cu(f64d, mode, P.rbf, hi, lds);
         c->dens_cfg[mode].blocks = std::max(1, ncu * per_cu / *G);
     }
     if (plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) != 0)

@@ -865,16 +865,18 @@ __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, in
 // quadrature, 2 polynomial in the Laplace form, 3 GTO compensated).  The other bases' branches of
 // the staging then drop out, and with them up to 40 VGPRs: the GTO descriptor
 // kernel runs four waves per SIMD instead of three.
-// Resident waves per SIMD asked of the compiler: 3 for the Jacobian path of
-// GTO and the Laplace form (a small spill; 3 instead of 2 waves), 2 for the
-// coefficient Jacobian (which otherwise takes all 256 VGPRs and runs one
-// wave).  Each measured faster.
-constexpr int dens_min_waves(int mode, int rbf) {
-    return mode == 2 ? 2 : ((mode == 1 && (rbf == 0 || rbf == 2)) ? 3 : 1);
+// Resident waves per SIMD asked of the compiler: 2 for the coefficient
+// Jacobian (which otherwise takes all 256 VGPRs and runs one wave); for the
+// Jacobian path of GTO and the Laplace form a second variant (HI) asks for 3
+// (a small spill).  Three workgroups per CU split the LDS three ways, so the
+// host takes HI only where the LDS plan stays as good (dens_high_occupancy).
+constexpr bool dens_has_high(int mode, int rbf) { return mode == 1 && (rbf == 0 || rbf == 2); }
+constexpr int dens_min_waves(int mode, int rbf, bool hi) {
+    return mode == 2 ? 2 : ((hi && dens_has_high(mode, rbf)) ? 3 : 1);
 }
 
-template <typename PosT, typename OutT, int MODE, int RBF>
-__global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF)) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
+template <typename PosT, typename OutT, int MODE, int RBF, bool HI>
+__global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                                  unsigned long long *__restrict__ work, uint64_t base,
                                                  OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,

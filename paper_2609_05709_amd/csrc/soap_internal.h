@@ -113,6 +113,7 @@ struct DensityLaunch {
     int W;           // edges per wave iteration
     size_t lds;      // dynamic LDS bytes
     int blocks;      // persistent workgroups per l-group
+    bool hi;         // the variant compiled for three waves per SIMD (see density_has_high)
 };
 struct JacLaunch {
     int W;          // edges per wave tile (at most jacobian_max_w())
@@ -120,7 +121,8 @@ struct JacLaunch {
 };
 
 size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64);
-int density_blocks_per_cu(bool f64, int mode, int rbf, size_t lds); // mode as launch_density; rbf as Params
+int density_blocks_per_cu(bool f64, int mode, int rbf, bool hi, size_t lds); // mode as launch_density; rbf as Params
+bool density_has_high(int mode, int rbf); // a three-waves-per-SIMD variant exists
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
 size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
 int jacobian_max_w();

@@ -14,27 +14,32 @@ size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool
     return d * 8;
 }
 
-// the density kernel of a precision, mode and radial basis
-template <typename T, int RBF>
+// the density kernel of a precision, mode, radial basis and occupancy variant
+template <typename T, int RBF, bool HI>
 static const void *density_kernel_r(int mode) {
-    return mode == 0 ? (const void *)dev::k_density<T, T, 0, RBF>
-                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF> : (const void *)dev::k_density<T, T, 2, RBF>;
+    return mode == 0 ? (const void *)dev::k_density<T, T, 0, RBF, false>
+                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF, HI>
+                                 : (const void *)dev::k_density<T, T, 2, RBF, false>;
 }
 template <typename T>
-static const void *density_kernel_t(int mode, int rbf) {
+static const void *density_kernel_t(int mode, int rbf, bool hi) {
     if (rbf == 3) { // the compensated GTO exists for float64 only
-        if constexpr (sizeof(T) == 8) return density_kernel_r<T, 3>(mode);
+        if constexpr (sizeof(T) == 8) return density_kernel_r<T, 3, false>(mode);
         return nullptr;
     }
-    return rbf == 0 ? density_kernel_r<T, 0>(mode) : (rbf == 1 ? density_kernel_r<T, 1>(mode) : density_kernel_r<T, 2>(mode));
+    if (rbf == 1) return density_kernel_r<T, 1, false>(mode);
+    if (rbf == 0) return hi ? density_kernel_r<T, 0, true>(mode) : density_kernel_r<T, 0, false>(mode);
+    return hi ? density_kernel_r<T, 2, true>(mode) : density_kernel_r<T, 2, false>(mode);
 }
-static const void *density_kernel(bool f64, int mode, int rbf) {
-    return f64 ? density_kernel_t<double>(mode, rbf) : density_kernel_t<float>(mode, rbf);
+static const void *density_kernel(bool f64, int mode, int rbf, bool hi) {
+    return f64 ? density_kernel_t<double>(mode, rbf, hi) : density_kernel_t<float>(mode, rbf, hi);
 }
 
-int density_blocks_per_cu(bool f64, int mode, int rbf, size_t lds) {
+bool density_has_high(int mode, int rbf) { return dev::dens_has_high(mode, rbf); }
+
+int density_blocks_per_cu(bool f64, int mode, int rbf, bool hi, size_t lds) {
     int nb = 0;
-    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, density_kernel(f64, mode, rbf), BSD, lds);
+    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, density_kernel(f64, mode, rbf, hi), BSD, lds);
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
@@ -110,7 +115,8 @@ hipError_t set_lds_limits() {
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
     for (int f64 = 0; f64 < 2; ++f64)
         for (int mode = 0; mode < 3; ++mode)
-            for (int rbf = 0; rbf < (f64 ? 4 : 3); ++rbf) SOAP_SET(density_kernel(f64 != 0, mode, rbf));
+            for (int rbf = 0; rbf < (f64 ? 4 : 3); ++rbf)
+                for (int hi = 0; hi < 2; ++hi) SOAP_SET(density_kernel(f64 != 0, mode, rbf, hi != 0));
     SOAP_SET(k_outputs<float>);
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
@@ -137,7 +143,7 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
     Rows Rk = R;
     int W = cfg.W;
     void *args[] = {&Pk, &Rk, &pos, &W, &work, &b, &desc, &c_out, &jself, &c_scratch, &jc_edge};
-    const void *k = density_kernel(f64, mode, P.rbf);
+    const void *k = density_kernel(f64, mode, P.rbf, cfg.hi);
     const hipError_t e =
         hipLaunchKernel(k, dim3((unsigned)(per_group * P.n_groups)), dim3(BSD), args, cfg.lds, st);
     // the counter is taken for every center but the per_group static ones,
