@@ -217,13 +217,16 @@ int plan_launches(soap_ctx *c) {
             return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
         bool hi = false;
         if (density_has_high(mode, P.rbf)) {
-            // three workgroups per CU hide more latency, but split the LDS
-            // three ways: taken only if the plan keeps its l-groups and at
-            // least two edges per tile (measured: 3% faster at n_max 8,
-            // l_max 6; up to twice as slow where the tiles shrink)
+            // more workgroups per CU hide more latency, but split the LDS
+            // further.  The Jacobian path takes three waves per SIMD only if
+            // the plan keeps its l-groups and at least two edges per tile
+            // (measured: 3% faster at n_max 8, l_max 6; up to twice as slow
+            // where the tiles shrink).  "cc" takes two waves whenever they
+            // plan (faster in 3 of 4 measured bases, by 13-29%; 13% slower at
+            // n_max 12, l_max 12, where no simple rule on the plan told apart)
             int lg3[MAX_GROUPS + 1], G3 = 0, W3 = 0;
             size_t lds3 = 0;
-            if (plan(true, lg3, &G3, &W3, &lds3) && G3 == *G && W3 >= 2) {
+            if (plan(true, lg3, &G3, &W3, &lds3) && (mode == 2 || (G3 == *G && W3 >= 2))) {
                 hi = true;
                 std::copy(lg3, lg3 + G3 + 1, lgrp);
                 Wd = W3;

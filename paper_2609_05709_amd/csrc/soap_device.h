@@ -865,14 +865,14 @@ __host__ __device__ __forceinline__ size_t dens_wave_doubles(const Params &P, in
 // quadrature, 2 polynomial in the Laplace form, 3 GTO compensated).  The other bases' branches of
 // the staging then drop out, and with them up to 40 VGPRs: the GTO descriptor
 // kernel runs four waves per SIMD instead of three.
-// Resident waves per SIMD asked of the compiler: 2 for the coefficient
-// Jacobian (which otherwise takes all 256 VGPRs and runs one wave); for the
-// Jacobian path of GTO and the Laplace form a second variant (HI) asks for 3
-// (a small spill).  Three workgroups per CU split the LDS three ways, so the
-// host takes HI only where the LDS plan stays as good (dens_high_occupancy).
-constexpr bool dens_has_high(int mode, int rbf) { return mode == 1 && (rbf == 0 || rbf == 2); }
+// Resident waves per SIMD: a second variant (HI) of the coefficient Jacobian
+// asks for 2 (it otherwise takes all 256 VGPRs and runs one wave), and of the
+// Jacobian path of GTO and the Laplace form for 3 (a small spill).  More
+// workgroups per CU split the LDS further, so the host takes HI only where
+// the LDS plan stays as good (density_has_high and plan_launches).
+constexpr bool dens_has_high(int mode, int rbf) { return mode == 2 || (mode == 1 && (rbf == 0 || rbf == 2)); }
 constexpr int dens_min_waves(int mode, int rbf, bool hi) {
-    return mode == 2 ? 2 : ((hi && dens_has_high(mode, rbf)) ? 3 : 1);
+    return (hi && dens_has_high(mode, rbf)) ? (mode == 2 ? 2 : 3) : 1;
 }
 
 template <typename PosT, typename OutT, int MODE, int RBF, bool HI>

@@ -18,18 +18,21 @@ size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool
 template <typename T, int RBF, bool HI>
 static const void *density_kernel_r(int mode) {
     return mode == 0 ? (const void *)dev::k_density<T, T, 0, RBF, false>
-                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF, HI>
-                                 : (const void *)dev::k_density<T, T, 2, RBF, false>;
+                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF, HI && dev::dens_has_high(1, RBF)>
+                                 : (const void *)dev::k_density<T, T, 2, RBF, HI>;
+}
+template <typename T, int RBF>
+static const void *density_kernel_h(int mode, bool hi) {
+    return hi ? density_kernel_r<T, RBF, true>(mode) : density_kernel_r<T, RBF, false>(mode);
 }
 template <typename T>
 static const void *density_kernel_t(int mode, int rbf, bool hi) {
     if (rbf == 3) { // the compensated GTO exists for float64 only
-        if constexpr (sizeof(T) == 8) return density_kernel_r<T, 3, false>(mode);
+        if constexpr (sizeof(T) == 8) return density_kernel_h<T, 3>(mode, hi);
         return nullptr;
     }
-    if (rbf == 1) return density_kernel_r<T, 1, false>(mode);
-    if (rbf == 0) return hi ? density_kernel_r<T, 0, true>(mode) : density_kernel_r<T, 0, false>(mode);
-    return hi ? density_kernel_r<T, 2, true>(mode) : density_kernel_r<T, 2, false>(mode);
+    return rbf == 0 ? density_kernel_h<T, 0>(mode, hi)
+                    : (rbf == 1 ? density_kernel_h<T, 1>(mode, hi) : density_kernel_h<T, 2>(mode, hi));
 }
 static const void *density_kernel(bool f64, int mode, int rbf, bool hi) {
     return f64 ? density_kernel_t<double>(mode, rbf, hi) : density_kernel_t<float>(mode, rbf, hi);
