@@ -74,15 +74,16 @@ def density_flops(wl, E, n_centers, F):
     return E * per_edge + n_centers * per_center
 
 
-def measured_traffic(workload_name, kernel):
+def measured_traffic(workload_name, kernel, output):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     runs (FETCH_SIZE, WRITE_SIZE, each scaled by the reading of a plain copy of
-    known size), or None if absent or taken on different kernel source."""
+    known size), or None if absent, taken at another output precision or on
+    different kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         doc = json.load(open(path))[workload_name]
         sha = kernels_source_sha()
-        if doc["kernels_source_sha256_16"] != sha:
+        if doc["kernels_source_sha256_16"] != sha or doc["output"] != output:
             return None
         k = doc["per_launch"][kernel]
         return k["fetch_bytes"] + k["write_bytes"]
@@ -116,11 +117,9 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "repeats": 3}))
 
 
-def cpu_baseline(wl, st, budget_s=12.0):
-    """The oracle as it stands, on the host cores, over a bounded sample of
-    centers (batches of 128 until ~budget_s of wall time)."""
-    import oracle
-    o = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+def _oracle_rate(o, wl, st, budget_s):
+    """Centers per second of the oracle over seeded random batches of 128
+    centers until ~budget_s of wall time; (rate, centers done, seconds)."""
     rng = np.random.default_rng(12345)
     order = rng.permutation(st.n_atoms)
     done, t0 = 0, time.perf_counter()
@@ -129,10 +128,39 @@ def cpu_baseline(wl, st, budget_s=12.0):
         o.compute(st.pos64, st.Z, centers=batch, jacobian=wl.jacobian)
         done += len(batch)
     dt = time.perf_counter() - t0
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": done / dt, "unit": "atoms/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} of {st.n_atoms} centers (seeded random), neighbour search + "
-                      f"{'descriptor + Jacobian' if wl.jacobian else 'descriptor'}, {dt:.1f} s"}
+    return done / dt, done, dt
+
+
+def _cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, st, budget_s=12.0, one_thread=False):
+    """The oracle as it stands, on the host cores, over a bounded sample of
+    centers; with one_thread, also a sample on a single thread."""
+    import oracle
+    o = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    threads = oracle.threads()
+    what = "descriptor + Jacobian" if wl.jacobian else "descriptor"
+    rate, done, dt = _oracle_rate(o, wl, st, budget_s)
+    out = {"value": rate, "unit": "atoms/s", "cores": threads, "kind": "oracle",
+           "sample": f"{done} of {st.n_atoms} centers (seeded random), neighbour search + {what}, "
+                     f"{dt:.1f} s on {threads} threads of {_cpu_model()} ({os.cpu_count()} logical CPUs)"}
+    if one_thread:
+        oracle.threads(1)
+        try:
+            rate1, done1, dt1 = _oracle_rate(o, wl, st, budget_s * 0.75)
+        finally:
+            oracle.threads(threads)
+        out["one_thread"] = {"value": rate1, "unit": "atoms/s", "cores": 1,
+                             "sample": f"{done1} of {st.n_atoms} centers, {dt1:.1f} s"}
+    return out
 
 
 def cc_bytes(sp, wl, nc, E, out_bytes):
@@ -224,14 +252,14 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         # the edge-block writes dominate: HBM-bound kernel
         t = kern["jacobian"] * 1e-3
         roof = {"kernel": "k_jacobian", "bound": "hbm", "achieved": alg["jacobian"] / t / 1e9, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "traffic": None if periodic else measured_traffic(wl.name, "k_jacobian"),
+                "unit": "GB/s", "traffic": None if periodic else measured_traffic(wl.name, "k_jacobian", dtype),
                 "alg_bytes_per_launch": alg["jacobian"]}
     else:
         fl = density_flops(wl, E, nc, sp.n_features)
         t = kern["density"] * 1e-3
         roof = {"kernel": "k_density", "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "traffic": measured_traffic(wl.name + ("" if mode == "derivatives" else "_" + mode),
-                                                               "k_density"), "alg_flops_per_launch": fl}
+                                                               "k_density", dtype), "alg_flops_per_launch": fl}
     roof["frac"] = roof["achieved"] / roof["peak"]
     line = {
         "metric": METRIC,
@@ -260,7 +288,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
     }
     sp.close()
     if with_cpu and mode == "derivatives" and not periodic:
-        line["cpu_baseline"] = cpu_baseline(wl, st)
+        line["cpu_baseline"] = cpu_baseline(wl, st, one_thread=wl.name in (
+            workload_by_name("water64").name, workload_by_name("water1000").name))
     return line
 
 

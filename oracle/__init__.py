@@ -78,8 +78,16 @@ def lib():
         L.oracle_num_features.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
         L.oracle_soap.restype = ctypes.c_int
         L.oracle_soap.argtypes = [vp, i64, vp, vp, vp, i64, vp, vp, vp, vp, ctypes.c_int, vp, vp, vp, vp]
+        L.oracle_threads.restype = ctypes.c_int
+        L.oracle_threads.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
+
+
+def threads(n: int = 0) -> int:
+    """Worker threads of the per-center loop (OpenMP): n > 0 sets them;
+    returns the count the next compute() uses."""
+    return int(lib().oracle_threads(int(n)))
 
 
 def _ptr(a):

@@ -32,6 +32,7 @@
  *    (n' >= n on the diagonal), then l innermost.
  */
 #include <math.h>
+#include <omp.h>
 #include <quadmath.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -392,6 +393,13 @@ static void onsite(const oracle_params *P, double *c0) {
 }
 
 /* ----------------------------------------------------------- features */
+/* Worker threads of the per-center loop: n > 0 sets them; returns the count
+ * the next oracle_soap call uses. */
+int oracle_threads(int n) {
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
+}
+
 int64_t oracle_num_features(int S, int n, int lmax) {
     int64_t F = 0;
     for (int mu = 0; mu < S; ++mu)

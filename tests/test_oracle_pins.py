@@ -662,3 +662,21 @@ def test_unknown_species_rejected(oracle_lib):
     o = oracle.OracleSOAP((1, 8), 5.0, 2, 2, 0.5)
     with pytest.raises(ValueError):
         o.compute(np.zeros((2, 3)) + [[0, 0, 0], [1, 0, 0]], np.array([1, 6]))
+
+
+def test_thread_count_does_not_change_results(oracle_lib):
+    # every center is computed on its own, so the result is the same bit for
+    # bit whatever the number of worker threads
+    s = workloads.random_small(24, 5, 3.0, species=(1, 8))
+    o = oracle.OracleSOAP((1, 8), 4.0, 3, 3, 0.5, "gto")
+    n0 = oracle.threads()
+    try:
+        assert oracle.threads(1) == 1
+        one = o.compute(s.pos64, s.Z, jacobian=True)
+        oracle.threads(max(n0, 2))
+        many = o.compute(s.pos64, s.Z, jacobian=True)
+    finally:
+        oracle.threads(n0)
+    assert oracle.threads() == n0
+    for k in ("desc", "jac"):
+        assert np.array_equal(one[k], many[k])
