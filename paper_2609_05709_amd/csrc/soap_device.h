@@ -1268,16 +1268,47 @@ __device__ __forceinline__ void store3(T *o, uint32_t Fe, uint32_t idx, V x, V y
     store_out(o + (2 * Fe + idx), z);
 }
 
+// float64 edge blocks are stored 16 bytes (two values) per lane and row.
+// For float32 output, 8- and 16-byte stores measured slower than one value
+// per lane (the per-slot decode and the strided LDS reads cost more than the
+// wider stores save), so only the float64 kernels carry this path.
+typedef double jv_f64x2 __attribute__((ext_vector_type(2)));
+template <typename T> struct Vec16;
+template <> struct Vec16<double> {
+    using type = jv_f64x2;
+    static constexpr int N = 2;
+};
+template <typename T> constexpr bool jac_vector_stores() { return sizeof(T) == 8; }
+template <typename T, typename V = typename Vec16<T>::type>
+__device__ __forceinline__ void store3v(T *o, uint32_t Fe, uint32_t idx, const V &x, const V &y, const V &z) {
+    *(V *)(o + idx) = x;
+    *(V *)(o + (Fe + idx)) = y;
+    *(V *)(o + (2 * Fe + idx)) = z;
+}
+// next slot (n, n' lw + l) of an off-diagonal pair block, nl = n_max lw
+__device__ __forceinline__ void jac_next_slot(int &a, int &tt, int &l, int nl, int lw) {
+    ++tt;
+    ++l;
+    if (l == lw) l = 0;
+    if (tt == nl) {
+        tt = 0;
+        ++a;
+    }
+}
+
 // NT, LWT: n_max and l_max + 1 fixed at compile time (0 = from P).  Three
 // resident waves per SIMD for the float32 kernel of small bases (its LDS
 // allows three workgroups per CU); larger bases keep the registers to avoid
-// spills.
-constexpr int jac_min_waves(int ab, int LWT) { return (ab == 4 && (LWT == 0 || LWT <= 7)) ? 3 : 2; }
+// spills (at l_max 6 from n_max 10 on, the three-wave budget of 168
+// registers spilled and ran ~1.4x slower than two waves).
+constexpr int jac_min_waves(int ab, int NT, int LWT) {
+    return (ab == 4 && (LWT == 0 || LWT <= 5 || (LWT == 7 && NT <= 8))) ? 3 : 2;
+}
 
 // RBF: -1 reads the radial basis from P (0..2); 3 is the compensated GTO
 template <typename PosT, typename OutT, int NT, int LWT, int RBF = -1>
-__global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
-                                                                            int W, const double *__restrict__ c_scratch,
+__global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), NT, LWT)) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
+                                                                            int W, int vec, const double *__restrict__ c_scratch,
                                                                             OutT *__restrict__ jedge) {
     using AT = OutT; // assembly precision
     using AT2 = typename Pair<AT>::type;
@@ -1315,7 +1346,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
     const int a_comp = (lane & 15) >> 2, a_e = lane & 3, kk = lane >> 4, bj = lane & 15, o_e = lane >> 4;
     const int ntile = (Sn + 15) >> 4, nj = chunks_below(lw);
     // assembly: lane pass p owns tt = lane + 64 p = n' lw + l
-    const float inv_lw = 1.0f / (float)lw;
+    const float inv_lw = 1.0f / (float)lw, inv_nl = 1.0f / (float)nl;
     const int NP = (nl + 63) >> 6;
     int tp[JAC_MAX_NP], lp[JAC_MAX_NP];
 #pragma unroll
@@ -1405,6 +1436,78 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), LWT)) void k_jacob
                 const AT2 *Be = BB + (size_t)e * nl;
                 const AT2 *Ua = U2a + (size_t)e * Sn * lw, *Ub = U2b + (size_t)e * Sn * lw;
                 OutT *o = jedge + (base + e) * 3 * Fe;
+                if constexpr (jac_vector_stores<OutT>()) if (vec) {
+                    // the same slots, a lane owning VN consecutive ones (one
+                    // 16-byte store per row); the host enables this when
+                    // n nl and tri_lw are multiples of VN and jedge is
+                    // 16-byte aligned, so every vector is aligned and whole
+                    using OV = typename Vec16<OutT>::type;
+                    constexpr int VN = Vec16<OutT>::N;
+                    // the lane index made opaque here: the slot decode below
+                    // is the same for every edge, and hoisted out of the tile
+                    // loops it would hold ~20 registers through the whole kernel
+                    int vl = lane;
+                    __asm__ volatile("" : "+v"(vl));
+                    // pairs (mu, s), mu < s
+                    for (int mu = 0; mu < s; ++mu) {
+                        const AT2 *Uma = Ua + mu * nl, *Umb = Ub + mu * nl;
+                        OutT *ob = o + mu * nnl;
+                        for (int g0 = VN * vl; g0 < nnl; g0 += 64 * VN) {
+                            int a = qdiv(g0, inv_nl), tt = g0 - a * nl, l = tt - qdiv(tt, inv_lw) * lw;
+                            OV vx, vy, vz;
+#pragma unroll
+                            for (int v = 0; v < VN; ++v) {
+                                const AT2 bb = Be[tt], q0 = Uma[a * lw + l], q1 = Umb[a * lw + l];
+                                const AT bhx = bb.y * rx, bhy = bb.y * ry, bhz = bb.y * rz;
+                                vx[v] = q0.x * bhx + q0.y * bb.x;
+                                vy[v] = q0.x * bhy + q1.x * bb.x;
+                                vz[v] = q0.x * bhz + q1.y * bb.x;
+                                jac_next_slot(a, tt, l, nl, lw);
+                            }
+                            store3v(ob, Fe, g0, vx, vy, vz);
+                        }
+                    }
+                    // diagonal pair (s, s), n' >= n, flat over (n, n', l)
+                    {
+                        OutT *ob = o + s * nnl;
+                        const AT2 *Usa = Ua + s * nl, *Usb = Ub + s * nl;
+                        for (int f0 = VN * vl; f0 < tri_lw; f0 += 64 * VN) {
+                            OV vx, vy, vz;
+#pragma unroll
+                            for (int v = 0; v < VN; ++v) {
+                                const uint32_t d = dtab[f0 + v];
+                                const int ta = d & 0xffff, tb = d >> 16;
+                                const AT2 A = Be[ta], B = Be[tb];
+                                const AT2 a0 = Usa[ta], a1 = Usb[ta], b0 = Usa[tb], b1 = Usb[tb];
+                                const AT hu = B.y * a0.x + A.y * b0.x;
+                                vx[v] = hu * rx + (B.x * a0.y + A.x * b0.y);
+                                vy[v] = hu * ry + (B.x * a1.x + A.x * b1.x);
+                                vz[v] = hu * rz + (B.x * a1.y + A.x * b1.y);
+                            }
+                            store3v(ob, Fe, f0, vx, vy, vz);
+                        }
+                    }
+                    // pairs (s, nu), nu > s
+                    for (int nu = s + 1; nu < S; ++nu) {
+                        const AT2 *Una = Ua + nu * nl, *Unb = Ub + nu * nl;
+                        OutT *ob = o + s * nnl + tri_lw + (nu - s - 1) * nnl;
+                        for (int g0 = VN * vl; g0 < nnl; g0 += 64 * VN) {
+                            int a = qdiv(g0, inv_nl), tt = g0 - a * nl, l = tt - qdiv(tt, inv_lw) * lw;
+                            OV vx, vy, vz;
+#pragma unroll
+                            for (int v = 0; v < VN; ++v) {
+                                const AT2 q0 = Una[tt], q1 = Unb[tt], bb = Be[a * lw + l];
+                                const AT ux = q0.x * rx, uy = q0.x * ry, uz = q0.x * rz;
+                                vx[v] = bb.y * ux + bb.x * q0.y;
+                                vy[v] = bb.y * uy + bb.x * q1.x;
+                                vz[v] = bb.y * uz + bb.x * q1.y;
+                                jac_next_slot(a, tt, l, nl, lw);
+                            }
+                            store3v(ob, Fe, g0, vx, vy, vz);
+                        }
+                    }
+                    continue;
+                }
                 // pairs (mu, s), mu < s
                 if (s > 0) {
 #pragma unroll

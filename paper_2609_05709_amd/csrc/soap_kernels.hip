@@ -161,7 +161,11 @@ hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool
     Params Pk = P;
     Rows Rk = R;
     int W = cfg.W;
-    void *args[] = {&Pk, &Rk, &pos, &W, &c_scratch, &jedge};
+    // float64: 16-byte vector stores when every section of an edge block is
+    // a whole number of vectors and the output is 16-byte aligned
+    const int nnl = P.n * P.n * (P.lmax + 1);
+    int vec = (f64 && nnl % 2 == 0 && P.tri_lw % 2 == 0 && ((uintptr_t)jedge & 15) == 0) ? 1 : 0;
+    void *args[] = {&Pk, &Rk, &pos, &W, &vec, &c_scratch, &jedge};
     return hipLaunchKernel(jacobian_kernel(f64, P.rbf, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args, cfg.lds, st);
 }
 

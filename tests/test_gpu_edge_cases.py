@@ -160,6 +160,38 @@ def test_bad_arguments_rejected():
     sp.close()
 
 
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+@pytest.mark.parametrize("nl,species", [((8, 6), (1, 8)), ((3, 3), (1, 6, 8)), ((4, 4), (1, 8))])
+def test_jacobian_vector_and_scalar_stores(dtype, nl, species):
+    """The edge blocks are stored as 16-byte vectors when the output is 16-byte
+    aligned and every section of a block is a whole number of vectors, else
+    one value per lane: an output view shifted by one element takes the
+    second path.  The first run is checked against the oracle, the shifted
+    one against the first."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    wl = _wl(species=species, n_max=nl[0], l_max=nl[1])
+    st = workloads.random_small(40, 13, 3.5, species=species)
+    g, _ = _compare(wl, st, dtype)
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
+    E = sp.build_neighbors(pos, torch.from_numpy(st.Z).cuda())
+    Fe = sp.n_edge_features
+    buf = torch.empty(E * 3 * Fe + 1, dtype=tdt, device="cuda")
+    jb = buf[1:].view(E, 3, Fe)
+    assert jb.data_ptr() % 16 != 0
+    sp.derivatives(jac_edge=jb)
+    torch.cuda.synchronize()
+    jb = jb.cpu().double().numpy()
+    sp.close()
+    tol = 1e-6 if dtype == "float32" else 1e-13
+    for c in range(st.n_atoms):
+        r0, r1 = int(g["row"][c]), int(g["row"][c + 1])
+        a = g["jedge"][c]
+        assert np.abs(jb[r0:r1] - a).max(initial=0.0) <= tol * max(np.abs(a).max(initial=0.0), 1e-30), c
+
+
 def test_repeatable_bitwise():
     wl = workloads.WATER64
     st = wl.structure()
