@@ -919,8 +919,11 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
     double *X = wv.take((size_t)W * stage_x_doubles(P, lgc, lg1));
 
     // the coefficient entries this lane owns: (a, lm) = ent / Lg, ent % Lg;
-    // oC: its offset a L + lm in a coefficient block of one species
-    int oY[KE], oB[KE], oC[KE];
+    // oC: its offset a L + lm in a coefficient block of one species (unsigned,
+    // so the gradient stores take the scalar-base + 32-bit-offset form instead
+    // of per-lane 64-bit addresses, which the compiler hoists and spills)
+    int oY[KE], oB[KE];
+    uint32_t oC[KE];
     bool own[KE];
 #pragma unroll
     for (int k = 0; k < KE; ++k) {
@@ -928,7 +931,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
         own[k] = e < nL;
         const int a = e / Lg, lmg = e - a * Lg;
         const int lm = lm0 + (own[k] ? lmg : 0);
-        oC[k] = a * Lfull + lm;
+        oC[k] = (uint32_t)(a * Lfull + lm);
         int l = (int)sqrtf((float)lm);
         while (l * l > lm) --l;
         while ((l + 1) * (l + 1) <= lm) ++l;
@@ -1017,8 +1020,16 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                     const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
                     const ST *Ye = YY + e * yl.es;
                     const ST2 *Be = BB + e * nlc;
-                    // this edge's block of the coefficient Jacobian: [3][n][L]
-                    OutT *je = CCJ ? jc_edge + (size_t)(rb0 + off + e) * 3 * n * Lfull : nullptr;
+                    // this edge's block of the coefficient Jacobian: [3][n][L],
+                    // one wave-uniform base per row.  The base is made opaque:
+                    // strength-reduced over the edges, it became one 64-bit
+                    // pointer per lane and entry, which spilled.
+                    OutT *je = nullptr;
+                    if (CCJ) {
+                        je = jc_edge + (size_t)(rb0 + off + e) * 3 * n * Lfull;
+                        __asm__ volatile("" : "+s"(je));
+                    }
+                    OutT *const je1 = je + (size_t)n * Lfull, *const je2 = je + 2 * (size_t)n * Lfull;
 #pragma unroll
                     for (int k = 0; k < KE; ++k) {
                         if (!own[k]) continue;
@@ -1036,8 +1047,8 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                             acc[k][3] += gz;
                             if (CCJ) {
                                 store_out(je + oC[k], gx);
-                                store_out(je + (n * Lfull + oC[k]), gy);
-                                store_out(je + (2 * n * Lfull + oC[k]), gz);
+                                store_out(je1 + oC[k], gy);
+                                store_out(je2 + oC[k], gz);
                             }
                         } else {
                             acc[k][0] += bx * (double)Ye[oY[k]];
