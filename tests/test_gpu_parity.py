@@ -49,6 +49,37 @@ def full_check(wl, dtype, sample=None, seed=0):
     return ed.max(), ej
 
 
+def all_centers_check(wl, dtype, batch=512):
+    """Every center and every block; the oracle's Jacobian is computed and
+    compared in batches of centers to bound its memory."""
+    st = structure(wl)
+    print(f"[parity] {wl.name} {dtype} all centers, atoms={st.n_atoms}", flush=True)
+    n = st.n_atoms
+    g = gpu_run(wl, st, dtype)
+    o = oracle_for(wl)
+    check_rows(g, st, wl.r_cut, np.arange(n), wl.species)
+    ed = row_errors(g["desc"], o.compute(st.pos64, st.Z)["desc"]).max()
+    ej = 0.0
+    for b0 in range(0, n, batch):
+        idx = np.arange(b0, min(n, b0 + batch))
+        ref = o.compute(st.pos64, st.Z, centers=idx, jacobian=True)
+        ej = max(ej, jacobian_errors(g, ref, st, wl.species, idx.tolist(), idx))
+        del ref
+    print(f"[parity] {wl.name} {dtype} all centers: desc {ed:.2e}  jac {ej:.2e}  E={g['E']}", flush=True)
+    assert ed < TOL[dtype]
+    assert ej < TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_water1000_gto_n8l6_all_centers(dtype):
+    all_centers_check(workloads.WATER1000, dtype)
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_chno4096_poly_n10l10_all_centers(dtype):
+    all_centers_check(workloads.CHNO4096, dtype)
+
+
 @pytest.mark.parametrize("dtype", ["float32", "float64"])
 def test_water64_gto_full(dtype):
     full_check(workloads.WATER64, dtype)
