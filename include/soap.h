@@ -245,7 +245,10 @@ int soap_compute_averaged(soap_ctx *ctx, int32_t mode, void *desc_dev, void *str
  *                                      is soap_feature_map(species(j)));
  *   jac_self_dev [n_centers][3][F]     d p_i / d r_i = - sum_j d p_i / d r_j.
  * All derivatives not stored are exactly zero (atoms outside the cutoff,
- * features whose pair lacks species(j)).  Errors: SOAP_ESTATE, SOAP_ENOMEM,
+ * features whose pair lacks species(j)).  Any element alignment works; in
+ * float64 mode a 16-byte aligned jac_edge_dev is written with 16-byte stores
+ * (faster) when both section lengths n_max^2 (l_max+1) and
+ * n_max (n_max+1)/2 (l_max+1) are even.  Errors: SOAP_ESTATE, SOAP_ENOMEM,
  * SOAP_EHIP.
  */
 int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *jac_self_dev, void *stream);
