@@ -580,6 +580,13 @@ static int build_rows(soap_ctx *c, int64_t n_atoms, int64_t center_bound, const 
                    n_centers, centers_dev, c->r_cut, row, st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
     c->work_epoch = 0; // the density work counters were zeroed with the flags
+    // With a rows buffer from an earlier build, the short rows are packed
+    // before the host reads the total: the GPU works through the round trip.
+    // k_pack writes nothing if the total exceeds the buffer; it runs again
+    // below once the buffer has grown.
+    const int64_t cap0 = c->b_cols.p ? (int64_t)(c->b_cols.cap / 4) : 0;
+    if (cap0 > 0 && (e = nbr_pack(w, n_centers, row, c->b_cols.as<int32_t>(), cap0, st)) != hipSuccess)
+        return hip_fail(c, e, "neighbour rows");
     // flags[0..3] and the total degree (int64 at flags + 4) in one copy
     if ((e = hipMemcpyAsync(c->h_flags, w.flags, 24, hipMemcpyDeviceToHost, st)) != hipSuccess ||
         (e = hipStreamSynchronize(st)) != hipSuccess)
@@ -591,10 +598,11 @@ static int build_rows(soap_ctx *c, int64_t n_atoms, int64_t center_bound, const 
     if (bad & 2) return fail(c, SOAP_EINVAL, "a center index is out of range");
     if (maxdeg > MAX_DEGREE)
         return fail(c, SOAP_ECAPACITY, "a center has %d neighbours (limit %d)", maxdeg, MAX_DEGREE);
+    const bool packed = cap0 > 0 && E <= cap0;
     if ((e = c->b_cols.ensure(4 * (size_t)std::max<int64_t>(E, 1))) != hipSuccess)
         return hip_fail(c, e, "hipMalloc(neighbour rows)");
-    e = nbr_phase2(w, n_atoms, pos_dev, f64, n_centers, centers_dev, c->r_cut, row, n_long > 0,
-                   c->b_cols.as<int32_t>(), st);
+    e = nbr_phase2(w, n_atoms, pos_dev, f64, n_centers, centers_dev, c->r_cut, row, n_long > 0, packed,
+                   c->b_cols.as<int32_t>(), (int64_t)(c->b_cols.cap / 4), st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour rows");
     *E_out = E;
     return SOAP_OK;

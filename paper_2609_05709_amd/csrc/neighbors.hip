@@ -286,11 +286,13 @@ __global__ __launch_bounds__(64 * NBR_WAVES) void k_collect(
 
 // CSR rows from the fixed-capacity slots; rows longer than TCAP are left to
 // k_collect_long.
+// cap: entries of cols; nothing is written if the rows need more
 __global__ __launch_bounds__(256) void k_pack(int64_t nc, const int64_t *__restrict__ row_ptr,
-                                              const int32_t *__restrict__ slots, int32_t *__restrict__ cols) {
+                                              const int32_t *__restrict__ slots, int32_t *__restrict__ cols,
+                                              int64_t cap) {
     const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
-    if (c >= nc) return;
+    if (c >= nc || row_ptr[nc] > cap) return;
     const int64_t r0 = row_ptr[c];
     const int dg = (int)(row_ptr[c + 1] - r0);
     if (dg > TCAP) return;
@@ -750,12 +752,19 @@ hipError_t map_edges(int64_t E, const int32_t *cols, const int32_t *map, const i
     return hipGetLastError();
 }
 
+hipError_t nbr_pack(const NbrWork &w, int64_t nc, const int64_t *row_ptr, int32_t *cols, int64_t cap,
+                    hipStream_t st) {
+    if (nc <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_pack, dim3(blocks_for(nc, 4)), dim3(256), 0, st, nc, row_ptr, w.slots, cols, cap);
+    return hipGetLastError();
+}
+
 hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,
-                      const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, int32_t *cols,
-                      hipStream_t st) {
+                      const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, bool packed,
+                      int32_t *cols, int64_t cap, hipStream_t st) {
     (void)n_atoms;
     const Geometry g = geometry(w, r_cut);
-    hipLaunchKernelGGL(k_pack, dim3(blocks_for(nc, 4)), dim3(256), 0, st, nc, row_ptr, w.slots, cols);
+    if (!packed) hipLaunchKernelGGL(k_pack, dim3(blocks_for(nc, 4)), dim3(256), 0, st, nc, row_ptr, w.slots, cols, cap);
     if (long_rows) {
         if (pos64)
             hipLaunchKernelGGL(k_collect_long<double>, dim3((unsigned)nc), dim3(64), 0, st, nc, centers,

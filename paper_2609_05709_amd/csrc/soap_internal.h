@@ -103,10 +103,16 @@ hipError_t map_edges(int64_t E, const int32_t *cols, const int32_t *map, const i
 hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, int64_t center_bound, const void *pos, bool pos64,
                       const int32_t *Z, const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers,
                       double r_cut, int64_t *row_ptr, hipStream_t st);
-// long_rows: some row is longer than TCAP (flags[2] > 0)
+// rows of up to TCAP neighbours from their slots into cols (cap entries);
+// writes nothing if the rows need more than cap, so it may run before the
+// host has read the total
+hipError_t nbr_pack(const NbrWork &w, int64_t nc, const int64_t *row_ptr, int32_t *cols, int64_t cap,
+                    hipStream_t st);
+// long_rows: some row is longer than TCAP (flags[2] > 0); packed: nbr_pack
+// has already written the short rows
 hipError_t nbr_phase2(const NbrWork &w, int64_t n_atoms, const void *pos, bool pos64, int64_t nc,
-                      const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, int32_t *cols,
-                      hipStream_t st);
+                      const int32_t *centers, double r_cut, const int64_t *row_ptr, bool long_rows, bool packed,
+                      int32_t *cols, int64_t cap, hipStream_t st);
 
 // ---- descriptor kernels (soap_kernels.hip) ----
 struct DensityLaunch {

@@ -235,6 +235,28 @@ def test_repeated_calls_on_one_neighbour_list():
     fresh.close()
 
 
+def test_rebuilds_alternating_small_and_large():
+    """One context rebuilt for a small structure, then a larger one whose
+    rows no longer fit the rows buffer (the rows packed before the host read
+    the edge count are then packed again), and back: each time the rows and
+    the outputs equal a fresh context's."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    wl = workloads.WATER64
+    small, big = workloads.random_small(40, 5, 4.0, species=(1, 8)), wl.structure()
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    for st in (small, big, small, big, big):
+        pos, Z = torch.from_numpy(st.pos).cuda(), torch.from_numpy(st.Z).cuda()
+        fresh = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+        assert sp.build_neighbors(pos, Z) == fresh.build_neighbors(pos, Z)
+        for x, y in zip(sp.neighbors(), fresh.neighbors()):
+            assert torch.equal(x, y)
+        for x, y in zip(sp.derivatives(), fresh.derivatives()):
+            assert torch.equal(x, y)
+        fresh.close()
+    sp.close()
+
+
 def test_dense_scatter_matches_blocks():
     import torch
     from paper_2609_05709_amd.soap import Soap
