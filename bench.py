@@ -9,8 +9,14 @@ Default workload: the 3000-atom water cluster (1000 H2O), GTO basis,
 r_cut 6 A, sigma 0.5 A, n_max 8, l_max 6, descriptor + Jacobian, float32
 outputs.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload NAME] [--dtype float32|float64]
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--dtype float32|float64] [--arith mixed|fp64]
                   [--mode derivatives|cc|inner|outer] [--periodic] [--grid OUT.jsonl] [--no-cpu-baseline]
+
+Without --workload the line also carries, under "configs", the same headline
+with float64 internal arithmetic, the 64-water cluster (GTO n4 l4), the CHNO
+condensed phase (polynomial n10 l10) and the 1,000,002-atom water descriptor
+(GTO n8 l6), each with its ms/step, atoms/s, kernel and step roofline
+fractions and (unless --no-cpu-baseline) the oracle's baseline.
 
 --mode picks the output of a Jacobian workload: the descriptor + Jacobian
 (default), the coefficients and their Jacobian ("cc"), or one averaged
@@ -72,6 +78,46 @@ def density_flops(wl, E, n_centers, F):
     per_edge = 3 * L + 2 * n * n * (l + 1) + n * (l + 1) + 2 * n * L
     per_center = sum(2 * (2 * ll + 1) for ll in range(l + 1)) * (F // (l + 1))
     return E * per_edge + n_centers * per_center
+
+
+def step_work(wl, nc, E, F, Fe, out_bytes, jac, quad_n=64):
+    """Algorithmic work of one step (the method's own work, no structural
+    zeros): float64-equivalent operations and HBM bytes.  Per edge: real
+    solid harmonics (~3 flops per (l, m); ~12 with gradients), the radial
+    factors (GTO: 2 n^2 (l+1) flops per factor and n (l+1) exponentials;
+    polynomial quadrature: 2 n Q (l+1) per factor and Q (l+2) Bessel values
+    plus 2 Q exponentials; Laplace form: 8 n (n+3) Clenshaw flops and ~10 per
+    (n, l)), the projection 2 n L; with the Jacobian the radial factor's
+    derivative (the radial flops again), the precontraction 8 S n L, the
+    assembly 12 (F_e + F_ss) and the center block 3 F_e.  Per center: the
+    power spectrum, 2 (2l+1) flops per feature.  Bytes: the outputs."""
+    n, l, S = wl.n_max, wl.l_max, len(wl.species)
+    L = (l + 1) ** 2
+    if wl.rbf == "gto":
+        radial = 2 * n * n * (l + 1) + n * (l + 1)
+    elif wl.rbf == "polynomial":
+        radial = 2 * n * quad_n * (l + 1) + quad_n * (l + 2) + 2 * quad_n
+    else:
+        radial = 8 * n * (n + 3) + 10 * n * (l + 1)
+    if jac:
+        F_ss = (l + 1) * n * (n + 1) // 2
+        per_edge = 12 * L + 2 * radial + 2 * n * L + 8 * S * n * L + 12 * (Fe + F_ss) + 3 * Fe
+    else:
+        per_edge = 3 * L + radial + 2 * n * L
+    per_center = sum(2 * (2 * ll + 1) for ll in range(l + 1)) * (F // (l + 1))
+    flops = E * per_edge + nc * per_center
+    nbytes = (nc * F + (3 * nc * F + 3 * E * Fe if jac else 0)) * out_bytes
+    return flops, nbytes
+
+
+def step_roofline(flops, nbytes, ms_step):
+    """The binding roofline of the whole step: floor = max(bytes / HBM peak,
+    flops / FP64 peak); frac = floor / measured step time."""
+    t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
+    t_alu = flops / (FP64_PEAK_TFLOPS * 1e12)
+    floor = max(t_hbm, t_alu)
+    return {"bound": "hbm" if t_hbm >= t_alu else "alu", "floor_ms": floor * 1e3, "alg_flops": flops,
+            "alg_bytes": nbytes, "frac": floor / (ms_step * 1e-3)}
 
 
 def measured_traffic(workload_name, kernel, output):
@@ -141,12 +187,44 @@ def _cpu_model():
     return "unknown"
 
 
+LARGE_SAMPLE = 20000  # centers timed for the oracle on structures above LARGE_ATOMS
+LARGE_ATOMS = 100000
+
+
+def _cpu_baseline_large(o, wl, st, threads):
+    """Large structures: the oracle's uniform-grid neighbour search over all
+    atoms (timed whole), then the descriptor of a seeded sample of centers
+    on those rows, scaled linearly to every center (each center's work is
+    independent given its row)."""
+    import oracle
+    t0 = time.perf_counter()
+    row, cols = oracle.neighbors_grid(st.pos64, wl.r_cut)
+    t_nb = time.perf_counter() - t0
+    rng = np.random.default_rng(12345)
+    idx = np.sort(rng.choice(st.n_atoms, size=min(LARGE_SAMPLE, st.n_atoms), replace=False))
+    deg = row[idx + 1] - row[idx]
+    rs = np.zeros(len(idx) + 1, dtype=np.int64)
+    rs[1:] = np.cumsum(deg)
+    cs = np.concatenate([cols[row[i]:row[i + 1]] for i in idx])
+    t0 = time.perf_counter()
+    o.compute(st.pos64, st.Z, centers=idx, nb=(rs, cs), jacobian=wl.jacobian)
+    t_c = time.perf_counter() - t0
+    total = t_nb + t_c * st.n_atoms / len(idx)
+    return {"value": st.n_atoms / total, "unit": "atoms/s", "cores": threads, "kind": "oracle",
+            "sample": f"uniform-grid neighbour search over all {st.n_atoms} atoms ({t_nb:.1f} s), then the "
+                      f"{'descriptor + Jacobian' if wl.jacobian else 'descriptor'} of {len(idx)} seeded random "
+                      f"centers ({t_c:.1f} s) scaled linearly to all centers: {total:.0f} s estimated; "
+                      f"{threads} threads of {_cpu_model()} ({os.cpu_count()} logical CPUs)"}
+
+
 def cpu_baseline(wl, st, budget_s=12.0, one_thread=False):
     """The oracle as it stands, on the host cores, over a bounded sample of
     centers; with one_thread, also a sample on a single thread."""
     import oracle
     o = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
     threads = oracle.threads()
+    if st.n_atoms > LARGE_ATOMS:
+        return _cpu_baseline_large(o, wl, st, threads)
     what = "descriptor + Jacobian" if wl.jacobian else "descriptor"
     rate, done, dt = _oracle_rate(o, wl, st, budget_s)
     out = {"value": rate, "unit": "atoms/s", "cores": threads, "kind": "oracle",
@@ -171,14 +249,24 @@ def cc_bytes(sp, wl, nc, E, out_bytes):
     return (nc * S * nL + E * 3 * nL + nc * 3 * S * nL) * out_bytes
 
 
-def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False):
+# what the timed path computes in, per output precision and internal arithmetic
+DTYPE_LABEL = {
+    ("float32", "mixed"): "mixed: f64 geometry/radial sums/accumulation/MFMA, f32 staging and final assembly",
+    ("float32", "fp64"): "f64 (outputs rounded to f32)",
+    ("float64", "mixed"): "f64",
+    ("float64", "fp64"): "f64",
+}
+
+
+def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False, arith="mixed",
+        cpu_budget_s=12.0):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
     tdt = torch.float64 if dtype == "float64" else torch.float32
     out_bytes = 8 if dtype == "float64" else 4
     dev = torch.device("cuda:0")
-    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype, arith=arith)
     if periodic:
         lo = st.pos.min(axis=0) - np.float32(0.8)
         st = type(st)((st.pos - lo).astype(np.float32), st.Z, st.radius, st.draws, dict(st.recipe, periodic=True))
@@ -272,12 +360,13 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64",
+        "dtype": DTYPE_LABEL[(dtype, arith)],
         "data": "synthetic",
         "config": {"workload": wl.name + ("" if mode == "derivatives" else "_" + mode) + ("_periodic" if periodic else ""),
                    "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
                    "l_max": wl.l_max, "r_cut": wl.r_cut, "sigma": wl.sigma, "species": list(wl.species),
-                   "output": dtype, "jacobian": jac or mode == "cc", "mode": mode, "features": sp.n_features,
+                   "output": dtype, "arith": arith, "jacobian": jac or mode == "cc", "mode": mode,
+                   "features": sp.n_features,
                    "edge_features": sp.n_edge_features},
         "kernel_ms": kern,
         "kernel_timing": "HIP events per segment over a second pass of the K steps",
@@ -286,11 +375,26 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         "wall_s": wall,
         "roofline": roof,
     }
+    if mode == "derivatives":
+        fl, nb = step_work(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, jac)
+        line["step_roofline"] = step_roofline(fl, nb, ms_step)
     sp.close()
     if with_cpu and mode == "derivatives" and not periodic:
-        line["cpu_baseline"] = cpu_baseline(wl, st, one_thread=wl.name in (
+        line["cpu_baseline"] = cpu_baseline(wl, st, budget_s=cpu_budget_s, one_thread=wl.name in (
             workload_by_name("water64").name, workload_by_name("water1000").name))
     return line
+
+
+# the other workloads of the default line: the 64-water cluster, the CHNO
+# condensed phase (polynomial basis) and the million-atom water descriptor
+EXTRA_WORKLOADS = ("water64", "chno4096", "water1m")
+
+
+def summary(line):
+    """The per-workload figures carried in the default line's "configs"."""
+    keep = ("value", "unit", "ms_per_step", "dtype", "config", "kernel_ms", "roofline", "step_roofline",
+            "cpu_baseline", "steps", "warmup")
+    return {k: line[k] for k in keep if k in line}
 
 
 def main():
@@ -298,8 +402,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="water1000")
+    ap.add_argument("--workload", default=None,
+                    help="one workload only (default: the 3000-atom water headline, plus the other workloads and "
+                         "the float64-arithmetic headline in the line's \"configs\")")
     ap.add_argument("--dtype", default="float32", choices=["float32", "float64"])
+    ap.add_argument("--arith", default="mixed", choices=["mixed", "fp64"],
+                    help="internal arithmetic of the float32 mode: float32 staging and assembly, or float64 throughout")
     ap.add_argument("--mode", default="derivatives", choices=["derivatives", "cc", "inner", "outer"])
     ap.add_argument("--periodic", action="store_true")
     ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for every radial basis; write JSONL here")
@@ -323,8 +431,23 @@ def main():
                 print(f"{wl.name}: {line['value']:.4g} atoms/s, {line['ms_per_step']:.3f} ms, "
                       f"jac {line['roofline']['frac']:.3f} of HBM", flush=True)
         return
-    wl = workload_by_name(a.workload)
-    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic)
+    wl = workload_by_name(a.workload or "water1000")
+    line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic,
+               arith=a.arith)
+    if a.workload is None and a.mode == "derivatives" and not a.periodic:
+        # the same headline in the paper's arithmetic (float64 internally,
+        # float32 outputs), and the other workloads, each with its own
+        # roofline fraction and oracle baseline
+        extra = {}
+        if a.dtype == "float32" and a.arith == "mixed":
+            extra[wl.name + "_arith_fp64"] = summary(run(wl, a.steps, a.warmup, a.dtype, with_cpu=False,
+                                                         arith="fp64"))
+        for name in EXTRA_WORKLOADS:
+            xl = workload_by_name(name)
+            extra[xl.name] = summary(run(xl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline,
+                                         arith=a.arith, cpu_budget_s=8.0))
+            print(f"[bench] {xl.name}: {extra[xl.name]['ms_per_step']:.3f} ms/step", file=sys.stderr, flush=True)
+        line["configs"] = extra
     print(json.dumps(line), flush=True)
 
 

@@ -32,8 +32,17 @@
  *     `stream` has completed.  `stream` is a hipStream_t (NULL = the default
  *     stream).  All calls are asynchronous on `stream` unless stated.
  *   - dtype (option "dtype"): SOAP_FP32 (default) = float32 positions and
- *     outputs; SOAP_FP64 = float64 positions and outputs.  Internal
- *     arithmetic is float64 in both modes.
+ *     outputs; SOAP_FP64 = float64 positions and outputs.  The float64 mode
+ *     computes everything in float64.  The float32 mode computes the edge
+ *     geometry, radial sums, projection sums, power spectrum, center block
+ *     and the Jacobian's precontraction in float64, but rounds the staged
+ *     harmonics and radial factors to float32 before the projection's
+ *     products, and the precontraction results and radial factors to
+ *     float32 before the Jacobian's final two-term assembly, which then
+ *     runs in float32.  Option "arith" = SOAP_ARITH_FP64 keeps float64
+ *     through every step in the float32 mode too and rounds only the
+ *     stored outputs (the paper's choice, Sec. 3.1: float64 internal
+ *     arithmetic, outputs cast at the end).
  *   - Every function returns SOAP_OK or a negative status; on error nothing
  *     is enqueued and soap_last_error() describes the cause.  No function
  *     aborts or throws across this interface.
@@ -72,6 +81,14 @@ typedef struct soap_ctx soap_ctx;
 /* Largest neighbour count per center the neighbour builder accepts. */
 #define SOAP_MAX_DEGREE 2048
 
+/* internal arithmetic of the float32 mode (option "arith") */
+#define SOAP_ARITH_MIXED 0 /* float32 staging and final assembly (default) */
+#define SOAP_ARITH_FP64 1  /* float64 throughout, outputs rounded at the store */
+
+/* outputs a center batch plan is sized for (soap_plan_batches) */
+#define SOAP_BATCH_DESCRIPTOR 0
+#define SOAP_BATCH_DERIVATIVES 1
+
 /*
  * Create a context on the current HIP device.  Arguments follow the paper's
  * problem statement (Sec. 3.1: r_cut, n_max, l_max, sigma, rbf, species).
@@ -88,17 +105,28 @@ typedef struct soap_ctx soap_ctx;
  *               on-site term of a center, and of a neighbour at distance 0,
  *               stays the quadrature's).
  * Basis constants (Loewdin coefficients, quadrature tables) are computed here
- * on the host in 113-bit floating point and uploaded once.
+ * on the host in 113-bit floating point and uploaded once.  The kernels keep
+ * a center's coefficients on chip: a basis whose descriptor path does not
+ * fit is rejected here (SOAP_EINVAL); one that fits the descriptor path but
+ * not a Jacobian path (large S n_max, e.g. 16 species at n_max 8, l_max 6)
+ * is accepted, and soap_derivatives / soap_coefficient_derivatives then
+ * return SOAP_EINVAL.
  * Errors: SOAP_EINVAL, SOAP_ENOMEM, SOAP_EHIP.  *out is NULL on error.
  */
 int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32_t n_max, int32_t l_max,
                 double sigma, int32_t rbf, soap_ctx **out);
 
 /*
- * Set an option.  Keys:
+ * Set an option of the constructor (Sec. 3.1 lists the constructor's
+ * arguments: the output dtype, the quadrature order of the polynomial
+ * radial integral, and the per-segment profiler).  Keys:
  *   "dtype"  : SOAP_FP32 or SOAP_FP64 (default SOAP_FP32);
+ *   "arith"  : SOAP_ARITH_MIXED (default) or SOAP_ARITH_FP64, the internal
+ *              arithmetic of the float32 mode (see dtype above; the float64
+ *              mode is float64 throughout either way);
  *   "quad_n" : Gauss-Legendre order for the polynomial basis, 8..256
- *              (default 64); rebuilds the quadrature table;
+ *              (default 64; Sec. 3.1, the fixed Gauss-Legendre rule on
+ *              [0, r_cut]); rebuilds the quadrature table;
  *   "timing" : 1 = record HIP events around every segment of later calls
  *              (see soap_timing), 0 = off (default).
  * Options take effect for calls made after this one; changing "dtype"
@@ -254,9 +282,55 @@ int soap_compute_averaged(soap_ctx *ctx, int32_t mode, void *desc_dev, void *str
 int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *jac_self_dev, void *stream);
 
 /*
+ * Center batches (Sec. 3.3: the work is split into batches of centers of one
+ * structure, and on one device the batches bound the memory of a single
+ * call, so that a structure of any size streams through the device).  The
+ * neighbour rows of every center are built once per structure by
+ * soap_build_neighbors (4 bytes per edge); the batch calls below compute the
+ * outputs of centers [first, first + count) of that list, indexed from the
+ * batch's first center and first edge:
+ *   soap_compute_batch     : desc_dev[count][F], as soap_compute;
+ *   soap_derivatives_batch : desc_dev[count][F], jac_edge_dev[E_b][3][F_e],
+ *                            jac_self_dev[count][3][F], as soap_derivatives,
+ *                            where E_b = edge_first[k+1] - edge_first[k] of
+ *                            the batch (soap_plan_batches), i.e. the edges of
+ *                            its centers' rows; jac_edge_dev may be NULL only
+ *                            when E_b = 0.
+ * Each center's outputs are bitwise identical to those of the single call
+ * over all centers (the per-center sums run in a fixed order).  The
+ * Jacobian's float64 coefficient scratch (32 S n_max (l_max+1)^2 bytes per
+ * center) is sized per batch.  count = 0 enqueues nothing.  Errors:
+ * SOAP_EINVAL (range outside the centers, NULL outputs), SOAP_ESTATE,
+ * SOAP_ENOMEM, SOAP_EHIP.
+ */
+int soap_compute_batch(soap_ctx *ctx, int64_t first, int64_t count, void *desc_dev, void *stream);
+int soap_derivatives_batch(soap_ctx *ctx, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
+                           void *jac_self_dev, void *stream);
+
+/*
+ * Split the centers of the neighbour list into consecutive batches whose
+ * memory stays within budget_bytes: for `what` = SOAP_BATCH_DESCRIPTOR the
+ * descriptor rows; for SOAP_BATCH_DERIVATIVES the descriptor rows, center
+ * blocks, neighbour blocks and the library's coefficient scratch of the
+ * batch.  Greedy in center order.  On return *n_batches_out = the number of
+ * batches B; if center_first (host, max_batches + 1 entries) is not NULL it
+ * receives the first center of each batch and center_first[B] = n_centers,
+ * and edge_first (host, may be NULL, max_batches + 1 entries) the first edge
+ * of each batch and edge_first[B] = E.  Pass center_first = NULL to count
+ * only.  Reads the row offsets back from the device (synchronous).
+ * Errors: SOAP_EINVAL, SOAP_ESTATE, SOAP_ECAPACITY (a single center exceeds
+ * the budget, or B > max_batches), SOAP_EHIP.
+ */
+int soap_plan_batches(soap_ctx *ctx, int32_t what, int64_t budget_bytes, int64_t max_batches,
+                      int64_t *center_first, int64_t *edge_first, int64_t *n_batches_out);
+
+/*
  * Expand a soap_derivatives result into the dense layout
- * dense_dev[n_centers][n_atoms][3][F] (dtype), zeros included.  Intended for
- * small structures (the dense array grows as n_centers * n_atoms).  With a
+ * dense_dev[n_centers][n_atoms][3][F] (dtype), zeros included: the
+ * derivative tensor of shape (centers, atoms, 3, features) that the paper's
+ * derivatives() returns (Sec. 3, the output layout shared with DScribe; the
+ * dense (center, atom) blocks of Eq. (powerspectrum-derivative)).  Intended
+ * for small structures (the dense array grows as n_centers * n_atoms).  With a
  * periodic cell the blocks of all images of an atom (and of the center's
  * own images) are summed into that atom's block: the derivative by the
  * atom's position, all of its images moving with it.

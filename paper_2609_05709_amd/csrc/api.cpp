@@ -54,7 +54,7 @@ struct soap_ctx {
     int device = 0;
     std::vector<int32_t> Z; // sorted
     double r_cut = 0, sigma = 0;
-    int n = 0, lmax = 0, rbf = 0, Q = 64, dtype = SOAP_FP32;
+    int n = 0, lmax = 0, rbf = 0, Q = 64, dtype = SOAP_FP32, arith = SOAP_ARITH_MIXED;
     int64_t F = 0, Fe = 0;
     int nq_full = 0;
     std::vector<uint32_t> fq;
@@ -72,7 +72,7 @@ struct soap_ctx {
     PeriodicCell cell{};
     int64_t n_ext = 0;
     DevBuf b_img_lohi, b_img_cnt, b_img_start, b_pos_ext, b_Z_ext, b_map_atom, b_map_img, b_iota;
-    uint64_t work_epoch = 0; // density work-counter increments since the counters were zeroed
+    WorkBase work_epoch{}; // per l-group: density work-counter increments since the counters were zeroed
     int32_t *h_flags = nullptr; // pinned: [0..3] flags, int64 E at byte 16, int64 image count at byte 32
     // state of the last neighbour build
     bool have_rows = false;
@@ -80,8 +80,12 @@ struct soap_ctx {
     const void *pos = nullptr;
     const int32_t *Zdev = nullptr, *centers = nullptr;
     bool built_f64 = false;
+    bool ar64 = false; // float64 staging and assembly with float32 outputs (option "arith")
     // launch configuration
     DensityLaunch dens_cfg[3]{};  // [density kernel mode: descriptor, Jacobian, coefficient Jacobian]
+    // whether each kernel's on-chip plan fits this basis: a basis too large for
+    // one path still serves the others (the descriptor path is required)
+    bool dens_ok[3] = {false, false, false}, out_ok = false, jac_ok = false;
     JacLaunch jac_cfg{};
     OutPlan out_plan{};
     int groups[3] = {1, 1, 1};
@@ -150,7 +154,7 @@ void build_feature_tables(soap_ctx *c) {
 // its LDS fits the budget (the LDS share of a workgroup at the occupancy the
 // kernel's registers allow); W = edges per wave iteration, the widest that
 // fits.
-int plan_groups(const Params &P, int jac, bool f64, size_t budget, int *lgrp, int *ngroups, int *W_out,
+int plan_groups(const Params &P, int jac, bool st64, size_t budget, int *lgrp, int *ngroups, int *W_out,
                 size_t *lds_out) {
     const int lw = P.lmax + 1;
     for (int G = 1; G <= lw; ++G) {
@@ -173,7 +177,7 @@ int plan_groups(const Params &P, int jac, bool f64, size_t budget, int *lgrp, in
         for (int W : {8, 4, 2, 1}) {
             size_t worst = 0;
             for (int k = 0; k < G; ++k)
-                worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], W, f64));
+                worst = std::max(worst, density_lds_bytes(P, jac, bounds[k], bounds[k + 1], W, st64));
             if (worst <= budget || (W == 1 && worst <= LDS_HARD_LIMIT)) {
                 for (int k = 0; k <= G; ++k) lgrp[k] = bounds[k];
                 *ngroups = G;
@@ -204,17 +208,22 @@ int plan_launches(soap_ctx *c) {
     int ncu = 256;
     (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
     const bool f64d = c->dtype == SOAP_FP64;
+    c->ar64 = !f64d && c->arith == SOAP_ARITH_FP64;
+    const bool ar64 = c->ar64, st64 = f64d || ar64;
     for (int mode = 0; mode < 3; ++mode) {
         const int jac = mode != 0; // modes 1 and 2 stage gradients
         int *lgrp = c->lgrp[mode], *G = &c->groups[mode];
         // workgroups per CU the registers allow (no LDS), and the LDS share of each
         auto plan = [&](bool hi, int *lg, int *g, int *w, size_t *ld) {
-            const int by_regs = std::max(1, density_blocks_per_cu(f64d, mode, P.rbf, hi, 0));
+            const int by_regs = std::max(1, density_blocks_per_cu(f64d, ar64, mode, P.rbf, hi, 0));
             const size_t budget = std::min(LDS_HARD_LIMIT, (size_t)(159 * 1024) / (size_t)by_regs);
-            return plan_groups(P, jac, f64d, budget, lg, g, w, ld) == 0;
+            return plan_groups(P, jac, st64, budget, lg, g, w, ld) == 0;
         };
-        if (!plan(false, lgrp, G, &Wd, &lds))
-            return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
+        c->dens_ok[mode] = plan(false, lgrp, G, &Wd, &lds);
+        if (!c->dens_ok[mode]) {
+            if (mode == 0) return fail(c, SOAP_EINVAL, "basis too large for the density kernel's on-chip memory");
+            continue;
+        }
         bool hi = false;
         if (density_has_high(mode, P.rbf)) {
             // more workgroups per CU hide more latency, but split the LDS
@@ -236,27 +245,26 @@ int plan_launches(soap_ctx *c) {
         c->dens_cfg[mode].W = Wd;
         c->dens_cfg[mode].lds = lds;
         c->dens_cfg[mode].hi = hi;
-        const int per_cu = density_blocks_per_cu(f64d, mode, P.rbf, hi, lds);
+        const int per_cu = density_blocks_per_cu(f64d, ar64, mode, P.rbf, hi, lds);
         c->dens_cfg[mode].blocks = std::max(1, ncu * per_cu / *G);
     }
-    if (plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) != 0)
-        return fail(c, SOAP_EINVAL, "basis too large for the output kernel's on-chip memory");
+    c->out_ok = plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) == 0;
     // Jacobian kernel: W edges per wave tile.  The most resident waves per CU
     // first (latency hiding for its LDS-bound staging), then the widest tile.
     const bool f64 = c->dtype == SOAP_FP64;
     int bestW = 0, bestB = 0;
     for (int W = jacobian_max_w(); W >= 1; --W) {
-        const size_t lds = jacobian_lds_bytes(P, W, f64);
+        const size_t lds = jacobian_lds_bytes(P, W, st64);
         if (lds > LDS_HARD_LIMIT) continue;
-        const int b = jacobian_blocks_per_cu(f64, P.rbf, P.n, P.lmax + 1, lds);
+        const int b = jacobian_blocks_per_cu(f64, ar64, P.rbf, P.n, P.lmax + 1, lds);
         if (b > bestB) {
             bestB = b;
             bestW = W;
         }
     }
-    if (bestW == 0) return fail(c, SOAP_EINVAL, "basis too large for the Jacobian kernel's on-chip memory");
+    c->jac_ok = bestW > 0;
     c->jac_cfg.W = bestW;
-    c->jac_cfg.lds = jacobian_lds_bytes(P, bestW, f64);
+    c->jac_cfg.lds = bestW > 0 ? jacobian_lds_bytes(P, bestW, st64) : 0;
     return SOAP_OK;
 }
 
@@ -416,16 +424,23 @@ int check_ctx_device(soap_ctx *c) {
     return SOAP_OK;
 }
 
-Rows rows_of(const soap_ctx *c) {
+// the rows of centers [first, first + count) of the neighbour list
+Rows rows_of(const soap_ctx *c, int64_t first, int64_t count) {
     Rows R;
     R.n_atoms = c->n_atoms;
-    R.nc = c->nc;
-    R.centers = c->centers;
+    R.nc = count;
+    R.c_base = first;
+    R.centers = c->centers ? c->centers + first : nullptr;
     R.spec = c->b_spec.as<uint8_t>();
-    R.row_ptr = c->b_row.as<int64_t>();
+    R.row_ptr = c->b_row.as<int64_t>() + first;
     R.cols = c->b_cols.as<int32_t>();
     return R;
 }
+Rows rows_of(const soap_ctx *c) { return rows_of(c, 0, c->nc); }
+
+// bytes of the float64 coefficient scratch the Jacobian path keeps per center
+// (c, Dx, Dy, Dz)
+size_t scratch_bytes_per_center(const soap_ctx *c) { return 8 * 4 * (size_t)c->P.S * c->P.n * c->P.L; }
 
 Params params_for(const soap_ctx *c, int mode) {
     Params P = c->P;
@@ -495,6 +510,13 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         c->have_rows = false;
         c->dtype = (int)value;
         return plan_launches(c); // occupancy of the float64 kernels
+    }
+    if (!std::strcmp(key, "arith")) {
+        if (value != SOAP_ARITH_MIXED && value != SOAP_ARITH_FP64)
+            return fail(c, SOAP_EINVAL, "arith must be SOAP_ARITH_MIXED or SOAP_ARITH_FP64");
+        if (value == c->arith) return SOAP_OK;
+        c->arith = (int)value;
+        return plan_launches(c); // staging sizes and occupancy of the kernels
     }
     if (!std::strcmp(key, "timing")) {
         if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "timing must be 0 or 1");
@@ -579,7 +601,7 @@ static int build_rows(soap_ctx *c, int64_t n_atoms, int64_t center_bound, const 
     e = nbr_phase1(w, n_atoms, center_bound, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(),
                    n_centers, centers_dev, c->r_cut, row, st);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
-    c->work_epoch = 0; // the density work counters were zeroed with the flags
+    c->work_epoch = WorkBase{}; // the density work counters were zeroed with the flags
     // With a rows buffer from an earlier build, the short rows are packed
     // before the host reads the total: the GPU works through the round trip.
     // k_pack writes nothing if the total exceeds the buffer; it runs again
@@ -758,28 +780,46 @@ int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, voi
     return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_get_neighbors");
 }
 
+// Centers [first, first + count) of the neighbour list; outputs are indexed
+// from the batch's first center (and edge).
 // mode as launch_density: 0 descriptor / coefficients, 1 descriptor + Jacobian,
-// 2 coefficient Jacobian
-static int run_density(soap_ctx *c, int mode, void *desc, void *c_out, void *jself, void *jc_edge, void *stream) {
+// 2 coefficient Jacobian.  scratch: the Jacobian path's coefficient scratch
+// (NULL = the context's, grown as needed).
+static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void *desc, void *c_out, void *jself,
+                       void *jc_edge, double *scratch, void *stream) {
     if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
     int rc;
     if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
+    if (!c->dens_ok[mode] || (mode == 1 && (!c->jac_ok || (c->groups[1] > 1 && !c->out_ok))))
+        return fail(c, SOAP_EINVAL, "basis too large for the on-chip memory of the %s kernels",
+                    mode == 2 ? "coefficient Jacobian" : "Jacobian");
     const Params P = params_for(c, mode);
-    double *scratch = nullptr;
-    if (mode == 1) {
-        hipError_t e = c->b_cscratch.ensure(8 * 4 * (size_t)c->nc * P.S * P.n * P.L); // c, Dx, Dy, Dz
+    if (mode == 1 && !scratch) {
+        hipError_t e = c->b_cscratch.ensure(scratch_bytes_per_center(c) * (size_t)count);
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
     SegTimer timer(c, 1, to_stream(stream));
-    hipError_t e = launch_density(P, rows_of(c), c->pos, c->built_f64, mode, c->dens_cfg[mode], c->nw.work,
-                                  &c->work_epoch, desc, c_out, jself, scratch, jc_edge, to_stream(stream));
+    hipError_t e = launch_density(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, mode, c->dens_cfg[mode],
+                                  c->nw.work, &c->work_epoch, desc, c_out, jself, scratch, jc_edge, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
     if (mode == 1 && P.n_groups > 1) { // with one l-group the density kernel writes desc and jself
-        e = launch_outputs(P, c->out_plan, c->nc, c->built_f64, scratch, desc, jself, to_stream(stream));
+        e = launch_outputs(P, c->out_plan, count, c->built_f64, scratch, desc, jself, to_stream(stream));
         if (e != hipSuccess) return hip_fail(c, e, "output kernel");
     }
     timer.done();
+    return SOAP_OK;
+}
+static int run_density(soap_ctx *c, int mode, void *desc, void *c_out, void *jself, void *jc_edge, void *stream) {
+    return run_density(c, mode, 0, c->nc, desc, c_out, jself, jc_edge, nullptr, stream);
+}
+
+// a batch [first, first + count) of the centers of the neighbour list
+static int check_batch(soap_ctx *c, int64_t first, int64_t count) {
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    if (first < 0 || count < 0 || first > c->nc || count > c->nc - first)
+        return fail(c, SOAP_EINVAL, "center batch [%lld, %lld) outside the %lld centers of the neighbour list",
+                    (long long)first, (long long)(first + count), (long long)c->nc);
     return SOAP_OK;
 }
 
@@ -826,18 +866,96 @@ int soap_compute_averaged(soap_ctx *c, int32_t mode, void *desc_dev, void *strea
     return SOAP_OK;
 }
 
+// descriptor + Jacobian of a center batch; scratch as run_density
+static int run_derivatives(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
+                           void *jac_self_dev, double *scratch, void *stream) {
+    if (count == 0) return SOAP_OK;
+    int rc = run_density(c, 1, first, count, desc_dev, nullptr, jac_self_dev, nullptr, scratch, stream);
+    if (rc != SOAP_OK) return rc;
+    if (c->E == 0) return SOAP_OK;
+    SegTimer timer(c, 2, to_stream(stream));
+    hipError_t e = launch_jacobian(c->P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, c->jac_cfg,
+                                   scratch ? scratch : c->b_cscratch.as<double>(), jac_edge_dev, to_stream(stream));
+    if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
+    timer.done();
+    return SOAP_OK;
+}
+
 int soap_derivatives(soap_ctx *c, void *desc_dev, void *jac_edge_dev, void *jac_self_dev, void *stream) {
     if (!c) return SOAP_EINVAL;
     if (!desc_dev || !jac_self_dev || (!jac_edge_dev && c->E > 0))
         return fail(c, SOAP_EINVAL, "output pointer is NULL");
-    int rc = run_density(c, 1, desc_dev, nullptr, jac_self_dev, nullptr, stream);
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    return run_derivatives(c, 0, c->nc, desc_dev, jac_edge_dev, jac_self_dev, nullptr, stream);
+}
+
+int soap_compute_batch(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    int rc = check_batch(c, first, count);
     if (rc != SOAP_OK) return rc;
-    if (c->E == 0) return SOAP_OK;
-    SegTimer timer(c, 2, to_stream(stream));
-    hipError_t e = launch_jacobian(c->P, rows_of(c), c->pos, c->built_f64, c->jac_cfg, c->b_cscratch.as<double>(),
-                                   jac_edge_dev, to_stream(stream));
-    if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
-    timer.done();
+    if (!desc_dev && count > 0) return fail(c, SOAP_EINVAL, "desc_dev is NULL");
+    if (count == 0) return SOAP_OK;
+    return run_density(c, 0, first, count, desc_dev, nullptr, nullptr, nullptr, nullptr, stream);
+}
+
+int soap_derivatives_batch(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
+                           void *jac_self_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    int rc = check_batch(c, first, count);
+    if (rc != SOAP_OK) return rc;
+    if (count > 0 && (!desc_dev || !jac_self_dev)) return fail(c, SOAP_EINVAL, "output pointer is NULL");
+    // a NULL jac_edge_dev is allowed only for a batch without edges
+    if (!jac_edge_dev && count > 0 && c->E > 0) {
+        int64_t r[2];
+        hipError_t e = hipMemcpy(r, c->b_row.as<int64_t>() + first, 8, hipMemcpyDeviceToHost);
+        if (e == hipSuccess) e = hipMemcpy(r + 1, c->b_row.as<int64_t>() + first + count, 8, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(c, e, "soap_derivatives_batch");
+        if (r[1] > r[0]) return fail(c, SOAP_EINVAL, "jac_edge_dev is NULL for a batch with edges");
+    }
+    return run_derivatives(c, first, count, desc_dev, jac_edge_dev, jac_self_dev, nullptr, stream);
+}
+
+int soap_plan_batches(soap_ctx *c, int32_t what, int64_t budget_bytes, int64_t max_batches, int64_t *center_first,
+                      int64_t *edge_first, int64_t *n_batches_out) {
+    if (!c) return SOAP_EINVAL;
+    if (!n_batches_out || budget_bytes <= 0 || (what != SOAP_BATCH_DESCRIPTOR && what != SOAP_BATCH_DERIVATIVES))
+        return fail(c, SOAP_EINVAL, "invalid arguments to soap_plan_batches");
+    if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
+    std::vector<int64_t> row((size_t)c->nc + 1);
+    hipError_t e = hipMemcpy(row.data(), c->b_row.p, 8 * row.size(), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(c, e, "soap_plan_batches");
+    const size_t elt = c->built_f64 ? 8 : 4;
+    const bool jac = what == SOAP_BATCH_DERIVATIVES;
+    // per center: descriptor row (+ center block and coefficient scratch);
+    // per edge: its neighbour block
+    const int64_t per_center = (int64_t)(elt * c->F * (jac ? 4 : 1) + (jac ? scratch_bytes_per_center(c) : 0));
+    const int64_t per_edge = jac ? (int64_t)(elt * 3 * c->Fe) : 0;
+    int64_t nb = 0, b0 = 0;
+    while (b0 < c->nc) {
+        int64_t b1 = b0, bytes = 0;
+        while (b1 < c->nc) {
+            const int64_t add = per_center + per_edge * (row[b1 + 1] - row[b1]);
+            if (bytes + add > budget_bytes) break;
+            bytes += add;
+            ++b1;
+        }
+        if (b1 == b0)
+            return fail(c, SOAP_ECAPACITY, "center %lld alone needs %lld bytes, above the budget of %lld", (long long)b0,
+                        (long long)(per_center + per_edge * (row[b0 + 1] - row[b0])), (long long)budget_bytes);
+        if (center_first && nb < max_batches) {
+            center_first[nb] = b0;
+            if (edge_first) edge_first[nb] = row[b0];
+        }
+        ++nb;
+        b0 = b1;
+    }
+    *n_batches_out = nb;
+    if (center_first) {
+        if (nb > max_batches)
+            return fail(c, SOAP_ECAPACITY, "%lld batches needed, room for %lld", (long long)nb, (long long)max_batches);
+        center_first[nb] = c->nc;
+        if (edge_first) edge_first[nb] = row[c->nc];
+    }
     return SOAP_OK;
 }
 

@@ -837,7 +837,11 @@ __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int x
 //   D^s_{a lm} += Bh_al r S_lm + B_al grad S_lm
 // (D = sum over neighbours of dc/dr_j = -dc/dr_i).  Rows are sorted by
 // species, so the registers are flushed into the shared LDS accumulators
-// (float64 LDS atomics) only when the species changes and at the end.  Then
+// only when the species changes and at the end.  The flushes of one species
+// go in wave order (each wave waits for its turn on that species, adds, and
+// hands the turn on), so every sum is formed in the same order on every run:
+// the results are bitwise repeatable and do not depend on which workgroup,
+// launch or center batch computes a center.  Then
 // the descriptor path writes the power spectrum of the group's l
 // (power_tiles); the Jacobian path leaves c and D in scratch for k_outputs
 // and k_jacobian.
@@ -845,6 +849,16 @@ __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int x
 constexpr int NWD = 4, BSD = 64 * NWD;
 
 constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 64 * KE
+
+// Wave-ordered flushes: a wave waits for its turn on a species at most this
+// many sleeps (~27 ns each; a turn comes within the time the lower waves take
+// to reach the same species boundary).  The order argument (wave 0 never
+// waits; wave w waits only for wave w-1 to pass a species that wave w-1
+// passes before its next workgroup barrier) makes every wait end; the bound
+// only guarantees it: past it the wave adds with LDS atomics instead, which
+// stays correct but gives up the fixed summation order.
+constexpr int TURN_SPIN_LIMIT = 1 << 18;
+constexpr int MAX_SPECIES = 64;
 
 __host__ __device__ __forceinline__ int dens_lgY0(int jac, int lg0) { return (jac && lg0 > 0) ? lg0 - 1 : lg0; }
 
@@ -875,9 +889,11 @@ constexpr int dens_min_waves(int mode, int rbf, bool hi) {
     return (hi && dens_has_high(mode, rbf)) ? (mode == 2 ? 2 : 3) : 1;
 }
 
-template <typename PosT, typename OutT, int MODE, int RBF, bool HI>
+// ST: precision of the staged harmonics and radial factors (OutT, or double
+// for float64 arithmetic with float32 outputs).
+template <typename PosT, typename OutT, int MODE, int RBF, bool HI, typename ST = OutT>
 __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
-                                                 unsigned long long *__restrict__ work, uint64_t base,
+                                                 unsigned long long *__restrict__ work, WorkBase base,
                                                  OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,
                                                  double *__restrict__ c_scratch, OutT *__restrict__ jc_edge) {
@@ -885,6 +901,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
     extern __shared__ __align__(16) double smem[];
     __shared__ int64_t s_next;
+    __shared__ int s_turn[MAX_SPECIES]; // per species: the wave whose partial sums go in next
     const int G = P.n_groups;
     const int g = blockIdx.x % G;
     const int lg0 = P.lgrp[g], lg1 = P.lgrp[g + 1], lgc = lg1 - lg0;
@@ -905,10 +922,10 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
     double *c0 = cv.take((size_t)n);
-    // staging at the output precision ST: the harmonics and radial factors
-    // enter the float64 accumulators as products with relative rounding
-    // error of ST's order, which float32 outputs carry anyway
-    using ST = OutT;
+    // staging at precision ST (by default the output precision): the
+    // harmonics and radial factors enter the float64 accumulators as
+    // products with relative rounding error of ST's order, which float32
+    // outputs carry anyway
     using ST2 = typename Pair<ST>::type;
     constexpr int SB = sizeof(ST);
     Carver wv{cv.take(0) + (size_t)wave * dens_wave_doubles(P, JAC, lg0, lg1, W, SB)};
@@ -942,6 +959,8 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
     // on-site terms in LDS: no global load may sit between output stores
     // (vmcnt counts loads and stores together)
     for (int k = tid; k < n; k += BSD) c0[k] = P.c0[k];
+    // structure index of the batch's first edge: edge outputs are batch-local
+    const int64_t ebase = CCJ ? R.row_ptr[0] : 0;
 
     // the next center: its rows are loaded before the current center's
     // outputs are stored, so those loads never wait behind the stores
@@ -959,13 +978,13 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
             ci = blockIdx.x / G;
             first = false;
         } else {
-            if (tid == 0) s_next = per_group + (int64_t)(atomicAdd(&work[g], 1ull) - base);
+            if (tid == 0) s_next = per_group + (int64_t)(atomicAdd(&work[g], 1ull) - base.b[g]);
             lds_barrier();
             ci = __builtin_amdgcn_readfirstlane((int)s_next); // uniform: scalar addressing
             lds_barrier();                                    // s_next is rewritten by the next fetch
         }
         if (ci >= R.nc) return;
-        i = R.centers ? (int64_t)R.centers[ci] : ci;
+        i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
         pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
         spec_i = R.spec[i];
         e0 = R.row_ptr[ci];
@@ -979,30 +998,66 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
 
     while (ci < R.nc) {
         for (int k = tid; k < SnL * (JAC ? 4 : 1); k += BSD) cacc[k] = 0.0;
-        lds_barrier(); // rows of this center and the cleared accumulators
+        for (int k = tid; k < S; k += BSD) s_turn[k] = 0;
+        lds_barrier(); // rows of this center, the cleared accumulators and turns
 
         double acc[KE][4];
 #pragma unroll
         for (int k = 0; k < KE; ++k) acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
-        int cur = -1; // species of the registers' edges
-        auto flush = [&]() {
-#pragma unroll
-            for (int k = 0; k < KE; ++k) {
-                if (!own[k]) continue;
-                const int idx = cur * nL + lane + 64 * k;
-                atomicAdd(&cacc[idx], acc[k][0]);
-                if (JAC) {
-                    atomicAdd(&Dacc[idx], acc[k][1]);
-                    atomicAdd(&Dacc[SnL + idx], acc[k][2]);
-                    atomicAdd(&Dacc[2 * SnL + idx], acc[k][3]);
+        int cur = -1;  // species of the registers' partial sums (-1: none held)
+        int nextp = 0; // the lowest species this wave has not passed yet
+        // Pass every species t in [nextp, upto): wait for this wave's turn on
+        // t, add the registers into the shared accumulators if they hold t,
+        // and hand the turn to the next wave.  Species go in increasing order
+        // (the rows are sorted), so each wave passes each species once per
+        // center and the sums of a species are taken in wave order.
+        auto pass = [&](int upto) {
+            for (int t = nextp; t < upto; ++t) {
+                bool turn = false;
+                for (int spin = 0; spin < TURN_SPIN_LIMIT; ++spin) {
+                    const int w = __hip_atomic_load(&s_turn[t], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    if (__builtin_amdgcn_readfirstlane(w) == wave) {
+                        turn = true;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
                 }
-                acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
+                if (t == cur) {
+#pragma unroll
+                    for (int k = 0; k < KE; ++k) {
+                        if (!own[k]) continue;
+                        const int idx = cur * nL + lane + 64 * k;
+                        if (turn) {
+                            cacc[idx] += acc[k][0];
+                            if (JAC) {
+                                Dacc[idx] += acc[k][1];
+                                Dacc[SnL + idx] += acc[k][2];
+                                Dacc[2 * SnL + idx] += acc[k][3];
+                            }
+                        } else {
+                            atomicAdd(&cacc[idx], acc[k][0]);
+                            if (JAC) {
+                                atomicAdd(&Dacc[idx], acc[k][1]);
+                                atomicAdd(&Dacc[SnL + idx], acc[k][2]);
+                                atomicAdd(&Dacc[2 * SnL + idx], acc[k][3]);
+                            }
+                        }
+                        acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
+                    }
+                    cur = -1;
+                }
+                if (turn) __hip_atomic_store(&s_turn[t], wave + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
             }
+            nextp = upto > nextp ? upto : nextp;
         };
 
         for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
             const int rbn = (int)((e1 - rb0) < RBk ? (e1 - rb0) : RBk);
             if (rb0 != e0) { // further row blocks of a long row (no output stores are pending here)
+                // before the barrier, pass the species below the last one of
+                // the block just done: a wave waiting for its turn on one of
+                // them is then never left waiting on a wave held at the barrier
+                pass(__builtin_amdgcn_readfirstlane(rsp[RBk - 1])); // the previous block is full
                 lds_barrier();
                 load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
                 lds_barrier();
@@ -1014,7 +1069,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                 for (int e = 0; e < nb; ++e) {
                     const int s = __builtin_amdgcn_readfirstlane(rsp[off + e]);
                     if (s != cur) {
-                        if (cur >= 0) flush();
+                        pass(s); // adds the registers if they hold a lower species
                         cur = s;
                     }
                     const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
@@ -1026,7 +1081,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                     // pointer per lane and entry, which spilled.
                     OutT *je = nullptr;
                     if (CCJ) {
-                        je = jc_edge + (size_t)(rb0 + off + e) * 3 * n * Lfull;
+                        je = jc_edge + (size_t)(rb0 + off + e - ebase) * 3 * n * Lfull;
                         __asm__ volatile("" : "+s"(je));
                     }
                     OutT *const je1 = je + (size_t)n * Lfull, *const je2 = je + 2 * (size_t)n * Lfull;
@@ -1058,7 +1113,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                 wave_sync(); // the next tile's staging overwrites YY and BB
             }
         }
-        if (cur >= 0) flush();
+        pass(S);
         lds_barrier();
         // on-site term of the center (its species, l = 0)
         if (lg0 == 0)
@@ -1317,11 +1372,12 @@ constexpr int jac_min_waves(int ab, int NT, int LWT) {
 }
 
 // RBF: -1 reads the radial basis from P (0..2); 3 is the compensated GTO
-template <typename PosT, typename OutT, int NT, int LWT, int RBF = -1>
-__global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), NT, LWT)) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
+// AT: precision of the final assembly (OutT, or double for float64
+// arithmetic with float32 outputs).
+template <typename PosT, typename OutT, int NT, int LWT, int RBF = -1, typename AT = OutT>
+__global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
                                                                             int W, int vec, const double *__restrict__ c_scratch,
                                                                             OutT *__restrict__ jedge) {
-    using AT = OutT; // assembly precision
     using AT2 = typename Pair<AT>::type;
     constexpr int ab = sizeof(AT);
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
@@ -1372,11 +1428,11 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), NT, LWT)) void k_j
     // stores to drain.)
     {
     const int64_t ci = blockIdx.x;
-    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
+    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1], ebase = R.row_ptr[0];
     if (e1 == e0) return;
     const double *cg = c_scratch + ci * 4 * (size_t)Sn * L; // component c of [c, Dx, Dy, Dz]
     copy_to_lds<BSJ, 4>(cT, cg, Sn * L, tid);
-    const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
+    const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
 
     for (int64_t rb0 = e0; rb0 < e1; rb0 += RBk) {
@@ -1386,7 +1442,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(OutT), NT, LWT)) void k_j
         lds_barrier();
         for (int off = wave * W; off < rbn; off += NWJ * W) {
             const int nb = (rbn - off) < W ? (rbn - off) : W;
-            const int64_t base = rb0 + off;
+            const int64_t base = rb0 + off - ebase; // batch-local edge index
             const double *geo = rgeo + 4 * off;
             const int *spc = rsp + off;
             stage_edges<true, AT, NT, LWT, double, RBF>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw,
@@ -1585,7 +1641,8 @@ __global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge
                                 OutT *__restrict__ dense) {
     const int64_t ci = blockIdx.x;
     const int F = P.F, Fe = P.Fe;
-    const int64_t i = R.centers ? (int64_t)R.centers[ci] : ci;
+    const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
+    const int64_t ebase = R.row_ptr[0];
     OutT *row = dense + ci * R.n_atoms * 3 * F;
     for (int k = threadIdx.x; k < 3 * F; k += blockDim.x) row[i * 3 * F + k] = jself[ci * 3 * F + k];
     __syncthreads(); // a periodic image of the center adds to the center block
@@ -1597,8 +1654,8 @@ __global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge
         for (int k = threadIdx.x; k < 3 * Fe; k += blockDim.x) {
             const int d = k / Fe, fe = k - d * Fe;
             OutT *o = row + (j * 3 + d) * F + fmap[s * Fe + fe];
-            if (atom_of) *o += jedge[(e * 3 + d) * Fe + fe];
-            else *o = jedge[(e * 3 + d) * Fe + fe];
+            if (atom_of) *o += jedge[((e - ebase) * 3 + d) * Fe + fe];
+            else *o = jedge[((e - ebase) * 3 + d) * Fe + fe];
         }
     }
 }

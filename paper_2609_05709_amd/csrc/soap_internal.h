@@ -36,13 +36,28 @@ struct Params {
     int lgrp[MAX_GROUPS + 1];  // group g covers l in [lgrp[g], lgrp[g+1])
 };
 
-// Neighbour rows of the current structure.
+// Neighbour rows of the current structure, or of one batch of its centers:
+// the batch's rows row_ptr[0..nc] are a slice of the structure's CSR offsets,
+// so edge e of the structure is edge e - row_ptr[0] of the batch's edge
+// outputs, while center ci of the batch is center c_base + ci of the
+// structure (its row, its atom index).
 struct Rows {
     int64_t n_atoms, nc;
-    const int32_t *centers; // NULL = identity
+    int64_t c_base;         // structure index of the batch's first center
+    const int32_t *centers; // [nc] atom of each center of the batch; NULL = c_base + ci
     const uint8_t *spec;    // species index per atom
     const int64_t *row_ptr; // [nc+1]
-    const int32_t *cols;    // [E]
+    const int32_t *cols;    // [E] (indexed by structure edge)
+};
+
+// Density work counters: one 64-bit counter per l-group, zeroed at the
+// neighbour build and never reset in between.  Every density launch advances
+// the counters of the groups it runs by exactly n_c (its centers but the
+// static first ones, plus one empty fetch per workgroup), so each group keeps
+// its own count of the increments taken so far; a launch planning fewer
+// groups leaves the other counters, and their counts, untouched.
+struct WorkBase {
+    uint64_t b[MAX_GROUPS];
 };
 
 // ---- neighbour search (neighbors.hip) ----
@@ -126,13 +141,16 @@ struct JacLaunch {
     size_t lds;
 };
 
-size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64);
-int density_blocks_per_cu(bool f64, int mode, int rbf, bool hi, size_t lds); // mode as launch_density; rbf as Params
+// st64: float64 staging (float64 outputs, or float64 arithmetic with float32 outputs)
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool st64);
+// f64: float64 positions and outputs; ar64: float64 arithmetic with float32 outputs
+int density_blocks_per_cu(bool f64, bool ar64, int mode, int rbf, bool hi, size_t lds); // mode as launch_density
 bool density_has_high(int mode, int rbf); // a three-waves-per-SIMD variant exists
 constexpr int DENSITY_KE = 8; // coefficient entries per lane in k_density: n * Lg <= 512
-size_t jacobian_lds_bytes(const Params &P, int W, bool f64);
+size_t jacobian_lds_bytes(const Params &P, int W, bool at64); // at64: float64 assembly
 int jacobian_max_w();
-int jacobian_blocks_per_cu(bool f64, int rbf, int n, int lw, size_t lds); // resident workgroups per CU (0 if it does not fit)
+// resident workgroups per CU (0 if it does not fit)
+int jacobian_blocks_per_cu(bool f64, bool ar64, int rbf, int n, int lw, size_t lds);
 // float32 Jacobian kernels for fixed (n_max, l_max + 1); NULL if not compiled
 const void *jacobian_fixed_0(int n, int lw);
 const void *jacobian_fixed_1(int n, int lw);
@@ -141,13 +159,14 @@ hipError_t set_lds_limits();
 
 // desc (may be NULL; descriptor path), c_out (may be NULL, dtype), c_scratch (jac only, float64,
 // [center][c, Dx, Dy, Dz][lm][species n])
-// work: per-group counters, zeroed at the neighbour build and never reset in
-// between; *epoch counts the increments made since then (advanced here).
+// work: per-group counters (WorkBase); *epoch holds each group's count of
+// the increments made since they were zeroed (advanced here for the groups
+// the launch runs).
 // mode 0: descriptor (desc, c_out may be NULL); 1: descriptor + Jacobian (desc,
 // jself, c_scratch); 2: coefficient Jacobian (c_out, jself = [n_c][3][S][n][L],
 // jc_edge = [E][3][n][L])
-hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, int mode,
-                          const DensityLaunch &cfg, unsigned long long *work, uint64_t *epoch, void *desc, void *c_out,
+hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, int mode,
+                          const DensityLaunch &cfg, unsigned long long *work, WorkBase *epoch, void *desc, void *c_out,
                           void *jself, double *c_scratch, void *jc_edge, hipStream_t st);
 // power spectrum and center block from the coefficient scratch (Jacobian
 // path): l-groups of the output kernel, each sized to its LDS budget
@@ -159,7 +178,7 @@ struct OutPlan {
 int plan_outputs(const Params &P, bool f64, OutPlan *O); // 0, or -1 if one l does not fit
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
                           void *jself, hipStream_t st);
-hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
+hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);
 // column means of a row-major (rows x cols) array of the output type, in
 // float64: part[AVG_CHUNKS][cols] partial sums, then mean[cols] (float64)

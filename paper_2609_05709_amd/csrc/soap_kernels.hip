@@ -5,49 +5,53 @@
 namespace soap {
 using namespace dev;
 
-size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool f64) {
+size_t density_lds_bytes(const Params &P, int jac, int lg0, int lg1, int W, bool st64) {
     const size_t Lg = (size_t)(lg1 * lg1 - lg0 * lg0);
     const size_t SnL = (size_t)P.S * P.n * Lg;
     const int RBk = row_block(NWD * W);
     size_t d = table_doubles(P, lg1 - lg0) + even(SnL * (jac ? 4 : 1)) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
-               even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W, f64 ? 8 : 4);
+               even((size_t)P.n) + NWD * dens_wave_doubles(P, jac, lg0, lg1, W, st64 ? 8 : 4);
     return d * 8;
 }
 
-// the density kernel of a precision, mode, radial basis and occupancy variant
-template <typename T, int RBF, bool HI>
+// the density kernel of a precision (positions and outputs T, staging ST),
+// mode, radial basis and occupancy variant
+template <typename T, typename ST, int RBF, bool HI>
 static const void *density_kernel_r(int mode) {
-    return mode == 0 ? (const void *)dev::k_density<T, T, 0, RBF, false>
-                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF, HI && dev::dens_has_high(1, RBF)>
-                                 : (const void *)dev::k_density<T, T, 2, RBF, HI>;
+    return mode == 0 ? (const void *)dev::k_density<T, T, 0, RBF, false, ST>
+                     : mode == 1 ? (const void *)dev::k_density<T, T, 1, RBF, HI && dev::dens_has_high(1, RBF), ST>
+                                 : (const void *)dev::k_density<T, T, 2, RBF, HI, ST>;
 }
-template <typename T, int RBF>
+template <typename T, typename ST, int RBF>
 static const void *density_kernel_h(int mode, bool hi) {
-    return hi ? density_kernel_r<T, RBF, true>(mode) : density_kernel_r<T, RBF, false>(mode);
+    return hi ? density_kernel_r<T, ST, RBF, true>(mode) : density_kernel_r<T, ST, RBF, false>(mode);
 }
-template <typename T>
+template <typename T, typename ST>
 static const void *density_kernel_t(int mode, int rbf, bool hi) {
     if (rbf == 3) { // the compensated GTO exists for float64 only
-        if constexpr (sizeof(T) == 8) return density_kernel_h<T, 3>(mode, hi);
+        if constexpr (sizeof(T) == 8) return density_kernel_h<T, ST, 3>(mode, hi);
         return nullptr;
     }
-    return rbf == 0 ? density_kernel_h<T, 0>(mode, hi)
-                    : (rbf == 1 ? density_kernel_h<T, 1>(mode, hi) : density_kernel_h<T, 2>(mode, hi));
+    return rbf == 0 ? density_kernel_h<T, ST, 0>(mode, hi)
+                    : (rbf == 1 ? density_kernel_h<T, ST, 1>(mode, hi) : density_kernel_h<T, ST, 2>(mode, hi));
 }
-static const void *density_kernel(bool f64, int mode, int rbf, bool hi) {
-    return f64 ? density_kernel_t<double>(mode, rbf, hi) : density_kernel_t<float>(mode, rbf, hi);
+// ar64: float64 staging with float32 outputs (ignored for float64 outputs)
+static const void *density_kernel(bool f64, bool ar64, int mode, int rbf, bool hi) {
+    if (f64) return density_kernel_t<double, double>(mode, rbf, hi);
+    return ar64 ? density_kernel_t<float, double>(mode, rbf, hi) : density_kernel_t<float, float>(mode, rbf, hi);
 }
 
 bool density_has_high(int mode, int rbf) { return dev::dens_has_high(mode, rbf); }
 
-int density_blocks_per_cu(bool f64, int mode, int rbf, bool hi, size_t lds) {
+int density_blocks_per_cu(bool f64, bool ar64, int mode, int rbf, bool hi, size_t lds) {
     int nb = 0;
-    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, density_kernel(f64, mode, rbf, hi), BSD, lds);
+    const hipError_t e =
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, density_kernel(f64, ar64, mode, rbf, hi), BSD, lds);
     return (e == hipSuccess && nb > 0) ? nb : 1;
 }
 
-size_t jacobian_lds_bytes(const Params &P, int W, bool f64) {
-    const int ab = f64 ? 8 : 4;
+size_t jacobian_lds_bytes(const Params &P, int W, bool at64) {
+    const int ab = at64 ? 8 : 4;
     const size_t L = (size_t)P.L, Sn = (size_t)P.S * P.n;
     const int RBk = row_block(NWJ * W);
     size_t d = table_doubles(P, P.lmax + 1) + even(Sn * L) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
@@ -94,20 +98,21 @@ int jacobian_max_w() { return JAC_MAX_W; }
 // The float32 Jacobian kernel is also compiled for fixed (n_max, l_max + 1)
 // pairs (jacobian_fixed.hip); the generic kernel covers every other basis and
 // float64.
-const void *jacobian_kernel(bool f64, int rbf, int n, int lw) {
+const void *jacobian_kernel(bool f64, bool ar64, int rbf, int n, int lw) {
     if (f64)
         return rbf == 3 ? reinterpret_cast<const void *>(&k_jacobian<double, double, 0, 0, 3>)
                         : reinterpret_cast<const void *>(&k_jacobian<double, double, 0, 0>);
     if (rbf == 3) return nullptr; // float64 only
+    if (ar64) return reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0, -1, double>);
     const void *k = jacobian_fixed_0(n, lw);
     if (!k) k = jacobian_fixed_1(n, lw);
     if (!k) k = jacobian_fixed_2(n, lw);
     return k ? k : reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>);
 }
 
-int jacobian_blocks_per_cu(bool f64, int rbf, int n, int lw, size_t lds) {
+int jacobian_blocks_per_cu(bool f64, bool ar64, int rbf, int n, int lw, size_t lds) {
     int nb = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, jacobian_kernel(f64, rbf, n, lw), BSJ, lds);
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, jacobian_kernel(f64, ar64, rbf, n, lw), BSJ, lds);
     return (e == hipSuccess && nb > 0) ? nb : 0;
 }
 
@@ -117,9 +122,10 @@ hipError_t set_lds_limits() {
 #define SOAP_SET(K)                                                                                          \
     if (e == hipSuccess) e = hipFuncSetAttribute((const void *)(K), hipFuncAttributeMaxDynamicSharedMemorySize, lim);
     for (int f64 = 0; f64 < 2; ++f64)
-        for (int mode = 0; mode < 3; ++mode)
-            for (int rbf = 0; rbf < (f64 ? 4 : 3); ++rbf)
-                for (int hi = 0; hi < 2; ++hi) SOAP_SET(density_kernel(f64 != 0, mode, rbf, hi != 0));
+        for (int ar64 = 0; ar64 < 2; ++ar64)
+            for (int mode = 0; mode < 3; ++mode)
+                for (int rbf = 0; rbf < (f64 ? 4 : 3); ++rbf)
+                    for (int hi = 0; hi < 2; ++hi) SOAP_SET(density_kernel(f64 != 0, ar64 != 0, mode, rbf, hi != 0));
     SOAP_SET(k_outputs<float>);
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
@@ -127,35 +133,38 @@ hipError_t set_lds_limits() {
     SOAP_SET((k_jacobian<float, float, 0, 0>));
     SOAP_SET((k_jacobian<double, double, 0, 0>));
     SOAP_SET((k_jacobian<double, double, 0, 0, 3>));
+    SOAP_SET((k_jacobian<float, float, 0, 0, -1, double>));
     for (int n = 1; n <= NMAX; ++n)
         for (int lw = 1; lw <= LMAX + 1; ++lw) {
-            const void *k = jacobian_kernel(false, 0, n, lw);
+            const void *k = jacobian_kernel(false, false, 0, n, lw);
             if (k != reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>)) SOAP_SET(k);
         }
 #undef SOAP_SET
     return e;
 }
 
-hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, int mode,
-                          const DensityLaunch &cfg, unsigned long long *work, uint64_t *epoch, void *desc, void *c_out,
+hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, int mode,
+                          const DensityLaunch &cfg, unsigned long long *work, WorkBase *epoch, void *desc, void *c_out,
                           void *jself, double *c_scratch, void *jc_edge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     const int64_t per_group = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
-    uint64_t b = *epoch;
+    WorkBase b = *epoch;
     Params Pk = P;
     Rows Rk = R;
     int W = cfg.W;
     void *args[] = {&Pk, &Rk, &pos, &W, &work, &b, &desc, &c_out, &jself, &c_scratch, &jc_edge};
-    const void *k = density_kernel(f64, mode, P.rbf, cfg.hi);
+    const void *k = density_kernel(f64, ar64, mode, P.rbf, cfg.hi);
     const hipError_t e =
         hipLaunchKernel(k, dim3((unsigned)(per_group * P.n_groups)), dim3(BSD), args, cfg.lds, st);
-    // the counter is taken for every center but the per_group static ones,
-    // plus one final, empty fetch per workgroup
-    if (e == hipSuccess) *epoch += (uint64_t)R.nc;
+    // each group's counter is taken for every center but the per_group
+    // static ones, plus one final, empty fetch per workgroup: n_c increments
+    // for every group this launch runs, none for the others
+    if (e == hipSuccess)
+        for (int g = 0; g < P.n_groups; ++g) epoch->b[g] += (uint64_t)R.nc;
     return e;
 }
 
-hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, const JacLaunch &cfg,
+hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     Params Pk = P;
@@ -166,7 +175,8 @@ hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool
     const int nnl = P.n * P.n * (P.lmax + 1);
     int vec = (f64 && nnl % 2 == 0 && P.tri_lw % 2 == 0 && ((uintptr_t)jedge & 15) == 0) ? 1 : 0;
     void *args[] = {&Pk, &Rk, &pos, &W, &vec, &c_scratch, &jedge};
-    return hipLaunchKernel(jacobian_kernel(f64, P.rbf, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args, cfg.lds, st);
+    return hipLaunchKernel(jacobian_kernel(f64, ar64, P.rbf, P.n, P.lmax + 1), dim3((unsigned)R.nc), dim3(BSJ), args,
+                           cfg.lds, st);
 }
 
 hipError_t launch_column_mean(const void *in, bool f64, int64_t rows, int64_t cols, double *part, void *out,

@@ -18,6 +18,9 @@ RBF_CODES = {"gto": SOAP_RBF_GTO, "polynomial": SOAP_RBF_POLYNOMIAL,
              "polynomial-laplace": SOAP_RBF_POLYNOMIAL_LAPLACE}
 SOAP_FP32, SOAP_FP64 = 0, 1
 SOAP_AVERAGE_INNER, SOAP_AVERAGE_OUTER = 1, 2
+SOAP_ARITH_MIXED, SOAP_ARITH_FP64 = 0, 1
+ARITH_CODES = {"mixed": SOAP_ARITH_MIXED, "fp64": SOAP_ARITH_FP64}
+SOAP_BATCH_DESCRIPTOR, SOAP_BATCH_DERIVATIVES = 0, 1
 MAX_DEGREE = 2048
 
 # every entry point declared in include/soap.h
@@ -25,7 +28,8 @@ ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_num_features", "soap_num_
                "soap_feature_labels", "soap_feature_map", "soap_build_neighbors", "soap_get_neighbors",
                "soap_set_cell", "soap_get_neighbor_images",
                "soap_compute", "soap_coefficients", "soap_coefficient_derivatives", "soap_compute_averaged",
-               "soap_derivatives", "soap_scatter_dense", "soap_timing",
+               "soap_derivatives", "soap_compute_batch", "soap_derivatives_batch", "soap_plan_batches",
+               "soap_scatter_dense", "soap_timing",
                "soap_last_error", "soap_destroy")
 
 _STATUS = {SOAP_EINVAL: "EINVAL", SOAP_ESPECIES: "ESPECIES", SOAP_ENOMEM: "ENOMEM", SOAP_EHIP: "EHIP",
@@ -72,6 +76,12 @@ def load_library(path: str = LIB_PATH):
     L.soap_coefficients.argtypes = [vp, vp, vp]
     L.soap_derivatives.restype = ctypes.c_int
     L.soap_derivatives.argtypes = [vp, vp, vp, vp, vp]
+    L.soap_compute_batch.restype = ctypes.c_int
+    L.soap_compute_batch.argtypes = [vp, i64, i64, vp, vp]
+    L.soap_derivatives_batch.restype = ctypes.c_int
+    L.soap_derivatives_batch.argtypes = [vp, i64, i64, vp, vp, vp, vp]
+    L.soap_plan_batches.restype = ctypes.c_int
+    L.soap_plan_batches.argtypes = [vp, i32, i64, i64, vp, vp, ctypes.POINTER(i64)]
     L.soap_scatter_dense.restype = ctypes.c_int
     L.soap_scatter_dense.argtypes = [vp, vp, vp, vp, vp]
     L.soap_set_cell.restype = ctypes.c_int
@@ -99,9 +109,11 @@ def _stream():
 
 class Soap:
     """One library context: species, r_cut, n_max, l_max, sigma, rbf
-    ("gto" | "polynomial" | "polynomial-laplace"), dtype ("float32" | "float64")."""
+    ("gto" | "polynomial" | "polynomial-laplace"), dtype ("float32" | "float64"),
+    arith ("mixed" | "fp64": the float32 mode's internal arithmetic)."""
 
-    def __init__(self, species, r_cut, n_max, l_max, sigma, rbf="gto", dtype="float32", quad_n=None):
+    def __init__(self, species, r_cut, n_max, l_max, sigma, rbf="gto", dtype="float32", quad_n=None,
+                 arith="mixed"):
         import numpy as np
         import torch
         self._L = load_library()
@@ -124,6 +136,10 @@ class Soap:
             self._check(self._L.soap_set_option(self._h, b"dtype", SOAP_FP64))
         if quad_n is not None:
             self._check(self._L.soap_set_option(self._h, b"quad_n", int(quad_n)))
+        if arith not in ARITH_CODES:
+            raise ValueError(f"unknown arith {arith!r}; expected one of {sorted(ARITH_CODES)}")
+        if arith != "mixed":
+            self._check(self._L.soap_set_option(self._h, b"arith", ARITH_CODES[arith]))
         self.n_features = int(self._L.soap_num_features(self._h))
         self.n_edge_features = int(self._L.soap_num_edge_features(self._h))
         self.E = None
@@ -276,6 +292,39 @@ class Soap:
         jac_self = self._out(jac_self, (self.n_centers, 3, self.n_features))
         self._check(self._L.soap_derivatives(self._h, desc.data_ptr(), jac_edge.data_ptr() if self.E else None,
                                              jac_self.data_ptr(), _stream()))
+        return desc, jac_edge, jac_self
+
+    # -- center batches ---------------------------------------------------------
+    def plan_batches(self, budget_bytes: int, jacobian: bool = True):
+        """Consecutive center batches whose outputs (and, with the Jacobian,
+        the library's scratch) fit budget_bytes: (center_first, edge_first),
+        each of length B + 1."""
+        import numpy as np
+        if self.E is None:
+            raise SoapError(SOAP_ESTATE, "no neighbour list: call build_neighbors first")
+        what = SOAP_BATCH_DERIVATIVES if jacobian else SOAP_BATCH_DESCRIPTOR
+        nb = ctypes.c_int64()
+        self._check(self._L.soap_plan_batches(self._h, what, int(budget_bytes), 0, None, None, ctypes.byref(nb)))
+        cf = np.empty(nb.value + 1, dtype=np.int64)
+        ef = np.empty(nb.value + 1, dtype=np.int64)
+        self._check(self._L.soap_plan_batches(self._h, what, int(budget_bytes), nb.value, cf.ctypes.data,
+                                              ef.ctypes.data, ctypes.byref(nb)))
+        return cf, ef
+
+    def compute_batch(self, first: int, count: int, out=None):
+        desc = self._out(out, (count, self.n_features))
+        self._check(self._L.soap_compute_batch(self._h, int(first), int(count), desc.data_ptr(), _stream()))
+        return desc
+
+    def derivatives_batch(self, first: int, count: int, n_edges: int, desc=None, jac_edge=None, jac_self=None):
+        """Descriptor and Jacobian of centers [first, first + count); n_edges =
+        the edges of their rows (edge_first[k + 1] - edge_first[k])."""
+        desc = self._out(desc, (count, self.n_features))
+        jac_edge = self._out(jac_edge, (n_edges, 3, self.n_edge_features))
+        jac_self = self._out(jac_self, (count, 3, self.n_features))
+        self._check(self._L.soap_derivatives_batch(self._h, int(first), int(count), desc.data_ptr(),
+                                                   jac_edge.data_ptr() if n_edges else None, jac_self.data_ptr(),
+                                                   _stream()))
         return desc, jac_edge, jac_self
 
     def scatter_dense(self, jac_edge, jac_self, out=None):

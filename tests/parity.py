@@ -14,14 +14,15 @@ import oracle
 TOL = {"float32": 1e-5, "float64": 1e-10}
 
 
-def gpu_run(wl, st, dtype="float32", centers=None, jacobian=True, sample=None, coefficients=False, quad_n=None):
+def gpu_run(wl, st, dtype="float32", centers=None, jacobian=True, sample=None, coefficients=False, quad_n=None,
+            arith="mixed"):
     """Run the HIP path; copy back the descriptor, neighbour rows and, for the
     centers in `sample` (indices into the center list; None = all), their
     Jacobian blocks."""
     import torch
     from paper_2609_05709_amd.soap import Soap
     tdt = torch.float64 if dtype == "float64" else torch.float32
-    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype, quad_n=quad_n)
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype, quad_n=quad_n, arith=arith)
     pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
     Z = torch.from_numpy(st.Z).to("cuda")
     cen = None if centers is None else torch.from_numpy(np.asarray(centers, dtype=np.int32)).to("cuda")

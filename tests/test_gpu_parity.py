@@ -132,13 +132,6 @@ def test_gto_float64_compensated(n_max, l_max, sigma):
     full_check(wl, "float64", sample=12, seed=n_max + l_max)
 
 
-@pytest.mark.parametrize("rbf", ["gto", "polynomial", "polynomial-laplace"])
-@pytest.mark.parametrize("nl", [(2, 2), (2, 12), (12, 2), (12, 12), (6, 8)])
-def test_hyperparameter_grid_points(rbf, nl):
-    wl = workloads.WATER1000.with_basis(nl[0], nl[1], rbf)
-    full_check(wl, "float32", sample=8, seed=nl[0] * 13 + nl[1])
-
-
 def test_water1m_descriptor_sampled():
     import torch
     from paper_2609_05709_amd.soap import Soap
