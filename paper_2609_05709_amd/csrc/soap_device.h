@@ -855,8 +855,8 @@ constexpr int KE = DENSITY_KE; // coefficient entries owned per lane: n * Lg <= 
 // to reach the same species boundary).  The order argument (wave 0 never
 // waits; wave w waits only for wave w-1 to pass a species that wave w-1
 // passes before its next workgroup barrier) makes every wait end; the bound
-// only guarantees it: past it the wave adds with LDS atomics instead, which
-// stays correct but gives up the fixed summation order.
+// only guarantees it: past it the wave adds without its turn, which stays
+// correct (the adds are LDS atomics) but gives up the fixed summation order.
 constexpr int TURN_SPIN_LIMIT = 1 << 18;
 constexpr int MAX_SPECIES = 64;
 
@@ -1023,24 +1023,18 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                     __builtin_amdgcn_s_sleep(1);
                 }
                 if (t == cur) {
+                    // LDS atomic adds (one instruction each): while the wave
+                    // holds the turn no other wave adds to species t, so the
+                    // order is the wave order
 #pragma unroll
                     for (int k = 0; k < KE; ++k) {
                         if (!own[k]) continue;
                         const int idx = cur * nL + lane + 64 * k;
-                        if (turn) {
-                            cacc[idx] += acc[k][0];
-                            if (JAC) {
-                                Dacc[idx] += acc[k][1];
-                                Dacc[SnL + idx] += acc[k][2];
-                                Dacc[2 * SnL + idx] += acc[k][3];
-                            }
-                        } else {
-                            atomicAdd(&cacc[idx], acc[k][0]);
-                            if (JAC) {
-                                atomicAdd(&Dacc[idx], acc[k][1]);
-                                atomicAdd(&Dacc[SnL + idx], acc[k][2]);
-                                atomicAdd(&Dacc[2 * SnL + idx], acc[k][3]);
-                            }
+                        atomicAdd(&cacc[idx], acc[k][0]);
+                        if (JAC) {
+                            atomicAdd(&Dacc[idx], acc[k][1]);
+                            atomicAdd(&Dacc[SnL + idx], acc[k][2]);
+                            atomicAdd(&Dacc[2 * SnL + idx], acc[k][3]);
                         }
                         acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.0;
                     }
