@@ -85,6 +85,9 @@ typedef struct soap_ctx soap_ctx;
 #define SOAP_ARITH_MIXED 0 /* float32 staging and final assembly (default) */
 #define SOAP_ARITH_FP64 1  /* float64 throughout, outputs rounded at the store */
 
+/* bytes of the fixed device scratch of soap_derivatives_batch_noalloc */
+#define SOAP_STATIC_SCRATCH_BYTES (64 * 1024 * 1024)
+
 /* outputs a center batch plan is sized for (soap_plan_batches) */
 #define SOAP_BATCH_DESCRIPTOR 0
 #define SOAP_BATCH_DERIVATIVES 1
@@ -306,6 +309,28 @@ int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *ja
 int soap_compute_batch(soap_ctx *ctx, int64_t first, int64_t count, void *desc_dev, void *stream);
 int soap_derivatives_batch(soap_ctx *ctx, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
                            void *jac_self_dev, void *stream);
+
+/*
+ * soap_derivatives_batch for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same outputs, bitwise, with the Jacobian path's float64
+ * coefficient scratch taken from a fixed device array of
+ * SOAP_STATIC_SCRATCH_BYTES (64 MiB) that the library holds on every device
+ * it runs on (resolved at soap_create) instead of the context's growable
+ * buffer.  This call allocates nothing and records no timing events; the
+ * neighbour list must already be built (soap_build_neighbors allocates).
+ * Limit: count * 32 S n_max (l_max+1)^2 bytes <= SOAP_STATIC_SCRATCH_BYTES
+ * (e.g. 2674 centers of the 2-species n_max 8, l_max 6 basis), else
+ * SOAP_ECAPACITY with nothing enqueued; larger structures go through in
+ * batches.  Every call on one device shares that device's array, which
+ * keeps the last call's contents (every entry read is written first, so
+ * nothing needs clearing): calls that overlap on one device, on different
+ * streams or from different contexts or host threads, race and must be
+ * serialised by the caller.  jac_edge_dev must not be NULL for count > 0.
+ * Errors: SOAP_EINVAL, SOAP_ESTATE, SOAP_ECAPACITY, SOAP_EHIP.
+ */
+int soap_derivatives_batch_noalloc(soap_ctx *ctx, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
+                                   void *jac_self_dev, void *stream);
 
 /*
  * Split the centers of the neighbour list into consecutive batches whose

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -47,6 +48,35 @@ struct DevBuf {
 constexpr size_t LDS_HARD_LIMIT = 159 * 1024; // leaves room for static LDS
 
 thread_local std::string g_create_error = "";
+
+// Coefficient scratch of soap_derivatives_batch_noalloc: a fixed device array
+// that every device the library runs on holds until the process ends.  Host
+// code never uses the array's name as an address (on the host it is only a
+// stand-in for the symbol): soap_create resolves each device's own address
+// once, with that device current, and the entry point passes that address
+// to the kernels.
+static __device__ __align__(256) unsigned char scratch[SOAP_STATIC_SCRATCH_BYTES];
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[MAX_DEVICES] = {};
+hipError_t g_scratch_err[MAX_DEVICES] = {};
+bool g_scratch_done[MAX_DEVICES] = {};
+
+// the static scratch of `device` (the current device), resolved on first use
+hipError_t static_scratch(int device, void **out) {
+    *out = nullptr;
+    if (device < 0 || device >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_done[device]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_err[device] = e;
+        g_scratch_ptr[device] = e == hipSuccess ? p : nullptr;
+        g_scratch_done[device] = true;
+    }
+    *out = g_scratch_ptr[device];
+    return g_scratch_err[device];
+}
 
 } // namespace
 
@@ -98,6 +128,7 @@ struct soap_ctx {
     };
     std::vector<Rec> recs;
     std::vector<hipEvent_t> pool;
+    void *static_scratch = nullptr; // this device's static scratch (soap_derivatives_batch_noalloc)
     std::string err;
 };
 
@@ -404,8 +435,8 @@ struct SegTimer {
     int seg;
     hipStream_t st;
     hipEvent_t a = nullptr;
-    SegTimer(soap_ctx *c_, int seg_, hipStream_t st_) : c(c_), seg(seg_), st(st_) {
-        if (c->timing && (a = take_event(c)) != nullptr) (void)hipEventRecord(a, st);
+    SegTimer(soap_ctx *c_, int seg_, hipStream_t st_, bool on = true) : c(c_), seg(seg_), st(st_) {
+        if (on && c->timing && (a = take_event(c)) != nullptr) (void)hipEventRecord(a, st);
     }
     void done() {
         if (!a) return;
@@ -488,6 +519,7 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
     hipError_t e = hipGetDevice(&c->device);
     if (e == hipSuccess) e = set_lds_limits();
     if (e == hipSuccess) e = hipHostMalloc((void **)&c->h_flags, 64, hipHostMallocDefault);
+    if (e == hipSuccess) e = static_scratch(c->device, &c->static_scratch);
     if (e != hipSuccess) {
         g_create_error = std::string("HIP setup failed: ") + hipGetErrorString(e);
         delete c;
@@ -785,8 +817,9 @@ int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, voi
 // mode as launch_density: 0 descriptor / coefficients, 1 descriptor + Jacobian,
 // 2 coefficient Jacobian.  scratch: the Jacobian path's coefficient scratch
 // (NULL = the context's, grown as needed).
+// timed = false: no timer events (they may allocate)
 static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void *desc, void *c_out, void *jself,
-                       void *jc_edge, double *scratch, void *stream) {
+                       void *jc_edge, double *scratch, void *stream, bool timed = true) {
     if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
     int rc;
     if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
@@ -799,7 +832,7 @@ static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
-    SegTimer timer(c, 1, to_stream(stream));
+    SegTimer timer(c, 1, to_stream(stream), timed);
     hipError_t e = launch_density(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, mode, c->dens_cfg[mode],
                                   c->nw.work, &c->work_epoch, desc, c_out, jself, scratch, jc_edge, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
@@ -868,12 +901,12 @@ int soap_compute_averaged(soap_ctx *c, int32_t mode, void *desc_dev, void *strea
 
 // descriptor + Jacobian of a center batch; scratch as run_density
 static int run_derivatives(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
-                           void *jac_self_dev, double *scratch, void *stream) {
+                           void *jac_self_dev, double *scratch, void *stream, bool timed = true) {
     if (count == 0) return SOAP_OK;
-    int rc = run_density(c, 1, first, count, desc_dev, nullptr, jac_self_dev, nullptr, scratch, stream);
+    int rc = run_density(c, 1, first, count, desc_dev, nullptr, jac_self_dev, nullptr, scratch, stream, timed);
     if (rc != SOAP_OK) return rc;
     if (c->E == 0) return SOAP_OK;
-    SegTimer timer(c, 2, to_stream(stream));
+    SegTimer timer(c, 2, to_stream(stream), timed);
     hipError_t e = launch_jacobian(c->P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, c->jac_cfg,
                                    scratch ? scratch : c->b_cscratch.as<double>(), jac_edge_dev, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
@@ -913,6 +946,27 @@ int soap_derivatives_batch(soap_ctx *c, int64_t first, int64_t count, void *desc
         if (r[1] > r[0]) return fail(c, SOAP_EINVAL, "jac_edge_dev is NULL for a batch with edges");
     }
     return run_derivatives(c, first, count, desc_dev, jac_edge_dev, jac_self_dev, nullptr, stream);
+}
+
+int soap_derivatives_batch_noalloc(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
+                                   void *jac_self_dev, void *stream) {
+    if (!c) return SOAP_EINVAL;
+    int rc = check_batch(c, first, count);
+    if (rc != SOAP_OK) return rc;
+    if (count > 0 && (!desc_dev || !jac_self_dev || !jac_edge_dev))
+        return fail(c, SOAP_EINVAL, "output pointer is NULL");
+    const size_t need = scratch_bytes_per_center(c) * (size_t)count;
+    if (need > (size_t)SOAP_STATIC_SCRATCH_BYTES)
+        return fail(c, SOAP_ECAPACITY,
+                    "%lld centers need %zu bytes of coefficient scratch, above the static %d bytes (at most %lld "
+                    "centers per call for this basis)",
+                    (long long)count, need, SOAP_STATIC_SCRATCH_BYTES,
+                    (long long)(SOAP_STATIC_SCRATCH_BYTES / scratch_bytes_per_center(c)));
+    if (!c->static_scratch) return fail(c, SOAP_EHIP, "the static scratch of device %d is not available", c->device);
+    // the density kernel writes every scratch entry the later kernels read,
+    // so nothing needs clearing
+    return run_derivatives(c, first, count, desc_dev, jac_edge_dev, jac_self_dev, (double *)c->static_scratch, stream,
+                           false);
 }
 
 int soap_plan_batches(soap_ctx *c, int32_t what, int64_t budget_bytes, int64_t max_batches, int64_t *center_first,

@@ -28,7 +28,8 @@ ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_num_features", "soap_num_
                "soap_feature_labels", "soap_feature_map", "soap_build_neighbors", "soap_get_neighbors",
                "soap_set_cell", "soap_get_neighbor_images",
                "soap_compute", "soap_coefficients", "soap_coefficient_derivatives", "soap_compute_averaged",
-               "soap_derivatives", "soap_compute_batch", "soap_derivatives_batch", "soap_plan_batches",
+               "soap_derivatives", "soap_compute_batch", "soap_derivatives_batch", "soap_derivatives_batch_noalloc",
+               "soap_plan_batches",
                "soap_scatter_dense", "soap_timing",
                "soap_last_error", "soap_destroy")
 
@@ -80,6 +81,8 @@ def load_library(path: str = LIB_PATH):
     L.soap_compute_batch.argtypes = [vp, i64, i64, vp, vp]
     L.soap_derivatives_batch.restype = ctypes.c_int
     L.soap_derivatives_batch.argtypes = [vp, i64, i64, vp, vp, vp, vp]
+    L.soap_derivatives_batch_noalloc.restype = ctypes.c_int
+    L.soap_derivatives_batch_noalloc.argtypes = [vp, i64, i64, vp, vp, vp, vp]
     L.soap_plan_batches.restype = ctypes.c_int
     L.soap_plan_batches.argtypes = [vp, i32, i64, i64, vp, vp, ctypes.POINTER(i64)]
     L.soap_scatter_dense.restype = ctypes.c_int
