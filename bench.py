@@ -259,7 +259,7 @@ DTYPE_LABEL = {
 
 
 def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False, arith="mixed",
-        cpu_budget_s=12.0):
+        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
@@ -267,6 +267,12 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
     out_bytes = 8 if dtype == "float64" else 4
     dev = torch.device("cuda:0")
     sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype, arith=arith)
+    if desc_tile:
+        sp._check(sp._L.soap_set_option(sp._h, b"desc_tile", int(desc_tile)))
+    if pipeline is not None:
+        sp._check(sp._L.soap_set_option(sp._h, b"pipeline", int(pipeline)))
+    if pipeline_density_wg is not None:
+        sp._check(sp._L.soap_set_option(sp._h, b"pipeline_density_wg", int(pipeline_density_wg)))
     if periodic:
         lo = st.pos.min(axis=0) - np.float32(0.8)
         st = type(st)((st.pos - lo).astype(np.float32), st.Z, st.radius, st.draws, dict(st.recipe, periodic=True))
@@ -327,8 +333,11 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
 
     jac = wl.jacobian and mode == "derivatives"
     alg = algorithmic(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, jac)
-    kern = {"neighbors": seg_ms[0] / max(seg_n[0], 1), "density": seg_ms[1] / max(seg_n[1], 1),
-            "jacobian": seg_ms[2] / max(seg_n[2], 1)}
+    # per step (a pipelined step launches its kernels once per center chunk;
+    # the chunks' Jacobian launches then overlap the density launches)
+    kern = {"neighbors": seg_ms[0] / steps, "density": seg_ms[1] / steps, "jacobian": seg_ms[2] / steps,
+            "launches_per_step": {"neighbors": int(seg_n[0]) // steps, "density": int(seg_n[1]) // steps,
+                                  "jacobian": int(seg_n[2]) // steps}}
     if mode == "cc":
         # the density kernel's gradient stores dominate: HBM-bound
         b = cc_bytes(sp, wl, nc, E, out_bytes)
@@ -369,7 +378,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
                    "features": sp.n_features,
                    "edge_features": sp.n_edge_features},
         "kernel_ms": kern,
-        "kernel_timing": "HIP events per segment over a second pass of the K steps",
+        "kernel_timing": "HIP events per segment, on the stream each kernel runs on, over a second pass of the "
+                         "K steps; per-step sums",
         "step_alg_bytes": alg["step"],
         "step_hbm_fraction": alg["step"] / (ms_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
         "wall_s": wall,
@@ -412,6 +422,11 @@ def main():
     ap.add_argument("--periodic", action="store_true")
     ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for every radial basis; write JSONL here")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pipeline", type=int, default=None, help="center chunks of a pipelined derivatives call")
+    ap.add_argument("--pipeline-density-wg", type=int, default=None,
+                    help="density workgroups per CU while pipelined (0 = as planned)")
+    ap.add_argument("--desc-tile", type=int, default=0, choices=[0, -1, 16, 32, 64],
+                    help="GTO descriptor kernel: 0 automatic, -1 the shared density kernel, else edges per chunk")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -433,7 +448,7 @@ def main():
         return
     wl = workload_by_name(a.workload or "water1000")
     line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic,
-               arith=a.arith)
+               arith=a.arith, desc_tile=a.desc_tile, pipeline=a.pipeline, pipeline_density_wg=a.pipeline_density_wg)
     if a.workload is None and a.mode == "derivatives" and not a.periodic:
         # the same headline in the paper's arithmetic (float64 internally,
         # float32 outputs), and the other workloads, each with its own

@@ -131,7 +131,13 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  *              (default 64; Sec. 3.1, the fixed Gauss-Legendre rule on
  *              [0, r_cut]); rebuilds the quadrature table;
  *   "timing" : 1 = record HIP events around every segment of later calls
- *              (see soap_timing), 0 = off (default).
+ *              (see soap_timing), 0 = off (default);
+ *   "desc_tile": kernel choice of the GTO descriptor path (a tuning knob;
+ *              results are identical either way up to rounding order):
+ *              0 = automatic (default), -1 = the density kernel shared with
+ *              the Jacobian path, 16 / 32 / 64 = the descriptor kernel
+ *              whose waves each own whole centers, with at most that many
+ *              edges per chunk (the widest that fits on chip).
  * Options take effect for calls made after this one; changing "dtype"
  * discards the neighbour list.  Errors: SOAP_EINVAL.
  */

@@ -117,6 +117,16 @@ struct soap_ctx {
     // one path still serves the others (the descriptor path is required)
     bool dens_ok[3] = {false, false, false}, out_ok = false, jac_ok = false;
     JacLaunch jac_cfg{};
+    DescLaunch desc_cfg{};
+    DjacLaunch djac_cfg{};
+    int djac_tile = -1; // option "djac_tile": 0 auto, -1 never k_djac (default), else the widest chunk
+    // pipelined derivatives: the density kernel of center chunk k + 1 on the
+    // caller's stream beside the Jacobian kernel of chunk k on a second one
+    int pipe_chunks = 1;         // option "pipeline": chunks per call (1 = one stream)
+    int pipe_density_wg = 0;     // option "pipeline_density_wg": density workgroups per CU (0 = as planned)
+    hipStream_t aux = nullptr;   // the second stream (default priority)
+    std::vector<hipEvent_t> pipe_ev;
+    int desc_tile = 0; // option "desc_tile": 0 auto, -1 never k_desc, else edges per chunk
     OutPlan out_plan{};
     int groups[3] = {1, 1, 1};
     int lgrp[3][MAX_GROUPS + 1]{};
@@ -293,6 +303,40 @@ int plan_launches(soap_ctx *c) {
             bestW = W;
         }
     }
+    // descriptor kernel: the widest chunk of edges that keeps at least two
+    // workgroups (of four waves) resident per CU; an explicit "desc_tile" is
+    // the widest chunk tried, and any chunk that fits at all is taken
+    c->desc_cfg = DescLaunch{};
+    int ql = 0, na = 0;
+    if (c->desc_tile >= 0 && desc_shape(P, &ql, &na)) {
+        const int cand[3] = {64, 32, 16};
+        for (int W : cand) {
+            if (c->desc_tile > 0 && W > c->desc_tile) continue;
+            const size_t lds = desc_lds_bytes(P, W, st64);
+            if (lds > LDS_HARD_LIMIT) continue;
+            const int b = desc_blocks_per_cu(f64, ar64, ql, na, lds);
+            if (b >= (c->desc_tile > 0 ? 1 : 2)) {
+                c->desc_cfg = DescLaunch{W, ql, na, lds, ncu * b};
+                break;
+            }
+        }
+    }
+    // density step of the Jacobian path (GTO): the widest chunk of edges that
+    // keeps at least two workgroups resident per CU
+    c->djac_cfg = DjacLaunch{};
+    int qt = 0, na2 = 0, sr = 0;
+    if (c->djac_tile >= 0 && djac_shape(P, &qt, &na2, &sr)) {
+        for (int W : {64, 32}) {
+            if (c->djac_tile > 0 && W > c->djac_tile) continue;
+            const size_t lds = djac_lds_bytes(P, W, st64);
+            if (lds > LDS_HARD_LIMIT) continue;
+            const int b = djac_blocks_per_cu(f64, ar64, qt, na2, sr, lds);
+            if (b >= (c->djac_tile > 0 ? 1 : 2)) {
+                c->djac_cfg = DjacLaunch{W, qt, na2, sr, lds, ncu * b};
+                break;
+            }
+        }
+    }
     c->jac_ok = bestW > 0;
     c->jac_cfg.W = bestW;
     c->jac_cfg.lds = bestW > 0 ? jacobian_lds_bytes(P, bestW, st64) : 0;
@@ -465,6 +509,13 @@ Rows rows_of(const soap_ctx *c, int64_t first, int64_t count) {
     R.spec = c->b_spec.as<uint8_t>();
     R.row_ptr = c->b_row.as<int64_t>() + first;
     R.cols = c->b_cols.as<int32_t>();
+    R.e_origin = R.row_ptr;
+    return R;
+}
+// centers [cf, cf + cn) of the output batch that starts at center `first`
+Rows rows_part(const soap_ctx *c, int64_t first, int64_t cf, int64_t cn) {
+    Rows R = rows_of(c, cf, cn);
+    R.e_origin = c->b_row.as<int64_t>() + first;
     return R;
 }
 Rows rows_of(const soap_ctx *c) { return rows_of(c, 0, c->nc); }
@@ -549,6 +600,28 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         if (value == c->arith) return SOAP_OK;
         c->arith = (int)value;
         return plan_launches(c); // staging sizes and occupancy of the kernels
+    }
+    if (!std::strcmp(key, "pipeline")) {
+        if (value < 1 || value > 16) return fail(c, SOAP_EINVAL, "pipeline must be in 1..16");
+        c->pipe_chunks = (int)value;
+        return SOAP_OK;
+    }
+    if (!std::strcmp(key, "pipeline_density_wg")) {
+        if (value < 0 || value > 16) return fail(c, SOAP_EINVAL, "pipeline_density_wg must be in 0..16");
+        c->pipe_density_wg = (int)value;
+        return SOAP_OK;
+    }
+    if (!std::strcmp(key, "djac_tile")) {
+        if (value != 0 && value != -1 && value != 32 && value != 64)
+            return fail(c, SOAP_EINVAL, "djac_tile must be 0, -1, 32 or 64");
+        c->djac_tile = (int)value;
+        return plan_launches(c);
+    }
+    if (!std::strcmp(key, "desc_tile")) {
+        if (value != 0 && value != -1 && value != 16 && value != 32 && value != 64)
+            return fail(c, SOAP_EINVAL, "desc_tile must be 0, -1, 16, 32 or 64");
+        c->desc_tile = (int)value;
+        return plan_launches(c);
     }
     if (!std::strcmp(key, "timing")) {
         if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "timing must be 0 or 1");
@@ -812,18 +885,27 @@ int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, voi
     return e == hipSuccess ? SOAP_OK : hip_fail(c, e, "soap_get_neighbors");
 }
 
+// whether the kernels of a density mode fit this basis (mode 1 also needs the
+// edge Jacobian kernel, and the output kernel when the density kernel splits
+// l into groups; the one-workgroup-per-center kernel needs neither split)
+static bool jacobian_path_ok(const soap_ctx *c, int mode) {
+    if (mode == 1 && c->djac_cfg.W > 0) return c->jac_ok;
+    return c->dens_ok[mode] && (mode != 1 || (c->jac_ok && (c->groups[1] == 1 || c->out_ok)));
+}
+
 // Centers [first, first + count) of the neighbour list; outputs are indexed
 // from the batch's first center (and edge).
 // mode as launch_density: 0 descriptor / coefficients, 1 descriptor + Jacobian,
 // 2 coefficient Jacobian.  scratch: the Jacobian path's coefficient scratch
 // (NULL = the context's, grown as needed).
-// timed = false: no timer events (they may allocate)
+// timed = false: no timer events (they may allocate).  wg_per_cu > 0 caps
+// the persistent density kernel's workgroups per CU.
 static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void *desc, void *c_out, void *jself,
-                       void *jc_edge, double *scratch, void *stream, bool timed = true) {
+                       void *jc_edge, double *scratch, void *stream, bool timed = true, int wg_per_cu = 0) {
     if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
     int rc;
     if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
-    if (!c->dens_ok[mode] || (mode == 1 && (!c->jac_ok || (c->groups[1] > 1 && !c->out_ok))))
+    if (!jacobian_path_ok(c, mode))
         return fail(c, SOAP_EINVAL, "basis too large for the on-chip memory of the %s kernels",
                     mode == 2 ? "coefficient Jacobian" : "Jacobian");
     const Params P = params_for(c, mode);
@@ -833,7 +915,33 @@ static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void
         scratch = c->b_cscratch.as<double>();
     }
     SegTimer timer(c, 1, to_stream(stream), timed);
-    hipError_t e = launch_density(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, mode, c->dens_cfg[mode],
+    if (mode == 0 && c->desc_cfg.W > 0) { // one wave per center
+        hipError_t e = launch_desc(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, c->desc_cfg, desc, c_out,
+                                   to_stream(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "descriptor kernel");
+        timer.done();
+        return SOAP_OK;
+    }
+    if (mode == 1 && c->djac_cfg.W > 0) { // one workgroup per center
+        DjacLaunch dj = c->djac_cfg;
+        if (wg_per_cu > 0) {
+            int ncu = 256;
+            (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
+            dj.blocks = std::max(1, std::min(dj.blocks, ncu * wg_per_cu));
+        }
+        hipError_t e = launch_djac(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, dj, desc, jself,
+                                   scratch, to_stream(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "density kernel");
+        timer.done();
+        return SOAP_OK;
+    }
+    DensityLaunch cfg = c->dens_cfg[mode];
+    if (wg_per_cu > 0) {
+        int ncu = 256;
+        (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
+        cfg.blocks = std::max(1, std::min(cfg.blocks, ncu * wg_per_cu / std::max(1, P.n_groups)));
+    }
+    hipError_t e = launch_density(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, mode, cfg,
                                   c->nw.work, &c->work_epoch, desc, c_out, jself, scratch, jc_edge, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "density kernel");
     if (mode == 1 && P.n_groups > 1) { // with one l-group the density kernel writes desc and jself
@@ -899,10 +1007,62 @@ int soap_compute_averaged(soap_ctx *c, int32_t mode, void *desc_dev, void *strea
     return SOAP_OK;
 }
 
+// Pipelined descriptor + Jacobian: the batch in K center chunks; the density
+// kernel of each chunk on `stream`, the Jacobian kernel of the chunk on the
+// context's second stream once the chunk's coefficients are in scratch, so
+// that the compute-bound density kernel of chunk k + 1 runs beside the
+// store-bound Jacobian kernel of chunk k; `stream` waits for the last one.
+static int run_derivatives_pipelined(soap_ctx *c, int64_t first, int64_t count, int K, void *desc_dev,
+                                     void *jac_edge_dev, void *jac_self_dev, void *stream) {
+    hipStream_t st = to_stream(stream);
+    hipError_t e = hipSuccess;
+    if (!c->aux) e = hipStreamCreateWithFlags(&c->aux, hipStreamNonBlocking);
+    while (e == hipSuccess && (int)c->pipe_ev.size() < K + 1) {
+        hipEvent_t ev = nullptr;
+        e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e == hipSuccess) c->pipe_ev.push_back(ev);
+    }
+    if (e == hipSuccess) e = c->b_cscratch.ensure(scratch_bytes_per_center(c) * (size_t)count);
+    if (e != hipSuccess) return hip_fail(c, e, "pipelined derivatives (setup)");
+    double *scratch = c->b_cscratch.as<double>();
+    const size_t elt = c->built_f64 ? 8 : 4, pc = scratch_bytes_per_center(c) / 8;
+    for (int k = 0; k < K; ++k) {
+        const int64_t cf = first + count * k / K, cn = first + count * (k + 1) / K - cf;
+        if (cn == 0) continue;
+        const size_t o = (size_t)(cf - first);
+        int rc = run_density(c, 1, cf, cn, (char *)desc_dev + o * c->F * elt, nullptr,
+                             (char *)jac_self_dev + o * 3 * c->F * elt, nullptr, scratch + o * pc, stream, true,
+                             c->pipe_density_wg);
+        if (rc != SOAP_OK) return rc;
+        if ((e = hipEventRecord(c->pipe_ev[k], st)) != hipSuccess ||
+            (e = hipStreamWaitEvent(c->aux, c->pipe_ev[k], 0)) != hipSuccess)
+            return hip_fail(c, e, "pipelined derivatives (events)");
+        SegTimer timer(c, 2, c->aux);
+        e = launch_jacobian(c->P, rows_part(c, first, cf, cn), c->pos, c->built_f64, c->ar64, c->jac_cfg,
+                            scratch + o * pc, jac_edge_dev, c->aux);
+        if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
+        timer.done();
+    }
+    if ((e = hipEventRecord(c->pipe_ev[K], c->aux)) != hipSuccess ||
+        (e = hipStreamWaitEvent(st, c->pipe_ev[K], 0)) != hipSuccess)
+        return hip_fail(c, e, "pipelined derivatives (join)");
+    return SOAP_OK;
+}
+
 // descriptor + Jacobian of a center batch; scratch as run_density
 static int run_derivatives(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
                            void *jac_self_dev, double *scratch, void *stream, bool timed = true) {
     if (count == 0) return SOAP_OK;
+    // the pipelined path needs its own stream, events and the context's
+    // scratch: not for the allocation-free entry point
+    if (timed && !scratch && c->pipe_chunks > 1 && c->E > 0 && count >= 2 * c->pipe_chunks) {
+        int rc;
+        if (!jacobian_path_ok(c, 1))
+            return fail(c, SOAP_EINVAL, "basis too large for the on-chip memory of the Jacobian kernels");
+        if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
+        return run_derivatives_pipelined(c, first, count, c->pipe_chunks, desc_dev, jac_edge_dev, jac_self_dev,
+                                         stream);
+    }
     int rc = run_density(c, 1, first, count, desc_dev, nullptr, jac_self_dev, nullptr, scratch, stream, timed);
     if (rc != SOAP_OK) return rc;
     if (c->E == 0) return SOAP_OK;
@@ -1063,6 +1223,8 @@ void soap_destroy(soap_ctx *c) {
                       &c->b_pos_ext, &c->b_Z_ext, &c->b_map_atom, &c->b_map_img, &c->b_iota})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
+    for (hipEvent_t e : c->pipe_ev) (void)hipEventDestroy(e);
+    if (c->aux) (void)hipStreamDestroy(c->aux);
     for (auto &r : c->recs) {
         (void)hipEventDestroy(r.a);
         (void)hipEventDestroy(r.b);

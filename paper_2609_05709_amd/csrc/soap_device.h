@@ -80,6 +80,13 @@ __device__ __forceinline__ void load4(const float *p, double &a, double &b, doub
 // next integer
 __device__ __forceinline__ int qdiv(int x, float inv) { return (int)(((float)x + 0.5f) * inv); }
 
+// Read-only basis tables seen through the constant address space: a
+// wave-uniform read then compiles to a scalar load from the scalar cache.
+// Through a generic pointer, which may alias the kernel's own LDS and
+// global stores, it stays a per-lane vector load on the latency path.
+typedef const __attribute__((address_space(4))) double *cdptr;
+__device__ __forceinline__ cdptr as_const(const double *p) { return (cdptr)p; }
+
 // ---------------------------------------------------------------------------
 // Double-double arithmetic (unevaluated sums hi + lo) for the compensated GTO
 // radial sums: Knuth's two-sum, the fused multiply-add two-product.  Device
@@ -156,10 +163,9 @@ __device__ __forceinline__ dd dd_exp_neg(dd x) {
 //   S_l,m = Nt_lm R_l C_m, S_l,-m = Nt_lm R_l S_m, Nt_lm = N_lm (2m-1)!! / (l-m)!.
 // Stores l in [l_lo, l_hi) at Y[(l^2 + l +- m - lm_base) * ls].
 // ---------------------------------------------------------------------------
-template <typename YT>
-__device__ __forceinline__ void sh_col_y(int m, int l_lo, int l_hi, double x, double y, double z,
-                                         const double *__restrict__ Nt, int ldN, YT *__restrict__ Y, int ls,
-                                         int lm_base) {
+template <typename YT, typename NtPtr = const double *__restrict__>
+__device__ __forceinline__ void sh_col_y(int m, int l_lo, int l_hi, double x, double y, double z, NtPtr Nt, int ldN,
+                                         YT *__restrict__ Y, int ls, int lm_base) {
     const double r2 = x * x + y * y + z * z;
     double c = 1.0, s = 0.0;
     for (int k = 0; k < m; ++k) {
@@ -960,7 +966,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
     // (vmcnt counts loads and stores together)
     for (int k = tid; k < n; k += BSD) c0[k] = P.c0[k];
     // structure index of the batch's first edge: edge outputs are batch-local
-    const int64_t ebase = CCJ ? R.row_ptr[0] : 0;
+    const int64_t ebase = CCJ ? *R.e_origin : 0;
 
     // the next center: its rows are loaded before the current center's
     // outputs are stored, so those loads never wait behind the stores
@@ -1153,6 +1159,499 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
             }
         }
         lds_barrier(); // the outputs are read from cacc before the next center clears it
+    }
+}
+
+// All real solid harmonics of one edge per lane (l < lw), by the column
+// recurrence of sh_col_y, into Y[lm * ls]; Nt in LDS (wave-uniform reads).
+template <typename YT>
+__device__ __forceinline__ void sh_all_lane(double x, double y, double z, const double *__restrict__ Nt, int ldN,
+                                            int lw, YT *__restrict__ Y, int ls) {
+    const double r2 = x * x + y * y + z * z;
+    double c = 1.0, s = 0.0; // (x + i y)^m
+    for (int m = 0; m < lw; ++m) {
+        double R1 = 0.0, R = 1.0; // R_{l-1}, R_l
+        for (int l = m; l < lw; ++l) {
+            if (l > m) {
+                const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
+                const double Rn = a * z * R - b * r2 * R1;
+                R1 = R;
+                R = Rn;
+            }
+            const double v = Nt[l * ldN + m] * R;
+            const int o = l * l + l;
+            if (m == 0) {
+                Y[o * ls] = (YT)v;
+            } else {
+                Y[(o + m) * ls] = (YT)(v * c);
+                Y[(o - m) * ls] = (YT)(v * s);
+            }
+        }
+        const double cn = x * c - y * s;
+        s = x * s + y * c;
+        c = cn;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_desc: the descriptor (and coefficients) of the GTO basis.  Persistent
+// workgroups of NWC waves, one center at a time per workgroup (centers
+// blockIdx + k gridDim), in two phases per chunk of up to W edges of the
+// center's row:
+//   1. staging, lane = edge, split over the waves by task: task l < l_max + 1
+//      is the radial factors of degree l, B_nl = sum_k betaC^l_nk e^{-a'_kl r^2}
+//      (Eq. gto-coefficients); task l_max + 1 is the real solid harmonics
+//      S_lm (sh_all_lane).  Wave w runs tasks w, w + NWC, ...  Every
+//      coefficient read is wave-uniform (the tables sit in LDS, copied once
+//      per workgroup), and every lane works on its own edge;
+//   2. projection, thread = (lm, group of AG radial indices a): each thread
+//      owns those coefficients c_{a lm} of the current species in float64
+//      registers and adds B_al S_lm over the chunk's edges in row order
+//      (Eq. projection); one harmonic read serves AG products.  Rows are sorted by species; at a species change the
+//      registers go to the center's coefficient block.
+// Every coefficient has one owner thread and every sum runs in row order:
+// the results are bitwise repeatable with no ordering protocol.  Then the
+// on-site term, and the power spectrum on the matrix cores (power_tiles,
+// Eq. powerspectrum).  The next center's first chunk of edge vectors is
+// gathered into registers before this center's output stores: a load issued
+// after a run of stores waits for all of them.
+// ST: staging precision (the output precision, or double for float64
+// arithmetic with float32 outputs).  QT (lm, group) tasks per thread, AG
+// radial indices per group and NA >= n_max, fixed at compile time so that
+// the accumulators stay in registers.
+// ---------------------------------------------------------------------------
+constexpr int NWC = 4, BSC = 64 * NWC;
+
+// LDS of k_desc.  Float64: K_l, the harmonic normalisations Nt, a'_kl [l][k],
+// betaC [l][n][k], the on-site terms, the coefficient block [S][n][L].  At
+// the staging precision: harmonics [lm][W + 1] and radial factors
+// [l][n][W + 1] (edge fastest: the staging lanes, one per edge, write
+// consecutive words), the rows of one l padded to an odd length desc_ldl;
+// the odd strides put the projection threads, which read one edge at
+// different lm (or l), on different banks.  Then the chunk's species.
+__host__ __device__ __forceinline__ int desc_ldl(int n, int W) { return (n * (W + 1)) | 1; }
+__host__ __device__ __forceinline__ size_t desc_lds_doubles(const Params &P, int W, int sb) {
+    const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n, L = (size_t)P.L;
+    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + even((size_t)P.S * n * L) +
+           even((L * (W + 1) * sb + 7) / 8) + even((lw * desc_ldl((int)n, W) * sb + 7) / 8) + even(((size_t)W + 1) / 2);
+}
+// (lm, group of ag radial indices) tasks per thread
+__host__ __device__ __forceinline__ int desc_tasks(const Params &P, int ag) {
+    return (P.L * ((P.n + ag - 1) / ag) + BSC - 1) / BSC;
+}
+
+template <typename PosT, typename OutT, typename ST, int QT, int AG, int NA>
+__global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__restrict__ pos, int W,
+                                              OutT *__restrict__ desc, OutT *__restrict__ c_out) {
+    extern __shared__ __align__(16) double smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int S = P.S, n = P.n, lmax = P.lmax, lw = lmax + 1, L = P.L, ldN = lmax + 2, Sn = S * n;
+    const int nL = n * L, SnL = S * nL, np = (n + AG - 1) / AG;
+    constexpr int SB = sizeof(ST);
+    Carver cv{smem};
+    double *Kl = cv.take(16);
+    double *Nt = cv.take((size_t)ldN * ldN);
+    double *apr = cv.take((size_t)lw * n);
+    double *bcf = cv.take((size_t)lw * n * n);
+    double *c0 = cv.take((size_t)n);
+    double *cb = cv.take((size_t)SnL); // [S][n][L]
+    const int WP = W + 1, ldl = desc_ldl(n, W);
+    ST *Yl = (ST *)cv.take(((size_t)L * WP * SB + 7) / 8);  // [lm][W + 1]
+    ST *Bl = (ST *)cv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1], rows of l padded to ldl
+    int *esp = (int *)cv.take(((size_t)W + 1) / 2);          // species of the chunk's edges
+    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
+    for (int k = tid; k < ldN * ldN; k += BSC) Nt[k] = P.Nt[k];
+    for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
+    for (int k = tid; k < lw * n * n; k += BSC) bcf[k] = P.betaC[k];
+    for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
+
+    // this thread's projection tasks: (lm, radial group) = (t % L, t / L), t = tid + BSC q
+    int lm_q[QT], l_q[QT], a_q[QT];
+    bool ok_q[QT];
+#pragma unroll
+    for (int q = 0; q < QT; ++q) {
+        const int t = tid + BSC * q, ap = t / L, lm = t - ap * L;
+        int l = (int)sqrtf((float)lm);
+        while (l * l > lm) --l;
+        while ((l + 1) * (l + 1) <= lm) ++l;
+        ok_q[q] = ap < np;
+        lm_q[q] = ok_q[q] ? lm : 0;
+        l_q[q] = ok_q[q] ? l : 0;
+        a_q[q] = ok_q[q] ? AG * ap : 0;
+    }
+    int64_t ci = blockIdx.x;
+    const int64_t stride = gridDim.x;
+    // the first chunk of a center's row, gathered by every wave, lane = edge:
+    // edge vector (float64, exact for float32 inputs) and species
+    double gx = 0.0, gy = 0.0, gz = 0.0;
+    int gs = 0;
+    int64_t e0 = 0, e1 = 0;
+    double3 pi = make_double3(0.0, 0.0, 0.0);
+    int spec_i = 0;
+    auto gather = [&](int64_t cs, int nb) {
+        if (lane < nb) {
+            const int64_t j = R.cols[cs + lane];
+            gx = (double)pos[3 * j] - pi.x;
+            gy = (double)pos[3 * j + 1] - pi.y;
+            gz = (double)pos[3 * j + 2] - pi.z;
+            gs = R.spec[j];
+        }
+    };
+    auto fetch = [&]() { // the center ci: its atom, row and first chunk
+        if (ci >= R.nc) return;
+        const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
+        pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
+        spec_i = R.spec[i];
+        e0 = R.row_ptr[ci];
+        e1 = R.row_ptr[ci + 1];
+        gather(e0, (int)((e1 - e0) < W ? (e1 - e0) : W));
+    };
+    fetch();
+    while (ci < R.nc) {
+        for (int k = tid; k < SnL; k += BSC) cb[k] = 0.0;
+        double acc[QT][AG];
+#pragma unroll
+        for (int q = 0; q < QT; ++q)
+#pragma unroll
+            for (int g = 0; g < AG; ++g) acc[q][g] = 0.0;
+        int cur = -1;
+        // registers of species cur into the coefficient block (one owner per entry)
+        auto flush = [&]() {
+#pragma unroll
+            for (int q = 0; q < QT; ++q)
+#pragma unroll
+                for (int g = 0; g < AG; ++g) {
+                    if (ok_q[q] && a_q[q] + g < n) cb[(cur * n + a_q[q] + g) * L + lm_q[q]] += acc[q][g];
+                    acc[q][g] = 0.0;
+                }
+        };
+        for (int64_t cs = e0; cs < e1; cs += W) {
+            const int nb = (int)((e1 - cs) < W ? (e1 - cs) : W);
+            if (cs != e0) gather(cs, nb); // later chunks of a long row (no stores pending)
+            lds_barrier();                // the tables, the cleared block, the previous chunk read
+            // ---- phase 1: staging, lane = edge, tasks over the waves ----
+            if (lane < nb) {
+                if (wave == 0) esp[lane] = gs;
+                const double r2 = gx * gx + gy * gy + gz * gz;
+                for (int task = wave; task <= lw; task += NWC) {
+                    if (task == lw) {
+                        sh_all_lane(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP);
+                        continue;
+                    }
+                    const int l = task;
+                    // exponentials past n_max are zero, so the clamped
+                    // coefficient reads past the row multiply zero
+                    double ex[NA];
+#pragma unroll
+                    for (int k = 0; k < NA; ++k) ex[k] = k < n ? exp(-apr[l * n + k] * r2) : 0.0;
+                    ST *bo = Bl + (size_t)l * ldl + lane;
+                    const double *bc = bcf + (size_t)l * n * n;
+                    for (int a = 0; a < n; ++a) {
+                        double b = 0.0;
+#pragma unroll
+                        for (int k = 0; k < NA; ++k) b += bc[a * n + (k < n ? k : n - 1)] * ex[k];
+                        bo[a * WP] = (ST)b;
+                    }
+                }
+            }
+            lds_barrier();
+            // ---- phase 2: projection, thread = (lm, radial pair) ----
+            for (int e = 0; e < nb; ++e) {
+                const int s = __builtin_amdgcn_readfirstlane(esp[e]);
+                if (s != cur) {
+                    if (cur >= 0) flush();
+                    cur = s;
+                }
+#pragma unroll
+                for (int q = 0; q < QT; ++q) {
+                    const double yv = ok_q[q] ? (double)Yl[lm_q[q] * WP + e] : 0.0;
+                    const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+#pragma unroll
+                    for (int g = 0; g < AG; ++g) acc[q][g] += (a_q[q] + g < n ? (double)bp[g * WP] : 0.0) * yv;
+                }
+            }
+        }
+        if (cur >= 0) flush();
+        lds_barrier();
+        // on-site term of the center (its species, l = 0)
+        if (tid < n) cb[(spec_i * n + tid) * L] += c0[tid];
+        lds_barrier();
+        // the next center's first chunk goes in before this center's stores
+        const int64_t cw = ci;
+        ci += stride;
+        fetch();
+        if (desc)
+            power_tiles<OutT>(CoefView{cb, nullptr, L, 1}, -1, Sn, 0, 0, lw, desc + cw * P.F, lw, 0,
+                              PairIndex{S, n, 1.0f / (float)n}, wave, NWC, lane, Kl);
+        if (c_out)
+            for (int k = tid; k < SnL; k += BSC) store_out(c_out + cw * SnL + k, cb[k]);
+        lds_barrier(); // cb is read before the next center clears it
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_djac: the density step of the Jacobian path for the GTO basis, in the
+// layout of k_desc (one center per workgroup of NWC waves, 64-edge chunks,
+// staging lane = edge split over the waves by task, every accumulated entry
+// owned by one thread):
+//   staging: task l: B_nl and Bh_nl = (1/r) dB_nl/dr = sum_k betaCa e_kl
+//     (Eqs. gto-coefficients, gto-derivative); the last task: the solid
+//     harmonics; wave 0 also keeps the chunk's edge vectors and species;
+//   projection, thread = (lm, pair of radial indices): per edge
+//       c_{a lm}  += B_al S_lm,
+//       D_{a lm}  += Bh_al r S_lm + B_al grad S_lm,
+//     (D = sum over neighbours of dc/dr_j = -dc/dr_i), the gradient of S_lm
+//     from at most five degree l-1 harmonics by the ladder identities of
+//     stage_edges (zero for an edge of length 0).  The sums of each species
+//     stay in registers (species slots SR >= S): the rows are sorted by
+//     species, so each species is a contiguous run of the chunk.
+// At the end of the row the registers go to the coefficient block [c, Dx, Dy,
+// Dz][S][n][L] (aliasing the staging buffers), the on-site term is added, and
+// the workgroup writes the power spectrum and the center block
+// -K_l sum_m (D^mu c^nu + c^mu D^nu) (power_tiles4, Eqs. powerspectrum,
+// powerspectrum-derivative with translational invariance) and the
+// coefficients, transposed to [lm][species n], for k_jacobian.  Each sum runs
+// in row order: deterministic with no ordering protocol.
+// ---------------------------------------------------------------------------
+// LDS doubles of k_djac: tables (K_l, Nt, a', betaC, betaCa, c0), then the
+// larger of the staging buffers (harmonics [lm][W+1], B and Bh [l][n][W+1]
+// with odd row lengths, edge vectors [W][4], species [W], species run bounds)
+// and the coefficient block 4 S n L
+__host__ __device__ __forceinline__ size_t djac_table_doubles(const Params &P) {
+    const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n;
+    return 16 + even(ldN * ldN) + even(lw * n) + 2 * even(lw * n * n) + even(n);
+}
+__host__ __device__ __forceinline__ size_t djac_stage_doubles(const Params &P, int W, int sb) {
+    const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1, n = (size_t)P.n;
+    const size_t stage = even((L * (W + 1) * sb + 7) / 8) + 2 * even((lw * desc_ldl((int)n, W) * sb + 7) / 8) +
+                         4 * (size_t)W + even(((size_t)W + 1) / 2) + 16;
+    const size_t block = 4 * (size_t)P.S * n * L;
+    return stage > block ? stage : block;
+}
+__host__ __device__ __forceinline__ size_t djac_lds_doubles(const Params &P, int W, int sb) {
+    return djac_table_doubles(P) + djac_stage_doubles(P, W, sb);
+}
+
+template <typename PosT, typename OutT, typename ST, int QT, int NA, int SR>
+__global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__restrict__ pos, int W,
+                                              OutT *__restrict__ desc, OutT *__restrict__ jself,
+                                              double *__restrict__ c_scratch) {
+    extern __shared__ __align__(16) double smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int S = P.S, n = P.n, lmax = P.lmax, lw = lmax + 1, L = P.L, ldN = lmax + 2, Sn = S * n;
+    const int nL = n * L, SnL = S * nL, np = (n + 1) / 2;
+    constexpr int SB = sizeof(ST);
+    Carver cv{smem};
+    double *Kl = cv.take(16);
+    double *Nt = cv.take((size_t)ldN * ldN);
+    double *apr = cv.take((size_t)lw * n);
+    double *bcf = cv.take((size_t)lw * n * n);
+    double *bca = cv.take((size_t)lw * n * n);
+    double *c0 = cv.take((size_t)n);
+    double *stage = cv.take(0);
+    const int WP = W + 1, ldl = desc_ldl(n, W);
+    Carver sv{stage};
+    ST *Yl = (ST *)sv.take(((size_t)L * WP * SB + 7) / 8);  // [lm][W + 1]
+    ST *Bl = (ST *)sv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1]
+    ST *Hl = (ST *)sv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1]
+    double *geo = sv.take(4 * (size_t)W);                    // [W][x, y, z, r]
+    int *esp = (int *)sv.take(((size_t)W + 1) / 2);          // species of the chunk's edges
+    int *run = (int *)sv.take(16);                           // species run bounds of the chunk
+    double *cb = stage;                                      // [c, Dx, Dy, Dz][S][n][L], after the row
+    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
+    for (int k = tid; k < ldN * ldN; k += BSC) Nt[k] = P.Nt[k];
+    for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
+    for (int k = tid; k < lw * n * n; k += BSC) {
+        bcf[k] = P.betaC[k];
+        bca[k] = P.betaCa[k];
+    }
+    for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
+
+    // this thread's tasks: (lm, radial pair) = (t % L, t / L), t = tid + BSC q,
+    // and the gradient of its S_lm: gx = g0 Y'_0 + g1 Y'_1, gy = g2 Y'_2 + g3 Y'_3,
+    // gz = g4 Y'_4, Y'_k = the degree l-1 harmonic gi[k] (coefficient 0 where
+    // the identity has no term or the order is out of range)
+    int lm_q[QT], l_q[QT], a_q[QT], gi[QT][5];
+    double gc[QT][5];
+    bool ok_q[QT];
+#pragma unroll
+    for (int q = 0; q < QT; ++q) {
+        const int t = tid + BSC * q, ap = t / L, lm = t - ap * L;
+        int l = (int)sqrtf((float)lm);
+        while (l * l > lm) --l;
+        while ((l + 1) * (l + 1) <= lm) ++l;
+        ok_q[q] = ap < np;
+        lm_q[q] = ok_q[q] ? lm : 0;
+        l_q[q] = ok_q[q] ? l : 0;
+        a_q[q] = ok_q[q] ? 2 * ap : 0;
+        const int m = lm_q[q] - l_q[q] * l_q[q] - l_q[q], mm = m < 0 ? -m : m, lp = l_q[q] - 1;
+        const int tg = l_q[q] * (l_q[q] + 1) / 2 + mm;
+        const double cA = P.gcoef[4 * tg], cB = P.gcoef[4 * tg + 1], cC = P.gcoef[4 * tg + 2];
+        int k[5];
+        double c[5];
+        if (m == 0) {
+            k[0] = 1; c[0] = -cA; k[1] = 0; c[1] = 0.0;
+            k[2] = -1; c[2] = -cA; k[3] = 0; c[3] = 0.0;
+            k[4] = 0; c[4] = cC;
+        } else if (m > 0) {
+            k[0] = m + 1; c[0] = -cA; k[1] = m - 1; c[1] = cB;
+            k[2] = -(m + 1); c[2] = -cA; k[3] = -(m - 1); c[3] = m > 1 ? -cB : 0.0;
+            k[4] = m; c[4] = cC;
+        } else {
+            k[0] = -(mm + 1); c[0] = -cA; k[1] = -(mm - 1); c[1] = mm > 1 ? cB : 0.0;
+            k[2] = mm + 1; c[2] = cA; k[3] = mm - 1; c[3] = cB;
+            k[4] = -mm; c[4] = cC;
+        }
+#pragma unroll
+        for (int j = 0; j < 5; ++j) {
+            const bool in = ok_q[q] && lp >= 0 && k[j] >= -lp && k[j] <= lp;
+            gi[q][j] = in ? lp * lp + lp + k[j] : 0;
+            gc[q][j] = in ? c[j] : 0.0;
+        }
+    }
+    int64_t ci = blockIdx.x;
+    const int64_t stride = gridDim.x;
+    double gx = 0.0, gy = 0.0, gz = 0.0;
+    int gs = 0;
+    int64_t e0 = 0, e1 = 0;
+    double3 pi = make_double3(0.0, 0.0, 0.0);
+    int spec_i = 0;
+    auto gather = [&](int64_t cs, int nb) {
+        if (lane < nb) {
+            const int64_t j = R.cols[cs + lane];
+            gx = (double)pos[3 * j] - pi.x;
+            gy = (double)pos[3 * j + 1] - pi.y;
+            gz = (double)pos[3 * j + 2] - pi.z;
+            gs = R.spec[j];
+        }
+    };
+    auto fetch = [&]() {
+        if (ci >= R.nc) return;
+        const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
+        pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
+        spec_i = R.spec[i];
+        e0 = R.row_ptr[ci];
+        e1 = R.row_ptr[ci + 1];
+        gather(e0, (int)((e1 - e0) < W ? (e1 - e0) : W));
+    };
+    fetch();
+    while (ci < R.nc) {
+        double acc[SR][QT][2][4];
+#pragma unroll
+        for (int sr = 0; sr < SR; ++sr)
+#pragma unroll
+            for (int q = 0; q < QT; ++q)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) acc[sr][q][a][d] = 0.0;
+        for (int64_t cs = e0; cs < e1; cs += W) {
+            const int nb = (int)((e1 - cs) < W ? (e1 - cs) : W);
+            if (cs != e0) gather(cs, nb);
+            lds_barrier(); // the tables; the previous chunk's (or center's) readers of the staging region
+            // ---- staging, lane = edge, tasks over the waves ----
+            if (wave == 0) {
+                if (lane < nb) {
+                    esp[lane] = gs;
+                    geo[4 * lane] = gx;
+                    geo[4 * lane + 1] = gy;
+                    geo[4 * lane + 2] = gz;
+                    geo[4 * lane + 3] = sqrt(gx * gx + gy * gy + gz * gz);
+                }
+                // run bounds: the chunk's edges of species below sr (rows are sorted by species)
+#pragma unroll
+                for (int sr = 0; sr <= SR; ++sr) {
+                    const int cnt = __popcll(__ballot(lane < nb && gs < sr));
+                    if (lane == 0) run[sr] = cnt;
+                }
+            }
+            if (lane < nb) {
+                const double r2 = gx * gx + gy * gy + gz * gz;
+                for (int task = wave; task <= lw; task += NWC) {
+                    if (task == lw) {
+                        sh_all_lane(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP);
+                        continue;
+                    }
+                    const int l = task;
+                    double ex[NA];
+#pragma unroll
+                    for (int k = 0; k < NA; ++k) ex[k] = k < n ? exp(-apr[l * n + k] * r2) : 0.0;
+                    ST *bo = Bl + (size_t)l * ldl + lane, *ho = Hl + (size_t)l * ldl + lane;
+                    const double *bc = bcf + (size_t)l * n * n, *hc = bca + (size_t)l * n * n;
+                    for (int a = 0; a < n; ++a) {
+                        double b = 0.0, h = 0.0;
+#pragma unroll
+                        for (int k = 0; k < NA; ++k) {
+                            const int kk = k < n ? k : n - 1;
+                            b += bc[a * n + kk] * ex[k];
+                            h += hc[a * n + kk] * ex[k];
+                        }
+                        bo[a * WP] = (ST)b;
+                        ho[a * WP] = (ST)h;
+                    }
+                }
+            }
+            lds_barrier();
+            // ---- projection, thread = (lm, radial pair), species run by run ----
+#pragma unroll
+            for (int sr = 0; sr < SR; ++sr) {
+                const int lo = run[sr], hi = run[sr + 1];
+                for (int e = lo; e < hi; ++e) {
+                    const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
+                    const double live = geo[4 * e + 3] != 0.0 ? 1.0 : 0.0;
+#pragma unroll
+                    for (int q = 0; q < QT; ++q) {
+                        const double y = (double)Yl[lm_q[q] * WP + e];
+                        const double t0 = (double)Yl[gi[q][0] * WP + e], t1 = (double)Yl[gi[q][1] * WP + e];
+                        const double t2 = (double)Yl[gi[q][2] * WP + e], t3 = (double)Yl[gi[q][3] * WP + e];
+                        const double t4 = (double)Yl[gi[q][4] * WP + e];
+                        const double dx = live * (gc[q][0] * t0 + gc[q][1] * t1);
+                        const double dy = live * (gc[q][2] * t2 + gc[q][3] * t3);
+                        const double dz = live * (gc[q][4] * t4);
+                        const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+                        const ST *hp = Hl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+#pragma unroll
+                        for (int a = 0; a < 2; ++a) {
+                            const bool in = a_q[q] + a < n;
+                            const double b = in ? (double)bp[a * WP] : 0.0;
+                            const double hs = in ? (double)hp[a * WP] * y : 0.0;
+                            acc[sr][q][a][0] += b * y;
+                            acc[sr][q][a][1] += hs * rx + b * dx;
+                            acc[sr][q][a][2] += hs * ry + b * dy;
+                            acc[sr][q][a][3] += hs * rz + b * dz;
+                        }
+                    }
+                }
+            }
+        }
+        lds_barrier(); // the staging region is read: the coefficient block goes over it
+#pragma unroll
+        for (int sr = 0; sr < SR; ++sr)
+#pragma unroll
+            for (int q = 0; q < QT; ++q)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    if (sr < S && ok_q[q] && a_q[q] + a < n)
+#pragma unroll
+                        for (int d = 0; d < 4; ++d)
+                            cb[(size_t)d * SnL + (sr * n + a_q[q] + a) * L + lm_q[q]] = acc[sr][q][a][d];
+        lds_barrier();
+        // on-site term of the center (its species, l = 0)
+        if (tid < n) cb[(spec_i * n + tid) * L] += c0[tid];
+        lds_barrier();
+        const int64_t cw = ci;
+        ci += stride;
+        fetch(); // the next center's first chunk before this center's stores
+        power_tiles4<OutT>(cb, SnL, L, 1, Sn, 0, 0, lw, desc + cw * P.F, jself + cw * 3 * P.F, P.F, lw, 0,
+                           PairIndex{S, n, 1.0f / (float)n}, wave, NWC, lane, Kl);
+        // the coefficients for k_jacobian, [lm][species n], in destination order
+        double *sc = c_scratch + cw * 4 * (size_t)L * Sn;
+        for (int it = tid; it < SnL; it += BSC) {
+            const int lm = it / Sn, sa = it - lm * Sn;
+            sc[it] = cb[sa * L + lm];
+        }
     }
 }
 
@@ -1422,7 +1921,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jac
     // stores to drain.)
     {
     const int64_t ci = blockIdx.x;
-    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1], ebase = R.row_ptr[0];
+    const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1], ebase = *R.e_origin;
     if (e1 == e0) return;
     const double *cg = c_scratch + ci * 4 * (size_t)Sn * L; // component c of [c, Dx, Dy, Dz]
     copy_to_lds<BSJ, 4>(cT, cg, Sn * L, tid);
@@ -1636,7 +2135,7 @@ __global__ void k_scatter_dense(Params P, Rows R, const OutT *__restrict__ jedge
     const int64_t ci = blockIdx.x;
     const int F = P.F, Fe = P.Fe;
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
-    const int64_t ebase = R.row_ptr[0];
+    const int64_t ebase = *R.e_origin;
     OutT *row = dense + ci * R.n_atoms * 3 * F;
     for (int k = threadIdx.x; k < 3 * F; k += blockDim.x) row[i * 3 * F + k] = jself[ci * 3 * F + k];
     __syncthreads(); // a periodic image of the center adds to the center block

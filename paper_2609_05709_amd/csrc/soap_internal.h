@@ -36,18 +36,21 @@ struct Params {
     int lgrp[MAX_GROUPS + 1];  // group g covers l in [lgrp[g], lgrp[g+1])
 };
 
-// Neighbour rows of the current structure, or of one batch of its centers:
-// the batch's rows row_ptr[0..nc] are a slice of the structure's CSR offsets,
-// so edge e of the structure is edge e - row_ptr[0] of the batch's edge
-// outputs, while center ci of the batch is center c_base + ci of the
-// structure (its row, its atom index).
+// Neighbour rows of the current structure, or of a range of its centers:
+// the range's rows row_ptr[0..nc] are a slice of the structure's CSR
+// offsets, and center ci of the range is center c_base + ci of the
+// structure (its row, its atom index).  Edge outputs are indexed from the
+// first edge of the output batch: edge e of the structure is entry
+// e - *e_origin (a launch may cover part of a batch, its edges then land
+// after the earlier part's).
 struct Rows {
     int64_t n_atoms, nc;
-    int64_t c_base;         // structure index of the batch's first center
-    const int32_t *centers; // [nc] atom of each center of the batch; NULL = c_base + ci
-    const uint8_t *spec;    // species index per atom
-    const int64_t *row_ptr; // [nc+1]
-    const int32_t *cols;    // [E] (indexed by structure edge)
+    int64_t c_base;           // structure index of the range's first center
+    const int32_t *centers;   // [nc] atom of each center of the range; NULL = c_base + ci
+    const uint8_t *spec;      // species index per atom
+    const int64_t *row_ptr;   // [nc+1]
+    const int32_t *cols;      // [E] (indexed by structure edge)
+    const int64_t *e_origin;  // row offset of the output batch's first center
 };
 
 // Density work counters: one 64-bit counter per l-group, zeroed at the
@@ -136,6 +139,18 @@ struct DensityLaunch {
     int blocks;      // persistent workgroups per l-group
     bool hi;         // the variant compiled for three waves per SIMD (see density_has_high)
 };
+struct DescLaunch {
+    int W;      // edges per chunk (0: the descriptor path uses k_density)
+    int ql, na; // lm slots per lane, accumulators per slot
+    size_t lds;
+    int blocks; // resident workgroups (persistent launch)
+};
+struct DjacLaunch {
+    int W;          // edges per chunk (0: the Jacobian path uses k_density)
+    int qt, na, sr; // tasks per thread, radial size, species slots
+    size_t lds;
+    int blocks;     // resident workgroups (persistent launch)
+};
 struct JacLaunch {
     int W;          // edges per wave tile (at most jacobian_max_w())
     size_t lds;
@@ -178,6 +193,22 @@ struct OutPlan {
 int plan_outputs(const Params &P, bool f64, OutPlan *O); // 0, or -1 if one l does not fit
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
                           void *jself, hipStream_t st);
+// one-wave-per-center descriptor kernel (GTO): the shape of its accumulators
+// (false if the basis has none), LDS bytes for W edges per chunk, resident
+// workgroups per CU, launch (desc and c_out may each be NULL)
+bool desc_shape(const Params &P, int *ql, int *na);
+size_t desc_lds_bytes(const Params &P, int W, bool st64);
+int desc_blocks_per_cu(bool f64, bool ar64, int ql, int na, size_t lds);
+hipError_t launch_desc(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DescLaunch &cfg,
+                       void *desc, void *c_out, hipStream_t st);
+// one-workgroup-per-center density step of the Jacobian path (GTO): shape,
+// LDS bytes, resident workgroups per CU, launch (writes desc, jself and the
+// coefficients for k_jacobian)
+bool djac_shape(const Params &P, int *qt, int *na, int *sr);
+size_t djac_lds_bytes(const Params &P, int W, bool st64);
+int djac_blocks_per_cu(bool f64, bool ar64, int qt, int na, int sr, size_t lds);
+hipError_t launch_djac(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjacLaunch &cfg,
+                       void *desc, void *jself, double *c_scratch, hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);
 // column means of a row-major (rows x cols) array of the output type, in

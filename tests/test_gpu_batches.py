@@ -221,3 +221,28 @@ def test_basis_too_large_for_the_jacobian_path():
     ref = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf).compute(
         st.pos64, st.Z, centers=idx)
     assert row_errors(desc[idx], ref["desc"]).max() < TOL["float32"]
+
+
+@pytest.mark.parametrize("chunks,wg", [(2, 0), (3, 1), (4, 2)])
+def test_pipelined_derivatives_bitwise(chunks, wg):
+    """The pipelined derivatives (center chunks, the Jacobian kernel of a
+    chunk on a second stream beside the density kernel of the next) give the
+    same bits as the single-stream call, for the whole list and for a batch."""
+    import torch
+    wl = workloads.WATER1000
+    st = wl.structure()
+    sp = _ctx(wl, st)
+    ref = [t.clone() for t in sp.derivatives()]
+    cf, ef = sp.plan_batches(10**9, jacobian=True)
+    a, b = 700, 1500
+    row, _ = sp.neighbors()
+    row = row.cpu().numpy()
+    ref_b = [t.clone() for t in sp.derivatives_batch(a, b - a, int(row[b] - row[a]))]
+    sp._check(sp._L.soap_set_option(sp._h, b"pipeline", chunks))
+    sp._check(sp._L.soap_set_option(sp._h, b"pipeline_density_wg", wg))
+    for _ in range(2):
+        for x, y in zip(sp.derivatives(), ref):
+            assert torch.equal(x, y)
+        for x, y in zip(sp.derivatives_batch(a, b - a, int(row[b] - row[a])), ref_b):
+            assert torch.equal(x, y)
+    sp.close()

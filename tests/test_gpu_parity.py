@@ -177,3 +177,40 @@ def test_fuzz_small_structures(seed):
     for dtype in ("float32", "float64"):
         full_check(wl, dtype)
     _structs.pop(wl.make)
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+@pytest.mark.parametrize("nl", [(4, 4), (8, 6), (2, 2), (12, 7), (8, 10), (1, 0)])
+def test_descriptor_kernel_chunk_widths(dtype, nl):
+    """The GTO descriptor path (one wave per center) at every chunk width and
+    the shared density kernel (desc_tile -1): sampled rows against the
+    oracle; the chunk widths give the same bits (each wave sums its center's
+    edges in row order whatever the chunking); the coefficients too."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    wl = workloads.WATER1000.with_basis(nl[0], nl[1], "gto")
+    st = structure(wl)
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
+    Z = torch.from_numpy(st.Z).cuda()
+    rng = np.random.default_rng(nl[0] * 31 + nl[1])
+    idx = np.sort(rng.choice(st.n_atoms, size=24, replace=False))
+    ref = oracle_for(wl).compute(st.pos64, st.Z, centers=idx, coefficients=True)
+    first = None
+    for tile in (64, 32, 16, -1):
+        sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+        sp._check(sp._L.soap_set_option(sp._h, b"desc_tile", tile))
+        sp.build_neighbors(pos, Z)
+        d = sp.compute()
+        c = sp.coefficients()
+        torch.cuda.synchronize()
+        err = row_errors(d.cpu().double().numpy()[idx], ref["desc"]).max()
+        cerr = row_errors(c.cpu().double().numpy()[idx].reshape(len(idx), -1), ref["c"].reshape(len(idx), -1)).max()
+        print(f"[desc] {wl.name} {dtype} tile {tile}: desc {err:.2e} c {cerr:.2e}", flush=True)
+        assert err < TOL[dtype] and cerr < TOL[dtype]
+        if tile > 0:
+            if first is None:
+                first = (d.clone(), c.clone())
+            else:
+                assert torch.equal(d, first[0]) and torch.equal(c, first[1])
+        sp.close()
