@@ -259,7 +259,7 @@ DTYPE_LABEL = {
 
 
 def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False, arith="mixed",
-        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None):
+        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None, djac_tile=None):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
@@ -269,6 +269,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
     sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype, arith=arith)
     if desc_tile:
         sp._check(sp._L.soap_set_option(sp._h, b"desc_tile", int(desc_tile)))
+    if djac_tile is not None:
+        sp._check(sp._L.soap_set_option(sp._h, b"djac_tile", int(djac_tile)))
     if pipeline is not None:
         sp._check(sp._L.soap_set_option(sp._h, b"pipeline", int(pipeline)))
     if pipeline_density_wg is not None:
@@ -333,6 +335,9 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
 
     jac = wl.jacobian and mode == "derivatives"
     alg = algorithmic(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, jac)
+    # the kernels the library's plan chose for this basis
+    desc_kernel = "k_desc" if sp.get_option("descriptor_kernel") else "k_density"
+    dens_kernel = "k_djac" if sp.get_option("jacobian_density_kernel") else "k_density"
     # per step (a pipelined step launches its kernels once per center chunk;
     # the chunks' Jacobian launches then overlap the density launches)
     kern = {"neighbors": seg_ms[0] / steps, "density": seg_ms[1] / steps, "jacobian": seg_ms[2] / steps,
@@ -354,9 +359,9 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
     else:
         fl = density_flops(wl, E, nc, sp.n_features)
         t = kern["density"] * 1e-3
-        roof = {"kernel": "k_density", "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
+        roof = {"kernel": desc_kernel, "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "traffic": measured_traffic(wl.name + ("" if mode == "derivatives" else "_" + mode),
-                                                               "k_density", dtype), "alg_flops_per_launch": fl}
+                                                               desc_kernel, dtype), "alg_flops_per_launch": fl}
     roof["frac"] = roof["achieved"] / roof["peak"]
     line = {
         "metric": METRIC,
@@ -378,6 +383,7 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
                    "features": sp.n_features,
                    "edge_features": sp.n_edge_features},
         "kernel_ms": kern,
+        "kernels": {"descriptor": desc_kernel, "jacobian_density": dens_kernel},
         "kernel_timing": "HIP events per segment, on the stream each kernel runs on, over a second pass of the "
                          "K steps; per-step sums",
         "step_alg_bytes": alg["step"],
@@ -425,6 +431,8 @@ def main():
     ap.add_argument("--pipeline", type=int, default=None, help="center chunks of a pipelined derivatives call")
     ap.add_argument("--pipeline-density-wg", type=int, default=None,
                     help="density workgroups per CU while pipelined (0 = as planned)")
+    ap.add_argument("--djac-tile", type=int, default=None, choices=[0, -1, 32, 64],
+                    help="Jacobian path's density step (GTO): 0 automatic, -1 the shared density kernel, else chunk")
     ap.add_argument("--desc-tile", type=int, default=0, choices=[0, -1, 16, 32, 64],
                     help="GTO descriptor kernel: 0 automatic, -1 the shared density kernel, else edges per chunk")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
@@ -448,7 +456,8 @@ def main():
         return
     wl = workload_by_name(a.workload or "water1000")
     line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic,
-               arith=a.arith, desc_tile=a.desc_tile, pipeline=a.pipeline, pipeline_density_wg=a.pipeline_density_wg)
+               arith=a.arith, desc_tile=a.desc_tile, pipeline=a.pipeline, pipeline_density_wg=a.pipeline_density_wg,
+               djac_tile=a.djac_tile)
     if a.workload is None and a.mode == "derivatives" and not a.periodic:
         # the same headline in the paper's arithmetic (float64 internally,
         # float32 outputs), and the other workloads, each with its own

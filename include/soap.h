@@ -143,6 +143,19 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  */
 int soap_set_option(soap_ctx *ctx, const char *key, int64_t value);
 
+/*
+ * Read an option (any key of soap_set_option) or a planning decision of the
+ * context into *value (host):
+ *   "descriptor_kernel"       : 1 if soap_compute / soap_coefficients run the
+ *                               descriptor kernel that gives each center a
+ *                               workgroup, 0 if the shared density kernel;
+ *   "jacobian_density_kernel" : 1 if the density step of soap_derivatives runs
+ *                               the kernel that gives each center a workgroup,
+ *                               0 if the shared density kernel.
+ * Errors: SOAP_EINVAL (NULL argument, unknown key).
+ */
+int soap_get_option(const soap_ctx *ctx, const char *key, int64_t *value);
+
 /* Number of descriptor features F (see feature order above); -1 if ctx is NULL. */
 int64_t soap_num_features(const soap_ctx *ctx);
 

@@ -119,7 +119,7 @@ struct soap_ctx {
     JacLaunch jac_cfg{};
     DescLaunch desc_cfg{};
     DjacLaunch djac_cfg{};
-    int djac_tile = -1; // option "djac_tile": 0 auto, -1 never k_djac (default), else the widest chunk
+    int djac_tile = 0; // option "djac_tile": 0 auto (default), -1 never k_djac, else the widest chunk
     // pipelined derivatives: the density kernel of center chunk k + 1 on the
     // caller's stream beside the Jacobian kernel of chunk k on a second one
     int pipe_chunks = 1;         // option "pipeline": chunks per call (1 = one stream)
@@ -635,6 +635,29 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         return upload_constants(c);
     }
     return fail(c, SOAP_EINVAL, "unknown option '%s'", key);
+}
+
+int soap_get_option(const soap_ctx *c, const char *key, int64_t *value) {
+    if (!c || !key || !value) return SOAP_EINVAL;
+    const struct {
+        const char *k;
+        int64_t v;
+    } tab[] = {{"dtype", c->dtype},
+               {"arith", c->arith},
+               {"quad_n", c->Q},
+               {"timing", c->timing ? 1 : 0},
+               {"desc_tile", c->desc_tile},
+               {"djac_tile", c->djac_tile},
+               {"pipeline", c->pipe_chunks},
+               {"pipeline_density_wg", c->pipe_density_wg},
+               {"descriptor_kernel", c->desc_cfg.W > 0 ? 1 : 0},
+               {"jacobian_density_kernel", c->djac_cfg.W > 0 ? 1 : 0}};
+    for (const auto &t : tab)
+        if (!std::strcmp(key, t.k)) {
+            *value = t.v;
+            return SOAP_OK;
+        }
+    return SOAP_EINVAL;
 }
 
 int64_t soap_num_features(const soap_ctx *c) { return c ? c->F : -1; }

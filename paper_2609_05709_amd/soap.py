@@ -24,7 +24,7 @@ SOAP_BATCH_DESCRIPTOR, SOAP_BATCH_DERIVATIVES = 0, 1
 MAX_DEGREE = 2048
 
 # every entry point declared in include/soap.h
-ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_num_features", "soap_num_edge_features",
+ABI_SYMBOLS = ("soap_create", "soap_set_option", "soap_get_option", "soap_num_features", "soap_num_edge_features",
                "soap_feature_labels", "soap_feature_map", "soap_build_neighbors", "soap_get_neighbors",
                "soap_set_cell", "soap_get_neighbor_images",
                "soap_compute", "soap_coefficients", "soap_coefficient_derivatives", "soap_compute_averaged",
@@ -59,6 +59,8 @@ def load_library(path: str = LIB_PATH):
     L.soap_create.argtypes = [vp, i32, dbl, i32, i32, dbl, i32, ctypes.POINTER(vp)]
     L.soap_set_option.restype = ctypes.c_int
     L.soap_set_option.argtypes = [vp, ctypes.c_char_p, i64]
+    L.soap_get_option.restype = ctypes.c_int
+    L.soap_get_option.argtypes = [vp, ctypes.c_char_p, ctypes.POINTER(i64)]
     L.soap_num_features.restype = i64
     L.soap_num_features.argtypes = [vp]
     L.soap_num_edge_features.restype = i64
@@ -167,6 +169,14 @@ class Soap:
 
     def set_timing(self, on: bool):
         self._check(self._L.soap_set_option(self._h, b"timing", 1 if on else 0))
+
+    def get_option(self, key: str) -> int:
+        v = ctypes.c_int64()
+        self._check(self._L.soap_get_option(self._h, key.encode(), ctypes.byref(v)))
+        return int(v.value)
+
+    def set_option(self, key: str, value: int):
+        self._check(self._L.soap_set_option(self._h, key.encode(), int(value)))
 
     def timing(self, reset: bool = True):
         """(ms[3], counts[3]) summed over timed calls: neighbour search, density

@@ -214,3 +214,54 @@ def test_descriptor_kernel_chunk_widths(dtype, nl):
             else:
                 assert torch.equal(d, first[0]) and torch.equal(c, first[1])
         sp.close()
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+@pytest.mark.parametrize("case", ["water64", "water1000", "water1000_n4l8", "three_species", "four_species_n6l4"])
+def test_jacobian_density_kernel_chunk_widths(dtype, case):
+    """The one-workgroup-per-center density step of the Jacobian path (GTO)
+    at both chunk widths: descriptor and every block of sampled centers
+    against the oracle, and the same bits at both widths."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    if case == "water64":
+        wl, st, sample = workloads.WATER64, structure(workloads.WATER64), None
+    elif case.startswith("water1000"):
+        wl = workloads.WATER1000 if case == "water1000" else workloads.WATER1000.with_basis(4, 8, "gto")
+        st, sample = structure(wl), 16
+    else:
+        species = (1, 6, 8) if case == "three_species" else (1, 6, 7, 8)
+        nl = (5, 5) if case == "three_species" else (6, 4)
+        wl = workloads.Workload(case, species, "gto", 5.0, 0.45, nl[0], nl[1], True, ("none",))
+        st = workloads.random_small(90, 31 + len(species), 5.0, species=species, dmin=0.85)
+        sample = None
+    n = st.n_atoms
+    idx = np.arange(n) if sample is None else np.sort(np.random.default_rng(7).choice(n, sample, replace=False))
+    ref = oracle_for(wl).compute(st.pos64, st.Z, centers=idx, jacobian=True)
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
+    Z = torch.from_numpy(st.Z).cuda()
+    first = None
+    for tile in (64, 32):
+        sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+        sp._check(sp._L.soap_set_option(sp._h, b"djac_tile", tile))
+        sp.build_neighbors(pos, Z)
+        d, je, js = sp.derivatives()
+        row, cols = sp.neighbors()
+        torch.cuda.synchronize()
+        g = dict(row=row.cpu().numpy(), cols=cols.cpu().numpy(), fmaps=[sp.feature_map(k) for k in range(len(wl.species))],
+                 jedge={}, jself={})
+        for c in idx:
+            r0, r1 = int(g["row"][c]), int(g["row"][c + 1])
+            g["jedge"][int(c)] = je[r0:r1].cpu().double().numpy()
+            g["jself"][int(c)] = js[int(c)].cpu().double().numpy()
+        ed = row_errors(d.cpu().double().numpy()[idx], ref["desc"]).max()
+        ej = jacobian_errors(g, ref, st, wl.species, idx.tolist(), idx)
+        print(f"[djac] {case} {dtype} tile {tile}: desc {ed:.2e} jac {ej:.2e}", flush=True)
+        assert ed < TOL[dtype] and ej < TOL[dtype]
+        if first is None:
+            first = (d.clone(), je.clone(), js.clone())
+        else:
+            for x, y in zip((d, je, js), first):
+                assert torch.equal(x, y)
+        sp.close()
