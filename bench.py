@@ -259,7 +259,7 @@ DTYPE_LABEL = {
 
 
 def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False, arith="mixed",
-        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None, djac_tile=None):
+        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None, djac_tile=None, batches=0):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
@@ -290,6 +290,17 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         jcs = torch.empty((nc, 3, S, wl.n_max, L), dtype=tdt, device=dev)
     elif mode in ("inner", "outer"):
         avg = torch.empty(sp.n_features, dtype=tdt, device=dev)
+    elif batches:
+        # the structure streamed in batches sized by a memory budget: buffers
+        # for the largest batch, reused by every batch
+        per_center = sp.n_features * out_bytes * (4 if wl.jacobian else 1)
+        total = nc * per_center + (E * 3 * sp.n_edge_features * out_bytes if wl.jacobian else 0)
+        cf, ef = sp.plan_batches(total // batches + 1, jacobian=wl.jacobian)
+        bmax, emax = int(np.diff(cf).max()), int(np.diff(ef).max())
+        desc = torch.empty((bmax, sp.n_features), dtype=tdt, device=dev)
+        if wl.jacobian:
+            jedge = torch.empty((max(emax, 1), 3, sp.n_edge_features), dtype=tdt, device=dev)
+            jself = torch.empty((bmax, 3, sp.n_features), dtype=tdt, device=dev)
     else:
         desc = torch.empty((nc, sp.n_features), dtype=tdt, device=dev)
         if wl.jacobian:
@@ -298,7 +309,15 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
 
     def step():
         sp.build_neighbors(pos, Z)
-        if mode == "cc":
+        if batches:
+            for k in range(len(cf) - 1):
+                a, n_c, n_e = int(cf[k]), int(cf[k + 1] - cf[k]), int(ef[k + 1] - ef[k])
+                if wl.jacobian:
+                    sp.derivatives_batch(a, n_c, n_e, desc[:n_c], jedge[:max(n_e, 1)] if n_e else jedge[:0],
+                                         jself[:n_c])
+                else:
+                    sp.compute_batch(a, n_c, desc[:n_c])
+        elif mode == "cc":
             sp.coefficient_derivatives(cc, jce, jcs)
         elif mode in ("inner", "outer"):
             sp.compute_averaged(mode, avg)
@@ -376,7 +395,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         "vs_baseline": None,
         "dtype": DTYPE_LABEL[(dtype, arith)],
         "data": "synthetic",
-        "config": {"workload": wl.name + ("" if mode == "derivatives" else "_" + mode) + ("_periodic" if periodic else ""),
+        "config": {"workload": wl.name + ("" if mode == "derivatives" else "_" + mode) + ("_periodic" if periodic else "")
+                   + (f"_batches{len(cf) - 1}" if batches else ""),
                    "n_atoms": nc, "edges": E, "rbf": wl.rbf, "n_max": wl.n_max,
                    "l_max": wl.l_max, "r_cut": wl.r_cut, "sigma": wl.sigma, "species": list(wl.species),
                    "output": dtype, "arith": arith, "jacobian": jac or mode == "cc", "mode": mode,
@@ -428,6 +448,9 @@ def main():
     ap.add_argument("--periodic", action="store_true")
     ap.add_argument("--grid", default=None, help="sweep n_max, l_max in {2..12}^2 for every radial basis; write JSONL here")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--batches", type=int, default=0,
+                    help="stream the structure through about this many center batches sized by a memory budget "
+                         "(one neighbour search per step, outputs in buffers of the largest batch)")
     ap.add_argument("--pipeline", type=int, default=None, help="center chunks of a pipelined derivatives call")
     ap.add_argument("--pipeline-density-wg", type=int, default=None,
                     help="density workgroups per CU while pipelined (0 = as planned)")
@@ -457,7 +480,7 @@ def main():
     wl = workload_by_name(a.workload or "water1000")
     line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic,
                arith=a.arith, desc_tile=a.desc_tile, pipeline=a.pipeline, pipeline_density_wg=a.pipeline_density_wg,
-               djac_tile=a.djac_tile)
+               djac_tile=a.djac_tile, batches=a.batches)
     if a.workload is None and a.mode == "derivatives" and not a.periodic:
         # the same headline in the paper's arithmetic (float64 internally,
         # float32 outputs), and the other workloads, each with its own

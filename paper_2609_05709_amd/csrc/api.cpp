@@ -307,16 +307,16 @@ int plan_launches(soap_ctx *c) {
     // workgroups (of four waves) resident per CU; an explicit "desc_tile" is
     // the widest chunk tried, and any chunk that fits at all is taken
     c->desc_cfg = DescLaunch{};
-    int ql = 0, na = 0;
-    if (c->desc_tile >= 0 && desc_shape(P, &ql, &na)) {
+    int ql = 0, na = 0, dsr = 0;
+    if (c->desc_tile >= 0 && desc_shape(P, &ql, &na, &dsr)) {
         const int cand[3] = {64, 32, 16};
         for (int W : cand) {
             if (c->desc_tile > 0 && W > c->desc_tile) continue;
             const size_t lds = desc_lds_bytes(P, W, st64);
             if (lds > LDS_HARD_LIMIT) continue;
-            const int b = desc_blocks_per_cu(f64, ar64, ql, na, lds);
+            const int b = desc_blocks_per_cu(f64, ar64, ql, na, dsr, lds);
             if (b >= (c->desc_tile > 0 ? 1 : 2)) {
-                c->desc_cfg = DescLaunch{W, ql, na, lds, ncu * b};
+                c->desc_cfg = DescLaunch{W, ql, na, dsr, lds, ncu * b};
                 break;
             }
         }

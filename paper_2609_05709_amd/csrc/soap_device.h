@@ -1205,10 +1205,12 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
 //      coefficient read is wave-uniform (the tables sit in LDS, copied once
 //      per workgroup), and every lane works on its own edge;
 //   2. projection, thread = (lm, group of AG radial indices a): each thread
-//      owns those coefficients c_{a lm} of the current species in float64
-//      registers and adds B_al S_lm over the chunk's edges in row order
-//      (Eq. projection); one harmonic read serves AG products.  Rows are sorted by species; at a species change the
-//      registers go to the center's coefficient block.
+//      owns those coefficients c_{a lm} in float64 registers, one set per
+//      species (SR >= S slots), and adds B_al S_lm over the chunk's edges in
+//      row order (Eq. projection); one harmonic read serves AG products.
+//      Rows are sorted by species, so each species is a contiguous run of the
+//      chunk.  After the row the registers go to the center's coefficient
+//      block, which aliases the staging buffers.
 // Every coefficient has one owner thread and every sum runs in row order:
 // the results are bitwise repeatable with no ordering protocol.  Then the
 // on-site term, and the power spectrum on the matrix cores (power_tiles,
@@ -1223,24 +1225,27 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
 constexpr int NWC = 4, BSC = 64 * NWC;
 
 // LDS of k_desc.  Float64: K_l, the harmonic normalisations Nt, a'_kl [l][k],
-// betaC [l][n][k], the on-site terms, the coefficient block [S][n][L].  At
-// the staging precision: harmonics [lm][W + 1] and radial factors
-// [l][n][W + 1] (edge fastest: the staging lanes, one per edge, write
-// consecutive words), the rows of one l padded to an odd length desc_ldl;
-// the odd strides put the projection threads, which read one edge at
-// different lm (or l), on different banks.  Then the chunk's species.
+// betaC [l][n][k], the on-site terms.  Then the larger of the staging
+// buffers and the coefficient block [S][n][L] (float64, after the row).
+// Staging, at the staging precision: harmonics [lm][W + 1] and radial
+// factors [l][n][W + 1] (edge fastest: the staging lanes, one per edge,
+// write consecutive words), the rows of one l padded to an odd length
+// desc_ldl; the odd strides put the projection threads, which read one edge
+// at different lm (or l), on different banks.  Then the chunk's species run
+// bounds.
 __host__ __device__ __forceinline__ int desc_ldl(int n, int W) { return (n * (W + 1)) | 1; }
 __host__ __device__ __forceinline__ size_t desc_lds_doubles(const Params &P, int W, int sb) {
     const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n, L = (size_t)P.L;
-    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + even((size_t)P.S * n * L) +
-           even((L * (W + 1) * sb + 7) / 8) + even((lw * desc_ldl((int)n, W) * sb + 7) / 8) + even(((size_t)W + 1) / 2);
+    const size_t stage = even((L * (W + 1) * sb + 7) / 8) + even((lw * desc_ldl((int)n, W) * sb + 7) / 8) + 16;
+    const size_t block = (size_t)P.S * n * L;
+    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + even(stage > block ? stage : block);
 }
 // (lm, group of ag radial indices) tasks per thread
 __host__ __device__ __forceinline__ int desc_tasks(const Params &P, int ag) {
     return (P.L * ((P.n + ag - 1) / ag) + BSC - 1) / BSC;
 }
 
-template <typename PosT, typename OutT, typename ST, int QT, int AG, int NA>
+template <typename PosT, typename OutT, typename ST, int QT, int AG, int NA, int SR>
 __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                               OutT *__restrict__ desc, OutT *__restrict__ c_out) {
     extern __shared__ __align__(16) double smem[];
@@ -1255,11 +1260,13 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
     double *apr = cv.take((size_t)lw * n);
     double *bcf = cv.take((size_t)lw * n * n);
     double *c0 = cv.take((size_t)n);
-    double *cb = cv.take((size_t)SnL); // [S][n][L]
+    double *stage = cv.take(0);
+    double *cb = stage; // [S][n][L], after the row
     const int WP = W + 1, ldl = desc_ldl(n, W);
-    ST *Yl = (ST *)cv.take(((size_t)L * WP * SB + 7) / 8);  // [lm][W + 1]
-    ST *Bl = (ST *)cv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1], rows of l padded to ldl
-    int *esp = (int *)cv.take(((size_t)W + 1) / 2);          // species of the chunk's edges
+    Carver sv{stage};
+    ST *Yl = (ST *)sv.take(((size_t)L * WP * SB + 7) / 8);  // [lm][W + 1]
+    ST *Bl = (ST *)sv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1], rows of l padded to ldl
+    int *run = (int *)sv.take(16);                           // species run bounds of the chunk
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     for (int k = tid; k < ldN * ldN; k += BSC) Nt[k] = P.Nt[k];
     for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
@@ -1309,30 +1316,27 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
     };
     fetch();
     while (ci < R.nc) {
-        for (int k = tid; k < SnL; k += BSC) cb[k] = 0.0;
-        double acc[QT][AG];
+        double acc[SR][QT][AG];
 #pragma unroll
-        for (int q = 0; q < QT; ++q)
-#pragma unroll
-            for (int g = 0; g < AG; ++g) acc[q][g] = 0.0;
-        int cur = -1;
-        // registers of species cur into the coefficient block (one owner per entry)
-        auto flush = [&]() {
+        for (int sr = 0; sr < SR; ++sr)
 #pragma unroll
             for (int q = 0; q < QT; ++q)
 #pragma unroll
-                for (int g = 0; g < AG; ++g) {
-                    if (ok_q[q] && a_q[q] + g < n) cb[(cur * n + a_q[q] + g) * L + lm_q[q]] += acc[q][g];
-                    acc[q][g] = 0.0;
-                }
-        };
+                for (int g = 0; g < AG; ++g) acc[sr][q][g] = 0.0;
         for (int64_t cs = e0; cs < e1; cs += W) {
             const int nb = (int)((e1 - cs) < W ? (e1 - cs) : W);
             if (cs != e0) gather(cs, nb); // later chunks of a long row (no stores pending)
             lds_barrier();                // the tables, the cleared block, the previous chunk read
             // ---- phase 1: staging, lane = edge, tasks over the waves ----
+            if (wave == 0) {
+                // run bounds: the chunk's edges of species below sr (rows are sorted by species)
+#pragma unroll
+                for (int sr = 0; sr <= SR; ++sr) {
+                    const int cnt = __popcll(__ballot(lane < nb && gs < sr));
+                    if (lane == 0) run[sr] = cnt;
+                }
+            }
             if (lane < nb) {
-                if (wave == 0) esp[lane] = gs;
                 const double r2 = gx * gx + gy * gy + gz * gz;
                 for (int task = wave; task <= lw; task += NWC) {
                     if (task == lw) {
@@ -1356,23 +1360,30 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                 }
             }
             lds_barrier();
-            // ---- phase 2: projection, thread = (lm, radial pair) ----
-            for (int e = 0; e < nb; ++e) {
-                const int s = __builtin_amdgcn_readfirstlane(esp[e]);
-                if (s != cur) {
-                    if (cur >= 0) flush();
-                    cur = s;
-                }
+            // ---- phase 2: projection, thread = (lm, radial group), species run by run ----
 #pragma unroll
-                for (int q = 0; q < QT; ++q) {
-                    const double yv = ok_q[q] ? (double)Yl[lm_q[q] * WP + e] : 0.0;
-                    const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+            for (int sr = 0; sr < SR; ++sr) {
+                const int lo = run[sr], hi = run[sr + 1];
+                for (int e = lo; e < hi; ++e) {
 #pragma unroll
-                    for (int g = 0; g < AG; ++g) acc[q][g] += (a_q[q] + g < n ? (double)bp[g * WP] : 0.0) * yv;
+                    for (int q = 0; q < QT; ++q) {
+                        const double yv = ok_q[q] ? (double)Yl[lm_q[q] * WP + e] : 0.0;
+                        const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+#pragma unroll
+                        for (int g = 0; g < AG; ++g)
+                            acc[sr][q][g] += (a_q[q] + g < n ? (double)bp[g * WP] : 0.0) * yv;
+                    }
                 }
             }
         }
-        if (cur >= 0) flush();
+        lds_barrier(); // the staging region is read: the coefficient block goes over it
+#pragma unroll
+        for (int sr = 0; sr < SR; ++sr)
+#pragma unroll
+            for (int q = 0; q < QT; ++q)
+#pragma unroll
+                for (int g = 0; g < AG; ++g)
+                    if (sr < S && ok_q[q] && a_q[q] + g < n) cb[(sr * n + a_q[q] + g) * L + lm_q[q]] = acc[sr][q][g];
         lds_barrier();
         // on-site term of the center (its species, l = 0)
         if (tid < n) cb[(spec_i * n + tid) * L] += c0[tid];
@@ -1414,13 +1425,13 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
 // coefficients, transposed to [lm][species n], for k_jacobian.  Each sum runs
 // in row order: deterministic with no ordering protocol.
 // ---------------------------------------------------------------------------
-// LDS doubles of k_djac: tables (K_l, Nt, a', betaC, betaCa, c0), then the
+// LDS doubles of k_djac: tables (K_l, Nt, a', betaC, c0), then the
 // larger of the staging buffers (harmonics [lm][W+1], B and Bh [l][n][W+1]
 // with odd row lengths, edge vectors [W][4], species [W], species run bounds)
 // and the coefficient block 4 S n L
 __host__ __device__ __forceinline__ size_t djac_table_doubles(const Params &P) {
     const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n;
-    return 16 + even(ldN * ldN) + even(lw * n) + 2 * even(lw * n * n) + even(n);
+    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n);
 }
 __host__ __device__ __forceinline__ size_t djac_stage_doubles(const Params &P, int W, int sb) {
     const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1, n = (size_t)P.n;
@@ -1448,7 +1459,6 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
     double *Nt = cv.take((size_t)ldN * ldN);
     double *apr = cv.take((size_t)lw * n);
     double *bcf = cv.take((size_t)lw * n * n);
-    double *bca = cv.take((size_t)lw * n * n);
     double *c0 = cv.take((size_t)n);
     double *stage = cv.take(0);
     const int WP = W + 1, ldl = desc_ldl(n, W);
@@ -1463,10 +1473,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     for (int k = tid; k < ldN * ldN; k += BSC) Nt[k] = P.Nt[k];
     for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
-    for (int k = tid; k < lw * n * n; k += BSC) {
-        bcf[k] = P.betaC[k];
-        bca[k] = P.betaCa[k];
-    }
+    for (int k = tid; k < lw * n * n; k += BSC) bcf[k] = P.betaC[k];
     for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
 
     // this thread's tasks: (lm, radial pair) = (t % L, t / L), t = tid + BSC q,
@@ -1575,18 +1582,23 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
                         continue;
                     }
                     const int l = task;
-                    double ex[NA];
+                    // e_k and -2 a'_k e_k: Bh = sum_k betaC (-2 a'_k) e_k
+                    double ex[NA], ea[NA];
 #pragma unroll
-                    for (int k = 0; k < NA; ++k) ex[k] = k < n ? exp(-apr[l * n + k] * r2) : 0.0;
+                    for (int k = 0; k < NA; ++k) {
+                        const double ap = apr[l * n + (k < n ? k : n - 1)];
+                        ex[k] = k < n ? exp(-ap * r2) : 0.0;
+                        ea[k] = -2.0 * ap * ex[k];
+                    }
                     ST *bo = Bl + (size_t)l * ldl + lane, *ho = Hl + (size_t)l * ldl + lane;
-                    const double *bc = bcf + (size_t)l * n * n, *hc = bca + (size_t)l * n * n;
+                    const double *bc = bcf + (size_t)l * n * n;
                     for (int a = 0; a < n; ++a) {
                         double b = 0.0, h = 0.0;
 #pragma unroll
                         for (int k = 0; k < NA; ++k) {
-                            const int kk = k < n ? k : n - 1;
-                            b += bc[a * n + kk] * ex[k];
-                            h += hc[a * n + kk] * ex[k];
+                            const double cf = bc[a * n + (k < n ? k : n - 1)];
+                            b += cf * ex[k];
+                            h += cf * ea[k];
                         }
                         bo[a * WP] = (ST)b;
                         ho[a * WP] = (ST)h;

@@ -140,8 +140,8 @@ struct DensityLaunch {
     bool hi;         // the variant compiled for three waves per SIMD (see density_has_high)
 };
 struct DescLaunch {
-    int W;      // edges per chunk (0: the descriptor path uses k_density)
-    int ql, na; // lm slots per lane, accumulators per slot
+    int W;          // edges per chunk (0: the descriptor path uses k_density)
+    int ql, na, sr; // tasks per thread, radial size, species slots
     size_t lds;
     int blocks; // resident workgroups (persistent launch)
 };
@@ -196,9 +196,9 @@ hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f6
 // one-wave-per-center descriptor kernel (GTO): the shape of its accumulators
 // (false if the basis has none), LDS bytes for W edges per chunk, resident
 // workgroups per CU, launch (desc and c_out may each be NULL)
-bool desc_shape(const Params &P, int *ql, int *na);
+bool desc_shape(const Params &P, int *ql, int *na, int *sr);
 size_t desc_lds_bytes(const Params &P, int W, bool st64);
-int desc_blocks_per_cu(bool f64, bool ar64, int ql, int na, size_t lds);
+int desc_blocks_per_cu(bool f64, bool ar64, int ql, int na, int sr, size_t lds);
 hipError_t launch_desc(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DescLaunch &cfg,
                        void *desc, void *c_out, hipStream_t st);
 // one-workgroup-per-center density step of the Jacobian path (GTO): shape,

@@ -41,22 +41,26 @@ static const void *density_kernel(bool f64, bool ar64, int mode, int rbf, bool h
     return ar64 ? density_kernel_t<float, double>(mode, rbf, hi) : density_kernel_t<float, float>(mode, rbf, hi);
 }
 
-// k_desc variants: QT (lm, pair of radial indices) tasks per thread and NA >=
-// n_max (groups of 4 measured 27% slower at 10^6 atoms: two waves then do the
-// projection while the other two wait at the barrier)
+// k_desc variants: QT (lm, pair of radial indices) tasks per thread, NA >=
+// n_max, SR >= S species slots (groups of 4 radial indices measured 27% slower
+// at 10^6 atoms: two waves then do the projection while the other two wait)
 constexpr int DESC_AG = 2;
-template <typename T, typename ST>
-static const void *desc_kernel_t(int qt, int na) {
-    if (qt == 1 && na == 8) return (const void *)dev::k_desc<T, T, ST, 1, DESC_AG, 8>;
-    if (qt == 1 && na == 16) return (const void *)dev::k_desc<T, T, ST, 1, DESC_AG, 16>;
-    if (qt == 2 && na == 8) return (const void *)dev::k_desc<T, T, ST, 2, DESC_AG, 8>;
-    if (qt == 2 && na == 16) return (const void *)dev::k_desc<T, T, ST, 2, DESC_AG, 16>;
-    if (qt == 4 && na == 16) return (const void *)dev::k_desc<T, T, ST, 4, DESC_AG, 16>;
+template <typename T, typename ST, int SR>
+static const void *desc_kernel_s(int qt, int na) {
+    if (qt == 1 && na == 8) return (const void *)dev::k_desc<T, T, ST, 1, DESC_AG, 8, SR>;
+    if (qt == 1 && na == 16) return (const void *)dev::k_desc<T, T, ST, 1, DESC_AG, 16, SR>;
+    if (qt == 2 && na == 8) return (const void *)dev::k_desc<T, T, ST, 2, DESC_AG, 8, SR>;
+    if (qt == 2 && na == 16) return (const void *)dev::k_desc<T, T, ST, 2, DESC_AG, 16, SR>;
+    if (qt == 4 && na == 16) return (const void *)dev::k_desc<T, T, ST, 4, DESC_AG, 16, SR>;
     return nullptr;
 }
-static const void *desc_kernel(bool f64, bool ar64, int ql, int na) {
-    if (f64) return desc_kernel_t<double, double>(ql, na);
-    return ar64 ? desc_kernel_t<float, double>(ql, na) : desc_kernel_t<float, float>(ql, na);
+template <typename T, typename ST>
+static const void *desc_kernel_t(int qt, int na, int sr) {
+    return sr == 2 ? desc_kernel_s<T, ST, 2>(qt, na) : (sr == 4 ? desc_kernel_s<T, ST, 4>(qt, na) : nullptr);
+}
+static const void *desc_kernel(bool f64, bool ar64, int qt, int na, int sr) {
+    if (f64) return desc_kernel_t<double, double>(qt, na, sr);
+    return ar64 ? desc_kernel_t<float, double>(qt, na, sr) : desc_kernel_t<float, float>(qt, na, sr);
 }
 
 // k_djac variants: QT (lm, pair) tasks per thread, NA >= n_max, SR >= S species slots
@@ -166,7 +170,9 @@ hipError_t set_lds_limits() {
         for (int ar64 = 0; ar64 < 2; ++ar64)
             for (int qt : {1, 2, 4})
                 for (int na : {8, 16})
-                    if (desc_kernel(f64 != 0, ar64 != 0, qt, na)) SOAP_SET(desc_kernel(f64 != 0, ar64 != 0, qt, na));
+                    for (int sr : {2, 4})
+                        if (desc_kernel(f64 != 0, ar64 != 0, qt, na, sr))
+                            SOAP_SET(desc_kernel(f64 != 0, ar64 != 0, qt, na, sr));
     for (int f64 = 0; f64 < 2; ++f64)
         for (int ar64 = 0; ar64 < 2; ++ar64)
             for (int qt : {1, 2})
@@ -210,19 +216,21 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
     return e;
 }
 
-bool desc_shape(const Params &P, int *qt, int *na) {
-    if (P.rbf != 0) return false;
+bool desc_shape(const Params &P, int *qt, int *na, int *sr) {
+    if (P.rbf != 0 || P.S > 4) return false;
     const int t = dev::desc_tasks(P, DESC_AG);
     *qt = t <= 1 ? 1 : (t <= 2 ? 2 : 4);
     *na = P.n <= 8 ? 8 : 16;
-    return t <= 4 && desc_kernel(false, false, *qt, *na) != nullptr;
+    *sr = P.S <= 2 ? 2 : 4;
+    return t <= 4 && desc_kernel(false, false, *qt, *na, *sr) != nullptr;
 }
 
 size_t desc_lds_bytes(const Params &P, int W, bool st64) { return 8 * dev::desc_lds_doubles(P, W, st64 ? 8 : 4); }
 
-int desc_blocks_per_cu(bool f64, bool ar64, int ql, int na, size_t lds) {
+int desc_blocks_per_cu(bool f64, bool ar64, int ql, int na, int sr, size_t lds) {
     int nb = 0;
-    const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, desc_kernel(f64, ar64, ql, na), BSC, lds);
+    const hipError_t e =
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, desc_kernel(f64, ar64, ql, na, sr), BSC, lds);
     return (e == hipSuccess && nb > 0) ? nb : 0;
 }
 
@@ -235,8 +243,8 @@ hipError_t launch_desc(const Params &P, const Rows &R, const void *pos, bool f64
     void *args[] = {&Pk, &Rk, &pos, &W, &desc, &c_out};
     // persistent: as many workgroups as stay resident, each striding over the centers
     const int64_t blocks = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
-    return hipLaunchKernel(desc_kernel(f64, ar64, cfg.ql, cfg.na), dim3((unsigned)blocks), dim3(BSC), args, cfg.lds,
-                           st);
+    return hipLaunchKernel(desc_kernel(f64, ar64, cfg.ql, cfg.na, cfg.sr), dim3((unsigned)blocks), dim3(BSC), args,
+                           cfg.lds, st);
 }
 
 bool djac_shape(const Params &P, int *qt, int *na, int *sr) {
