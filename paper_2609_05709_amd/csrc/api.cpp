@@ -97,6 +97,8 @@ struct soap_ctx {
     NbrWork nw{};
     DevBuf b_zero, b_bstart, b_acell, b_srec, b_sspec, b_deg, b_slots, b_scan, b_spec, b_row, b_cols, b_cscratch;
     DevBuf b_avg, b_avg_part; // averaged modes: per-center rows, column partial sums and means
+    DevBuf b_radial;          // polynomial quadrature: radial factors of a call's edges
+    std::vector<int64_t> h_row; // polynomial quadrature: host copy of the CSR row offsets
     // periodic cell (soap_set_cell) and the extended structure of the last build
     bool periodic = false, built_periodic = false;
     PeriodicCell cell{};
@@ -524,6 +526,13 @@ Rows rows_of(const soap_ctx *c) { return rows_of(c, 0, c->nc); }
 // (c, Dx, Dy, Dz)
 size_t scratch_bytes_per_center(const soap_ctx *c) { return 8 * 4 * (size_t)c->P.S * c->P.n * c->P.L; }
 
+// the radial pass (polynomial quadrature): bytes for the edges of centers [first, first + count)
+size_t radial_bytes(const soap_ctx *c, int64_t first, int64_t count) {
+    if (c->P.rbf != 1 || count == 0 || c->h_row.size() != (size_t)c->nc + 1) return 0;
+    return radial_bytes_per_edge(c->P) * (size_t)(c->h_row[first + count] - c->h_row[first]);
+}
+size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
 Params params_for(const soap_ctx *c, int mode) {
     Params P = c->P;
     const int G = c->groups[mode];
@@ -827,6 +836,13 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     }
     if ((rc = build_rows(c, n_rows_atoms, n_atoms, pos_rows, Z_rows, n_centers, cen_rows, &E, st)) != SOAP_OK)
         return rc;
+    c->h_row.clear();
+    if (c->rbf == SOAP_RBF_POLYNOMIAL) { // the radial pass sizes and places each call's edges from it
+        c->h_row.resize((size_t)n_centers + 1);
+        hipError_t e = hipMemcpyAsync(c->h_row.data(), c->b_row.p, 8 * c->h_row.size(), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) return hip_fail(c, e, "neighbour row offsets");
+    }
     timer.done();
     c->have_rows = true;
     c->n_atoms = n_atoms;
@@ -916,6 +932,28 @@ static bool jacobian_path_ok(const soap_ctx *c, int mode) {
     return c->dens_ok[mode] && (mode != 1 || (c->jac_ok && (c->groups[1] == 1 || c->out_ok)));
 }
 
+// The polynomial quadrature's radial factors (B_nl, Bh_nl) of the edges of
+// centers [first, first + count), evaluated once per call by k_radial into
+// buf (NULL = the context's buffer, grown as needed) and read by every
+// kernel of the call through P.rad.  Nothing to do for the other bases.
+static int prepare_radial(soap_ctx *c, int64_t first, int64_t count, void *buf, hipStream_t st) {
+    c->P.rad = nullptr;
+    c->P.rad_e0 = 0;
+    if (c->P.rbf != 1 || count == 0) return SOAP_OK;
+    if (c->h_row.size() != (size_t)c->nc + 1) return fail(c, SOAP_ESTATE, "neighbour row offsets missing");
+    if (!buf) {
+        hipError_t e = c->b_radial.ensure(radial_bytes(c, first, count));
+        if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(radial factors)");
+        buf = c->b_radial.p;
+    }
+    const int64_t e0 = c->h_row[first];
+    hipError_t e = launch_radial(c->P, rows_of(c, first, count), c->pos, c->built_f64, e0, buf, st);
+    if (e != hipSuccess) return hip_fail(c, e, "radial kernel");
+    c->P.rad = (const double2 *)buf;
+    c->P.rad_e0 = e0;
+    return SOAP_OK;
+}
+
 // Centers [first, first + count) of the neighbour list; outputs are indexed
 // from the batch's first center (and edge).
 // mode as launch_density: 0 descriptor / coefficients, 1 descriptor + Jacobian,
@@ -924,20 +962,25 @@ static bool jacobian_path_ok(const soap_ctx *c, int mode) {
 // timed = false: no timer events (they may allocate).  wg_per_cu > 0 caps
 // the persistent density kernel's workgroups per CU.
 static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void *desc, void *c_out, void *jself,
-                       void *jc_edge, double *scratch, void *stream, bool timed = true, int wg_per_cu = 0) {
+                       void *jc_edge, double *scratch, void *stream, bool timed = true, int wg_per_cu = 0,
+                       bool prep_radial = true) {
     if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
     int rc;
     if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
     if (!jacobian_path_ok(c, mode))
         return fail(c, SOAP_EINVAL, "basis too large for the on-chip memory of the %s kernels",
                     mode == 2 ? "coefficient Jacobian" : "Jacobian");
-    const Params P = params_for(c, mode);
+    // a caller-given scratch also holds the radial factors, after the coefficients
+    void *rbuf = (scratch && mode == 1) ? (char *)scratch + align256(scratch_bytes_per_center(c) * (size_t)count)
+                                        : nullptr;
     if (mode == 1 && !scratch) {
         hipError_t e = c->b_cscratch.ensure(scratch_bytes_per_center(c) * (size_t)count);
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
         scratch = c->b_cscratch.as<double>();
     }
     SegTimer timer(c, 1, to_stream(stream), timed);
+    if (prep_radial && (rc = prepare_radial(c, first, count, rbuf, to_stream(stream))) != SOAP_OK) return rc;
+    const Params P = params_for(c, mode);
     if (mode == 0 && c->desc_cfg.W > 0) { // one wave per center
         hipError_t e = launch_desc(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, c->desc_cfg, desc, c_out,
                                    to_stream(stream));
@@ -1048,6 +1091,12 @@ static int run_derivatives_pipelined(soap_ctx *c, int64_t first, int64_t count, 
     if (e == hipSuccess) e = c->b_cscratch.ensure(scratch_bytes_per_center(c) * (size_t)count);
     if (e != hipSuccess) return hip_fail(c, e, "pipelined derivatives (setup)");
     double *scratch = c->b_cscratch.as<double>();
+    { // the radial factors of every chunk at once: the chunks' Jacobian launches read them on the other stream
+        SegTimer timer(c, 1, st);
+        const int rc = prepare_radial(c, first, count, nullptr, st);
+        if (rc != SOAP_OK) return rc;
+        timer.done();
+    }
     const size_t elt = c->built_f64 ? 8 : 4, pc = scratch_bytes_per_center(c) / 8;
     for (int k = 0; k < K; ++k) {
         const int64_t cf = first + count * k / K, cn = first + count * (k + 1) / K - cf;
@@ -1055,7 +1104,7 @@ static int run_derivatives_pipelined(soap_ctx *c, int64_t first, int64_t count, 
         const size_t o = (size_t)(cf - first);
         int rc = run_density(c, 1, cf, cn, (char *)desc_dev + o * c->F * elt, nullptr,
                              (char *)jac_self_dev + o * 3 * c->F * elt, nullptr, scratch + o * pc, stream, true,
-                             c->pipe_density_wg);
+                             c->pipe_density_wg, false);
         if (rc != SOAP_OK) return rc;
         if ((e = hipEventRecord(c->pipe_ev[k], st)) != hipSuccess ||
             (e = hipStreamWaitEvent(c->aux, c->pipe_ev[k], 0)) != hipSuccess)
@@ -1138,12 +1187,12 @@ int soap_derivatives_batch_noalloc(soap_ctx *c, int64_t first, int64_t count, vo
     if (rc != SOAP_OK) return rc;
     if (count > 0 && (!desc_dev || !jac_self_dev || !jac_edge_dev))
         return fail(c, SOAP_EINVAL, "output pointer is NULL");
-    const size_t need = scratch_bytes_per_center(c) * (size_t)count;
+    const size_t need = align256(scratch_bytes_per_center(c) * (size_t)count) + radial_bytes(c, first, count);
     if (need > (size_t)SOAP_STATIC_SCRATCH_BYTES)
         return fail(c, SOAP_ECAPACITY,
-                    "%lld centers need %zu bytes of coefficient scratch, above the static %d bytes (at most %lld "
+                    "%lld centers need %zu bytes of coefficient scratch%s, above the static %d bytes (at most %lld "
                     "centers per call for this basis)",
-                    (long long)count, need, SOAP_STATIC_SCRATCH_BYTES,
+                    (long long)count, need, c->P.rbf == 1 ? " and radial factors" : "", SOAP_STATIC_SCRATCH_BYTES,
                     (long long)(SOAP_STATIC_SCRATCH_BYTES / scratch_bytes_per_center(c)));
     if (!c->static_scratch) return fail(c, SOAP_EHIP, "the static scratch of device %d is not available", c->device);
     // the density kernel writes every scratch entry the later kernels read,
@@ -1166,7 +1215,7 @@ int soap_plan_batches(soap_ctx *c, int32_t what, int64_t budget_bytes, int64_t m
     // per center: descriptor row (+ center block and coefficient scratch);
     // per edge: its neighbour block
     const int64_t per_center = (int64_t)(elt * c->F * (jac ? 4 : 1) + (jac ? scratch_bytes_per_center(c) : 0));
-    const int64_t per_edge = jac ? (int64_t)(elt * 3 * c->Fe) : 0;
+    const int64_t per_edge = (jac ? (int64_t)(elt * 3 * c->Fe) : 0) + (c->P.rbf == 1 ? (int64_t)radial_bytes_per_edge(c->P) : 0);
     int64_t nb = 0, b0 = 0;
     while (b0 < c->nc) {
         int64_t b1 = b0, bytes = 0;

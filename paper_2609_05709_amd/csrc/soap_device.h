@@ -282,7 +282,6 @@ struct Tables {
     const double *Kl;      // K_l = pi sqrt(8/(2l+1)), l < 16
     const double2 *bcp;    // GTO: [k][n][lc] = (betaC, -2 betaC a') of B_nl = sum_k betaC_nk e^{-a'_kl r^2}
     const double *aprime;  // GTO: [k][lc]
-    const double *G, *rq;  // polynomial: [n][Q], [Q]
     const double *WN, *B0; // polynomial, Laplace form: [n][n+3][4] Chebyshev coefficients (stage_edges); B_n0(0) [n]
     const double2 *bcdd;   // GTO, compensated: [k][n][lc] = (betaC, its remainder)
     const double2 *apdd;   // GTO, compensated: [k][lc] = (a', its remainder)
@@ -296,7 +295,6 @@ __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lg
     const size_t ldN = (size_t)P.lmax + 2, n = (size_t)P.n;
     size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
     if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
-    else if (P.rbf == 1) d += even(n * P.Q) + even((size_t)P.Q);
     else if (P.rbf == 2) d += 4 * n * (n + 3) + even(n);
     else d += 2 * (size_t)lgc * n * n + 2 * (size_t)lgc * n;
     return d;
@@ -316,8 +314,8 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     // (betaC, betaCa) pairs | G | WN | (betaC, remainder) pairs, then aprime | rq | B0 | (a', remainder) pairs
     const size_t szA = rbf == 0 ? 2 * (size_t)lgc * n * n
-                                : (rbf == 1 ? (size_t)n * P.Q : (rbf == 2 ? 4 * (size_t)n * (n + 3) : 2 * (size_t)lgc * n * n));
-    const size_t szB = rbf == 0 ? (size_t)lgc * n : (rbf == 1 ? (size_t)P.Q : (rbf == 2 ? (size_t)n : 2 * (size_t)lgc * n));
+                                : (rbf == 1 ? 0 : (rbf == 2 ? 4 * (size_t)n * (n + 3) : 2 * (size_t)lgc * n * n));
+    const size_t szB = rbf == 0 ? (size_t)lgc * n : (rbf == 1 ? 0 : (rbf == 2 ? (size_t)n : 2 * (size_t)lgc * n));
     double *A = cv.take(szA), *B = cv.take(szB);
     for (int k = tid; k < ldN * ldN; k += bs) Ntl[k] = P.Nt[k];
     for (int k = tid; k < 4 * grad_pairs(lmax); k += bs) gc[k] = P.gcoef[k];
@@ -334,9 +332,6 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
             const int lc = s / n, k = s - lc * n;
             B[k * lgc + lc] = P.aprime[(size_t)lg0 * n + s];
         }
-    } else if (rbf == 1) {
-        for (int k = tid; k < (int)szA; k += bs) A[k] = P.G[k];
-        for (int k = tid; k < (int)szB; k += bs) B[k] = P.rq[k];
     } else if (rbf == 3) {
         // global [l][n][k] -> LDS [k][n][lc] pairs; global [l][k] -> LDS [k][lc] pairs
         const size_t o = (size_t)lg0 * n * n;
@@ -351,7 +346,7 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
             B[2 * (k * lgc + lc)] = P.aprime[(size_t)lg0 * n + s];
             B[2 * (k * lgc + lc) + 1] = P.aprime_lo[(size_t)lg0 * n + s];
         }
-    } else {
+    } else if (rbf == 2) {
         // a neighbour at distance 0 adds the on-site term: B_n0 S_00 = c0_n
         for (int k = tid; k < (int)szA; k += bs) A[k] = P.WN[k];
         for (int k = tid; k < (int)szB; k += bs) B[k] = P.c0[k] * sqrt(4.0 * M_PI);
@@ -360,22 +355,20 @@ __device__ __forceinline__ void load_tables(const Params &P, Carver &cv, Tables 
     T.Nt = Ntl;
     T.gcoef = (const double2 *)gc;
     T.bcp = (const double2 *)A;
-    T.G = A;
     T.WN = A;
     T.aprime = B;
-    T.rq = B;
     T.B0 = B;
     T.bcdd = (const double2 *)A;
     T.apdd = (const double2 *)B;
 }
 
-// X scratch per edge: GTO exponentials n * lgc; polynomial quadrature table
-// Q * (lg1 + 1) (all orders 0..lg1 so the Bessel recurrences run in place);
-// Laplace form: the four l-independent values P_j per n, 4 n; compensated
-// GTO: the exponentials in double-double, 2 n * lgc
+// X scratch per edge: GTO exponentials n * lgc; none for the polynomial
+// quadrature (its radial factors come from k_radial); Laplace form: the four
+// l-independent values P_j per n, 4 n; compensated GTO: the exponentials in
+// double-double, 2 n * lgc
 __host__ __device__ __forceinline__ size_t stage_x_doubles(const Params &P, int lgc, int lg1) {
-    return P.rbf == 0 ? (size_t)P.n * lgc
-                      : (P.rbf == 1 ? (size_t)P.Q * (lg1 + 1) : (P.rbf == 2 ? 4 * (size_t)P.n : 2 * (size_t)P.n * lgc));
+    (void)lg1;
+    return P.rbf == 0 ? (size_t)P.n * lgc : (P.rbf == 1 ? 0 : (P.rbf == 2 ? 4 * (size_t)P.n : 2 * (size_t)P.n * lgc));
 }
 
 // Synchronisation inside one wave: LDS writes become visible to the other
@@ -425,11 +418,11 @@ template <bool GRAD, typename BT = double, int NT = 0, int LWT = 0, typename YT 
 __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT *__restrict__ YY, YLayout yl,
                                             typename Pair<BT>::type *__restrict__ BB, double *__restrict__ X,
                                             const double *__restrict__ geo, int nb, int lane, int lg0, int lg1,
-                                            bool scaleK) {
+                                            bool scaleK, int64_t r0) {
     const int n = NT ? NT : P.n, ldN = (LWT ? LWT - 1 : P.lmax) + 2, lgc = lg1 - lg0, nlc = n * lgc;
     const int lgY0 = (GRAD && lg0 > 0) ? lg0 - 1 : lg0;
     const float inv_lg1 = 1.0f / (float)lg1, inv_nlc = 1.0f / (float)nlc, inv_lgc = 1.0f / (float)lgc;
-    const int rbf = RBF >= 0 ? RBF : P.rbf, Q = P.Q, tw = lg1 + 1;
+    const int rbf = RBF >= 0 ? RBF : P.rbf;
     // phase 1: harmonic columns (edge, m), then the radial scratch (two
     // independent exponentials per lane trip)
     for (int it = lane; it < nb * lg1; it += 64) {
@@ -459,31 +452,23 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
             X[it] = v1;
             X[i2] = v2;
         }
-    } else {
-        // polynomial: the quadrature table [e][q][0..lg1] (rbf 1), or the Laplace form's (rbf 2)
-        // P_j(u) = d^j/du^j sum_k WN_nk u^(k+2), u = r_cut - r, at [e][n][j] from their Chebyshev
-        // series in t = 2u/r_cut - 1 (Clenshaw's recurrence).  One loop serves both: a separate loop
-        // for the Laplace form costs every kernel that inlines this staging two more registers.
-        const int per = rbf == 1 ? Q : 4 * n;
+    } else if (rbf == 2) {
+        // the Laplace form's P_j(u) = d^j/du^j sum_k WN_nk u^(k+2), u = r_cut - r, at [e][n][j]
+        // from their Chebyshev series in t = 2u/r_cut - 1 (Clenshaw's recurrence)
+        const int per = 4 * n;
         const float inv_per = 1.0f / (float)per;
         for (int it = lane; it < nb * per; it += 64) {
             const int e = qdiv(it, inv_per), q = it - e * per;
             const double r = geo[4 * e + 3];
-            if (rbf == 1) {
-                const double rq = T.rq[q];
-                const double gq = exp(-0.5 * (rq - r) * (rq - r) * P.inv_s2);
-                bessel_scaled_lds(lg1, rq * r * P.inv_s2, gq, X + (size_t)it * tw);
-            } else {
-                const double tt = (P.rc - r) * P.inv_rc2 - 1.0, t2 = tt + tt;
-                const double *ch = T.WN + (size_t)(q >> 2) * (n + 3) * 4 + (q & 3);
-                double b1 = 0.0, b2 = 0.0;
-                for (int i = n + 2; i >= 1; --i) {
-                    const double nb1 = t2 * b1 - b2 + ch[4 * i];
-                    b2 = b1;
-                    b1 = nb1;
-                }
-                X[it] = tt * b1 - b2 + ch[0];
+            const double tt = (P.rc - r) * P.inv_rc2 - 1.0, t2 = tt + tt;
+            const double *ch = T.WN + (size_t)(q >> 2) * (n + 3) * 4 + (q & 3);
+            double b1 = 0.0, b2 = 0.0;
+            for (int i = n + 2; i >= 1; --i) {
+                const double nb1 = t2 * b1 - b2 + ch[4 * i];
+                b2 = b1;
+                b1 = nb1;
             }
+            X[it] = tt * b1 - b2 + ch[0];
         }
     }
     wave_sync();
@@ -601,28 +586,14 @@ __device__ __forceinline__ void stage_edges(const Params &P, const Tables &T, YT
             BB[it] = Pair<BT>::make(K * b, K * bh);
         }
     } else {
+        // polynomial quadrature: the factors k_radial left for this call's edges, [edge][n][l]
+        const int lwa = P.lmax + 1;
+        const double2 *rad = P.rad + (r0 - P.rad_e0) * (size_t)n * lwa + lg0;
         for (int it = lane; it < nd; it += 64) {
-            const int e = qdiv(it, inv_nlc), t = it - e * nlc, a = qdiv(t, inv_lgc), l = lg0 + t - a * lgc;
-            const double r = geo[4 * e + 3];
-            const double *G = T.G + (size_t)a * Q;
-            const double *tq = X + (size_t)e * Q * tw;
-            double b = 0.0, bh = 0.0;
-            for (int q = 0; q < Q; ++q) {
-                const double tl = tq[q * tw + l];
-                b += G[q] * tl;
-                if (GRAD) bh += G[q] * (T.rq[q] * tq[q * tw + l + 1] - r * tl);
-            }
-            if (r == 0.0) {
-                b = (l == 0) ? b : 0.0;
-                bh = 0.0;
-            } else {
-                double ir = 1.0 / r, rl = 1.0;
-                for (int k = 0; k < l; ++k) rl *= ir;
-                b *= rl;
-                bh *= rl * ir * P.inv_s2;
-            }
-            const double K = scaleK ? T.Kl[l] : 1.0;
-            BB[it] = Pair<BT>::make(K * b, K * bh);
+            const int e = qdiv(it, inv_nlc), t = it - e * nlc, a = qdiv(t, inv_lgc), lc = t - a * lgc;
+            const double2 v = rad[((size_t)e * n + a) * lwa + lc];
+            const double K = scaleK ? T.Kl[lg0 + lc] : 1.0;
+            BB[it] = Pair<BT>::make(K * v.x, K * v.y);
         }
     }
     wave_sync();
@@ -643,6 +614,115 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
         geo[4 * t + 2] = z;
         geo[4 * t + 3] = sqrt(x * x + y * y + z * z);
         sp[t] = spec[j];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_radial: the polynomial basis's radial factors of every edge of a range of
+// centers, evaluated once per call and read by every density and Jacobian
+// kernel (quadrature form of the radial integral, Sec. 2.3: the sums over the
+// basis and over the nodes swapped, G[n][q] = w_q r_q^2 g_n(r_q) 4 pi):
+//   B_nl  = r^-l sum_q G_nq ii_l(x_q) g_q,
+//   Bh_nl = (1/r) dB_nl/dr
+//         = r^-l (1/r) sigma^-2 sum_q G_nq (r_q ii_{l+1}(x_q) - r ii_l(x_q)) g_q,
+// x_q = r r_q / sigma^2, g_q = exp(-(r_q - r)^2 / (2 sigma^2)) (ii_l the
+// exponentially scaled modified spherical Bessel function, the derivative
+// from i_l' = i_{l+1} + (l/x) i_l), and for an edge of length 0 only the
+// l = 0 factor, B_n0(0).  Output [edge - e_base][n][l] = (B_nl, Bh_nl) for
+// l <= l_max, unscaled by K_l.
+// One wave per center, four edges at a time: the Bessel values of (edge,
+// node) for 16 nodes at once go to the wave's LDS slab, then lane = (edge, l)
+// accumulates all NA radial indices over those nodes (G broadcast from LDS).
+// The node sums run in node order, as in the in-kernel evaluation.
+// ---------------------------------------------------------------------------
+constexpr int NWR = 4, BSR = 64 * NWR;
+constexpr int RAD_EC = 4, RAD_QC = 16; // edges per wave pass; nodes per Bessel slab
+
+__host__ __device__ __forceinline__ int radial_qpad(int Q) { return (Q + RAD_QC - 1) / RAD_QC * RAD_QC; }
+// LDS doubles of k_radial: G [NA][Qp], r_q [Qp], and per wave the Bessel slab [64][l_max + 2]
+__host__ __device__ __forceinline__ size_t radial_lds_doubles(const Params &P, int na) {
+    const size_t qp = (size_t)radial_qpad(P.Q);
+    return even((size_t)na * qp) + even(qp) + NWR * even(64 * ((size_t)P.lmax + 2));
+}
+
+template <typename PosT, int NA>
+__global__ __launch_bounds__(BSR) void k_radial(Params P, Rows R, const PosT *__restrict__ pos, int64_t e_base,
+                                                double2 *__restrict__ out) {
+    extern __shared__ __align__(16) double smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = P.n, Q = P.Q, Qp = radial_qpad(Q), lw = P.lmax + 1, tw = lw + 1;
+    Carver cv{smem};
+    double *G = cv.take((size_t)NA * Qp);
+    double *rq = cv.take((size_t)Qp);
+    double *slab = cv.take(0) + (size_t)wave * even(64 * (size_t)tw);
+    for (int k = tid; k < NA * Qp; k += BSR) {
+        const int a = k / Qp, q = k - a * Qp;
+        G[k] = (a < n && q < Q) ? P.G[(size_t)a * Q + q] : 0.0;
+    }
+    for (int k = tid; k < Qp; k += BSR) rq[k] = k < Q ? P.rq[k] : 0.0;
+    __syncthreads();
+    const int es = lane >> 4, sub = lane & 15; // edge slot; node (Bessel phase) or l (sum phase)
+    const int64_t nwaves = (int64_t)gridDim.x * NWR;
+    for (int64_t ci = (int64_t)blockIdx.x * NWR + wave; ci < R.nc; ci += nwaves) {
+        const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
+        const double px = (double)pos[3 * i], py = (double)pos[3 * i + 1], pz = (double)pos[3 * i + 2];
+        const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
+        for (int64_t eb = e0; eb < e1; eb += RAD_EC) {
+            const int64_t e = eb + es;
+            const bool live = e < e1;
+            double r = 0.0;
+            if (live) {
+                const int64_t j = R.cols[e];
+                const double x = (double)pos[3 * j] - px, y = (double)pos[3 * j + 1] - py,
+                             z = (double)pos[3 * j + 2] - pz;
+                r = sqrt(x * x + y * y + z * z);
+            }
+            double b[NA], h[NA];
+#pragma unroll
+            for (int a = 0; a < NA; ++a) b[a] = h[a] = 0.0;
+            double *mine = slab + (size_t)lane * tw;          // this lane's (edge, node) Bessel row
+            const double *col = slab + (size_t)es * RAD_QC * tw; // this lane's edge, all 16 nodes
+            const int l = sub < lw ? sub : lw - 1;
+            for (int q0 = 0; q0 < Qp; q0 += RAD_QC) {
+                const int q = q0 + sub;
+                if (live && q < Q) {
+                    const double xq = rq[q];
+                    const double gq = exp(-0.5 * (xq - r) * (xq - r) * P.inv_s2);
+                    bessel_scaled_lds(lw, xq * r * P.inv_s2, gq, mine);
+                } else {
+                    for (int k = 0; k < tw; ++k) mine[k] = 0.0;
+                }
+                wave_sync();
+                for (int qq = 0; qq < RAD_QC; ++qq) {
+                    const double tl = col[qq * tw + l], d = rq[q0 + qq] * col[qq * tw + l + 1] - r * tl;
+                    const double *g = G + q0 + qq;
+#pragma unroll
+                    for (int a = 0; a < NA; ++a) {
+                        const double ga = g[(size_t)a * Qp];
+                        b[a] += ga * tl;
+                        h[a] += ga * d;
+                    }
+                }
+                wave_sync(); // the slab is read before the next nodes overwrite it
+            }
+            if (live && sub < lw) {
+                double sb = 1.0, sh = 0.0;
+                if (r == 0.0) {
+                    sb = l == 0 ? 1.0 : 0.0;
+                } else {
+                    const double ir = 1.0 / r;
+                    double rl = 1.0;
+                    for (int k = 0; k < l; ++k) rl *= ir;
+                    sb = rl;
+                    sh = rl * ir * P.inv_s2;
+                }
+                double2 *o = out + (e - e_base) * (size_t)n * lw + l;
+#pragma unroll
+                for (int a = 0; a < NA; ++a)
+                    if (a < n) o[(size_t)a * lw] = make_double2(b[a] * sb, h[a] * sh);
+            }
+        }
     }
 }
 
@@ -1065,7 +1145,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
             for (int off = wave * W; off < rbn; off += NWD * W) {
                 const int nb = (rbn - off) < W ? (rbn - off) : W;
                 const double *geo = rgeo + 4 * off;
-                stage_edges<JAC, ST, 0, 0, ST, RBF>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false);
+                stage_edges<JAC, ST, 0, 0, ST, RBF>(P, T, YY, yl, BB, X, geo, nb, lane, lg0, lg1, false, rb0 + off);
                 for (int e = 0; e < nb; ++e) {
                     const int s = __builtin_amdgcn_readfirstlane(rsp[off + e]);
                     if (s != cur) {
@@ -1951,7 +2031,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jac
             const double *geo = rgeo + 4 * off;
             const int *spc = rsp + off;
             stage_edges<true, AT, NT, LWT, double, RBF>(P, T, YY, YLayout{4 * L, L, 1, 0}, BB, XU, geo, nb, lane, 0, lw,
-                                                        true);
+                                                        true, rb0 + off);
 
             // ---- precontraction on the matrix cores ----
             // chunks j = (l, ch) in l-major order, operands loaded JB at a time

@@ -27,6 +27,9 @@ struct Params {
     const double *G;           // polynomial [n][Q], includes 4 pi
     const double *rq;          // polynomial [Q]
     const double *WN;          // polynomial, Laplace form [n][n+3][4]: Chebyshev series of P_n0..P_n3 on [0, rc]
+    const double2 *rad;        // polynomial quadrature: radial factors (B_nl, Bh_nl) of the call's edges,
+                               // [edge - rad_e0][n][l] (k_radial)
+    int64_t rad_e0;            // structure index of the first edge of rad
     const double *c0;          // on-site term [n]
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)
@@ -206,6 +209,11 @@ hipError_t launch_desc(const Params &P, const Rows &R, const void *pos, bool f64
 // coefficients for k_jacobian)
 bool djac_shape(const Params &P, int *qt, int *na, int *sr);
 size_t djac_lds_bytes(const Params &P, int W, bool st64);
+// the polynomial quadrature's radial pass: (B_nl, Bh_nl) of every edge of the
+// rows, at out[edge - e_base][n][l]
+size_t radial_bytes_per_edge(const Params &P);
+hipError_t launch_radial(const Params &P, const Rows &R, const void *pos, bool f64, int64_t e_base, void *out,
+                         hipStream_t st);
 int djac_blocks_per_cu(bool f64, bool ar64, int qt, int na, int sr, size_t lds);
 hipError_t launch_djac(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjacLaunch &cfg,
                        void *desc, void *jself, double *c_scratch, hipStream_t st);

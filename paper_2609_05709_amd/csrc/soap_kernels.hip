@@ -81,6 +81,38 @@ static const void *djac_kernel(bool f64, bool ar64, int qt, int na, int sr) {
     return ar64 ? djac_kernel_t<float, double>(qt, na, sr) : djac_kernel_t<float, float>(qt, na, sr);
 }
 
+// k_radial variants: NA >= n_max radial indices per lane
+template <typename T> static const void *radial_kernel_t(int na) {
+    if (na == 4) return (const void *)dev::k_radial<T, 4>;
+    if (na == 8) return (const void *)dev::k_radial<T, 8>;
+    if (na == 12) return (const void *)dev::k_radial<T, 12>;
+    if (na == 16) return (const void *)dev::k_radial<T, 16>;
+    return nullptr;
+}
+static const void *radial_kernel(bool f64, int na) { return f64 ? radial_kernel_t<double>(na) : radial_kernel_t<float>(na); }
+static int radial_na(int n) { return n <= 4 ? 4 : (n <= 8 ? 8 : (n <= 12 ? 12 : 16)); }
+
+size_t radial_bytes_per_edge(const Params &P) { return 16 * (size_t)P.n * (P.lmax + 1); }
+
+hipError_t launch_radial(const Params &P, const Rows &R, const void *pos, bool f64, int64_t e_base, void *out,
+                         hipStream_t st) {
+    if (R.nc <= 0) return hipSuccess;
+    const int na = radial_na(P.n);
+    const void *k = radial_kernel(f64, na);
+    const size_t lds = 8 * dev::radial_lds_doubles(P, na);
+    int ncu = 256, dev_id = 0, per = 0;
+    (void)hipGetDevice(&dev_id);
+    (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev_id);
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k, BSR, lds) != hipSuccess || per < 1) per = 1;
+    // one wave per center, striding: enough workgroups to fill the chip, no more than the centers need
+    const int64_t need = (R.nc + NWR - 1) / NWR;
+    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(need, (int64_t)ncu * per));
+    Params Pk = P;
+    Rows Rk = R;
+    void *args[] = {&Pk, &Rk, &pos, &e_base, &out};
+    return hipLaunchKernel(k, dim3(blocks), dim3(BSR), args, lds, st);
+}
+
 bool density_has_high(int mode, int rbf) { return dev::dens_has_high(mode, rbf); }
 
 int density_blocks_per_cu(bool f64, bool ar64, int mode, int rbf, bool hi, size_t lds) {
@@ -178,6 +210,8 @@ hipError_t set_lds_limits() {
             for (int qt : {1, 2})
                 for (int na : {8, 16})
                     for (int sr : {2, 4}) SOAP_SET(djac_kernel(f64 != 0, ar64 != 0, qt, na, sr));
+    for (int f64 = 0; f64 < 2; ++f64)
+        for (int na : {4, 8, 12, 16}) SOAP_SET(radial_kernel(f64 != 0, na));
     SOAP_SET(k_outputs<float>);
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
