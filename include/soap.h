@@ -137,7 +137,22 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  *              0 = automatic (default), -1 = the density kernel shared with
  *              the Jacobian path, 16 / 32 / 64 = the descriptor kernel
  *              whose waves each own whole centers, with at most that many
- *              edges per chunk (the widest that fits on chip).
+ *              edges per chunk (the widest that fits on chip);
+ *   "djac_tile": kernel choice of the density step of the GTO Jacobian path
+ *              (a tuning knob, results identical up to rounding order):
+ *              0 = automatic (default), -1 = the shared density kernel and
+ *              the output kernel, 32 / 64 = the kernel that gives each
+ *              center a workgroup, with at most that many edges per chunk;
+ *   "out_rows" : 1 (default) = the output kernel of the Jacobian path
+ *              writes whole rows where c and one component of D fit on
+ *              chip, 0 = always in l-groups (a tuning knob, results
+ *              identical);
+ *   "pipeline" : 1..16 (default 1): soap_derivatives splits its centers
+ *              into that many chunks and overlaps each chunk's edge
+ *              Jacobian (a second stream) with the next chunk's density
+ *              step;
+ *   "pipeline_density_wg": 0..16 (default 0 = no cap), workgroups per
+ *              CU of the density kernel while pipelined.
  * Options take effect for calls made after this one; changing "dtype"
  * discards the neighbour list.  Errors: SOAP_EINVAL.
  */
@@ -151,7 +166,14 @@ int soap_set_option(soap_ctx *ctx, const char *key, int64_t value);
  *                               workgroup, 0 if the shared density kernel;
  *   "jacobian_density_kernel" : 1 if the density step of soap_derivatives runs
  *                               the kernel that gives each center a workgroup,
- *                               0 if the shared density kernel.
+ *                               0 if the shared density kernel;
+ *   "output_kernel_rows"      : 1 if the output kernel of the Jacobian path
+ *                               (run when the shared density kernel splits
+ *                               l into groups) writes whole rows, 0 if it
+ *                               works in l-groups;
+ *   "jacobian_l_groups"       : l-groups of the shared density kernel on the
+ *                               Jacobian path (above 1, the output kernel
+ *                               runs after it).
  * Errors: SOAP_EINVAL (NULL argument, unknown key).
  */
 int soap_get_option(const soap_ctx *ctx, const char *key, int64_t *value);

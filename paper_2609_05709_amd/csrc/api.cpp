@@ -130,6 +130,7 @@ struct soap_ctx {
     std::vector<hipEvent_t> pipe_ev;
     int desc_tile = 0; // option "desc_tile": 0 auto, -1 never k_desc, else edges per chunk
     OutPlan out_plan{};
+    bool out_rows = true; // option "out_rows": whole-row output kernel where it fits
     int groups[3] = {1, 1, 1};
     int lgrp[3][MAX_GROUPS + 1]{};
     // per-segment timing
@@ -291,7 +292,7 @@ int plan_launches(soap_ctx *c) {
         const int per_cu = density_blocks_per_cu(f64d, ar64, mode, P.rbf, hi, lds);
         c->dens_cfg[mode].blocks = std::max(1, ncu * per_cu / *G);
     }
-    c->out_ok = plan_outputs(P, c->dtype == SOAP_FP64, &c->out_plan) == 0;
+    c->out_ok = plan_outputs(P, c->dtype == SOAP_FP64, c->out_rows, &c->out_plan) == 0;
     // Jacobian kernel: W edges per wave tile.  The most resident waves per CU
     // first (latency hiding for its LDS-bound staging), then the widest tile.
     const bool f64 = c->dtype == SOAP_FP64;
@@ -632,6 +633,11 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         c->desc_tile = (int)value;
         return plan_launches(c);
     }
+    if (!std::strcmp(key, "out_rows")) {
+        if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "out_rows must be 0 or 1");
+        c->out_rows = value == 1;
+        return plan_launches(c);
+    }
     if (!std::strcmp(key, "timing")) {
         if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "timing must be 0 or 1");
         c->timing = value == 1;
@@ -659,6 +665,9 @@ int soap_get_option(const soap_ctx *c, const char *key, int64_t *value) {
                {"djac_tile", c->djac_tile},
                {"pipeline", c->pipe_chunks},
                {"pipeline_density_wg", c->pipe_density_wg},
+               {"out_rows", c->out_rows ? 1 : 0},
+               {"output_kernel_rows", c->out_plan.rows ? 1 : 0},
+               {"jacobian_l_groups", c->groups[1]},
                {"descriptor_kernel", c->desc_cfg.W > 0 ? 1 : 0},
                {"jacobian_density_kernel", c->djac_cfg.W > 0 ? 1 : 0}};
     for (const auto &t : tab)

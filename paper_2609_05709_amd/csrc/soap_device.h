@@ -630,29 +630,35 @@ __device__ __forceinline__ void load_rows(double *geo, int *sp, const PosT *__re
 // from i_l' = i_{l+1} + (l/x) i_l), and for an edge of length 0 only the
 // l = 0 factor, B_n0(0).  Output [edge - e_base][n][l] = (B_nl, Bh_nl) for
 // l <= l_max, unscaled by K_l.
-// One wave per center, four edges at a time: the Bessel values of (edge,
-// node) for 16 nodes at once go to the wave's LDS slab, then lane = (edge, l)
-// accumulates all NA radial indices over those nodes (G broadcast from LDS).
-// The node sums run in node order, as in the in-kernel evaluation.
+// A workgroup takes a block of cb consecutive centers, whose edges are
+// contiguous; its waves take four edges at a time, round-robin, each lane
+// finding its edge's center in the block's row offsets.  Per four edges the
+// Bessel values of (edge, node) for 16 nodes at once go to the wave's LDS
+// slab, then lane = (edge, l) accumulates all NA radial indices over those
+// nodes (G broadcast from LDS).  The node sums run in node order, as in the
+// in-kernel evaluation.
 // ---------------------------------------------------------------------------
 constexpr int NWR = 4, BSR = 64 * NWR;
 constexpr int RAD_EC = 4, RAD_QC = 16; // edges per wave pass; nodes per Bessel slab
+constexpr int RAD_CB_MAX = 256;        // centers per workgroup block
 
 __host__ __device__ __forceinline__ int radial_qpad(int Q) { return (Q + RAD_QC - 1) / RAD_QC * RAD_QC; }
-// LDS doubles of k_radial: G [NA][Qp], r_q [Qp], and per wave the Bessel slab [64][l_max + 2]
+// LDS doubles of k_radial: the block's row offsets [RAD_CB_MAX + 1], G [NA][Qp], r_q [Qp], and
+// per wave the Bessel slab [64][l_max + 2]
 __host__ __device__ __forceinline__ size_t radial_lds_doubles(const Params &P, int na) {
     const size_t qp = (size_t)radial_qpad(P.Q);
-    return even((size_t)na * qp) + even(qp) + NWR * even(64 * ((size_t)P.lmax + 2));
+    return even(RAD_CB_MAX + 1) + even((size_t)na * qp) + even(qp) + NWR * even(64 * ((size_t)P.lmax + 2));
 }
 
 template <typename PosT, int NA>
 __global__ __launch_bounds__(BSR) void k_radial(Params P, Rows R, const PosT *__restrict__ pos, int64_t e_base,
-                                                double2 *__restrict__ out) {
+                                                int cb, double2 *__restrict__ out) {
     extern __shared__ __align__(16) double smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = P.n, Q = P.Q, Qp = radial_qpad(Q), lw = P.lmax + 1, tw = lw + 1;
     Carver cv{smem};
+    int64_t *rp = (int64_t *)cv.take(RAD_CB_MAX + 1);
     double *G = cv.take((size_t)NA * Qp);
     double *rq = cv.take((size_t)Qp);
     double *slab = cv.take(0) + (size_t)wave * even(64 * (size_t)tw);
@@ -661,29 +667,37 @@ __global__ __launch_bounds__(BSR) void k_radial(Params P, Rows R, const PosT *__
         G[k] = (a < n && q < Q) ? P.G[(size_t)a * Q + q] : 0.0;
     }
     for (int k = tid; k < Qp; k += BSR) rq[k] = k < Q ? P.rq[k] : 0.0;
-    __syncthreads();
     const int es = lane >> 4, sub = lane & 15; // edge slot; node (Bessel phase) or l (sum phase)
-    const int64_t nwaves = (int64_t)gridDim.x * NWR;
-    for (int64_t ci = (int64_t)blockIdx.x * NWR + wave; ci < R.nc; ci += nwaves) {
-        const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
-        const double px = (double)pos[3 * i], py = (double)pos[3 * i + 1], pz = (double)pos[3 * i + 2];
-        const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1];
-        for (int64_t eb = e0; eb < e1; eb += RAD_EC) {
+    double *mine = slab + (size_t)lane * tw;          // this lane's (edge, node) Bessel row
+    const double *col = slab + (size_t)es * RAD_QC * tw; // this lane's edge, all 16 nodes
+    const int l = sub < lw ? sub : lw - 1;
+    for (int64_t c0 = (int64_t)blockIdx.x * cb; c0 < R.nc; c0 += (int64_t)gridDim.x * cb) {
+        const int ncb = (int)((R.nc - c0) < cb ? (R.nc - c0) : cb);
+        __syncthreads(); // the tables; the previous block's readers of rp
+        for (int t = tid; t <= ncb; t += BSR) rp[t] = R.row_ptr[c0 + t];
+        __syncthreads();
+        const int64_t E1 = rp[ncb];
+        for (int64_t eb = rp[0] + (int64_t)RAD_EC * wave; eb < E1; eb += (int64_t)RAD_EC * NWR) {
             const int64_t e = eb + es;
-            const bool live = e < e1;
+            const bool live = e < E1;
             double r = 0.0;
             if (live) {
+                int lo = 0, hi = ncb - 1; // the center of e: the last k with rp[k] <= e
+                while (lo < hi) {
+                    const int mid = (lo + hi + 1) >> 1;
+                    if (rp[mid] <= e) lo = mid;
+                    else hi = mid - 1;
+                }
+                const int64_t ci = c0 + lo;
+                const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
                 const int64_t j = R.cols[e];
-                const double x = (double)pos[3 * j] - px, y = (double)pos[3 * j + 1] - py,
-                             z = (double)pos[3 * j + 2] - pz;
+                const double x = (double)pos[3 * j] - (double)pos[3 * i], y = (double)pos[3 * j + 1] - (double)pos[3 * i + 1],
+                             z = (double)pos[3 * j + 2] - (double)pos[3 * i + 2];
                 r = sqrt(x * x + y * y + z * z);
             }
             double b[NA], h[NA];
 #pragma unroll
             for (int a = 0; a < NA; ++a) b[a] = h[a] = 0.0;
-            double *mine = slab + (size_t)lane * tw;          // this lane's (edge, node) Bessel row
-            const double *col = slab + (size_t)es * RAD_QC * tw; // this lane's edge, all 16 nodes
-            const int l = sub < lw ? sub : lw - 1;
             for (int q0 = 0; q0 < Qp; q0 += RAD_QC) {
                 const int q = q0 + sub;
                 if (live && q < Q) {
@@ -694,6 +708,7 @@ __global__ __launch_bounds__(BSR) void k_radial(Params P, Rows R, const PosT *__
                     for (int k = 0; k < tw; ++k) mine[k] = 0.0;
                 }
                 wave_sync();
+#pragma unroll 2
                 for (int qq = 0; qq < RAD_QC; ++qq) {
                     const double tl = col[qq * tw + l], d = rq[q0 + qq] * col[qq * tw + l + 1] - r * tl;
                     const double *g = G + q0 + qq;
@@ -1821,6 +1836,78 @@ __global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const doub
                 dst[q * lw + lg0 + lc] = rows[c * rstr + r];
             }
         }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// k_outputs_rows: the output kernel for bases whose c and one component of D
+// (every l) fit in LDS beside one output row.  One workgroup of NWO waves per
+// center, four passes: the power spectrum from c, then the three components
+// of the center block from c and D_x, D_y, D_z (power_tiles).  c stays in LDS
+// for all four; the next component of D is loaded into registers while the
+// current pass runs its tiles.  Each pass leaves one whole output row in LDS,
+// which goes out in contiguous lines (an l-group split writes part of every
+// line of a row per group).
+// ---------------------------------------------------------------------------
+constexpr int NWO = 16, BSO2 = 64 * NWO;
+constexpr int OUT_PF = 12; // prefetched doubles per thread: one slab of at most OUT_PF * BSO2
+
+__host__ __device__ __forceinline__ size_t outputs_rows_doubles(const Params &P, int out_bytes) {
+    const size_t slab = (size_t)P.L * P.S * P.n;
+    return 2 * even(slab) + even(((size_t)P.F * out_bytes + 7) / 8);
+}
+
+template <typename OutT>
+__global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *__restrict__ scratch,
+                                                       OutT *__restrict__ desc, OutT *__restrict__ jself) {
+    extern __shared__ __align__(16) double smem[];
+    __shared__ double Kl[16];
+    const int64_t ci = blockIdx.x;
+    const int S = P.S, n = P.n, Sn = S * n, lw = P.lmax + 1, F = P.F, tid = threadIdx.x;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int slab = P.L * Sn, sstr = (int)even((size_t)slab);
+    if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
+    double *Xc = smem, *Xd = smem + sstr;
+    OutT *row = (OutT *)(smem + 2 * sstr);
+    const double *src = scratch + ci * 4 * (size_t)slab; // [c, Dx, Dy, Dz][lm][species n]
+    // c and D_x, eight loads in flight per thread
+    for (int k0 = 0; k0 < 2 * slab; k0 += 8 * BSO2) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int k = k0 + u * BSO2 + tid;
+            v[u] = src[k < 2 * slab ? k : 0];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int k = k0 + u * BSO2 + tid;
+            if (k < 2 * slab) (k < slab ? Xc[k] : Xd[k - slab]) = v[u];
+        }
+    }
+    lds_barrier();
+    const PairIndex pq{S, n, 1.0f / (float)n};
+    for (int p = 0; p < 4; ++p) {
+        double pf[OUT_PF];
+        if (p == 1 || p == 2) {
+            const double *nx = src + (size_t)(p + 1) * slab;
+#pragma unroll
+            for (int u = 0; u < OUT_PF; ++u) {
+                const int k = u * BSO2 + tid;
+                pf[u] = nx[k < slab ? k : 0];
+            }
+        }
+        power_tiles<OutT>(CoefView{Xc, Xd, 1, Sn}, p - 1, Sn, 0, 0, lw, row, lw, 0, pq, wave, NWO, lane, Kl);
+        lds_barrier(); // the row is complete; D of this pass is read
+        OutT *dst = p == 0 ? desc + ci * F : jself + (ci * 3 + (p - 1)) * F;
+        for (int f = tid; f < F; f += BSO2) dst[f] = row[f];
+        if (p == 1 || p == 2) {
+#pragma unroll
+            for (int u = 0; u < OUT_PF; ++u) {
+                const int k = u * BSO2 + tid;
+                if (k < slab) Xd[k] = pf[u];
+            }
+        }
+        lds_barrier(); // the row is read and the next D is in place before the next pass
     }
 }
 

@@ -187,13 +187,16 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
                           const DensityLaunch &cfg, unsigned long long *work, WorkBase *epoch, void *desc, void *c_out,
                           void *jself, double *c_scratch, void *jc_edge, hipStream_t st);
 // power spectrum and center block from the coefficient scratch (Jacobian
-// path): l-groups of the output kernel, each sized to its LDS budget
+// path): whole rows (rows = true: c and one component of D for every l in
+// LDS), else l-groups of the output kernel, each sized to its LDS budget
 struct OutPlan {
+    bool rows;
     int n_groups;
     int lgrp[MAX_GROUPS + 1];
     size_t lds;
 };
-int plan_outputs(const Params &P, bool f64, OutPlan *O); // 0, or -1 if one l does not fit
+// allow_rows = false keeps the l-group kernel; 0, or -1 if one l does not fit
+int plan_outputs(const Params &P, bool f64, bool allow_rows, OutPlan *O);
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
                           void *jself, hipStream_t st);
 // one-wave-per-center descriptor kernel (GTO): the shape of its accumulators

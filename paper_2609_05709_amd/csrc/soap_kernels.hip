@@ -104,12 +104,14 @@ hipError_t launch_radial(const Params &P, const Rows &R, const void *pos, bool f
     (void)hipGetDevice(&dev_id);
     (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev_id);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k, BSR, lds) != hipSuccess || per < 1) per = 1;
-    // one wave per center, striding: enough workgroups to fill the chip, no more than the centers need
-    const int64_t need = (R.nc + NWR - 1) / NWR;
-    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(need, (int64_t)ncu * per));
+    // blocks of cb centers: about 16 workgroups per CU of work, at most
+    // RAD_CB_MAX centers a block, the blocks striding over the centers
+    int cb = (int)std::min<int64_t>(RAD_CB_MAX, std::max<int64_t>(1, R.nc / (16 * (int64_t)ncu)));
+    const int64_t need = (R.nc + cb - 1) / cb;
+    const int blocks = (int)std::max<int64_t>(1, std::min<int64_t>(need, (int64_t)ncu * per * 64));
     Params Pk = P;
     Rows Rk = R;
-    void *args[] = {&Pk, &Rk, &pos, &e_base, &out};
+    void *args[] = {&Pk, &Rk, &pos, &e_base, &cb, &out};
     return hipLaunchKernel(k, dim3(blocks), dim3(BSR), args, lds, st);
 }
 
@@ -134,10 +136,21 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool at64) {
 // Fewest contiguous l-groups whose LDS (c and one component of D for the
 // group, plus the group's part of an output row) stays within 80 KB, two
 // workgroups per CU; a single l above the budget may use up to the hard limit.
-int plan_outputs(const Params &P, bool f64, OutPlan *O) {
+int plan_outputs(const Params &P, bool f64, bool allow_rows, OutPlan *O) {
     const int lw = P.lmax + 1, ob = f64 ? 8 : 4;
-    // up to 52 KB (three workgroups per CU); a single l may use up to the hard limit
-    const size_t budget = 52 * 1024, hard = 159 * 1024;
+    const size_t hard = 159 * 1024;
+    // whole rows (k_outputs_rows) where c, one component of D and a row fit
+    const size_t rows_lds = 8 * outputs_rows_doubles(P, ob);
+    O->rows = allow_rows && rows_lds <= hard && (size_t)P.L * P.S * P.n <= (size_t)OUT_PF * BSO2;
+    if (O->rows) {
+        O->n_groups = 1;
+        O->lgrp[0] = 0;
+        O->lgrp[1] = lw;
+        O->lds = rows_lds;
+        return 0;
+    }
+    // l-groups of up to 52 KB (three workgroups per CU); a single l may use up to the hard limit
+    const size_t budget = 52 * 1024;
     int G = 0, l = 0;
     size_t worst = 0;
     O->lgrp[0] = 0;
@@ -157,6 +170,15 @@ int plan_outputs(const Params &P, bool f64, OutPlan *O) {
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
                           void *jself, hipStream_t st) {
     if (nc <= 0) return hipSuccess;
+    if (O.rows) {
+        if (f64)
+            hipLaunchKernelGGL(k_outputs_rows<double>, dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+                               (double *)desc, (double *)jself);
+        else
+            hipLaunchKernelGGL(k_outputs_rows<float>, dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+                               (float *)desc, (float *)jself);
+        return hipGetLastError();
+    }
     dim3 grid((unsigned)nc), block(BSO);
     if (f64)
         hipLaunchKernelGGL(k_outputs<double>, grid, block, O.lds, st, P, O, scratch, (double *)desc, (double *)jself);
@@ -213,6 +235,8 @@ hipError_t set_lds_limits() {
     for (int f64 = 0; f64 < 2; ++f64)
         for (int na : {4, 8, 12, 16}) SOAP_SET(radial_kernel(f64 != 0, na));
     SOAP_SET(k_outputs<float>);
+    SOAP_SET(k_outputs_rows<float>);
+    SOAP_SET(k_outputs_rows<double>);
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
     SOAP_SET(k_power_single<double>);

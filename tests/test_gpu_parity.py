@@ -265,3 +265,54 @@ def test_jacobian_density_kernel_chunk_widths(dtype, case):
             for x, y in zip((d, je, js), first):
                 assert torch.equal(x, y)
         sp.close()
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+@pytest.mark.parametrize("case", ["chno_poly_n10l10", "chno_poly_n6l8", "water_poly_n12l12"])
+def test_output_kernel_rows_and_groups(dtype, case):
+    """The output kernel of the Jacobian path (power spectrum and center block
+    from the coefficient scratch) writing whole rows and in l-groups:
+    descriptor and every block of every center against the oracle, and the
+    same bits both ways."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    if case.startswith("chno"):
+        nl = (10, 10) if case.endswith("n10l10") else (6, 8)
+        wl = workloads.Workload(case, (1, 6, 7, 8), "polynomial", 5.0, 0.4, nl[0], nl[1], True, ("none",))
+        st = workloads.random_small(60, 41, 5.0, species=(1, 6, 7, 8), dmin=0.85)
+    else:
+        wl = workloads.Workload(case, (1, 8), "polynomial", 5.0, 0.5, 12, 12, True, ("none",))
+        st = workloads.random_small(48, 43, 4.5, species=(1, 8), dmin=0.85)
+    idx = np.arange(st.n_atoms)
+    ref = oracle_for(wl).compute(st.pos64, st.Z, centers=idx, jacobian=True)
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
+    Z = torch.from_numpy(st.Z).cuda()
+    first = None
+    for rows in (1, 0):
+        sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+        sp._check(sp._L.soap_set_option(sp._h, b"out_rows", rows))
+        groups, used_rows = sp.get_option("jacobian_l_groups"), sp.get_option("output_kernel_rows")
+        sp.build_neighbors(pos, Z)
+        d, je, js = sp.derivatives()
+        row, cols = sp.neighbors()
+        torch.cuda.synchronize()
+        g = dict(row=row.cpu().numpy(), cols=cols.cpu().numpy(), fmaps=[sp.feature_map(k) for k in range(len(wl.species))],
+                 jedge={}, jself={})
+        for c in idx:
+            r0, r1 = int(g["row"][c]), int(g["row"][c + 1])
+            g["jedge"][int(c)] = je[r0:r1].cpu().double().numpy()
+            g["jself"][int(c)] = js[int(c)].cpu().double().numpy()
+        ed = row_errors(d.cpu().double().numpy()[idx], ref["desc"]).max()
+        ej = jacobian_errors(g, ref, st, wl.species, idx.tolist(), idx)
+        print(f"[outputs] {case} {dtype} out_rows {rows} (groups {groups}, rows kernel {used_rows}): "
+              f"desc {ed:.2e} jac {ej:.2e}", flush=True)
+        assert ed < TOL[dtype] and ej < TOL[dtype]
+        if rows == 0:
+            assert used_rows == 0
+        if first is None:
+            first = (d.clone(), je.clone(), js.clone())
+        else:
+            for x, y in zip((d, je, js), first):
+                assert torch.equal(x, y)
+        sp.close()
