@@ -1369,7 +1369,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
     for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
 
     // this thread's projection tasks: (lm, radial group) = (t % L, t / L), t = tid + BSC q
-    int lm_q[QT], l_q[QT], a_q[QT];
+    int lm_q[QT], l_q[QT], a_q[QT], goff[QT][AG];
     bool ok_q[QT];
 #pragma unroll
     for (int q = 0; q < QT; ++q) {
@@ -1381,6 +1381,8 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
         lm_q[q] = ok_q[q] ? lm : 0;
         l_q[q] = ok_q[q] ? l : 0;
         a_q[q] = ok_q[q] ? AG * ap : 0;
+#pragma unroll
+        for (int g = 0; g < AG; ++g) goff[q][g] = (a_q[q] + g < n ? g : 0) * WP;
     }
     int64_t ci = blockIdx.x;
     const int64_t stride = gridDim.x;
@@ -1459,14 +1461,17 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
 #pragma unroll
             for (int sr = 0; sr < SR; ++sr) {
                 const int lo = run[sr], hi = run[sr + 1];
+#pragma unroll 4
                 for (int e = lo; e < hi; ++e) {
 #pragma unroll
                     for (int q = 0; q < QT; ++q) {
-                        const double yv = ok_q[q] ? (double)Yl[lm_q[q] * WP + e] : 0.0;
+                        // every load unconditional (a guarded load becomes a branch that waits for it
+                        // alone): a thread with no task reads lm 0, a radial index past n_max reads
+                        // index a_q; neither sum is ever written
+                        const double yv = (double)Yl[lm_q[q] * WP + e];
                         const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
 #pragma unroll
-                        for (int g = 0; g < AG; ++g)
-                            acc[sr][q][g] += (a_q[q] + g < n ? (double)bp[g * WP] : 0.0) * yv;
+                        for (int g = 0; g < AG; ++g) acc[sr][q][g] += (double)bp[goff[q][g]] * yv;
                     }
                 }
             }
@@ -1575,7 +1580,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
     // and the gradient of its S_lm: gx = g0 Y'_0 + g1 Y'_1, gy = g2 Y'_2 + g3 Y'_3,
     // gz = g4 Y'_4, Y'_k = the degree l-1 harmonic gi[k] (coefficient 0 where
     // the identity has no term or the order is out of range)
-    int lm_q[QT], l_q[QT], a_q[QT], gi[QT][5];
+    int lm_q[QT], l_q[QT], a_q[QT], o1_q[QT], gi[QT][5];
     double gc[QT][5];
     bool ok_q[QT];
 #pragma unroll
@@ -1588,6 +1593,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
         lm_q[q] = ok_q[q] ? lm : 0;
         l_q[q] = ok_q[q] ? l : 0;
         a_q[q] = ok_q[q] ? 2 * ap : 0;
+        o1_q[q] = a_q[q] + 1 < n ? WP : 0;
         const int m = lm_q[q] - l_q[q] * l_q[q] - l_q[q], mm = m < 0 ? -m : m, lp = l_q[q] - 1;
         const int tg = l_q[q] * (l_q[q] + 1) / 2 + mm;
         const double cA = P.gcoef[4 * tg], cB = P.gcoef[4 * tg + 1], cC = P.gcoef[4 * tg + 2];
@@ -1717,13 +1723,16 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
                         const double dx = live * (gc[q][0] * t0 + gc[q][1] * t1);
                         const double dy = live * (gc[q][2] * t2 + gc[q][3] * t3);
                         const double dz = live * (gc[q][4] * t4);
+                        // unconditional loads (a guarded load becomes a branch that waits for
+                        // it alone): radial index a_q + 1 past n_max reads index a_q, a sum
+                        // that is never written
                         const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
                         const ST *hp = Hl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
 #pragma unroll
                         for (int a = 0; a < 2; ++a) {
-                            const bool in = a_q[q] + a < n;
-                            const double b = in ? (double)bp[a * WP] : 0.0;
-                            const double hs = in ? (double)hp[a * WP] * y : 0.0;
+                            const int o = a == 0 ? 0 : o1_q[q];
+                            const double b = (double)bp[o];
+                            const double hs = (double)hp[o] * y;
                             acc[sr][q][a][0] += b * y;
                             acc[sr][q][a][1] += hs * rx + b * dx;
                             acc[sr][q][a][2] += hs * ry + b * dy;
