@@ -404,6 +404,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
                    "edge_features": sp.n_edge_features},
         "kernel_ms": kern,
         "kernels": {"descriptor": desc_kernel, "jacobian_density": dens_kernel},
+        "plan": {k: sp.get_option(k) for k in ("jacobian_l_groups", "jacobian_density_tile", "jacobian_density_lds",
+                                                "jacobian_tile", "jacobian_lds", "output_kernel_rows", "output_lds")},
         "kernel_timing": "HIP events per segment, on the stream each kernel runs on, over a second pass of the "
                          "K steps; per-step sums",
         "step_alg_bytes": alg["step"],

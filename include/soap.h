@@ -173,7 +173,13 @@ int soap_set_option(soap_ctx *ctx, const char *key, int64_t value);
  *                               works in l-groups;
  *   "jacobian_l_groups"       : l-groups of the shared density kernel on the
  *                               Jacobian path (above 1, the output kernel
- *                               runs after it).
+ *                               runs after it);
+ *   "jacobian_density_tile", "jacobian_density_lds": edges per chunk and
+ *                               LDS bytes per workgroup of the density step
+ *                               of the Jacobian path;
+ *   "jacobian_tile", "jacobian_lds": edges per wave tile and LDS bytes per
+ *                               workgroup of the edge Jacobian kernel;
+ *   "output_lds"              : LDS bytes per workgroup of the output kernel.
  * Errors: SOAP_EINVAL (NULL argument, unknown key).
  */
 int soap_get_option(const soap_ctx *ctx, const char *key, int64_t *value);

@@ -292,7 +292,7 @@ int plan_launches(soap_ctx *c) {
         const int per_cu = density_blocks_per_cu(f64d, ar64, mode, P.rbf, hi, lds);
         c->dens_cfg[mode].blocks = std::max(1, ncu * per_cu / *G);
     }
-    c->out_ok = plan_outputs(P, c->dtype == SOAP_FP64, c->out_rows, &c->out_plan) == 0;
+    c->out_ok = plan_outputs(P, c->dtype == SOAP_FP64, st64, c->out_rows, &c->out_plan) == 0;
     // Jacobian kernel: W edges per wave tile.  The most resident waves per CU
     // first (latency hiding for its LDS-bound staging), then the widest tile.
     const bool f64 = c->dtype == SOAP_FP64;
@@ -668,6 +668,11 @@ int soap_get_option(const soap_ctx *c, const char *key, int64_t *value) {
                {"out_rows", c->out_rows ? 1 : 0},
                {"output_kernel_rows", c->out_plan.rows ? 1 : 0},
                {"jacobian_l_groups", c->groups[1]},
+               {"jacobian_density_tile", c->djac_cfg.W > 0 ? c->djac_cfg.W : c->dens_cfg[1].W},
+               {"jacobian_density_lds", (int64_t)(c->djac_cfg.W > 0 ? c->djac_cfg.lds : c->dens_cfg[1].lds)},
+               {"jacobian_tile", c->jac_cfg.W},
+               {"jacobian_lds", (int64_t)c->jac_cfg.lds},
+               {"output_lds", (int64_t)c->out_plan.lds},
                {"descriptor_kernel", c->desc_cfg.W > 0 ? 1 : 0},
                {"jacobian_density_kernel", c->djac_cfg.W > 0 ? 1 : 0}};
     for (const auto &t : tab)

@@ -771,8 +771,10 @@ __host__ __device__ __forceinline__ int chunks_below(int l) { // sum over l' < l
 // Coefficients of one l-range as a matrix view: entry (u, lm) at
 // C[u * ldu + (lm - lm0) * ldm], u = species * n + radial index; D holds
 // one Cartesian component of the center derivative in the same layout.
-struct CoefView {
-    const double *C, *D;
+// coefficients c (and one component of D) in LDS, entry (u, lm) at
+// u * ldu + lm * ldm, stored at precision T (read as float64)
+template <typename T = double> struct CoefView {
+    const T *C, *D;
     int ldu, ldm;
 };
 
@@ -814,8 +816,8 @@ __device__ __forceinline__ void lane_pair_index(const PairIndex &pq, int Sn, int
     }
 }
 
-template <typename OutT>
-__device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn, int lm0, int lg0, int lgc,
+template <typename OutT, typename CT = double>
+__device__ __forceinline__ void power_tiles(const CoefView<CT> cv, int comp, int Sn, int lm0, int lg0, int lgc,
                                             OutT *__restrict__ row, int ldq, int lbase, const PairIndex pq,
                                             int wave, int nw, int lane, const double *__restrict__ Kl) {
     const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
@@ -841,12 +843,12 @@ __device__ __forceinline__ void power_tiles(const CoefView cv, int comp, int Sn,
             const int m = 4 * ch + kk;
             const bool mok = m <= 2 * l;
             const int mo = (mok ? m : 0) * cv.ldm;
-            const double ca = cv.C[oa + mo], cb = cv.C[ob + mo];
+            const double ca = (double)cv.C[oa + mo], cb = (double)cv.C[ob + mo];
             const double xa = (mok && uok) ? ca : 0.0, xb = (mok && vok) ? cb : 0.0;
             if (comp < 0) {
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, xb, acc, 0, 0, 0);
             } else {
-                const double da = cv.D[oa + mo], db = cv.D[ob + mo];
+                const double da = (double)cv.D[oa + mo], db = (double)cv.D[ob + mo];
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64((mok && uok) ? da : 0.0, xb, acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, (mok && vok) ? db : 0.0, acc, 0, 0, 0);
             }
@@ -1219,7 +1221,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
         // power spectrum (descriptor path): per l, 16 x 16 matrix-core tiles
         // (ti <= tj) of u = (species, n) rows and v = (species, n') columns
         if (!JAC && desc)
-            power_tiles<OutT>(CoefView{cacc, nullptr, Lg, 1}, -1, Sn, lm0, lg0, lgc, desc + cw * P.F, lw, 0, pq,
+            power_tiles<OutT>(CoefView<double>{cacc, nullptr, Lg, 1}, -1, Sn, lm0, lg0, lgc, desc + cw * P.F, lw, 0, pq,
                               wave, NWD, lane, T.Kl);
         if (c_out)
             for (int it = tid; it < SnL; it += BSD) {
@@ -1493,7 +1495,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
         ci += stride;
         fetch();
         if (desc)
-            power_tiles<OutT>(CoefView{cb, nullptr, L, 1}, -1, Sn, 0, 0, lw, desc + cw * P.F, lw, 0,
+            power_tiles<OutT>(CoefView<double>{cb, nullptr, L, 1}, -1, Sn, 0, 0, lw, desc + cw * P.F, lw, 0,
                               PairIndex{S, n, 1.0f / (float)n}, wave, NWC, lane, Kl);
         if (c_out)
             for (int k = tid; k < SnL; k += BSC) store_out(c_out + cw * SnL + k, cb[k]);
@@ -1858,15 +1860,18 @@ __global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const doub
 // which goes out in contiguous lines (an l-group split writes part of every
 // line of a row per group).
 // ---------------------------------------------------------------------------
-constexpr int NWO = 16, BSO2 = 64 * NWO;
-constexpr int OUT_PF = 12; // prefetched doubles per thread: one slab of at most OUT_PF * BSO2
+constexpr int NWO = 8, BSO2 = 64 * NWO;
+constexpr int OUT_PF = 24; // prefetched doubles per thread: one slab of at most OUT_PF * BSO2
 
-__host__ __device__ __forceinline__ size_t outputs_rows_doubles(const Params &P, int out_bytes) {
+// sb: bytes per staged coefficient (ST)
+__host__ __device__ __forceinline__ size_t outputs_rows_doubles(const Params &P, int out_bytes, int sb) {
     const size_t slab = (size_t)P.L * P.S * P.n;
-    return 2 * even(slab) + even(((size_t)P.F * out_bytes + 7) / 8);
+    return 2 * even((slab * sb + 7) / 8) + even(((size_t)P.F * out_bytes + 7) / 8);
 }
 
-template <typename OutT>
+// ST: precision of the staged c and D (float64, or float32 in the mixed mode;
+// the products and sums stay float64 on the matrix cores)
+template <typename OutT, typename ST>
 __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *__restrict__ scratch,
                                                        OutT *__restrict__ desc, OutT *__restrict__ jself) {
     extern __shared__ __align__(16) double smem[];
@@ -1874,9 +1879,9 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *_
     const int64_t ci = blockIdx.x;
     const int S = P.S, n = P.n, Sn = S * n, lw = P.lmax + 1, F = P.F, tid = threadIdx.x;
     const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int slab = P.L * Sn, sstr = (int)even((size_t)slab);
+    const int slab = P.L * Sn, sstr = (int)even(((size_t)slab * sizeof(ST) + 7) / 8);
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
-    double *Xc = smem, *Xd = smem + sstr;
+    ST *Xc = (ST *)smem, *Xd = (ST *)(smem + sstr);
     OutT *row = (OutT *)(smem + 2 * sstr);
     const double *src = scratch + ci * 4 * (size_t)slab; // [c, Dx, Dy, Dz][lm][species n]
     // c and D_x, eight loads in flight per thread
@@ -1890,7 +1895,7 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *_
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int k = k0 + u * BSO2 + tid;
-            if (k < 2 * slab) (k < slab ? Xc[k] : Xd[k - slab]) = v[u];
+            if (k < 2 * slab) (k < slab ? Xc[k] : Xd[k - slab]) = (ST)v[u];
         }
     }
     lds_barrier();
@@ -1905,7 +1910,7 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *_
                 pf[u] = nx[k < slab ? k : 0];
             }
         }
-        power_tiles<OutT>(CoefView{Xc, Xd, 1, Sn}, p - 1, Sn, 0, 0, lw, row, lw, 0, pq, wave, NWO, lane, Kl);
+        power_tiles<OutT, ST>(CoefView<ST>{Xc, Xd, 1, Sn}, p - 1, Sn, 0, 0, lw, row, lw, 0, pq, wave, NWO, lane, Kl);
         lds_barrier(); // the row is complete; D of this pass is read
         OutT *dst = p == 0 ? desc + ci * F : jself + (ci * 3 + (p - 1)) * F;
         for (int f = tid; f < F; f += BSO2) dst[f] = row[f];
@@ -1913,7 +1918,7 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *_
 #pragma unroll
             for (int u = 0; u < OUT_PF; ++u) {
                 const int k = u * BSO2 + tid;
-                if (k < slab) Xd[k] = pf[u];
+                if (k < slab) Xd[k] = (ST)pf[u];
             }
         }
         lds_barrier(); // the row is read and the next D is in place before the next pass
@@ -1957,7 +1962,7 @@ __global__ __launch_bounds__(256) void k_power_single(Params P, const double *__
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     copy_to_lds<256, 4>(smem, c, Sn * L, tid);
     lds_barrier();
-    power_tiles<OutT>(CoefView{smem, nullptr, L, 1}, -1, Sn, 0, 0, P.lmax + 1, out, P.lmax + 1, 0,
+    power_tiles<OutT>(CoefView<double>{smem, nullptr, L, 1}, -1, Sn, 0, 0, P.lmax + 1, out, P.lmax + 1, 0,
                       PairIndex{P.S, P.n, 1.0f / (float)P.n}, wave, 4,
                       lane, Kl);
 }

@@ -191,12 +191,13 @@ hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool 
 // LDS), else l-groups of the output kernel, each sized to its LDS budget
 struct OutPlan {
     bool rows;
+    bool st64; // whole rows: c and D staged in float64 (else float32, the mixed mode)
     int n_groups;
     int lgrp[MAX_GROUPS + 1];
     size_t lds;
 };
 // allow_rows = false keeps the l-group kernel; 0, or -1 if one l does not fit
-int plan_outputs(const Params &P, bool f64, bool allow_rows, OutPlan *O);
+int plan_outputs(const Params &P, bool f64, bool st64, bool allow_rows, OutPlan *O);
 hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
                           void *jself, hipStream_t st);
 // one-wave-per-center descriptor kernel (GTO): the shape of its accumulators

@@ -136,11 +136,12 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool at64) {
 // Fewest contiguous l-groups whose LDS (c and one component of D for the
 // group, plus the group's part of an output row) stays within 80 KB, two
 // workgroups per CU; a single l above the budget may use up to the hard limit.
-int plan_outputs(const Params &P, bool f64, bool allow_rows, OutPlan *O) {
+int plan_outputs(const Params &P, bool f64, bool st64, bool allow_rows, OutPlan *O) {
     const int lw = P.lmax + 1, ob = f64 ? 8 : 4;
     const size_t hard = 159 * 1024;
     // whole rows (k_outputs_rows) where c, one component of D and a row fit
-    const size_t rows_lds = 8 * outputs_rows_doubles(P, ob);
+    const size_t rows_lds = 8 * outputs_rows_doubles(P, ob, st64 ? 8 : 4);
+    O->st64 = st64;
     O->rows = allow_rows && rows_lds <= hard && (size_t)P.L * P.S * P.n <= (size_t)OUT_PF * BSO2;
     if (O->rows) {
         O->n_groups = 1;
@@ -172,10 +173,13 @@ hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f6
     if (nc <= 0) return hipSuccess;
     if (O.rows) {
         if (f64)
-            hipLaunchKernelGGL(k_outputs_rows<double>, dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+            hipLaunchKernelGGL((k_outputs_rows<double, double>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
                                (double *)desc, (double *)jself);
+        else if (O.st64)
+            hipLaunchKernelGGL((k_outputs_rows<float, double>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+                               (float *)desc, (float *)jself);
         else
-            hipLaunchKernelGGL(k_outputs_rows<float>, dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+            hipLaunchKernelGGL((k_outputs_rows<float, float>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
                                (float *)desc, (float *)jself);
         return hipGetLastError();
     }
@@ -235,8 +239,9 @@ hipError_t set_lds_limits() {
     for (int f64 = 0; f64 < 2; ++f64)
         for (int na : {4, 8, 12, 16}) SOAP_SET(radial_kernel(f64 != 0, na));
     SOAP_SET(k_outputs<float>);
-    SOAP_SET(k_outputs_rows<float>);
-    SOAP_SET(k_outputs_rows<double>);
+    SOAP_SET((k_outputs_rows<float, float>));
+    SOAP_SET((k_outputs_rows<float, double>));
+    SOAP_SET((k_outputs_rows<double, double>));
     SOAP_SET(k_outputs<double>);
     SOAP_SET(k_power_single<float>);
     SOAP_SET(k_power_single<double>);

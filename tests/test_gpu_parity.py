@@ -272,8 +272,9 @@ def test_jacobian_density_kernel_chunk_widths(dtype, case):
 def test_output_kernel_rows_and_groups(dtype, case):
     """The output kernel of the Jacobian path (power spectrum and center block
     from the coefficient scratch) writing whole rows and in l-groups:
-    descriptor and every block of every center against the oracle, and the
-    same bits both ways."""
+    descriptor and every block of every center against the oracle, and in
+    float64 the same bits both ways (the mixed mode stages the whole-row
+    kernel's coefficients in float32, the l-group kernel's in float64)."""
     import torch
     from paper_2609_05709_amd.soap import Soap
     if case.startswith("chno"):
@@ -312,7 +313,7 @@ def test_output_kernel_rows_and_groups(dtype, case):
             assert used_rows == 0
         if first is None:
             first = (d.clone(), je.clone(), js.clone())
-        else:
+        elif dtype == "float64":
             for x, y in zip((d, je, js), first):
                 assert torch.equal(x, y)
         sp.close()
