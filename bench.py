@@ -356,7 +356,7 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
     alg = algorithmic(wl, nc, E, sp.n_features, sp.n_edge_features, out_bytes, jac)
     # the kernels the library's plan chose for this basis
     desc_kernel = "k_desc" if sp.get_option("descriptor_kernel") else "k_density"
-    dens_kernel = "k_djac" if sp.get_option("jacobian_density_kernel") else "k_density"
+    dens_kernel = ("k_density", "k_djac", "k_djs")[int(sp.get_option("jacobian_density_kernel"))]
     # per step (a pipelined step launches its kernels once per center chunk;
     # the chunks' Jacobian launches then overlap the density launches)
     kern = {"neighbors": seg_ms[0] / steps, "density": seg_ms[1] / steps, "jacobian": seg_ms[2] / steps,

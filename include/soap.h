@@ -143,6 +143,14 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  *              0 = automatic (default), -1 = the shared density kernel and
  *              the output kernel, 32 / 64 = the kernel that gives each
  *              center a workgroup, with at most that many edges per chunk;
+ *   "djs_tile" : kernel choice of the density step of the Jacobian path for
+ *              the GTO bases outside "djac_tile"'s kernel and the polynomial
+ *              quadrature bases (a tuning knob, results identical up to
+ *              rounding order): 0 = automatic (default), -1 = the shared
+ *              density kernel, 16 / 32 / 64 = the kernel that gives each
+ *              center a workgroup and streams its coefficients to the
+ *              scratch, with at most that many edges per chunk (then the
+ *              output kernel writes the descriptor and center blocks);
  *   "out_rows" : 1 (default) = the output kernel of the Jacobian path
  *              writes whole rows where c and one component of D fit on
  *              chip, 0 = always in l-groups (a tuning knob, results
@@ -164,12 +172,15 @@ int soap_set_option(soap_ctx *ctx, const char *key, int64_t value);
  *   "descriptor_kernel"       : 1 if soap_compute / soap_coefficients run the
  *                               descriptor kernel that gives each center a
  *                               workgroup, 0 if the shared density kernel;
- *   "jacobian_density_kernel" : 1 if the density step of soap_derivatives runs
- *                               the kernel that gives each center a workgroup,
- *                               0 if the shared density kernel;
+ *   "jacobian_density_kernel" : the density step of soap_derivatives: 1 the
+ *                               kernel that gives each center a workgroup and
+ *                               writes its outputs ("djac_tile"), 2 the one
+ *                               that streams the coefficients to the scratch
+ *                               ("djs_tile"), 0 the shared density kernel;
  *   "output_kernel_rows"      : 1 if the output kernel of the Jacobian path
  *                               (run when the shared density kernel splits
- *                               l into groups) writes whole rows, 0 if it
+ *                               l into groups, and after the streaming
+ *                               density kernel) writes whole rows, 0 if it
  *                               works in l-groups;
  *   "jacobian_l_groups"       : l-groups of the shared density kernel on the
  *                               Jacobian path (above 1, the output kernel

@@ -26,7 +26,7 @@ HIP_FLAGS = [
 ]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=gnu++17", "-fext-numeric-literals", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
-HIP_SOURCES = ["neighbors.hip", "soap_kernels.hip"]
+HIP_SOURCES = ["neighbors.hip", "soap_kernels.hip", "density_streamed.hip"]
 HIP_HOST_SOURCES = ["api.cpp"]
 HOST_SOURCES = ["basis.cpp"]
 

@@ -122,6 +122,8 @@ struct soap_ctx {
     DescLaunch desc_cfg{};
     DjacLaunch djac_cfg{};
     int djac_tile = 0; // option "djac_tile": 0 auto (default), -1 never k_djac, else the widest chunk
+    DjsLaunch djs_cfg{};
+    int djs_tile = 0; // option "djs_tile": 0 auto (default), -1 never k_djs, else the widest chunk
     // pipelined derivatives: the density kernel of center chunk k + 1 on the
     // caller's stream beside the Jacobian kernel of chunk k on a second one
     int pipe_chunks = 1;         // option "pipeline": chunks per call (1 = one stream)
@@ -336,6 +338,24 @@ int plan_launches(soap_ctx *c) {
             const int b = djac_blocks_per_cu(f64, ar64, qt, na2, sr, lds);
             if (b >= (c->djac_tile > 0 ? 1 : 2)) {
                 c->djac_cfg = DjacLaunch{W, qt, na2, sr, lds, ncu * b};
+                break;
+            }
+        }
+    }
+    // density step of the Jacobian path for the other GTO and polynomial
+    // quadrature bases: coefficients streamed to the scratch, outputs by the
+    // output kernel.  The widest chunk of edges that keeps at least two
+    // workgroups resident per CU.
+    c->djs_cfg = DjsLaunch{};
+    int qs = 0, nas = 0;
+    if (c->djac_cfg.W == 0 && c->djs_tile >= 0 && c->out_ok && djs_shape(P, &qs, &nas)) {
+        for (int W : {64, 32, 16}) {
+            if (c->djs_tile > 0 && W > c->djs_tile) continue;
+            const size_t lds = djs_lds_bytes(P, W, st64);
+            if (lds > LDS_HARD_LIMIT) continue;
+            const int b = djs_blocks_per_cu(f64d, ar64, P.rbf, qs, nas, lds);
+            if (b >= (c->djs_tile > 0 ? 1 : 2)) {
+                c->djs_cfg = DjsLaunch{W, qs, nas, lds, ncu * b};
                 break;
             }
         }
@@ -627,6 +647,12 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         c->djac_tile = (int)value;
         return plan_launches(c);
     }
+    if (!std::strcmp(key, "djs_tile")) {
+        if (value != 0 && value != -1 && value != 16 && value != 32 && value != 64)
+            return fail(c, SOAP_EINVAL, "djs_tile must be 0, -1, 16, 32 or 64");
+        c->djs_tile = (int)value;
+        return plan_launches(c);
+    }
     if (!std::strcmp(key, "desc_tile")) {
         if (value != 0 && value != -1 && value != 16 && value != 32 && value != 64)
             return fail(c, SOAP_EINVAL, "desc_tile must be 0, -1, 16, 32 or 64");
@@ -663,18 +689,23 @@ int soap_get_option(const soap_ctx *c, const char *key, int64_t *value) {
                {"timing", c->timing ? 1 : 0},
                {"desc_tile", c->desc_tile},
                {"djac_tile", c->djac_tile},
+               {"djs_tile", c->djs_tile},
                {"pipeline", c->pipe_chunks},
                {"pipeline_density_wg", c->pipe_density_wg},
                {"out_rows", c->out_rows ? 1 : 0},
                {"output_kernel_rows", c->out_plan.rows ? 1 : 0},
                {"jacobian_l_groups", c->groups[1]},
-               {"jacobian_density_tile", c->djac_cfg.W > 0 ? c->djac_cfg.W : c->dens_cfg[1].W},
-               {"jacobian_density_lds", (int64_t)(c->djac_cfg.W > 0 ? c->djac_cfg.lds : c->dens_cfg[1].lds)},
+               {"jacobian_density_tile",
+                c->djac_cfg.W > 0 ? c->djac_cfg.W : (c->djs_cfg.W > 0 ? c->djs_cfg.W : c->dens_cfg[1].W)},
+               {"jacobian_density_lds", (int64_t)(c->djac_cfg.W > 0 ? c->djac_cfg.lds
+                                                                    : (c->djs_cfg.W > 0 ? c->djs_cfg.lds
+                                                                                        : c->dens_cfg[1].lds))},
                {"jacobian_tile", c->jac_cfg.W},
                {"jacobian_lds", (int64_t)c->jac_cfg.lds},
                {"output_lds", (int64_t)c->out_plan.lds},
                {"descriptor_kernel", c->desc_cfg.W > 0 ? 1 : 0},
-               {"jacobian_density_kernel", c->djac_cfg.W > 0 ? 1 : 0}};
+               // 0 k_density, 1 k_djac, 2 k_djs (then the output kernel)
+               {"jacobian_density_kernel", c->djac_cfg.W > 0 ? 1 : (c->djs_cfg.W > 0 ? 2 : 0)}};
     for (const auto &t : tab)
         if (!std::strcmp(key, t.k)) {
             *value = t.v;
@@ -943,6 +974,7 @@ int soap_get_neighbors(soap_ctx *c, int64_t *row_ptr_dev, int32_t *cols_dev, voi
 // l into groups; the one-workgroup-per-center kernel needs neither split)
 static bool jacobian_path_ok(const soap_ctx *c, int mode) {
     if (mode == 1 && c->djac_cfg.W > 0) return c->jac_ok;
+    if (mode == 1 && c->djs_cfg.W > 0) return c->jac_ok && c->out_ok;
     return c->dens_ok[mode] && (mode != 1 || (c->jac_ok && (c->groups[1] == 1 || c->out_ok)));
 }
 
@@ -1012,6 +1044,21 @@ static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void
         hipError_t e = launch_djac(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, dj, desc, jself,
                                    scratch, to_stream(stream));
         if (e != hipSuccess) return hip_fail(c, e, "density kernel");
+        timer.done();
+        return SOAP_OK;
+    }
+    if (mode == 1 && c->djs_cfg.W > 0) { // one workgroup per center, then the output kernel
+        DjsLaunch dj = c->djs_cfg;
+        if (wg_per_cu > 0) {
+            int ncu = 256;
+            (void)hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c->device);
+            dj.blocks = std::max(1, std::min(dj.blocks, ncu * wg_per_cu));
+        }
+        hipError_t e = launch_djs(P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, dj, scratch,
+                                  to_stream(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "density kernel");
+        e = launch_outputs(P, c->out_plan, count, c->built_f64, scratch, desc, jself, to_stream(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "output kernel");
         timer.done();
         return SOAP_OK;
     }

@@ -1774,6 +1774,323 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
 }
 
 // ---------------------------------------------------------------------------
+// k_djs: the density step of the Jacobian path with the coefficients
+// streamed to scratch.  The layout of k_djac (one center per workgroup of NWC
+// waves, chunks of W edges of the row, staging lane = edge, every
+// accumulated entry owned by one thread), for the bases whose coefficient
+// block c, D does not fit on chip beside the staging (the polynomial basis of
+// the multi-species workloads) or whose projection exceeds k_djac's two tasks
+// per thread.  A thread's sums hold one species at a time: rows are sorted by
+// species, so when the row reaches a new species the sums of the previous one
+// go straight to the scratch [c, Dx, Dy, Dz][lm][species n] (each entry
+// written once, by its owner; a species without neighbours gets zeros, and c
+// of the center's own species its on-site term).  The output kernel then
+// writes the power spectrum and the center block from the scratch, and
+// k_jacobian reads c from it.
+//   staging: the chunk's edge vectors and species (wave 0); the radial
+//     factors B_nl, Bh_nl: GTO (RBF 0) from the exponentials as in k_djac,
+//     one l per task over the waves; polynomial quadrature (RBF 1) copied
+//     from the factors k_radial left for the call's edges, all threads, in
+//     the buffer's order; the solid harmonics, their columns m spread over
+//     the waves (sh_cols_lane);
+//   projection: thread = (radial pair, lm), per edge
+//       c_{a lm} += B_al S_lm,  D_{a lm} += Bh_al r S_lm + B_al grad S_lm,
+//     each sum in row order (deterministic with no ordering protocol).
+// Task t is radial pair t % np of harmonic lm = t / np, so that neighbouring
+// threads own neighbouring entries of a scratch row.
+// ---------------------------------------------------------------------------
+// the real solid harmonics of columns m = m0, m0 + ms, ... (lane = edge; the
+// column recurrence of sh_all_lane, (x + i y)^m advanced by (x + i y)^ms)
+template <typename YT>
+__device__ __forceinline__ void sh_cols_lane(double x, double y, double z, const double *__restrict__ Nt, int ldN,
+                                             int lw, YT *__restrict__ Y, int ls, int m0, int ms) {
+    const double r2 = x * x + y * y + z * z;
+    double c = 1.0, s = 0.0, cs = 1.0, ss = 0.0;
+    for (int k = 0; k < m0; ++k) {
+        const double cn = x * c - y * s;
+        s = x * s + y * c;
+        c = cn;
+    }
+    for (int k = 0; k < ms; ++k) {
+        const double cn = x * cs - y * ss;
+        ss = x * ss + y * cs;
+        cs = cn;
+    }
+    for (int m = m0; m < lw; m += ms) {
+        double R1 = 0.0, R = 1.0; // R_{l-1}, R_l
+        for (int l = m; l < lw; ++l) {
+            if (l > m) {
+                const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
+                const double Rn = a * z * R - b * r2 * R1;
+                R1 = R;
+                R = Rn;
+            }
+            const double v = Nt[l * ldN + m] * R;
+            const int o = l * l + l;
+            if (m == 0) {
+                Y[o * ls] = (YT)v;
+            } else {
+                Y[(o + m) * ls] = (YT)(v * c);
+                Y[(o - m) * ls] = (YT)(v * s);
+            }
+        }
+        const double cn = c * cs - s * ss;
+        s = c * ss + s * cs;
+        c = cn;
+    }
+}
+
+// LDS doubles of k_djs: tables (Nt, on-site terms; GTO: a', betaC), then the
+// staging (harmonics [lm][W+1], B and Bh [l][n][W+1] with odd row lengths,
+// edge vectors [W][4], species [W], species run bounds)
+__host__ __device__ __forceinline__ size_t djs_lds_doubles(const Params &P, int W, int sb) {
+    const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n, L = (size_t)P.L;
+    const size_t tables = even(ldN * ldN) + even(n) + (P.rbf == 0 ? even(lw * n) + even(lw * n * n) : 0);
+    return tables + even((L * (W + 1) * sb + 7) / 8) + 2 * even((lw * desc_ldl((int)n, W) * sb + 7) / 8) +
+           4 * (size_t)W + even(((size_t)W + 1) / 2) + 16;
+}
+// (radial pair, lm) tasks per thread
+__host__ __device__ __forceinline__ int djs_tasks(const Params &P) {
+    return (P.L * ((P.n + 1) / 2) + BSC - 1) / BSC;
+}
+
+template <typename PosT, typename ST, int QT, int NA, int RBF>
+__global__ __launch_bounds__(BSC) void k_djs(Params P, Rows R, const PosT *__restrict__ pos, int W,
+                                             double *__restrict__ c_scratch) {
+    extern __shared__ __align__(16) double smem[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int S = P.S, n = P.n, lmax = P.lmax, lw = lmax + 1, L = P.L, ldN = lmax + 2, Sn = S * n;
+    const int np = (n + 1) / 2;
+    constexpr int SB = sizeof(ST);
+    Carver cv{smem};
+    double *Nt = cv.take((size_t)ldN * ldN);
+    double *c0 = cv.take((size_t)n);
+    double *apr = RBF == 0 ? cv.take((size_t)lw * n) : nullptr;
+    double *bcf = RBF == 0 ? cv.take((size_t)lw * n * n) : nullptr;
+    const int WP = W + 1, ldl = desc_ldl(n, W);
+    ST *Yl = (ST *)cv.take(((size_t)L * WP * SB + 7) / 8);  // [lm][W + 1]
+    ST *Bl = (ST *)cv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1]
+    ST *Hl = (ST *)cv.take(((size_t)lw * ldl * SB + 7) / 8); // [l][n][W + 1]
+    double *geo = cv.take(4 * (size_t)W);                    // [W][x, y, z, r]
+    int *run = (int *)cv.take(16);                           // species run bounds of the chunk
+    for (int k = tid; k < ldN * ldN; k += BSC) Nt[k] = P.Nt[k];
+    for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
+    if constexpr (RBF == 0) {
+        for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
+        for (int k = tid; k < lw * n * n; k += BSC) bcf[k] = P.betaC[k];
+    }
+    lds_barrier(); // the tables (a center without neighbours reads the on-site terms before any chunk)
+
+    // this thread's tasks: (radial pair, lm) = (t % np, t / np), t = tid + BSC q,
+    // and the gradient of its S_lm (as in k_djac)
+    int lm_q[QT], l_q[QT], a_q[QT], o1_q[QT], gi[QT][5];
+    double gc[QT][5];
+    bool ok_q[QT];
+#pragma unroll
+    for (int q = 0; q < QT; ++q) {
+        const int t = tid + BSC * q, lm = t / np, ap = t - lm * np;
+        int l = (int)sqrtf((float)lm);
+        while (l * l > lm) --l;
+        while ((l + 1) * (l + 1) <= lm) ++l;
+        ok_q[q] = lm < L;
+        lm_q[q] = ok_q[q] ? lm : 0;
+        l_q[q] = ok_q[q] ? l : 0;
+        a_q[q] = ok_q[q] ? 2 * ap : 0;
+        o1_q[q] = a_q[q] + 1 < n ? WP : 0;
+        const int m = lm_q[q] - l_q[q] * l_q[q] - l_q[q], mm = m < 0 ? -m : m, lp = l_q[q] - 1;
+        const int tg = l_q[q] * (l_q[q] + 1) / 2 + mm;
+        const double cA = P.gcoef[4 * tg], cB = P.gcoef[4 * tg + 1], cC = P.gcoef[4 * tg + 2];
+        int k[5];
+        double c[5];
+        if (m == 0) {
+            k[0] = 1; c[0] = -cA; k[1] = 0; c[1] = 0.0;
+            k[2] = -1; c[2] = -cA; k[3] = 0; c[3] = 0.0;
+            k[4] = 0; c[4] = cC;
+        } else if (m > 0) {
+            k[0] = m + 1; c[0] = -cA; k[1] = m - 1; c[1] = cB;
+            k[2] = -(m + 1); c[2] = -cA; k[3] = -(m - 1); c[3] = m > 1 ? -cB : 0.0;
+            k[4] = m; c[4] = cC;
+        } else {
+            k[0] = -(mm + 1); c[0] = -cA; k[1] = -(mm - 1); c[1] = mm > 1 ? cB : 0.0;
+            k[2] = mm + 1; c[2] = cA; k[3] = mm - 1; c[3] = cB;
+            k[4] = -mm; c[4] = cC;
+        }
+#pragma unroll
+        for (int j = 0; j < 5; ++j) {
+            const bool in = ok_q[q] && lp >= 0 && k[j] >= -lp && k[j] <= lp;
+            gi[q][j] = in ? lp * lp + lp + k[j] : 0;
+            gc[q][j] = in ? c[j] : 0.0;
+        }
+    }
+    const int per = n * lw;
+    const float inv_per = 1.0f / (float)per, inv_lw = 1.0f / (float)lw;
+    int64_t ci = blockIdx.x;
+    const int64_t stride = gridDim.x;
+    double gx = 0.0, gy = 0.0, gz = 0.0;
+    int gs = 0;
+    int64_t e0 = 0, e1 = 0;
+    double3 pi = make_double3(0.0, 0.0, 0.0);
+    int spec_i = 0;
+    auto gather = [&](int64_t cs, int nb) {
+        if (lane < nb) {
+            const int64_t j = R.cols[cs + lane];
+            gx = (double)pos[3 * j] - pi.x;
+            gy = (double)pos[3 * j + 1] - pi.y;
+            gz = (double)pos[3 * j + 2] - pi.z;
+            gs = R.spec[j];
+        }
+    };
+    auto fetch = [&]() {
+        if (ci >= R.nc) return;
+        const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
+        pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);
+        spec_i = R.spec[i];
+        e0 = R.row_ptr[ci];
+        e1 = R.row_ptr[ci + 1];
+        gather(e0, (int)((e1 - e0) < W ? (e1 - e0) : W));
+    };
+    fetch();
+    while (ci < R.nc) {
+        double acc[QT][2][4];
+        const int64_t cw = ci;
+        const int spec_c = spec_i;
+        double *sc = c_scratch + cw * 4 * (size_t)L * Sn; // [c, Dx, Dy, Dz][lm][species n]
+        // the sums of species s (or zeros) to the scratch; c of the center's
+        // own species gets the on-site term
+        auto flush = [&](int s, bool sums) {
+#pragma unroll
+            for (int q = 0; q < QT; ++q)
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    if (ok_q[q] && a_q[q] + a < n) {
+                        double *o = sc + (size_t)lm_q[q] * Sn + s * n + a_q[q] + a;
+#pragma unroll
+                        for (int d = 0; d < 4; ++d) {
+                            double v = sums ? acc[q][a][d] : 0.0;
+                            if (d == 0 && s == spec_c && lm_q[q] == 0) v += c0[a_q[q] + a];
+                            o[(size_t)d * L * Sn] = v;
+                        }
+                    }
+        };
+#pragma unroll
+        for (int q = 0; q < QT; ++q)
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int d = 0; d < 4; ++d) acc[q][a][d] = 0.0;
+        int cur = 0; // the species the sums hold
+        for (int64_t cs = e0; cs < e1; cs += W) {
+            const int nb = (int)((e1 - cs) < W ? (e1 - cs) : W);
+            if (cs != e0) gather(cs, nb);
+            lds_barrier(); // the tables; the previous chunk's (or center's) readers of the staging region
+            // ---- staging, lane = edge ----
+            if (wave == 0) {
+                if (lane < nb) {
+                    geo[4 * lane] = gx;
+                    geo[4 * lane + 1] = gy;
+                    geo[4 * lane + 2] = gz;
+                    geo[4 * lane + 3] = sqrt(gx * gx + gy * gy + gz * gz);
+                }
+                // run bounds: the chunk's edges of species below s (rows are sorted by species)
+                for (int s = 0; s <= S; ++s) {
+                    const int cnt = __popcll(__ballot(lane < nb && gs < s));
+                    if (lane == 0) run[s] = cnt;
+                }
+            }
+            if constexpr (RBF == 1) {
+                // the chunk's radial factors, [edge][n][l] in the buffer, contiguous over the chunk
+                const double2 *rad = P.rad + (cs - P.rad_e0) * (size_t)per;
+                for (int k = tid; k < nb * per; k += BSC) {
+                    const int e = qdiv(k, inv_per), t = k - e * per, a = qdiv(t, inv_lw), l = t - a * lw;
+                    const double2 v = rad[k];
+                    Bl[l * ldl + a * WP + e] = (ST)v.x;
+                    Hl[l * ldl + a * WP + e] = (ST)v.y;
+                }
+            }
+            if (lane < nb) {
+                if constexpr (RBF == 0) {
+                    const double r2 = gx * gx + gy * gy + gz * gz;
+                    for (int l = wave; l < lw; l += NWC) {
+                        // e_k and -2 a'_k e_k: Bh = sum_k betaC (-2 a'_k) e_k
+                        double ex[NA], ea[NA];
+#pragma unroll
+                        for (int k = 0; k < NA; ++k) {
+                            const double ap = apr[l * n + (k < n ? k : n - 1)];
+                            ex[k] = k < n ? exp(-ap * r2) : 0.0;
+                            ea[k] = -2.0 * ap * ex[k];
+                        }
+                        ST *bo = Bl + (size_t)l * ldl + lane, *ho = Hl + (size_t)l * ldl + lane;
+                        const double *bc = bcf + (size_t)l * n * n;
+                        for (int a = 0; a < n; ++a) {
+                            double b = 0.0, h = 0.0;
+#pragma unroll
+                            for (int k = 0; k < NA; ++k) {
+                                const double cf = bc[a * n + (k < n ? k : n - 1)];
+                                b += cf * ex[k];
+                                h += cf * ea[k];
+                            }
+                            bo[a * WP] = (ST)b;
+                            ho[a * WP] = (ST)h;
+                        }
+                    }
+                }
+                sh_cols_lane(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP, wave, NWC);
+            }
+            lds_barrier();
+            // ---- projection, thread = (radial pair, lm), species run by run ----
+            for (int s = 0; s < S; ++s) {
+                const int lo = run[s], hi = run[s + 1];
+                if (lo == hi) continue; // uniform
+                if (s != cur) {
+                    flush(cur, true);
+                    for (int z = cur + 1; z < s; ++z) flush(z, false);
+                    cur = s;
+#pragma unroll
+                    for (int q = 0; q < QT; ++q)
+#pragma unroll
+                        for (int a = 0; a < 2; ++a)
+#pragma unroll
+                            for (int d = 0; d < 4; ++d) acc[q][a][d] = 0.0;
+                }
+                for (int e = lo; e < hi; ++e) {
+                    const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
+                    const double live = geo[4 * e + 3] != 0.0 ? 1.0 : 0.0;
+#pragma unroll
+                    for (int q = 0; q < QT; ++q) {
+                        const double y = (double)Yl[lm_q[q] * WP + e];
+                        const double t0 = (double)Yl[gi[q][0] * WP + e], t1 = (double)Yl[gi[q][1] * WP + e];
+                        const double t2 = (double)Yl[gi[q][2] * WP + e], t3 = (double)Yl[gi[q][3] * WP + e];
+                        const double t4 = (double)Yl[gi[q][4] * WP + e];
+                        const double dx = live * (gc[q][0] * t0 + gc[q][1] * t1);
+                        const double dy = live * (gc[q][2] * t2 + gc[q][3] * t3);
+                        const double dz = live * (gc[q][4] * t4);
+                        // unconditional loads: radial index a_q + 1 past n_max reads
+                        // index a_q, a sum that is never written
+                        const ST *bp = Bl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+                        const ST *hp = Hl + (size_t)l_q[q] * ldl + a_q[q] * WP + e;
+#pragma unroll
+                        for (int a = 0; a < 2; ++a) {
+                            const int o = a == 0 ? 0 : o1_q[q];
+                            const double b = (double)bp[o];
+                            const double hs = (double)hp[o] * y;
+                            acc[q][a][0] += b * y;
+                            acc[q][a][1] += hs * rx + b * dx;
+                            acc[q][a][2] += hs * ry + b * dy;
+                            acc[q][a][3] += hs * rz + b * dz;
+                        }
+                    }
+                }
+            }
+        }
+        ci += stride;
+        fetch(); // the next center's first chunk before this center's last stores
+        flush(cur, true);
+        for (int z = cur + 1; z < S; ++z) flush(z, false);
+    }
+}
+
+// ---------------------------------------------------------------------------
 // k_outputs: power spectrum and center block for the Jacobian path, from the
 // coefficients c and D that k_density left in scratch
 // ([center][c, Dx, Dy, Dz][lm][species n]).  One workgroup per center.  Per

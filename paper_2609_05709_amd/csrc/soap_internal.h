@@ -154,6 +154,12 @@ struct DjacLaunch {
     size_t lds;
     int blocks;     // resident workgroups (persistent launch)
 };
+struct DjsLaunch {
+    int W;          // edges per chunk (0: not used)
+    int qt, na;     // tasks per thread, radial size (GTO)
+    size_t lds;
+    int blocks;     // resident workgroups (persistent launch)
+};
 struct JacLaunch {
     int W;          // edges per wave tile (at most jacobian_max_w())
     size_t lds;
@@ -223,6 +229,14 @@ hipError_t launch_djac(const Params &P, const Rows &R, const void *pos, bool f64
                        void *desc, void *jself, double *c_scratch, hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const JacLaunch &cfg,
                            const double *c_scratch, void *jedge, hipStream_t st);
+// density step of the Jacobian path with the coefficients streamed to the
+// scratch (k_djs, density_streamed.hip): GTO and polynomial quadrature bases
+// of at most four (radial pair, lm) tasks per thread
+bool djs_shape(const Params &P, int *qt, int *na);
+size_t djs_lds_bytes(const Params &P, int W, bool st64);
+int djs_blocks_per_cu(bool f64, bool ar64, int rbf, int qt, int na, size_t lds);
+hipError_t launch_djs(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjsLaunch &cfg,
+                      double *c_scratch, hipStream_t st);
 // column means of a row-major (rows x cols) array of the output type, in
 // float64: part[AVG_CHUNKS][cols] partial sums, then mean[cols] (float64)
 // and, if out is not NULL, out[cols] at the output type

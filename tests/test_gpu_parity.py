@@ -317,3 +317,66 @@ def test_output_kernel_rows_and_groups(dtype, case):
             for x, y in zip((d, je, js), first):
                 assert torch.equal(x, y)
         sp.close()
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+@pytest.mark.parametrize("case", ["chno_poly_n10l10", "water_poly_n8l6", "water_gto_n8l12", "five_species_gto_n4l4"])
+def test_streamed_density_kernel(dtype, case):
+    """The density step of the Jacobian path that streams the coefficients to
+    the scratch (one workgroup per center, one species' sums in registers at
+    a time; the output kernel then writes the descriptor and center blocks):
+    descriptor and every block of every center against the oracle at each
+    chunk width that fits, the same bits at every width, and the shared
+    density kernel (l-groups) within the tolerance of the oracle too."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    if case == "chno_poly_n10l10":
+        wl = workloads.Workload(case, (1, 6, 7, 8), "polynomial", 5.0, 0.4, 10, 10, True, ("none",))
+        st = workloads.random_small(60, 41, 5.0, species=(1, 6, 7, 8), dmin=0.85)
+    elif case == "water_poly_n8l6":
+        wl = dataclasses.replace(workloads.WATER64, name=case, rbf="polynomial", n_max=8, l_max=6)
+        st = structure(workloads.WATER64)
+    elif case == "water_gto_n8l12":
+        wl = dataclasses.replace(workloads.WATER64, name=case, n_max=8, l_max=12)
+        st = structure(workloads.WATER64)
+    else:
+        wl = workloads.Workload(case, (1, 6, 7, 8, 16), "gto", 5.0, 0.45, 4, 4, True, ("none",))
+        st = workloads.random_small(70, 53, 5.0, species=(1, 6, 7, 8, 16), dmin=0.85)
+    idx = np.arange(st.n_atoms)
+    ref = oracle_for(wl).compute(st.pos64, st.Z, centers=idx, jacobian=True)
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
+    Z = torch.from_numpy(st.Z).cuda()
+    first, ran = None, 0
+    for tile in (64, 32, 16, -1):
+        sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+        sp._check(sp._L.soap_set_option(sp._h, b"djs_tile", tile))
+        kern, got = sp.get_option("jacobian_density_kernel"), sp.get_option("jacobian_density_tile")
+        if tile > 0 and (kern != 2 or got != tile):
+            sp.close()  # this width does not fit the on-chip plan
+            continue
+        if tile == -1:
+            assert kern == 0
+        sp.build_neighbors(pos, Z)
+        d, je, js = sp.derivatives()
+        row, cols = sp.neighbors()
+        torch.cuda.synchronize()
+        g = dict(row=row.cpu().numpy(), cols=cols.cpu().numpy(), fmaps=[sp.feature_map(k) for k in range(len(wl.species))],
+                 jedge={}, jself={})
+        for c in idx:
+            r0, r1 = int(g["row"][c]), int(g["row"][c + 1])
+            g["jedge"][int(c)] = je[r0:r1].cpu().double().numpy()
+            g["jself"][int(c)] = js[int(c)].cpu().double().numpy()
+        ed = row_errors(d.cpu().double().numpy()[idx], ref["desc"]).max()
+        ej = jacobian_errors(g, ref, st, wl.species, idx.tolist(), idx)
+        print(f"[djs] {case} {dtype} tile {tile} (kernel {kern}): desc {ed:.2e} jac {ej:.2e}", flush=True)
+        assert ed < TOL[dtype] and ej < TOL[dtype]
+        if tile > 0:
+            ran += 1
+            if first is None:
+                first = (d.clone(), je.clone(), js.clone())
+            else:
+                for x, y in zip((d, je, js), first):
+                    assert torch.equal(x, y)
+        sp.close()
+    assert ran >= 1
