@@ -296,8 +296,8 @@ __host__ __device__ __forceinline__ size_t table_doubles(const Params &P, int lg
     size_t d = 16 + even(ldN * ldN) + 4 * (size_t)grad_pairs(P.lmax);
     if (P.rbf == 0) d += 2 * (size_t)lgc * n * n + even((size_t)lgc * n);
     else if (P.rbf == 2) d += 4 * n * (n + 3) + even(n);
-    else d += 2 * (size_t)lgc * n * n + 2 * (size_t)lgc * n;
-    return d;
+    else if (P.rbf == 3) d += 2 * (size_t)lgc * n * n + 2 * (size_t)lgc * n;
+    return d; // the polynomial quadrature reads its radial factors from k_radial: no tables
 }
 
 // RBF: the radial basis fixed at compile time (0 GTO), or -1 to read it from P
@@ -743,10 +743,10 @@ __global__ __launch_bounds__(BSR) void k_radial(Params P, Rows R, const PosT *__
 
 typedef double dbl4 __attribute__((ext_vector_type(4)));
 
-// Workgroup copy of cnt doubles from global memory to LDS with U loads in
-// flight per thread (a plain strided loop waits for each load in turn).
-template <int BS, int U>
-__device__ __forceinline__ void copy_to_lds(double *__restrict__ dst, const double *__restrict__ src, int cnt,
+// Workgroup copy of cnt doubles from global memory to LDS (as DT) with U
+// loads in flight per thread (a plain strided loop waits for each load in turn).
+template <int BS, int U, typename DT = double>
+__device__ __forceinline__ void copy_to_lds(DT *__restrict__ dst, const double *__restrict__ src, int cnt,
                                             int tid) {
     for (int base = 0; base < cnt; base += U * BS) {
         double v[U];
@@ -758,7 +758,7 @@ __device__ __forceinline__ void copy_to_lds(double *__restrict__ dst, const doub
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int k = base + u * BS + tid;
-            if (k < cnt) dst[k] = v[u];
+            if (k < cnt) dst[k] = (DT)v[u];
         }
     }
 }
@@ -2394,7 +2394,11 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jac
     Carver cv{smem};
     Tables T;
     load_tables<NT, LWT, RBF>(P, cv, T, 0, lw);
-    double *cT = cv.take((size_t)Sn * L); // [L][Sn]
+    // [L][Sn] at the assembly precision: in the mixed mode the coefficients
+    // enter the (float64) precontraction rounded to float32, which halves the
+    // largest LDS table (the bases of four species and l_max 10 then keep
+    // two workgroups per CU instead of one)
+    AT *cT = (AT *)cv.take(((size_t)Sn * L * ab + 7) / 8);
     double *rgeo = cv.take(4 * (size_t)RBk);
     int *rsp = (int *)cv.take((RBk + 1) / 2);
     uint32_t *dtab = (uint32_t *)cv.take(((size_t)tri_lw + 1) / 2);
@@ -2470,7 +2474,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jac
                             const int m = 4 * cq + kk;
                             const bool ok = j0 + q < nj && m <= 2 * lq;
                             const int row = lq * lq + (ok ? m : 0);
-                            const double a = Arow[row], b = cT[row * Sn + uc];
+                            const double a = Arow[row], b = (double)cT[row * Sn + uc];
                             av[q] = (ok && aok) ? a : 0.0;
                             bv[q] = (ok && uok) ? b : 0.0;
                             if (++cq == (lq >> 1) + 1) {

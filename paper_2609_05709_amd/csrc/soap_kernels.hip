@@ -128,7 +128,7 @@ size_t jacobian_lds_bytes(const Params &P, int W, bool at64) {
     const int ab = at64 ? 8 : 4;
     const size_t L = (size_t)P.L, Sn = (size_t)P.S * P.n;
     const int RBk = row_block(NWJ * W);
-    size_t d = table_doubles(P, P.lmax + 1) + even(Sn * L) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
+    size_t d = table_doubles(P, P.lmax + 1) + even((Sn * L * ab + 7) / 8) + even(4 * (size_t)RBk) + even((RBk + 1) / 2) +
                even(((size_t)P.tri_lw + 1) / 2) + NWJ * jac_wave_doubles(P, W, ab);
     return d * 8;
 }
