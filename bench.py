@@ -251,7 +251,7 @@ def cc_bytes(sp, wl, nc, E, out_bytes):
 
 # what the timed path computes in, per output precision and internal arithmetic
 DTYPE_LABEL = {
-    ("float32", "mixed"): "mixed: f64 geometry/radial sums/accumulation/MFMA, f32 staging and final assembly",
+    ("float32", "mixed"): "mixed: f64 geometry/radial sums/accumulation/MFMA, f32 staged operands and final assembly",
     ("float32", "fp64"): "f64 (outputs rounded to f32)",
     ("float64", "mixed"): "f64",
     ("float64", "fp64"): "f64",

@@ -33,13 +33,15 @@
  *     stream).  All calls are asynchronous on `stream` unless stated.
  *   - dtype (option "dtype"): SOAP_FP32 (default) = float32 positions and
  *     outputs; SOAP_FP64 = float64 positions and outputs.  The float64 mode
- *     computes everything in float64.  The float32 mode computes the edge
+ *     computes everything in float64.  The float32 mode forms the edge
  *     geometry, radial sums, projection sums, power spectrum, center block
- *     and the Jacobian's precontraction in float64, but rounds the staged
- *     harmonics and radial factors to float32 before the projection's
- *     products, and the precontraction results and radial factors to
- *     float32 before the Jacobian's final two-term assembly, which then
- *     runs in float32.  Option "arith" = SOAP_ARITH_FP64 keeps float64
+ *     and the Jacobian's precontraction with float64 products and sums, but
+ *     rounds operands to float32 where they are staged on chip: the
+ *     harmonics and radial factors before the projection's products, the
+ *     coefficients before the Jacobian's precontraction (and c, D before
+ *     the output kernel's products where that kernel runs), and the
+ *     precontraction results and radial factors before the Jacobian's final
+ *     two-term assembly, which then runs in float32.  Option "arith" = SOAP_ARITH_FP64 keeps float64
  *     through every step in the float32 mode too and rounds only the
  *     stored outputs (the paper's choice, Sec. 3.1: float64 internal
  *     arithmetic, outputs cast at the end).

@@ -168,12 +168,23 @@ def test_degree_above_limit_is_a_capacity_error():
         assert jacobian_errors(g, ref, st, wl.species, sample, np.asarray(sample)) < TOL["float32"]
 
 
+def _shared_density_kernel(sp):
+    """Route the Jacobian path through the shared (work-counter) density
+    kernel, as the streaming one would otherwise take these bases."""
+    sp._check(sp._L.soap_set_option(sp._h, b"djs_tile", -1))
+    assert sp.get_option("jacobian_density_kernel") == 0
+    return sp
+
+
 @pytest.mark.parametrize("case", ["8species_n8l6", "chno_quad128"])
-def test_modes_with_different_group_counts(case):
+@pytest.mark.parametrize("density", ["shared", "auto"])
+def test_modes_with_different_group_counts(case, density):
     """Descriptor, Jacobian and coefficient calls in any order on one
     neighbour list, for bases whose density modes split l into different
     numbers of groups (each group's work counter keeps its own count): every
-    result equals a fresh context's, and the first ones match the oracle."""
+    result equals a fresh context's, and the first ones match the oracle.
+    "shared": the Jacobian path on the shared density kernel as well (three
+    modes, three group counts); "auto": the planner's choice."""
     import torch
     if case == "8species_n8l6":
         species = tuple(range(1, 9))
@@ -187,6 +198,8 @@ def test_modes_with_different_group_counts(case):
     print(f"[modes] {case}", flush=True)
     sp = _ctx(wl, st, **kw)
     fresh = _ctx(wl, st, **kw)
+    if density == "shared":
+        sp, fresh = _shared_density_kernel(sp), _shared_density_kernel(fresh)
     d0 = fresh.compute().clone()
     j0 = [t.clone() for t in fresh.derivatives()]
     c0 = fresh.coefficients().clone()
