@@ -137,7 +137,7 @@ def measured_traffic(workload_name, kernel, output):
         return None
 
 
-KERNEL_SOURCES = ("soap_device.h", "soap_kernels.hip", "jacobian_fixed.hip", "soap_internal.h")
+KERNEL_SOURCES = ("soap_device.h", "soap_kernels.hip", "density_streamed.hip", "jacobian_fixed.hip", "soap_internal.h")
 
 
 def kernels_source_sha():
@@ -259,7 +259,8 @@ DTYPE_LABEL = {
 
 
 def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives", periodic=False, arith="mixed",
-        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None, djac_tile=None, batches=0):
+        cpu_budget_s=12.0, desc_tile=0, pipeline=None, pipeline_density_wg=None, djac_tile=None, batches=0,
+        options=()):
     import torch
     from paper_2609_05709_amd.soap import Soap
     st = wl.structure()
@@ -273,6 +274,8 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         sp._check(sp._L.soap_set_option(sp._h, b"djac_tile", int(djac_tile)))
     if pipeline is not None:
         sp._check(sp._L.soap_set_option(sp._h, b"pipeline", int(pipeline)))
+    for key, value in options:
+        sp._check(sp._L.soap_set_option(sp._h, key.encode(), int(value)))
     if pipeline_density_wg is not None:
         sp._check(sp._L.soap_set_option(sp._h, b"pipeline_density_wg", int(pipeline_density_wg)))
     if periodic:
@@ -460,6 +463,8 @@ def main():
                     help="Jacobian path's density step (GTO): 0 automatic, -1 the shared density kernel, else chunk")
     ap.add_argument("--desc-tile", type=int, default=0, choices=[0, -1, 16, 32, 64],
                     help="GTO descriptor kernel: 0 automatic, -1 the shared density kernel, else edges per chunk")
+    ap.add_argument("--option", action="append", default=[], metavar="KEY=VALUE",
+                    help="any soap_set_option tuning knob (e.g. out_rows=0, djs_tile=32); repeatable")
     ap.add_argument("--copy-calibration", action="store_true", help="run only a 1 GiB device copy (counter scaling)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -482,7 +487,8 @@ def main():
     wl = workload_by_name(a.workload or "water1000")
     line = run(wl, a.steps, a.warmup, a.dtype, with_cpu=not a.no_cpu_baseline, mode=a.mode, periodic=a.periodic,
                arith=a.arith, desc_tile=a.desc_tile, pipeline=a.pipeline, pipeline_density_wg=a.pipeline_density_wg,
-               djac_tile=a.djac_tile, batches=a.batches)
+               djac_tile=a.djac_tile, batches=a.batches,
+               options=[tuple(o.split("=", 1)) for o in a.option])
     if a.workload is None and a.mode == "derivatives" and not a.periodic:
         # the same headline in the paper's arithmetic (float64 internally,
         # float32 outputs), and the other workloads, each with its own
