@@ -50,6 +50,21 @@ int djs_blocks_per_cu(bool f64, bool ar64, int rbf, int qt, int na, size_t lds) 
     return (e == hipSuccess && nb > 0) ? nb : 0;
 }
 
+// dynamic LDS above the default limit for every variant (set_lds_limits)
+hipError_t djs_set_lds_limit(int lim) {
+    hipError_t e = hipSuccess;
+    for (int f64 = 0; f64 < 2; ++f64)
+        for (int ar64 = 0; ar64 < 2; ++ar64)
+            for (int rbf = 0; rbf < 2; ++rbf)
+                for (int qt = 1; qt <= 4; ++qt)
+                    for (int na : {8, 16}) {
+                        const void *k = djs_kernel(f64 != 0, ar64 != 0, rbf, qt, na);
+                        if (k && e == hipSuccess)
+                            e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, lim);
+                    }
+    return e;
+}
+
 hipError_t launch_djs(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjsLaunch &cfg,
                       double *c_scratch, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;

@@ -237,6 +237,7 @@ size_t djs_lds_bytes(const Params &P, int W, bool st64);
 int djs_blocks_per_cu(bool f64, bool ar64, int rbf, int qt, int na, size_t lds);
 hipError_t launch_djs(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjsLaunch &cfg,
                       double *c_scratch, hipStream_t st);
+hipError_t djs_set_lds_limit(int lim);
 // column means of a row-major (rows x cols) array of the output type, in
 // float64: part[AVG_CHUNKS][cols] partial sums, then mean[cols] (float64)
 // and, if out is not NULL, out[cols] at the output type
