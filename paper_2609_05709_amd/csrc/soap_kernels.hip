@@ -255,6 +255,7 @@ hipError_t set_lds_limits() {
             if (k != reinterpret_cast<const void *>(&k_jacobian<float, float, 0, 0>)) SOAP_SET(k);
         }
 #undef SOAP_SET
+    if (e == hipSuccess) e = djs_set_lds_limit(lim);
     return e;
 }
 
