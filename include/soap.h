@@ -157,6 +157,14 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  *              writes whole rows where c and one component of D fit on
  *              chip, 0 = always in l-groups (a tuning knob, results
  *              identical);
+ *   "batch_centers": >= 0 (default 0 = one batch): soap_derivatives
+ *              computes its centers in consecutive batches of at most that
+ *              many, one after another on the stream, so that the library's
+ *              scratch (the coefficients c, D of the Jacobian path:
+ *              32 S n_max (l_max+1)^2 bytes per center, and the polynomial
+ *              quadrature's radial factors) is sized for one batch (Sec. 3.3:
+ *              center batches bound the memory of one call); the outputs are
+ *              the same arrays, bit for bit, as in one batch;
  *   "pipeline" : 1..16 (default 1): soap_derivatives splits its centers
  *              into that many chunks and overlaps each chunk's edge
  *              Jacobian (a second stream) with the next chunk's density
@@ -171,6 +179,10 @@ int soap_set_option(soap_ctx *ctx, const char *key, int64_t value);
 /*
  * Read an option (any key of soap_set_option) or a planning decision of the
  * context into *value (host):
+ *   "device"                  : the HIP device ordinal the context was created
+ *                               on (the current device at soap_create: the
+ *                               device argument of the paper's constructor,
+ *                               Sec. 3.1); every call must run with it current;
  *   "descriptor_kernel"       : 1 if soap_compute / soap_coefficients run the
  *                               descriptor kernel that gives each center a
  *                               workgroup, 0 if the shared density kernel;

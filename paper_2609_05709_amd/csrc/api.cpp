@@ -127,6 +127,8 @@ struct soap_ctx {
     // pipelined derivatives: the density kernel of center chunk k + 1 on the
     // caller's stream beside the Jacobian kernel of chunk k on a second one
     int pipe_chunks = 1;         // option "pipeline": chunks per call (1 = one stream)
+    int64_t batch_centers = 0;   // option "batch_centers": soap_derivatives in center batches of at most
+                                 // this many (0 = one batch), the scratch sized for one batch
     int pipe_density_wg = 0;     // option "pipeline_density_wg": density workgroups per CU (0 = as planned)
     hipStream_t aux = nullptr;   // the second stream (default priority)
     std::vector<hipEvent_t> pipe_ev;
@@ -631,6 +633,11 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         c->arith = (int)value;
         return plan_launches(c); // staging sizes and occupancy of the kernels
     }
+    if (!std::strcmp(key, "batch_centers")) {
+        if (value < 0) return fail(c, SOAP_EINVAL, "batch_centers must be >= 0");
+        c->batch_centers = value;
+        return SOAP_OK;
+    }
     if (!std::strcmp(key, "pipeline")) {
         if (value < 1 || value > 16) return fail(c, SOAP_EINVAL, "pipeline must be in 1..16");
         c->pipe_chunks = (int)value;
@@ -691,6 +698,8 @@ int soap_get_option(const soap_ctx *c, const char *key, int64_t *value) {
                {"djac_tile", c->djac_tile},
                {"djs_tile", c->djs_tile},
                {"pipeline", c->pipe_chunks},
+               {"batch_centers", c->batch_centers},
+               {"device", c->device},
                {"pipeline_density_wg", c->pipe_density_wg},
                {"out_rows", c->out_rows ? 1 : 0},
                {"output_kernel_rows", c->out_plan.rows ? 1 : 0},
@@ -1182,10 +1191,41 @@ static int run_derivatives_pipelined(soap_ctx *c, int64_t first, int64_t count, 
     return SOAP_OK;
 }
 
+// descriptor + Jacobian of the centers [first, first + count) in consecutive
+// batches of at most B centers, one after another on `stream`: the density
+// step and the Jacobian kernel of each batch, the coefficient scratch (and the
+// polynomial radial factors) sized for one batch.  Every output is indexed
+// from `first`, as in one call (the edge blocks through Rows::e_origin).
+static int run_derivatives_batched(soap_ctx *c, int64_t first, int64_t count, int64_t B, void *desc_dev,
+                                   void *jac_edge_dev, void *jac_self_dev, void *stream) {
+    const size_t elt = c->built_f64 ? 8 : 4;
+    for (int64_t cf = first; cf < first + count; cf += B) {
+        const int64_t cn = std::min(B, first + count - cf), o = cf - first;
+        int rc = run_density(c, 1, cf, cn, (char *)desc_dev + o * c->F * elt, nullptr,
+                             (char *)jac_self_dev + o * 3 * c->F * elt, nullptr, nullptr, stream);
+        if (rc != SOAP_OK) return rc;
+        if (c->E == 0) continue;
+        SegTimer timer(c, 2, to_stream(stream));
+        hipError_t e = launch_jacobian(c->P, rows_part(c, first, cf, cn), c->pos, c->built_f64, c->ar64, c->jac_cfg,
+                                       c->b_cscratch.as<double>(), jac_edge_dev, to_stream(stream));
+        if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
+        timer.done();
+    }
+    return SOAP_OK;
+}
+
 // descriptor + Jacobian of a center batch; scratch as run_density
 static int run_derivatives(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
                            void *jac_self_dev, double *scratch, void *stream, bool timed = true) {
     if (count == 0) return SOAP_OK;
+    if (timed && !scratch && c->batch_centers > 0 && count > c->batch_centers) {
+        int rc;
+        if (!jacobian_path_ok(c, 1))
+            return fail(c, SOAP_EINVAL, "basis too large for the on-chip memory of the Jacobian kernels");
+        if ((rc = check_ctx_device(c)) != SOAP_OK) return rc;
+        return run_derivatives_batched(c, first, count, c->batch_centers, desc_dev, jac_edge_dev, jac_self_dev,
+                                       stream);
+    }
     // the pipelined path needs its own stream, events and the context's
     // scratch: not for the allocation-free entry point
     if (timed && !scratch && c->pipe_chunks > 1 && c->E > 0 && count >= 2 * c->pipe_chunks) {

@@ -115,15 +115,19 @@ def _stream():
 class Soap:
     """One library context: species, r_cut, n_max, l_max, sigma, rbf
     ("gto" | "polynomial" | "polynomial-laplace"), dtype ("float32" | "float64"),
-    arith ("mixed" | "fp64": the float32 mode's internal arithmetic)."""
+    arith ("mixed" | "fp64": the float32 mode's internal arithmetic), device
+    (made current before soap_create; None = the current device)."""
 
     def __init__(self, species, r_cut, n_max, l_max, sigma, rbf="gto", dtype="float32", quad_n=None,
-                 arith="mixed"):
+                 arith="mixed", device=None):
         import numpy as np
         import torch
         self._L = load_library()
         if not torch.cuda.is_available():
             raise RuntimeError("no HIP device available")
+        if device is not None:
+            # the context lives on the device current at soap_create
+            torch.cuda.set_device(torch.device(device))
         self.species = sorted(int(z) for z in species)
         self.r_cut, self.n_max, self.l_max, self.sigma = float(r_cut), int(n_max), int(l_max), float(sigma)
         if rbf not in RBF_CODES:

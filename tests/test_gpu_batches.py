@@ -259,3 +259,26 @@ def test_pipelined_derivatives_bitwise(chunks, wg):
         for x, y in zip(sp.derivatives_batch(a, b - a, int(row[b] - row[a])), ref_b):
             assert torch.equal(x, y)
     sp.close()
+
+
+@pytest.mark.parametrize("case", ["water1000", "chno4096"])
+def test_batch_centers_option(case):
+    """soap_derivatives with the "batch_centers" option (the call's centers in
+    consecutive batches, the scratch sized for one batch): every output bit
+    for bit equal to one batch; the context reports its device."""
+    import torch
+    wl = workloads.WATER1000 if case == "water1000" else workloads.CHNO4096
+    st = wl.structure()
+    print(f"[batch_centers] {case}", flush=True)
+    sp = _ctx(wl, st)
+    assert sp.get_option("device") == torch.cuda.current_device()
+    ref = [t.clone() for t in sp.derivatives()]
+    for B in (997, 64):
+        sp.set_option("batch_centers", B)
+        assert sp.get_option("batch_centers") == B
+        out = sp.derivatives()
+        torch.cuda.synchronize()
+        for x, y in zip(out, ref):
+            assert torch.equal(x, y), (case, B)
+    sp.set_option("batch_centers", 0)
+    sp.close()
