@@ -376,14 +376,18 @@ def run(wl, steps, warmup, dtype, with_cpu=True, quiet=False, mode="derivatives"
         # the edge-block writes dominate: HBM-bound kernel
         t = kern["jacobian"] * 1e-3
         roof = {"kernel": "k_jacobian", "bound": "hbm", "achieved": alg["jacobian"] / t / 1e9, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "traffic": None if periodic else measured_traffic(wl.name, "k_jacobian", dtype),
+                "unit": "GB/s",
+                # the counters were taken on the default (mixed-arithmetic) kernels
+                "traffic": None if periodic or arith != "mixed" else measured_traffic(wl.name, "k_jacobian", dtype),
                 "alg_bytes_per_launch": alg["jacobian"]}
     else:
         fl = density_flops(wl, E, nc, sp.n_features)
         t = kern["density"] * 1e-3
         roof = {"kernel": desc_kernel, "bound": "alu", "achieved": fl / t / 1e12, "peak": FP64_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "traffic": measured_traffic(wl.name + ("" if mode == "derivatives" else "_" + mode),
-                                                               desc_kernel, dtype), "alg_flops_per_launch": fl}
+                "unit": "TFLOP/s",
+                "traffic": None if arith != "mixed" else measured_traffic(
+                    wl.name + ("" if mode == "derivatives" else "_" + mode), desc_kernel, dtype),
+                "alg_flops_per_launch": fl}
     roof["frac"] = roof["achieved"] / roof["peak"]
     line = {
         "metric": METRIC,
