@@ -825,7 +825,13 @@ __device__ __forceinline__ void power_tiles(const CoefView<CT> cv, int comp, int
     const int ro = lane & 15, kk = lane >> 4;
     int q[4];
     if (ntp == 1) lane_pair_index(pq, Sn, 0, 0, kk, ro, q);
-    for (int item = wave; item < nitem; item += nw) { // uniform per wave
+    // items dealt in snake order over the waves, longest chains first (an
+    // item's chain has (l >> 1) + 1 chunks): every wave gets about the same
+    // number of products, and the slowest wave sets the end of the phase
+    for (int rd = 0;; ++rd) { // uniform per wave
+        const int pos = rd * nw + ((rd & 1) ? nw - 1 - wave : wave);
+        if (pos >= nitem) break;
+        const int item = nitem - 1 - pos;
         const int lc = item / ntp, l = lg0 + lc;
         int tp = item - lc * ntp, ti = 0;
         while (tp >= ntile - ti) {
@@ -879,7 +885,13 @@ __device__ __forceinline__ void power_tiles4(const double *__restrict__ X, int x
     const int ro = lane & 15, kk = lane >> 4;
     int q[4];
     if (ntp == 1) lane_pair_index(pq, Sn, 0, 0, kk, ro, q);
-    for (int item = wave; item < nitem; item += nw) { // uniform per wave
+    // items dealt in snake order over the waves, longest chains first (an
+    // item's chain has (l >> 1) + 1 chunks): every wave gets about the same
+    // number of products, and the slowest wave sets the end of the phase
+    for (int rd = 0;; ++rd) { // uniform per wave
+        const int pos = rd * nw + ((rd & 1) ? nw - 1 - wave : wave);
+        if (pos >= nitem) break;
+        const int item = nitem - 1 - pos;
         const int lc = item / ntp, l = lg0 + lc;
         int tp = item - lc * ntp, ti = 0;
         while (tp >= ntile - ti) {
