@@ -2459,8 +2459,16 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jac
         lds_barrier();
         load_rows(rgeo, rsp, pos, R.spec, R.cols, rb0, rbn, pi);
         lds_barrier();
-        for (int off = wave * W; off < rbn; off += NWJ * W) {
-            const int nb = (rbn - off) < W ? (rbn - off) : W;
+        // full rounds of NWJ tiles of W edges, then the remaining edges split
+        // as evenly as possible over the waves (at most W each): the slowest
+        // wave, which sets the workgroup's end, carries at most one edge more
+        // than the others in the last round instead of a whole tile
+        const int FW = NWJ * W, nfull = rbn / FW, rem = rbn - nfull * FW;
+        const int rq = rem / NWJ, rr = rem - rq * NWJ, mine = rq + (wave < rr ? 1 : 0);
+        const int ntiles = nfull + (mine > 0 ? 1 : 0);
+        for (int t = 0; t < ntiles; ++t) { // uniform per wave
+            const int off = t < nfull ? t * FW + wave * W : nfull * FW + wave * rq + (wave < rr ? wave : rr);
+            const int nb = t < nfull ? W : mine;
             const int64_t base = rb0 + off - ebase; // batch-local edge index
             const double *geo = rgeo + 4 * off;
             const int *spc = rsp + off;
