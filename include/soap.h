@@ -161,7 +161,8 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  *              computes its centers in consecutive batches of at most that
  *              many, one after another on the stream, so that the library's
  *              scratch (the coefficients c, D of the Jacobian path:
- *              32 S n_max (l_max+1)^2 bytes per center, and the polynomial
+ *              4 S n_max (l_max+1)^2 values per center, float32 in the mixed
+ *              arithmetic and float64 otherwise, and the polynomial
  *              quadrature's radial factors) is sized for one batch (Sec. 3.3:
  *              center batches bound the memory of one call); the outputs are
  *              the same arrays, bit for bit, as in one batch;
@@ -373,8 +374,9 @@ int soap_derivatives(soap_ctx *ctx, void *desc_dev, void *jac_edge_dev, void *ja
  *                            when E_b = 0.
  * Each center's outputs are bitwise identical to those of the single call
  * over all centers (the per-center sums run in a fixed order).  The
- * Jacobian's float64 coefficient scratch (32 S n_max (l_max+1)^2 bytes per
- * center) is sized per batch.  count = 0 enqueues nothing.  Errors:
+ * Jacobian's coefficient scratch (4 S n_max (l_max+1)^2 values per center:
+ * float32 in the mixed arithmetic, whose readers round c and D to float32,
+ * float64 with dtype float64 or arith "fp64") is sized per batch.  count = 0 enqueues nothing.  Errors:
  * SOAP_EINVAL (range outside the centers, NULL outputs), SOAP_ESTATE,
  * SOAP_ENOMEM, SOAP_EHIP.
  */
@@ -385,14 +387,16 @@ int soap_derivatives_batch(soap_ctx *ctx, int64_t first, int64_t count, void *de
 /*
  * soap_derivatives_batch for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid
- * hipMalloc): the same outputs, bitwise, with the Jacobian path's float64
+ * hipMalloc): the same outputs, bitwise, with the Jacobian path's
  * coefficient scratch taken from a fixed device array of
  * SOAP_STATIC_SCRATCH_BYTES (64 MiB) that the library holds on every device
  * it runs on (resolved at soap_create) instead of the context's growable
  * buffer.  This call allocates nothing and records no timing events; the
  * neighbour list must already be built (soap_build_neighbors allocates).
- * Limit: count * 32 S n_max (l_max+1)^2 bytes <= SOAP_STATIC_SCRATCH_BYTES
- * (e.g. 2674 centers of the 2-species n_max 8, l_max 6 basis), else
+ * Limit: count * 4 S n_max (l_max+1)^2 scratch values (4 bytes each in the
+ * mixed arithmetic, else 8; plus the polynomial quadrature's radial factors)
+ * <= SOAP_STATIC_SCRATCH_BYTES (e.g. 5349 centers of the 2-species n_max 8,
+ * l_max 6 basis in the mixed arithmetic, 2674 in float64), else
  * SOAP_ECAPACITY with nothing enqueued; larger structures go through in
  * batches.  Every call on one device shares that device's array, which
  * keeps the last call's contents (every entry read is written first, so

@@ -545,9 +545,13 @@ Rows rows_part(const soap_ctx *c, int64_t first, int64_t cf, int64_t cn) {
 }
 Rows rows_of(const soap_ctx *c) { return rows_of(c, 0, c->nc); }
 
-// bytes of the float64 coefficient scratch the Jacobian path keeps per center
-// (c, Dx, Dy, Dz)
-size_t scratch_bytes_per_center(const soap_ctx *c) { return 8 * 4 * (size_t)c->P.S * c->P.n * c->P.L; }
+// bytes of the coefficient scratch the Jacobian path keeps per center:
+// (c, Dx, Dy, Dz) at the staging precision: float32 in the mixed mode (every
+// reader of the scratch rounds it to float32), else float64
+size_t scratch_bytes_per_center(const soap_ctx *c) {
+    const size_t elt = (c->dtype == SOAP_FP64 || c->ar64) ? 8 : 4;
+    return elt * 4 * (size_t)c->P.S * c->P.n * c->P.L;
+}
 
 // the radial pass (polynomial quadrature): bytes for the edges of centers [first, first + count)
 size_t radial_bytes(const soap_ctx *c, int64_t first, int64_t count) {
@@ -1017,7 +1021,7 @@ static int prepare_radial(soap_ctx *c, int64_t first, int64_t count, void *buf, 
 // timed = false: no timer events (they may allocate).  wg_per_cu > 0 caps
 // the persistent density kernel's workgroups per CU.
 static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void *desc, void *c_out, void *jself,
-                       void *jc_edge, double *scratch, void *stream, bool timed = true, int wg_per_cu = 0,
+                       void *jc_edge, void *scratch, void *stream, bool timed = true, int wg_per_cu = 0,
                        bool prep_radial = true) {
     if (!c->have_rows) return fail(c, SOAP_ESTATE, "no neighbour list: call soap_build_neighbors first");
     int rc;
@@ -1031,7 +1035,7 @@ static int run_density(soap_ctx *c, int mode, int64_t first, int64_t count, void
     if (mode == 1 && !scratch) {
         hipError_t e = c->b_cscratch.ensure(scratch_bytes_per_center(c) * (size_t)count);
         if (e != hipSuccess) return hip_fail(c, e, "hipMalloc(coefficient scratch)");
-        scratch = c->b_cscratch.as<double>();
+        scratch = c->b_cscratch.p;
     }
     SegTimer timer(c, 1, to_stream(stream), timed);
     if (prep_radial && (rc = prepare_radial(c, first, count, rbuf, to_stream(stream))) != SOAP_OK) return rc;
@@ -1160,14 +1164,14 @@ static int run_derivatives_pipelined(soap_ctx *c, int64_t first, int64_t count, 
     }
     if (e == hipSuccess) e = c->b_cscratch.ensure(scratch_bytes_per_center(c) * (size_t)count);
     if (e != hipSuccess) return hip_fail(c, e, "pipelined derivatives (setup)");
-    double *scratch = c->b_cscratch.as<double>();
+    char *scratch = (char *)c->b_cscratch.p;
     { // the radial factors of every chunk at once: the chunks' Jacobian launches read them on the other stream
         SegTimer timer(c, 1, st);
         const int rc = prepare_radial(c, first, count, nullptr, st);
         if (rc != SOAP_OK) return rc;
         timer.done();
     }
-    const size_t elt = c->built_f64 ? 8 : 4, pc = scratch_bytes_per_center(c) / 8;
+    const size_t elt = c->built_f64 ? 8 : 4, pc = scratch_bytes_per_center(c);
     for (int k = 0; k < K; ++k) {
         const int64_t cf = first + count * k / K, cn = first + count * (k + 1) / K - cf;
         if (cn == 0) continue;
@@ -1207,7 +1211,7 @@ static int run_derivatives_batched(soap_ctx *c, int64_t first, int64_t count, in
         if (c->E == 0) continue;
         SegTimer timer(c, 2, to_stream(stream));
         hipError_t e = launch_jacobian(c->P, rows_part(c, first, cf, cn), c->pos, c->built_f64, c->ar64, c->jac_cfg,
-                                       c->b_cscratch.as<double>(), jac_edge_dev, to_stream(stream));
+                                       c->b_cscratch.p, jac_edge_dev, to_stream(stream));
         if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
         timer.done();
     }
@@ -1216,7 +1220,7 @@ static int run_derivatives_batched(soap_ctx *c, int64_t first, int64_t count, in
 
 // descriptor + Jacobian of a center batch; scratch as run_density
 static int run_derivatives(soap_ctx *c, int64_t first, int64_t count, void *desc_dev, void *jac_edge_dev,
-                           void *jac_self_dev, double *scratch, void *stream, bool timed = true) {
+                           void *jac_self_dev, void *scratch, void *stream, bool timed = true) {
     if (count == 0) return SOAP_OK;
     if (timed && !scratch && c->batch_centers > 0 && count > c->batch_centers) {
         int rc;
@@ -1241,7 +1245,7 @@ static int run_derivatives(soap_ctx *c, int64_t first, int64_t count, void *desc
     if (c->E == 0) return SOAP_OK;
     SegTimer timer(c, 2, to_stream(stream), timed);
     hipError_t e = launch_jacobian(c->P, rows_of(c, first, count), c->pos, c->built_f64, c->ar64, c->jac_cfg,
-                                   scratch ? scratch : c->b_cscratch.as<double>(), jac_edge_dev, to_stream(stream));
+                                   scratch ? scratch : c->b_cscratch.p, jac_edge_dev, to_stream(stream));
     if (e != hipSuccess) return hip_fail(c, e, "Jacobian kernel");
     timer.done();
     return SOAP_OK;
@@ -1298,7 +1302,7 @@ int soap_derivatives_batch_noalloc(soap_ctx *c, int64_t first, int64_t count, vo
     if (!c->static_scratch) return fail(c, SOAP_EHIP, "the static scratch of device %d is not available", c->device);
     // the density kernel writes every scratch entry the later kernels read,
     // so nothing needs clearing
-    return run_derivatives(c, first, count, desc_dev, jac_edge_dev, jac_self_dev, (double *)c->static_scratch, stream,
+    return run_derivatives(c, first, count, desc_dev, jac_edge_dev, jac_self_dev, c->static_scratch, stream,
                            false);
 }
 

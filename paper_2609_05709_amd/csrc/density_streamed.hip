@@ -66,7 +66,7 @@ hipError_t djs_set_lds_limit(int lim) {
 }
 
 hipError_t launch_djs(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjsLaunch &cfg,
-                      double *c_scratch, hipStream_t st) {
+                      void *c_scratch, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     Params Pk = P;
     Rows Rk = R;

@@ -27,7 +27,8 @@
 //   center), then writes the power spectrum Eq. (powerspectrum) and the
 //   center's own Jacobian block -K_l sum_m (D^mu c^nu + c^mu D^nu)
 //   (Eq. powerspectrum-derivative with translational invariance).  c goes to
-//   a float64 scratch for k_jacobian.
+//   a scratch for k_jacobian, at the staging precision (float32 in the mixed
+//   mode, where every reader rounds it to float32 anyway).
 // k_jacobian: one workgroup per center; per edge the precontraction
 //   U = sum_m S_lm c, V = sum_m grad S_lm c on the matrix cores, then the
 //   neighbour block from U, V, B, Bh (see the kernel).
@@ -745,8 +746,8 @@ typedef double dbl4 __attribute__((ext_vector_type(4)));
 
 // Workgroup copy of cnt doubles from global memory to LDS (as DT) with U
 // loads in flight per thread (a plain strided loop waits for each load in turn).
-template <int BS, int U, typename DT = double>
-__device__ __forceinline__ void copy_to_lds(DT *__restrict__ dst, const double *__restrict__ src, int cnt,
+template <int BS, int U, typename DT = double, typename SRT = double>
+__device__ __forceinline__ void copy_to_lds(DT *__restrict__ dst, const SRT *__restrict__ src, int cnt,
                                             int tid) {
     for (int base = 0; base < cnt; base += U * BS) {
         double v[U];
@@ -1005,13 +1006,13 @@ constexpr int dens_min_waves(int mode, int rbf, bool hi) {
 }
 
 // ST: precision of the staged harmonics and radial factors (OutT, or double
-// for float64 arithmetic with float32 outputs).
+// for float64 arithmetic with float32 outputs), and of the coefficient scratch.
 template <typename PosT, typename OutT, int MODE, int RBF, bool HI, typename ST = OutT>
 __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                                  unsigned long long *__restrict__ work, WorkBase base,
                                                  OutT *__restrict__ desc,
                                                  OutT *__restrict__ c_out, OutT *__restrict__ jself,
-                                                 double *__restrict__ c_scratch, OutT *__restrict__ jc_edge) {
+                                                 ST *__restrict__ c_scratch, OutT *__restrict__ jc_edge) {
     constexpr bool JAC = MODE != 0, CCJ = MODE == 2;
     // 16-byte aligned: the carved regions are read with 16-byte LDS accesses
     extern __shared__ __align__(16) double smem[];
@@ -1260,11 +1261,11 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
                                    pq, wave, NWD, lane, T.Kl);
             // in destination order (consecutive lanes, consecutive addresses);
             // the transposition falls on the LDS reads
-            double *sc = c_scratch + cw * 4 * (size_t)Lfull * Sn;
+            ST *sc = c_scratch + cw * 4 * (size_t)Lfull * Sn;
             for (int it = tid; it < (whole ? 1 : 4) * SnL; it += BSD) {
                 const int comp = it / SnL, rem = it - comp * SnL;
                 const int lmg = qdiv(rem, inv_Sn), sa = rem - lmg * Sn;
-                sc[((size_t)comp * Lfull + lm0 + lmg) * Sn + sa] = cacc[comp * SnL + sa * Lg + lmg];
+                sc[((size_t)comp * Lfull + lm0 + lmg) * Sn + sa] = (ST)cacc[comp * SnL + sa * Lg + lmg];
             }
         }
         lds_barrier(); // the outputs are read from cacc before the next center clears it
@@ -1561,7 +1562,7 @@ __host__ __device__ __forceinline__ size_t djac_lds_doubles(const Params &P, int
 template <typename PosT, typename OutT, typename ST, int QT, int NA, int SR>
 __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__restrict__ pos, int W,
                                               OutT *__restrict__ desc, OutT *__restrict__ jself,
-                                              double *__restrict__ c_scratch) {
+                                              ST *__restrict__ c_scratch) {
     extern __shared__ __align__(16) double smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1777,10 +1778,10 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
         power_tiles4<OutT>(cb, SnL, L, 1, Sn, 0, 0, lw, desc + cw * P.F, jself + cw * 3 * P.F, P.F, lw, 0,
                            PairIndex{S, n, 1.0f / (float)n}, wave, NWC, lane, Kl);
         // the coefficients for k_jacobian, [lm][species n], in destination order
-        double *sc = c_scratch + cw * 4 * (size_t)L * Sn;
+        ST *sc = c_scratch + cw * 4 * (size_t)L * Sn;
         for (int it = tid; it < SnL; it += BSC) {
             const int lm = it / Sn, sa = it - lm * Sn;
-            sc[it] = cb[sa * L + lm];
+            sc[it] = (ST)cb[sa * L + lm];
         }
     }
 }
@@ -1868,7 +1869,7 @@ __host__ __device__ __forceinline__ int djs_tasks(const Params &P) {
 
 template <typename PosT, typename ST, int QT, int NA, int RBF>
 __global__ __launch_bounds__(BSC) void k_djs(Params P, Rows R, const PosT *__restrict__ pos, int W,
-                                             double *__restrict__ c_scratch) {
+                                             ST *__restrict__ c_scratch) {
     extern __shared__ __align__(16) double smem[];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1967,7 +1968,7 @@ __global__ __launch_bounds__(BSC) void k_djs(Params P, Rows R, const PosT *__res
         double acc[QT][2][4];
         const int64_t cw = ci;
         const int spec_c = spec_i;
-        double *sc = c_scratch + cw * 4 * (size_t)L * Sn; // [c, Dx, Dy, Dz][lm][species n]
+        ST *sc = c_scratch + cw * 4 * (size_t)L * Sn; // [c, Dx, Dy, Dz][lm][species n]
         // the sums of species s (or zeros) to the scratch; c of the center's
         // own species gets the on-site term
         auto flush = [&](int s, bool sums) {
@@ -1976,12 +1977,12 @@ __global__ __launch_bounds__(BSC) void k_djs(Params P, Rows R, const PosT *__res
 #pragma unroll
                 for (int a = 0; a < 2; ++a)
                     if (ok_q[q] && a_q[q] + a < n) {
-                        double *o = sc + (size_t)lm_q[q] * Sn + s * n + a_q[q] + a;
+                        ST *o = sc + (size_t)lm_q[q] * Sn + s * n + a_q[q] + a;
 #pragma unroll
                         for (int d = 0; d < 4; ++d) {
                             double v = sums ? acc[q][a][d] : 0.0;
                             if (d == 0 && s == spec_c && lm_q[q] == 0) v += c0[a_q[q] + a];
-                            o[(size_t)d * L * Sn] = v;
+                            o[(size_t)d * L * Sn] = (ST)v;
                         }
                     }
         };
@@ -2120,8 +2121,8 @@ __host__ __device__ __forceinline__ size_t outputs_group_doubles(const Params &P
     return 4 * even(slab) + 4 * even(((size_t)P.nq_full * (lg1 - lg0) * out_bytes + 7) / 8);
 }
 
-template <typename OutT>
-__global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const double *__restrict__ scratch,
+template <typename OutT, typename ST = OutT>
+__global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const ST *__restrict__ scratch,
                                                  OutT *__restrict__ desc, OutT *__restrict__ jself) {
     extern __shared__ __align__(16) double smem[];
     __shared__ double Kl[16];
@@ -2132,7 +2133,7 @@ __global__ __launch_bounds__(BSO) void k_outputs(Params P, OutPlan O, const doub
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     double *base = smem;
     const PairIndex pq{P.S, P.n, 1.0f / (float)P.n};
-    const double *src = scratch + ci * 4 * (size_t)L * Sn;
+    const ST *src = scratch + ci * 4 * (size_t)L * Sn;
     OutT *drow = desc + ci * F, *jrow = jself + ci * 3 * F; // jself rows d = 0..2 are consecutive
     for (int g = 0; g < O.n_groups; ++g) {
         const int lg0 = O.lgrp[g], lg1 = O.lgrp[g + 1], lgc = lg1 - lg0, lm0 = lg0 * lg0;
@@ -2201,7 +2202,7 @@ __host__ __device__ __forceinline__ size_t outputs_rows_doubles(const Params &P,
 // ST: precision of the staged c and D (float64, or float32 in the mixed mode;
 // the products and sums stay float64 on the matrix cores)
 template <typename OutT, typename ST>
-__global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *__restrict__ scratch,
+__global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const ST *__restrict__ scratch,
                                                        OutT *__restrict__ desc, OutT *__restrict__ jself) {
     extern __shared__ __align__(16) double smem[];
     __shared__ double Kl[16];
@@ -2212,7 +2213,7 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *_
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     ST *Xc = (ST *)smem, *Xd = (ST *)(smem + sstr);
     OutT *row = (OutT *)(smem + 2 * sstr);
-    const double *src = scratch + ci * 4 * (size_t)slab; // [c, Dx, Dy, Dz][lm][species n]
+    const ST *src = scratch + ci * 4 * (size_t)slab; // [c, Dx, Dy, Dz][lm][species n]
     // c and D_x, eight loads in flight per thread
     for (int k0 = 0; k0 < 2 * slab; k0 += 8 * BSO2) {
         double v[8];
@@ -2230,9 +2231,9 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const double *_
     lds_barrier();
     const PairIndex pq{S, n, 1.0f / (float)n};
     for (int p = 0; p < 4; ++p) {
-        double pf[OUT_PF];
+        ST pf[OUT_PF];
         if (p == 1 || p == 2) {
-            const double *nx = src + (size_t)(p + 1) * slab;
+            const ST *nx = src + (size_t)(p + 1) * slab;
 #pragma unroll
             for (int u = 0; u < OUT_PF; ++u) {
                 const int k = u * BSO2 + tid;
@@ -2391,7 +2392,7 @@ constexpr int jac_min_waves(int ab, int NT, int LWT) {
 // arithmetic with float32 outputs).
 template <typename PosT, typename OutT, int NT, int LWT, int RBF = -1, typename AT = OutT>
 __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jacobian(Params P, Rows R, const PosT *__restrict__ pos,
-                                                                            int W, int vec, const double *__restrict__ c_scratch,
+                                                                            int W, int vec, const AT *__restrict__ c_scratch,
                                                                             OutT *__restrict__ jedge) {
     using AT2 = typename Pair<AT>::type;
     constexpr int ab = sizeof(AT);
@@ -2449,7 +2450,7 @@ __global__ __launch_bounds__(BSJ, jac_min_waves(sizeof(AT), NT, LWT)) void k_jac
     const int64_t ci = blockIdx.x;
     const int64_t e0 = R.row_ptr[ci], e1 = R.row_ptr[ci + 1], ebase = *R.e_origin;
     if (e1 == e0) return;
-    const double *cg = c_scratch + ci * 4 * (size_t)Sn * L; // component c of [c, Dx, Dy, Dz]
+    const AT *cg = c_scratch + ci * 4 * (size_t)Sn * L; // component c of [c, Dx, Dy, Dz]
     copy_to_lds<BSJ, 4>(cT, cg, Sn * L, tid);
     const int64_t i = R.centers ? (int64_t)R.centers[ci] : R.c_base + ci;
     const double3 pi = make_double3((double)pos[3 * i], (double)pos[3 * i + 1], (double)pos[3 * i + 2]);

@@ -191,7 +191,7 @@ hipError_t set_lds_limits();
 // jc_edge = [E][3][n][L])
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, int mode,
                           const DensityLaunch &cfg, unsigned long long *work, WorkBase *epoch, void *desc, void *c_out,
-                          void *jself, double *c_scratch, void *jc_edge, hipStream_t st);
+                          void *jself, void *c_scratch, void *jc_edge, hipStream_t st);
 // power spectrum and center block from the coefficient scratch (Jacobian
 // path): whole rows (rows = true: c and one component of D for every l in
 // LDS), else l-groups of the output kernel, each sized to its LDS budget
@@ -204,7 +204,7 @@ struct OutPlan {
 };
 // allow_rows = false keeps the l-group kernel; 0, or -1 if one l does not fit
 int plan_outputs(const Params &P, bool f64, bool st64, bool allow_rows, OutPlan *O);
-hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
+hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const void *scratch, void *desc,
                           void *jself, hipStream_t st);
 // one-wave-per-center descriptor kernel (GTO): the shape of its accumulators
 // (false if the basis has none), LDS bytes for W edges per chunk, resident
@@ -226,9 +226,9 @@ hipError_t launch_radial(const Params &P, const Rows &R, const void *pos, bool f
                          hipStream_t st);
 int djac_blocks_per_cu(bool f64, bool ar64, int qt, int na, int sr, size_t lds);
 hipError_t launch_djac(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjacLaunch &cfg,
-                       void *desc, void *jself, double *c_scratch, hipStream_t st);
+                       void *desc, void *jself, void *c_scratch, hipStream_t st);
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const JacLaunch &cfg,
-                           const double *c_scratch, void *jedge, hipStream_t st);
+                           const void *c_scratch, void *jedge, hipStream_t st);
 // density step of the Jacobian path with the coefficients streamed to the
 // scratch (k_djs, density_streamed.hip): GTO and polynomial quadrature bases
 // of at most four (radial pair, lm) tasks per thread
@@ -236,7 +236,7 @@ bool djs_shape(const Params &P, int *qt, int *na);
 size_t djs_lds_bytes(const Params &P, int W, bool st64);
 int djs_blocks_per_cu(bool f64, bool ar64, int rbf, int qt, int na, size_t lds);
 hipError_t launch_djs(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjsLaunch &cfg,
-                      double *c_scratch, hipStream_t st);
+                      void *c_scratch, hipStream_t st);
 hipError_t djs_set_lds_limit(int lim);
 // column means of a row-major (rows x cols) array of the output type, in
 // float64: part[AVG_CHUNKS][cols] partial sums, then mean[cols] (float64)

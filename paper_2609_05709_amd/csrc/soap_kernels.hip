@@ -168,26 +168,34 @@ int plan_outputs(const Params &P, bool f64, bool st64, bool allow_rows, OutPlan 
     return 0;
 }
 
-hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const double *scratch, void *desc,
+hipError_t launch_outputs(const Params &P, const OutPlan &O, int64_t nc, bool f64, const void *scratch, void *desc,
                           void *jself, hipStream_t st) {
     if (nc <= 0) return hipSuccess;
     if (O.rows) {
         if (f64)
-            hipLaunchKernelGGL((k_outputs_rows<double, double>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+            hipLaunchKernelGGL((k_outputs_rows<double, double>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P,
+                               (const double *)scratch,
                                (double *)desc, (double *)jself);
         else if (O.st64)
-            hipLaunchKernelGGL((k_outputs_rows<float, double>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+            hipLaunchKernelGGL((k_outputs_rows<float, double>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P,
+                               (const double *)scratch,
                                (float *)desc, (float *)jself);
         else
-            hipLaunchKernelGGL((k_outputs_rows<float, float>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P, scratch,
+            hipLaunchKernelGGL((k_outputs_rows<float, float>), dim3((unsigned)nc), dim3(BSO2), O.lds, st, P,
+                               (const float *)scratch,
                                (float *)desc, (float *)jself);
         return hipGetLastError();
     }
     dim3 grid((unsigned)nc), block(BSO);
     if (f64)
-        hipLaunchKernelGGL(k_outputs<double>, grid, block, O.lds, st, P, O, scratch, (double *)desc, (double *)jself);
+        hipLaunchKernelGGL((k_outputs<double, double>), grid, block, O.lds, st, P, O, (const double *)scratch,
+                           (double *)desc, (double *)jself);
+    else if (O.st64)
+        hipLaunchKernelGGL((k_outputs<float, double>), grid, block, O.lds, st, P, O, (const double *)scratch,
+                           (float *)desc, (float *)jself);
     else
-        hipLaunchKernelGGL(k_outputs<float>, grid, block, O.lds, st, P, O, scratch, (float *)desc, (float *)jself);
+        hipLaunchKernelGGL((k_outputs<float, float>), grid, block, O.lds, st, P, O, (const float *)scratch,
+                           (float *)desc, (float *)jself);
     return hipGetLastError();
 }
 
@@ -238,11 +246,12 @@ hipError_t set_lds_limits() {
                     for (int sr : {2, 4}) SOAP_SET(djac_kernel(f64 != 0, ar64 != 0, qt, na, sr));
     for (int f64 = 0; f64 < 2; ++f64)
         for (int na : {4, 8, 12, 16}) SOAP_SET(radial_kernel(f64 != 0, na));
-    SOAP_SET(k_outputs<float>);
+    SOAP_SET((k_outputs<float, float>));
+    SOAP_SET((k_outputs<float, double>));
     SOAP_SET((k_outputs_rows<float, float>));
     SOAP_SET((k_outputs_rows<float, double>));
     SOAP_SET((k_outputs_rows<double, double>));
-    SOAP_SET(k_outputs<double>);
+    SOAP_SET((k_outputs<double, double>));
     SOAP_SET(k_power_single<float>);
     SOAP_SET(k_power_single<double>);
     SOAP_SET((k_jacobian<float, float, 0, 0>));
@@ -261,7 +270,7 @@ hipError_t set_lds_limits() {
 
 hipError_t launch_density(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, int mode,
                           const DensityLaunch &cfg, unsigned long long *work, WorkBase *epoch, void *desc, void *c_out,
-                          void *jself, double *c_scratch, void *jc_edge, hipStream_t st) {
+                          void *jself, void *c_scratch, void *jc_edge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     const int64_t per_group = std::min<int64_t>(R.nc, (int64_t)cfg.blocks);
     WorkBase b = *epoch;
@@ -331,7 +340,7 @@ int djac_blocks_per_cu(bool f64, bool ar64, int qt, int na, int sr, size_t lds) 
 }
 
 hipError_t launch_djac(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const DjacLaunch &cfg,
-                       void *desc, void *jself, double *c_scratch, hipStream_t st) {
+                       void *desc, void *jself, void *c_scratch, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     Params Pk = P;
     Rows Rk = R;
@@ -343,7 +352,7 @@ hipError_t launch_djac(const Params &P, const Rows &R, const void *pos, bool f64
 }
 
 hipError_t launch_jacobian(const Params &P, const Rows &R, const void *pos, bool f64, bool ar64, const JacLaunch &cfg,
-                           const double *c_scratch, void *jedge, hipStream_t st) {
+                           const void *c_scratch, void *jedge, hipStream_t st) {
     if (R.nc <= 0) return hipSuccess;
     Params Pk = P;
     Rows Rk = R;

@@ -49,7 +49,8 @@ def test_noalloc_matches_batch_entry_point():
     import torch
     from paper_2609_05709_amd.soap import load_library
     L = load_library()
-    # first call: 2000 centers of the 3000-atom water cluster (50 MB of scratch)
+    # first call: 2000 centers of the 3000-atom water cluster (25 MB of float32
+    # scratch in the mixed mode)
     wl = workloads.WATER1000
     print("[noalloc] water1000 centers [500, 2500)", flush=True)
     a, b = _run_pair(L, wl, wl.structure(), 500, 2000)
@@ -69,18 +70,19 @@ def test_noalloc_refuses_batches_above_the_static_scratch():
     import torch
     from paper_2609_05709_amd.soap import RBF_CODES, SOAP_ECAPACITY, SOAP_OK, load_library
     L = load_library()
-    wl = workloads.WATER1000
+    wl = workloads.CHNO4096
     st = wl.structure()
     z = np.ascontiguousarray(sorted(wl.species), dtype=np.int32)
     h = ctypes.c_void_p()
-    assert L.soap_create(z.ctypes.data, 2, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, RBF_CODES[wl.rbf],
+    assert L.soap_create(z.ctypes.data, len(z), wl.r_cut, wl.n_max, wl.l_max, wl.sigma, RBF_CODES[wl.rbf],
                          ctypes.byref(h)) == SOAP_OK
     pos, Z = torch.from_numpy(st.pos).cuda(), torch.from_numpy(st.Z).cuda()
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     E = ctypes.c_int64()
     assert L.soap_build_neighbors(h, st.n_atoms, pos.data_ptr(), Z.data_ptr(), st.n_atoms, None, ctypes.byref(E),
                                   stream) == SOAP_OK
-    # 3000 centers need 75 MB of scratch: above the 64 MiB array
+    # 4096 centers need 317 MB of float32 coefficient scratch (16 S n L bytes
+    # per center, S = 4, n = 10, L = 121): above the 64 MiB array
     desc = torch.empty(1, device="cuda")
     assert L.soap_derivatives_batch_noalloc(h, 0, st.n_atoms, desc.data_ptr(), desc.data_ptr(), desc.data_ptr(),
                                             stream) == SOAP_ECAPACITY
