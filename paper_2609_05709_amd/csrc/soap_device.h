@@ -1319,12 +1319,17 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
 //      species (SR >= S slots), and adds B_al S_lm over the chunk's edges in
 //      row order (Eq. projection); one harmonic read serves AG products.
 //      Rows are sorted by species, so each species is a contiguous run of the
-//      chunk.  After the row the registers go to the center's coefficient
-//      block, which aliases the staging buffers.
+//      chunk.  After the row the owner of (l = 0, a) of the center's species
+//      adds the on-site term, and the registers go to the center's
+//      coefficient block (its own LDS region).
 // Every coefficient has one owner thread and every sum runs in row order:
 // the results are bitwise repeatable with no ordering protocol.  Then the
-// on-site term, and the power spectrum on the matrix cores (power_tiles,
-// Eq. powerspectrum).  The next center's first chunk of edge vectors is
+// power spectrum on the matrix cores (power_tiles, Eq. powerspectrum).
+// Two barriers per center of one chunk: staging -> projection, and block ->
+// power spectrum.  The block's next writers pass the next center's first
+// barrier, which every wave reaches only after its power spectrum tiles; the
+// staging's next writers come after the block barrier, which every wave
+// reaches only after its projection reads.  The next center's first chunk of edge vectors is
 // gathered into registers before this center's output stores: a load issued
 // after a run of stores waits for all of them.
 // ST: staging precision (the output precision, or double for float64
@@ -1335,8 +1340,8 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
 constexpr int NWC = 4, BSC = 64 * NWC;
 
 // LDS of k_desc.  Float64: K_l, the harmonic normalisations Nt, a'_kl [l][k],
-// betaC [l][n][k], the on-site terms.  Then the larger of the staging
-// buffers and the coefficient block [S][n][L] (float64, after the row).
+// betaC [l][n][k], the on-site terms, the coefficient block [S][n][L].  Then
+// the staging buffers.
 // Staging, at the staging precision: harmonics [lm][W + 1] and radial
 // factors [l][n][W + 1] (edge fastest: the staging lanes, one per edge,
 // write consecutive words), the rows of one l padded to an odd length
@@ -1348,7 +1353,7 @@ __host__ __device__ __forceinline__ size_t desc_lds_doubles(const Params &P, int
     const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n, L = (size_t)P.L;
     const size_t stage = even((L * (W + 1) * sb + 7) / 8) + even((lw * desc_ldl((int)n, W) * sb + 7) / 8) + 16;
     const size_t block = (size_t)P.S * n * L;
-    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + even(stage > block ? stage : block);
+    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + even(block) + even(stage);
 }
 // (lm, group of ag radial indices) tasks per thread
 __host__ __device__ __forceinline__ int desc_tasks(const Params &P, int ag) {
@@ -1370,8 +1375,8 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
     double *apr = cv.take((size_t)lw * n);
     double *bcf = cv.take((size_t)lw * n * n);
     double *c0 = cv.take((size_t)n);
+    double *cb = cv.take((size_t)S * n * L); // [S][n][L], written after the row
     double *stage = cv.take(0);
-    double *cb = stage; // [S][n][L], after the row
     const int WP = W + 1, ldl = desc_ldl(n, W);
     Carver sv{stage};
     ST *Yl = (ST *)sv.take(((size_t)L * WP * SB + 7) / 8);  // [lm][W + 1]
@@ -1427,6 +1432,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
         gather(e0, (int)((e1 - e0) < W ? (e1 - e0) : W));
     };
     fetch();
+    lds_barrier(); // the tables
     while (ci < R.nc) {
         double acc[SR][QT][AG];
 #pragma unroll
@@ -1437,8 +1443,10 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                 for (int g = 0; g < AG; ++g) acc[sr][q][g] = 0.0;
         for (int64_t cs = e0; cs < e1; cs += W) {
             const int nb = (int)((e1 - cs) < W ? (e1 - cs) : W);
-            if (cs != e0) gather(cs, nb); // later chunks of a long row (no stores pending)
-            lds_barrier();                // the tables, the cleared block, the previous chunk read
+            if (cs != e0) { // later chunks of a long row (no stores pending)
+                gather(cs, nb);
+                lds_barrier(); // the previous chunk is read
+            }
             // ---- phase 1: staging, lane = edge, tasks over the waves ----
             if (wave == 0) {
                 // run bounds: the chunk's edges of species below sr (rows are sorted by species)
@@ -1491,7 +1499,15 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                 }
             }
         }
-        lds_barrier(); // the staging region is read: the coefficient block goes over it
+        // on-site term of the center (its species, l = 0), added by the owner
+        // after the row's sum
+#pragma unroll
+        for (int sr = 0; sr < SR; ++sr)
+#pragma unroll
+            for (int q = 0; q < QT; ++q)
+#pragma unroll
+                for (int g = 0; g < AG; ++g)
+                    if (sr == spec_i && lm_q[q] == 0 && ok_q[q] && a_q[q] + g < n) acc[sr][q][g] += c0[a_q[q] + g];
 #pragma unroll
         for (int sr = 0; sr < SR; ++sr)
 #pragma unroll
@@ -1499,10 +1515,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
 #pragma unroll
                 for (int g = 0; g < AG; ++g)
                     if (sr < S && ok_q[q] && a_q[q] + g < n) cb[(sr * n + a_q[q] + g) * L + lm_q[q]] = acc[sr][q][g];
-        lds_barrier();
-        // on-site term of the center (its species, l = 0)
-        if (tid < n) cb[(spec_i * n + tid) * L] += c0[tid];
-        lds_barrier();
+        lds_barrier(); // the block is complete (and every wave is done with the staging)
         // the next center's first chunk goes in before this center's stores
         const int64_t cw = ci;
         ci += stride;
@@ -1512,7 +1525,6 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                               PairIndex{S, n, 1.0f / (float)n}, wave, NWC, lane, Kl);
         if (c_out)
             for (int k = tid; k < SnL; k += BSC) store_out(c_out + cw * SnL + k, cb[k]);
-        lds_barrier(); // cb is read before the next center clears it
     }
 }
 
