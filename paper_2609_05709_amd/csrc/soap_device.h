@@ -1277,6 +1277,7 @@ __global__ __launch_bounds__(BSD, dens_min_waves(MODE, RBF, HI)) void k_density(
 template <typename YT>
 __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const double *__restrict__ Nt, int ldN,
                                             int lw, YT *__restrict__ Y, int ls) {
+#pragma clang fp contract(off) // the roundings of sh_all_fixed, bit for bit
     const double r2 = x * x + y * y + z * z;
     double c = 1.0, s = 0.0; // (x + i y)^m
     for (int m = 0; m < lw; ++m) {
@@ -1284,7 +1285,7 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
         for (int l = m; l < lw; ++l) {
             if (l > m) {
                 const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
-                const double Rn = a * z * R - b * r2 * R1;
+                const double Rn = __builtin_fma(a * z, R, -(b * r2 * R1));
                 R1 = R;
                 R = Rn;
             }
@@ -1297,9 +1298,80 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
                 Y[(o - m) * ls] = (YT)(v * s);
             }
         }
-        const double cn = x * c - y * s;
-        s = x * s + y * c;
+        const double cn = __builtin_fma(x, c, -(y * s));
+        s = __builtin_fma(x, s, y * c);
         c = cn;
+    }
+}
+
+// sh_all_lane for a degree count LW and a row stride LS fixed at compile
+// time (Nt rows of LW + 1 entries): the same recurrence fully unrolled, so
+// that the constants a, b, the table and store offsets and the loop control
+// are resolved at compile time; what stays is the per-lane arithmetic and
+// the LDS traffic.
+template <int LW, int LS, typename YT>
+__device__ __forceinline__ void sh_all_fixed(double x, double y, double z, const double *__restrict__ Nt,
+                                             YT *__restrict__ Y) {
+#pragma clang fp contract(off) // the roundings of sh_all_lane, bit for bit
+    constexpr int ls = LS;
+    constexpr int ldN = LW + 1;
+    // the edge vector passes through an empty asm: the unrolled products
+    // depend only on it, and hoisted out of the caller's task loop they
+    // would all be live across the other tasks
+    __asm__ volatile("" : "+v"(x), "+v"(y), "+v"(z));
+    const double r2 = x * x + y * y + z * z;
+    double c = 1.0, s = 0.0; // (x + i y)^m
+#pragma unroll
+    for (int m = 0; m < LW; ++m) {
+        // an opaque zero offset per column keeps the table reads here (the
+        // table is invariant too)
+        int t0 = 0;
+        __asm__ volatile("" : "+s"(t0));
+        const double *Ntc = Nt + t0;
+        double R1 = 0.0, R = 1.0; // R_{l-1}, R_l
+#pragma unroll
+        for (int l = m; l < LW; ++l) {
+            if (l > m) {
+                const double a = (double)(2 * l - 1), b = (double)((l + m - 1) * (l - m - 1));
+                const double Rn = __builtin_fma(a * z, R, -(b * r2 * R1));
+                R1 = R;
+                R = Rn;
+            }
+            const double v = Ntc[l * ldN + m] * R;
+            const int o = l * l + l;
+            if (m == 0) {
+                Y[o * ls] = (YT)v;
+            } else {
+                Y[(o + m) * ls] = (YT)(v * c);
+                Y[(o - m) * ls] = (YT)(v * s);
+            }
+        }
+        const double cn = __builtin_fma(x, c, -(y * s));
+        s = __builtin_fma(x, s, y * c);
+        c = cn;
+    }
+}
+
+// the solid harmonics of one edge per lane: unrolled for lw <= 8 at the row
+// stride of 64-edge chunks (both uniform, so one case runs per wave), else
+// the loop
+template <typename YT>
+__device__ __forceinline__ void sh_all_any(double x, double y, double z, const double *__restrict__ Nt, int ldN,
+                                           int lw, YT *__restrict__ Y, int ls) {
+    constexpr int LS = 65;
+    if (ls != LS) {
+        sh_all_lane(x, y, z, Nt, ldN, lw, Y, ls);
+        return;
+    }
+    switch (lw) {
+    case 2: sh_all_fixed<2, LS>(x, y, z, Nt, Y); break;
+    case 3: sh_all_fixed<3, LS>(x, y, z, Nt, Y); break;
+    case 4: sh_all_fixed<4, LS>(x, y, z, Nt, Y); break;
+    case 5: sh_all_fixed<5, LS>(x, y, z, Nt, Y); break;
+    case 6: sh_all_fixed<6, LS>(x, y, z, Nt, Y); break;
+    case 7: sh_all_fixed<7, LS>(x, y, z, Nt, Y); break;
+    case 8: sh_all_fixed<8, LS>(x, y, z, Nt, Y); break;
+    default: sh_all_lane(x, y, z, Nt, ldN, lw, Y, ls); break;
     }
 }
 
@@ -1311,7 +1383,7 @@ __device__ __forceinline__ void sh_all_lane(double x, double y, double z, const 
 //   1. staging, lane = edge, split over the waves by task: task l < l_max + 1
 //      is the radial factors of degree l, B_nl = sum_k betaC^l_nk e^{-a'_kl r^2}
 //      (Eq. gto-coefficients); task l_max + 1 is the real solid harmonics
-//      S_lm (sh_all_lane).  Wave w runs tasks w, w + NWC, ...  Every
+//      S_lm (sh_all_any).  Wave w runs tasks w, w + NWC, ...  Every
 //      coefficient read is wave-uniform (the tables sit in LDS, copied once
 //      per workgroup), and every lane works on its own edge;
 //   2. projection, thread = (lm, group of AG radial indices a): each thread
@@ -1460,7 +1532,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                 const double r2 = gx * gx + gy * gy + gz * gz;
                 for (int task = wave; task <= lw; task += NWC) {
                     if (task == lw) {
-                        sh_all_lane(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP);
+                        sh_all_any(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP);
                         continue;
                     }
                     const int l = task;
@@ -1706,7 +1778,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
                 const double r2 = gx * gx + gy * gy + gz * gz;
                 for (int task = wave; task <= lw; task += NWC) {
                     if (task == lw) {
-                        sh_all_lane(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP);
+                        sh_all_any(gx, gy, gz, Nt, ldN, lw, Yl + lane, WP);
                         continue;
                     }
                     const int l = task;
