@@ -422,7 +422,8 @@ int upload_constants(soap_ctx *c) {
             for (int k = 2; k <= l - m; ++k) v /= (long double)k;
             Nt[(size_t)l * ldN + m] = (double)v;
         }
-    // one constant buffer: betaC | betaCa | aprime | remainders of betaC, aprime | G | rq | WN | c0 | Nt | gcoef
+    // one constant buffer: betaC | betaCa | aprime | remainders of betaC, aprime | G | rq | WN | c0 | Nt | gcoef |
+    // exp2 table
     std::vector<double> all;
     size_t o_bc = all.size(); all.insert(all.end(), betaC.begin(), betaC.end());
     size_t o_ba = all.size(); all.insert(all.end(), betaCa.begin(), betaCa.end());
@@ -435,6 +436,10 @@ int upload_constants(soap_ctx *c) {
     size_t o_c0 = all.size(); all.insert(all.end(), c0.begin(), c0.end());
     size_t o_Nt = all.size(); all.insert(all.end(), Nt.begin(), Nt.end());
     size_t o_gc = all.size(); all.insert(all.end(), gcoef.begin(), gcoef.end());
+    double e2t[128];
+    soap_exp2_table64(e2t);
+    while (all.size() % 2) all.push_back(0.0); // 16-byte aligned pairs
+    size_t o_e2 = all.size(); all.insert(all.end(), e2t, e2t + 128);
     hipError_t e;
     if ((e = c->d_const.ensure(all.size() * 8)) != hipSuccess) return hip_fail(c, e, "hipMalloc(constants)");
     if ((e = hipMemcpy(c->d_const.p, all.data(), all.size() * 8, hipMemcpyHostToDevice)) != hipSuccess)
@@ -480,6 +485,7 @@ int upload_constants(soap_ctx *c) {
     P.c0 = d + o_c0;
     P.Nt = d + o_Nt;
     P.gcoef = d + o_gc;
+    P.e2t = d + o_e2;
     P.dtab = c->d_dtab.as<uint32_t>();
     P.tri_lw = (int)c->dtab.size();
     return plan_launches(c);

@@ -160,6 +160,14 @@ void set_err(char *err, int errlen, const char *msg) {
 
 } // namespace
 
+extern "C" void soap_exp2_table64(double *t) {
+    for (int j = 0; j < 64; ++j) {
+        const q128 v = exp2q((q128)j / 64);
+        t[2 * j] = (double)v;
+        t[2 * j + 1] = (double)(v - (q128)t[2 * j]);
+    }
+}
+
 extern "C" int soap_basis_gto(double r_cut, int n_max, int l_max, double sigma, double *betaC, double *betaCa,
                               double *aprime, double *c0, char *err, int errlen, double *betaC_lo, double *betaCa_lo,
                               double *aprime_lo) {

@@ -38,6 +38,11 @@ int soap_basis_poly_laplace(double r_cut, int n_max, double sigma, double *CH, c
 // Real solid-harmonic normalisation N[l][m], 0 <= m <= l, row stride l_max+1.
 void soap_basis_sh_norms(int l_max, double *Nlm);
 
+// 2^(j/64), j = 0..63, as pairs t[2j] = (double)v, t[2j+1] = v - t[2j]
+// (v in 113-bit arithmetic): the table of the exponential of the GTO
+// radial factors.
+void soap_exp2_table64(double *t);
+
 #ifdef __cplusplus
 }
 #endif

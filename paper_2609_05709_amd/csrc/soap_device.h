@@ -156,6 +156,32 @@ __device__ __forceinline__ dd dd_exp_neg(dd x) {
     return dd{ldexp(p.hi, -ki), ldexp(p.lo, -ki)};
 }
 
+// e^{-x} for x >= 0 to about half an ulp, by the table-driven reduction of
+// Tang (ACM TOMS 15(2), 1989): -x = (64 k + j) ln2/64 + r with |r| <=
+// ln2/128, e^{-x} = 2^k 2^{j/64} e^r, 2^{j/64} as (value, remainder) pairs
+// t2[2j], t2[2j+1] (in LDS) and e^r - 1 = r + r^2 (1/2 + r/6) + r^4/24 (1 +
+// r/5 + r^2/30), whose first omitted term is below 3e-20.  The polynomial
+// takes its constants only as multiplicands or inline constants, so no
+// constant is an accumulator that has to be copied first.  Branch-free;
+// below e^-745 the result flushes to zero in the final ldexp.
+__device__ __forceinline__ double exp_neg_tab(double x, const double *__restrict__ t2) {
+#pragma clang fp contract(off)
+    const double y = -x;
+    const double nn = __builtin_rint(y * 92.33248261689366); // 64 / ln 2
+    const int k = (int)nn;
+    double r = __builtin_fma(nn, -0.010830424696249145, y); // ln 2 / 64: leading part
+    r = __builtin_fma(nn, -3.623510646634843e-19, r);       // and the rest
+    const double2 tj = *(const double2 *)(t2 + 2 * (k & 63));
+    const double r2 = r * r;
+    const double A = __builtin_fma(r, 0.16666666666666666, 0.5);
+    double t = __builtin_fma(r, 0.2, 1.0);
+    t = __builtin_fma(r2, 0.03333333333333333, t);
+    const double r4c = r2 * (r2 * 0.041666666666666664);
+    double p = __builtin_fma(r2, A, r);
+    p = __builtin_fma(r4c, t, p);
+    return __builtin_ldexp(tj.x + __builtin_fma(tj.x, p, tj.y), k >> 6);
+}
+
 // ---------------------------------------------------------------------------
 // Real solid harmonics of one column m without gradients and without
 // divisions.  With (C_m + i S_m) = (x + i y)^m, R_m = 1, R_{m+1} = (2m+1) z,
@@ -1412,8 +1438,8 @@ __device__ __forceinline__ void sh_all_any(double x, double y, double z, const d
 constexpr int NWC = 4, BSC = 64 * NWC;
 
 // LDS of k_desc.  Float64: K_l, the harmonic normalisations Nt, a'_kl [l][k],
-// betaC [l][n][k], the on-site terms, the coefficient block [S][n][L].  Then
-// the staging buffers.
+// betaC [l][n][k], the on-site terms, the exponential's table, the
+// coefficient block [S][n][L].  Then the staging buffers.
 // Staging, at the staging precision: harmonics [lm][W + 1] and radial
 // factors [l][n][W + 1] (edge fastest: the staging lanes, one per edge,
 // write consecutive words), the rows of one l padded to an odd length
@@ -1425,7 +1451,7 @@ __host__ __device__ __forceinline__ size_t desc_lds_doubles(const Params &P, int
     const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n, L = (size_t)P.L;
     const size_t stage = even((L * (W + 1) * sb + 7) / 8) + even((lw * desc_ldl((int)n, W) * sb + 7) / 8) + 16;
     const size_t block = (size_t)P.S * n * L;
-    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + even(block) + even(stage);
+    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + 128 + even(block) + even(stage);
 }
 // (lm, group of ag radial indices) tasks per thread
 __host__ __device__ __forceinline__ int desc_tasks(const Params &P, int ag) {
@@ -1447,6 +1473,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
     double *apr = cv.take((size_t)lw * n);
     double *bcf = cv.take((size_t)lw * n * n);
     double *c0 = cv.take((size_t)n);
+    double *e2 = cv.take(128);               // 2^(j/64) pairs of exp_neg_tab
     double *cb = cv.take((size_t)S * n * L); // [S][n][L], written after the row
     double *stage = cv.take(0);
     const int WP = W + 1, ldl = desc_ldl(n, W);
@@ -1459,6 +1486,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
     for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
     for (int k = tid; k < lw * n * n; k += BSC) bcf[k] = P.betaC[k];
     for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
+    for (int k = tid; k < 128; k += BSC) e2[k] = P.e2t[k];
 
     // this thread's projection tasks: (lm, radial group) = (t % L, t / L), t = tid + BSC q
     int lm_q[QT], l_q[QT], a_q[QT], goff[QT][AG];
@@ -1540,7 +1568,10 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                     // coefficient reads past the row multiply zero
                     double ex[NA];
 #pragma unroll
-                    for (int k = 0; k < NA; ++k) ex[k] = k < n ? exp(-apr[l * n + k] * r2) : 0.0;
+                    for (int k = 0; k < NA; ++k) {
+                        const double v = exp_neg_tab(apr[l * n + (k < n ? k : n - 1)] * r2, e2);
+                        ex[k] = k < n ? v : 0.0;
+                    }
                     ST *bo = Bl + (size_t)l * ldl + lane;
                     const double *bc = bcf + (size_t)l * n * n;
                     for (int a = 0; a < n; ++a) {
@@ -1630,7 +1661,7 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
 // and the coefficient block 4 S n L
 __host__ __device__ __forceinline__ size_t djac_table_doubles(const Params &P) {
     const size_t ldN = (size_t)P.lmax + 2, lw = (size_t)P.lmax + 1, n = (size_t)P.n;
-    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n);
+    return 16 + even(ldN * ldN) + even(lw * n) + even(lw * n * n) + even(n) + 128;
 }
 __host__ __device__ __forceinline__ size_t djac_stage_doubles(const Params &P, int W, int sb) {
     const size_t L = (size_t)P.L, lw = (size_t)P.lmax + 1, n = (size_t)P.n;
@@ -1659,6 +1690,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
     double *apr = cv.take((size_t)lw * n);
     double *bcf = cv.take((size_t)lw * n * n);
     double *c0 = cv.take((size_t)n);
+    double *e2 = cv.take(128); // 2^(j/64) pairs of exp_neg_tab
     double *stage = cv.take(0);
     const int WP = W + 1, ldl = desc_ldl(n, W);
     Carver sv{stage};
@@ -1674,6 +1706,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
     for (int k = tid; k < lw * n; k += BSC) apr[k] = P.aprime[k];
     for (int k = tid; k < lw * n * n; k += BSC) bcf[k] = P.betaC[k];
     for (int k = tid; k < n; k += BSC) c0[k] = P.c0[k];
+    for (int k = tid; k < 128; k += BSC) e2[k] = P.e2t[k];
 
     // this thread's tasks: (lm, radial pair) = (t % L, t / L), t = tid + BSC q,
     // and the gradient of its S_lm: gx = g0 Y'_0 + g1 Y'_1, gy = g2 Y'_2 + g3 Y'_3,
@@ -1787,7 +1820,8 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
 #pragma unroll
                     for (int k = 0; k < NA; ++k) {
                         const double ap = apr[l * n + (k < n ? k : n - 1)];
-                        ex[k] = k < n ? exp(-ap * r2) : 0.0;
+                        const double v = exp_neg_tab(ap * r2, e2);
+                        ex[k] = k < n ? v : 0.0;
                         ea[k] = -2.0 * ap * ex[k];
                     }
                     ST *bo = Bl + (size_t)l * ldl + lane, *ho = Hl + (size_t)l * ldl + lane;

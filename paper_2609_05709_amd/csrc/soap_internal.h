@@ -31,6 +31,7 @@ struct Params {
                                // [edge - rad_e0][n][l] (k_radial)
     int64_t rad_e0;            // structure index of the first edge of rad
     const double *c0;          // on-site term [n]
+    const double *e2t;         // GTO: [64][2] 2^(j/64) as (value, remainder) (soap_exp2_table64)
     const double *Nt;          // [lmax+2][lmax+2] N_lm (2m-1)!! / (l-m)! (division-free recurrence)
     const double *gcoef;       // [(l, m >= 0)][4] gradient identities of the harmonics (cA, cB, cC, l | m << 8)
     const uint32_t *dtab;      // [tri_lw] diagonal-pair slots: (n lw + l) | (n' lw + l) << 16, n' >= n
