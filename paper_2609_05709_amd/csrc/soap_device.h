@@ -1844,6 +1844,7 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
 #pragma unroll
             for (int sr = 0; sr < SR; ++sr) {
                 const int lo = run[sr], hi = run[sr + 1];
+#pragma unroll 2
                 for (int e = lo; e < hi; ++e) {
                     const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
                     const double live = geo[4 * e + 3] != 0.0 ? 1.0 : 0.0;
@@ -1866,10 +1867,11 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
                             const int o = a == 0 ? 0 : o1_q[q];
                             const double b = (double)bp[o];
                             const double hs = (double)hp[o] * y;
-                            acc[sr][q][a][0] += b * y;
-                            acc[sr][q][a][1] += hs * rx + b * dx;
-                            acc[sr][q][a][2] += hs * ry + b * dy;
-                            acc[sr][q][a][3] += hs * rz + b * dz;
+                            // two fused steps per component, no separate sum
+                            acc[sr][q][a][0] = __builtin_fma(b, y, acc[sr][q][a][0]);
+                            acc[sr][q][a][1] = __builtin_fma(b, dx, __builtin_fma(hs, rx, acc[sr][q][a][1]));
+                            acc[sr][q][a][2] = __builtin_fma(b, dy, __builtin_fma(hs, ry, acc[sr][q][a][2]));
+                            acc[sr][q][a][3] = __builtin_fma(b, dz, __builtin_fma(hs, rz, acc[sr][q][a][3]));
                         }
                     }
                 }
