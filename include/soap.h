@@ -140,6 +140,12 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
  *              the Jacobian path, 16 / 32 / 64 = the descriptor kernel
  *              whose waves each own whole centers, with at most that many
  *              edges per chunk (the widest that fits on chip);
+ *   "jac_tile" : edges per matrix-core tile of the edge Jacobian kernel (a
+ *              tuning knob, results identical up to rounding order): 0 =
+ *              automatic (default: the most resident workgroups, then the
+ *              widest tile), 1..4 = that width (a width whose LDS does not
+ *              fit leaves the Jacobian path without a plan: the calls that
+ *              need it return SOAP_EINVAL, as for a basis too large);
  *   "djac_tile": kernel choice of the density step of the GTO Jacobian path
  *              (a tuning knob, results identical up to rounding order):
  *              0 = automatic (default), -1 = the shared density kernel and

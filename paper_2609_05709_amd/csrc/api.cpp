@@ -133,6 +133,7 @@ struct soap_ctx {
     hipStream_t aux = nullptr;   // the second stream (default priority)
     std::vector<hipEvent_t> pipe_ev;
     int desc_tile = 0; // option "desc_tile": 0 auto, -1 never k_desc, else edges per chunk
+    int jac_tile = 0;  // option "jac_tile": 0 auto, else edges per matrix-core tile of k_jacobian
     OutPlan out_plan{};
     bool out_rows = true; // option "out_rows": whole-row output kernel where it fits
     int groups[3] = {1, 1, 1};
@@ -302,6 +303,7 @@ int plan_launches(soap_ctx *c) {
     const bool f64 = c->dtype == SOAP_FP64;
     int bestW = 0, bestB = 0;
     for (int W = jacobian_max_w(); W >= 1; --W) {
+        if (c->jac_tile > 0 && W != c->jac_tile) continue;
         const size_t lds = jacobian_lds_bytes(P, W, st64);
         if (lds > LDS_HARD_LIMIT) continue;
         const int b = jacobian_blocks_per_cu(f64, ar64, P.rbf, P.n, P.lmax + 1, lds);
@@ -676,6 +678,12 @@ int soap_set_option(soap_ctx *c, const char *key, int64_t value) {
         c->desc_tile = (int)value;
         return plan_launches(c);
     }
+    if (!std::strcmp(key, "jac_tile")) {
+        if (value < 0 || value > jacobian_max_w())
+            return fail(c, SOAP_EINVAL, "jac_tile must be in 0..%d", jacobian_max_w());
+        c->jac_tile = (int)value;
+        return plan_launches(c);
+    }
     if (!std::strcmp(key, "out_rows")) {
         if (value != 0 && value != 1) return fail(c, SOAP_EINVAL, "out_rows must be 0 or 1");
         c->out_rows = value == 1;
@@ -705,6 +713,7 @@ int soap_get_option(const soap_ctx *c, const char *key, int64_t *value) {
                {"quad_n", c->Q},
                {"timing", c->timing ? 1 : 0},
                {"desc_tile", c->desc_tile},
+               {"jac_tile", c->jac_tile},
                {"djac_tile", c->djac_tile},
                {"djs_tile", c->djs_tile},
                {"pipeline", c->pipe_chunks},

@@ -268,6 +268,49 @@ def test_jacobian_density_kernel_chunk_widths(dtype, case):
 
 
 @pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_jacobian_kernel_tile_widths(dtype):
+    """The edge Jacobian kernel at every matrix-core tile width that fits
+    (option "jac_tile"): every block of the 64-water cluster against the
+    oracle, and the same bits at every width (a tile's rows are the
+    (component, edge) pairs of its edges, each summed on its own)."""
+    import torch
+    from paper_2609_05709_amd.soap import Soap
+    wl, st = workloads.WATER64, structure(workloads.WATER64)
+    idx = np.arange(st.n_atoms)
+    ref = oracle_for(wl).compute(st.pos64, st.Z, centers=idx, jacobian=True)
+    tdt = torch.float64 if dtype == "float64" else torch.float32
+    pos = torch.from_numpy(st.pos.astype(np.float64) if dtype == "float64" else st.pos).to("cuda", tdt)
+    Z = torch.from_numpy(st.Z).cuda()
+    first, ran = None, 0
+    for tile in (1, 2, 3, 4):
+        sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf, dtype=dtype)
+        sp._check(sp._L.soap_set_option(sp._h, b"jac_tile", tile))
+        if sp.get_option("jacobian_tile") != tile:
+            sp.close()  # this width does not fit on chip
+            continue
+        sp.build_neighbors(pos, Z)
+        d, je, js = sp.derivatives()
+        row, cols = sp.neighbors()
+        torch.cuda.synchronize()
+        g = dict(row=row.cpu().numpy(), cols=cols.cpu().numpy(), fmaps=[sp.feature_map(k) for k in range(len(wl.species))],
+                 jedge={}, jself={})
+        for c in idx:
+            r0, r1 = int(g["row"][c]), int(g["row"][c + 1])
+            g["jedge"][int(c)] = je[r0:r1].cpu().double().numpy()
+            g["jself"][int(c)] = js[int(c)].cpu().double().numpy()
+        ej = jacobian_errors(g, ref, st, wl.species, idx.tolist(), idx)
+        print(f"[jac] {wl.name} {dtype} tile {tile}: jac {ej:.2e}", flush=True)
+        assert ej < TOL[dtype]
+        ran += 1
+        if first is None:
+            first = je.clone()
+        else:
+            assert torch.equal(je, first)
+        sp.close()
+    assert ran >= 2
+
+
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
 @pytest.mark.parametrize("case", ["chno_poly_n10l10", "chno_poly_n6l8", "water_poly_n12l12"])
 def test_output_kernel_rows_and_groups(dtype, case):
     """The output kernel of the Jacobian path (power spectrum and center block
