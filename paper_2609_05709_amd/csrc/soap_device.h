@@ -1574,11 +1574,23 @@ __global__ __launch_bounds__(BSC) void k_desc(Params P, Rows R, const PosT *__re
                     }
                     ST *bo = Bl + (size_t)l * ldl + lane;
                     const double *bc = bcf + (size_t)l * n * n;
-                    for (int a = 0; a < n; ++a) {
-                        double b = 0.0;
+                    if (n == NA) {
+                        // unrolled: compile-time coefficient offsets and NA
+                        // independent sums (the same sums, in the same order)
 #pragma unroll
-                        for (int k = 0; k < NA; ++k) b += bc[a * n + (k < n ? k : n - 1)] * ex[k];
-                        bo[a * WP] = (ST)b;
+                        for (int a = 0; a < NA; ++a) {
+                            double b = 0.0;
+#pragma unroll
+                            for (int k = 0; k < NA; ++k) b += bc[a * NA + k] * ex[k];
+                            bo[a * WP] = (ST)b;
+                        }
+                    } else {
+                        for (int a = 0; a < n; ++a) {
+                            double b = 0.0;
+#pragma unroll
+                            for (int k = 0; k < NA; ++k) b += bc[a * n + (k < n ? k : n - 1)] * ex[k];
+                            bo[a * WP] = (ST)b;
+                        }
                     }
                 }
             }
