@@ -1856,7 +1856,11 @@ __global__ __launch_bounds__(BSC) void k_djac(Params P, Rows R, const PosT *__re
 #pragma unroll
             for (int sr = 0; sr < SR; ++sr) {
                 const int lo = run[sr], hi = run[sr + 1];
-#pragma unroll 2
+                // two edges per iteration at one task per thread; at two
+                // tasks the second edge's operands would cost the kernel its
+                // second wave per SIMD
+                constexpr int EU = QT == 1 ? 2 : 1;
+#pragma unroll EU
                 for (int e = lo; e < hi; ++e) {
                     const double rx = geo[4 * e], ry = geo[4 * e + 1], rz = geo[4 * e + 2];
                     const double live = geo[4 * e + 3] != 0.0 ? 1.0 : 0.0;
