@@ -299,14 +299,20 @@ int plan_launches(soap_ctx *c) {
     }
     c->out_ok = plan_outputs(P, c->dtype == SOAP_FP64, st64, c->out_rows, &c->out_plan) == 0;
     // Jacobian kernel: W edges per wave tile.  The most resident waves per CU
-    // first (latency hiding for its LDS-bound staging), then the widest tile.
+    // first (latency hiding for its LDS-bound staging), then the widest tile;
+    // a one-edge tile fills a quarter of the matrix-core rows, so at two or
+    // more workgroups per CU a wider tile counts double (measured: two
+    // workgroups of two-edge tiles beat three of one-edge tiles, GTO n4 l12
+    // 0.76 against 1.05 ms per Jacobian launch; one workgroup of two-edge
+    // tiles loses to two of one-edge tiles, CHNO 0.91 against 0.81 ms)
     const bool f64 = c->dtype == SOAP_FP64;
     int bestW = 0, bestB = 0;
     for (int W = jacobian_max_w(); W >= 1; --W) {
         if (c->jac_tile > 0 && W != c->jac_tile) continue;
         const size_t lds = jacobian_lds_bytes(P, W, st64);
         if (lds > LDS_HARD_LIMIT) continue;
-        const int b = jacobian_blocks_per_cu(f64, ar64, P.rbf, P.n, P.lmax + 1, lds);
+        int b = jacobian_blocks_per_cu(f64, ar64, P.rbf, P.n, P.lmax + 1, lds);
+        if (W >= 2 && b >= 2) b *= 2;
         if (b > bestB) {
             bestB = b;
             bestW = W;
