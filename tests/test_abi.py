@@ -39,6 +39,22 @@ def test_python_binding_declares_abi(lib):
         assert getattr(L, n).restype is not None or n == "soap_destroy"
 
 
+def test_host_exp2_table(lib):
+    """The table of the GTO kernels' exponential: 2^(j/64) as a double and
+    its remainder, against 50-digit values (the double correctly rounded,
+    the pair exact to ~2^-106 relative)."""
+    t = np.empty(128)
+    f = lib.soap_exp2_table64
+    f.argtypes = [ctypes.c_void_p]
+    f.restype = None
+    f(t.ctypes.data)
+    with mp.workdps(50):
+        for j in range(64):
+            v = mp.power(2, mp.mpf(j) / 64)
+            assert t[2 * j] == float(v), j
+            assert abs((mp.mpf(t[2 * j]) + mp.mpf(t[2 * j + 1]) - v) / v) < mp.mpf(2) ** -104, j
+
+
 @pytest.mark.parametrize("r_cut,n_max,l_max,sigma", [(5.0, 4, 4, 0.5), (6.0, 8, 6, 0.5), (6.0, 12, 12, 0.5),
                                                      (6.0, 1, 2, 0.4)])
 def test_host_gto_constants_match_oracle(lib, r_cut, n_max, l_max, sigma):
