@@ -843,10 +843,38 @@ __device__ __forceinline__ void lane_pair_index(const PairIndex &pq, int Sn, int
     }
 }
 
+// qtab (may be NULL): the lanes' pair indices per tile pair, [tile pair][lane][4]
+// (pair_index_table), read instead of computed per item
+// The pair indices of every lane for every tile pair (ti <= tj, in the order
+// power_tiles deals them), [tile pair][lane][4] as shorts (pair indices are
+// below Sn (Sn + 1) / 2, which fits for the Sn <= 80 the table is kept for),
+// built by all threads.
+__device__ __forceinline__ void pair_index_table(const PairIndex &pq, int Sn, short *__restrict__ qtab, int tid,
+                                                 int nthreads) {
+    const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
+    for (int k = tid; k < 64 * ntp; k += nthreads) {
+        const int tpi = k >> 6, ln = k & 63;
+        int tp = tpi, ti = 0;
+        while (tp >= ntile - ti) {
+            tp -= ntile - ti;
+            ++ti;
+        }
+        int q[4];
+        lane_pair_index(pq, Sn, ti, ti + tp, ln >> 4, ln & 15, q);
+        short4 v;
+        v.x = (short)q[0];
+        v.y = (short)q[1];
+        v.z = (short)q[2];
+        v.w = (short)q[3];
+        *(short4 *)(qtab + 4 * k) = v;
+    }
+}
+
 template <typename OutT, typename CT = double>
 __device__ __forceinline__ void power_tiles(const CoefView<CT> cv, int comp, int Sn, int lm0, int lg0, int lgc,
                                             OutT *__restrict__ row, int ldq, int lbase, const PairIndex pq,
-                                            int wave, int nw, int lane, const double *__restrict__ Kl) {
+                                            int wave, int nw, int lane, const double *__restrict__ Kl,
+                                            const short *__restrict__ qtab = nullptr) {
     const int ntile = (Sn + 15) >> 4, ntp = ntile * (ntile + 1) / 2;
     const int nitem = lgc * ntp;
     const int ro = lane & 15, kk = lane >> 4;
@@ -860,13 +888,24 @@ __device__ __forceinline__ void power_tiles(const CoefView<CT> cv, int comp, int
         if (pos >= nitem) break;
         const int item = nitem - 1 - pos;
         const int lc = item / ntp, l = lg0 + lc;
-        int tp = item - lc * ntp, ti = 0;
+        const int tpi = item - lc * ntp;
+        int tp = tpi, ti = 0;
         while (tp >= ntile - ti) {
             tp -= ntile - ti;
             ++ti;
         }
         const int tj = ti + tp;
-        if (ntp > 1) lane_pair_index(pq, Sn, ti, tj, kk, ro, q);
+        if (ntp > 1) {
+            if (qtab) {
+                const short4 qs = *(const short4 *)(qtab + 4 * (64 * tpi + lane));
+                q[0] = qs.x;
+                q[1] = qs.y;
+                q[2] = qs.z;
+                q[3] = qs.w;
+            } else {
+                lane_pair_index(pq, Sn, ti, tj, kk, ro, q);
+            }
+        }
         const int ua = 16 * ti + ro, vb = 16 * tj + ro; // A row, B column of this lane
         const bool uok = ua < Sn, vok = vb < Sn;
         const int oa = (uok ? ua : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
@@ -2330,9 +2369,17 @@ constexpr int NWO = 8, BSO2 = 64 * NWO;
 constexpr int OUT_PF = 24; // prefetched doubles per thread: one slab of at most OUT_PF * BSO2
 
 // sb: bytes per staged coefficient (ST)
+// the pair-index table of k_outputs_rows, in doubles: kept for up to five 16-row
+// tiles (S n <= 80: at most 15 tile pairs, 7.5 KB), else the indices are
+// computed per item
+__host__ __device__ __forceinline__ size_t outputs_qtab_doubles(const Params &P) {
+    const size_t ntile = ((size_t)P.S * P.n + 15) / 16, ntp = ntile * (ntile + 1) / 2;
+    return (ntile > 1 && ntile <= 5) ? ntp * 64 : 0;
+}
 __host__ __device__ __forceinline__ size_t outputs_rows_doubles(const Params &P, int out_bytes, int sb) {
     const size_t slab = (size_t)P.L * P.S * P.n;
-    return 2 * even((slab * sb + 7) / 8) + even(((size_t)P.F * out_bytes + 7) / 8);
+    // c, one component of D, a row, the pair-index table
+    return 2 * even((slab * sb + 7) / 8) + even(((size_t)P.F * out_bytes + 7) / 8) + outputs_qtab_doubles(P);
 }
 
 // ST: precision of the staged c and D (float64, or float32 in the mixed mode;
@@ -2349,6 +2396,9 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const ST *__res
     if (tid < 16) Kl[tid] = M_PI * sqrt(8.0 / (double)(2 * tid + 1));
     ST *Xc = (ST *)smem, *Xd = (ST *)(smem + sstr);
     OutT *row = (OutT *)(smem + 2 * sstr);
+    const int rstr = (int)even(((size_t)F * sizeof(OutT) + 7) / 8);
+    // [tile pair][lane][4], built below, read after the barrier (NULL: computed per item)
+    short *qtab = outputs_qtab_doubles(P) ? (short *)(smem + 2 * sstr + rstr) : nullptr;
     const ST *src = scratch + ci * 4 * (size_t)slab; // [c, Dx, Dy, Dz][lm][species n]
     // c and D_x, eight loads in flight per thread
     for (int k0 = 0; k0 < 2 * slab; k0 += 8 * BSO2) {
@@ -2364,8 +2414,9 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const ST *__res
             if (k < 2 * slab) (k < slab ? Xc[k] : Xd[k - slab]) = (ST)v[u];
         }
     }
-    lds_barrier();
     const PairIndex pq{S, n, 1.0f / (float)n};
+    if (qtab) pair_index_table(pq, Sn, qtab, tid, BSO2);
+    lds_barrier();
     for (int p = 0; p < 4; ++p) {
         ST pf[OUT_PF];
         if (p == 1 || p == 2) {
@@ -2376,7 +2427,8 @@ __global__ __launch_bounds__(BSO2) void k_outputs_rows(Params P, const ST *__res
                 pf[u] = nx[k < slab ? k : 0];
             }
         }
-        power_tiles<OutT, ST>(CoefView<ST>{Xc, Xd, 1, Sn}, p - 1, Sn, 0, 0, lw, row, lw, 0, pq, wave, NWO, lane, Kl);
+        power_tiles<OutT, ST>(CoefView<ST>{Xc, Xd, 1, Sn}, p - 1, Sn, 0, 0, lw, row, lw, 0, pq, wave, NWO, lane, Kl,
+                              qtab);
         lds_barrier(); // the row is complete; D of this pass is read
         OutT *dst = p == 0 ? desc + ci * F : jself + (ci * 3 + (p - 1)) * F;
         for (int f = tid; f < F; f += BSO2) dst[f] = row[f];
