@@ -911,15 +911,24 @@ __device__ __forceinline__ void power_tiles(const CoefView<CT> cv, int comp, int
         const int oa = (uok ? ua : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
         const int ob = (vok ? vb : 0) * cv.ldu + (l * l - lm0) * cv.ldm;
         dbl4 acc = {0.0, 0.0, 0.0, 0.0};
-        for (int ch = 0; ch < (l >> 1) + 1; ++ch) {
-            const int m = 4 * ch + kk;
-            const bool mok = m <= 2 * l;
-            const int mo = (mok ? m : 0) * cv.ldm;
-            const double ca = (double)cv.C[oa + mo], cb = (double)cv.C[ob + mo];
-            const double xa = (mok && uok) ? ca : 0.0, xb = (mok && vok) ? cb : 0.0;
-            if (comp < 0) {
+        // one loop per kind (comp is uniform): a branch inside the chain made
+        // the two kinds' accumulators meet in copies at every chunk
+        if (comp < 0) {
+            for (int ch = 0; ch < (l >> 1) + 1; ++ch) {
+                const int m = 4 * ch + kk;
+                const bool mok = m <= 2 * l;
+                const int mo = (mok ? m : 0) * cv.ldm;
+                const double ca = (double)cv.C[oa + mo], cb = (double)cv.C[ob + mo];
+                const double xa = (mok && uok) ? ca : 0.0, xb = (mok && vok) ? cb : 0.0;
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, xb, acc, 0, 0, 0);
-            } else {
+            }
+        } else {
+            for (int ch = 0; ch < (l >> 1) + 1; ++ch) {
+                const int m = 4 * ch + kk;
+                const bool mok = m <= 2 * l;
+                const int mo = (mok ? m : 0) * cv.ldm;
+                const double ca = (double)cv.C[oa + mo], cb = (double)cv.C[ob + mo];
+                const double xa = (mok && uok) ? ca : 0.0, xb = (mok && vok) ? cb : 0.0;
                 const double da = (double)cv.D[oa + mo], db = (double)cv.D[ob + mo];
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64((mok && uok) ? da : 0.0, xb, acc, 0, 0, 0);
                 acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, (mok && vok) ? db : 0.0, acc, 0, 0, 0);
