@@ -163,10 +163,11 @@ __device__ __forceinline__ dd dd_exp_neg(dd x) {
 // r/5 + r^2/30), whose first omitted term is below 3e-20.  The polynomial
 // takes its constants only as multiplicands or inline constants, so no
 // constant is an accumulator that has to be copied first.  Branch-free;
-// below e^-745 the result flushes to zero in the final ldexp.
+// below e^-745 the result flushes to zero in the final ldexp (arguments past
+// 746 are clamped there first, which keeps the integer part in range).
 __device__ __forceinline__ double exp_neg_tab(double x, const double *__restrict__ t2) {
 #pragma clang fp contract(off)
-    const double y = -x;
+    const double y = -__builtin_fmin(x, 746.0);
     const double nn = __builtin_rint(y * 92.33248261689366); // 64 / ln 2
     const int k = (int)nn;
     double r = __builtin_fma(nn, -0.010830424696249145, y); // ln 2 / 64: leading part
