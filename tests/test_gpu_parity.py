@@ -174,8 +174,14 @@ def test_fuzz_small_structures(seed):
     wl = workloads.Workload(f"fuzz{seed}", species, rbf, 4.5, float(rng.uniform(0.3, 0.6)), n_max, l_max, True,
                             ("none",))
     _structs[wl.make] = st
+    ref_d = oracle_for(wl).compute(st.pos64, st.Z)["desc"]
     for dtype in ("float32", "float64"):
         full_check(wl, dtype)
+        # the descriptor-only path (its own kernels) on the same structure
+        d = gpu_run(wl, st, dtype, jacobian=False)
+        ed = row_errors(d["desc"], ref_d).max()
+        print(f"[parity] {wl.name} {dtype}: descriptor path {ed:.2e}", flush=True)
+        assert ed < TOL[dtype]
     _structs.pop(wl.make)
 
 
