@@ -129,6 +129,25 @@ def test_neighbors_diagonal_far_from_origin():
         check_rows(g, st, rc, np.arange(st.n_atoms), wl.species)
 
 
+@pytest.mark.parametrize("n_atoms,centers", [(1, None), (63, None), (64, None), (65, [64, 0, 3, 3]), (200, None),
+                                              (257, None), (256, list(range(255, -1, -1))),
+                                              (40, list(range(40)) * 7)])
+@pytest.mark.parametrize("dtype", ["float32", "float64"])
+def test_rows_at_wave_and_size_boundaries(n_atoms, centers, dtype):
+    """Neighbour rows of structures one atom either side of a wave's 64
+    lanes, with center lists in reverse order, repeated and longer than the
+    structure, against the brute-force search; the descriptor of the listed
+    centers against the oracle."""
+    wl = _wl(species=(1, 6, 8), r_cut=4.5, n_max=2, l_max=2)
+    st = workloads.random_small(n_atoms, 100 + n_atoms, max(2.0, (n_atoms / 0.42) ** (1 / 3)), species=(1, 6, 8))
+    g = gpu_run(wl, st, dtype, centers=centers, jacobian=False)
+    cen = np.arange(st.n_atoms) if centers is None else np.asarray(centers)
+    check_rows(g, st, wl.r_cut, cen, wl.species)
+    o = oracle.OracleSOAP(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    ref = o.compute(st.pos64, st.Z, centers=cen, jacobian=False)
+    assert row_errors(g["desc"], ref["desc"]).max() < TOL[dtype]
+
+
 def test_unknown_species_is_an_error():
     import torch
     from paper_2609_05709_amd.soap import SOAP_ESPECIES, Soap, SoapError
