@@ -255,8 +255,13 @@ int soap_feature_map(const soap_ctx *ctx, int32_t species_index, int32_t *out);
  *   n_edges_out : host; receives E = sum_i |N(i)|.
  * Rows are ordered by species index (sorted Z), then by ascending atom
  * index.  The context keeps the rows and the input pointers for the calls
- * below.  This call synchronises `stream` once (to read E and device-side
- * checks).  Errors: SOAP_EINVAL, SOAP_ESPECIES (unknown Z),
+ * below.  This call waits once for the device (to read E and the results of
+ * the device-side checks): for up to 16384 centers it waits for a record
+ * that the search writes to pinned host memory as soon as E is known, so the
+ * last rows may still be in flight on `stream` when it returns (work queued
+ * on `stream` afterwards sees them); with more centers, or when the stream
+ * has not reached the search within 20 ms, it synchronises `stream`.
+ * Errors: SOAP_EINVAL, SOAP_ESPECIES (unknown Z),
  * SOAP_ECAPACITY (a row longer than SOAP_MAX_DEGREE), SOAP_ENOMEM, SOAP_EHIP.
  *
  * With a periodic cell (soap_set_cell) the edges run over periodic images:

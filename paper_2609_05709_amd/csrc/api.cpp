@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -106,6 +107,12 @@ struct soap_ctx {
     DevBuf b_img_lohi, b_img_cnt, b_img_start, b_pos_ext, b_Z_ext, b_map_atom, b_map_img, b_iota;
     WorkBase work_epoch{}; // per l-group: density work-counter increments since the counters were zeroed
     int32_t *h_flags = nullptr; // pinned: [0..3] flags, int64 E at byte 16, int64 image count at byte 32
+    // pinned coherent record that the neighbour search's degree scan writes
+    // (error bits | largest degree << 32, rows above TCAP, E, sequence number)
+    int64_t *h_rec = nullptr, *d_rec = nullptr;
+    int64_t rec_seq = 0;
+    int64_t *h_rowp = nullptr; // pinned staging of the row offsets (polynomial quadrature)
+    size_t h_rowp_cap = 0;     // entries
     // state of the last neighbour build
     bool have_rows = false;
     int64_t n_atoms = 0, nc = 0, E = 0;
@@ -620,6 +627,11 @@ int soap_create(const int32_t *species_Z, int32_t n_species, double r_cut, int32
     hipError_t e = hipGetDevice(&c->device);
     if (e == hipSuccess) e = set_lds_limits();
     if (e == hipSuccess) e = hipHostMalloc((void **)&c->h_flags, 64, hipHostMallocDefault);
+    if (e == hipSuccess) e = hipHostMalloc((void **)&c->h_rec, 64, hipHostMallocCoherent);
+    if (e == hipSuccess) {
+        std::memset(c->h_rec, 0, 64);
+        e = hipHostGetDevicePointer((void **)&c->d_rec, c->h_rec, 0);
+    }
     if (e == hipSuccess) e = static_scratch(c->device, &c->static_scratch);
     if (e != hipSuccess) {
         g_create_error = std::string("HIP setup failed: ") + hipGetErrorString(e);
@@ -814,8 +826,10 @@ static int build_rows(soap_ctx *c, int64_t n_atoms, int64_t center_bound, const 
     w.slots = c->b_slots.as<int32_t>();
     w.scan_tmp = c->b_scan.as<int64_t>();
     int64_t *row = c->b_row.as<int64_t>();
+    const int64_t seq = ++c->rec_seq;
+    bool rec_written = false;
     e = nbr_phase1(w, n_atoms, center_bound, pos_dev, f64, Z_dev, c->d_lut.as<int8_t>(), c->b_spec.as<uint8_t>(),
-                   n_centers, centers_dev, c->r_cut, row, st);
+                   n_centers, centers_dev, c->r_cut, row, st, c->d_rec, seq, &rec_written);
     if (e != hipSuccess) return hip_fail(c, e, "neighbour search");
     c->work_epoch = WorkBase{}; // the density work counters were zeroed with the flags
     // With a rows buffer from an earlier build, the short rows are packed
@@ -825,13 +839,63 @@ static int build_rows(soap_ctx *c, int64_t n_atoms, int64_t center_bound, const 
     const int64_t cap0 = c->b_cols.p ? (int64_t)(c->b_cols.cap / 4) : 0;
     if (cap0 > 0 && (e = nbr_pack(w, n_centers, row, c->b_cols.as<int32_t>(), cap0, st)) != hipSuccess)
         return hip_fail(c, e, "neighbour rows");
-    // flags[0..3] and the total degree (int64 at flags + 4) in one copy
-    if ((e = hipMemcpyAsync(c->h_flags, w.flags, 24, hipMemcpyDeviceToHost, st)) != hipSuccess ||
-        (e = hipStreamSynchronize(st)) != hipSuccess)
-        return hip_fail(c, e, "neighbour search (sync)");
-    const int32_t bad = c->h_flags[0], maxdeg = c->h_flags[1], n_long = c->h_flags[2];
+    // The polynomial quadrature's radial pass places each call's edges from a
+    // host copy of the row offsets: copied with the flags, one synchronisation.
+    c->h_row.clear();
+    const bool rows_to_host = c->rbf == SOAP_RBF_POLYNOMIAL;
+    if (rows_to_host) {
+        const size_t m = (size_t)n_centers + 1;
+        if (m > c->h_rowp_cap) {
+            if (c->h_rowp) (void)hipHostFree(c->h_rowp);
+            c->h_rowp = nullptr;
+            c->h_rowp_cap = 0;
+            if ((e = hipHostMalloc((void **)&c->h_rowp, 8 * m, hipHostMallocDefault)) != hipSuccess)
+                return hip_fail(c, e, "hipHostMalloc(row offsets)");
+            c->h_rowp_cap = m;
+        }
+        if ((e = hipMemcpyAsync(c->h_rowp, row, 8 * m, hipMemcpyDeviceToHost, st)) != hipSuccess)
+            return hip_fail(c, e, "neighbour row offsets");
+    }
+    // The degree scan's host record when it writes one: waiting for its
+    // sequence number returns as soon as the scan has ended (the short rows may
+    // still be packing), where a copy and a stream synchronisation would wait
+    // for a copy launch and the end of the stream.  After a bounded spin the
+    // stream is synchronised instead (work queued before this call).
+    bool have_rec = false;
+    if (rec_written && !rows_to_host) {
+        const auto t0 = std::chrono::steady_clock::now();
+        for (;;) {
+            if (__atomic_load_n(c->h_rec + 3, __ATOMIC_ACQUIRE) == seq) {
+                have_rec = true;
+                break;
+            }
+            if (std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) {
+                if ((e = hipStreamSynchronize(st)) != hipSuccess) return hip_fail(c, e, "neighbour search (sync)");
+                have_rec = __atomic_load_n(c->h_rec + 3, __ATOMIC_ACQUIRE) == seq;
+                break;
+            }
+            __builtin_ia32_pause();
+        }
+    }
+    int32_t bad, maxdeg, n_long;
     int64_t E;
-    std::memcpy(&E, c->h_flags + 4, 8);
+    if (have_rec) {
+        const uint64_t r0 = (uint64_t)c->h_rec[0];
+        bad = (int32_t)(uint32_t)r0;
+        maxdeg = (int32_t)(uint32_t)(r0 >> 32);
+        n_long = (int32_t)c->h_rec[1];
+        E = c->h_rec[2];
+    } else {
+        // flags[0..3] and the total degree (int64 at flags + 4) in one copy
+        if ((e = hipMemcpyAsync(c->h_flags, w.flags, 24, hipMemcpyDeviceToHost, st)) != hipSuccess ||
+            (e = hipStreamSynchronize(st)) != hipSuccess)
+            return hip_fail(c, e, "neighbour search (sync)");
+        bad = c->h_flags[0];
+        maxdeg = c->h_flags[1];
+        n_long = c->h_flags[2];
+        std::memcpy(&E, c->h_flags + 4, 8);
+    }
+    if (rows_to_host) c->h_row.assign(c->h_rowp, c->h_rowp + n_centers + 1);
     if (bad & 1) return fail(c, SOAP_ESPECIES, "an atomic number is not in the species list");
     if (bad & 2) return fail(c, SOAP_EINVAL, "a center index is out of range");
     if (maxdeg > MAX_DEGREE)
@@ -915,13 +979,6 @@ int soap_build_neighbors(soap_ctx *c, int64_t n_atoms, const void *pos_dev, cons
     }
     if ((rc = build_rows(c, n_rows_atoms, n_atoms, pos_rows, Z_rows, n_centers, cen_rows, &E, st)) != SOAP_OK)
         return rc;
-    c->h_row.clear();
-    if (c->rbf == SOAP_RBF_POLYNOMIAL) { // the radial pass sizes and places each call's edges from it
-        c->h_row.resize((size_t)n_centers + 1);
-        hipError_t e = hipMemcpyAsync(c->h_row.data(), c->b_row.p, 8 * c->h_row.size(), hipMemcpyDeviceToHost, st);
-        if (e == hipSuccess) e = hipStreamSynchronize(st);
-        if (e != hipSuccess) return hip_fail(c, e, "neighbour row offsets");
-    }
     timer.done();
     c->have_rows = true;
     c->n_atoms = n_atoms;
@@ -1421,6 +1478,8 @@ void soap_destroy(soap_ctx *c) {
                       &c->b_pos_ext, &c->b_Z_ext, &c->b_map_atom, &c->b_map_img, &c->b_iota})
         b->release();
     if (c->h_flags) (void)hipHostFree(c->h_flags);
+    if (c->h_rec) (void)hipHostFree(c->h_rec);
+    if (c->h_rowp) (void)hipHostFree(c->h_rowp);
     for (hipEvent_t e : c->pipe_ev) (void)hipEventDestroy(e);
     if (c->aux) (void)hipStreamDestroy(c->aux);
     for (auto &r : c->recs) {

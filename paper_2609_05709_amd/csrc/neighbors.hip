@@ -356,9 +356,10 @@ __device__ __forceinline__ int64_t block_exclusive(int64_t s, int64_t *part, int
 }
 
 // Largest value and number of values above TCAP of the workgroup's inputs,
-// folded into stats[0] (max) and stats[1] (count) with one atomic each.
+// folded into stats[0] (max) and stats[1] (count) with one atomic each; thread
+// 0 also gets the workgroup's pair as the return value.
 template <int BS>
-__device__ __forceinline__ void block_degree_stats(int vmax, int over, int *red, int32_t *__restrict__ stats) {
+__device__ __forceinline__ int2 block_degree_stats(int vmax, int over, int *red, int32_t *__restrict__ stats) {
     for (int off = 32; off > 0; off >>= 1) {
         vmax = max(vmax, __shfl_down(vmax, off, 64));
         over += __shfl_down(over, off, 64);
@@ -376,6 +377,7 @@ __device__ __forceinline__ void block_degree_stats(int vmax, int over, int *red,
         atomicMax(&stats[0], vmax);
         atomicAdd(&stats[1], over);
     }
+    return make_int2(vmax, over);
 }
 
 // one workgroup for n <= SMALL_MAX; total also to *total_copy and degree
@@ -385,10 +387,18 @@ __device__ __forceinline__ void block_degree_stats(int vmax, int over, int *red,
 // wave totals.  The wave-total array alternates between rounds, so a round's
 // two barriers also order the previous round's reads of it.  All loads are
 // issued first; the cross-lane shuffles set the time, so rounds are few.
+//
+// rec (may be NULL; needs stats): a host-visible record that thread 0 writes
+// last, once the scan and the statistics are final: [0] err[0] | stats[0] <<
+// 32, [1] stats[1], [2] the total, then [3] = seq with a system-scope release,
+// so that the host can wait for this value instead of synchronising the
+// stream.
 template <typename OutT>
 __global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const int32_t *__restrict__ in,
                                                               OutT *__restrict__ out, int64_t *__restrict__ total_copy,
-                                                              int32_t *__restrict__ stats) {
+                                                              int32_t *__restrict__ stats,
+                                                              const int32_t *__restrict__ err, int64_t *rec,
+                                                              int64_t seq) {
     constexpr int NW = SMALL_THREADS / 64, VEC = 4, ROUND = SMALL_THREADS * VEC, MAXR = SMALL_MAX / ROUND;
     __shared__ int64_t part[2][NW];
     __shared__ int red[2 * NW];
@@ -449,10 +459,20 @@ __global__ __launch_bounds__(SMALL_THREADS) void k_scan_small(int64_t n, const i
         }
         carry += part[buf][NW - 1];
     }
-    if (stats) block_degree_stats<SMALL_THREADS>(vmax, over, red, stats);
+    int2 ws = make_int2(0, 0);
+    if (stats) ws = block_degree_stats<SMALL_THREADS>(vmax, over, red, stats);
     if (threadIdx.x == 0) {
         out[n] = (OutT)carry;
         if (total_copy) *total_copy = carry;
+        if (rec) {
+            // one workgroup, and the caller zeroed stats: the workgroup's pair
+            // is the final value; err was set by earlier kernels
+            const int32_t e0 = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            rec[0] = (int64_t)(uint32_t)e0 | ((int64_t)(uint32_t)ws.x << 32);
+            rec[1] = ws.y;
+            rec[2] = carry;
+            __hip_atomic_store(rec + 3, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
     }
 }
 
@@ -514,11 +534,18 @@ __global__ void k_scan_add(int64_t n, OutT *__restrict__ out, const int64_t *__r
 
 // stats (may be NULL): [0] max of in, [1] count of in > TCAP, both folded in
 // with atomics (the caller zeroes them)
+// rec, err, seq: k_scan_small's host record, written only by the one-workgroup
+// scan (n <= SMALL_MAX); *rec_written says whether it will be
 template <typename OutT>
 hipError_t exclusive_scan(int64_t n, const int32_t *in, OutT *out, int64_t *tmp, int64_t *total_copy, int32_t *stats,
-                          hipStream_t st) {
+                          hipStream_t st, const int32_t *err = nullptr, int64_t *rec = nullptr, int64_t seq = 0,
+                          bool *rec_written = nullptr) {
+    if (rec_written) *rec_written = false;
     if (n <= SMALL_MAX) {
-        hipLaunchKernelGGL(k_scan_small<OutT>, dim3(1), dim3(SMALL_THREADS), 0, st, n, in, out, total_copy, stats);
+        const bool r = rec && stats && err;
+        hipLaunchKernelGGL(k_scan_small<OutT>, dim3(1), dim3(SMALL_THREADS), 0, st, n, in, out, total_copy, stats,
+                           err, r ? rec : nullptr, seq);
+        if (rec_written) *rec_written = r;
         return hipGetLastError();
     }
     const int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
@@ -676,7 +703,8 @@ Geometry geometry(const NbrWork &w, double r_cut) {
 
 hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, int64_t center_bound, const void *pos, bool pos64,
                       const int32_t *Z, const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers,
-                      double r_cut, int64_t *row_ptr, hipStream_t st) {
+                      double r_cut, int64_t *row_ptr, hipStream_t st, int64_t *rec, int64_t seq,
+                      bool *rec_written) {
     const Geometry g = geometry(w, r_cut);
     hipError_t e;
     // flags, density work counters and both bucket arrays are one zeroed block
@@ -706,7 +734,8 @@ hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, int64_t center_bound, c
                            w.sorted_spec, g.mask, g.b, g.inv_h, g.lim2, g.rc2, w.deg, w.slots, w.flags);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, (int64_t *)(w.flags + 4), w.flags + 1, st);
+    return exclusive_scan<int64_t>(nc, w.deg, row_ptr, w.scan_tmp, (int64_t *)(w.flags + 4), w.flags + 1, st,
+                                   w.flags, rec, seq, rec_written);
 }
 
 hipError_t periodic_count(int64_t n, const void *pos, bool pos64, const PeriodicCell &C, double *lohi, int32_t *cnt,

@@ -121,10 +121,15 @@ hipError_t map_edges(int64_t E, const int32_t *cols, const int32_t *map, const i
                      int32_t *img_out, hipStream_t st);
 
 // center_bound: centers must index atoms below it (the atoms of an extended
-// periodic structure that are not images)
+// periodic structure that are not images).  rec (may be NULL): device address
+// of a host-visible record of four int64, error bits | largest degree << 32,
+// rows above TCAP, total degree, then seq (stored last, with a system-scope
+// release); *rec_written says whether this launch writes it (one-workgroup
+// scan of the degrees only, n_centers <= 16384)
 hipError_t nbr_phase1(const NbrWork &w, int64_t n_atoms, int64_t center_bound, const void *pos, bool pos64,
                       const int32_t *Z, const int8_t *lut, uint8_t *spec, int64_t nc, const int32_t *centers,
-                      double r_cut, int64_t *row_ptr, hipStream_t st);
+                      double r_cut, int64_t *row_ptr, hipStream_t st, int64_t *rec, int64_t seq,
+                      bool *rec_written);
 // rows of up to TCAP neighbours from their slots into cols (cap entries);
 // writes nothing if the rows need more than cap, so it may run before the
 // host has read the total

@@ -254,6 +254,45 @@ def test_repeated_calls_on_one_neighbour_list():
     fresh.close()
 
 
+def test_build_queued_behind_other_work():
+    """A neighbour build queued behind ~0.1 s of other work on the stream:
+    the host's bounded wait for the search's edge-count record gives way to a
+    stream synchronisation.  E, the rows and the outputs equal an idle
+    build's, and the errors found on the device are still reported."""
+    import torch
+    from paper_2609_05709_amd.soap import SOAP_ESPECIES, Soap, SoapError
+    wl = workloads.WATER64
+    st = wl.structure()
+    pos, Z = torch.from_numpy(st.pos).cuda(), torch.from_numpy(st.Z).cuda()
+    ref = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    E0 = ref.build_neighbors(pos, Z)
+    sp = Soap(wl.species, wl.r_cut, wl.n_max, wl.l_max, wl.sigma, wl.rbf)
+    x = torch.full((4096, 4096), 1e-4, device="cuda")
+    y = torch.empty_like(x)
+
+    def queue_work():
+        for _ in range(40):
+            torch.mm(x, x, out=y)
+            torch.mm(y, y, out=x)
+
+    torch.cuda.synchronize()
+    queue_work()
+    assert sp.build_neighbors(pos, Z) == E0
+    for a, b in zip(sp.neighbors(), ref.neighbors()):
+        assert torch.equal(a, b)
+    for a, b in zip(sp.derivatives(), ref.derivatives()):
+        assert torch.equal(a, b)
+    Zbad = Z.clone()
+    Zbad[7] = 6
+    queue_work()
+    with pytest.raises(SoapError) as ei:
+        sp.build_neighbors(pos, Zbad)
+    assert ei.value.code == SOAP_ESPECIES
+    torch.cuda.synchronize()
+    sp.close()
+    ref.close()
+
+
 def test_rebuilds_alternating_small_and_large():
     """One context rebuilt for a small structure, then a larger one whose
     rows no longer fit the rows buffer (the rows packed before the host read
